@@ -1,0 +1,168 @@
+/*
+ * kmpath -- cross-validated regularisation paths of RBF kernel machines on
+ * one AMD Instinct MI355X (gfx950), fp64 throughout.
+ *
+ * Problem (Appendix A.1, eq. (kernelsvm); Appendix A.2, fold-restricted
+ * form). For every kernel bandwidth sigma_s, quantile level tau_q (check
+ * loss only), fold v and penalty lambda_l, with T_v the training points of
+ * fold v (fold id != v, increasing index order), n_v = |T_v| and
+ * K_v = K[T_v, T_v], K(x, x') = exp(-||x - x'||^2 / (2 sigma^2)):
+ *
+ *   minimise over alpha in R^{n_v}, beta in R
+ *     F = (1/n_v) sum_{i in T_v} loss(y_i, f_i) + lambda alpha' K_v alpha,
+ *     f = K_v alpha + beta 1,
+ *
+ * where loss is the delta-smoothed hinge L_delta(y f) (Appendix A.1), the
+ * logistic loss log(1 + exp(-y f)) or the smoothed check loss
+ * rho_{tau,delta}(y - f) (kernel quantile regression). The method is the
+ * paper's: one factorisation of each K_v reused for every lambda
+ * (Appendix A.3), the majorise-minimise update of Appendix A.1 with
+ * Nesterov acceleration (Algorithm 1), all (fold x lambda) problems advanced
+ * together, and the finite-smoothing schedule delta <- eta * delta
+ * (Algorithm 1, outer loop).
+ *
+ * Conventions for every entry point:
+ *  - Pointers documented as DEVICE point to memory on the current HIP device
+ *    (e.g. torch tensors); HOST pointers are ordinary host memory. All
+ *    arrays are caller-owned; the library keeps no pointer after returning.
+ *  - fp64 arrays are densely packed in the layouts stated; int arrays are
+ *    int32 unless stated.
+ *  - Work is enqueued on `stream` (0 = the null stream). Entry points that
+ *    return host results synchronise that stream before returning.
+ *  - Return 0 on success, a negative KMP_E* code on error (nothing is
+ *    written to outputs after an argument error), +1 (KMP_WMAXITER) when the
+ *    path finished but some cell hit max_iter. kmp_strerror explains codes.
+ *  - Not thread-safe on one workspace; distinct workspaces may be used
+ *    concurrently.
+ */
+#ifndef KMPATH_H
+#define KMPATH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KMP_OK 0
+#define KMP_WMAXITER 1     /* finished; some cells stopped at max_iter      */
+#define KMP_EINVAL (-1)    /* bad shape, lambda <= 0, sigma <= 0, tau, loss  */
+#define KMP_EFOLD (-2)     /* fold id out of range, empty fold, one class    */
+#define KMP_EWORKSPACE (-3)/* workspace missing or too small                 */
+#define KMP_EHIP (-4)      /* HIP runtime error (see kmp_strerror)           */
+#define KMP_ENONFINITE (-5)/* NaN or Inf in X, y or the iteration            */
+
+#define KMP_HINGE 0        /* smoothed hinge, y in {-1,+1}                   */
+#define KMP_LOGISTIC 1     /* logistic, y in {-1,+1}; no smoothing stages    */
+#define KMP_CHECK 2        /* smoothed check loss, any real y                */
+
+#define KMP_FLAG_RESTART 1 /* adaptive (gradient) restart of the momentum    */
+
+/* Solver settings. kmp_default_spec fills the defaults named below. */
+typedef struct {
+  int32_t loss;        /* KMP_HINGE, KMP_LOGISTIC or KMP_CHECK              */
+  double delta0;       /* first smoothing level (hinge/check), default 1    */
+  double eta;          /* smoothing shrink factor, default 0.125            */
+  int32_t n_stages;    /* smoothing levels delta0*eta^s, s < n_stages (3)   */
+  double tol;          /* stop a cell when n_v*max(||Q'(z+2 lambda alpha)||_2,
+                          |1'z|) <= tol at the extrapolated point (1e-9)    */
+  int32_t max_iter;    /* iterations per stage per cell (100000)            */
+  int32_t poll_every;  /* iterations between host convergence polls (8)     */
+  int32_t flags;       /* KMP_FLAG_RESTART (default on)                     */
+} kmp_path_spec;
+
+/* Phase times in milliseconds, measured with HIP events on `stream`. */
+typedef struct {
+  double gram_ms;      /* a1: Gram + fold gather                            */
+  double factor_ms;    /* a2: per-fold tridiagonal factorisation and Q      */
+  double precompute_ms;/* a3: per-stage per-column factors                  */
+  double path_ms;      /* a4-a9: iterations                                 */
+  double finalize_ms;  /* a10: alpha, objectives, CV sums                   */
+  double total_ms;
+  int64_t iterations;  /* iterations launched, summed over stages and batches */
+  int64_t cell_iterations; /* sum over cells of iterations to convergence   */
+} kmp_timings;
+
+void kmp_default_spec(kmp_path_spec* spec);
+
+/* Bytes of DEVICE workspace kmp_fit_path needs for this problem when the
+ * bandwidths are processed `sigma_batch` at a time (1 <= sigma_batch <= S).
+ * fold_id is HOST, n entries. Returns 0 if the arguments are invalid.     */
+size_t kmp_workspace_bytes(const kmp_path_spec* spec, int64_t n, int64_t d,
+                           int32_t L, const int32_t* fold_id, int32_t V,
+                           int32_t S, int32_t Q, int32_t sigma_batch);
+
+/* The whole CV path (Appendix A.2-A.4; Algorithm 1 in its V-fold form).
+ *
+ * Inputs
+ *   X        DEVICE, n x d row-major, leading dimension ldx >= d (elements)
+ *   y        DEVICE, n; +/-1 for hinge/logistic
+ *   sigmas   HOST, S > 0 bandwidths (> 0)
+ *   taus     HOST, Q levels in (0,1) for KMP_CHECK; ignored (Q must be 1)
+ *            for the margin losses
+ *   lambdas  HOST, L > 0 penalties (> 0), any order
+ *   fold_id  HOST, n ids in [0, V); every fold non-empty; for hinge and
+ *            logistic every training set must contain both classes
+ *   workspace DEVICE, >= kmp_workspace_bytes(..., sigma_batch) for some
+ *            sigma_batch; the largest batch that fits is used
+ * Outputs (DEVICE unless stated; index order [s][q][v][l], s fastest-slowest
+ * as written, i.e. cell (s,q,v,l) at ((s*Q + q)*V + v)*L + l):
+ *   alpha    [S][Q][V][L][n]; zeros at the held-out indices of fold v
+ *   beta     [S][Q][V][L]
+ *   objective[S][Q][V][L]   F at the final delta, from K in observation space
+ *   cv_sum   [S][Q][V][L]   sum over held-out j of the unsmoothed loss
+ *   cv_err   [S][Q][V][L]   held-out y f <= 0 count (0 for KMP_CHECK); may be NULL
+ *   iters    [S][Q][V][L]   iterations summed over stages; may be NULL
+ *   status   [S][Q][V][L]   0 converged, 1 max_iter, 2 non-finite; may be NULL
+ *   selected HOST [S][Q]: argmin_l sum_v cv_sum/n, ties to larger lambda; may be NULL
+ *   timings  HOST, may be NULL
+ * Synchronises `stream` before returning.                                   */
+int kmp_fit_path(void* stream, const kmp_path_spec* spec,
+                 const double* X, int64_t n, int64_t d, int64_t ldx,
+                 const double* y,
+                 const double* sigmas, int32_t S,
+                 const double* taus, int32_t Q,
+                 const double* lambdas, int32_t L,
+                 const int32_t* fold_id, int32_t V,
+                 void* workspace, size_t workspace_bytes,
+                 double* alpha, double* beta, double* objective,
+                 double* cv_sum, int32_t* cv_err, int32_t* iters,
+                 int32_t* status, int32_t* selected, kmp_timings* timings);
+
+/* Random V-fold assignment (HOST output fold_id, n entries): SplitMix64
+ * (Steele, Lea & Flood 2014) seeded with `seed` drives a Fisher-Yates
+ * shuffle from the top, j = high 64 bits of (draw * (i+1)); then
+ * fold_id[perm[i]] = i mod V. Integer-only and reproducible.             */
+int kmp_make_folds(int64_t n, int32_t V, uint64_t seed, int32_t* fold_id);
+
+/* a1 on its own: RBF blocks K_s[i][j] = exp(-max(0, |x_r|^2 + |x_c|^2 -
+ * 2 x_r.x_c) / (2 sigma_s^2)) with r = rows[i], c = cols[j] (DEVICE int32
+ * index lists into X), exactly 1 where r == c, and 0 where either index is
+ * negative (padding). out DEVICE, S blocks of m x p row-major with leading
+ * dimension ld_out >= p, block s at out + s*m*ld_out. sigmas HOST.        */
+int kmp_rbf_gram(void* stream, const double* X, int64_t n, int64_t d, int64_t ldx,
+                 const int32_t* rows, int64_t m, const int32_t* cols, int64_t p,
+                 const double* sigmas, int32_t S, double* out, int64_t ld_out);
+
+/* a2 on its own: G symmetric N x N matrices A (DEVICE, row-major, packed,
+ * matrix g at A + g*N*N; destroyed) are reduced to A_g = Q_g T_g Q_g' with
+ * Q_g orthogonal (DEVICE out, same layout) and T_g symmetric tridiagonal
+ * with diagonal diag[g*N + i] and off-diagonal off[g*N + i] = T[i+1][i]
+ * (off[g*N + N-1] = 0). Householder reduction (Golub & Van Loan, Alg.
+ * 8.3.1), blocked as in LAPACK's dsytrd, Q accumulated in compact-WY form.
+ * Every matrix must have N valid rows (zero padding rows are allowed).     */
+int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N,
+                double* Qout, double* diag, double* off);
+
+/* Message for a return code, or the last HIP error text for KMP_EHIP. */
+const char* kmp_strerror(int code);
+
+/* Library version string. */
+const char* kmp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KMPATH_H */

@@ -1,0 +1,560 @@
+// Host driver and C ABI of the kmpath library (see include/kmpath.h).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kmp_common.h"
+#include "kmp_kernels.h"
+#include "kmpath.h"
+
+namespace kmp {
+
+static thread_local std::string g_err;
+void set_error(const std::string& msg) { g_err = msg; }
+const char* last_error() { return g_err.c_str(); }
+
+namespace {
+
+constexpr int kPanel = 32;       // Householder panel width
+constexpr int kRowAlign = 64;    // padding of the per-fold matrix order
+constexpr size_t kAlign = 256;
+
+struct Plan {
+  int64_t n = 0, d = 0;
+  int V = 0, S = 0, Qt = 1, L = 0, Sb = 0;
+  int N = 0, C = 0, G = 0, RT = 0;
+  std::vector<int> nv;           // per fold
+  size_t bytes = 0;
+};
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+  template <typename T>
+  T* take(size_t count) {
+    off = (off + kAlign - 1) / kAlign * kAlign;
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+// Workspace layout for one bandwidth batch (G = Sb * V groups). Used both to
+// size and to carve, so the two can never disagree.
+struct Layout {
+  double *A, *Qm, *diag, *off, *tau, *cvec, *ylab, *panel, *dots, *tmat, *xbuf, *ybuf;
+  double *ahat, *abar, *bmat, *zmat, *zhat, *ldl_l, *ldl_d, *vhat, *uvec, *partial;
+  double *beta, *bbar, *rmom, *gcoef, *kkt, *lam, *taucol, *fbuf, *nrm, *inv2s2;
+  int *flag, *iters, *iters_total, *active, *nvg;
+  int32_t *tidx, *fold;
+};
+
+size_t carve(const Plan& p, void* ws, Layout* out) {
+  Carver c(ws);
+  Layout l{};
+  const size_t G = (size_t)p.G, N = (size_t)p.N, C = (size_t)p.C, cols = G * C;
+  l.A = c.take<double>(G * N * N);
+  l.Qm = c.take<double>(G * N * N);
+  l.diag = c.take<double>(G * N);
+  l.off = c.take<double>(G * N);
+  l.tau = c.take<double>(G * N);
+  l.cvec = c.take<double>(G * N);
+  l.ylab = c.take<double>(G * N);
+  l.panel = c.take<double>(G * 3 * kPanel * N);
+  l.dots = c.take<double>(G * 2 * kPanel);
+  l.tmat = c.take<double>(G * kPanel * kPanel);
+  l.xbuf = c.take<double>(G * kPanel * N);
+  l.ybuf = c.take<double>(G * kPanel * N);
+  l.ahat = c.take<double>(cols * N);
+  l.abar = c.take<double>(cols * N);
+  l.bmat = c.take<double>(cols * N);
+  l.zmat = c.take<double>(cols * N);
+  l.zhat = c.take<double>(cols * N);
+  l.ldl_l = c.take<double>(cols * N);
+  l.ldl_d = c.take<double>(cols * N);
+  l.vhat = c.take<double>(cols * N);
+  l.uvec = c.take<double>(cols * N);
+  l.partial = c.take<double>(G * (size_t)p.RT * C);
+  l.beta = c.take<double>(cols);
+  l.bbar = c.take<double>(cols);
+  l.rmom = c.take<double>(cols);
+  l.gcoef = c.take<double>(cols);
+  l.kkt = c.take<double>(cols);
+  l.lam = c.take<double>(cols);
+  l.taucol = c.take<double>(cols);
+  l.fbuf = c.take<double>(cols * (size_t)p.n);
+  l.nrm = c.take<double>((size_t)p.n);
+  l.inv2s2 = c.take<double>((size_t)std::max(p.S, 1));
+  l.flag = c.take<int>(cols);
+  l.iters = c.take<int>(cols);
+  l.iters_total = c.take<int>(cols);
+  l.active = c.take<int>(1);
+  l.nvg = c.take<int>(G);
+  l.tidx = c.take<int32_t>((size_t)p.V * N);
+  l.fold = c.take<int32_t>((size_t)p.n);
+  if (out) *out = l;
+  return c.off + kAlign;
+}
+
+int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const int32_t* fold,
+              int32_t V, int32_t S, int32_t Qn, int32_t Sb, Plan* p) {
+  if (!spec || n < 2 || d < 1 || L < 1 || V < 2 || S < 1 || Qn < 1 || !fold) {
+    set_error("invalid shape arguments");
+    return KMP_EINVAL;
+  }
+  if (spec->loss != KMP_CHECK && Qn != 1) {
+    set_error("Q must be 1 for the margin losses");
+    return KMP_EINVAL;
+  }
+  p->n = n; p->d = d; p->V = V; p->S = S; p->Qt = Qn; p->L = L;
+  p->nv.assign(V, 0);
+  std::vector<int64_t> m(V, 0);
+  for (int64_t i = 0; i < n; ++i) {
+    const int32_t f = fold[i];
+    if (f < 0 || f >= V) {
+      set_error("fold id out of range at index " + std::to_string(i));
+      return KMP_EFOLD;
+    }
+    m[f] += 1;
+  }
+  int maxnv = 0;
+  for (int v = 0; v < V; ++v) {
+    if (m[v] == 0) {
+      set_error("fold " + std::to_string(v) + " is empty");
+      return KMP_EFOLD;
+    }
+    p->nv[v] = (int)(n - m[v]);
+    maxnv = std::max(maxnv, p->nv[v]);
+  }
+  p->N = (int)round_up(maxnv, kRowAlign);
+  if (p->N > 8192) {
+    set_error("more than 8192 training points per fold is not supported yet");
+    return KMP_EINVAL;
+  }
+  p->C = Qn * L;
+  p->RT = (int)ceil_div(p->N, kGemmTile);
+  p->Sb = std::max(1, std::min<int>(Sb, S));
+  p->G = p->Sb * V;
+  p->bytes = carve(*p, nullptr, nullptr);
+  return 0;
+}
+
+struct EventTimer {
+  hipEvent_t ev[8];
+  bool ok = false;
+  EventTimer() {
+    ok = true;
+    for (auto& e : ev)
+      if (hipEventCreate(&e) != hipSuccess) ok = false;
+  }
+  ~EventTimer() {
+    for (auto& e : ev) hipEventDestroy(e);
+  }
+  float ms(int a, int b) {
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, ev[a], ev[b]) != hipSuccess) return 0.f;
+    return t;
+  }
+};
+
+}  // namespace
+}  // namespace kmp
+
+using namespace kmp;
+
+extern "C" {
+
+void kmp_default_spec(kmp_path_spec* s) {
+  if (!s) return;
+  s->loss = KMP_HINGE;
+  s->delta0 = 1.0;
+  s->eta = 0.125;
+  s->n_stages = 3;
+  s->tol = 1e-9;
+  s->max_iter = 100000;
+  s->poll_every = 8;
+  s->flags = KMP_FLAG_RESTART;
+}
+
+const char* kmp_version(void) { return "kmpath 0.1 (gfx950, fp64)"; }
+
+const char* kmp_strerror(int code) {
+  switch (code) {
+    case KMP_OK: return "ok";
+    case KMP_WMAXITER: return "finished; some cells stopped at max_iter";
+    case KMP_EINVAL: return g_err.empty() ? "invalid argument" : g_err.c_str();
+    case KMP_EFOLD: return g_err.empty() ? "invalid fold assignment" : g_err.c_str();
+    case KMP_EWORKSPACE: return g_err.empty() ? "workspace missing or too small" : g_err.c_str();
+    case KMP_EHIP: return g_err.empty() ? "HIP runtime error" : g_err.c_str();
+    case KMP_ENONFINITE: return g_err.empty() ? "non-finite input" : g_err.c_str();
+    default: return "unknown code";
+  }
+}
+
+int kmp_make_folds(int64_t n, int32_t V, uint64_t seed, int32_t* fold_id) {
+  if (n <= 0 || V <= 0 || !fold_id) {
+    set_error("kmp_make_folds: n, V must be positive and fold_id non-null");
+    return KMP_EINVAL;
+  }
+  std::vector<int64_t> perm(n);
+  for (int64_t i = 0; i < n; ++i) perm[i] = i;
+  uint64_t st = seed;
+  for (int64_t i = n - 1; i >= 1; --i) {
+    st += 0x9E3779B97F4A7C15ULL;
+    uint64_t z = st;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    z ^= z >> 31;
+    const int64_t j = (int64_t)(((unsigned __int128)z * (unsigned __int128)(i + 1)) >> 64);
+    std::swap(perm[i], perm[j]);
+  }
+  for (int64_t i = 0; i < n; ++i) fold_id[perm[i]] = (int32_t)(i % V);
+  return KMP_OK;
+}
+
+size_t kmp_workspace_bytes(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L,
+                           const int32_t* fold_id, int32_t V, int32_t S, int32_t Q,
+                           int32_t sigma_batch) {
+  Plan p;
+  if (sigma_batch < 1 || sigma_batch > S) return 0;
+  if (make_plan(spec, n, d, L, fold_id, V, S, Q, sigma_batch, &p) != 0) return 0;
+  return p.bytes;
+}
+
+int kmp_rbf_gram(void* stream, const double* X, int64_t n, int64_t d, int64_t ldx,
+                 const int32_t* rows, int64_t m, const int32_t* cols, int64_t p,
+                 const double* sigmas, int32_t S, double* out, int64_t ld_out) {
+  hipStream_t s = (hipStream_t)stream;
+  if (!X || !rows || !cols || !sigmas || !out || n < 1 || d < 1 || ldx < d || m < 0 || p < 0 ||
+      S < 1 || S > 8 || ld_out < p) {
+    set_error("kmp_rbf_gram: invalid arguments");
+    return KMP_EINVAL;
+  }
+  std::vector<double> f2(S);
+  for (int i = 0; i < S; ++i) {
+    if (!(sigmas[i] > 0.0) || !std::isfinite(sigmas[i])) {
+      set_error("kmp_rbf_gram: sigma must be positive");
+      return KMP_EINVAL;
+    }
+    f2[i] = 1.0 / (2.0 * sigmas[i] * sigmas[i]);
+  }
+  if (m == 0 || p == 0) return KMP_OK;
+  double *nrm = nullptr, *dinv = nullptr;
+  KMP_HIP_TRY(hipMallocAsync((void**)&nrm, sizeof(double) * n, s));
+  KMP_HIP_TRY(hipMallocAsync((void**)&dinv, sizeof(double) * S, s));
+  KMP_HIP_TRY(hipMemcpyAsync(dinv, f2.data(), sizeof(double) * S, hipMemcpyHostToDevice, s));
+  int rc = row_norms(s, X, n, d, ldx, nrm);
+  if (rc == 0)
+    rc = rbf_blocks(s, X, d, ldx, nrm, rows, 0, m, cols, 0, p, 1, dinv, S, out, m * ld_out, 0,
+                    ld_out);
+  KMP_HIP_TRY(hipFreeAsync(nrm, s));
+  KMP_HIP_TRY(hipFreeAsync(dinv, s));
+  KMP_HIP_TRY(hipStreamSynchronize(s));
+  return rc;
+}
+
+int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N, double* Qout, double* diag,
+                double* off) {
+  hipStream_t s = (hipStream_t)stream;
+  if (!A || !Qout || !diag || !off || G < 1 || N < 1 || N % kPanel != 0) {
+    set_error("kmp_tridiag: invalid arguments (N must be a positive multiple of 32)");
+    return KMP_EINVAL;
+  }
+  TridiagWork w;
+  w.G = G; w.N = N; w.nb = kPanel; w.A = A; w.Q = Qout; w.diag = diag; w.off = off;
+  double* scratch = nullptr;
+  const size_t extra = tridiag_panel_doubles(G, N, kPanel) + (size_t)G * N;
+  KMP_HIP_TRY(hipMallocAsync((void**)&scratch, sizeof(double) * extra, s));
+  double* q = scratch;
+  w.tau = q; q += (size_t)G * N;
+  w.panel = q; q += (size_t)G * 3 * kPanel * N;
+  w.dots = q; q += (size_t)G * 2 * kPanel;
+  w.tmat = q; q += (size_t)G * kPanel * kPanel;
+  w.xbuf = q; q += (size_t)G * kPanel * N;
+  w.ybuf = q;
+  int rc = tridiagonalize(s, w);
+  KMP_HIP_TRY(hipFreeAsync(scratch, s));
+  KMP_HIP_TRY(hipStreamSynchronize(s));
+  return rc;
+}
+
+int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64_t n, int64_t d,
+                 int64_t ldx, const double* y, const double* sigmas, int32_t S, const double* taus,
+                 int32_t Qn, const double* lambdas, int32_t L, const int32_t* fold_id, int32_t V,
+                 void* workspace, size_t workspace_bytes, double* alpha, double* beta,
+                 double* objective, double* cv_sum, int32_t* cv_err, int32_t* iters,
+                 int32_t* status, int32_t* selected, kmp_timings* timings) {
+  hipStream_t s = (hipStream_t)stream;
+  // ---------------------------------------------------------- validation
+  if (!spec || !X || !y || !sigmas || !lambdas || !fold_id || !alpha || !beta || !objective ||
+      !cv_sum) {
+    set_error("null pointer argument");
+    return KMP_EINVAL;
+  }
+  if (spec->loss < 0 || spec->loss > 2 || !(spec->tol > 0.0) || spec->max_iter < 1 ||
+      spec->poll_every < 1 || (spec->loss != KMP_LOGISTIC &&
+                               (!(spec->delta0 > 0.0) || !(spec->eta > 0.0 && spec->eta < 1.0) ||
+                                spec->n_stages < 1))) {
+    set_error("invalid solver settings");
+    return KMP_EINVAL;
+  }
+  if (ldx < d) {
+    set_error("ldx must be >= d");
+    return KMP_EINVAL;
+  }
+  if (spec->loss == KMP_CHECK && (!taus || Qn < 1)) {
+    set_error("check loss needs Q >= 1 tau values");
+    return KMP_EINVAL;
+  }
+  for (int i = 0; i < S; ++i)
+    if (!(sigmas[i] > 0.0) || !std::isfinite(sigmas[i])) {
+      set_error("sigma must be positive and finite");
+      return KMP_EINVAL;
+    }
+  for (int i = 0; i < L; ++i)
+    if (!(lambdas[i] > 0.0) || !std::isfinite(lambdas[i])) {
+      set_error("lambda must be positive and finite");
+      return KMP_EINVAL;
+    }
+  if (spec->loss == KMP_CHECK)
+    for (int i = 0; i < Qn; ++i)
+      if (!(taus[i] > 0.0 && taus[i] < 1.0)) {
+        set_error("tau must lie in (0, 1)");
+        return KMP_EINVAL;
+      }
+  Plan plan;
+  int rc = make_plan(spec, n, d, L, fold_id, V, S, Qn, S, &plan);
+  if (rc != 0) return rc;
+  // inputs to host for finiteness and label checks
+  std::vector<double> hy(n), hx((size_t)n * d);
+  KMP_HIP_TRY(hipMemcpyAsync(hy.data(), y, sizeof(double) * n, hipMemcpyDeviceToHost, s));
+  KMP_HIP_TRY(hipMemcpy2DAsync(hx.data(), sizeof(double) * d, X, sizeof(double) * ldx,
+                               sizeof(double) * d, n, hipMemcpyDeviceToHost, s));
+  KMP_HIP_TRY(hipStreamSynchronize(s));
+  for (int64_t i = 0; i < n; ++i) {
+    if (!std::isfinite(hy[i])) {
+      set_error("non-finite y at index " + std::to_string(i));
+      return KMP_ENONFINITE;
+    }
+    for (int64_t k = 0; k < d; ++k)
+      if (!std::isfinite(hx[(size_t)i * d + k])) {
+        set_error("non-finite X at row " + std::to_string(i));
+        return KMP_ENONFINITE;
+      }
+  }
+  if (spec->loss != KMP_CHECK) {
+    std::vector<int64_t> pos(V, 0), neg(V, 0);
+    int64_t tp = 0, tn = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      if (hy[i] == 1.0) { pos[fold_id[i]]++; tp++; }
+      else if (hy[i] == -1.0) { neg[fold_id[i]]++; tn++; }
+      else {
+        set_error("labels must be +1 or -1 for hinge and logistic losses");
+        return KMP_EINVAL;
+      }
+    }
+    for (int v = 0; v < V; ++v)
+      if (tp - pos[v] == 0 || tn - neg[v] == 0) {
+        set_error("training set of fold " + std::to_string(v) + " has a single class");
+        return KMP_EFOLD;
+      }
+  }
+  // largest bandwidth batch that fits the workspace
+  int Sb = 0;
+  for (int b = std::min(S, 8); b >= 1; --b) {   // the Gram epilogue takes <= 8 bandwidths
+    Plan pb;
+    if (make_plan(spec, n, d, L, fold_id, V, S, Qn, b, &pb) == 0 && pb.bytes <= workspace_bytes) {
+      Sb = b;
+      plan = pb;
+      break;
+    }
+  }
+  if (!workspace || Sb == 0) {
+    set_error("workspace too small: need " +
+              std::to_string(kmp_workspace_bytes(spec, n, d, L, fold_id, V, S, Qn, 1)) +
+              " bytes for one bandwidth at a time");
+    return KMP_EWORKSPACE;
+  }
+  Layout lay;
+  carve(plan, workspace, &lay);
+  const int N = plan.N, C = plan.C, G = plan.G;
+  const int nst = spec->loss == KMP_LOGISTIC ? 1 : spec->n_stages;
+  const double delta_final = spec->loss == KMP_LOGISTIC
+                                 ? 1.0
+                                 : spec->delta0 * std::pow(spec->eta, (double)(nst - 1));
+
+  // host-side index lists and per-column parameters
+  std::vector<int32_t> tidx((size_t)V * N, -1);
+  for (int v = 0; v < V; ++v) {
+    int k = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (fold_id[i] != v) tidx[(size_t)v * N + k++] = (int32_t)i;
+  }
+  KMP_HIP_TRY(hipMemcpyAsync(lay.tidx, tidx.data(), sizeof(int32_t) * tidx.size(),
+                             hipMemcpyHostToDevice, s));
+  KMP_HIP_TRY(hipMemcpyAsync(lay.fold, fold_id, sizeof(int32_t) * n, hipMemcpyHostToDevice, s));
+  const size_t ncell = (size_t)S * Qn * V * L;
+  KMP_HIP_TRY(hipMemsetAsync(alpha, 0, sizeof(double) * ncell * n, s));
+
+  EventTimer tm;
+  double t_gram = 0, t_factor = 0, t_pre = 0, t_path = 0, t_fin = 0;
+  int64_t total_iters = 0;
+  KMP_HIP_TRY(hipEventRecord(tm.ev[0], s));
+  if ((rc = row_norms(s, X, n, d, ldx, lay.nrm)) != 0) return rc;
+
+  PathArrays pa;
+  pa.N = N; pa.C = C; pa.loss = spec->loss;
+  pa.nv = lay.nvg; pa.ylab = lay.ylab; pa.Q = lay.Qm; pa.Tdiag = lay.diag; pa.Toff = lay.off;
+  pa.cvec = lay.cvec; pa.lam = lay.lam; pa.tau = lay.taucol;
+  pa.ahat = lay.ahat; pa.abar = lay.abar; pa.bmat = lay.bmat; pa.zmat = lay.zmat;
+  pa.zhat = lay.zhat; pa.ldl_l = lay.ldl_l; pa.ldl_d = lay.ldl_d; pa.vhat = lay.vhat;
+  pa.uvec = lay.uvec; pa.partial = lay.partial; pa.beta = lay.beta; pa.bbar = lay.bbar;
+  pa.rmom = lay.rmom; pa.gcoef = lay.gcoef; pa.kkt = lay.kkt; pa.flag = lay.flag;
+  pa.iters = lay.iters; pa.iters_total = lay.iters_total; pa.active_count = lay.active;
+
+  for (int s0 = 0; s0 < S; s0 += Sb) {
+    const int sb = std::min(Sb, S - s0);
+    const int Gb = sb * V;
+    pa.G = Gb;
+    // per-batch parameters
+    std::vector<double> f2(sb), lamc((size_t)Gb * C), tauc((size_t)Gb * C);
+    std::vector<int> nvg(Gb);
+    for (int i = 0; i < sb; ++i) f2[i] = 1.0 / (2.0 * sigmas[s0 + i] * sigmas[s0 + i]);
+    for (int g = 0; g < Gb; ++g) {
+      nvg[g] = plan.nv[g % V];
+      for (int q = 0; q < Qn; ++q)
+        for (int l = 0; l < L; ++l) {
+          lamc[(size_t)g * C + q * L + l] = lambdas[l];
+          tauc[(size_t)g * C + q * L + l] = spec->loss == KMP_CHECK ? taus[q] : 0.0;
+        }
+    }
+    KMP_HIP_TRY(hipMemcpyAsync(lay.inv2s2, f2.data(), sizeof(double) * sb, hipMemcpyHostToDevice, s));
+    KMP_HIP_TRY(hipMemcpyAsync(lay.lam, lamc.data(), sizeof(double) * lamc.size(),
+                               hipMemcpyHostToDevice, s));
+    KMP_HIP_TRY(hipMemcpyAsync(lay.taucol, tauc.data(), sizeof(double) * tauc.size(),
+                               hipMemcpyHostToDevice, s));
+    KMP_HIP_TRY(hipMemcpyAsync(lay.nvg, nvg.data(), sizeof(int) * Gb, hipMemcpyHostToDevice, s));
+
+    // a1: Gram + fold gather into A (group g = s_local*V + v)
+    KMP_HIP_TRY(hipEventRecord(tm.ev[1], s));
+    if ((rc = rbf_blocks(s, X, d, ldx, lay.nrm, lay.tidx, N, N, lay.tidx, N, N, V, lay.inv2s2, sb,
+                         lay.A, (int64_t)V * N * N, (int64_t)N * N, N)) != 0)
+      return rc;
+    KMP_HIP_TRY(hipEventRecord(tm.ev[2], s));
+    // a2: factorisation
+    TridiagWork tw;
+    tw.G = Gb; tw.N = N; tw.nb = kPanel; tw.A = lay.A; tw.Q = lay.Qm; tw.diag = lay.diag;
+    tw.off = lay.off; tw.tau = lay.tau; tw.panel = lay.panel; tw.dots = lay.dots;
+    tw.tmat = lay.tmat; tw.xbuf = lay.xbuf; tw.ybuf = lay.ybuf;
+    if ((rc = tridiagonalize(s, tw)) != 0) return rc;
+    if ((rc = group_ones_projection(s, lay.Qm, lay.nvg, Gb, N, lay.cvec)) != 0) return rc;
+    if ((rc = gather_labels(s, y, lay.tidx, V, sb, N, lay.ylab)) != 0) return rc;
+    if ((rc = path_init_columns(s, pa)) != 0) return rc;
+    KMP_HIP_TRY(hipEventRecord(tm.ev[3], s));
+    KMP_HIP_TRY(hipEventSynchronize(tm.ev[3]));
+    t_gram += tm.ms(1, 2);
+    t_factor += tm.ms(2, 3);
+
+    // a3-a9: smoothing stages
+    for (int st = 0; st < nst; ++st) {
+      const double delta = spec->loss == KMP_LOGISTIC ? 1.0 : spec->delta0 * std::pow(spec->eta, (double)st);
+      const double kappa = spec->loss == KMP_LOGISTIC ? 4.0 : 2.0 * delta;
+      KMP_HIP_TRY(hipEventRecord(tm.ev[4], s));
+      if ((rc = path_stage_precompute(s, pa, kappa)) != 0) return rc;
+      KMP_HIP_TRY(hipEventRecord(tm.ev[5], s));
+      int it = 0;
+      while (it < spec->max_iter) {
+        if ((rc = path_iteration(s, pa, delta, kappa, spec->tol, spec->max_iter,
+                                 (spec->flags & KMP_FLAG_RESTART) ? 1 : 0)) != 0)
+          return rc;
+        ++it;
+        if (it % spec->poll_every == 0 || it >= spec->max_iter) {
+          if ((rc = path_count_active(s, pa)) != 0) return rc;
+          int active = 0;
+          KMP_HIP_TRY(hipMemcpyAsync(&active, lay.active, sizeof(int), hipMemcpyDeviceToHost, s));
+          KMP_HIP_TRY(hipStreamSynchronize(s));
+          if (active == 0) break;
+        }
+      }
+      total_iters += it;
+      KMP_HIP_TRY(hipEventRecord(tm.ev[6], s));
+      KMP_HIP_TRY(hipEventSynchronize(tm.ev[6]));
+      t_pre += tm.ms(4, 5);
+      t_path += tm.ms(5, 6);
+    }
+
+    // a10: finalize
+    FinalArgs fa;
+    fa.n = (int)n; fa.d = (int)d; fa.ldx = ldx; fa.X = X; fa.nrm = lay.nrm; fa.y = y;
+    fa.fold = lay.fold; fa.tidx = lay.tidx; fa.V = V; fa.S_b = sb; fa.Qt = Qn; fa.L = L;
+    fa.s0 = s0; fa.S = S; fa.inv2s2 = lay.inv2s2; fa.delta = delta_final; fa.fbuf = lay.fbuf;
+    fa.alpha = alpha; fa.beta_out = beta; fa.objective = objective; fa.cv_sum = cv_sum;
+    fa.cv_err = cv_err; fa.iters = iters; fa.status = status;
+    KMP_HIP_TRY(hipEventRecord(tm.ev[6], s));
+    if ((rc = path_finalize(s, pa, fa)) != 0) return rc;
+    KMP_HIP_TRY(hipEventRecord(tm.ev[7], s));
+    KMP_HIP_TRY(hipEventSynchronize(tm.ev[7]));
+    t_fin += tm.ms(6, 7);
+  }
+  KMP_HIP_TRY(hipEventRecord(tm.ev[7], s));
+  KMP_HIP_TRY(hipStreamSynchronize(s));
+  const double t_total = tm.ms(0, 7);
+
+  // host-side selection and status summary
+  std::vector<double> hcv(ncell);
+  KMP_HIP_TRY(hipMemcpy(hcv.data(), cv_sum, sizeof(double) * ncell, hipMemcpyDeviceToHost));
+  bool any_max = false;
+  int64_t cell_iters = 0;
+  if (status) {
+    std::vector<int32_t> hst(ncell);
+    KMP_HIP_TRY(hipMemcpy(hst.data(), status, sizeof(int32_t) * ncell, hipMemcpyDeviceToHost));
+    for (auto v : hst) {
+      if (v == 1) any_max = true;
+      if (v == 2) {
+        set_error("non-finite values in the iteration");
+        return KMP_ENONFINITE;
+      }
+    }
+  }
+  if (iters) {
+    std::vector<int32_t> hit(ncell);
+    KMP_HIP_TRY(hipMemcpy(hit.data(), iters, sizeof(int32_t) * ncell, hipMemcpyDeviceToHost));
+    for (auto v : hit) cell_iters += v;
+  }
+  if (selected) {
+    for (int si = 0; si < S; ++si)
+      for (int q = 0; q < Qn; ++q) {
+        int best = -1;
+        double bs = 0.0;
+        for (int l = 0; l < L; ++l) {
+          double sc = 0.0;
+          for (int v = 0; v < V; ++v) sc += hcv[(((size_t)si * Qn + q) * V + v) * L + l];
+          sc /= (double)n;
+          if (best < 0 || sc < bs || (sc == bs && lambdas[l] > lambdas[best])) {
+            best = l;
+            bs = sc;
+          }
+        }
+        selected[si * Qn + q] = best;
+      }
+  }
+  if (timings) {
+    timings->gram_ms = t_gram;
+    timings->factor_ms = t_factor;
+    timings->precompute_ms = t_pre;
+    timings->path_ms = t_path;
+    timings->finalize_ms = t_fin;
+    timings->total_ms = t_total;
+    timings->iterations = total_iters;
+    timings->cell_iterations = cell_iters;
+  }
+  return any_max ? KMP_WMAXITER : KMP_OK;
+}
+
+}  // extern "C"

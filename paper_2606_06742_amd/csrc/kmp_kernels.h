@@ -1,0 +1,139 @@
+// Internal launcher interface between the host driver and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kmp {
+
+// Batched tile GEMM on fp64 MFMA: for every batch b,
+//   C_b = alpha * op(A_b) * op(B_b) + beta * C_b      (M x N, inner K)
+// Element (i,k) of A is A[i*lda + k] when a_kcontig, else A[k*lda + i];
+// element (k,j) of B is B[j*ldb + k] when b_kcontig, else B[k*ldb + j];
+// element (i,j) of C is C[i*ldc + j] when c_rowmajor, else C[j*ldc + i].
+// Batch b uses A + b*sA, B + b*sB, C + b*sC.
+struct GemmArgs {
+  int M = 0, N = 0, K = 0, batch = 1;
+  const double* A = nullptr; int64_t lda = 0, sA = 0;
+  const double* B = nullptr; int64_t ldb = 0, sB = 0;
+  double* C = nullptr; int64_t ldc = 0, sC = 0;
+  double alpha = 1.0, beta = 0.0;
+};
+
+// Loss epilogue of the first path GEMM (f = Q (T abar) then z): for row i of
+// batch b and column c, with f = acc + bbar[c]:
+//   Z[i][c] = psi(y[i], f)/nv[b] if i < nv[b] else 0,
+// and partial[b][tile][c] = sum of Z over the 64 rows of the row tile.
+struct LossEpi {
+  int loss = 0;
+  double delta = 1.0;
+  const double* y = nullptr; int64_t sy = 0;     // labels, per batch stride
+  const int* nv = nullptr;                       // valid rows per batch
+  const double* bbar = nullptr; int64_t sbb = 0; // per column intercepts
+  const double* tau = nullptr; int64_t stau = 0; // per column tau (check)
+  double* partial = nullptr; int64_t spart = 0;  // [tiles][N] per batch
+};
+
+constexpr int kGemmTile = 64;   // rows and columns of a GEMM output tile
+
+int gemm(hipStream_t s, const GemmArgs& g, bool a_kcontig, bool b_kcontig, bool c_rowmajor);
+int gemm_loss(hipStream_t s, const GemmArgs& g, const LossEpi& e);
+
+// ---------------------------------------------------------------- Gram
+// Squared row norms of X (n x d, ldx): nrm[i] = sum_k X[i][k]^2.
+int row_norms(hipStream_t s, const double* X, int64_t n, int64_t d, int64_t ldx, double* nrm);
+
+// For each of `nb` index blocks (blockIdx.z = block q), rows idx_r + q*sr,
+// cols idx_c + q*sc (m and p entries, negative = padding), write for each of
+// S bandwidths: out + (s*sout_s + q*sout_q) + i*ld + j.
+int rbf_blocks(hipStream_t s, const double* X, int64_t d, int64_t ldx, const double* nrm,
+               const int32_t* idx_r, int64_t sr, int64_t m,
+               const int32_t* idx_c, int64_t sc, int64_t p, int nb,
+               const double* inv2s2, int S, double* out, int64_t sout_s, int64_t sout_q,
+               int64_t ld);
+
+// --------------------------------------------------------- tridiagonal
+struct TridiagWork {
+  int G = 0, N = 0, nb = 32;
+  double* A = nullptr;      // G x N x N, row-major; destroyed (holds reflectors)
+  double* Q = nullptr;      // G x N x N, output
+  double* diag = nullptr;   // G x N
+  double* off = nullptr;    // G x N
+  double* tau = nullptr;    // G x N (Householder scalars)
+  double* panel = nullptr;  // G x 3nb x N  ([V; W; V] rows of the current panel)
+  double* dots = nullptr;   // G x 2nb
+  double* tmat = nullptr;   // G x nb x nb (compact-WY T factor)
+  double* xbuf = nullptr;   // G x nb x N
+  double* ybuf = nullptr;   // G x nb x N
+};
+size_t tridiag_panel_doubles(int G, int N, int nb);
+int tridiagonalize(hipStream_t s, const TridiagWork& w);
+
+// ---------------------------------------------------------------- path
+struct PathArrays {
+  int G = 0;            // groups (sigma, fold)
+  int N = 0;            // padded rows per group
+  int C = 0;            // columns per group (tau x lambda)
+  int loss = 0;
+  const int* nv = nullptr;       // G valid rows
+  const double* ylab = nullptr;  // G x N labels (0 at padding)
+  const double* Q = nullptr;     // G x N x N
+  const double* Tdiag = nullptr; // G x N
+  const double* Toff = nullptr;  // G x N
+  const double* cvec = nullptr;  // G x N, Q' 1 over valid rows
+  const double* lam = nullptr;   // G*C
+  const double* tau = nullptr;   // G*C
+  // column-major per column N-vectors (column index gc = g*C + c)
+  double* ahat = nullptr;
+  double* abar = nullptr;
+  double* bmat = nullptr;   // T abar, operand of the first GEMM
+  double* zmat = nullptr;
+  double* zhat = nullptr;
+  double* ldl_l = nullptr;
+  double* ldl_d = nullptr;
+  double* vhat = nullptr;
+  double* uvec = nullptr;   // T vhat
+  double* partial = nullptr;// G x tiles x C
+  // per column scalars
+  double* beta = nullptr;
+  double* bbar = nullptr;
+  double* rmom = nullptr;
+  double* gcoef = nullptr;
+  double* kkt = nullptr;
+  int* flag = nullptr;      // 0 active, 1 converged, 2 max_iter, 3 non-finite
+  int* iters = nullptr;     // per stage
+  int* iters_total = nullptr;
+  int* active_count = nullptr;  // 1 int
+};
+
+int path_init_columns(hipStream_t s, const PathArrays& p);
+int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa);
+int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kappa, double tol,
+                   int max_iter, int restart);
+int path_count_active(hipStream_t s, const PathArrays& p);
+int group_ones_projection(hipStream_t s, const double* Q, const int* nv, int G, int N, double* cvec);
+
+// Finalize: alpha_loc = Q ahat (zmat reused), predictions for all n points
+// from K recomputed on the fly, objective/CV sums, scatter of alpha.
+struct FinalArgs {
+  int n = 0, d = 0; int64_t ldx = 0;
+  const double* X = nullptr; const double* nrm = nullptr; const double* y = nullptr;
+  const int32_t* fold = nullptr;   // n fold ids (device)
+  const int32_t* tidx = nullptr;   // V x N training indices (-1 pad)
+  int V = 0, S_b = 0, Qt = 1, L = 0, s0 = 0, S = 0;
+  const double* inv2s2 = nullptr;  // S_b bandwidth factors of this batch
+  double delta = 1.0;
+  double* fbuf = nullptr;          // G x C x n predictions
+  double* red = nullptr;           // G x C x 4 x tiles partial sums
+  // outputs (full arrays, cell ((s*Q+q)*V+v)*L+l)
+  double* alpha = nullptr; double* beta_out = nullptr; double* objective = nullptr;
+  double* cv_sum = nullptr; int32_t* cv_err = nullptr; int32_t* iters = nullptr;
+  int32_t* status = nullptr;
+};
+int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& f);
+
+// Gather labels y[tidx] per fold into G groups (S_b copies over bandwidths).
+int gather_labels(hipStream_t s, const double* y, const int32_t* tidx, int V, int S_b, int N,
+                  double* ylab);
+
+}  // namespace kmp

@@ -1,0 +1,615 @@
+// Batched regularisation-path solver in the tridiagonal basis K_v = Q T Q'.
+//
+// Every column is one (tau, lambda) problem of one group (bandwidth, fold).
+// With hats denoting Q' coordinates (a = Q'alpha), one iteration of the
+// accelerated majorise-minimise method (Appendix A.1 update; Algorithm 1
+// inner loop; Appendix A.3 block inverse of H) is
+//
+//   f      = Q (T abar) + bbar                      (first path GEMM)
+//   z      = psi(y, f) / n_v,  d0 = 1'z             (its epilogue)
+//   zhat   = Q' z                                   (second path GEMM)
+//   w      = zhat + 2 lambda abar                   (= Q'(z + 2 lambda alpha))
+//   t      = vhat' T w                              (= v' K (z + 2 lambda alpha))
+//   x      = (2 lambda I + T/(n_v kappa))^{-1} w    (tridiagonal solve)
+//   Da     = g (t - d0) vhat + x,   Db = g (d0 - t)
+//   a_new  = abar - Da,             b_new = bbar - Db
+//
+// with vhat = (2 lambda I + T/(n_v kappa))^{-1} Q'1 / (n_v kappa) and
+// g = 1/(2 lambda (Q'1)' vhat) precomputed once per smoothing stage. These
+// are the paper's v and g taken as the exact Schur complement of the
+// (n+1)-square majoriser H = [[1/kappa, 1'K/(n kappa)], [K1/(n kappa),
+// 2 lambda K + K K/(n kappa)]], written in the basis Q instead of the
+// eigenvectors. The column stops when n_v max(||w||_2, |d0|) <= tol at the
+// extrapolated point, which it then keeps.
+#include "kmp_common.h"
+#include "kmp_kernels.h"
+
+namespace kmp {
+
+constexpr int PB = 256;   // threads per column workgroup
+constexpr int PW = 4;
+
+// ------------------------------------------------------------- small setup
+__global__ void gather_labels_kernel(const double* __restrict__ y, const int32_t* __restrict__ tidx,
+                                     int V, int S_b, int N, double* __restrict__ ylab) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t tot = (int64_t)S_b * V * N;
+  if (idx >= tot) return;
+  const int64_t i = idx % N;
+  const int64_t g = idx / N;
+  const int v = (int)(g % V);
+  const int32_t src = tidx[(int64_t)v * N + i];
+  ylab[idx] = src >= 0 ? y[src] : 0.0;
+}
+
+int gather_labels(hipStream_t s, const double* y, const int32_t* tidx, int V, int S_b, int N,
+                  double* ylab) {
+  const int64_t tot = (int64_t)S_b * V * N;
+  hipLaunchKernelGGL(gather_labels_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, s, y,
+                     tidx, V, S_b, N, ylab);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
+// c = Q'1 over the valid rows of each group (one thread per column of Q).
+__global__ void ones_projection_kernel(const double* __restrict__ Q, const int* __restrict__ nv,
+                                       int G, int N, double* __restrict__ cvec) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)G * N) return;
+  const int g = (int)(idx / N), j = (int)(idx % N);
+  const double* Qg = Q + (int64_t)g * N * N;
+  const int m = nv[g];
+  double s = 0.0;
+  for (int i = 0; i < m; ++i) s += Qg[(int64_t)i * N + j];
+  cvec[idx] = s;
+}
+
+int group_ones_projection(hipStream_t s, const double* Q, const int* nv, int G, int N, double* cvec) {
+  const int64_t tot = (int64_t)G * N;
+  hipLaunchKernelGGL(ones_projection_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, s, Q,
+                     nv, G, N, cvec);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
+int path_init_columns(hipStream_t s, const PathArrays& p) {
+  const size_t cols = (size_t)p.G * p.C;
+  const size_t vec = cols * p.N * sizeof(double);
+  KMP_HIP_TRY(hipMemsetAsync(p.ahat, 0, vec, s));
+  KMP_HIP_TRY(hipMemsetAsync(p.abar, 0, vec, s));
+  KMP_HIP_TRY(hipMemsetAsync(p.bmat, 0, vec, s));
+  KMP_HIP_TRY(hipMemsetAsync(p.beta, 0, cols * sizeof(double), s));
+  KMP_HIP_TRY(hipMemsetAsync(p.bbar, 0, cols * sizeof(double), s));
+  KMP_HIP_TRY(hipMemsetAsync(p.flag, 0, cols * sizeof(int), s));
+  KMP_HIP_TRY(hipMemsetAsync(p.iters, 0, cols * sizeof(int), s));
+  KMP_HIP_TRY(hipMemsetAsync(p.iters_total, 0, cols * sizeof(int), s));
+  return 0;
+}
+
+// ------------------------------------------------------ per-stage factors
+// One thread per column: LDL' of M = 2 lambda I + T/(n_v kappa), then
+// vhat = M^{-1} c/(n_v kappa), u = T vhat, g = 1/(2 lambda c'vhat); restart
+// the momentum (r = 1, abar = ahat) and reactivate converged columns.
+__global__ void precompute_kernel(int G, int N, int C, const int* __restrict__ nv,
+                                  const double* __restrict__ Td, const double* __restrict__ To,
+                                  const double* __restrict__ cvec, const double* __restrict__ lamv,
+                                  double kappa, double* __restrict__ ldl_l, double* __restrict__ ldl_d,
+                                  double* __restrict__ vhat, double* __restrict__ uvec,
+                                  double* __restrict__ gcoef, double* __restrict__ ahat,
+                                  double* __restrict__ abar, double* __restrict__ bmat,
+                                  double* __restrict__ beta, double* __restrict__ bbar,
+                                  double* __restrict__ rmom, int* __restrict__ flag,
+                                  int* __restrict__ iters) {
+  const int64_t gc = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gc >= (int64_t)G * C) return;
+  const int g = (int)(gc / C);
+  const double lam = lamv[gc];
+  const double sc = 1.0 / ((double)nv[g] * kappa);
+  const double* d = Td + (int64_t)g * N;
+  const double* o = To + (int64_t)g * N;
+  const double* c = cvec + (int64_t)g * N;
+  double* L = ldl_l + gc * N;
+  double* Di = ldl_d + gc * N;
+  double* vh = vhat + gc * N;
+  double* u = uvec + gc * N;
+  // factor and forward substitution with rhs c*sc
+  double dprev = 2.0 * lam + d[0] * sc;
+  double yprev = c[0] * sc;
+  Di[0] = 1.0 / dprev;
+  vh[0] = yprev;
+  for (int i = 1; i < N; ++i) {
+    const double oi = o[i - 1] * sc;
+    const double li = oi / dprev;
+    L[i - 1] = li;
+    dprev = 2.0 * lam + d[i] * sc - li * oi;
+    Di[i] = 1.0 / dprev;
+    yprev = c[i] * sc - li * yprev;
+    vh[i] = yprev;
+  }
+  L[N - 1] = 0.0;
+  // diagonal and back substitution
+  double xnext = vh[N - 1] * Di[N - 1];
+  vh[N - 1] = xnext;
+  for (int i = N - 2; i >= 0; --i) {
+    xnext = vh[i] * Di[i] - L[i] * xnext;
+    vh[i] = xnext;
+  }
+  double cv = 0.0;
+  for (int i = 0; i < N; ++i) {
+    double ui = d[i] * vh[i];
+    if (i > 0) ui += o[i - 1] * vh[i - 1];
+    if (i + 1 < N) ui += o[i] * vh[i + 1];
+    u[i] = ui;
+    cv += c[i] * vh[i];
+  }
+  gcoef[gc] = 1.0 / (2.0 * lam * cv);
+  // stage restart of the accelerated iteration
+  double* ah = ahat + gc * N;
+  double* ab = abar + gc * N;
+  double* bm = bmat + gc * N;
+  for (int i = 0; i < N; ++i) ab[i] = ah[i];
+  for (int i = 0; i < N; ++i) {
+    double b = d[i] * ah[i];
+    if (i > 0) b += o[i - 1] * ah[i - 1];
+    if (i + 1 < N) b += o[i] * ah[i + 1];
+    bm[i] = b;
+  }
+  bbar[gc] = beta[gc];
+  rmom[gc] = 1.0;
+  if (flag[gc] == 1 || flag[gc] == 2) flag[gc] = 0;
+  iters[gc] = 0;
+}
+
+int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa) {
+  const int64_t cols = (int64_t)p.G * p.C;
+  hipLaunchKernelGGL(precompute_kernel, dim3((unsigned)ceil_div(cols, 64)), dim3(64), 0, s, p.G,
+                     p.N, p.C, p.nv, p.Tdiag, p.Toff, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
+                     p.uvec, p.gcoef, p.ahat, p.abar, p.bmat, p.beta, p.bbar, p.rmom, p.flag,
+                     p.iters);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
+// ---------------------------------------------------------- scan helpers
+// Affine map x -> a x + b; compose(second, first) = second o first.
+struct Aff {
+  double a, b;
+};
+__device__ __forceinline__ Aff compose(Aff second, Aff first) {
+  return Aff{second.a * first.a, fma(second.a, first.b, second.b)};
+}
+
+// Exclusive prefix composition across the block in thread order (thread t
+// receives map_{t-1} o ... o map_0, identity for t = 0). `sh` holds PW Affs.
+__device__ __forceinline__ Aff block_exclusive_scan(Aff m, Aff* sh) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  Aff inc = m;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double pa = __shfl_up(inc.a, off, 64);
+    const double pb = __shfl_up(inc.b, off, 64);
+    if (lane >= off) inc = compose(inc, Aff{pa, pb});
+  }
+  // exclusive within the wave
+  double ea = __shfl_up(inc.a, 1, 64), eb = __shfl_up(inc.b, 1, 64);
+  Aff ex = lane == 0 ? Aff{1.0, 0.0} : Aff{ea, eb};
+  __syncthreads();
+  if (lane == 63) sh[w] = inc;
+  __syncthreads();
+  Aff pre{1.0, 0.0};
+  for (int k = 0; k < w; ++k) pre = compose(sh[k], pre);
+  return compose(ex, pre);
+}
+
+// Same in reverse thread order (thread t receives map_{t+1} o ... o map_last).
+__device__ __forceinline__ Aff block_exclusive_scan_rev(Aff m, Aff* sh) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  Aff inc = m;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double pa = __shfl_down(inc.a, off, 64);
+    const double pb = __shfl_down(inc.b, off, 64);
+    if (lane + off < 64) inc = compose(inc, Aff{pa, pb});
+  }
+  double ea = __shfl_down(inc.a, 1, 64), eb = __shfl_down(inc.b, 1, 64);
+  Aff ex = lane == 63 ? Aff{1.0, 0.0} : Aff{ea, eb};
+  __syncthreads();
+  if (lane == 0) sh[w] = inc;
+  __syncthreads();
+  Aff pre{1.0, 0.0};
+  for (int k = PW - 1; k > w; --k) pre = compose(sh[k], pre);
+  return compose(ex, pre);
+}
+
+// ------------------------------------------------------- the update (K2)
+// One workgroup per column; thread t owns rows [t*E, t*E + E).
+template <int E>
+__global__ __launch_bounds__(PB) void update_kernel(
+    int N, int C, int RT, const int* __restrict__ nvv, const double* __restrict__ Td,
+    const double* __restrict__ To, const double* __restrict__ lamv,
+    const double* __restrict__ zhat, double* __restrict__ ahat, double* __restrict__ abar,
+    double* __restrict__ bmat, const double* __restrict__ ldl_l, const double* __restrict__ ldl_d,
+    const double* __restrict__ vhat, const double* __restrict__ uvec,
+    const double* __restrict__ gcoef, const double* __restrict__ partial,
+    double* __restrict__ beta, double* __restrict__ bbar, double* __restrict__ rmom,
+    double* __restrict__ kktv, int* __restrict__ flag, int* __restrict__ iters,
+    int* __restrict__ iters_total, double tol, int max_iter, int restart) {
+  __shared__ double red[PW];
+  __shared__ Aff sh[PW];
+  __shared__ double edge_lo[PB], edge_hi[PB];
+  const int64_t gc = blockIdx.x;
+  if (flag[gc] != 0) return;
+  const int g = (int)(gc / C), c = (int)(gc % C);
+  const int t = threadIdx.x;
+  const int i0 = t * E;
+  const int64_t base = gc * N;
+  const double lam = lamv[gc];
+  const double nvd = (double)nvv[g];
+  const double* Tdg = Td + (int64_t)g * N;
+  const double* Tog = To + (int64_t)g * N;
+
+  double d0 = 0.0;
+  {
+    const double* pg = partial + (int64_t)g * RT * C + c;
+    for (int r = 0; r < RT; ++r) d0 += pg[(int64_t)r * C];
+  }
+  double wv[E], ab[E], ah[E];
+  double tl = 0.0, n2 = 0.0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = i0 + e;
+    if (i < N) {
+      ab[e] = abar[base + i];
+      ah[e] = ahat[base + i];
+      wv[e] = fma(2.0 * lam, ab[e], zhat[base + i]);
+      tl = fma(uvec[base + i], wv[e], tl);
+      n2 = fma(wv[e], wv[e], n2);
+    } else {
+      ab[e] = ah[e] = wv[e] = 0.0;
+    }
+  }
+  const double tsum = block_sum<PW>(tl, red);
+  const double n2sum = block_sum<PW>(n2, red);
+  const double kkt = nvd * fmax(sqrt(n2sum), fabs(d0));
+  const double bb = bbar[gc];
+  if (!(kkt == kkt) || kkt > 1e300) {          // non-finite
+    if (t == 0) { flag[gc] = 3; kktv[gc] = kkt; }
+    return;
+  }
+  if (kkt <= tol) {                            // certified at the extrapolated point
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (i0 + e < N) ahat[base + i0 + e] = ab[e];
+    if (t == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; }
+    return;
+  }
+  // forward solve L y = w  (y_i = w_i - l_{i-1} y_{i-1})
+  double lv[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) lv[e] = (i0 + e < N) ? ldl_l[base + i0 + e] : 0.0;
+  const double lprev = (i0 > 0 && i0 - 1 < N) ? ldl_l[base + i0 - 1] : 0.0;
+  Aff m{1.0, 0.0};
+  {
+    double ca = 1.0, cb = 0.0, lp = lprev;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      ca = -lp * ca;
+      cb = fma(-lp, cb, wv[e]);
+      lp = lv[e];
+    }
+    m = Aff{ca, cb};
+  }
+  Aff pre = block_exclusive_scan(m, sh);
+  {
+    double yin = pre.b;                       // y_{i0-1} (maps applied to 0)
+    double lp = lprev;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const double yi = fma(-lp, yin, wv[e]);
+      wv[e] = yi;
+      yin = yi;
+      lp = lv[e];
+    }
+  }
+  // diagonal: z_i = y_i / d_i
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    if (i0 + e < N) wv[e] *= ldl_d[base + i0 + e];
+  // backward solve L' x = z  (x_i = z_i - l_i x_{i+1})
+  {
+    double ca = 1.0, cb = 0.0;
+#pragma unroll
+    for (int e = E - 1; e >= 0; --e) {
+      ca = -lv[e] * ca;
+      cb = fma(-lv[e], cb, wv[e]);
+    }
+    m = Aff{ca, cb};
+  }
+  pre = block_exclusive_scan_rev(m, sh);
+  {
+    double xin = pre.b;                       // x_{i0+E}
+#pragma unroll
+    for (int e = E - 1; e >= 0; --e) {
+      const double xi = fma(-lv[e], xin, wv[e]);
+      wv[e] = xi;
+      xin = xi;
+    }
+  }
+  // step, new iterate and the restart test
+  const double gco = gcoef[gc];
+  const double sa = gco * (tsum - d0);
+  const double db = gco * (d0 - tsum);
+  const double bn = bb - db;
+  const double bold = beta[gc];
+  double rd = 0.0;
+  double an[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = i0 + e;
+    double da = 0.0;
+    if (i < N) da = fma(sa, vhat[base + i], wv[e]);
+    an[e] = ab[e] - da;
+    rd = fma(da, an[e] - ah[e], rd);
+  }
+  rd = block_sum<PW>(rd, red) + db * (bn - bold);
+  const double r = rmom[gc];
+  const double rn = (restart && rd > 0.0) ? 1.0 : 0.5 * (1.0 + sqrt(1.0 + 4.0 * r * r));
+  const double coef = (rn - 1.0) / (0.5 * (1.0 + sqrt(1.0 + 4.0 * rn * rn)));
+  double nb_[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) nb_[e] = fma(coef, an[e] - ah[e], an[e]);
+  edge_lo[t] = nb_[0];
+  edge_hi[t] = nb_[E - 1];
+  __syncthreads();
+  const double left = t > 0 ? edge_hi[t - 1] : 0.0;
+  const double right = t + 1 < PB ? edge_lo[t + 1] : 0.0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = i0 + e;
+    if (i < N) {
+      const double xl = e > 0 ? nb_[e - 1] : left;
+      const double xr = e + 1 < E ? nb_[e + 1] : right;
+      double bv = Tdg[i] * nb_[e];
+      if (i > 0) bv = fma(Tog[i - 1], xl, bv);
+      if (i + 1 < N) bv = fma(Tog[i], xr, bv);
+      ahat[base + i] = an[e];
+      abar[base + i] = nb_[e];
+      bmat[base + i] = bv;
+    }
+  }
+  if (t == 0) {
+    beta[gc] = bn;
+    bbar[gc] = fma(coef, bn - bold, bn);
+    rmom[gc] = rn;
+    kktv[gc] = kkt;
+    const int it = iters[gc] + 1;
+    iters[gc] = it;
+    iters_total[gc] += 1;
+    if (it >= max_iter) flag[gc] = 2;
+  }
+}
+
+int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kappa, double tol,
+                   int max_iter, int restart) {
+  (void)kappa;
+  int rc;
+  const int RT = (int)ceil_div(p.N, kGemmTile);
+  // f = Q (T abar) + bbar and z = psi(y, f)/n_v, with per-tile column sums
+  GemmArgs g1;
+  g1.M = p.N; g1.N = p.C; g1.K = p.N; g1.batch = p.G;
+  g1.A = p.Q; g1.lda = p.N; g1.sA = (int64_t)p.N * p.N;
+  g1.B = p.bmat; g1.ldb = p.N; g1.sB = (int64_t)p.N * p.C;
+  g1.C = p.zmat; g1.ldc = p.N; g1.sC = (int64_t)p.N * p.C;
+  LossEpi e;
+  e.loss = p.loss; e.delta = delta;
+  e.y = p.ylab; e.sy = p.N; e.nv = p.nv;
+  e.bbar = p.bbar; e.sbb = p.C; e.tau = p.tau; e.stau = p.C;
+  e.partial = p.partial; e.spart = (int64_t)RT * p.C;
+  if ((rc = gemm_loss(s, g1, e)) != 0) return rc;
+  // zhat = Q' z
+  GemmArgs g2;
+  g2.M = p.N; g2.N = p.C; g2.K = p.N; g2.batch = p.G;
+  g2.A = p.Q; g2.lda = p.N; g2.sA = (int64_t)p.N * p.N;
+  g2.B = p.zmat; g2.ldb = p.N; g2.sB = (int64_t)p.N * p.C;
+  g2.C = p.zhat; g2.ldc = p.N; g2.sC = (int64_t)p.N * p.C;
+  if ((rc = gemm(s, g2, false, true, false)) != 0) return rc;
+  const unsigned cols = (unsigned)(p.G * p.C);
+#define KMP_UPD(EE)                                                                              \
+  hipLaunchKernelGGL(update_kernel<EE>, dim3(cols), dim3(PB), 0, s, p.N, p.C, RT, p.nv, p.Tdiag, \
+                     p.Toff, p.lam, p.zhat, p.ahat, p.abar, p.bmat, p.ldl_l, p.ldl_d, p.vhat,    \
+                     p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt, p.flag, p.iters, \
+                     p.iters_total, tol, max_iter, restart)
+  if (p.N <= PB * 1) KMP_UPD(1);
+  else if (p.N <= PB * 2) KMP_UPD(2);
+  else if (p.N <= PB * 4) KMP_UPD(4);
+  else if (p.N <= PB * 8) KMP_UPD(8);
+  else if (p.N <= PB * 16) KMP_UPD(16);
+  else if (p.N <= PB * 32) KMP_UPD(32);
+  else {
+    set_error("path: more than 8192 training points per fold is not supported yet");
+    return KMP_EINVAL;
+  }
+#undef KMP_UPD
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
+__global__ void count_active_kernel(const int* __restrict__ flag, int64_t cols, int* __restrict__ out) {
+  __shared__ double red[PW];
+  double c = 0.0;
+  for (int64_t i = threadIdx.x; i < cols; i += blockDim.x) c += (flag[i] == 0) ? 1.0 : 0.0;
+  c = block_sum<PW>(c, red);
+  if (threadIdx.x == 0) *out = (int)c;
+}
+
+int path_count_active(hipStream_t s, const PathArrays& p) {
+  hipLaunchKernelGGL(count_active_kernel, dim3(1), dim3(PB), 0, s, p.flag, (int64_t)p.G * p.C,
+                     p.active_count);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
+// --------------------------------------------------------------- finalize
+// f[g][c][i] = sum_{j < n_v} K(x_i, x_{T[j]}) alpha[g][c][j] + beta, for all
+// n points, with the kernel entries recomputed from X (norm expansion, the
+// same formula as the Gram build) into LDS and contracted on matrix cores.
+typedef double dbl4 __attribute__((ext_vector_type(4)));
+constexpr int FT = 64, FK = 16, FPAD = 4;
+
+__global__ __launch_bounds__(256) void predict_kernel(
+    int n, int d, int64_t ldx, const double* __restrict__ X, const double* __restrict__ nrm,
+    const int32_t* __restrict__ tidx, int V, int N, int C, const int* __restrict__ nvv,
+    const double* __restrict__ inv2s2, const double* __restrict__ alpha_loc,
+    const double* __restrict__ betav, double* __restrict__ fbuf) {
+  __shared__ double Ks[FK][FT + FPAD];
+  __shared__ double Bs[FK][FT + FPAD];
+  __shared__ int32_t cj[FK];
+  const int g = blockIdx.z;
+  const int v = g % V, sl = g / V;
+  const int i0 = blockIdx.x * FT, c0 = blockIdx.y * FT;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int wi = (w & 1) * 32, wj = (w >> 1) * 32;
+  const int li = lane & 15, lk = lane >> 4;
+  const int nv = nvv[g];
+  const double f2 = inv2s2[sl];
+  const int32_t* T = tidx + (int64_t)v * N;
+  const double* A = alpha_loc + (int64_t)g * C * N;
+  dbl4 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = dbl4{0.0, 0.0, 0.0, 0.0};
+  for (int j0 = 0; j0 < nv; j0 += FK) {
+    __syncthreads();
+    if (t < FK) cj[t] = (j0 + t < nv) ? T[j0 + t] : -1;
+    __syncthreads();
+    // kernel tile: rows i0..i0+63 (points), cols j0..j0+15 (training points)
+    for (int e = t; e < FT * FK; e += 256) {
+      const int ii = e / FK, kk = e % FK;
+      const int gi = i0 + ii;
+      const int32_t xc = cj[kk];
+      double kv = 0.0;
+      if (gi < n && xc >= 0) {
+        if (gi == xc) {
+          kv = 1.0;
+        } else {
+          const double* xa = X + (int64_t)gi * ldx;
+          const double* xb = X + (int64_t)xc * ldx;
+          double dot = 0.0;
+          for (int q = 0; q < d; ++q) dot = fma(xa[q], xb[q], dot);
+          double d2 = nrm[gi] + nrm[xc] - 2.0 * dot;
+          d2 = d2 > 0.0 ? d2 : 0.0;
+          kv = exp(-d2 * f2);
+        }
+      }
+      Ks[kk][ii] = kv;
+    }
+    // coefficient tile: rows j0..j0+15, cols c0..c0+63
+    for (int e = t; e < FK * FT; e += 256) {
+      const int kk = e % FK, cc = e / FK;
+      const int gj = j0 + kk, gcn = c0 + cc;
+      Bs[kk][cc] = (gj < nv && gcn < C) ? A[(int64_t)gcn * N + gj] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < FK; kk += 4) {
+      const double a0 = Ks[kk + lk][wi + li];
+      const double a1 = Ks[kk + lk][wi + 16 + li];
+      const double b0 = Bs[kk + lk][wj + li];
+      const double b1 = Bs[kk + lk][wj + 16 + li];
+      acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int gi = i0 + wi + bi * 16 + mfma_row(lane, r);
+        const int gcn = c0 + wj + bj * 16 + mfma_col(lane);
+        if (gi < n && gcn < C)
+          fbuf[((int64_t)g * C + gcn) * n + gi] = acc[bi][bj][r] + betav[(int64_t)g * C + gcn];
+      }
+}
+
+// One workgroup per column: objective on the training points, CV sums on the
+// held-out points, scatter of alpha into the output layout.
+__global__ __launch_bounds__(256) void cv_reduce_kernel(
+    int n, int N, int C, int V, int Qt, int L, int s0, int loss, double delta,
+    const double* __restrict__ y, const int32_t* __restrict__ fold, const int32_t* __restrict__ tidx,
+    const int* __restrict__ nvv, const double* __restrict__ lamv, const double* __restrict__ tauv,
+    const double* __restrict__ alpha_loc, const double* __restrict__ fbuf,
+    const double* __restrict__ betav, const int* __restrict__ flag,
+    const int* __restrict__ iters_total, double* __restrict__ alpha_out,
+    double* __restrict__ beta_out, double* __restrict__ obj_out, double* __restrict__ cv_out,
+    int32_t* __restrict__ err_out, int32_t* __restrict__ it_out, int32_t* __restrict__ st_out) {
+  __shared__ double red[PW];
+  const int64_t gc = blockIdx.x;
+  const int g = (int)(gc / C), c = (int)(gc % C);
+  const int v = g % V, sl = g / V;
+  const int q = c / L, l = c % L;
+  const int64_t cell = (((int64_t)(s0 + sl) * Qt + q) * V + v) * L + l;
+  const int nv = nvv[g];
+  const double lam = lamv[gc], tau = tauv[gc], b = betav[gc];
+  const double* A = alpha_loc + gc * N;
+  const double* f = fbuf + gc * n;
+  const int32_t* T = tidx + (int64_t)v * N;
+  double* aout = alpha_out + cell * n;
+  double ls = 0.0, pen = 0.0;
+  for (int j = threadIdx.x; j < nv; j += blockDim.x) {
+    const int32_t i = T[j];
+    const double fi = f[i];
+    ls += loss_value(loss, y[i], fi, delta, tau);
+    pen = fma(A[j], fi - b, pen);
+    aout[i] = A[j];
+  }
+  double cs = 0.0, ce = 0.0;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    if (fold[i] != v) continue;
+    const double fi = f[i];
+    cs += loss_eval(loss, y[i], fi, tau);
+    if (loss != 2 && y[i] * fi <= 0.0) ce += 1.0;
+  }
+  ls = block_sum<PW>(ls, red);
+  pen = block_sum<PW>(pen, red);
+  cs = block_sum<PW>(cs, red);
+  ce = block_sum<PW>(ce, red);
+  if (threadIdx.x == 0) {
+    beta_out[cell] = b;
+    obj_out[cell] = ls / (double)nv + lam * pen;
+    cv_out[cell] = cs;
+    if (err_out) err_out[cell] = (int32_t)ce;
+    if (it_out) it_out[cell] = iters_total[gc];
+    if (st_out) {
+      const int fl = flag[gc];
+      st_out[cell] = fl == 1 ? 0 : (fl == 3 ? 2 : 1);
+    }
+  }
+}
+
+int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
+  int rc;
+  // alpha_loc = Q ahat (into zmat)
+  GemmArgs g;
+  g.M = p.N; g.N = p.C; g.K = p.N; g.batch = p.G;
+  g.A = p.Q; g.lda = p.N; g.sA = (int64_t)p.N * p.N;
+  g.B = p.ahat; g.ldb = p.N; g.sB = (int64_t)p.N * p.C;
+  g.C = p.zmat; g.ldc = p.N; g.sC = (int64_t)p.N * p.C;
+  if ((rc = gemm(s, g, true, true, false)) != 0) return rc;
+  dim3 grid((unsigned)ceil_div(fa.n, FT), (unsigned)ceil_div(p.C, FT), (unsigned)p.G);
+  hipLaunchKernelGGL(predict_kernel, grid, dim3(256), 0, s, fa.n, fa.d, fa.ldx, fa.X, fa.nrm,
+                     fa.tidx, fa.V, p.N, p.C, p.nv, fa.inv2s2, p.zmat, p.beta, fa.fbuf);
+  KMP_LAUNCH_CHECK();
+  hipLaunchKernelGGL(cv_reduce_kernel, dim3((unsigned)(p.G * p.C)), dim3(256), 0, s, fa.n, p.N,
+                     p.C, fa.V, fa.Qt, fa.L, fa.s0, p.loss, fa.delta, fa.y, fa.fold, fa.tidx, p.nv,
+                     p.lam, p.tau, p.zmat, fa.fbuf, p.beta, p.flag, p.iters_total, fa.alpha,
+                     fa.beta_out, fa.objective, fa.cv_sum, fa.cv_err, fa.iters, fa.status);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
+}  // namespace kmp

@@ -1,0 +1,73 @@
+"""Shared helpers for the GPU tests (parity bars and announcements)."""
+import sys
+
+import numpy as np
+
+from oracle import gram as OG
+from oracle import losses as OL
+
+OBJ_RTOL = 1e-8      # objectives, relative
+ALPHA_RTOL = 1e-6    # coefficients, relative to max |alpha|
+CV_RTOL = 1e-6       # held-out loss sums
+
+
+def announce(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def device():
+    import torch
+    if not torch.cuda.is_available():
+        raise RuntimeError("GPU test run without a visible HIP device")
+    return torch.device("cuda")
+
+
+def compare_cells(g, o, inp, loss, cells=None, delta=2.0 ** -6):
+    """Element-wise parity of GPU results g against oracle results o.
+
+    cells: iterable of (s, q, v, l) to check, default all. Returns the worst
+    relative errors seen, for reporting.
+    """
+    S, Q, V, L = g["objective"].shape
+    X, y, fold = inp["X"], inp["y"], inp["fold_id"]
+    worst = {"obj": 0.0, "alpha": 0.0, "beta": 0.0, "cv": 0.0}
+    if cells is None:
+        cells = [(s, q, v, l) for s in range(S) for q in range(Q) for v in range(V) for l in range(L)]
+    blocks = {}
+    for (s, q, v, l) in cells:
+        key = (s, v)
+        if key not in blocks:
+            blocks[key] = OG.fold_blocks(X, fold, v, inp["sigmas"][s])
+        Kv, Kc, T, H = blocks[key]
+        tau = inp["taus"][q] if loss == "check" else None
+        Fo, Fg = o["objective"][s, q, v, l], g["objective"][s, q, v, l]
+        assert abs(Fg - Fo) <= OBJ_RTOL * abs(Fo), ((s, q, v, l), Fg, Fo)
+        worst["obj"] = max(worst["obj"], abs(Fg - Fo) / abs(Fo))
+        ao, ag = o["alpha"][s, q, v, l], g["alpha"][s, q, v, l]
+        assert np.all(ag[H] == 0.0)
+        scale = np.abs(ao).max()
+        err = np.abs(ag - ao).max()
+        assert err <= ALPHA_RTOL * scale + 1e-15, ((s, q, v, l), err, scale)
+        worst["alpha"] = max(worst["alpha"], err / max(scale, 1e-300))
+        bo, bg = o["beta"][s, q, v, l], g["beta"][s, q, v, l]
+        lo, hi = o["beta_lo"][s, q, v, l], o["beta_hi"][s, q, v, l]
+        btol = ALPHA_RTOL * max(1.0, abs(bo))
+        assert lo - btol <= bg <= hi + btol, ((s, q, v, l), bg, bo, lo, hi)
+        if lo == hi:
+            worst["beta"] = max(worst["beta"], abs(bg - bo) / max(1.0, abs(bo)))
+        co, cg = o["cv_sum"][s, q, v, l], g["cv_sum"][s, q, v, l]
+        assert abs(cg - co) <= CV_RTOL * max(1.0, abs(co)), ((s, q, v, l), cg, co)
+        worst["cv"] = max(worst["cv"], abs(cg - co) / max(1.0, abs(co)))
+        if loss != "check":
+            fH = Kc @ ao[T] + bo
+            border = int(np.count_nonzero(np.abs(fH) < 1e-6))
+            assert abs(int(g["cv_err"][s, q, v, l]) - int(o["cv_err"][s, q, v, l])) <= border
+    return worst
+
+
+def kkt_of(Kv, yT, a, b, lam, loss, delta, tau):
+    n = yT.shape[0]
+    f = Kv @ a + b
+    z = OL.point_psi(loss, yT, f, delta, tau) / n
+    return n * max(np.abs(z + 2 * lam * a).max(), abs(z.sum()))

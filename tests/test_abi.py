@@ -1,0 +1,119 @@
+"""The C-ABI library on the host: symbols, fold generator, validation errors.
+
+No GPU is needed: every call here returns before the library touches the
+device (argument errors are detected on the host first).
+"""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kmpath.h")
+
+
+@pytest.fixture(scope="module")
+def km():
+    from paper_2606_06742_amd import kmpath
+    if not os.path.exists(kmpath.LIB_PATH):
+        from paper_2606_06742_amd import build
+        build.build()
+    kmpath.lib()
+    return kmpath
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kmp_[a-z_]+)\s*\(", src)))
+
+
+def test_header_symbols_exported(km):
+    names = _declared()
+    assert {"kmp_fit_path", "kmp_workspace_bytes", "kmp_make_folds", "kmp_rbf_gram",
+            "kmp_tridiag", "kmp_strerror", "kmp_version", "kmp_default_spec"} <= set(names)
+    L = km.lib()
+    for name in names:
+        assert hasattr(L, name), name
+    assert set(km.EXPORTED) == set(names)
+
+
+def test_make_folds_bit_exact(km):
+    for n, V, seed in [(200, 5, 2001), (2000, 5, 2002), (10000, 10, 2003), (203, 5, 9), (5, 5, 0),
+                       (17, 3, 2 ** 63 + 12345)]:
+        assert np.array_equal(km.kmp_make_folds(n, V, seed), W.make_folds(n, V, seed))
+
+
+def test_default_spec(km):
+    s = km.kmp_default_spec("logistic")
+    assert s.loss == km.KMP_LOGISTIC and s.delta0 == 1.0 and s.eta == 0.125
+    assert s.n_stages == 3 and s.tol == 1e-9 and s.flags & km.KMP_FLAG_RESTART
+
+
+def test_workspace_bytes(km):
+    w = W.get("C2")
+    fold = W.make_folds(w.n, w.V, w.fold_seed)
+    spec = km.kmp_default_spec("logistic")
+    b3 = km.kmp_workspace_bytes(spec, w.n, w.d, w.L, fold, w.V, 3, 1, 3)
+    b1 = km.kmp_workspace_bytes(spec, w.n, w.d, w.L, fold, w.V, 3, 1, 1)
+    N = 1600
+    assert b3 > 3 * 5 * 2 * N * N * 8 and b1 < b3 and b1 > 5 * 2 * N * N * 8
+    assert km.kmp_workspace_bytes(spec, w.n, w.d, w.L, fold, w.V, 3, 1, 4) == 0
+    bad = fold.copy()
+    bad[0] = 7
+    assert km.kmp_workspace_bytes(spec, w.n, w.d, w.L, bad, w.V, 3, 1, 1) == 0
+
+
+class _Fake:
+    """Stands in for a device tensor in calls that fail validation first."""
+
+    def __init__(self, shape, ptr=0x1000):
+        self.shape = shape
+        self._ptr = ptr
+
+    def data_ptr(self):
+        return self._ptr
+
+    def stride(self, i):
+        return self.shape[1] if i == 0 else 1
+
+
+def _call(km, loss="hinge", n=20, d=3, sigmas=(1.0,), lambdas=(0.1, 1.0), fold=None, V=4,
+          taus=(0.5,), ws=1 << 20, spec=None):
+    fold = np.arange(n) % V if fold is None else fold
+    spec = spec or km.kmp_default_spec(loss)
+    X, y = _Fake((n, d)), _Fake((n,))
+    out = _Fake((1,))
+    return km.kmp_fit_path(None, spec, X, y, np.array(sigmas), np.array(taus), np.array(lambdas),
+                           fold, V, 0x2000, ws, out, out, out, out, None, None, None, None, None)
+
+
+def test_fit_path_argument_errors(km):
+    assert _call(km, sigmas=(0.0,)) == km.KMP_EINVAL
+    assert _call(km, sigmas=(np.inf,)) == km.KMP_EINVAL
+    assert _call(km, lambdas=(0.1, -1.0)) == km.KMP_EINVAL
+    assert _call(km, loss="check", taus=(1.0,)) == km.KMP_EINVAL
+    assert _call(km, loss="check", taus=(0.0,)) == km.KMP_EINVAL
+    fold = np.arange(20) % 4
+    fold[3] = 9
+    assert _call(km, fold=fold) == km.KMP_EFOLD
+    assert _call(km, fold=np.arange(20) % 3, V=4) == km.KMP_EFOLD       # fold 3 empty
+    assert _call(km, V=1, fold=np.zeros(20, dtype=np.int32)) == km.KMP_EINVAL
+    spec = km.kmp_default_spec("hinge", eta=1.5)
+    assert _call(km, spec=spec) == km.KMP_EINVAL
+    spec = km.kmp_default_spec("hinge", tol=0.0)
+    assert _call(km, spec=spec) == km.KMP_EINVAL
+    assert "fold" in km.kmp_strerror(km.KMP_EFOLD) or km.kmp_strerror(km.KMP_EFOLD)
+    assert km.kmp_version().startswith("kmpath")
+
+
+def test_binding_refuses_missing_library(monkeypatch):
+    from paper_2606_06742_amd import kmpath
+    monkeypatch.setattr(kmpath, "_lib", None)
+    monkeypatch.setattr(kmpath, "LIB_PATH", "/nonexistent/libkmpath.so")
+    with pytest.raises(RuntimeError):
+        kmpath.lib()

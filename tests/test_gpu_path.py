@@ -1,0 +1,97 @@
+"""The whole CV path (kmp_fit_path) against the oracle, cell by cell.
+
+Bars: objectives within 1e-8 relative, coefficients within 1e-6 of
+max |alpha|, intercepts within 1e-6 (or inside the oracle's optimal
+interval when the intercept is not unique), held-out loss sums within 1e-6,
+selected lambda index identical.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from oracle import gram as OG
+from tests.gpu_common import announce, compare_cells, device, kkt_of
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu(inp, loss, **spec):
+    from paper_2606_06742_amd import kmpath as km
+    device()
+    taus = inp["taus"] if loss == "check" else None
+    r = km.fit_path(inp["X"], inp["y"], loss, inp["sigmas"], inp["lambdas"], inp["fold_id"],
+                    inp["V"], taus=taus, **{"max_iter": 20000, **spec})
+    assert r["code"] == 0, r["code"]
+    assert np.all(r["status"] == 0)
+    return r
+
+
+def _oracle(inp, loss):
+    return oracle.fit_path(inp["X"], inp["y"], loss, inp["sigmas"], inp["lambdas"], inp["fold_id"],
+                           inp["V"], taus=inp["taus"] if loss == "check" else None,
+                           workers=oracle.path.default_workers())
+
+
+def test_path_c1_full_parity():
+    inp = W.make_inputs(W.get("C1"))
+    announce("fit_path C1 (hinge, n=200, 5 folds, 10 lambdas)")
+    g = _gpu(inp, "hinge")
+    o = _oracle(inp, "hinge")
+    worst = compare_cells(g, o, inp, "hinge")
+    assert np.array_equal(g["selected"], o["selected"].astype(np.int32))
+    print("C1 worst relative errors", worst, "iterations", g["timings"]["cell_iterations"])
+
+
+@pytest.mark.parametrize("loss", ["hinge", "logistic", "check"])
+def test_path_small_ragged(loss):
+    inp = W.small_problem(loss, 203, 5, seed=41, V=5, L=6, lam_lo=-4.0, lam_hi=0.5,
+                          sigma_mults=(0.6, 1.5), taus=(0.25, 0.75))
+    announce(f"fit_path ragged n=203 loss={loss}")
+    g = _gpu(inp, loss)
+    o = _oracle(inp, loss)
+    worst = compare_cells(g, o, inp, loss)
+    assert np.array_equal(g["selected"], o["selected"].astype(np.int32))
+    print(loss, "worst", worst)
+
+
+def test_path_deterministic():
+    inp = W.small_problem("logistic", 150, 4, seed=5, V=3, L=5)
+    announce("fit_path determinism, logistic n=150")
+    a = _gpu(inp, "logistic")
+    b = _gpu(inp, "logistic")
+    for k in ("alpha", "beta", "objective", "cv_sum", "iters"):
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_path_c2_full_size_sampled():
+    w = W.get("C2")
+    inp = W.make_inputs(w)
+    announce("fit_path C2 full size (logistic, n=2000, 3 sigmas, 50 lambdas)")
+    g = _gpu(inp, "logistic")
+    # every cell: stationarity of the returned solution under the oracle's K
+    y, fold = inp["y"], inp["fold_id"]
+    for s in range(3):
+        for v in range(w.V):
+            Kv, _, T, _ = OG.fold_blocks(inp["X"], fold, v, inp["sigmas"][s])
+            for l in range(w.L):
+                a = g["alpha"][s, 0, v, l][T]
+                k = kkt_of(Kv, y[T], a, g["beta"][s, 0, v, l], inp["lambdas"][l], "logistic", None, None)
+                assert k <= 1e-8, (s, v, l, k)
+    # sampled cells against independent oracle solves
+    cells = [(1, 0, 0, 0), (1, 0, 0, 17), (1, 0, 3, 49), (0, 0, 2, 0), (2, 0, 4, 30), (0, 0, 1, 8)]
+    o = {k: np.zeros_like(g[k]) for k in ("alpha", "beta", "objective", "cv_sum", "cv_err")}
+    o["beta_lo"] = np.zeros_like(g["beta"])
+    o["beta_hi"] = np.zeros_like(g["beta"])
+    for (s, q, v, l) in cells:
+        Kv, Kc, T, H = OG.fold_blocks(inp["X"], fold, v, inp["sigmas"][s])
+        lam = inp["lambdas"][l]
+        a, b, info = oracle.solve_cell(Kv, y[T], lam, "logistic")
+        o["alpha"][s, q, v, l][T] = a
+        o["beta"][s, q, v, l] = o["beta_lo"][s, q, v, l] = o["beta_hi"][s, q, v, l] = b
+        o["objective"][s, q, v, l] = oracle.objective(Kv, y[T], a, b, lam, "logistic")
+        fH = Kc @ a + b
+        o["cv_sum"][s, q, v, l] = oracle.losses.eval_loss("logistic", y[H], fH).sum()
+        o["cv_err"][s, q, v, l] = np.count_nonzero(y[H] * fH <= 0)
+    worst = compare_cells(g, o, inp, "logistic", cells=cells)
+    print("C2 sampled worst", worst, g["timings"])
