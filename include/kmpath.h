@@ -59,6 +59,20 @@ extern "C" {
 
 #define KMP_FLAG_RESTART 1 /* adaptive (gradient) restart of the momentum    */
 
+/* Kernel classes timed with HIP events when their bit is set in
+ * kmp_path_spec.timing_mask (1 << class). */
+#define KMP_KC_GRAM 0         /* a1 Gram + fold gather                         */
+#define KMP_KC_TRI_COL 1      /* a2 per-column Householder step (one block/fold) */
+#define KMP_KC_TRI_SYMV 2     /* a2 trailing-matrix product of each step       */
+#define KMP_KC_TRI_SYR2K 3    /* a2 rank-2nb trailing update per panel (MFMA)  */
+#define KMP_KC_QFORM 4        /* a2 compact-WY accumulation of Q (MFMA)        */
+#define KMP_KC_PRECOMPUTE 5   /* a3 per-stage column factors                   */
+#define KMP_KC_GEMM_F 6       /* a4+a5 f = Q (T abar) with the loss epilogue   */
+#define KMP_KC_GEMM_ZHAT 7    /* a6 zhat = Q' z                                */
+#define KMP_KC_UPDATE 8       /* a7 spectral update, KKT, restart              */
+#define KMP_KC_FINALIZE 9     /* a10                                           */
+#define KMP_NKC 10
+
 /* Solver settings. kmp_default_spec fills the defaults named below. */
 typedef struct {
   int32_t loss;        /* KMP_HINGE, KMP_LOGISTIC or KMP_CHECK              */
@@ -70,6 +84,9 @@ typedef struct {
   int32_t max_iter;    /* iterations per stage per cell (100000)            */
   int32_t poll_every;  /* iterations between host convergence polls (8)     */
   int32_t flags;       /* KMP_FLAG_RESTART (default on)                     */
+  int32_t timing_mask; /* kernel classes to time with HIP events (default 0) */
+  int32_t timing_every;/* bracket one launch in every timing_every launches
+                          of a timed class (default 1: all)                 */
 } kmp_path_spec;
 
 /* Phase times in milliseconds, measured with HIP events on `stream`. */
@@ -82,6 +99,15 @@ typedef struct {
   double total_ms;
   int64_t iterations;  /* iterations launched, summed over stages and batches */
   int64_t cell_iterations; /* sum over cells of iterations to convergence   */
+  /* per kernel class (only classes in timing_mask are filled): summed event
+   * time, launches, and algorithmic work of those launches (bytes that must
+   * move to or from device memory, and flops), as defined per class in the
+   * documentation of the kernels                                             */
+  double kernel_ms[KMP_NKC];
+  int64_t kernel_launches[KMP_NKC];  /* bracketed (sampled) launches         */
+  int64_t kernel_seen[KMP_NKC];      /* all launches of the class            */
+  double kernel_bytes[KMP_NKC];
+  double kernel_flops[KMP_NKC];
 } kmp_timings;
 
 void kmp_default_spec(kmp_path_spec* spec);
@@ -157,6 +183,9 @@ int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N,
 
 /* Message for a return code, or the last HIP error text for KMP_EHIP. */
 const char* kmp_strerror(int code);
+
+/* Name of kernel class `cls` (0 <= cls < KMP_NKC), or "" if out of range. */
+const char* kmp_kernel_class_name(int cls);
 
 /* Library version string. */
 const char* kmp_version(void);

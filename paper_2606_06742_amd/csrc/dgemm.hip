@@ -1,10 +1,11 @@
 // Batched fp64 tile GEMM on CDNA4 matrix cores (v_mfma_f64_16x16x4_f64).
 //
-// One 256-thread workgroup (four 64-lane waves) computes a 64 x 64 tile of C.
-// Wave w owns the 32 x 32 quadrant (rows 32*(w&1), cols 32*(w>>1)) as 2 x 2
-// MFMA blocks of 16 x 16. The K loop stages 64 x 16 slices of A and 16 x 64
-// slices of B through LDS, stored k-major so that the MFMA operand fetch of a
-// wave (lane l reads row/col l%16 of k-row l/16) is a contiguous LDS read.
+// One 256-thread workgroup (four 64-lane waves) computes a BM x 64 tile of C
+// (BM = 64, or 32 when 64-row tiles would leave compute units idle). Wave w
+// owns rows (BM/2)*(w&1) .. and cols 32*(w>>1) .. as (BM/32) x 2 MFMA blocks
+// of 16 x 16. The K loop stages BM x 32 slices of A and 32 x 64 slices of B
+// through LDS, stored k-major so that the MFMA operand fetch of a wave (lane
+// l reads row/col l%16 of k-row l/16) is a contiguous LDS read.
 //
 // MFMA f64 16x16x4 operand layout (per lane l of the wave):
 //   A: element (i = l%16, k = l/16);  B: element (k = l/16, j = l%16);
@@ -12,109 +13,172 @@
 #include "kmp_common.h"
 #include "kmp_kernels.h"
 
+#include <algorithm>
+
 namespace kmp {
 
 typedef double dbl4 __attribute__((ext_vector_type(4)));
 
-constexpr int TM = 64, TN = 64, TK = 16, LPAD = 4;
+constexpr int TN = 64, LPAD = 4;
 
-template <bool AK, bool BK>
-__device__ __forceinline__ void load_tiles(int M, int N, int K, int i0, int j0, int k0,
-                                           const double* __restrict__ A, int64_t lda,
-                                           const double* __restrict__ B, int64_t ldb,
-                                           double (*As)[TM + LPAD], double (*Bs)[TN + LPAD]) {
+// Tile geometry: BM x 64 outputs per 256-thread block, K slices of BK.
+// Four waves in a 2 x 2 grid; each wave owns (BM/2) x 32 outputs, i.e.
+// MB = BM/32 row blocks by 2 column blocks of 16 x 16.
+template <int BM, int BK>
+struct Tile {
+  static constexpr int MB = BM / 32;
+  static constexpr int APT = BM * BK / 256;   // A elements per thread per slice
+  static constexpr int BPT = BK * TN / 256;   // B elements per thread per slice
+};
+
+// Global -> register fetch of one K slice, and register -> LDS store.
+// Splitting the two lets the next slice be in flight while the matrix
+// cores work on the current one.
+template <int BM, int BK, bool AK, bool BKC>
+__device__ __forceinline__ void fetch_slice(int M, int N, int K, int i0, int j0, int k0,
+                                            const double* __restrict__ A, int64_t lda,
+                                            const double* __restrict__ B, int64_t ldb,
+                                            double (&ra)[Tile<BM, BK>::APT],
+                                            double (&rb)[Tile<BM, BK>::BPT]) {
+  constexpr int APT = Tile<BM, BK>::APT, BPT = Tile<BM, BK>::BPT;
   const int t = threadIdx.x;
-  // A slice: 64 (i) x 16 (k)
-  if (AK) {
-    const int i = t >> 2, kb = (t & 3) * 4;
+  if (AK) {                       // A[i*lda + k]: threads walk k within a row
+    constexpr int TPR = BK / APT;
+    const int i = t / TPR, kb = (t % TPR) * APT;
     const int gi = i0 + i;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < APT; ++q) {
       const int gk = k0 + kb + q;
-      As[kb + q][i] = (gi < M && gk < K) ? A[(int64_t)gi * lda + gk] : 0.0;
+      ra[q] = (gi < M && gk < K) ? A[(int64_t)gi * lda + gk] : 0.0;
     }
-  } else {
-    const int k = t >> 4, ib = (t & 15) * 4;
+  } else {                        // A[k*lda + i]: threads walk i within a k row
+    constexpr int TPR = BM / APT;
+    const int k = t / TPR, ib = (t % TPR) * APT;
     const int gk = k0 + k;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < APT; ++q) {
       const int gi = i0 + ib + q;
-      As[k][ib + q] = (gi < M && gk < K) ? A[(int64_t)gk * lda + gi] : 0.0;
+      ra[q] = (gi < M && gk < K) ? A[(int64_t)gk * lda + gi] : 0.0;
     }
   }
-  // B slice: 16 (k) x 64 (j)
-  if (BK) {
-    const int j = t >> 2, kb = (t & 3) * 4;
+  if (BKC) {                      // B[j*ldb + k]
+    constexpr int TPR = BK / BPT;
+    const int j = t / TPR, kb = (t % TPR) * BPT;
     const int gj = j0 + j;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < BPT; ++q) {
       const int gk = k0 + kb + q;
-      Bs[kb + q][j] = (gj < N && gk < K) ? B[(int64_t)gj * ldb + gk] : 0.0;
+      rb[q] = (gj < N && gk < K) ? B[(int64_t)gj * ldb + gk] : 0.0;
     }
-  } else {
-    const int k = t >> 4, jb = (t & 15) * 4;
+  } else {                        // B[k*ldb + j]
+    constexpr int TPR = TN / BPT;
+    const int k = t / TPR, jb = (t % TPR) * BPT;
     const int gk = k0 + k;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < BPT; ++q) {
       const int gj = j0 + jb + q;
-      Bs[k][jb + q] = (gj < N && gk < K) ? B[(int64_t)gk * ldb + gj] : 0.0;
+      rb[q] = (gj < N && gk < K) ? B[(int64_t)gk * ldb + gj] : 0.0;
     }
   }
 }
 
-// Main loop shared by all variants: accumulates the 2 x 2 blocks of the
-// calling wave. acc[bi][bj] covers rows wi+16*bi.., cols wj+16*bj...
-template <bool AK, bool BK>
-__device__ __forceinline__ void tile_mainloop(int M, int N, int K, int i0, int j0,
+template <int BM, int BK, bool AK, bool BKC>
+__device__ __forceinline__ void store_slice(const double (&ra)[Tile<BM, BK>::APT],
+                                            const double (&rb)[Tile<BM, BK>::BPT],
+                                            double (*As)[BM + LPAD], double (*Bs)[TN + LPAD]) {
+  constexpr int APT = Tile<BM, BK>::APT, BPT = Tile<BM, BK>::BPT;
+  const int t = threadIdx.x;
+  if (AK) {
+    constexpr int TPR = BK / APT;
+    const int i = t / TPR, kb = (t % TPR) * APT;
+#pragma unroll
+    for (int q = 0; q < APT; ++q) As[kb + q][i] = ra[q];
+  } else {
+    constexpr int TPR = BM / APT;
+    const int k = t / TPR, ib = (t % TPR) * APT;
+#pragma unroll
+    for (int q = 0; q < APT; ++q) As[k][ib + q] = ra[q];
+  }
+  if (BKC) {
+    constexpr int TPR = BK / BPT;
+    const int j = t / TPR, kb = (t % TPR) * BPT;
+#pragma unroll
+    for (int q = 0; q < BPT; ++q) Bs[kb + q][j] = rb[q];
+  } else {
+    constexpr int TPR = TN / BPT;
+    const int k = t / TPR, jb = (t % TPR) * BPT;
+#pragma unroll
+    for (int q = 0; q < BPT; ++q) Bs[k][jb + q] = rb[q];
+  }
+}
+
+// Main loop shared by all variants. acc[bi][bj] covers rows
+// wi + 16 bi .., cols wj + 16 bj ... Two LDS stages: slice k+1 is fetched
+// into registers before the MFMAs on slice k and stored into the other
+// stage afterwards (one barrier per slice).
+template <int BM, int BK, bool AK, bool BKC>
+__device__ __forceinline__ void tile_mainloop(int M, int N, int kbeg, int K, int i0, int j0,
                                               const double* __restrict__ A, int64_t lda,
                                               const double* __restrict__ B, int64_t ldb,
-                                              dbl4 (&acc)[2][2]) {
-  __shared__ double As[TK][TM + LPAD];
-  __shared__ double Bs[TK][TN + LPAD];
+                                              dbl4 (&acc)[Tile<BM, BK>::MB][2]) {
+  constexpr int MB = Tile<BM, BK>::MB;
+  __shared__ double As[2][BK][BM + LPAD];
+  __shared__ double Bs[2][BK][TN + LPAD];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int wi = (w & 1) * 32, wj = (w >> 1) * 32;
+  const int wi = (w & 1) * (BM / 2), wj = (w >> 1) * 32;
   const int li = lane & 15, lk = lane >> 4;
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MB; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = dbl4{0.0, 0.0, 0.0, 0.0};
-  for (int k0 = 0; k0 < K; k0 += TK) {
-    __syncthreads();
-    load_tiles<AK, BK>(M, N, K, i0, j0, k0, A, lda, B, ldb, As, Bs);
-    __syncthreads();
+  double ra[Tile<BM, BK>::APT], rb[Tile<BM, BK>::BPT];
+  fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg, A, lda, B, ldb, ra, rb);
+  store_slice<BM, BK, AK, BKC>(ra, rb, As[0], Bs[0]);
+  __syncthreads();
+  const int nk = (K - kbeg + BK - 1) / BK;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more)
+      fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + (kt + 1) * BK, A, lda, B, ldb, ra, rb);
 #pragma unroll
-    for (int kk = 0; kk < TK; kk += 4) {
-      const double a0 = As[kk + lk][wi + li];
-      const double a1 = As[kk + lk][wi + 16 + li];
-      const double b0 = Bs[kk + lk][wj + li];
-      const double b1 = Bs[kk + lk][wj + 16 + li];
-      acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
+    for (int kk = 0; kk < BK; kk += 4) {
+      double av[MB];
+#pragma unroll
+      for (int a = 0; a < MB; ++a) av[a] = As[cur][kk + lk][wi + 16 * a + li];
+      const double b0 = Bs[cur][kk + lk][wj + li];
+      const double b1 = Bs[cur][kk + lk][wj + 16 + li];
+#pragma unroll
+      for (int a = 0; a < MB; ++a) {
+        acc[a][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b0, acc[a][0], 0, 0, 0);
+        acc[a][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b1, acc[a][1], 0, 0, 0);
+      }
     }
+    if (more) store_slice<BM, BK, AK, BKC>(ra, rb, As[cur ^ 1], Bs[cur ^ 1]);
+    __syncthreads();
   }
 }
 
-template <bool AK, bool BK, bool CR>
+template <int BM, int BK, bool AK, bool BKC, bool CR>
 __global__ __launch_bounds__(256) void dgemm_kernel(int M, int N, int K,
                                                      const double* __restrict__ A, int64_t lda, int64_t sA,
                                                      const double* __restrict__ B, int64_t ldb, int64_t sB,
                                                      double* __restrict__ C, int64_t ldc, int64_t sC,
                                                      double alpha, double beta) {
+  constexpr int MB = Tile<BM, BK>::MB;
   const int b = blockIdx.z;
   A += (int64_t)b * sA;
   B += (int64_t)b * sB;
   C += (int64_t)b * sC;
-  const int i0 = blockIdx.x * TM, j0 = blockIdx.y * TN;
-  dbl4 acc[2][2];
-  tile_mainloop<AK, BK>(M, N, K, i0, j0, A, lda, B, ldb, acc);
+  const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TN;
+  dbl4 acc[MB][2];
+  tile_mainloop<BM, BK, AK, BKC>(M, N, 0, K, i0, j0, A, lda, B, ldb, acc);
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int wi = (w & 1) * 32, wj = (w >> 1) * 32;
+  const int wi = (w & 1) * (BM / 2), wj = (w >> 1) * 32;
 #pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
+  for (int bi = 0; bi < MB; ++bi)
 #pragma unroll
     for (int bj = 0; bj < 2; ++bj)
 #pragma unroll
@@ -130,23 +194,26 @@ __global__ __launch_bounds__(256) void dgemm_kernel(int M, int N, int K,
 }
 
 // First path GEMM with the loss-derivative epilogue (A = Q row-major,
-// B = T abar column-major, C = Z column-major).
+// B = T abar column-major, C = Z column-major). The per-tile column sums
+// of z are written to partial[b][tile][c] (BM rows per tile).
+template <int BM, int BK>
 __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
                                                           const double* __restrict__ A, int64_t lda, int64_t sA,
                                                           const double* __restrict__ B, int64_t ldb, int64_t sB,
                                                           double* __restrict__ C, int64_t ldc, int64_t sC,
                                                           LossEpi e) {
+  constexpr int MB = Tile<BM, BK>::MB;
   __shared__ double red[4][32];
   const int b = blockIdx.z;
   A += (int64_t)b * sA;
   B += (int64_t)b * sB;
   C += (int64_t)b * sC;
-  const int i0 = blockIdx.x * TM, j0 = blockIdx.y * TN;
-  dbl4 acc[2][2];
-  tile_mainloop<true, true>(M, N, K, i0, j0, A, lda, B, ldb, acc);
+  const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TN;
+  dbl4 acc[MB][2];
+  tile_mainloop<BM, BK, true, true>(M, N, 0, K, i0, j0, A, lda, B, ldb, acc);
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int wi = (w & 1) * 32, wj = (w >> 1) * 32;
+  const int wi = (w & 1) * (BM / 2), wj = (w >> 1) * 32;
   const int nv = e.nv[b];
   const double inv_nv = 1.0 / (double)nv;
   const double* y = e.y + (int64_t)b * e.sy;
@@ -155,12 +222,12 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
   double colsum[2] = {0.0, 0.0};
 #pragma unroll
   for (int bj = 0; bj < 2; ++bj) {
-    const int gj = j0 + wj + bj * 16 + (lane & 15);
+    const int gj = j0 + wj + bj * 16 + mfma_col(lane);
     const bool cj = gj < N;
     const double bb = cj ? bbar[gj] : 0.0;
     const double tj = cj ? tau[gj] : 0.0;
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
+    for (int bi = 0; bi < MB; ++bi)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int gi = i0 + wi + bi * 16 + mfma_row(lane, r);
@@ -195,34 +262,152 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
   }
 }
 
+// Split-K partial products for the path GEMMs: block z = b * S + s computes
+// the K range [s*Kc, min(K, (s+1)*Kc)) of batch b and stores its BM x 64
+// tile of A B (column-major, ldc) into part + s*sP + b*sC. The S partials
+// are added later in a fixed order, so results do not depend on timing.
+template <int BM, int BK, bool AK>
+__global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int N, int K, int S, int Kc,
+                                                             const double* __restrict__ A, int64_t lda, int64_t sA,
+                                                             const double* __restrict__ B, int64_t ldb, int64_t sB,
+                                                             double* __restrict__ part, int64_t ldc, int64_t sC,
+                                                             int64_t sP) {
+  constexpr int MB = Tile<BM, BK>::MB;
+  const int b = blockIdx.z / S, sk = blockIdx.z % S;
+  A += (int64_t)b * sA;
+  B += (int64_t)b * sB;
+  double* C = part + (int64_t)sk * sP + (int64_t)b * sC;
+  const int kbeg = sk * Kc;
+  const int kend = min(K, kbeg + Kc);
+  const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TN;
+  dbl4 acc[MB][2];
+  if (kbeg < kend) {
+    tile_mainloop<BM, BK, AK, true>(M, N, kbeg, kend, i0, j0, A, lda, B, ldb, acc);
+  } else {
+#pragma unroll
+    for (int a = 0; a < MB; ++a) acc[a][0] = acc[a][1] = dbl4{0.0, 0.0, 0.0, 0.0};
+  }
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int wi = (w & 1) * (BM / 2), wj = (w >> 1) * 32;
+#pragma unroll
+  for (int bi = 0; bi < MB; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int gi = i0 + wi + bi * 16 + mfma_row(lane, r);
+        const int gj = j0 + wj + bj * 16 + mfma_col(lane);
+        if (gi < M && gj < N) C[(int64_t)gj * ldc + gi] = acc[bi][bj][r];
+      }
+}
+
+// Loss epilogue over split-K partials of f: for row i < M of batch b and
+// column c < N, F = sum_s part_s[c][i] + bbar[c]; Z[c][i] = psi(y_i, F)/nv
+// (0 at padding rows); partial[b][tile][c] = sum of Z over the 64 rows of
+// the tile (lanes = rows, so the column sums are wave reductions).
+__global__ __launch_bounds__(256) void loss_epilogue_kernel(int M, int N, int S,
+                                                             const double* __restrict__ part,
+                                                             int64_t ldc, int64_t sC, int64_t sP,
+                                                             double* __restrict__ Z, LossEpi e) {
+  const int b = blockIdx.z;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int i = blockIdx.x * 64 + lane;
+  const int nv = e.nv[b];
+  const double inv_nv = 1.0 / (double)nv;
+  const double yi = (i < nv) ? e.y[(int64_t)b * e.sy + i] : 0.0;
+  const double* bbar = e.bbar + (int64_t)b * e.sbb;
+  const double* tau = e.tau + (int64_t)b * e.stau;
+  for (int c = w; c < N; c += 4) {
+    double z = 0.0;
+    if (i < M) {
+      double f = 0.0;
+      for (int sk = 0; sk < S; ++sk) f += part[(int64_t)sk * sP + (int64_t)b * sC + (int64_t)c * ldc + i];
+      if (i < nv) z = loss_psi(e.loss, yi, f + bbar[c], e.delta, tau[c]) * inv_nv;
+      Z[(int64_t)b * sC + (int64_t)c * ldc + i] = z;
+    }
+    const double cs = wave_sum(z);
+    if (lane == 0) e.partial[(int64_t)b * e.spart + (int64_t)blockIdx.x * N + c] = cs;
+  }
+}
+
+// Output tiles of 64 rows unless that leaves the chip under-filled (fewer
+// than two blocks per compute unit), then 32.
+static int pick_bm(const GemmArgs& g) {
+  const int64_t tiles64 = ceil_div(g.M, 64) * ceil_div(g.N, TN) * g.batch;
+  return tiles64 < 512 ? 32 : 64;
+}
+
 int gemm(hipStream_t s, const GemmArgs& g, bool ak, bool bk, bool cr) {
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return 0;
-  dim3 grid((unsigned)ceil_div(g.M, TM), (unsigned)ceil_div(g.N, TN), (unsigned)g.batch);
+  const int bm = pick_bm(g);
+  dim3 grid((unsigned)ceil_div(g.M, bm), (unsigned)ceil_div(g.N, TN), (unsigned)g.batch);
   dim3 block(256);
-#define KMP_GEMM_CASE(a, b, c)                                                              \
-  if (ak == a && bk == b && cr == c) {                                                      \
-    hipLaunchKernelGGL((dgemm_kernel<a, b, c>), grid, block, 0, s, g.M, g.N, g.K, g.A, g.lda, \
-                       g.sA, g.B, g.ldb, g.sB, g.C, g.ldc, g.sC, g.alpha, g.beta);          \
-    KMP_LAUNCH_CHECK();                                                                     \
-    return 0;                                                                               \
+#define KMP_GEMM_CASE(BMV, a, b, c)                                                          \
+  if (bm == BMV && ak == a && bk == b && cr == c) {                                          \
+    hipLaunchKernelGGL((dgemm_kernel<BMV, 32, a, b, c>), grid, block, 0, s, g.M, g.N, g.K, g.A, \
+                       g.lda, g.sA, g.B, g.ldb, g.sB, g.C, g.ldc, g.sC, g.alpha, g.beta);     \
+    KMP_LAUNCH_CHECK();                                                                      \
+    return 0;                                                                                \
   }
-  KMP_GEMM_CASE(true, true, true)
-  KMP_GEMM_CASE(true, true, false)
-  KMP_GEMM_CASE(true, false, true)
-  KMP_GEMM_CASE(true, false, false)
-  KMP_GEMM_CASE(false, true, true)
-  KMP_GEMM_CASE(false, true, false)
-  KMP_GEMM_CASE(false, false, true)
-  KMP_GEMM_CASE(false, false, false)
+#define KMP_GEMM_CASES(BMV)                \
+  KMP_GEMM_CASE(BMV, true, true, true)     \
+  KMP_GEMM_CASE(BMV, true, true, false)    \
+  KMP_GEMM_CASE(BMV, true, false, true)    \
+  KMP_GEMM_CASE(BMV, true, false, false)   \
+  KMP_GEMM_CASE(BMV, false, true, true)    \
+  KMP_GEMM_CASE(BMV, false, true, false)   \
+  KMP_GEMM_CASE(BMV, false, false, true)   \
+  KMP_GEMM_CASE(BMV, false, false, false)
+  KMP_GEMM_CASES(32)
+  KMP_GEMM_CASES(64)
+#undef KMP_GEMM_CASES
 #undef KMP_GEMM_CASE
   return KMP_EINVAL;
 }
 
+int gemm_loss_tile_rows(const GemmArgs& g) { return pick_bm(g); }
+
+int splitk_parts(const GemmArgs& g) {
+  const int64_t tiles = ceil_div(g.M, 64) * ceil_div(g.N, TN) * g.batch;
+  int S = (int)std::min<int64_t>(4, std::max<int64_t>(1, ceil_div(1024, tiles)));
+  while (S > 1 && g.K / S < 8 * 16) --S;          // keep >= 8 K slices per part
+  return S;
+}
+
+int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP) {
+  if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return 0;
+  const int Kc = (int)round_up(ceil_div(g.K, S), 16);
+  dim3 grid((unsigned)ceil_div(g.M, 64), (unsigned)ceil_div(g.N, TN), (unsigned)(g.batch * S));
+  if (a_kcontig)
+    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, true>), grid, dim3(256), 0, s, g.M, g.N, g.K, S,
+                       Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP);
+  else
+    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, false>), grid, dim3(256), 0, s, g.M, g.N, g.K, S,
+                       Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
+int loss_epilogue(hipStream_t s, int M, int N, int batch, int S, const double* part, int64_t ldc,
+                  int64_t sC, int64_t sP, double* Z, const LossEpi& e) {
+  if (M <= 0 || N <= 0 || batch <= 0) return 0;
+  dim3 grid((unsigned)ceil_div(M, 64), 1, (unsigned)batch);
+  hipLaunchKernelGGL(loss_epilogue_kernel, grid, dim3(256), 0, s, M, N, S, part, ldc, sC, sP, Z, e);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
 int gemm_loss(hipStream_t s, const GemmArgs& g, const LossEpi& e) {
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return 0;
-  dim3 grid((unsigned)ceil_div(g.M, TM), (unsigned)ceil_div(g.N, TN), (unsigned)g.batch);
-  hipLaunchKernelGGL(dgemm_loss_kernel, grid, dim3(256), 0, s, g.M, g.N, g.K, g.A, g.lda, g.sA,
-                     g.B, g.ldb, g.sB, g.C, g.ldc, g.sC, e);
+  const int bm = pick_bm(g);
+  dim3 grid((unsigned)ceil_div(g.M, bm), (unsigned)ceil_div(g.N, TN), (unsigned)g.batch);
+  if (bm == 32)
+    hipLaunchKernelGGL((dgemm_loss_kernel<32, 32>), grid, dim3(256), 0, s, g.M, g.N, g.K, g.A,
+                       g.lda, g.sA, g.B, g.ldb, g.sB, g.C, g.ldc, g.sC, e);
+  else
+    hipLaunchKernelGGL((dgemm_loss_kernel<64, 32>), grid, dim3(256), 0, s, g.M, g.N, g.K, g.A,
+                       g.lda, g.sA, g.B, g.ldb, g.sB, g.C, g.ldc, g.sC, e);
   KMP_LAUNCH_CHECK();
   return 0;
 }

@@ -18,6 +18,61 @@ static thread_local std::string g_err;
 void set_error(const std::string& msg) { g_err = msg; }
 const char* last_error() { return g_err.c_str(); }
 
+// Event brackets around selected launches; events come from a per-thread
+// pool that lives as long as the thread and is reused by every call.
+struct KernelClock {
+  uint32_t mask = 0;
+  int every = 1;
+  int64_t seen[KMP_NKC] = {0};
+  struct Rec {
+    int cls;
+    size_t ia, ib;
+    double bytes, flops;
+  };
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  std::vector<Rec> recs;
+  int open_cls = -1;
+  size_t open_ev = 0;
+  bool failed = false;
+  hipEvent_t* next(size_t* idx) {
+    if (used == pool.size()) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) {
+        failed = true;
+        return nullptr;
+      }
+      pool.push_back(e);
+    }
+    *idx = used;
+    return &pool[used++];
+  }
+};
+static thread_local KernelClock g_clock_obj;
+static thread_local KernelClock* g_clock = nullptr;
+KernelClock* current_clock() { return g_clock; }
+
+void kc_begin(int cls, hipStream_t s) {
+  KernelClock* c = g_clock;
+  if (!c || !((c->mask >> cls) & 1u) || c->failed) return;
+  if ((c->seen[cls]++) % c->every != 0) return;    // not sampled
+  size_t ia;
+  hipEvent_t* e = c->next(&ia);
+  if (!e || hipEventRecord(*e, s) != hipSuccess) { c->failed = true; return; }
+  c->open_cls = cls;
+  c->open_ev = ia;
+}
+
+void kc_end(int cls, hipStream_t s, double bytes, double flops) {
+  KernelClock* c = g_clock;
+  if (!c || !((c->mask >> cls) & 1u) || c->failed || c->open_cls != cls) return;
+  size_t ib;
+  hipEvent_t* e = c->next(&ib);
+  if (!e || hipEventRecord(*e, s) != hipSuccess) { c->failed = true; return; }
+  c->recs.push_back({cls, c->open_ev, ib, bytes, flops});
+  c->open_cls = -1;
+}
+
 namespace {
 
 constexpr int kPanel = 32;       // Householder panel width
@@ -48,8 +103,8 @@ struct Carver {
 // Workspace layout for one bandwidth batch (G = Sb * V groups). Used both to
 // size and to carve, so the two can never disagree.
 struct Layout {
-  double *A, *Qm, *diag, *off, *tau, *cvec, *ylab, *panel, *dots, *tmat, *xbuf, *ybuf;
-  double *ahat, *abar, *bmat, *zmat, *zhat, *ldl_l, *ldl_d, *vhat, *uvec, *partial;
+  double *A, *Qm, *diag, *off, *tau, *cvec, *ylab, *panel, *dots, *tmat, *xbuf, *ybuf, *pgram;
+  double *ahat, *abar, *bmat, *zmat, *zhat, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
   double *beta, *bbar, *rmom, *gcoef, *kkt, *lam, *taucol, *fbuf, *nrm, *inv2s2;
   int *flag, *iters, *iters_total, *active, *nvg;
   int32_t *tidx, *fold;
@@ -71,6 +126,7 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.tmat = c.take<double>(G * kPanel * kPanel);
   l.xbuf = c.take<double>(G * kPanel * N);
   l.ybuf = c.take<double>(G * kPanel * N);
+  l.pgram = c.take<double>(G * kPanel * N);
   l.ahat = c.take<double>(cols * N);
   l.abar = c.take<double>(cols * N);
   l.bmat = c.take<double>(cols * N);
@@ -81,6 +137,8 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.vhat = c.take<double>(cols * N);
   l.uvec = c.take<double>(cols * N);
   l.partial = c.take<double>(G * (size_t)p.RT * C);
+  l.fpart = c.take<double>((size_t)kMaxSplitK * cols * N);
+  l.zpart = c.take<double>((size_t)kMaxSplitK * cols * N);
   l.beta = c.take<double>(cols);
   l.bbar = c.take<double>(cols);
   l.rmom = c.take<double>(cols);
@@ -138,7 +196,7 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
     return KMP_EINVAL;
   }
   p->C = Qn * L;
-  p->RT = (int)ceil_div(p->N, kGemmTile);
+  p->RT = (int)ceil_div(p->N, kMinTileRows);
   p->Sb = std::max(1, std::min<int>(Sb, S));
   p->G = p->Sb * V;
   p->bytes = carve(*p, nullptr, nullptr);
@@ -180,6 +238,15 @@ void kmp_default_spec(kmp_path_spec* s) {
   s->max_iter = 100000;
   s->poll_every = 8;
   s->flags = KMP_FLAG_RESTART;
+  s->timing_mask = 0;
+  s->timing_every = 1;
+}
+
+const char* kmp_kernel_class_name(int cls) {
+  static const char* names[KMP_NKC] = {"gram",        "tri_col",  "tri_symv", "tri_syr2k",
+                                       "q_form",      "precompute", "gemm_f", "gemm_zhat",
+                                       "update",      "finalize"};
+  return (cls >= 0 && cls < KMP_NKC) ? names[cls] : "";
 }
 
 const char* kmp_version(void) { return "kmpath 0.1 (gfx950, fp64)"; }
@@ -277,7 +344,8 @@ int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N, double* Qout, dou
   w.dots = q; q += (size_t)G * 2 * kPanel;
   w.tmat = q; q += (size_t)G * kPanel * kPanel;
   w.xbuf = q; q += (size_t)G * kPanel * N;
-  w.ybuf = q;
+  w.ybuf = q; q += (size_t)G * kPanel * N;
+  w.pgram = q;
   int rc = tridiagonalize(s, w);
   KMP_HIP_TRY(hipFreeAsync(scratch, s));
   KMP_HIP_TRY(hipStreamSynchronize(s));
@@ -404,6 +472,19 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
 
   EventTimer tm;
   double t_gram = 0, t_factor = 0, t_pre = 0, t_path = 0, t_fin = 0;
+  struct ClockGuard {
+    ClockGuard(uint32_t mask) {
+      g_clock_obj.mask = mask;
+      g_clock_obj.used = 0;
+      for (auto& v : g_clock_obj.seen) v = 0;
+      g_clock_obj.recs.clear();
+      g_clock_obj.open_cls = -1;
+      g_clock_obj.failed = false;
+      g_clock = mask ? &g_clock_obj : nullptr;
+    }
+    ~ClockGuard() { g_clock = nullptr; }
+  } clock_guard((uint32_t)spec->timing_mask);
+  g_clock_obj.every = spec->timing_every > 0 ? spec->timing_every : 1;
   int64_t total_iters = 0;
   KMP_HIP_TRY(hipEventRecord(tm.ev[0], s));
   if ((rc = row_norms(s, X, n, d, ldx, lay.nrm)) != 0) return rc;
@@ -415,6 +496,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   pa.ahat = lay.ahat; pa.abar = lay.abar; pa.bmat = lay.bmat; pa.zmat = lay.zmat;
   pa.zhat = lay.zhat; pa.ldl_l = lay.ldl_l; pa.ldl_d = lay.ldl_d; pa.vhat = lay.vhat;
   pa.uvec = lay.uvec; pa.partial = lay.partial; pa.beta = lay.beta; pa.bbar = lay.bbar;
+  pa.fpart = lay.fpart; pa.zpart = lay.zpart;
   pa.rmom = lay.rmom; pa.gcoef = lay.gcoef; pa.kkt = lay.kkt; pa.flag = lay.flag;
   pa.iters = lay.iters; pa.iters_total = lay.iters_total; pa.active_count = lay.active;
 
@@ -440,18 +522,28 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     KMP_HIP_TRY(hipMemcpyAsync(lay.taucol, tauc.data(), sizeof(double) * tauc.size(),
                                hipMemcpyHostToDevice, s));
     KMP_HIP_TRY(hipMemcpyAsync(lay.nvg, nvg.data(), sizeof(int) * Gb, hipMemcpyHostToDevice, s));
+    pa.nv_host = nvg.data();
 
     // a1: Gram + fold gather into A (group g = s_local*V + v)
     KMP_HIP_TRY(hipEventRecord(tm.ev[1], s));
+    kc_begin(KMP_KC_GRAM, s);
     if ((rc = rbf_blocks(s, X, d, ldx, lay.nrm, lay.tidx, N, N, lay.tidx, N, N, V, lay.inv2s2, sb,
                          lay.A, (int64_t)V * N * N, (int64_t)N * N, N)) != 0)
       return rc;
+    {
+      // every kernel entry of every group is written once; the inner products
+      // (2d flops each) are shared by the bandwidths of the batch
+      double e2 = 0.0;
+      for (int v = 0; v < V; ++v) e2 += (double)plan.nv[v] * plan.nv[v];
+      kc_end(KMP_KC_GRAM, s, 8.0 * sb * e2, 2.0 * d * e2);
+    }
     KMP_HIP_TRY(hipEventRecord(tm.ev[2], s));
     // a2: factorisation
     TridiagWork tw;
     tw.G = Gb; tw.N = N; tw.nb = kPanel; tw.A = lay.A; tw.Q = lay.Qm; tw.diag = lay.diag;
     tw.off = lay.off; tw.tau = lay.tau; tw.panel = lay.panel; tw.dots = lay.dots;
-    tw.tmat = lay.tmat; tw.xbuf = lay.xbuf; tw.ybuf = lay.ybuf;
+    tw.tmat = lay.tmat; tw.xbuf = lay.xbuf; tw.ybuf = lay.ybuf; tw.pgram = lay.pgram;
+    tw.nv_host = nvg.data();
     if ((rc = tridiagonalize(s, tw)) != 0) return rc;
     if ((rc = group_ones_projection(s, lay.Qm, lay.nvg, Gb, N, lay.cvec)) != 0) return rc;
     if ((rc = gather_labels(s, y, lay.tidx, V, sb, N, lay.ylab)) != 0) return rc;
@@ -545,6 +637,23 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
       }
   }
   if (timings) {
+    for (int k = 0; k < KMP_NKC; ++k) {
+      timings->kernel_ms[k] = 0.0;
+      timings->kernel_launches[k] = 0;
+      timings->kernel_seen[k] = g_clock ? g_clock->seen[k] : 0;
+      timings->kernel_bytes[k] = 0.0;
+      timings->kernel_flops[k] = 0.0;
+    }
+    if (g_clock && !g_clock->failed) {
+      for (const auto& r : g_clock->recs) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, g_clock->pool[r.ia], g_clock->pool[r.ib]) != hipSuccess) continue;
+        timings->kernel_ms[r.cls] += ms;
+        timings->kernel_launches[r.cls] += 1;
+        timings->kernel_bytes[r.cls] += r.bytes;
+        timings->kernel_flops[r.cls] += r.flops;
+      }
+    }
     timings->gram_ms = t_gram;
     timings->factor_ms = t_factor;
     timings->precompute_ms = t_pre;

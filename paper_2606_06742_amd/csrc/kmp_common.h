@@ -34,6 +34,14 @@ const char* last_error();
 
 constexpr int kWave = 64;
 
+// Optional per-class kernel timing with HIP events (see kmp_path_spec
+// timing_mask). The driver installs a clock for the duration of a call;
+// launchers bracket their launches with kc_begin / kc_end.
+struct KernelClock;
+KernelClock* current_clock();
+void kc_begin(int cls, hipStream_t s);
+void kc_end(int cls, hipStream_t s, double bytes, double flops);
+
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 

@@ -23,7 +23,7 @@ struct GemmArgs {
 // Loss epilogue of the first path GEMM (f = Q (T abar) then z): for row i of
 // batch b and column c, with f = acc + bbar[c]:
 //   Z[i][c] = psi(y[i], f)/nv[b] if i < nv[b] else 0,
-// and partial[b][tile][c] = sum of Z over the 64 rows of the row tile.
+// and partial[b][tile][c] = sum of Z over the rows of the row tile.
 struct LossEpi {
   int loss = 0;
   double delta = 1.0;
@@ -34,10 +34,20 @@ struct LossEpi {
   double* partial = nullptr; int64_t spart = 0;  // [tiles][N] per batch
 };
 
-constexpr int kGemmTile = 64;   // rows and columns of a GEMM output tile
-
 int gemm(hipStream_t s, const GemmArgs& g, bool a_kcontig, bool b_kcontig, bool c_rowmajor);
 int gemm_loss(hipStream_t s, const GemmArgs& g, const LossEpi& e);
+// Rows per output tile gemm_loss uses for g (the partial sums hold one row
+// per tile): 32 or 64.
+int gemm_loss_tile_rows(const GemmArgs& g);
+constexpr int kMinTileRows = 32;
+constexpr int kMaxSplitK = 4;
+// Split-K: number of K parts for g (1..4), the partial products (column-
+// major C layout per part, part stride sP), and the loss epilogue that adds
+// the parts in order and writes Z plus 64-row column sums (see LossEpi).
+int splitk_parts(const GemmArgs& g);
+int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP);
+int loss_epilogue(hipStream_t s, int M, int N, int batch, int S, const double* part, int64_t ldc,
+                  int64_t sC, int64_t sP, double* Z, const LossEpi& e);
 
 // ---------------------------------------------------------------- Gram
 // Squared row norms of X (n x d, ldx): nrm[i] = sum_k X[i][k]^2.
@@ -65,6 +75,8 @@ struct TridiagWork {
   double* tmat = nullptr;   // G x nb x nb (compact-WY T factor)
   double* xbuf = nullptr;   // G x nb x N
   double* ybuf = nullptr;   // G x nb x N
+  double* pgram = nullptr;  // G x N x nb (Gram of each panel's reflectors)
+  const int* nv_host = nullptr;  // G valid orders (host), for the work counters; N if null
 };
 size_t tridiag_panel_doubles(int G, int N, int nb);
 int tridiagonalize(hipStream_t s, const TridiagWork& w);
@@ -94,6 +106,8 @@ struct PathArrays {
   double* vhat = nullptr;
   double* uvec = nullptr;   // T vhat
   double* partial = nullptr;// G x tiles x C
+  double* fpart = nullptr;  // kMaxSplitK x G x N x C split-K partials of f
+  double* zpart = nullptr;  // kMaxSplitK x G x N x C split-K partials of zhat
   // per column scalars
   double* beta = nullptr;
   double* bbar = nullptr;
@@ -104,6 +118,7 @@ struct PathArrays {
   int* iters = nullptr;     // per stage
   int* iters_total = nullptr;
   int* active_count = nullptr;  // 1 int
+  const int* nv_host = nullptr;  // G valid rows (host), for the work counters
 };
 
 int path_init_columns(hipStream_t s, const PathArrays& p);

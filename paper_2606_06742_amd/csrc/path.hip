@@ -160,13 +160,25 @@ __global__ void precompute_kernel(int G, int N, int C, const int* __restrict__ n
   iters[gc] = 0;
 }
 
+// Sum over groups of f(valid rows) for the work counters.
+template <typename F>
+static double over_groups(const PathArrays& p, F f) {
+  double a = 0.0;
+  for (int g = 0; g < p.G; ++g) a += f((double)(p.nv_host ? p.nv_host[g] : p.N));
+  return a;
+}
+
 int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa) {
   const int64_t cols = (int64_t)p.G * p.C;
+  kc_begin(KMP_KC_PRECOMPUTE, s);
   hipLaunchKernelGGL(precompute_kernel, dim3((unsigned)ceil_div(cols, 64)), dim3(64), 0, s, p.G,
                      p.N, p.C, p.nv, p.Tdiag, p.Toff, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
                      p.uvec, p.gcoef, p.ahat, p.abar, p.bmat, p.beta, p.bbar, p.rmom, p.flag,
                      p.iters);
   KMP_LAUNCH_CHECK();
+  // reads T, c, ahat; writes l, d, vhat, u, abar, T ahat
+  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * 8.0; }),
+         over_groups(p, [&](double n) { return 20.0 * n * p.C; }));
   return 0;
 }
 
@@ -227,7 +239,8 @@ template <int E>
 __global__ __launch_bounds__(PB) void update_kernel(
     int N, int C, int RT, const int* __restrict__ nvv, const double* __restrict__ Td,
     const double* __restrict__ To, const double* __restrict__ lamv,
-    const double* __restrict__ zhat, double* __restrict__ ahat, double* __restrict__ abar,
+    const double* __restrict__ zpart, int S2, int64_t sP, double* __restrict__ ahat,
+    double* __restrict__ abar,
     double* __restrict__ bmat, const double* __restrict__ ldl_l, const double* __restrict__ ldl_d,
     const double* __restrict__ vhat, const double* __restrict__ uvec,
     const double* __restrict__ gcoef, const double* __restrict__ partial,
@@ -261,7 +274,9 @@ __global__ __launch_bounds__(PB) void update_kernel(
     if (i < N) {
       ab[e] = abar[base + i];
       ah[e] = ahat[base + i];
-      wv[e] = fma(2.0 * lam, ab[e], zhat[base + i]);
+      double zh = 0.0;
+      for (int sk = 0; sk < S2; ++sk) zh += zpart[(int64_t)sk * sP + base + i];
+      wv[e] = fma(2.0 * lam, ab[e], zh);
       tl = fma(uvec[base + i], wv[e], tl);
       n2 = fma(wv[e], wv[e], n2);
     } else {
@@ -393,30 +408,44 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
                    int max_iter, int restart) {
   (void)kappa;
   int rc;
-  const int RT = (int)ceil_div(p.N, kGemmTile);
-  // f = Q (T abar) + bbar and z = psi(y, f)/n_v, with per-tile column sums
+  const int RT = (int)ceil_div(p.N, 64);
+  const int64_t sC = (int64_t)p.N * p.C;
+  const int64_t sP = (int64_t)p.G * sC;
+  // f = Q (T abar) as split-K partials, then z = psi(y, f + bbar)/n_v with
+  // 64-row column sums
   GemmArgs g1;
   g1.M = p.N; g1.N = p.C; g1.K = p.N; g1.batch = p.G;
   g1.A = p.Q; g1.lda = p.N; g1.sA = (int64_t)p.N * p.N;
-  g1.B = p.bmat; g1.ldb = p.N; g1.sB = (int64_t)p.N * p.C;
-  g1.C = p.zmat; g1.ldc = p.N; g1.sC = (int64_t)p.N * p.C;
+  g1.B = p.bmat; g1.ldb = p.N; g1.sB = sC;
+  g1.ldc = p.N; g1.sC = sC;
+  const int S1 = splitk_parts(g1);
   LossEpi e;
   e.loss = p.loss; e.delta = delta;
   e.y = p.ylab; e.sy = p.N; e.nv = p.nv;
   e.bbar = p.bbar; e.sbb = p.C; e.tau = p.tau; e.stau = p.C;
   e.partial = p.partial; e.spart = (int64_t)RT * p.C;
-  if ((rc = gemm_loss(s, g1, e)) != 0) return rc;
-  // zhat = Q' z
+  const double gflops = over_groups(p, [&](double n) { return 2.0 * n * n * p.C; });
+  const double gbytes = over_groups(p, [&](double n) { return 8.0 * (n * n + 2.0 * n * p.C); });
+  kc_begin(KMP_KC_GEMM_F, s);
+  if ((rc = gemm_partial(s, g1, true, S1, p.fpart, sP)) != 0) return rc;
+  if ((rc = loss_epilogue(s, p.N, p.C, p.G, S1, p.fpart, p.N, sC, sP, p.zmat, e)) != 0) return rc;
+  kc_end(KMP_KC_GEMM_F, s, gbytes, gflops);
+  // zhat = Q' z as split-K partials (added by the update kernel)
   GemmArgs g2;
   g2.M = p.N; g2.N = p.C; g2.K = p.N; g2.batch = p.G;
   g2.A = p.Q; g2.lda = p.N; g2.sA = (int64_t)p.N * p.N;
-  g2.B = p.zmat; g2.ldb = p.N; g2.sB = (int64_t)p.N * p.C;
-  g2.C = p.zhat; g2.ldc = p.N; g2.sC = (int64_t)p.N * p.C;
-  if ((rc = gemm(s, g2, false, true, false)) != 0) return rc;
+  g2.B = p.zmat; g2.ldb = p.N; g2.sB = sC;
+  g2.ldc = p.N; g2.sC = sC;
+  const int S2 = splitk_parts(g2);
+  kc_begin(KMP_KC_GEMM_ZHAT, s);
+  if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP)) != 0) return rc;
+  kc_end(KMP_KC_GEMM_ZHAT, s, gbytes, gflops);
   const unsigned cols = (unsigned)(p.G * p.C);
+  kc_begin(KMP_KC_UPDATE, s);
 #define KMP_UPD(EE)                                                                              \
   hipLaunchKernelGGL(update_kernel<EE>, dim3(cols), dim3(PB), 0, s, p.N, p.C, RT, p.nv, p.Tdiag, \
-                     p.Toff, p.lam, p.zhat, p.ahat, p.abar, p.bmat, p.ldl_l, p.ldl_d, p.vhat,    \
+                     p.Toff, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.bmat, p.ldl_l, p.ldl_d,   \
+                     p.vhat,                                                                     \
                      p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt, p.flag, p.iters, \
                      p.iters_total, tol, max_iter, restart)
   if (p.N <= PB * 1) KMP_UPD(1);
@@ -431,6 +460,10 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   }
 #undef KMP_UPD
   KMP_LAUNCH_CHECK();
+  // per column element: read zhat, abar, ahat, l, 1/d, vhat, u; write ahat,
+  // abar, T abar (80 bytes), counted for every column of the launch
+  kc_end(KMP_KC_UPDATE, s, over_groups(p, [&](double n) { return 80.0 * n * p.C; }),
+         over_groups(p, [&](double n) { return 30.0 * n * p.C; }));
   return 0;
 }
 
@@ -593,6 +626,7 @@ __global__ __launch_bounds__(256) void cv_reduce_kernel(
 
 int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
   int rc;
+  kc_begin(KMP_KC_FINALIZE, s);
   // alpha_loc = Q ahat (into zmat)
   GemmArgs g;
   g.M = p.N; g.N = p.C; g.K = p.N; g.batch = p.G;
@@ -609,6 +643,12 @@ int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
                      p.lam, p.tau, p.zmat, fa.fbuf, p.beta, p.flag, p.iters_total, fa.alpha,
                      fa.beta_out, fa.objective, fa.cv_sum, fa.cv_err, fa.iters, fa.status);
   KMP_LAUNCH_CHECK();
+  // alpha = Q ahat, then K(x_i, T) alpha for all n points: kernel entries
+  // recomputed (d + ~20 flops each) and contracted over the C columns
+  kc_end(KMP_KC_FINALIZE, s,
+         over_groups(p, [&](double n) { return 8.0 * (n * n + 2.0 * n * p.C + (double)fa.n * p.C); }),
+         over_groups(p, [&](double n) {
+           return 2.0 * n * n * p.C + (double)fa.n * n * (2.0 * fa.d + 20.0 + 2.0 * p.C); }));
   return 0;
 }
 

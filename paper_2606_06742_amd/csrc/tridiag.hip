@@ -17,24 +17,31 @@
 #include "kmp_common.h"
 #include "kmp_kernels.h"
 
+#include <algorithm>
+
 namespace kmp {
 
-constexpr int TB = 256;   // threads per block
-constexpr int TW = 4;     // waves per block
+constexpr int TB = 512;   // threads per block of the one-workgroup-per-matrix kernels
+constexpr int TW = 8;     // waves per block
 
 // One workgroup per matrix. Step j of the panel starting at p (jj = j - p):
 //  1. (jj > 0) finish w_{jj-1} = w_raw - (tau/2)(w_raw' v) v   (dlatrd)
 //  2. bring column j up to date with the panel's rank-2 updates
 //  3. Householder vector of column j below the diagonal (dlarfg)
-//  4. dot products W_k'v, V_k'v (k < jj) for the symv corrections
+//  4. dot products W_k'v, V_k'v (k < jj) for the symv corrections; the
+//     V_k'v are also the panel's Gram entries, kept for the WY factor
+// Loops over k are unrolled with independent accumulators so that many
+// loads are in flight (the panel rows live in L2).
 __global__ __launch_bounds__(TB) void tri_col_kernel(double* __restrict__ A, double* __restrict__ P,
                                                      double* __restrict__ dots,
                                                      double* __restrict__ taus,
                                                      double* __restrict__ diag,
-                                                     double* __restrict__ off, int N, int nb, int j,
+                                                     double* __restrict__ off,
+                                                     double* __restrict__ pgram, int N, int nb, int j,
                                                      int jj) {
   __shared__ double red[TW];
   __shared__ double sh[2];
+  __shared__ double coef[128];
   const int g = blockIdx.x;
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
@@ -45,6 +52,8 @@ __global__ __launch_bounds__(TB) void tri_col_kernel(double* __restrict__ A, dou
   double* V2 = Pg + (int64_t)2 * nb * N;
   double* dg = dots + (int64_t)g * 2 * nb;
   const double* tg = taus + (int64_t)g * N;
+  const int p0 = j - jj;
+  double* gr = pgram + (int64_t)g * N * nb + (int64_t)p0 * nb;   // this panel's nb x nb Gram
 
   // 1. finish the previous w (its v has support rows >= j)
   if (jj > 0) {
@@ -57,28 +66,55 @@ __global__ __launch_bounds__(TB) void tri_col_kernel(double* __restrict__ A, dou
     for (int i = j + t; i < N; i += TB) wr[i] = fma(c, v[i], wr[i]);
     __syncthreads();
   }
+  // coefficients W_k[j], V_k[j] of the pending rank-2 updates
+  if (t < jj) coef[t] = Wr[(int64_t)t * N + j];
+  else if (t >= 64 && t < 64 + jj) coef[t] = Vr[(int64_t)(t - 64) * N + j];
+  __syncthreads();
 
-  // 2. a = A[j:, j] - sum_k (V_k W_k[j] + W_k V_k[j]); A[j][i] by symmetry
-  // 3. Householder of a[j+1:], alpha = a[j+1]
+  // 2. a = A[j:, j] - sum_k (V_k W_k[j] + W_k V_k[j]); A[j][i] by symmetry.
+  // Each thread updates up to RPT of its rows at once, k unrolled by 8, so
+  // that 2*8*RPT independent loads are in flight.
+  constexpr int RPT = 4;
   double* rowj = Ag + (int64_t)j * N;
   double ss = 0.0;
   double aj = 0.0, a1 = 0.0;
-  for (int i = j + t; i < N; i += TB) {
-    double a = rowj[i];
-    for (int k = 0; k < jj; ++k) {
-      const double* vk = Vr + (int64_t)k * N;
-      const double* wk = Wr + (int64_t)k * N;
-      a -= vk[i] * wk[j] + wk[i] * vk[j];
+  for (int base = j + t; base < N; base += TB * RPT) {
+    double acc[RPT];
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+      const int i = base + r * TB;
+      acc[r] = i < N ? rowj[i] : 0.0;
     }
-    rowj[i] = a;
-    if (i == j) aj = a;
-    else if (i == j + 1) a1 = a;
-    else ss = fma(a, a, ss);
+    for (int k0 = 0; k0 < jj; k0 += 8) {
+#pragma unroll
+      for (int kq = 0; kq < 8; ++kq) {
+        const int k = k0 + kq;
+        if (k < jj) {
+          const double cw = coef[k], cv = coef[64 + k];
+          const double* vk = Vr + (int64_t)k * N;
+          const double* wk = Wr + (int64_t)k * N;
+#pragma unroll
+          for (int r = 0; r < RPT; ++r) {
+            const int i = base + r * TB;
+            if (i < N) acc[r] = fma(-vk[i], cw, fma(-wk[i], cv, acc[r]));
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+      const int i = base + r * TB;
+      if (i < N) {
+        rowj[i] = acc[r];
+        if (i == j) aj = acc[r];
+        else if (i == j + 1) a1 = acc[r];
+        else ss = fma(acc[r], acc[r], ss);
+      }
+    }
   }
-  // broadcast a[j] and a[j+1] (owned by threads 0 and 1 of the first pass)
   if (t == 0) sh[0] = aj;
   if (t == 1) sh[1] = a1;
-  ss = block_sum<TW>(ss, red);   // contains a __syncthreads after the writes above
+  ss = block_sum<TW>(ss, red);   // its barriers publish sh[] and rowj[]
   const double dj = sh[0];
   const double alpha = (j + 1 < N) ? sh[1] : 0.0;
   double tau = 0.0, beta = alpha, scale = 0.0;
@@ -91,8 +127,9 @@ __global__ __launch_bounds__(TB) void tri_col_kernel(double* __restrict__ A, dou
     diag[(int64_t)g * N + j] = dj;
     off[(int64_t)g * N + j] = (j + 1 < N) ? beta : 0.0;
     taus[(int64_t)g * N + j] = tau;
+    gr[jj * nb + jj] = (j + 1 < N) ? 1.0 + ss * scale * scale : 0.0;   // v_j'v_j
   }
-  // v: zeros up to j, 1 at j+1, scaled a below. Stored in P (rows jj and
+  // 3. v: zeros up to j, 1 at j+1, scaled a below. Stored in P (rows jj and
   // 2nb+jj) and in row j of A (for the accumulation of Q); W row jj is
   // cleared up to j so the symv only fills rows > j.
   double* vj = Vr + (int64_t)jj * N;
@@ -100,31 +137,55 @@ __global__ __launch_bounds__(TB) void tri_col_kernel(double* __restrict__ A, dou
   double* wj = Wr + (int64_t)jj * N;
   for (int i = t; i < N; i += TB) {
     double v = 0.0;
-    if (i == j + 1) v = 1.0;
-    else if (i > j + 1) v = (scale != 0.0) ? rowj[i] * scale : 0.0;
+    if (j + 1 < N) {
+      if (i == j + 1) v = 1.0;
+      else if (i > j + 1) v = (scale != 0.0) ? rowj[i] * scale : 0.0;
+    }
     vj[i] = v;
     vj2[i] = v;
     rowj[i] = v;                      // row j of A now holds v_j (0 at and left of j)
     if (i <= j) wj[i] = 0.0;
   }
   __syncthreads();
-  // 4. dot products for the symv corrections, one wave per k
-  for (int k = w; k < 2 * jj; k += TW) {
-    const double* src = (k < jj) ? (Wr + (int64_t)k * N) : (Vr + (int64_t)(k - jj) * N);
-    double s = 0.0;
-    for (int i = j + 1 + lane; i < N; i += 64) s = fma(src[i], vj[i], s);
-    s = wave_sum(s);
-    if (lane == 0) dg[k] = s;          // dg[k<jj] = W_k'v, dg[jj+k] = V_k'v
+  // 4. dot products, four k at a time per wave
+  const int nk = 2 * jj;
+  for (int k0 = 4 * w; k0 < nk; k0 += 4 * TW) {
+    double s[4] = {0.0, 0.0, 0.0, 0.0};
+    const double* src[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int k = k0 + q < nk ? k0 + q : k0;
+      src[q] = (k < jj) ? (Wr + (int64_t)k * N) : (Vr + (int64_t)(k - jj) * N);
+    }
+#pragma unroll 4
+    for (int i = j + 1 + lane; i < N; i += 64) {
+      const double vi = vj[i];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s[q] = fma(src[q][i], vi, s[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const double r = wave_sum(s[q]);
+      const int k = k0 + q;
+      if (lane == 0 && k < nk) {
+        dg[k] = r;                     // dg[k<jj] = W_k'v, dg[jj+k] = V_k'v
+        if (k >= jj) gr[(k - jj) * nb + jj] = r;
+      }
+    }
   }
 }
 
-// w_raw = tau * (A[j+1:, j+1:] v - V (W'v) - W (V'v)) for rows > j, 16 rows
-// per workgroup (4 rows per wave, lanes stride the columns).
-__global__ __launch_bounds__(TB) void tri_symv_kernel(const double* __restrict__ A,
-                                                      double* __restrict__ P,
-                                                      const double* __restrict__ dots,
-                                                      const double* __restrict__ taus, int N, int nb,
-                                                      int j, int jj) {
+// w_raw = tau * (A[j+1:, j+1:] v - V (W'v) - W (V'v)) for rows > j. Four
+// rows per wave: lanes stride the columns of the row-major trailing matrix
+// (coalesced, two column blocks in flight), then the rank-2jj corrections
+// are spread over the lanes.
+constexpr int SR = 4;           // rows per wave
+constexpr int SW = 4;           // waves per block
+__global__ __launch_bounds__(SW * 64) void tri_symv_kernel(const double* __restrict__ A,
+                                                           double* __restrict__ P,
+                                                           const double* __restrict__ dots,
+                                                           const double* __restrict__ taus, int N,
+                                                           int nb, int j, int jj) {
   const int g = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const double* Ag = A + (int64_t)g * N * N;
@@ -134,30 +195,38 @@ __global__ __launch_bounds__(TB) void tri_symv_kernel(const double* __restrict__
   const double* v = Vr + (int64_t)jj * N;
   const double* dg = dots + (int64_t)g * 2 * nb;
   const double tau = taus[(int64_t)g * N + j];
-  const int r0 = j + 1 + blockIdx.x * 16 + w * 4;
-  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  const int r0 = j + 1 + (blockIdx.x * SW + w) * SR;
+  if (r0 >= N) return;
+  double acc[SR];
+#pragma unroll
+  for (int q = 0; q < SR; ++q) acc[q] = 0.0;
+  const double* rowp[SR];
+#pragma unroll
+  for (int q = 0; q < SR; ++q) rowp[q] = Ag + (int64_t)(r0 + q < N ? r0 + q : r0) * N;
+#pragma unroll 2
   for (int c = j + 1 + lane; c < N; c += 64) {
     const double vc = v[c];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = r0 + q;
-      if (r < N) acc[q] = fma(Ag[(int64_t)r * N + c], vc, acc[q]);
-    }
+    for (int q = 0; q < SR; ++q) acc[q] = fma(rowp[q][c], vc, acc[q]);
   }
 #pragma unroll
-  for (int q = 0; q < 4; ++q) acc[q] = wave_sum(acc[q]);
-  if (lane < 4) {
-    const int r = r0 + lane;
-    if (r < N) {
-      double s = acc[0];
-      if (lane == 1) s = acc[1];
-      if (lane == 2) s = acc[2];
-      if (lane == 3) s = acc[3];
-      for (int k = 0; k < jj; ++k)
-        s -= Vr[(int64_t)k * N + r] * dg[k] + Wr[(int64_t)k * N + r] * dg[jj + k];
-      Wr[(int64_t)jj * N + r] = tau * s;
-    }
-  }
+  for (int q = 0; q < SR; ++q) acc[q] = wave_sum(acc[q]);
+  // corrections: lane = 16*q + kl handles row q, terms k = kl, kl+16, ...
+  const int q = lane >> 4, kl = lane & 15;
+  const int r = r0 + q;
+  double corr = 0.0;
+  if (r < N)
+    for (int k = kl; k < jj; k += 16)
+      corr = fma(Vr[(int64_t)k * N + r], dg[k], fma(Wr[(int64_t)k * N + r], dg[jj + k], corr));
+  corr += __shfl_xor(corr, 1, 64);
+  corr += __shfl_xor(corr, 2, 64);
+  corr += __shfl_xor(corr, 4, 64);
+  corr += __shfl_xor(corr, 8, 64);
+  double mine = acc[0];
+#pragma unroll
+  for (int qq = 1; qq < SR; ++qq)
+    if (q == qq) mine = acc[qq];
+  if (kl == 0 && r < N) Wr[(int64_t)jj * N + r] = tau * (mine - corr);
 }
 
 // Finish the last w of a panel (step 1 of tri_col_kernel alone).
@@ -185,44 +254,48 @@ __global__ void set_identity_kernel(double* __restrict__ Q, int N, int64_t total
 
 // Compact-WY factor of the panel's reflectors (LAPACK dlarft, forward,
 // columnwise): H_p ... H_{p+nb-1} = I - V T V', T upper triangular,
-// T[i][i] = tau_i, T[0:i, i] = -tau_i T[0:i, 0:i] (V[:, 0:i]' v_i).
-__global__ __launch_bounds__(TB) void form_t_kernel(const double* __restrict__ A,
+// T[i][i] = tau_i, T[0:i, i] = -tau_i T[0:i, 0:i] (V[:, 0:i]' v_i). The
+// Gram entries V' v_i were recorded by the reduction (pgram); column i of T
+// is formed by nb threads in parallel, columns in sequence.
+__global__ __launch_bounds__(64) void form_t_kernel(const double* __restrict__ pgram,
                                                     const double* __restrict__ taus,
-                                                    double* __restrict__ tmat, int N, int nb, int p) {
-  __shared__ double gram[64][65];
-  const int g = blockIdx.x, t = threadIdx.x;
-  const int lane = t & 63, w = t >> 6;
-  const double* Ag = A + (int64_t)g * N * N;
-  double* Tg = tmat + (int64_t)g * nb * nb;
+                                                    double* __restrict__ tmat, int N, int nbs,
+                                                    int nb, int p) {
+  __shared__ double T[64][65];
+  __shared__ double gcol[64];
+  const int g = blockIdx.x, r = threadIdx.x;
+  const double* gr = pgram + (int64_t)g * N * nbs + (int64_t)p * nbs;
   const double* tg = taus + (int64_t)g * N;
-  // Gram matrix of the panel vectors (rows p..p+nb-1 of A), upper part
-  for (int pair = w; pair < nb * nb; pair += TW) {
-    const int a = pair / nb, b = pair % nb;
-    if (a > b) continue;
-    const double* va = Ag + (int64_t)(p + a) * N;
-    const double* vb = Ag + (int64_t)(p + b) * N;
-    double s = 0.0;
-    for (int i = p + 1 + lane; i < N; i += 64) s = fma(va[i], vb[i], s);
-    s = wave_sum(s);
-    if (lane == 0) gram[a][b] = s;
-  }
+  if (r < nb)
+    for (int c = 0; c < nb; ++c) T[r][c] = 0.0;
   __syncthreads();
-  if (t == 0) {
-    for (int i = 0; i < nb; ++i) {
-      const double ti = (p + i < N) ? tg[p + i] : 0.0;
-      for (int r = 0; r < i; ++r) {
-        double s = 0.0;
-        for (int c = r; c < i; ++c) s += Tg[r * nb + c] * gram[c][i];
-        Tg[r * nb + i] = -ti * s;
-      }
-      Tg[i * nb + i] = ti;
-      for (int r = i + 1; r < nb; ++r) Tg[r * nb + i] = 0.0;
-    }
+  for (int i = 0; i < nb; ++i) {
+    const double ti = (p + i < N) ? tg[p + i] : 0.0;
+    if (r < i) gcol[r] = gr[r * nbs + i];
+    __syncthreads();
+    double s = 0.0;
+    if (r < i)
+      for (int c = r; c < i; ++c) s = fma(T[r][c], gcol[c], s);
+    __syncthreads();
+    if (r < i) T[r][i] = -ti * s;
+    if (r == i) T[i][i] = ti;
+    __syncthreads();
   }
+  double* Tg = tmat + (int64_t)g * nbs * nbs;
+  if (r < nb)
+    for (int c = 0; c < nb; ++c) Tg[r * nb + c] = T[r][c];
 }
 
 size_t tridiag_panel_doubles(int G, int N, int nb) {
-  return (size_t)G * (3 * (size_t)nb * N + 2 * nb + (size_t)nb * nb + 2 * (size_t)nb * N);
+  return (size_t)G * (3 * (size_t)nb * N + 2 * nb + (size_t)nb * nb + 3 * (size_t)nb * N);
+}
+
+// Sum over matrices of f(valid order) for the work counters.
+template <typename F>
+static double over_groups(const TridiagWork& wk, F f) {
+  double a = 0.0;
+  for (int g = 0; g < wk.G; ++g) a += f((double)(wk.nv_host ? wk.nv_host[g] : wk.N));
+  return a;
 }
 
 int tridiagonalize(hipStream_t s, const TridiagWork& wk) {
@@ -238,14 +311,27 @@ int tridiagonalize(hipStream_t s, const TridiagWork& wk) {
     const int pe = (p + nb < N) ? p + nb : N;
     for (int j = p; j < pe; ++j) {
       const int jj = j - p;
+      kc_begin(KMP_KC_TRI_COL, s);
       hipLaunchKernelGGL(tri_col_kernel, dim3(G), dim3(TB), 0, s, wk.A, wk.panel, wk.dots, wk.tau,
-                         wk.diag, wk.off, N, nb, j, jj);
+                         wk.diag, wk.off, wk.pgram, N, nb, j, jj);
       KMP_LAUNCH_CHECK();
+      // panel rows (2jj) read twice, finish/update/store of ~6 vectors
+      kc_end(KMP_KC_TRI_COL, s,
+             over_groups(wk, [&](double n) { return 8.0 * std::max(0.0, n - j) * (4.0 * jj + 6.0); }),
+             over_groups(wk, [&](double n) { return 2.0 * std::max(0.0, n - j) * (4.0 * jj + 4.0); }));
       const int rows = N - j - 1;
       if (rows > 0) {
-        hipLaunchKernelGGL(tri_symv_kernel, dim3((unsigned)ceil_div(rows, 16), G), dim3(TB), 0, s,
-                           wk.A, wk.panel, wk.dots, wk.tau, N, nb, j, jj);
+        kc_begin(KMP_KC_TRI_SYMV, s);
+        hipLaunchKernelGGL(tri_symv_kernel, dim3((unsigned)ceil_div(rows, SR * SW), G), dim3(SW * 64),
+                           0, s, wk.A, wk.panel, wk.dots, wk.tau, N, nb, j, jj);
         KMP_LAUNCH_CHECK();
+        // the trailing matrix is read once (m^2 doubles)
+        kc_end(KMP_KC_TRI_SYMV, s, over_groups(wk, [&](double n) {
+                 const double m = std::max(0.0, n - j - 1);
+                 return 8.0 * (m * m + 2.0 * jj * m); }),
+               over_groups(wk, [&](double n) {
+                 const double m = std::max(0.0, n - j - 1);
+                 return 2.0 * m * m + 4.0 * jj * m; }));
       }
     }
     if (pe < N) {
@@ -259,7 +345,12 @@ int tridiagonalize(hipStream_t s, const TridiagWork& wk) {
       ga.B = wk.panel + (int64_t)nb * N + pe; ga.ldb = N; ga.sB = (int64_t)3 * nb * N;
       ga.C = wk.A + (int64_t)pe * N + pe; ga.ldc = N; ga.sC = (int64_t)N * N;
       ga.alpha = -1.0; ga.beta = 1.0;
+      kc_begin(KMP_KC_TRI_SYR2K, s);
       if ((rc = gemm(s, ga, false, false, true)) != 0) return rc;
+      kc_end(KMP_KC_TRI_SYR2K, s, over_groups(wk, [&](double n) {
+               const double m = std::max(0.0, n - pe); return 16.0 * m * m; }),
+             over_groups(wk, [&](double n) {
+               const double m = std::max(0.0, n - pe); return 4.0 * nb * m * m; }));
     }
   }
   // Q = H_0 H_1 ... H_{N-2}, accumulated backwards panel by panel:
@@ -273,7 +364,9 @@ int tridiagonalize(hipStream_t s, const TridiagWork& wk) {
     const int m = N - p - 1;
     if (m <= 0) continue;
     const int kb = (p + nb <= N) ? nb : N - p;
-    hipLaunchKernelGGL(form_t_kernel, dim3(G), dim3(TB), 0, s, wk.A, wk.tau, wk.tmat, N, kb, p);
+    kc_begin(KMP_KC_QFORM, s);
+    hipLaunchKernelGGL(form_t_kernel, dim3(G), dim3(64), 0, s, wk.pgram, wk.tau, wk.tmat, N, nb,
+                       kb, p);
     KMP_LAUNCH_CHECK();
     GemmArgs g1;   // X = V[:, p+1:] Q[p+1:, p+1:]   (kb x m)
     g1.M = kb; g1.N = m; g1.K = m; g1.batch = G;
@@ -294,6 +387,11 @@ int tridiagonalize(hipStream_t s, const TridiagWork& wk) {
     g3.C = wk.Q + (int64_t)(p + 1) * N + p + 1; g3.ldc = N; g3.sC = (int64_t)N * N;
     g3.alpha = -1.0; g3.beta = 1.0;
     if ((rc = gemm(s, g3, false, false, true)) != 0) return rc;
+    // Q block read by the first product, read and written by the update
+    kc_end(KMP_KC_QFORM, s, over_groups(wk, [&](double n) {
+             const double mm = std::max(0.0, n - p - 1); return 24.0 * mm * mm; }),
+           over_groups(wk, [&](double n) {
+             const double mm = std::max(0.0, n - p - 1); return 4.0 * kb * mm * mm + 2.0 * kb * kb * mm; }));
   }
   return 0;
 }

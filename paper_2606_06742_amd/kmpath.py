@@ -19,23 +19,39 @@ KMP_OK, KMP_WMAXITER = 0, 1
 KMP_EINVAL, KMP_EFOLD, KMP_EWORKSPACE, KMP_EHIP, KMP_ENONFINITE = -1, -2, -3, -4, -5
 KMP_HINGE, KMP_LOGISTIC, KMP_CHECK = 0, 1, 2
 KMP_FLAG_RESTART = 1
+KMP_NKC = 10
+KERNEL_CLASSES = ("gram", "tri_col", "tri_symv", "tri_syr2k", "q_form", "precompute", "gemm_f",
+                  "gemm_zhat", "update", "finalize")
 LOSS_CODES = {"hinge": KMP_HINGE, "logistic": KMP_LOGISTIC, "check": KMP_CHECK}
 
 
 class kmp_path_spec(C.Structure):
     _fields_ = [("loss", C.c_int32), ("delta0", C.c_double), ("eta", C.c_double),
                 ("n_stages", C.c_int32), ("tol", C.c_double), ("max_iter", C.c_int32),
-                ("poll_every", C.c_int32), ("flags", C.c_int32)]
+                ("poll_every", C.c_int32), ("flags", C.c_int32), ("timing_mask", C.c_int32),
+                ("timing_every", C.c_int32)]
 
 
 class kmp_timings(C.Structure):
     _fields_ = [("gram_ms", C.c_double), ("factor_ms", C.c_double),
                 ("precompute_ms", C.c_double), ("path_ms", C.c_double),
                 ("finalize_ms", C.c_double), ("total_ms", C.c_double),
-                ("iterations", C.c_int64), ("cell_iterations", C.c_int64)]
+                ("iterations", C.c_int64), ("cell_iterations", C.c_int64),
+                ("kernel_ms", C.c_double * KMP_NKC), ("kernel_launches", C.c_int64 * KMP_NKC),
+                ("kernel_seen", C.c_int64 * KMP_NKC),
+                ("kernel_bytes", C.c_double * KMP_NKC), ("kernel_flops", C.c_double * KMP_NKC)]
 
     def as_dict(self):
-        return {k: getattr(self, k) for k, _ in self._fields_}
+        return {k: (list(getattr(self, k)) if k.startswith("kernel_") else getattr(self, k))
+                for k, _ in self._fields_}
+
+    def kernels(self):
+        """{class: (ms, bracketed launches, all launches, bytes, flops)} of the
+        timed classes; ms, bytes and flops cover the bracketed launches."""
+        return {KERNEL_CLASSES[i]: (self.kernel_ms[i], int(self.kernel_launches[i]),
+                                    int(self.kernel_seen[i]), self.kernel_bytes[i],
+                                    self.kernel_flops[i])
+                for i in range(KMP_NKC) if self.kernel_launches[i] > 0}
 
 
 class KmpError(RuntimeError):
@@ -77,12 +93,18 @@ def lib():
         L.kmp_strerror.restype = C.c_char_p
         L.kmp_version.argtypes = []
         L.kmp_version.restype = C.c_char_p
+        L.kmp_kernel_class_name.argtypes = [C.c_int]
+        L.kmp_kernel_class_name.restype = C.c_char_p
         _lib = L
     return _lib
 
 
 EXPORTED = ("kmp_default_spec", "kmp_workspace_bytes", "kmp_fit_path", "kmp_make_folds",
-            "kmp_rbf_gram", "kmp_tridiag", "kmp_strerror", "kmp_version")
+            "kmp_rbf_gram", "kmp_tridiag", "kmp_strerror", "kmp_version", "kmp_kernel_class_name")
+
+
+def kmp_kernel_class_name(cls: int) -> str:
+    return lib().kmp_kernel_class_name(int(cls)).decode()
 
 
 def kmp_strerror(code: int) -> str:
@@ -173,11 +195,12 @@ class PathRunner:
     """Holds the workspace and output tensors for repeated fits of one problem shape."""
 
     def __init__(self, X, y, loss, sigmas, lambdas, fold_id, V, taus=None, device="cuda",
-                 sigma_batch: Optional[int] = None, **spec_overrides):
+                 sigma_batch: Optional[int] = None, kernel_timing=(), **spec_overrides):
         import torch
         self.torch = torch
         self.loss = loss
         self.spec = kmp_default_spec(loss, **spec_overrides)
+        self.set_kernel_timing(kernel_timing)
         self.X = torch.as_tensor(np.ascontiguousarray(X), dtype=torch.float64, device=device) \
             if not isinstance(X, torch.Tensor) else X
         self.y = torch.as_tensor(np.ascontiguousarray(y), dtype=torch.float64, device=device) \
@@ -206,6 +229,18 @@ class PathRunner:
         self.selected = np.zeros((S, Q), dtype=np.int32)
         self.timings = kmp_timings()
         self.cells = cells
+
+    def set_kernel_timing(self, classes, every: int = 1) -> None:
+        """Time the named kernel classes with HIP events on the next runs,
+        bracketing one launch in every `every` of each class."""
+        mask = 0
+        for c in classes:
+            mask |= 1 << (KERNEL_CLASSES.index(c) if isinstance(c, str) else int(c))
+        self.spec.timing_mask = mask
+        self.spec.timing_every = int(every)
+
+    def kernel_times(self) -> dict:
+        return self.timings.kernels()
 
     def run(self, stream=None) -> int:
         code = kmp_fit_path(_stream_ptr(stream), self.spec, self.X, self.y, self.sigmas,
