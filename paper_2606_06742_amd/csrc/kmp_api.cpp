@@ -76,6 +76,7 @@ void kc_end(int cls, hipStream_t s, double bytes, double flops) {
 namespace {
 
 constexpr int kPanel = 32;       // Householder panel width
+constexpr int kWyBlock = 64;     // reflectors per compact-WY block when forming Q
 constexpr int kRowAlign = 64;    // padding of the per-fold matrix order
 constexpr size_t kAlign = 256;
 
@@ -103,7 +104,8 @@ struct Carver {
 // Workspace layout for one bandwidth batch (G = Sb * V groups). Used both to
 // size and to carve, so the two can never disagree.
 struct Layout {
-  double *A, *Qm, *diag, *off, *tau, *cvec, *ylab, *panel, *dots, *tmat, *xbuf, *ybuf, *pgram;
+  double *A, *Qm, *diag, *off, *tau, *cvec, *ylab, *panel, *dots, *tmat, *gram, *xbuf, *ybuf;
+  double *spart, *pnext;
   double *ahat, *abar, *bmat, *zmat, *zhat, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
   double *beta, *bbar, *rmom, *gcoef, *kkt, *lam, *taucol, *fbuf, *nrm, *inv2s2;
   int *flag, *iters, *iters_total, *active, *nvg;
@@ -123,10 +125,12 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.ylab = c.take<double>(G * N);
   l.panel = c.take<double>(G * 3 * kPanel * N);
   l.dots = c.take<double>(G * 2 * kPanel);
-  l.tmat = c.take<double>(G * kPanel * kPanel);
-  l.xbuf = c.take<double>(G * kPanel * N);
-  l.ybuf = c.take<double>(G * kPanel * N);
-  l.pgram = c.take<double>(G * kPanel * N);
+  l.tmat = c.take<double>(G * kWyBlock * kWyBlock);
+  l.gram = c.take<double>(G * kWyBlock * kWyBlock);
+  l.xbuf = c.take<double>(G * kWyBlock * N);
+  l.ybuf = c.take<double>(G * kWyBlock * N);
+  l.spart = c.take<double>(G * (size_t)tridiag_parts((int)N));
+  l.pnext = c.take<double>(G * N);
   l.ahat = c.take<double>(cols * N);
   l.abar = c.take<double>(cols * N);
   l.bmat = c.take<double>(cols * N);
@@ -342,10 +346,12 @@ int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N, double* Qout, dou
   w.tau = q; q += (size_t)G * N;
   w.panel = q; q += (size_t)G * 3 * kPanel * N;
   w.dots = q; q += (size_t)G * 2 * kPanel;
-  w.tmat = q; q += (size_t)G * kPanel * kPanel;
-  w.xbuf = q; q += (size_t)G * kPanel * N;
-  w.ybuf = q; q += (size_t)G * kPanel * N;
-  w.pgram = q;
+  w.tmat = q; q += (size_t)G * kWyBlock * kWyBlock;
+  w.gram = q; q += (size_t)G * kWyBlock * kWyBlock;
+  w.xbuf = q; q += (size_t)G * kWyBlock * N;
+  w.ybuf = q; q += (size_t)G * kWyBlock * N;
+  w.spart = q; q += (size_t)G * tridiag_parts(N);
+  w.pnext = q;
   int rc = tridiagonalize(s, w);
   KMP_HIP_TRY(hipFreeAsync(scratch, s));
   KMP_HIP_TRY(hipStreamSynchronize(s));
@@ -542,7 +548,8 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     TridiagWork tw;
     tw.G = Gb; tw.N = N; tw.nb = kPanel; tw.A = lay.A; tw.Q = lay.Qm; tw.diag = lay.diag;
     tw.off = lay.off; tw.tau = lay.tau; tw.panel = lay.panel; tw.dots = lay.dots;
-    tw.tmat = lay.tmat; tw.xbuf = lay.xbuf; tw.ybuf = lay.ybuf; tw.pgram = lay.pgram;
+    tw.tmat = lay.tmat; tw.gram = lay.gram; tw.xbuf = lay.xbuf; tw.ybuf = lay.ybuf;
+    tw.spart = lay.spart; tw.pnext = lay.pnext;
     tw.nv_host = nvg.data();
     if ((rc = tridiagonalize(s, tw)) != 0) return rc;
     if ((rc = group_ones_projection(s, lay.Qm, lay.nvg, Gb, N, lay.cvec)) != 0) return rc;

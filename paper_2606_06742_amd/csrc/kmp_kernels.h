@@ -72,14 +72,21 @@ struct TridiagWork {
   double* tau = nullptr;    // G x N (Householder scalars)
   double* panel = nullptr;  // G x 3nb x N  ([V; W; V] rows of the current panel)
   double* dots = nullptr;   // G x 2nb
-  double* tmat = nullptr;   // G x nb x nb (compact-WY T factor)
-  double* xbuf = nullptr;   // G x nb x N
-  double* ybuf = nullptr;   // G x nb x N
-  double* pgram = nullptr;  // G x N x nb (Gram of each panel's reflectors)
+  double* tmat = nullptr;   // G x 64 x 64 (compact-WY T factor of a block of Q)
+  double* gram = nullptr;   // G x 64 x 64 (Gram of that block's reflectors)
+  double* xbuf = nullptr;   // G x 64 x N
+  double* ybuf = nullptr;   // G x 64 x N
+  double* spart = nullptr;  // G x tridiag_parts(N) partial sums of w_raw'v
+  double* pnext = nullptr;  // G x N next column, partially updated
   const int* nv_host = nullptr;  // G valid orders (host), for the work counters; N if null
 };
+// Per-matrix length of the spart buffer (partial sums of the products).
+int tridiag_parts(int N);
+// Doubles of scratch tridiagonalize needs beyond A, Q, diag, off, tau.
 size_t tridiag_panel_doubles(int G, int N, int nb);
 int tridiagonalize(hipStream_t s, const TridiagWork& w);
+// nch independent parts, part k on stream ss[k] (launches interleaved).
+int tridiagonalize_multi(const hipStream_t* ss, const TridiagWork* ws, int nch);
 
 // ---------------------------------------------------------------- path
 struct PathArrays {
