@@ -39,7 +39,47 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-cells", type=int, default=48)
     ap.add_argument("--timing-every", type=int, default=16)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device-to-device three times (a plain copy of known "
+                         "size, the reference for the HBM byte counters) and exit")
     return ap.parse_args()
+
+
+def copy_calibration(mib):
+    """Three plain device copies of `mib` MiB: under the counter profiler they
+    give the FETCH_SIZE / WRITE_SIZE readings of a known byte count."""
+    import torch
+    dev = torch.device("cuda:0")
+    n = mib * (1 << 20) // 8
+    src = torch.ones(n, dtype=torch.float64, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize(dev)
+    print(json.dumps({"copy_bytes_per_launch": n * 8, "launches": 3}), flush=True)
+
+
+def profiled_traffic(kernel_class, workload):
+    """HBM bytes per launch of `kernel_class` on `workload` from the committed
+    counter summary profiles/pmc_<class>_<workload>.txt, or None when there is
+    none or when a source file it lists has changed since the counters were
+    taken (its recorded sha256 no longer matches)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"pmc_{kernel_class}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    traffic = None
+    for line in open(path):
+        parts = line.split()
+        if len(parts) == 4 and parts[0] == "source" and parts[2] == "sha256":
+            src = os.path.join(ROOT, parts[1])
+            if not os.path.exists(src):
+                return None
+            if hashlib.sha256(open(src, "rb").read()).hexdigest() != parts[3]:
+                return None
+        elif len(parts) == 2 and parts[0] == "traffic_bytes_per_launch:":
+            traffic = float(parts[1])
+    return traffic
 
 
 def cpu_baseline(inp, w, ncells):
@@ -75,7 +115,7 @@ def cpu_baseline(inp, w, ncells):
 MFMA_CLASSES = ("gemm_f", "gemm_zhat", "tri_syr2k", "q_form", "gram")
 
 
-def roofline(kt):
+def roofline(kt, workload):
     """Roofline object of the dominant timed kernel class."""
     if not kt:
         return None
@@ -86,20 +126,27 @@ def roofline(kt):
     if name in MFMA_CLASSES:
         achieved = flops / sec / 1e12
         return {"kernel": name, "bound": "mfma", "achieved": achieved, "peak": FP64_PEAK_TFS,
-                "unit": "TFLOP/s", "frac": achieved / FP64_PEAK_TFS, "traffic": None,
+                "unit": "TFLOP/s", "frac": achieved / FP64_PEAK_TFS,
+                "traffic": profiled_traffic(name, workload),
+                "algorithmic_flops_per_launch": flops / launches,
                 "avg_launch_us": 1e3 * ms / launches, "timed_launches": launches}
     achieved = nbytes / sec / 1e9
     return {"kernel": name, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+            "traffic": profiled_traffic(name, workload),
+            "algorithmic_bytes_per_launch": nbytes / launches,
             "avg_launch_us": 1e3 * ms / launches, "timed_launches": launches}
 
 
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
+        print(json.dumps({"error": "this benchmark runs on one GPU; --gpus must be 1",
                           "requested_gpus": args.gpus}))
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     import torch
     import workloads as W
     from paper_2606_06742_amd import kmpath as km
@@ -139,7 +186,7 @@ def main():
     res = runner.results()
     assert np.all(res["status"] == 0), "some cells did not converge"
 
-    roof = roofline(kt)
+    roof = roofline(kt, w.name)
     out = {
         "metric": METRIC, "value": value, "unit": "fits/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
