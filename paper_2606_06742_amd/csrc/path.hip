@@ -51,23 +51,33 @@ int gather_labels(hipStream_t s, const double* y, const int32_t* tidx, int V, in
   return 0;
 }
 
-// c = Q'1 over the valid rows of each group (one thread per column of Q).
-__global__ void ones_projection_kernel(const double* __restrict__ Q, const int* __restrict__ nv,
-                                       int G, int N, double* __restrict__ cvec) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)G * N) return;
-  const int g = (int)(idx / N), j = (int)(idx % N);
+// c = Q'1 over the valid rows of each group. Block (64 columns x 16 row
+// groups): lanes read consecutive columns of a row (coalesced), the 16 row
+// groups are added in a fixed order.
+constexpr int OPC = 64, OPR = 16;
+__global__ __launch_bounds__(OPC * OPR) void ones_projection_kernel(const double* __restrict__ Q,
+                                                                    const int* __restrict__ nv,
+                                                                    int N, double* __restrict__ cvec) {
+  __shared__ double part[OPR][OPC];
+  const int g = blockIdx.y;
+  const int j = blockIdx.x * OPC + threadIdx.x, ry = threadIdx.y;
   const double* Qg = Q + (int64_t)g * N * N;
   const int m = nv[g];
   double s = 0.0;
-  for (int i = 0; i < m; ++i) s += Qg[(int64_t)i * N + j];
-  cvec[idx] = s;
+  if (j < N)
+    for (int i = ry; i < m; i += OPR) s += Qg[(int64_t)i * N + j];
+  part[ry][threadIdx.x] = s;
+  __syncthreads();
+  if (ry == 0 && j < N) {
+    double t = 0.0;
+    for (int r = 0; r < OPR; ++r) t += part[r][threadIdx.x];
+    cvec[(int64_t)g * N + j] = t;
+  }
 }
 
 int group_ones_projection(hipStream_t s, const double* Q, const int* nv, int G, int N, double* cvec) {
-  const int64_t tot = (int64_t)G * N;
-  hipLaunchKernelGGL(ones_projection_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, s, Q,
-                     nv, G, N, cvec);
+  hipLaunchKernelGGL(ones_projection_kernel, dim3((unsigned)ceil_div(N, OPC), (unsigned)G),
+                     dim3(OPC, OPR), 0, s, Q, nv, N, cvec);
   KMP_LAUNCH_CHECK();
   return 0;
 }
@@ -86,100 +96,12 @@ int path_init_columns(hipStream_t s, const PathArrays& p) {
   return 0;
 }
 
-// ------------------------------------------------------ per-stage factors
-// One thread per column: LDL' of M = 2 lambda I + T/(n_v kappa), then
-// vhat = M^{-1} c/(n_v kappa), u = T vhat, g = 1/(2 lambda c'vhat); restart
-// the momentum (r = 1, abar = ahat) and reactivate converged columns.
-__global__ void precompute_kernel(int G, int N, int C, const int* __restrict__ nv,
-                                  const double* __restrict__ Td, const double* __restrict__ To,
-                                  const double* __restrict__ cvec, const double* __restrict__ lamv,
-                                  double kappa, double* __restrict__ ldl_l, double* __restrict__ ldl_d,
-                                  double* __restrict__ vhat, double* __restrict__ uvec,
-                                  double* __restrict__ gcoef, double* __restrict__ ahat,
-                                  double* __restrict__ abar, double* __restrict__ bmat,
-                                  double* __restrict__ beta, double* __restrict__ bbar,
-                                  double* __restrict__ rmom, int* __restrict__ flag,
-                                  int* __restrict__ iters) {
-  const int64_t gc = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (gc >= (int64_t)G * C) return;
-  const int g = (int)(gc / C);
-  const double lam = lamv[gc];
-  const double sc = 1.0 / ((double)nv[g] * kappa);
-  const double* d = Td + (int64_t)g * N;
-  const double* o = To + (int64_t)g * N;
-  const double* c = cvec + (int64_t)g * N;
-  double* L = ldl_l + gc * N;
-  double* Di = ldl_d + gc * N;
-  double* vh = vhat + gc * N;
-  double* u = uvec + gc * N;
-  // factor and forward substitution with rhs c*sc
-  double dprev = 2.0 * lam + d[0] * sc;
-  double yprev = c[0] * sc;
-  Di[0] = 1.0 / dprev;
-  vh[0] = yprev;
-  for (int i = 1; i < N; ++i) {
-    const double oi = o[i - 1] * sc;
-    const double li = oi / dprev;
-    L[i - 1] = li;
-    dprev = 2.0 * lam + d[i] * sc - li * oi;
-    Di[i] = 1.0 / dprev;
-    yprev = c[i] * sc - li * yprev;
-    vh[i] = yprev;
-  }
-  L[N - 1] = 0.0;
-  // diagonal and back substitution
-  double xnext = vh[N - 1] * Di[N - 1];
-  vh[N - 1] = xnext;
-  for (int i = N - 2; i >= 0; --i) {
-    xnext = vh[i] * Di[i] - L[i] * xnext;
-    vh[i] = xnext;
-  }
-  double cv = 0.0;
-  for (int i = 0; i < N; ++i) {
-    double ui = d[i] * vh[i];
-    if (i > 0) ui += o[i - 1] * vh[i - 1];
-    if (i + 1 < N) ui += o[i] * vh[i + 1];
-    u[i] = ui;
-    cv += c[i] * vh[i];
-  }
-  gcoef[gc] = 1.0 / (2.0 * lam * cv);
-  // stage restart of the accelerated iteration
-  double* ah = ahat + gc * N;
-  double* ab = abar + gc * N;
-  double* bm = bmat + gc * N;
-  for (int i = 0; i < N; ++i) ab[i] = ah[i];
-  for (int i = 0; i < N; ++i) {
-    double b = d[i] * ah[i];
-    if (i > 0) b += o[i - 1] * ah[i - 1];
-    if (i + 1 < N) b += o[i] * ah[i + 1];
-    bm[i] = b;
-  }
-  bbar[gc] = beta[gc];
-  rmom[gc] = 1.0;
-  if (flag[gc] == 1 || flag[gc] == 2) flag[gc] = 0;
-  iters[gc] = 0;
-}
-
 // Sum over groups of f(valid rows) for the work counters.
 template <typename F>
 static double over_groups(const PathArrays& p, F f) {
   double a = 0.0;
   for (int g = 0; g < p.G; ++g) a += f((double)(p.nv_host ? p.nv_host[g] : p.N));
   return a;
-}
-
-int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa) {
-  const int64_t cols = (int64_t)p.G * p.C;
-  kc_begin(KMP_KC_PRECOMPUTE, s);
-  hipLaunchKernelGGL(precompute_kernel, dim3((unsigned)ceil_div(cols, 64)), dim3(64), 0, s, p.G,
-                     p.N, p.C, p.nv, p.Tdiag, p.Toff, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
-                     p.uvec, p.gcoef, p.ahat, p.abar, p.bmat, p.beta, p.bbar, p.rmom, p.flag,
-                     p.iters);
-  KMP_LAUNCH_CHECK();
-  // reads T, c, ahat; writes l, d, vhat, u, abar, T ahat
-  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * 8.0; }),
-         over_groups(p, [&](double n) { return 20.0 * n * p.C; }));
-  return 0;
 }
 
 // ---------------------------------------------------------- scan helpers
@@ -231,6 +153,216 @@ __device__ __forceinline__ Aff block_exclusive_scan_rev(Aff m, Aff* sh) {
   Aff pre{1.0, 0.0};
   for (int k = PW - 1; k > w; --k) pre = compose(sh[k], pre);
   return compose(ex, pre);
+}
+
+// Solve (L D L') x = w on the rows [i0, i0 + E) owned by this thread, L unit
+// lower bidiagonal (l[i] = L[i+1][i]), dv = 1/D. lv holds l on the own rows,
+// lprev = l[i0 - 1] (0 for the first thread). wv holds w on entry and x on
+// exit. Both triangular solves are first-order affine recurrences, done as
+// block-wide scans of affine maps.
+template <int E>
+__device__ __forceinline__ void ldl_solve(double (&wv)[E], const double (&lv)[E], double lprev,
+                                          const double (&dv)[E], Aff* sh) {
+  // forward: y_i = w_i - l_{i-1} y_{i-1}
+  Aff m{1.0, 0.0};
+  {
+    double ca = 1.0, cb = 0.0, lp = lprev;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      ca = -lp * ca;
+      cb = fma(-lp, cb, wv[e]);
+      lp = lv[e];
+    }
+    m = Aff{ca, cb};
+  }
+  Aff pre = block_exclusive_scan(m, sh);
+  {
+    double yin = pre.b;                       // y_{i0-1} (maps applied to 0)
+    double lp = lprev;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const double yi = fma(-lp, yin, wv[e]);
+      wv[e] = yi;
+      yin = yi;
+      lp = lv[e];
+    }
+  }
+  // diagonal
+#pragma unroll
+  for (int e = 0; e < E; ++e) wv[e] *= dv[e];
+  // backward: x_i = z_i - l_i x_{i+1}
+  {
+    double ca = 1.0, cb = 0.0;
+#pragma unroll
+    for (int e = E - 1; e >= 0; --e) {
+      ca = -lv[e] * ca;
+      cb = fma(-lv[e], cb, wv[e]);
+    }
+    m = Aff{ca, cb};
+  }
+  pre = block_exclusive_scan_rev(m, sh);
+  {
+    double xin = pre.b;                       // x_{i0+E}
+#pragma unroll
+    for (int e = E - 1; e >= 0; --e) {
+      const double xi = fma(-lv[e], xin, wv[e]);
+      wv[e] = xi;
+      xin = xi;
+    }
+  }
+}
+
+// y = T x for the own rows of a thread (T tridiagonal, diagonal Td, off-
+// diagonal To[i] = T[i+1][i]); neighbours across threads through LDS.
+template <int E>
+__device__ __forceinline__ void tri_apply(const double (&x)[E], double (&y)[E], int i0, int N,
+                                          const double* __restrict__ Tdg,
+                                          const double* __restrict__ Tog, double* edge_lo,
+                                          double* edge_hi) {
+  const int t = threadIdx.x;
+  __syncthreads();
+  edge_lo[t] = x[0];
+  edge_hi[t] = x[E - 1];
+  __syncthreads();
+  const double left = t > 0 ? edge_hi[t - 1] : 0.0;
+  const double right = t + 1 < (int)blockDim.x ? edge_lo[t + 1] : 0.0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = i0 + e;
+    double bv = 0.0;
+    if (i < N) {
+      const double xl = e > 0 ? x[e - 1] : left;
+      const double xr = e + 1 < E ? x[e + 1] : right;
+      bv = Tdg[i] * x[e];
+      if (i > 0) bv = fma(Tog[i - 1], xl, bv);
+      if (i + 1 < N) bv = fma(Tog[i], xr, bv);
+    }
+    y[e] = bv;
+  }
+}
+
+// ------------------------------------------------------ per-stage factors
+// One workgroup per column: LDL' of M = 2 lambda I + T/(n_v kappa) (the
+// pivot recurrence is sequential, run by one thread over LDS-staged chunks
+// of T), then vhat = M^{-1} c/(n_v kappa), u = T vhat, g = 1/(2 lambda
+// c'vhat); restart the momentum (r = 1, abar = ahat, B = T ahat) and
+// reactivate the columns that stopped in the previous stage.
+template <int E>
+__global__ __launch_bounds__(PB) void precompute_kernel(
+    int N, int C, const int* __restrict__ nv, const double* __restrict__ Td,
+    const double* __restrict__ To, const double* __restrict__ cvec, const double* __restrict__ lamv,
+    double kappa, double* __restrict__ ldl_l, double* __restrict__ ldl_d, double* __restrict__ vhat,
+    double* __restrict__ uvec, double* __restrict__ gcoef, const double* __restrict__ ahat,
+    double* __restrict__ abar, double* __restrict__ bmat, const double* __restrict__ beta,
+    double* __restrict__ bbar, double* __restrict__ rmom, int* __restrict__ flag,
+    int* __restrict__ iters) {
+  __shared__ double red[PW];
+  __shared__ Aff sh[PW];
+  __shared__ double sd[PB], so[PB], sl[PB], sdi[PB];
+  __shared__ double edge_lo[PB], edge_hi[PB];
+  const int64_t gc = blockIdx.x;
+  const int g = (int)(gc / C);
+  const int t = threadIdx.x;
+  const int i0 = t * E;
+  const int64_t base = gc * N;
+  const double lam = lamv[gc];
+  const double sc = 1.0 / ((double)nv[g] * kappa);
+  const double* d = Td + (int64_t)g * N;
+  const double* o = To + (int64_t)g * N;
+  const double* c = cvec + (int64_t)g * N;
+  // pivots: D_i = 2 lambda + T_ii sc - l_{i-1} T_{i,i-1} sc, l_i = T_{i+1,i} sc / D_i
+  double lrun = 0.0, orun = 0.0;
+  for (int c0 = 0; c0 < N; c0 += PB) {
+    const int i = c0 + t;
+    sd[t] = i < N ? d[i] : 0.0;
+    so[t] = i < N ? o[i] : 0.0;
+    __syncthreads();
+    if (t == 0) {
+      const int cnt = (N - c0 < PB) ? N - c0 : PB;
+      for (int k = 0; k < cnt; ++k) {
+        const double piv = fma(-lrun, orun, fma(sd[k], sc, 2.0 * lam));
+        const double dinv = 1.0 / piv;
+        orun = so[k] * sc;
+        lrun = (c0 + k + 1 < N) ? orun * dinv : 0.0;
+        sl[k] = lrun;
+        sdi[k] = dinv;
+      }
+    }
+    __syncthreads();
+    if (i < N) {
+      ldl_l[base + i] = sl[t];
+      ldl_d[base + i] = sdi[t];
+    }
+    __syncthreads();
+  }
+  double lv[E], dv[E], wv[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = i0 + e;
+    lv[e] = i < N ? ldl_l[base + i] : 0.0;
+    dv[e] = i < N ? ldl_d[base + i] : 0.0;
+    wv[e] = i < N ? c[i] * sc : 0.0;
+  }
+  const double lprev = (i0 > 0 && i0 - 1 < N) ? ldl_l[base + i0 - 1] : 0.0;
+  ldl_solve<E>(wv, lv, lprev, dv, sh);
+  double u[E];
+  tri_apply<E>(wv, u, i0, N, d, o, edge_lo, edge_hi);
+  double cv = 0.0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = i0 + e;
+    if (i < N) {
+      vhat[base + i] = wv[e];
+      uvec[base + i] = u[e];
+      cv = fma(c[i], wv[e], cv);
+    }
+  }
+  cv = block_sum<PW>(cv, red);
+  // stage restart of the accelerated iteration
+  double ah[E], bm[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) ah[e] = (i0 + e < N) ? ahat[base + i0 + e] : 0.0;
+  tri_apply<E>(ah, bm, i0, N, d, o, edge_lo, edge_hi);
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = i0 + e;
+    if (i < N) {
+      abar[base + i] = ah[e];
+      bmat[base + i] = bm[e];
+    }
+  }
+  if (t == 0) {
+    gcoef[gc] = 1.0 / (2.0 * lam * cv);
+    bbar[gc] = beta[gc];
+    rmom[gc] = 1.0;
+    if (flag[gc] == 1 || flag[gc] == 2) flag[gc] = 0;
+    iters[gc] = 0;
+  }
+}
+
+int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa) {
+  const unsigned cols = (unsigned)(p.G * p.C);
+  kc_begin(KMP_KC_PRECOMPUTE, s);
+#define KMP_PRE(EE)                                                                              \
+  hipLaunchKernelGGL(precompute_kernel<EE>, dim3(cols), dim3(PB), 0, s, p.N, p.C, p.nv, p.Tdiag, \
+                     p.Toff, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat, p.uvec, p.gcoef,    \
+                     p.ahat, p.abar, p.bmat, p.beta, p.bbar, p.rmom, p.flag, p.iters)
+  if (p.N <= PB * 1) KMP_PRE(1);
+  else if (p.N <= PB * 2) KMP_PRE(2);
+  else if (p.N <= PB * 4) KMP_PRE(4);
+  else if (p.N <= PB * 8) KMP_PRE(8);
+  else if (p.N <= PB * 16) KMP_PRE(16);
+  else if (p.N <= PB * 32) KMP_PRE(32);
+  else {
+    set_error("path: more than 8192 training points per fold is not supported yet");
+    return KMP_EINVAL;
+  }
+#undef KMP_PRE
+  KMP_LAUNCH_CHECK();
+  // reads T, c, ahat; writes l, 1/d, vhat, u, abar, T ahat
+  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * 8.0; }),
+         over_groups(p, [&](double n) { return 20.0 * n * p.C; }));
+  return 0;
 }
 
 // ------------------------------------------------------- the update (K2)
@@ -298,58 +430,14 @@ __global__ __launch_bounds__(PB) void update_kernel(
     if (t == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; }
     return;
   }
-  // forward solve L y = w  (y_i = w_i - l_{i-1} y_{i-1})
-  double lv[E];
+  double lv[E], dv[E];
 #pragma unroll
-  for (int e = 0; e < E; ++e) lv[e] = (i0 + e < N) ? ldl_l[base + i0 + e] : 0.0;
+  for (int e = 0; e < E; ++e) {
+    lv[e] = (i0 + e < N) ? ldl_l[base + i0 + e] : 0.0;
+    dv[e] = (i0 + e < N) ? ldl_d[base + i0 + e] : 0.0;
+  }
   const double lprev = (i0 > 0 && i0 - 1 < N) ? ldl_l[base + i0 - 1] : 0.0;
-  Aff m{1.0, 0.0};
-  {
-    double ca = 1.0, cb = 0.0, lp = lprev;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      ca = -lp * ca;
-      cb = fma(-lp, cb, wv[e]);
-      lp = lv[e];
-    }
-    m = Aff{ca, cb};
-  }
-  Aff pre = block_exclusive_scan(m, sh);
-  {
-    double yin = pre.b;                       // y_{i0-1} (maps applied to 0)
-    double lp = lprev;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const double yi = fma(-lp, yin, wv[e]);
-      wv[e] = yi;
-      yin = yi;
-      lp = lv[e];
-    }
-  }
-  // diagonal: z_i = y_i / d_i
-#pragma unroll
-  for (int e = 0; e < E; ++e)
-    if (i0 + e < N) wv[e] *= ldl_d[base + i0 + e];
-  // backward solve L' x = z  (x_i = z_i - l_i x_{i+1})
-  {
-    double ca = 1.0, cb = 0.0;
-#pragma unroll
-    for (int e = E - 1; e >= 0; --e) {
-      ca = -lv[e] * ca;
-      cb = fma(-lv[e], cb, wv[e]);
-    }
-    m = Aff{ca, cb};
-  }
-  pre = block_exclusive_scan_rev(m, sh);
-  {
-    double xin = pre.b;                       // x_{i0+E}
-#pragma unroll
-    for (int e = E - 1; e >= 0; --e) {
-      const double xi = fma(-lv[e], xin, wv[e]);
-      wv[e] = xi;
-      xin = xi;
-    }
-  }
+  ldl_solve<E>(wv, lv, lprev, dv, sh);
   // step, new iterate and the restart test
   const double gco = gcoef[gc];
   const double sa = gco * (tsum - d0);
