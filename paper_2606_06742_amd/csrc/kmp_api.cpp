@@ -84,6 +84,7 @@ struct Plan {
   int64_t n = 0, d = 0;
   int V = 0, S = 0, Qt = 1, L = 0, Sb = 0;
   int N = 0, C = 0, G = 0, RT = 0;
+  int Mh = 0;                    // held-out rows per fold, padded (max m_v rounded up to 64)
   std::vector<int> nv;           // per fold
   size_t bytes = 0;
 };
@@ -109,7 +110,7 @@ struct Layout {
   double *ahat, *abar, *bmat, *zmat, *zhat, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
   double *beta, *bbar, *rmom, *gcoef, *kkt, *lam, *taucol, *fbuf, *nrm, *inv2s2;
   int *flag, *iters, *iters_total, *active, *nvg;
-  int32_t *tidx, *fold;
+  int32_t *tidx, *hidx, *fold;
 };
 
 size_t carve(const Plan& p, void* ws, Layout* out) {
@@ -150,7 +151,7 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.kkt = c.take<double>(cols);
   l.lam = c.take<double>(cols);
   l.taucol = c.take<double>(cols);
-  l.fbuf = c.take<double>(cols * (size_t)p.n);
+  l.fbuf = c.take<double>(cols * (size_t)p.Mh);
   l.nrm = c.take<double>((size_t)p.n);
   l.inv2s2 = c.take<double>((size_t)std::max(p.S, 1));
   l.flag = c.take<int>(cols);
@@ -159,6 +160,7 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.active = c.take<int>(1);
   l.nvg = c.take<int>(G);
   l.tidx = c.take<int32_t>((size_t)p.V * N);
+  l.hidx = c.take<int32_t>((size_t)p.V * p.Mh);
   l.fold = c.take<int32_t>((size_t)p.n);
   if (out) *out = l;
   return c.off + kAlign;
@@ -186,6 +188,7 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
     m[f] += 1;
   }
   int maxnv = 0;
+  int64_t maxm = 0;
   for (int v = 0; v < V; ++v) {
     if (m[v] == 0) {
       set_error("fold " + std::to_string(v) + " is empty");
@@ -193,8 +196,12 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
     }
     p->nv[v] = (int)(n - m[v]);
     maxnv = std::max(maxnv, p->nv[v]);
+    maxm = std::max(maxm, m[v]);
   }
   p->N = (int)round_up(maxnv, kRowAlign);
+  // a fold's held-out set is no larger than any other fold's training set,
+  // so the padded held-out block fits in the N x N factor buffer
+  p->Mh = (int)round_up(maxm, kRowAlign);
   if (p->N > 8192) {
     set_error("more than 8192 training points per fold is not supported yet");
     return KMP_EINVAL;
@@ -472,6 +479,14 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   }
   KMP_HIP_TRY(hipMemcpyAsync(lay.tidx, tidx.data(), sizeof(int32_t) * tidx.size(),
                              hipMemcpyHostToDevice, s));
+  std::vector<int32_t> hidx((size_t)V * plan.Mh, -1);
+  for (int v = 0; v < V; ++v) {
+    int k = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (fold_id[i] == v) hidx[(size_t)v * plan.Mh + k++] = (int32_t)i;
+  }
+  KMP_HIP_TRY(hipMemcpyAsync(lay.hidx, hidx.data(), sizeof(int32_t) * hidx.size(),
+                             hipMemcpyHostToDevice, s));
   KMP_HIP_TRY(hipMemcpyAsync(lay.fold, fold_id, sizeof(int32_t) * n, hipMemcpyHostToDevice, s));
   const size_t ncell = (size_t)S * Qn * V * L;
   KMP_HIP_TRY(hipMemsetAsync(alpha, 0, sizeof(double) * ncell * n, s));
@@ -593,6 +608,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     fa.n = (int)n; fa.d = (int)d; fa.ldx = ldx; fa.X = X; fa.nrm = lay.nrm; fa.y = y;
     fa.fold = lay.fold; fa.tidx = lay.tidx; fa.V = V; fa.S_b = sb; fa.Qt = Qn; fa.L = L;
     fa.s0 = s0; fa.S = S; fa.inv2s2 = lay.inv2s2; fa.delta = delta_final; fa.fbuf = lay.fbuf;
+    fa.hidx = lay.hidx; fa.Mh = plan.Mh; fa.kh = lay.A; fa.ftrain = lay.fpart;
     fa.alpha = alpha; fa.beta_out = beta; fa.objective = objective; fa.cv_sum = cv_sum;
     fa.cv_err = cv_err; fa.iters = iters; fa.status = status;
     KMP_HIP_TRY(hipEventRecord(tm.ev[6], s));

@@ -135,18 +135,23 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
 int path_count_active(hipStream_t s, const PathArrays& p);
 int group_ones_projection(hipStream_t s, const double* Q, const int* nv, int G, int N, double* cvec);
 
-// Finalize: alpha_loc = Q ahat (zmat reused), predictions for all n points
-// from K recomputed on the fly, objective/CV sums, scatter of alpha.
+// Finalize: alpha_loc = Q ahat (zmat reused), training predictions
+// f = Q (T ahat) + beta, held-out predictions K[H_v, T_v] alpha + beta with
+// the held-out kernel block built on matrix cores, objective/CV sums,
+// scatter of alpha.
 struct FinalArgs {
   int n = 0, d = 0; int64_t ldx = 0;
   const double* X = nullptr; const double* nrm = nullptr; const double* y = nullptr;
   const int32_t* fold = nullptr;   // n fold ids (device)
   const int32_t* tidx = nullptr;   // V x N training indices (-1 pad)
+  const int32_t* hidx = nullptr;   // V x Mh held-out indices (-1 pad)
+  int Mh = 0;                      // padded held-out rows per fold (<= N)
   int V = 0, S_b = 0, Qt = 1, L = 0, s0 = 0, S = 0;
   const double* inv2s2 = nullptr;  // S_b bandwidth factors of this batch
   double delta = 1.0;
-  double* fbuf = nullptr;          // G x C x n predictions
-  double* red = nullptr;           // G x C x 4 x tiles partial sums
+  double* kh = nullptr;            // G x Mh x N held-out kernel blocks (ld N, stride N*N)
+  double* ftrain = nullptr;        // G x C x N training predictions (without beta)
+  double* fbuf = nullptr;          // G x C x Mh held-out predictions (without beta)
   // outputs (full arrays, cell ((s*Q+q)*V+v)*L+l)
   double* alpha = nullptr; double* beta_out = nullptr; double* objective = nullptr;
   double* cv_sum = nullptr; int32_t* cv_err = nullptr; int32_t* iters = nullptr;

@@ -571,99 +571,32 @@ int path_count_active(hipStream_t s, const PathArrays& p) {
 }
 
 // --------------------------------------------------------------- finalize
-// f[g][c][i] = sum_{j < n_v} K(x_i, x_{T[j]}) alpha[g][c][j] + beta, for all
-// n points, with the kernel entries recomputed from X (norm expansion, the
-// same formula as the Gram build) into LDS and contracted on matrix cores.
-typedef double dbl4 __attribute__((ext_vector_type(4)));
-constexpr int FT = 64, FK = 16, FPAD = 4;
-
-__global__ __launch_bounds__(256) void predict_kernel(
-    int n, int d, int64_t ldx, const double* __restrict__ X, const double* __restrict__ nrm,
-    const int32_t* __restrict__ tidx, int V, int N, int C, const int* __restrict__ nvv,
-    const double* __restrict__ inv2s2, const double* __restrict__ alpha_loc,
-    const double* __restrict__ betav, double* __restrict__ fbuf) {
-  __shared__ double Ks[FK][FT + FPAD];
-  __shared__ double Bs[FK][FT + FPAD];
-  __shared__ int32_t cj[FK];
-  const int g = blockIdx.z;
-  const int v = g % V, sl = g / V;
-  const int i0 = blockIdx.x * FT, c0 = blockIdx.y * FT;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int wi = (w & 1) * 32, wj = (w >> 1) * 32;
-  const int li = lane & 15, lk = lane >> 4;
-  const int nv = nvv[g];
-  const double f2 = inv2s2[sl];
-  const int32_t* T = tidx + (int64_t)v * N;
-  const double* A = alpha_loc + (int64_t)g * C * N;
-  dbl4 acc[2][2];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = dbl4{0.0, 0.0, 0.0, 0.0};
-  for (int j0 = 0; j0 < nv; j0 += FK) {
-    __syncthreads();
-    if (t < FK) cj[t] = (j0 + t < nv) ? T[j0 + t] : -1;
-    __syncthreads();
-    // kernel tile: rows i0..i0+63 (points), cols j0..j0+15 (training points)
-    for (int e = t; e < FT * FK; e += 256) {
-      const int ii = e / FK, kk = e % FK;
-      const int gi = i0 + ii;
-      const int32_t xc = cj[kk];
-      double kv = 0.0;
-      if (gi < n && xc >= 0) {
-        if (gi == xc) {
-          kv = 1.0;
-        } else {
-          const double* xa = X + (int64_t)gi * ldx;
-          const double* xb = X + (int64_t)xc * ldx;
-          double dot = 0.0;
-          for (int q = 0; q < d; ++q) dot = fma(xa[q], xb[q], dot);
-          double d2 = nrm[gi] + nrm[xc] - 2.0 * dot;
-          d2 = d2 > 0.0 ? d2 : 0.0;
-          kv = exp(-d2 * f2);
-        }
-      }
-      Ks[kk][ii] = kv;
-    }
-    // coefficient tile: rows j0..j0+15, cols c0..c0+63
-    for (int e = t; e < FK * FT; e += 256) {
-      const int kk = e % FK, cc = e / FK;
-      const int gj = j0 + kk, gcn = c0 + cc;
-      Bs[kk][cc] = (gj < nv && gcn < C) ? A[(int64_t)gcn * N + gj] : 0.0;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < FK; kk += 4) {
-      const double a0 = Ks[kk + lk][wi + li];
-      const double a1 = Ks[kk + lk][wi + 16 + li];
-      const double b0 = Bs[kk + lk][wj + li];
-      const double b1 = Bs[kk + lk][wj + 16 + li];
-      acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
-    }
-  }
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int gi = i0 + wi + bi * 16 + mfma_row(lane, r);
-        const int gcn = c0 + wj + bj * 16 + mfma_col(lane);
-        if (gi < n && gcn < C)
-          fbuf[((int64_t)g * C + gcn) * n + gi] = acc[bi][bj][r] + betav[(int64_t)g * C + gcn];
-      }
+// B = T ahat for every column (T tridiagonal per group).
+__global__ void tri_mult_kernel(int N, int C, int64_t total, const double* __restrict__ Td,
+                                const double* __restrict__ To, const double* __restrict__ x,
+                                double* __restrict__ y) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int64_t col = idx / N;
+  const int i = (int)(idx % N);
+  const int g = (int)(col / C);
+  const double* d = Td + (int64_t)g * N;
+  const double* o = To + (int64_t)g * N;
+  const double* xc = x + col * N;
+  double v = d[i] * xc[i];
+  if (i > 0) v = fma(o[i - 1], xc[i - 1], v);
+  if (i + 1 < N) v = fma(o[i], xc[i + 1], v);
+  y[idx] = v;
 }
 
 // One workgroup per column: objective on the training points, CV sums on the
 // held-out points, scatter of alpha into the output layout.
 __global__ __launch_bounds__(256) void cv_reduce_kernel(
-    int n, int N, int C, int V, int Qt, int L, int s0, int loss, double delta,
-    const double* __restrict__ y, const int32_t* __restrict__ fold, const int32_t* __restrict__ tidx,
-    const int* __restrict__ nvv, const double* __restrict__ lamv, const double* __restrict__ tauv,
-    const double* __restrict__ alpha_loc, const double* __restrict__ fbuf,
+    int n, int N, int Mh, int C, int V, int Qt, int L, int s0, int loss, double delta,
+    const double* __restrict__ y, const int32_t* __restrict__ tidx,
+    const int32_t* __restrict__ hidx, const int* __restrict__ nvv, const double* __restrict__ lamv,
+    const double* __restrict__ tauv, const double* __restrict__ alpha_loc,
+    const double* __restrict__ ftrain, const double* __restrict__ fheld,
     const double* __restrict__ betav, const int* __restrict__ flag,
     const int* __restrict__ iters_total, double* __restrict__ alpha_out,
     double* __restrict__ beta_out, double* __restrict__ obj_out, double* __restrict__ cv_out,
@@ -677,21 +610,24 @@ __global__ __launch_bounds__(256) void cv_reduce_kernel(
   const int nv = nvv[g];
   const double lam = lamv[gc], tau = tauv[gc], b = betav[gc];
   const double* A = alpha_loc + gc * N;
-  const double* f = fbuf + gc * n;
+  const double* ft = ftrain + gc * N;
+  const double* fh = fheld + gc * Mh;
   const int32_t* T = tidx + (int64_t)v * N;
+  const int32_t* H = hidx + (int64_t)v * Mh;
   double* aout = alpha_out + cell * n;
   double ls = 0.0, pen = 0.0;
   for (int j = threadIdx.x; j < nv; j += blockDim.x) {
     const int32_t i = T[j];
-    const double fi = f[i];
-    ls += loss_value(loss, y[i], fi, delta, tau);
-    pen = fma(A[j], fi - b, pen);
+    const double kf = ft[j];                 // (K_v alpha)_j
+    ls += loss_value(loss, y[i], kf + b, delta, tau);
+    pen = fma(A[j], kf, pen);
     aout[i] = A[j];
   }
   double cs = 0.0, ce = 0.0;
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    if (fold[i] != v) continue;
-    const double fi = f[i];
+  for (int k = threadIdx.x; k < Mh; k += blockDim.x) {
+    const int32_t i = H[k];
+    if (i < 0) continue;
+    const double fi = fh[k] + b;
     cs += loss_eval(loss, y[i], fi, tau);
     if (loss != 2 && y[i] * fi <= 0.0) ce += 1.0;
   }
@@ -715,28 +651,47 @@ __global__ __launch_bounds__(256) void cv_reduce_kernel(
 int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
   int rc;
   kc_begin(KMP_KC_FINALIZE, s);
+  const int64_t sNC = (int64_t)p.N * p.C;
   // alpha_loc = Q ahat (into zmat)
   GemmArgs g;
   g.M = p.N; g.N = p.C; g.K = p.N; g.batch = p.G;
   g.A = p.Q; g.lda = p.N; g.sA = (int64_t)p.N * p.N;
-  g.B = p.ahat; g.ldb = p.N; g.sB = (int64_t)p.N * p.C;
-  g.C = p.zmat; g.ldc = p.N; g.sC = (int64_t)p.N * p.C;
+  g.B = p.ahat; g.ldb = p.N; g.sB = sNC;
+  g.C = p.zmat; g.ldc = p.N; g.sC = sNC;
   if ((rc = gemm(s, g, true, true, false)) != 0) return rc;
-  dim3 grid((unsigned)ceil_div(fa.n, FT), (unsigned)ceil_div(p.C, FT), (unsigned)p.G);
-  hipLaunchKernelGGL(predict_kernel, grid, dim3(256), 0, s, fa.n, fa.d, fa.ldx, fa.X, fa.nrm,
-                     fa.tidx, fa.V, p.N, p.C, p.nv, fa.inv2s2, p.zmat, p.beta, fa.fbuf);
+  // training predictions K_v alpha = Q (T ahat)
+  const int64_t tot = (int64_t)p.G * sNC;
+  hipLaunchKernelGGL(tri_mult_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, s, p.N, p.C,
+                     tot, p.Tdiag, p.Toff, p.ahat, p.bmat);
   KMP_LAUNCH_CHECK();
+  GemmArgs gt = g;
+  gt.B = p.bmat;
+  gt.C = fa.ftrain;
+  if ((rc = gemm(s, gt, true, true, false)) != 0) return rc;
+  // held-out kernel blocks K[H_v, T_v] (into the factor buffer, no longer
+  // needed), then held-out predictions K[H_v, T_v] alpha
+  if ((rc = rbf_blocks(s, fa.X, fa.d, fa.ldx, fa.nrm, fa.hidx, fa.Mh, fa.Mh, fa.tidx, p.N, p.N,
+                       fa.V, fa.inv2s2, fa.S_b, fa.kh, (int64_t)fa.V * p.N * p.N,
+                       (int64_t)p.N * p.N, p.N)) != 0)
+    return rc;
+  GemmArgs gh;
+  gh.M = fa.Mh; gh.N = p.C; gh.K = p.N; gh.batch = p.G;
+  gh.A = fa.kh; gh.lda = p.N; gh.sA = (int64_t)p.N * p.N;
+  gh.B = p.zmat; gh.ldb = p.N; gh.sB = sNC;
+  gh.C = fa.fbuf; gh.ldc = fa.Mh; gh.sC = (int64_t)fa.Mh * p.C;
+  if ((rc = gemm(s, gh, true, true, false)) != 0) return rc;
   hipLaunchKernelGGL(cv_reduce_kernel, dim3((unsigned)(p.G * p.C)), dim3(256), 0, s, fa.n, p.N,
-                     p.C, fa.V, fa.Qt, fa.L, fa.s0, p.loss, fa.delta, fa.y, fa.fold, fa.tidx, p.nv,
-                     p.lam, p.tau, p.zmat, fa.fbuf, p.beta, p.flag, p.iters_total, fa.alpha,
-                     fa.beta_out, fa.objective, fa.cv_sum, fa.cv_err, fa.iters, fa.status);
+                     fa.Mh, p.C, fa.V, fa.Qt, fa.L, fa.s0, p.loss, fa.delta, fa.y, fa.tidx, fa.hidx,
+                     p.nv, p.lam, p.tau, p.zmat, fa.ftrain, fa.fbuf, p.beta, p.flag, p.iters_total,
+                     fa.alpha, fa.beta_out, fa.objective, fa.cv_sum, fa.cv_err, fa.iters, fa.status);
   KMP_LAUNCH_CHECK();
-  // alpha = Q ahat, then K(x_i, T) alpha for all n points: kernel entries
-  // recomputed (d + ~20 flops each) and contracted over the C columns
+  // three N x C x N products (alpha, training f, held-out f on Mh rows), the
+  // held-out kernel block (2d flops per entry) and the column reads/writes
   kc_end(KMP_KC_FINALIZE, s,
-         over_groups(p, [&](double n) { return 8.0 * (n * n + 2.0 * n * p.C + (double)fa.n * p.C); }),
          over_groups(p, [&](double n) {
-           return 2.0 * n * n * p.C + (double)fa.n * n * (2.0 * fa.d + 20.0 + 2.0 * p.C); }));
+           return 8.0 * (2.0 * n * n + 5.0 * n * p.C + 2.0 * fa.Mh * n + fa.Mh * p.C); }),
+         over_groups(p, [&](double n) {
+           return 4.0 * n * n * p.C + 2.0 * fa.Mh * n * (p.C + fa.d); }));
   return 0;
 }
 

@@ -300,37 +300,51 @@ __global__ void set_identity_kernel(double* __restrict__ Q, int N, int64_t total
   Q[idx] = (e / N == e % N) ? 1.0 : 0.0;
 }
 
-// Compact-WY factor of kb consecutive reflectors (LAPACK dlarft, forward,
-// columnwise): H_p ... H_{p+kb-1} = I - V T V', T upper triangular,
-// T[i][i] = tau_i, T[0:i, i] = -tau_i T[0:i, 0:i] (V[:, 0:i]' v_i), from the
-// Gram matrix V V' (gram, ld NBQ). Column i of T is formed by kb threads in
-// parallel, columns in sequence.
+// Compact-WY factor of kb consecutive reflectors (LAPACK dlarft, forward):
+// H_p ... H_{p+kb-1} = I - V T V' with T upper triangular. Built by
+// recursive doubling from T[i][i] = tau_i: two adjacent blocks with factors
+// T1, T2 combine into [[T1, -T1 (V1'V2) T2], [0, T2]], where V1'V2 is a block
+// of the Gram matrix of the reflectors (gram, ld NBQ, valid for i, j < kb).
+// Everything stays in LDS; six levels of small products for kb <= 64.
 constexpr int NBQ = 64;
-__global__ __launch_bounds__(NBQ) void form_t_kernel(const double* __restrict__ gram,
+constexpr int FTT = 256;   // threads of form_t_kernel
+__global__ __launch_bounds__(FTT) void form_t_kernel(const double* __restrict__ gram,
                                                      const double* __restrict__ taus,
                                                      double* __restrict__ tmat, int N, int kb,
                                                      int p) {
   __shared__ double T[NBQ][NBQ + 1];
-  __shared__ double gcol[NBQ];
-  const int g = blockIdx.x, r = threadIdx.x;
+  __shared__ double Gs[NBQ][NBQ + 1];
+  __shared__ double Ws[NBQ][NBQ + 1];
+  const int g = blockIdx.x, t = threadIdx.x;
   const double* gr = gram + (int64_t)g * NBQ * NBQ;
-  const double* tg = taus + (int64_t)g * N;
-  for (int c = 0; c < NBQ; ++c) T[r][c] = 0.0;
+  for (int e = t; e < NBQ * NBQ; e += FTT) {
+    const int a = e / NBQ, b = e % NBQ;
+    Gs[a][b] = (a < kb && b < kb) ? gr[e] : 0.0;
+    T[a][b] = (a == b && a < kb && p + a < N) ? taus[(int64_t)g * N + p + a] : 0.0;
+  }
   __syncthreads();
-  for (int i = 0; i < kb; ++i) {
-    const double ti = (p + i < N) ? tg[p + i] : 0.0;
-    if (r < i) gcol[r] = gr[r * NBQ + i];
+  for (int sz = 1; sz < NBQ; sz *= 2) {
+    // pairs of blocks [2qs, 2qs+s) and [2qs+s, 2qs+2s): 32*sz outputs
+    const int outs = (NBQ / 2) * sz;
+    for (int e = t; e < outs; e += FTT) {       // W = G12 T2
+      const int q = e / (sz * sz), rem = e % (sz * sz);
+      const int a = 2 * q * sz + rem / sz, b = 2 * q * sz + sz + rem % sz;
+      double acc = 0.0;
+      for (int c = 2 * q * sz + sz; c <= b; ++c) acc = fma(Gs[a][c], T[c][b], acc);
+      Ws[a][b] = acc;
+    }
     __syncthreads();
-    double sacc = 0.0;
-    if (r < i)
-      for (int c = r; c < i; ++c) sacc = fma(T[r][c], gcol[c], sacc);
-    __syncthreads();
-    if (r < i) T[r][i] = -ti * sacc;
-    if (r == i) T[i][i] = ti;
+    for (int e = t; e < outs; e += FTT) {       // T12 = -T1 W
+      const int q = e / (sz * sz), rem = e % (sz * sz);
+      const int a = 2 * q * sz + rem / sz, b = 2 * q * sz + sz + rem % sz;
+      double acc = 0.0;
+      for (int c = a; c < 2 * q * sz + sz; ++c) acc = fma(T[a][c], Ws[c][b], acc);
+      T[a][b] = -acc;
+    }
     __syncthreads();
   }
   double* Tg = tmat + (int64_t)g * NBQ * NBQ;
-  for (int c = 0; c < NBQ; ++c) Tg[r * NBQ + c] = T[r][c];
+  for (int e = t; e < NBQ * NBQ; e += FTT) Tg[e] = T[e / NBQ][e % NBQ];
 }
 
 int tridiag_parts(int N) { return (N + SRB - 1) / SRB; }
@@ -483,7 +497,7 @@ int tridiagonalize_multi(const hipStream_t* ss, const TridiagWork* ws, int nch) 
       g0.B = wk.A + (int64_t)p * N + p + 1; g0.ldb = N; g0.sB = (int64_t)N * N;
       g0.C = wk.gram; g0.ldc = NBQ; g0.sC = (int64_t)NBQ * NBQ;
       if ((rc = gemm(s, g0, true, true, true)) != 0) return rc;
-      hipLaunchKernelGGL(form_t_kernel, dim3(G), dim3(NBQ), 0, s, wk.gram, wk.tau, wk.tmat, N, kb, p);
+      hipLaunchKernelGGL(form_t_kernel, dim3(G), dim3(FTT), 0, s, wk.gram, wk.tau, wk.tmat, N, kb, p);
       KMP_LAUNCH_CHECK();
       GemmArgs g1;   // X = V[:, p+1:] Q[p+1:, p+1:]   (kb x m)
       g1.M = kb; g1.N = m; g1.K = m; g1.batch = G;
