@@ -181,6 +181,18 @@ int kmp_rbf_gram(void* stream, const double* X, int64_t n, int64_t d, int64_t ld
 int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N,
                 double* Qout, double* diag, double* off);
 
+/* a2 on its own, band form: G symmetric N x N matrices A (DEVICE, row-major,
+ * packed, matrix g at A + g*N*N; destroyed) are reduced to A_g = Q_g B_g Q_g'
+ * with Q_g orthogonal (DEVICE out, same layout) and B_g symmetric banded with
+ * lower bandwidth KMP_BAND: band[g*(KMP_BAND+1)*N + r*N + j] = B_g[j+r][j]
+ * (DEVICE out; entries with j + r >= N are 0). Blocked Householder reduction
+ * (first stage of the successive band reduction, Bischof, Lang & Sun 2000):
+ * panel QR, compact-WY two-sided trailing updates on matrix cores, Q
+ * accumulated in compact-WY blocks. N must be a multiple of 64 in
+ * [64, 8192]; zero padding rows are allowed.                              */
+#define KMP_BAND 16
+int kmp_band_reduce(void* stream, double* A, int32_t G, int32_t N, double* Qout, double* band);
+
 /* Message for a return code, or the last HIP error text for KMP_EHIP. */
 const char* kmp_strerror(int code);
 

@@ -1,0 +1,506 @@
+// Per-fold factorisation K_v = Q B Q' with B symmetric banded (lower
+// bandwidth kBand) and Q orthogonal.
+//
+// The paper factorises the kernel matrix once and reuses the factor for
+// every lambda (Appendix A.3). Here the one-time factorisation stops at a
+// band matrix: the resolvent (2 lambda I + K/(n kappa))^{-1} equals
+// Q (2 lambda I + B/(n kappa))^{-1} Q' exactly, and the banded system is
+// solved per column by a banded LDL' factorisation. Unlike the reduction to
+// tridiagonal form, whose trailing matrix-vector product per column bounds it
+// by memory latency and bandwidth, the reduction to band form is blocked:
+// each panel of kBand columns is factored by a Householder QR (Golub & Van
+// Loan Alg. 5.2.1; compact WY form, Schreiber & Van Loan 1989) and the
+// trailing matrix receives one two-sided update built from matrix-core GEMMs
+// (the first stage of the successive band reduction of Bischof, Lang & Sun,
+// 2000, as in LAPACK's dsytrd_sy2sb).
+//
+// Per panel p (columns p .. p+b-1, trailing block rows/columns m0 = p+b ..):
+//   P = A[m0:, p:p+b] = Q_p R,  Q_p = I - V T V'
+//   X = A22 V T,  W = X - 1/2 V (T' (V' X)),  A22 <- A22 - V W' - W V'.
+// The reflectors of panel p are kept transposed in rows p .. p+b-1 of A
+// (row p+i holds v_i from column m0+i, where v_i has its leading 1), so that
+// Q = H_0 H_1 ... is accumulated afterwards in compact-WY blocks exactly as
+// for the one-reflector-per-row layout, with the leading 1 of row r at
+// column r + b.
+#include "kmp_common.h"
+#include "kmp_kernels.h"
+
+#include <algorithm>
+
+namespace kmp {
+
+constexpr int BB = kBand;        // band width = panel width
+
+constexpr int PQT = 512;         // threads of the panel factorisation
+constexpr int PQW = PQT / 64;
+
+// Sum over the block of h[c] for c in [lo, BB); result in out[c] (LDS).
+__device__ __forceinline__ void block_sum_vec(double (&h)[BB], int lo, double (*red)[BB],
+                                              double* out) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+#pragma unroll
+  for (int c = 0; c < BB; ++c) {
+    if (c >= lo) {                       // uniform
+      const double v = wave_sum(h[c]);
+      if (lane == 0) red[w][c] = v;
+    }
+  }
+  __syncthreads();
+  if (t < BB) {
+    double s = 0.0;
+    for (int q = 0; q < PQW; ++q) s += red[q][t];
+    out[t] = s;
+  }
+  __syncthreads();
+}
+
+// Householder QR of the panel P = A[m0:N, p:p+BB] of every matrix (one
+// workgroup per matrix), in place: R on and above the diagonal of P, v_i
+// below it (dlarfg convention, v_i[i] = 1 implicit). Thread t owns rows
+// r = t + PQT q of P. Step i needs, over rows r > i, the products
+// h_c = sum_r P[r][i] P[r][c] (c >= i): sigma = h_i, and v_i'P[:, c] =
+// P[i][c] + h_c / (alpha - beta). The update of step i and the products of
+// step i+1 are made in one pass over the rows.
+// Outputs: tau[p+i], and v_i transposed into row p+i of A (columns m0 ..,
+// zeros before its leading 1) and into rows i and 2BB+i of the panel buffer.
+__global__ __launch_bounds__(PQT) void panel_qr_kernel(double* __restrict__ A, int N, int p,
+                                                        double* __restrict__ taus,
+                                                        double* __restrict__ panel) {
+  __shared__ double red[PQW][BB];
+  __shared__ double hs[BB];
+  __shared__ double ws[BB];
+  const int g = blockIdx.x, t = threadIdx.x;
+  double* Ag = A + (int64_t)g * N * N;
+  const int m0 = p + BB, mrow = N - m0;
+  double* P = Ag + (int64_t)m0 * N + p;    // P[r][c] = P[r*N + c]
+  double h[BB];
+#pragma unroll
+  for (int c = 0; c < BB; ++c) h[c] = 0.0;
+  for (int r = 1 + t; r < mrow; r += PQT) {
+    const double* row = P + (int64_t)r * N;
+    const double x0 = row[0];
+#pragma unroll
+    for (int c = 0; c < BB; ++c) h[c] = fma(x0, row[c], h[c]);
+  }
+  block_sum_vec(h, 0, red, hs);
+  for (int i = 0; i < BB && i < mrow; ++i) {
+    const double* rowi = P + (int64_t)i * N;
+    const double alpha = rowi[i];
+    const double sigma = hs[i];
+    double tau = 0.0, beta = alpha, scale = 0.0;
+    if (sigma > 0.0) {
+      beta = -copysign(sqrt(alpha * alpha + sigma), alpha);
+      tau = (beta - alpha) / beta;
+      scale = 1.0 / (alpha - beta);
+    }
+    if (t < BB) ws[t] = (t > i) ? fma(scale, hs[t], rowi[t]) : 0.0;   // v_i' P[:, t]
+    if (t == 0) taus[(int64_t)g * N + p + i] = tau;
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < BB; ++c) h[c] = 0.0;
+    for (int r = t; r < mrow; r += PQT) {
+      if (r < i) continue;
+      double* row = P + (int64_t)r * N;
+      double x[BB];
+#pragma unroll
+      for (int c = 0; c < BB; ++c) x[c] = row[c];
+      const double vr = (r == i) ? 1.0 : x[i] * scale;
+#pragma unroll
+      for (int c = 0; c < BB; ++c)
+        if (c > i) x[c] = fma(-tau * vr, ws[c], x[c]);
+#pragma unroll
+      for (int c = 0; c < BB; ++c)
+        if (c == i) x[c] = (r == i) ? beta : vr;
+#pragma unroll
+      for (int c = 0; c < BB; ++c)
+        if (c >= i) row[c] = x[c];
+      if (r > i + 1 && i + 1 < BB) {
+        double x1 = 0.0;
+#pragma unroll
+        for (int c = 0; c < BB; ++c)
+          if (c == i + 1) x1 = x[c];
+#pragma unroll
+        for (int c = 0; c < BB; ++c)
+          if (c > i) h[c] = fma(x1, x[c], h[c]);
+      }
+    }
+    block_sum_vec(h, i + 1 < BB ? i + 1 : BB - 1, red, hs);
+  }
+  // reflectors, transposed: row i of Vt is v_i over rows m0 .. N-1
+  double* Vt = panel + (int64_t)g * 3 * BB * N;
+  for (int e = t; e < BB * mrow; e += PQT) {
+    const int i = e / mrow, r = e % mrow;
+    double v = 0.0;
+    if (r == i) v = 1.0;
+    else if (r > i) v = P[(int64_t)r * N + i];
+    Ag[(int64_t)(p + i) * N + m0 + r] = v;
+    Vt[(int64_t)i * N + m0 + r] = v;
+    Vt[(int64_t)(2 * BB + i) * N + m0 + r] = v;
+  }
+}
+
+// Register-resident variant for panels of at most 32 * RS rows, laid out for
+// the matrix cores: lane l of wave w holds column c = l % 16 of row
+// r = 32 m + 4 w + l / 16 in slot m (m < RS). Every column step needs only
+// the Gram matrix G = sum_{r > i} P[r][:]' P[r][:] of the current panel
+// (16 x 16): with alpha = P[i][i] and sigma = G[i][i],
+//   v_i' P[:, c] = P[i][c] + G[i][c] / (alpha - beta)            (c > i)
+//   V[:, k]' v_i = P[i][k] + G[k][i] / (alpha - beta)            (k < i)
+// the second giving column i of the compact-WY factor T (dlarft):
+// T[0:i, i] = -tau_i T[0:i, 0:i] (V[:, 0:i]' v_i), T[i][i] = tau_i.
+// One v_mfma_f64_16x16x4 per slot accumulates G (A and B operands are the
+// same register: element (c, row) of the slot), then one LDS pass adds the
+// eight waves.
+template <int RS>
+__global__ __launch_bounds__(PQT) void panel_qr_reg_kernel(double* __restrict__ A, int N, int p,
+                                                            double* __restrict__ taus,
+                                                            double* __restrict__ panel,
+                                                            double* __restrict__ tmat) {
+  __shared__ double red[PQW][BB * BB];
+  __shared__ double Gs[BB * BB];
+  __shared__ double rowb[2][BB];         // row i of P before step i (double-buffered)
+  __shared__ double Ts[BB][BB + 1];
+  const int g = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int c = lane & 15, sub = lane >> 4;
+  double* Ag = A + (int64_t)g * N * N;
+  const int m0 = p + BB, mrow = N - m0;
+  double* P = Ag + (int64_t)m0 * N + p;
+  double x[RS];
+#pragma unroll
+  for (int m = 0; m < RS; ++m) {
+    const int r = 32 * m + 4 * w + sub;
+    x[m] = (r < mrow) ? P[(int64_t)r * N + c] : 0.0;
+  }
+  for (int e = t; e < BB * (BB + 1); e += PQT) Ts[e / (BB + 1)][e % (BB + 1)] = 0.0;
+  if (w == 0 && sub == 0) rowb[0][c] = x[0];          // row 0: slot 0, wave 0, sub 0
+  typedef double dbl4 __attribute__((ext_vector_type(4)));
+  const int nstep = mrow < BB ? mrow : BB;
+  for (int i = 0; i < nstep; ++i) {
+    // Gram of the rows below i (two independent accumulation chains)
+    dbl4 acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int m = 0; m < RS; m += 2) {
+      const int r = 32 * m + 4 * w + sub;
+      const double a0 = (r > i && r < mrow) ? x[m] : 0.0;
+      const double a1 = (r + 32 > i && r + 32 < mrow) ? x[m + 1] : 0.0;
+      acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, a0, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, a1, acc1, 0, 0, 0);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) red[w][mfma_row(lane, q) * BB + mfma_col(lane)] = acc0[q] + acc1[q];
+    __syncthreads();
+    if (t < BB * BB) {
+      double sacc = 0.0;
+#pragma unroll
+      for (int ww = 0; ww < PQW; ++ww) sacc += red[ww][t];
+      Gs[t] = sacc;
+    }
+    __syncthreads();
+    const double* ri = rowb[i & 1];
+    const double alpha = ri[i];
+    const double sigma = Gs[i * BB + i];
+    double tau = 0.0, beta = alpha, scale = 0.0;
+    if (sigma > 0.0) {
+      beta = -copysign(sqrt(alpha * alpha + sigma), alpha);
+      tau = (beta - alpha) / beta;
+      scale = 1.0 / (alpha - beta);
+    }
+    // column i of T
+    if (t < i) {
+      double sacc = 0.0;
+      for (int k = t; k < i; ++k) sacc = fma(Ts[t][k], fma(scale, Gs[k * BB + i], ri[k]), sacc);
+      Ts[t][i] = -tau * sacc;
+    }
+    if (t == i) Ts[i][i] = tau;
+    if (t == 0) taus[(int64_t)g * N + p + i] = tau;
+    const double wc = (c > i) ? fma(scale, Gs[i * BB + c], ri[c]) : 0.0;   // v_i' P[:, c]
+#pragma unroll
+    for (int m = 0; m < RS; ++m) {
+      const int r = 32 * m + 4 * w + sub;
+      const double xi = __shfl(x[m], (lane & 48) + i, 64);   // P[r][i]
+      if (r >= i && r < mrow) {
+        const double vr = (r == i) ? 1.0 : xi * scale;
+        if (c > i) x[m] = fma(-tau * vr, wc, x[m]);
+        else if (c == i) x[m] = (r == i) ? beta : vr;
+      }
+      if (r == i + 1) rowb[(i + 1) & 1][c] = x[m];
+    }
+    // the next step's first barrier orders these LDS writes and reads
+  }
+  __syncthreads();
+  // panel back to A (R on and above the diagonal, v_k below), reflectors
+  // transposed into row p+k of A and rows k, 2BB+k of the panel buffer, T
+  double* Vt = panel + (int64_t)g * 3 * BB * N;
+#pragma unroll
+  for (int m = 0; m < RS; ++m) {
+    const int r = 32 * m + 4 * w + sub;
+    if (r < mrow) {
+      P[(int64_t)r * N + c] = x[m];
+      const double v = (r == c) ? 1.0 : ((r > c) ? x[m] : 0.0);
+      Ag[(int64_t)(p + c) * N + m0 + r] = v;
+      Vt[(int64_t)c * N + m0 + r] = v;
+      Vt[(int64_t)(2 * BB + c) * N + m0 + r] = v;
+    }
+  }
+  double* Tg = tmat + (int64_t)g * kWyBlock * kWyBlock;
+  for (int e = t; e < BB * BB; e += PQT) Tg[(e / BB) * kWyBlock + e % BB] = Ts[e / BB][e % BB];
+}
+
+// C[i][j] = sum_k A[i*lda + k] B[j*ldb + k] for M, Nc <= 64 and long K (per
+// matrix b: A + b*sA, B + b*sB, C + b*sC, ld ldc). Every block takes one
+// 16 x 16 output tile over one chunk of TSK indices (one output per thread);
+// a second pass adds the chunks in order.
+constexpr int TSK = 128;
+__global__ __launch_bounds__(256) void ts_gram_partial_kernel(
+    int M, int Nc, int K, const double* __restrict__ A, int64_t lda, int64_t sA,
+    const double* __restrict__ B, int64_t ldb, int64_t sB, double* __restrict__ part) {
+  __shared__ double As[16][TSK + 1];
+  __shared__ double Bs[16][TSK + 1];
+  const int chunk = blockIdx.x, b = blockIdx.z, t = threadIdx.x;
+  const int nch = gridDim.x, ntj = (Nc + 15) / 16;
+  const int ti = blockIdx.y / ntj, tj = blockIdx.y % ntj;
+  const int k0 = chunk * TSK;
+  const int kn = (K - k0 < TSK) ? K - k0 : TSK;
+  A += (int64_t)b * sA;
+  B += (int64_t)b * sB;
+  for (int e = t; e < 16 * TSK; e += 256) {
+    const int rr = e / TSK, kk = e % TSK;
+    const int ia = ti * 16 + rr, jb = tj * 16 + rr;
+    As[rr][kk] = (ia < M && kk < kn) ? A[(int64_t)ia * lda + k0 + kk] : 0.0;
+    Bs[rr][kk] = (jb < Nc && kk < kn) ? B[(int64_t)jb * ldb + k0 + kk] : 0.0;
+  }
+  __syncthreads();
+  const int il = t / 16, jl = t % 16;
+  double s0 = 0.0, s1 = 0.0;
+  for (int kk = 0; kk < TSK; kk += 2) {
+    s0 = fma(As[il][kk], Bs[jl][kk], s0);
+    s1 = fma(As[il][kk + 1], Bs[jl][kk + 1], s1);
+  }
+  const int i = ti * 16 + il, j = tj * 16 + jl;
+  if (i < M && j < Nc) part[(((int64_t)b * nch + chunk) * 64 + i) * 64 + j] = s0 + s1;
+}
+
+__global__ void ts_gram_sum_kernel(int M, int Nc, int nch, const double* __restrict__ part,
+                                   double* __restrict__ C, int64_t ldc, int64_t sC) {
+  const int b = blockIdx.x, t = threadIdx.x;
+  for (int e = t; e < M * Nc; e += blockDim.x) {
+    const int i = e / Nc, j = e % Nc;
+    double s = 0.0;
+    for (int c = 0; c < nch; ++c) s += part[(((int64_t)b * nch + c) * 64 + i) * 64 + j];
+    C[(int64_t)b * sC + (int64_t)i * ldc + j] = s;
+  }
+}
+
+static int ts_gram(hipStream_t s, int M, int Nc, int K, int batch, const double* A, int64_t lda,
+                   int64_t sA, const double* B, int64_t ldb, int64_t sB, double* C, int64_t ldc,
+                   int64_t sC, double* part) {
+  const int nch = (int)ceil_div(K, TSK);
+  const int tiles = (int)(ceil_div(M, 16) * ceil_div(Nc, 16));
+  hipLaunchKernelGGL(ts_gram_partial_kernel, dim3((unsigned)nch, (unsigned)tiles, (unsigned)batch),
+                     dim3(256), 0, s, M, Nc, K, A, lda, sA, B, ldb, sB, part);
+  KMP_LAUNCH_CHECK();
+  hipLaunchKernelGGL(ts_gram_sum_kernel, dim3((unsigned)batch), dim3(256), 0, s, M, Nc, nch, part,
+                     C, ldc, sC);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
+// band[g][r*N + j] = B[j+r][j] (r <= BB) from the lower triangle of A.
+__global__ void band_extract_kernel(const double* __restrict__ A, int N, int64_t total,
+                                    double* __restrict__ band) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int64_t per = (int64_t)(BB + 1) * N;
+  const int g = (int)(idx / per);
+  const int64_t e = idx % per;
+  const int r = (int)(e / N), j = (int)(e % N);
+  band[idx] = (j + r < N) ? A[(int64_t)g * N * N + (int64_t)(j + r) * N + j] : 0.0;
+}
+
+// Clear row r of A (a reflector row, r < N - BB) to the left of its stored
+// vector, from column max(0, r - 64) up to column r + BB - 1, so that any
+// compact-WY block of up to 64 consecutive reflector rows reads zeros there.
+__global__ void clear_reflector_rows_kernel(double* __restrict__ A, int N, int64_t total) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int64_t rows = N - BB;
+  const int g = (int)(idx / (rows * (64 + BB)));
+  const int64_t e = idx % (rows * (64 + BB));
+  const int r = (int)(e / (64 + BB)), q = (int)(e % (64 + BB));
+  const int c = r - 64 + q;              // c in [r - 64, r + BB)
+  if (c < 0) return;
+  A[(int64_t)g * N * N + (int64_t)r * N + c] = 0.0;
+}
+
+__global__ void set_identity_band_kernel(double* __restrict__ Q, int N, int64_t total) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int64_t e = idx % ((int64_t)N * N);
+  Q[idx] = (e / N == e % N) ? 1.0 : 0.0;
+}
+
+template <typename F>
+static double over_groups(const BandWork& wk, F f) {
+  double a = 0.0;
+  for (int g = 0; g < wk.G; ++g) a += f((double)(wk.nv_host ? wk.nv_host[g] : wk.N));
+  return a;
+}
+
+size_t band_part_doubles(int G, int N) {
+  return (size_t)G * ceil_div(N, TSK) * 64 * 64;
+}
+
+size_t band_work_doubles(int G, int N) {
+  return (size_t)G * (3 * (size_t)BB * N + 2 * (size_t)kWyBlock * kWyBlock +
+                      2 * (size_t)kWyBlock * N) + band_part_doubles(G, N);
+}
+
+int band_reduce(hipStream_t s, const BandWork& wk) {
+  const int G = wk.G, N = wk.N;
+  if (G <= 0) return 0;
+  if (N % 64 != 0 || N < 64 || N > 8192) {
+    set_error("band_reduce: N must be a multiple of 64 in [64, 8192]");
+    return KMP_EINVAL;
+  }
+  int rc;
+  const int64_t sP = (int64_t)3 * BB * N;
+  KMP_HIP_TRY(hipMemsetAsync(wk.tau, 0, sizeof(double) * (size_t)G * N, s));
+  for (int p = 0; p + BB < N; p += BB) {
+    const int m0 = p + BB, mrow = N - m0;
+    kc_begin(KMP_KC_TRI_COL, s);
+    const int rs = (int)ceil_div(mrow, 32);
+    const bool reg = rs <= 64;
+#define KMP_PQR(RSV)                                                                            \
+  hipLaunchKernelGGL(panel_qr_reg_kernel<RSV>, dim3(G), dim3(PQT), 0, s, wk.A, N, p, wk.tau, \
+                     wk.panel, wk.tmat)
+    if (rs <= 8) KMP_PQR(8);
+    else if (rs <= 16) KMP_PQR(16);
+    else if (rs <= 32) KMP_PQR(32);
+    else if (rs <= 48) KMP_PQR(48);
+    else if (rs <= 64) KMP_PQR(64);
+#undef KMP_PQR
+    else
+      hipLaunchKernelGGL(panel_qr_kernel, dim3(G), dim3(PQT), 0, s, wk.A, N, p, wk.tau, wk.panel);
+    KMP_LAUNCH_CHECK();
+    // panel read twice per column step and written once (algorithmic: once)
+    kc_end(KMP_KC_TRI_COL, s, over_groups(wk, [&](double n) {
+             return 16.0 * std::max(0.0, n - m0) * BB; }),
+           over_groups(wk, [&](double n) { return 4.0 * std::max(0.0, n - m0) * BB * BB; }));
+    kc_begin(KMP_KC_TRI_SYMV, s);
+    // T of the panel's block reflector (formed by the register kernel):
+    // otherwise the Gram of V, then dlarft
+    if (!reg) {
+      if ((rc = ts_gram(s, BB, BB, mrow, G, wk.panel + m0, N, sP, wk.panel + m0, N, sP, wk.gram,
+                        kWyBlock, (int64_t)kWyBlock * kWyBlock, wk.part)) != 0)
+        return rc;
+      if ((rc = wy_form_t(s, wk.gram, wk.tau, wk.tmat, G, N, BB, p)) != 0) return rc;
+    }
+    // Y' = T' V'   (BB x mrow, in xbuf)
+    GemmArgs g1;
+    g1.M = BB; g1.N = mrow; g1.K = BB; g1.batch = G;
+    g1.A = wk.tmat; g1.lda = kWyBlock; g1.sA = (int64_t)kWyBlock * kWyBlock;
+    g1.B = wk.panel + m0; g1.ldb = N; g1.sB = sP;
+    g1.C = wk.xbuf + m0; g1.ldc = N; g1.sC = (int64_t)kWyBlock * N;
+    if ((rc = gemm(s, g1, false, false, true)) != 0) return rc;
+    // X' = Y' A22   (BB x mrow, rows BB .. 2BB-1 of the panel buffer)
+    GemmArgs g2;
+    g2.M = BB; g2.N = mrow; g2.K = mrow; g2.batch = G;
+    g2.A = wk.xbuf + m0; g2.lda = N; g2.sA = (int64_t)kWyBlock * N;
+    g2.B = wk.A + (int64_t)m0 * N + m0; g2.ldb = N; g2.sB = (int64_t)N * N;
+    g2.C = wk.panel + (int64_t)BB * N + m0; g2.ldc = N; g2.sC = sP;
+    if ((rc = gemm(s, g2, true, false, true)) != 0) return rc;
+    // M2 = V' X  (BB x BB, in gram)
+    if ((rc = ts_gram(s, BB, BB, mrow, G, wk.panel + m0, N, sP, wk.panel + (int64_t)BB * N + m0, N,
+                      sP, wk.gram, kWyBlock, (int64_t)kWyBlock * kWyBlock, wk.part)) != 0)
+      return rc;
+    // S = T' M2  (BB x BB, in ybuf)
+    GemmArgs g4;
+    g4.M = BB; g4.N = BB; g4.K = BB; g4.batch = G;
+    g4.A = wk.tmat; g4.lda = kWyBlock; g4.sA = (int64_t)kWyBlock * kWyBlock;
+    g4.B = wk.gram; g4.ldb = kWyBlock; g4.sB = (int64_t)kWyBlock * kWyBlock;
+    g4.C = wk.ybuf; g4.ldc = kWyBlock; g4.sC = (int64_t)kWyBlock * N;
+    if ((rc = gemm(s, g4, false, false, true)) != 0) return rc;
+    // W' = X' - 1/2 S' V'
+    GemmArgs g5;
+    g5.M = BB; g5.N = mrow; g5.K = BB; g5.batch = G;
+    g5.A = wk.ybuf; g5.lda = kWyBlock; g5.sA = (int64_t)kWyBlock * N;
+    g5.B = wk.panel + m0; g5.ldb = N; g5.sB = sP;
+    g5.C = wk.panel + (int64_t)BB * N + m0; g5.ldc = N; g5.sC = sP;
+    g5.alpha = -0.5; g5.beta = 1.0;
+    if ((rc = gemm(s, g5, false, false, true)) != 0) return rc;
+    kc_end(KMP_KC_TRI_SYMV, s, over_groups(wk, [&](double n) {
+             const double m = std::max(0.0, n - m0); return 8.0 * m * m; }),
+           over_groups(wk, [&](double n) {
+             const double m = std::max(0.0, n - m0); return 2.0 * BB * m * m; }));
+    // A22 -= V W' + W V'  as one GEMM with K = 2 BB over the [V; W; V] rows
+    GemmArgs ga;
+    ga.M = mrow; ga.N = mrow; ga.K = 2 * BB; ga.batch = G;
+    ga.A = wk.panel + m0; ga.lda = N; ga.sA = sP;
+    ga.B = wk.panel + (int64_t)BB * N + m0; ga.ldb = N; ga.sB = sP;
+    ga.C = wk.A + (int64_t)m0 * N + m0; ga.ldc = N; ga.sC = (int64_t)N * N;
+    ga.alpha = -1.0; ga.beta = 1.0;
+    kc_begin(KMP_KC_TRI_SYR2K, s);
+    if ((rc = gemm(s, ga, false, false, true)) != 0) return rc;
+    kc_end(KMP_KC_TRI_SYR2K, s, over_groups(wk, [&](double n) {
+             const double m = std::max(0.0, n - m0); return 16.0 * m * m; }),
+           over_groups(wk, [&](double n) {
+             const double m = std::max(0.0, n - m0); return 4.0 * BB * m * m; }));
+  }
+  // the band, then clean reflector rows for the accumulation of Q
+  {
+    const int64_t tot = (int64_t)G * (BB + 1) * N;
+    hipLaunchKernelGGL(band_extract_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, s,
+                       wk.A, N, tot, wk.band);
+    KMP_LAUNCH_CHECK();
+    const int64_t tz = (int64_t)G * (N - BB) * (64 + BB);
+    hipLaunchKernelGGL(clear_reflector_rows_kernel, dim3((unsigned)ceil_div(tz, 256)), dim3(256), 0,
+                       s, wk.A, N, tz);
+    KMP_LAUNCH_CHECK();
+    const int64_t tq = (int64_t)G * N * N;
+    hipLaunchKernelGGL(set_identity_band_kernel, dim3((unsigned)ceil_div(tq, 256)), dim3(256), 0, s,
+                       wk.Q, N, tq);
+    KMP_LAUNCH_CHECK();
+  }
+  // Q = H_0 H_1 ... (reflector rows 0 .. N-BB-1), accumulated backwards in
+  // blocks of kWyBlock rows: Q[q+BB:, q+BB:] -= V' (T (V Q[q+BB:, q+BB:])).
+  const int nref = N - BB;
+  const int last = ((nref - 1) / kWyBlock) * kWyBlock;
+  for (int q = last; q >= 0; q -= kWyBlock) {
+    const int kb = std::min(kWyBlock, nref - q);
+    const int m = N - q - BB;
+    kc_begin(KMP_KC_QFORM, s);
+    // Gram of the block's reflectors
+    const double* Vq = wk.A + (int64_t)q * N + q + BB;
+    if ((rc = ts_gram(s, kb, kb, m, G, Vq, N, (int64_t)N * N, Vq, N, (int64_t)N * N, wk.gram,
+                      kWyBlock, (int64_t)kWyBlock * kWyBlock, wk.part)) != 0)
+      return rc;
+    if ((rc = wy_form_t(s, wk.gram, wk.tau, wk.tmat, G, N, kb, q)) != 0) return rc;
+    GemmArgs h1;   // X = V Q[q+BB:, q+BB:]   (kb x m)
+    h1.M = kb; h1.N = m; h1.K = m; h1.batch = G;
+    h1.A = wk.A + (int64_t)q * N + q + BB; h1.lda = N; h1.sA = (int64_t)N * N;
+    h1.B = wk.Q + (int64_t)(q + BB) * N + q + BB; h1.ldb = N; h1.sB = (int64_t)N * N;
+    h1.C = wk.xbuf; h1.ldc = N; h1.sC = (int64_t)kWyBlock * N;
+    if ((rc = gemm(s, h1, true, false, true)) != 0) return rc;
+    GemmArgs h2;   // Y = T X
+    h2.M = kb; h2.N = m; h2.K = kb; h2.batch = G;
+    h2.A = wk.tmat; h2.lda = kWyBlock; h2.sA = (int64_t)kWyBlock * kWyBlock;
+    h2.B = wk.xbuf; h2.ldb = N; h2.sB = (int64_t)kWyBlock * N;
+    h2.C = wk.ybuf; h2.ldc = N; h2.sC = (int64_t)kWyBlock * N;
+    if ((rc = gemm(s, h2, true, false, true)) != 0) return rc;
+    GemmArgs h3;   // Q[q+BB:, q+BB:] -= V' Y
+    h3.M = m; h3.N = m; h3.K = kb; h3.batch = G;
+    h3.A = wk.A + (int64_t)q * N + q + BB; h3.lda = N; h3.sA = (int64_t)N * N;
+    h3.B = wk.ybuf; h3.ldb = N; h3.sB = (int64_t)kWyBlock * N;
+    h3.C = wk.Q + (int64_t)(q + BB) * N + q + BB; h3.ldc = N; h3.sC = (int64_t)N * N;
+    h3.alpha = -1.0; h3.beta = 1.0;
+    if ((rc = gemm(s, h3, false, false, true)) != 0) return rc;
+    kc_end(KMP_KC_QFORM, s, over_groups(wk, [&](double n) {
+             const double mm = std::max(0.0, n - q - BB); return 24.0 * mm * mm; }),
+           over_groups(wk, [&](double n) {
+             const double mm = std::max(0.0, n - q - BB);
+             return 4.0 * kb * mm * mm + 2.0 * kb * kb * mm; }));
+  }
+  return 0;
+}
+
+}  // namespace kmp

@@ -76,7 +76,6 @@ void kc_end(int cls, hipStream_t s, double bytes, double flops) {
 namespace {
 
 constexpr int kPanel = 32;       // Householder panel width
-constexpr int kWyBlock = 64;     // reflectors per compact-WY block when forming Q
 constexpr int kRowAlign = 64;    // padding of the per-fold matrix order
 constexpr size_t kAlign = 256;
 
@@ -360,6 +359,32 @@ int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N, double* Qout, dou
   w.spart = q; q += (size_t)G * tridiag_parts(N);
   w.pnext = q;
   int rc = tridiagonalize(s, w);
+  KMP_HIP_TRY(hipFreeAsync(scratch, s));
+  KMP_HIP_TRY(hipStreamSynchronize(s));
+  return rc;
+}
+
+int kmp_band_reduce(void* stream, double* A, int32_t G, int32_t N, double* Qout, double* band) {
+  hipStream_t s = (hipStream_t)stream;
+  static_assert(KMP_BAND == kBand, "band width of the header and the kernels differ");
+  if (!A || !Qout || !band || G < 1 || N < 64 || N > 8192 || N % 64 != 0) {
+    set_error("kmp_band_reduce: invalid arguments (N must be a multiple of 64 in [64, 8192])");
+    return KMP_EINVAL;
+  }
+  BandWork w;
+  w.G = G; w.N = N; w.A = A; w.Q = Qout; w.band = band;
+  double* scratch = nullptr;
+  const size_t extra = band_work_doubles(G, N) + (size_t)G * N;
+  KMP_HIP_TRY(hipMallocAsync((void**)&scratch, sizeof(double) * extra, s));
+  double* q = scratch;
+  w.tau = q; q += (size_t)G * N;
+  w.panel = q; q += (size_t)G * 3 * kBand * N;
+  w.tmat = q; q += (size_t)G * kWyBlock * kWyBlock;
+  w.gram = q; q += (size_t)G * kWyBlock * kWyBlock;
+  w.xbuf = q; q += (size_t)G * kWyBlock * N;
+  w.ybuf = q; q += (size_t)G * kWyBlock * N;
+  w.part = q;
+  int rc = band_reduce(s, w);
   KMP_HIP_TRY(hipFreeAsync(scratch, s));
   KMP_HIP_TRY(hipStreamSynchronize(s));
   return rc;

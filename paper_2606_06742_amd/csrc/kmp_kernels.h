@@ -62,6 +62,36 @@ int rbf_blocks(hipStream_t s, const double* X, int64_t d, int64_t ldx, const dou
                const double* inv2s2, int S, double* out, int64_t sout_s, int64_t sout_q,
                int64_t ld);
 
+// ------------------------------------------------------------ band form
+constexpr int kBand = 16;      // lower bandwidth of B (= panel width of the reduction)
+constexpr int kWyBlock = 64;   // reflectors per compact-WY block when forming Q
+
+// Reduction of G symmetric N x N matrices (row-major, packed, destroyed) to
+// A_g = Q_g B_g Q_g' with B_g banded; band[g][r*N + j] = B_g[j+r][j], r <= kBand.
+struct BandWork {
+  int G = 0, N = 0;
+  double* A = nullptr;      // G x N x N
+  double* Q = nullptr;      // G x N x N, output
+  double* band = nullptr;   // G x (kBand+1) x N, output
+  double* tau = nullptr;    // G x N
+  double* panel = nullptr;  // G x 3 kBand x N ([V; W; V] rows of the current panel)
+  double* tmat = nullptr;   // G x 64 x 64
+  double* gram = nullptr;   // G x 64 x 64
+  double* xbuf = nullptr;   // G x 64 x N
+  double* ybuf = nullptr;   // G x 64 x N
+  double* part = nullptr;   // band_part_doubles(G, N): chunk partials of the Gram products
+  const int* nv_host = nullptr;  // G valid orders (host), for the work counters; N if null
+};
+// Doubles of scratch band_reduce needs beyond A, Q, band and tau (the chunk
+// partials included), and of the chunk partials alone.
+size_t band_work_doubles(int G, int N);
+size_t band_part_doubles(int G, int N);
+int band_reduce(hipStream_t s, const BandWork& w);
+// Compact-WY T factor (kb x kb, ld 64, per matrix) of reflectors p .. p+kb-1
+// from their Gram matrix (ld 64) and tau[g*N + p + i].
+int wy_form_t(hipStream_t s, const double* gram, const double* taus, double* tmat, int G, int N,
+              int kb, int p);
+
 // --------------------------------------------------------- tridiagonal
 struct TridiagWork {
   int G = 0, N = 0, nb = 32;

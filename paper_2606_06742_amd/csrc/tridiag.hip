@@ -347,6 +347,13 @@ __global__ __launch_bounds__(FTT) void form_t_kernel(const double* __restrict__ 
   for (int e = t; e < NBQ * NBQ; e += FTT) Tg[e] = T[e / NBQ][e % NBQ];
 }
 
+int wy_form_t(hipStream_t s, const double* gram, const double* taus, double* tmat, int G, int N,
+              int kb, int p) {
+  hipLaunchKernelGGL(form_t_kernel, dim3(G), dim3(FTT), 0, s, gram, taus, tmat, N, kb, p);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
 int tridiag_parts(int N) { return (N + SRB - 1) / SRB; }
 
 size_t tridiag_panel_doubles(int G, int N, int nb) {

@@ -89,6 +89,8 @@ def lib():
         L.kmp_rbf_gram.restype = C.c_int
         L.kmp_tridiag.argtypes = [_VP, _VP, C.c_int32, C.c_int32, _VP, _VP, _VP]
         L.kmp_tridiag.restype = C.c_int
+        L.kmp_band_reduce.argtypes = [_VP, _VP, C.c_int32, C.c_int32, _VP, _VP]
+        L.kmp_band_reduce.restype = C.c_int
         L.kmp_strerror.argtypes = [C.c_int]
         L.kmp_strerror.restype = C.c_char_p
         L.kmp_version.argtypes = []
@@ -100,7 +102,9 @@ def lib():
 
 
 EXPORTED = ("kmp_default_spec", "kmp_workspace_bytes", "kmp_fit_path", "kmp_make_folds",
-            "kmp_rbf_gram", "kmp_tridiag", "kmp_strerror", "kmp_version", "kmp_kernel_class_name")
+            "kmp_rbf_gram", "kmp_tridiag", "kmp_band_reduce", "kmp_strerror", "kmp_version",
+            "kmp_kernel_class_name")
+KMP_BAND = 16
 
 
 def kmp_kernel_class_name(cls: int) -> str:
@@ -173,6 +177,14 @@ def kmp_tridiag(A, Q, diag, off, stream=None) -> None:
     G, N = A.shape[0], A.shape[1]
     _check(lib().kmp_tridiag(_stream_ptr(stream), A.data_ptr(), G, N, Q.data_ptr(),
                              diag.data_ptr(), off.data_ptr()))
+
+
+def kmp_band_reduce(A, Q, band, stream=None) -> None:
+    """a2 on its own, band form: A (G, N, N) device tensor, destroyed; Q
+    (G, N, N) and band (G, KMP_BAND+1, N) outputs, band[g, r, j] = B[j+r, j]."""
+    G, N = A.shape[0], A.shape[1]
+    _check(lib().kmp_band_reduce(_stream_ptr(stream), A.data_ptr(), G, N, Q.data_ptr(),
+                                 band.data_ptr()))
 
 
 def kmp_fit_path(stream, spec, X, y, sigmas, taus, lambdas, fold_id, V, workspace, ws_bytes,
