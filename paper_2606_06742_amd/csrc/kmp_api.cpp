@@ -105,7 +105,7 @@ struct Carver {
 // size and to carve, so the two can never disagree.
 struct Layout {
   double *A, *Qm, *diag, *off, *tau, *cvec, *ylab, *panel, *dots, *tmat, *gram, *xbuf, *ybuf;
-  double *spart, *pnext;
+  double *spart, *pnext, *band, *bpart;
   double *ahat, *abar, *bmat, *zmat, *zhat, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
   double *beta, *bbar, *rmom, *gcoef, *kkt, *lam, *taucol, *fbuf, *nrm, *inv2s2;
   int *flag, *iters, *iters_total, *active, *nvg;
@@ -131,12 +131,14 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.ybuf = c.take<double>(G * kWyBlock * N);
   l.spart = c.take<double>(G * (size_t)tridiag_parts((int)N));
   l.pnext = c.take<double>(G * N);
+  l.band = c.take<double>(G * (kBand + 1) * N);
+  l.bpart = c.take<double>(band_part_doubles((int)G, (int)N));
   l.ahat = c.take<double>(cols * N);
   l.abar = c.take<double>(cols * N);
   l.bmat = c.take<double>(cols * N);
   l.zmat = c.take<double>(cols * N);
   l.zhat = c.take<double>(cols * N);
-  l.ldl_l = c.take<double>(cols * N);
+  l.ldl_l = c.take<double>(cols * kBand * N);
   l.ldl_d = c.take<double>(cols * N);
   l.vhat = c.take<double>(cols * N);
   l.uvec = c.take<double>(cols * N);
@@ -537,7 +539,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
 
   PathArrays pa;
   pa.N = N; pa.C = C; pa.loss = spec->loss;
-  pa.nv = lay.nvg; pa.ylab = lay.ylab; pa.Q = lay.Qm; pa.Tdiag = lay.diag; pa.Toff = lay.off;
+  pa.nv = lay.nvg; pa.ylab = lay.ylab; pa.Q = lay.Qm; pa.band = lay.band;
   pa.cvec = lay.cvec; pa.lam = lay.lam; pa.tau = lay.taucol;
   pa.ahat = lay.ahat; pa.abar = lay.abar; pa.bmat = lay.bmat; pa.zmat = lay.zmat;
   pa.zhat = lay.zhat; pa.ldl_l = lay.ldl_l; pa.ldl_d = lay.ldl_d; pa.vhat = lay.vhat;
@@ -585,13 +587,11 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     }
     KMP_HIP_TRY(hipEventRecord(tm.ev[2], s));
     // a2: factorisation
-    TridiagWork tw;
-    tw.G = Gb; tw.N = N; tw.nb = kPanel; tw.A = lay.A; tw.Q = lay.Qm; tw.diag = lay.diag;
-    tw.off = lay.off; tw.tau = lay.tau; tw.panel = lay.panel; tw.dots = lay.dots;
-    tw.tmat = lay.tmat; tw.gram = lay.gram; tw.xbuf = lay.xbuf; tw.ybuf = lay.ybuf;
-    tw.spart = lay.spart; tw.pnext = lay.pnext;
-    tw.nv_host = nvg.data();
-    if ((rc = tridiagonalize(s, tw)) != 0) return rc;
+    BandWork bw;
+    bw.G = Gb; bw.N = N; bw.A = lay.A; bw.Q = lay.Qm; bw.band = lay.band; bw.tau = lay.tau;
+    bw.panel = lay.panel; bw.tmat = lay.tmat; bw.gram = lay.gram; bw.xbuf = lay.xbuf;
+    bw.ybuf = lay.ybuf; bw.part = lay.bpart; bw.nv_host = nvg.data();
+    if ((rc = band_reduce(s, bw)) != 0) return rc;
     if ((rc = group_ones_projection(s, lay.Qm, lay.nvg, Gb, N, lay.cvec)) != 0) return rc;
     if ((rc = gather_labels(s, y, lay.tidx, V, sb, N, lay.ylab)) != 0) return rc;
     if ((rc = path_init_columns(s, pa)) != 0) return rc;

@@ -127,8 +127,7 @@ struct PathArrays {
   const int* nv = nullptr;       // G valid rows
   const double* ylab = nullptr;  // G x N labels (0 at padding)
   const double* Q = nullptr;     // G x N x N
-  const double* Tdiag = nullptr; // G x N
-  const double* Toff = nullptr;  // G x N
+  const double* band = nullptr;  // G x (kBand+1) x N, band[g][r*N + j] = B[j+r][j]
   const double* cvec = nullptr;  // G x N, Q' 1 over valid rows
   const double* lam = nullptr;   // G*C
   const double* tau = nullptr;   // G*C
@@ -138,8 +137,8 @@ struct PathArrays {
   double* bmat = nullptr;   // T abar, operand of the first GEMM
   double* zmat = nullptr;
   double* zhat = nullptr;
-  double* ldl_l = nullptr;
-  double* ldl_d = nullptr;
+  double* ldl_l = nullptr;  // kBand x N per column: tiles of the banded LDL' factor
+  double* ldl_d = nullptr;  // N per column: 1/D
   double* vhat = nullptr;
   double* uvec = nullptr;   // T vhat
   double* partial = nullptr;// G x tiles x C

@@ -1,20 +1,20 @@
-// Batched regularisation-path solver in the tridiagonal basis K_v = Q T Q'.
+// Batched regularisation-path solver in the band basis K_v = Q B Q'.
 //
 // Every column is one (tau, lambda) problem of one group (bandwidth, fold).
 // With hats denoting Q' coordinates (a = Q'alpha), one iteration of the
 // accelerated majorise-minimise method (Appendix A.1 update; Algorithm 1
 // inner loop; Appendix A.3 block inverse of H) is
 //
-//   f      = Q (T abar) + bbar                      (first path GEMM)
+//   f      = Q (B abar) + bbar                      (first path GEMM)
 //   z      = psi(y, f) / n_v,  d0 = 1'z             (its epilogue)
 //   zhat   = Q' z                                   (second path GEMM)
 //   w      = zhat + 2 lambda abar                   (= Q'(z + 2 lambda alpha))
-//   t      = vhat' T w                              (= v' K (z + 2 lambda alpha))
-//   x      = (2 lambda I + T/(n_v kappa))^{-1} w    (tridiagonal solve)
+//   t      = vhat' B w                              (= v' K (z + 2 lambda alpha))
+//   x      = (2 lambda I + B/(n_v kappa))^{-1} w    (banded solve)
 //   Da     = g (t - d0) vhat + x,   Db = g (d0 - t)
 //   a_new  = abar - Da,             b_new = bbar - Db
 //
-// with vhat = (2 lambda I + T/(n_v kappa))^{-1} Q'1 / (n_v kappa) and
+// with vhat = (2 lambda I + B/(n_v kappa))^{-1} Q'1 / (n_v kappa) and
 // g = 1/(2 lambda (Q'1)' vhat) precomputed once per smoothing stage. These
 // are the paper's v and g taken as the exact Schur complement of the
 // (n+1)-square majoriser H = [[1/kappa, 1'K/(n kappa)], [K1/(n kappa),
@@ -104,234 +104,338 @@ static double over_groups(const PathArrays& p, F f) {
   return a;
 }
 
-// ---------------------------------------------------------- scan helpers
-// Affine map x -> a x + b; compose(second, first) = second o first.
-struct Aff {
-  double a, b;
-};
-__device__ __forceinline__ Aff compose(Aff second, Aff first) {
-  return Aff{second.a * first.a, fma(second.a, first.b, second.b)};
+// ------------------------------------------------------------ band solver
+// One wavefront per column. The column's working vector lives in LDS (xs,
+// N doubles); elementwise work spreads rows over the lanes as i = lane + 64 k.
+//
+// Per column and smoothing stage, M = 2 lambda I + B/(n_v kappa) (B banded,
+// lower bandwidth BND) is factored blockwise in BND x BND blocks,
+//   M = L D L',  L unit lower block-bidiagonal with diagonal blocks L_I and
+//   subdiagonal blocks C_I = L_{I,I-1} (upper triangular: the band),
+//   S_I = M_II - C_I D_{I-1} C_I',  S_I = L_I D_I L_I',
+//   C_{I+1} = M_{I+1,I} L_I^{-T} D_I^{-1},
+// and stored per block as one BND x BND tile V_I with V_I[a][j] =
+// (L_I^{-1})[a][j] for j < a and C_I[a][j] for j >= a (the two triangles
+// are complementary), element (a, j) of block I at V[j*N + BND*I + a]. With
+// it both triangular solves are two small products per block:
+//   forward   r = w_I - C_I y_{I-1},   y_I = L_I^{-1} r
+//   backward  s = z_I - C_{I+1}' x_{I+1},   x_I = L_I^{-T} s.
+constexpr int BND = kBand;
+
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Exclusive prefix composition across the block in thread order (thread t
-// receives map_{t-1} o ... o map_0, identity for t = 0). `sh` holds PW Affs.
-__device__ __forceinline__ Aff block_exclusive_scan(Aff m, Aff* sh) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  Aff inc = m;
+// (B x)[i] with x in LDS; bg[r*N + j] = B[j+r][j], zero for j + r >= N.
+// All loads are unconditional (clamped addresses, masked products) so that
+// they are issued together.
+__device__ __forceinline__ double band_row(const double* __restrict__ bg, const double* xs, int N,
+                                           int i) {
+  double y = bg[i] * xs[i];
 #pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const double pa = __shfl_up(inc.a, off, 64);
-    const double pb = __shfl_up(inc.b, off, 64);
-    if (lane >= off) inc = compose(inc, Aff{pa, pb});
+  for (int r = 1; r <= BND; ++r) {
+    const int il = (i - r >= 0) ? i - r : 0;
+    const int iu = (i + r < N) ? i + r : N - 1;
+    const double bl = bg[(int64_t)r * N + il];
+    const double bu = bg[(int64_t)r * N + i];          // zero when i + r >= N
+    y = fma((i - r >= 0) ? bl : 0.0, xs[il], y);
+    y = fma(bu, xs[iu], y);
   }
-  // exclusive within the wave
-  double ea = __shfl_up(inc.a, 1, 64), eb = __shfl_up(inc.b, 1, 64);
-  Aff ex = lane == 0 ? Aff{1.0, 0.0} : Aff{ea, eb};
-  __syncthreads();
-  if (lane == 63) sh[w] = inc;
-  __syncthreads();
-  Aff pre{1.0, 0.0};
-  for (int k = 0; k < w; ++k) pre = compose(sh[k], pre);
-  return compose(ex, pre);
+  return y;
 }
 
-// Same in reverse thread order (thread t receives map_{t+1} o ... o map_last).
-__device__ __forceinline__ Aff block_exclusive_scan_rev(Aff m, Aff* sh) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  Aff inc = m;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const double pa = __shfl_down(inc.a, off, 64);
-    const double pb = __shfl_down(inc.b, off, 64);
-    if (lane + off < 64) inc = compose(inc, Aff{pa, pb});
-  }
-  double ea = __shfl_down(inc.a, 1, 64), eb = __shfl_down(inc.b, 1, 64);
-  Aff ex = lane == 63 ? Aff{1.0, 0.0} : Aff{ea, eb};
-  __syncthreads();
-  if (lane == 0) sh[w] = inc;
-  __syncthreads();
-  Aff pre{1.0, 0.0};
-  for (int k = PW - 1; k > w; --k) pre = compose(sh[k], pre);
-  return compose(ex, pre);
-}
+// xs <- M^{-1} xs from the stored factor (Vc: BND x N tiles, Dc: 1/D).
+// The tiles pass through LDS (vs, VSTAGE doubles) in chunks of SCH blocks:
+// all 64 lanes load the next chunk into registers while the current one is
+// used, so the block recurrence does not wait on device memory. Chunk
+// element (j, 16 q + a) of blocks I0 .. I0+SCH-1 sits at vs[j * VLD + 16 q + a].
+constexpr int SCH = 4;
+constexpr int VLD = BND * SCH + 1;                  // padded row: conflict-free transposed reads
+constexpr int VSTAGE = BND * VLD;
+constexpr int VPL = BND * BND * SCH / 64;           // chunk doubles per lane
 
-// Solve (L D L') x = w on the rows [i0, i0 + E) owned by this thread, L unit
-// lower bidiagonal (l[i] = L[i+1][i]), dv = 1/D. lv holds l on the own rows,
-// lprev = l[i0 - 1] (0 for the first thread). wv holds w on entry and x on
-// exit. Both triangular solves are first-order affine recurrences, done as
-// block-wide scans of affine maps.
-template <int E>
-__device__ __forceinline__ void ldl_solve(double (&wv)[E], const double (&lv)[E], double lprev,
-                                          const double (&dv)[E], Aff* sh) {
-  // forward: y_i = w_i - l_{i-1} y_{i-1}
-  Aff m{1.0, 0.0};
-  {
-    double ca = 1.0, cb = 0.0, lp = lprev;
+__device__ __forceinline__ void vchunk_load(const double* __restrict__ Vc, int N, int I0,
+                                            int lane, double (&buf)[VPL]) {
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      ca = -lp * ca;
-      cb = fma(-lp, cb, wv[e]);
-      lp = lv[e];
-    }
-    m = Aff{ca, cb};
+  for (int q = 0; q < VPL; ++q) {
+    const int e = lane + 64 * q;
+    const int j = e / (BND * SCH), rem = e % (BND * SCH);
+    // rows past the last block are never read: clamp the address, no mask
+    const int col = (BND * I0 + rem < N) ? BND * I0 + rem : N - 1;
+    buf[q] = Vc[(int64_t)j * N + col];
   }
-  Aff pre = block_exclusive_scan(m, sh);
-  {
-    double yin = pre.b;                       // y_{i0-1} (maps applied to 0)
-    double lp = lprev;
+}
+__device__ __forceinline__ void vchunk_store(double* vs, int lane, const double (&buf)[VPL]) {
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const double yi = fma(-lp, yin, wv[e]);
-      wv[e] = yi;
-      yin = yi;
-      lp = lv[e];
-    }
-  }
-  // diagonal
-#pragma unroll
-  for (int e = 0; e < E; ++e) wv[e] *= dv[e];
-  // backward: x_i = z_i - l_i x_{i+1}
-  {
-    double ca = 1.0, cb = 0.0;
-#pragma unroll
-    for (int e = E - 1; e >= 0; --e) {
-      ca = -lv[e] * ca;
-      cb = fma(-lv[e], cb, wv[e]);
-    }
-    m = Aff{ca, cb};
-  }
-  pre = block_exclusive_scan_rev(m, sh);
-  {
-    double xin = pre.b;                       // x_{i0+E}
-#pragma unroll
-    for (int e = E - 1; e >= 0; --e) {
-      const double xi = fma(-lv[e], xin, wv[e]);
-      wv[e] = xi;
-      xin = xi;
-    }
+  for (int q = 0; q < VPL; ++q) {
+    const int e = lane + 64 * q;
+    vs[(e / (BND * SCH)) * VLD + e % (BND * SCH)] = buf[q];
   }
 }
 
-// y = T x for the own rows of a thread (T tridiagonal, diagonal Td, off-
-// diagonal To[i] = T[i+1][i]); neighbours across threads through LDS.
-template <int E>
-__device__ __forceinline__ void tri_apply(const double (&x)[E], double (&y)[E], int i0, int N,
-                                          const double* __restrict__ Tdg,
-                                          const double* __restrict__ Tog, double* edge_lo,
-                                          double* edge_hi) {
-  const int t = threadIdx.x;
-  __syncthreads();
-  edge_lo[t] = x[0];
-  edge_hi[t] = x[E - 1];
-  __syncthreads();
-  const double left = t > 0 ? edge_hi[t - 1] : 0.0;
-  const double right = t + 1 < (int)blockDim.x ? edge_lo[t + 1] : 0.0;
+__device__ __forceinline__ void band_solve(const double* __restrict__ Vc,
+                                           const double* __restrict__ Dc, double* xs, double* vs,
+                                           int N, int lane) {
+  const int NB = N / BND;
+  const int a = lane & (BND - 1);
+  const bool wr = lane < BND;
+  double buf[VPL];
+  // forward: chunks I0 = 0, SCH, ...
+  vchunk_load(Vc, N, 0, lane, buf);
+  for (int I0 = 0; I0 < NB; I0 += SCH) {
+    wave_sync();
+    vchunk_store(vs, lane, buf);
+    wave_sync();
+    if (I0 + SCH < NB) vchunk_load(Vc, N, I0 + SCH, lane, buf);
+    const int nbk = (NB - I0 < SCH) ? NB - I0 : SCH;
+    for (int q = 0; q < nbk; ++q) {
+      const int I = I0 + q, i0 = BND * I;
+      double vr[BND];
 #pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int i = i0 + e;
-    double bv = 0.0;
-    if (i < N) {
-      const double xl = e > 0 ? x[e - 1] : left;
-      const double xr = e + 1 < E ? x[e + 1] : right;
-      bv = Tdg[i] * x[e];
-      if (i > 0) bv = fma(Tog[i - 1], xl, bv);
-      if (i + 1 < N) bv = fma(Tog[i], xr, bv);
+      for (int j = 0; j < BND; ++j) vr[j] = vs[j * VLD + BND * q + a];
+      double r0 = xs[i0 + a], r1 = 0.0;
+      if (I > 0) {
+#pragma unroll
+        for (int j = 0; j < BND; j += 2) {
+          r0 = fma((j >= a) ? -vr[j] : 0.0, xs[i0 - BND + j], r0);
+          r1 = fma((j + 1 >= a) ? -vr[j + 1] : 0.0, xs[i0 - BND + j + 1], r1);
+        }
+      }
+      const double r = r0 + r1;
+      wave_sync();
+      if (wr) xs[i0 + a] = r;
+      wave_sync();
+      double y0 = r, y1 = 0.0;
+#pragma unroll
+      for (int j = 0; j < BND; j += 2) {
+        y0 = fma((j < a) ? vr[j] : 0.0, xs[i0 + j], y0);
+        y1 = fma((j + 1 < a) ? vr[j + 1] : 0.0, xs[i0 + j + 1], y1);
+      }
+      wave_sync();
+      if (wr) xs[i0 + a] = y0 + y1;
+      wave_sync();
     }
-    y[e] = bv;
   }
+#pragma unroll 8
+  for (int i = lane; i < N; i += 64) xs[i] *= Dc[i];
+  // backward: chunks from the last one down; vp = tile of block I+1, transposed
+  double vp[BND];
+#pragma unroll
+  for (int j = 0; j < BND; ++j) vp[j] = 0.0;
+  const int last0 = ((NB - 1) / SCH) * SCH;
+  vchunk_load(Vc, N, last0, lane, buf);
+  for (int I0 = last0; I0 >= 0; I0 -= SCH) {
+    wave_sync();
+    vchunk_store(vs, lane, buf);
+    wave_sync();
+    if (I0 - SCH >= 0) vchunk_load(Vc, N, I0 - SCH, lane, buf);
+    const int nbk = (NB - I0 < SCH) ? NB - I0 : SCH;
+    for (int q = nbk - 1; q >= 0; --q) {
+      const int I = I0 + q, i0 = BND * I;
+      double vt[BND];                    // vt[j] = V_I[j][a]
+#pragma unroll
+      for (int j = 0; j < BND; ++j) vt[j] = vs[a * VLD + BND * q + j];
+      double s0 = xs[i0 + a], s1 = 0.0;
+      if (I + 1 < NB) {
+#pragma unroll
+        for (int j = 0; j < BND; j += 2) {
+          s0 = fma((j <= a) ? -vp[j] : 0.0, xs[i0 + BND + j], s0);
+          s1 = fma((j + 1 <= a) ? -vp[j + 1] : 0.0, xs[i0 + BND + j + 1], s1);
+        }
+      }
+      const double sv = s0 + s1;
+      wave_sync();
+      if (wr) xs[i0 + a] = sv;
+      wave_sync();
+      double x0 = sv, x1 = 0.0;
+#pragma unroll
+      for (int j = 0; j < BND; j += 2) {
+        x0 = fma((j > a) ? vt[j] : 0.0, xs[i0 + j], x0);
+        x1 = fma((j + 1 > a) ? vt[j + 1] : 0.0, xs[i0 + j + 1], x1);
+      }
+      wave_sync();
+      if (wr) xs[i0 + a] = x0 + x1;
+      wave_sync();
+#pragma unroll
+      for (int j = 0; j < BND; ++j) vp[j] = vt[j];
+    }
+  }
+}
+
+// Columns (wavefronts) per workgroup for order N: the LDS of a workgroup
+// holds one N-vector per column plus small per-column tiles.
+constexpr int PTILE = 3 * BND * (BND + 1) + 2 * BND;   // precompute LDS tiles per column
+constexpr int PEXTRA = (VSTAGE > PTILE) ? VSTAGE : PTILE;   // per-column LDS beyond the vector
+static int path_waves(int N) {
+  const size_t per = sizeof(double) * ((size_t)N + PEXTRA);
+  int cw = 4;
+  while (cw > 1 && cw * per > 64 * 1024) cw /= 2;
+  return cw;
 }
 
 // ------------------------------------------------------ per-stage factors
-// One workgroup per column: LDL' of M = 2 lambda I + T/(n_v kappa) (the
-// pivot recurrence is sequential, run by one thread over LDS-staged chunks
-// of T), then vhat = M^{-1} c/(n_v kappa), u = T vhat, g = 1/(2 lambda
-// c'vhat); restart the momentum (r = 1, abar = ahat, B = T ahat) and
-// reactivate the columns that stopped in the previous stage.
-template <int E>
-__global__ __launch_bounds__(PB) void precompute_kernel(
-    int N, int C, const int* __restrict__ nv, const double* __restrict__ Td,
-    const double* __restrict__ To, const double* __restrict__ cvec, const double* __restrict__ lamv,
-    double kappa, double* __restrict__ ldl_l, double* __restrict__ ldl_d, double* __restrict__ vhat,
+// One wavefront per column: the blockwise LDL' of M = 2 lambda I + B/(n_v
+// kappa) (stored as above), vhat = M^{-1} c/(n_v kappa), u = B vhat,
+// g = 1/(2 lambda c'vhat); restart the momentum (r = 1, abar = ahat,
+// B abar) and reactivate the columns that stopped in the previous stage.
+__global__ __launch_bounds__(256) void precompute_kernel(
+    int N, int C, int64_t cols, const int* __restrict__ nv, const double* __restrict__ band,
+    const double* __restrict__ cvec, const double* __restrict__ lamv, double kappa,
+    double* __restrict__ Vfac, double* __restrict__ Dfac, double* __restrict__ vhat,
     double* __restrict__ uvec, double* __restrict__ gcoef, const double* __restrict__ ahat,
     double* __restrict__ abar, double* __restrict__ bmat, const double* __restrict__ beta,
     double* __restrict__ bbar, double* __restrict__ rmom, int* __restrict__ flag,
     int* __restrict__ iters) {
-  __shared__ double red[PW];
-  __shared__ Aff sh[PW];
-  __shared__ double sd[PB], so[PB], sl[PB], sdi[PB];
-  __shared__ double edge_lo[PB], edge_hi[PB];
-  const int64_t gc = blockIdx.x;
+  extern __shared__ double lds_dyn[];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t gc = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
+  if (gc >= cols) return;
+  double* xs = lds_dyn + (int64_t)wv * (N + PEXTRA);
+  double (*T1)[BND + 1] = reinterpret_cast<double (*)[BND + 1]>(xs + N);
+  double (*T2)[BND + 1] = T1 + BND;
+  double (*T3)[BND + 1] = T2 + BND;
+  double* dcur = xs + N + 3 * BND * (BND + 1);
+  double* dprv = dcur + BND;
   const int g = (int)(gc / C);
-  const int t = threadIdx.x;
-  const int i0 = t * E;
-  const int64_t base = gc * N;
   const double lam = lamv[gc];
   const double sc = 1.0 / ((double)nv[g] * kappa);
-  const double* d = Td + (int64_t)g * N;
-  const double* o = To + (int64_t)g * N;
-  const double* c = cvec + (int64_t)g * N;
-  // pivots: D_i = 2 lambda + T_ii sc - l_{i-1} T_{i,i-1} sc, l_i = T_{i+1,i} sc / D_i
-  double lrun = 0.0, orun = 0.0;
-  for (int c0 = 0; c0 < N; c0 += PB) {
-    const int i = c0 + t;
-    sd[t] = i < N ? d[i] : 0.0;
-    so[t] = i < N ? o[i] : 0.0;
-    __syncthreads();
-    if (t == 0) {
-      const int cnt = (N - c0 < PB) ? N - c0 : PB;
-      for (int k = 0; k < cnt; ++k) {
-        const double piv = fma(-lrun, orun, fma(sd[k], sc, 2.0 * lam));
-        const double dinv = 1.0 / piv;
-        orun = so[k] * sc;
-        lrun = (c0 + k + 1 < N) ? orun * dinv : 0.0;
-        sl[k] = lrun;
-        sdi[k] = dinv;
+  const double* bg = band + (int64_t)g * (BND + 1) * N;
+  const double* cg = cvec + (int64_t)g * N;
+  double* Vc = Vfac + gc * (int64_t)BND * N;
+  double* Dc = Dfac + gc * (int64_t)N;
+  const int64_t base = gc * (int64_t)N;
+  const int a = lane & (BND - 1);
+  const bool wr = lane < BND;
+  const int NB = N / BND;
+  double cp[BND];                        // row a of C_I (zero for I = 0)
+#pragma unroll
+  for (int j = 0; j < BND; ++j) cp[j] = 0.0;
+  if (wr) dprv[a] = 0.0;
+  for (int I = 0; I < NB; ++I) {
+    const int i0 = BND * I;
+    // S = M_II - C_I D_{I-1} C_I'  (row a)
+    wave_sync();
+    if (wr) {
+#pragma unroll
+      for (int j = 0; j < BND; ++j) T1[a][j] = cp[j];
+    }
+    wave_sync();
+    double sr[BND];
+#pragma unroll
+    for (int c = 0; c < BND; ++c) {
+      const int64_t off = (c <= a) ? (int64_t)(a - c) * N + i0 + c : (int64_t)(c - a) * N + i0 + a;
+      const double bv = bg[off];
+      double m = sc * bv;
+      if (c == a) m += 2.0 * lam;
+      double acc = 0.0;
+#pragma unroll
+      for (int j = 0; j < BND; ++j) acc = fma(cp[j] * dprv[j], T1[c][j], acc);
+      sr[c] = m - acc;
+    }
+    // dense LDL' of S, row a of L in sr (columns < a), D in dcur
+#pragma unroll
+    for (int k = 0; k < BND; ++k) {
+      if (a == k) {
+        double d = sr[k];
+#pragma unroll
+        for (int m = 0; m < BND; ++m)
+          if (m < k) d = fma(-sr[m] * sr[m], dcur[m], d);
+        if (wr) dcur[k] = d;
+#pragma unroll
+        for (int m = 0; m < BND; ++m)
+          if (wr && m < k) T2[k][m] = sr[m];
+      }
+      wave_sync();
+      if (a > k) {
+        double v = sr[k];
+#pragma unroll
+        for (int m = 0; m < BND; ++m)
+          if (m < k) v = fma(-sr[m] * T2[k][m], dcur[m], v);
+        sr[k] = v / dcur[k];
+      }
+      wave_sync();
+    }
+    // rows of L in T2 (strict lower part)
+    if (wr) {
+#pragma unroll
+      for (int m = 0; m < BND; ++m)
+        if (m < a) T2[a][m] = sr[m];
+    }
+    wave_sync();
+    // L^{-1}: lane a computes column a, stored transposed in T3[row][a]
+    {
+      double xcol[BND];
+#pragma unroll
+      for (int r = 0; r < BND; ++r) {
+        double v = (r == a) ? 1.0 : 0.0;
+        if (r > a) {
+#pragma unroll
+          for (int m = 0; m < BND; ++m)
+            if (m >= a && m < r) v = fma(-T2[r][m], xcol[m], v);
+        }
+        xcol[r] = v;
+      }
+      if (wr) {
+#pragma unroll
+        for (int r = 0; r < BND; ++r) T3[r][a] = xcol[r];
       }
     }
-    __syncthreads();
-    if (i < N) {
-      ldl_l[base + i] = sl[t];
-      ldl_d[base + i] = sdi[t];
-    }
-    __syncthreads();
-  }
-  double lv[E], dv[E], wv[E];
+    wave_sync();
+    // store the tile: j < a from L^{-1}, j >= a from C_I; 1/D
+    if (wr) {
 #pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int i = i0 + e;
-    lv[e] = i < N ? ldl_l[base + i] : 0.0;
-    dv[e] = i < N ? ldl_d[base + i] : 0.0;
-    wv[e] = i < N ? c[i] * sc : 0.0;
+      for (int j = 0; j < BND; ++j) Vc[(int64_t)j * N + i0 + a] = (j < a) ? T3[a][j] : cp[j];
+      Dc[i0 + a] = 1.0 / dcur[a];
+    }
+    // C_{I+1} = M_{I+1,I} L^{-T} D^{-1}: C[a][c] = sum_{j=a..c} Mn[a][j] Linv[c][j] / D[c]
+    if (I + 1 < NB) {
+      double mn[BND];
+#pragma unroll
+      for (int j = 0; j < BND; ++j) {
+        const int r = (j >= a) ? BND + a - j : BND;
+        const double bv = bg[(int64_t)r * N + i0 + j];
+        mn[j] = (j >= a) ? sc * bv : 0.0;
+      }
+#pragma unroll
+      for (int c = 0; c < BND; ++c) {
+        double acc = 0.0;
+#pragma unroll
+        for (int j = 0; j < BND; ++j)
+          if (j >= a && j <= c) acc = fma(mn[j], T3[c][j], acc);
+        cp[c] = (c >= a) ? acc / dcur[c] : 0.0;
+      }
+    }
+    wave_sync();
+    if (wr) dprv[a] = dcur[a];
+    wave_sync();
   }
-  const double lprev = (i0 > 0 && i0 - 1 < N) ? ldl_l[base + i0 - 1] : 0.0;
-  ldl_solve<E>(wv, lv, lprev, dv, sh);
-  double u[E];
-  tri_apply<E>(wv, u, i0, N, d, o, edge_lo, edge_hi);
+  // vhat = M^{-1} c sc, u = B vhat, c'vhat
+#pragma unroll 8
+  for (int i = lane; i < N; i += 64) xs[i] = cg[i] * sc;
+  wave_sync();
+  band_solve(Vc, Dc, xs, xs + N, N, lane);
   double cv = 0.0;
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int i = i0 + e;
-    if (i < N) {
-      vhat[base + i] = wv[e];
-      uvec[base + i] = u[e];
-      cv = fma(c[i], wv[e], cv);
-    }
+#pragma unroll 2
+  for (int i = lane; i < N; i += 64) {
+    vhat[base + i] = xs[i];
+    uvec[base + i] = band_row(bg, xs, N, i);
+    cv = fma(cg[i], xs[i], cv);
   }
-  cv = block_sum<PW>(cv, red);
+  cv = wave_sum(cv);
   // stage restart of the accelerated iteration
-  double ah[E], bm[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) ah[e] = (i0 + e < N) ? ahat[base + i0 + e] : 0.0;
-  tri_apply<E>(ah, bm, i0, N, d, o, edge_lo, edge_hi);
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int i = i0 + e;
-    if (i < N) {
-      abar[base + i] = ah[e];
-      bmat[base + i] = bm[e];
-    }
+  wave_sync();
+#pragma unroll 8
+  for (int i = lane; i < N; i += 64) {
+    const double ah = ahat[base + i];
+    xs[i] = ah;
+    abar[base + i] = ah;
   }
-  if (t == 0) {
+  wave_sync();
+#pragma unroll 2
+  for (int i = lane; i < N; i += 64) bmat[base + i] = band_row(bg, xs, N, i);
+  if (lane == 0) {
     gcoef[gc] = 1.0 / (2.0 * lam * cv);
     bbar[gc] = beta[gc];
     rmom[gc] = 1.0;
@@ -341,103 +445,85 @@ __global__ __launch_bounds__(PB) void precompute_kernel(
 }
 
 int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa) {
-  const unsigned cols = (unsigned)(p.G * p.C);
+  const int64_t cols = (int64_t)p.G * p.C;
+  const int cw = path_waves(p.N);
+  const size_t lds = sizeof(double) * (size_t)cw * (p.N + PEXTRA);
+  KMP_HIP_TRY(hipFuncSetAttribute((const void*)precompute_kernel,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   kc_begin(KMP_KC_PRECOMPUTE, s);
-#define KMP_PRE(EE)                                                                              \
-  hipLaunchKernelGGL(precompute_kernel<EE>, dim3(cols), dim3(PB), 0, s, p.N, p.C, p.nv, p.Tdiag, \
-                     p.Toff, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat, p.uvec, p.gcoef,    \
-                     p.ahat, p.abar, p.bmat, p.beta, p.bbar, p.rmom, p.flag, p.iters)
-  if (p.N <= PB * 1) KMP_PRE(1);
-  else if (p.N <= PB * 2) KMP_PRE(2);
-  else if (p.N <= PB * 4) KMP_PRE(4);
-  else if (p.N <= PB * 8) KMP_PRE(8);
-  else if (p.N <= PB * 16) KMP_PRE(16);
-  else if (p.N <= PB * 32) KMP_PRE(32);
-  else {
-    set_error("path: more than 8192 training points per fold is not supported yet");
-    return KMP_EINVAL;
-  }
-#undef KMP_PRE
+  hipLaunchKernelGGL(precompute_kernel, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, s,
+                     p.N, p.C, cols, p.nv, p.band, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
+                     p.uvec, p.gcoef, p.ahat, p.abar, p.bmat, p.beta, p.bbar, p.rmom, p.flag,
+                     p.iters);
   KMP_LAUNCH_CHECK();
-  // reads T, c, ahat; writes l, 1/d, vhat, u, abar, T ahat
-  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * 8.0; }),
-         over_groups(p, [&](double n) { return 20.0 * n * p.C; }));
+  // reads the band and c, writes the factor tiles (BND per element), 1/d,
+  // vhat, u, abar, B abar
+  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 8.0); }),
+         over_groups(p, [&](double n) { return 4.0 * BND * BND * n * p.C; }));
   return 0;
 }
 
 // ------------------------------------------------------- the update (K2)
-// One workgroup per column; thread t owns rows [t*E, t*E + E).
-template <int E>
-__global__ __launch_bounds__(PB) void update_kernel(
-    int N, int C, int RT, const int* __restrict__ nvv, const double* __restrict__ Td,
-    const double* __restrict__ To, const double* __restrict__ lamv,
+// One wavefront per column.
+__global__ __launch_bounds__(256) void update_kernel(
+    int N, int C, int64_t cols, int RT, const int* __restrict__ nvv,
+    const double* __restrict__ band, const double* __restrict__ lamv,
     const double* __restrict__ zpart, int S2, int64_t sP, double* __restrict__ ahat,
-    double* __restrict__ abar,
-    double* __restrict__ bmat, const double* __restrict__ ldl_l, const double* __restrict__ ldl_d,
-    const double* __restrict__ vhat, const double* __restrict__ uvec,
-    const double* __restrict__ gcoef, const double* __restrict__ partial,
-    double* __restrict__ beta, double* __restrict__ bbar, double* __restrict__ rmom,
-    double* __restrict__ kktv, int* __restrict__ flag, int* __restrict__ iters,
-    int* __restrict__ iters_total, double tol, int max_iter, int restart) {
-  __shared__ double red[PW];
-  __shared__ Aff sh[PW];
-  __shared__ double edge_lo[PB], edge_hi[PB];
-  const int64_t gc = blockIdx.x;
+    double* __restrict__ abar, double* __restrict__ bmat, const double* __restrict__ Vfac,
+    const double* __restrict__ Dfac, const double* __restrict__ vhat,
+    const double* __restrict__ uvec, const double* __restrict__ gcoef,
+    const double* __restrict__ partial, double* __restrict__ beta, double* __restrict__ bbar,
+    double* __restrict__ rmom, double* __restrict__ kktv, int* __restrict__ flag,
+    int* __restrict__ iters, int* __restrict__ iters_total, double tol, int max_iter,
+    int restart) {
+  extern __shared__ double lds_dyn[];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t gc = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
+  if (gc >= cols) return;
   if (flag[gc] != 0) return;
+  double* xs = lds_dyn + (int64_t)wv * (N + PEXTRA);
   const int g = (int)(gc / C), c = (int)(gc % C);
-  const int t = threadIdx.x;
-  const int i0 = t * E;
-  const int64_t base = gc * N;
+  const int64_t base = gc * (int64_t)N;
   const double lam = lamv[gc];
   const double nvd = (double)nvv[g];
-  const double* Tdg = Td + (int64_t)g * N;
-  const double* Tog = To + (int64_t)g * N;
-
+  const double* bg = band + (int64_t)g * (BND + 1) * N;
   double d0 = 0.0;
   {
     const double* pg = partial + (int64_t)g * RT * C + c;
-    for (int r = 0; r < RT; ++r) d0 += pg[(int64_t)r * C];
+    for (int r = lane; r < RT; r += 64) d0 += pg[(int64_t)r * C];
+    d0 = wave_sum(d0);
   }
-  double wv[E], ab[E], ah[E];
   double tl = 0.0, n2 = 0.0;
+#pragma unroll 8
+  for (int i = lane; i < N; i += 64) {
+    // split-K parts added in order; parts beyond S2 are not used
+    double zp[kMaxSplitK];
 #pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int i = i0 + e;
-    if (i < N) {
-      ab[e] = abar[base + i];
-      ah[e] = ahat[base + i];
-      double zh = 0.0;
-      for (int sk = 0; sk < S2; ++sk) zh += zpart[(int64_t)sk * sP + base + i];
-      wv[e] = fma(2.0 * lam, ab[e], zh);
-      tl = fma(uvec[base + i], wv[e], tl);
-      n2 = fma(wv[e], wv[e], n2);
-    } else {
-      ab[e] = ah[e] = wv[e] = 0.0;
-    }
+    for (int sk = 0; sk < kMaxSplitK; ++sk) zp[sk] = zpart[(int64_t)sk * sP + base + i];
+    double zh = zp[0];
+#pragma unroll
+    for (int sk = 1; sk < kMaxSplitK; ++sk) zh += (sk < S2) ? zp[sk] : 0.0;
+    const double w = fma(2.0 * lam, abar[base + i], zh);
+    xs[i] = w;
+    tl = fma(uvec[base + i], w, tl);
+    n2 = fma(w, w, n2);
   }
-  const double tsum = block_sum<PW>(tl, red);
-  const double n2sum = block_sum<PW>(n2, red);
+  const double tsum = wave_sum(tl);
+  const double n2sum = wave_sum(n2);
   const double kkt = nvd * fmax(sqrt(n2sum), fabs(d0));
   const double bb = bbar[gc];
   if (!(kkt == kkt) || kkt > 1e300) {          // non-finite
-    if (t == 0) { flag[gc] = 3; kktv[gc] = kkt; }
+    if (lane == 0) { flag[gc] = 3; kktv[gc] = kkt; }
     return;
   }
   if (kkt <= tol) {                            // certified at the extrapolated point
-#pragma unroll
-    for (int e = 0; e < E; ++e)
-      if (i0 + e < N) ahat[base + i0 + e] = ab[e];
-    if (t == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; }
+#pragma unroll 8
+    for (int i = lane; i < N; i += 64) ahat[base + i] = abar[base + i];
+    if (lane == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; }
     return;
   }
-  double lv[E], dv[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    lv[e] = (i0 + e < N) ? ldl_l[base + i0 + e] : 0.0;
-    dv[e] = (i0 + e < N) ? ldl_d[base + i0 + e] : 0.0;
-  }
-  const double lprev = (i0 > 0 && i0 - 1 < N) ? ldl_l[base + i0 - 1] : 0.0;
-  ldl_solve<E>(wv, lv, lprev, dv, sh);
+  wave_sync();
+  band_solve(Vfac + gc * (int64_t)BND * N, Dfac + base, xs, xs + N, N, lane);
   // step, new iterate and the restart test
   const double gco = gcoef[gc];
   const double sa = gco * (tsum - d0);
@@ -445,42 +531,29 @@ __global__ __launch_bounds__(PB) void update_kernel(
   const double bn = bb - db;
   const double bold = beta[gc];
   double rd = 0.0;
-  double an[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int i = i0 + e;
-    double da = 0.0;
-    if (i < N) da = fma(sa, vhat[base + i], wv[e]);
-    an[e] = ab[e] - da;
-    rd = fma(da, an[e] - ah[e], rd);
+#pragma unroll 8
+  for (int i = lane; i < N; i += 64) {
+    const double da = fma(sa, vhat[base + i], xs[i]);
+    const double an = abar[base + i] - da;
+    rd = fma(da, an - ahat[base + i], rd);
+    xs[i] = an;
   }
-  rd = block_sum<PW>(rd, red) + db * (bn - bold);
+  rd = wave_sum(rd) + db * (bn - bold);
   const double r = rmom[gc];
   const double rn = (restart && rd > 0.0) ? 1.0 : 0.5 * (1.0 + sqrt(1.0 + 4.0 * r * r));
   const double coef = (rn - 1.0) / (0.5 * (1.0 + sqrt(1.0 + 4.0 * rn * rn)));
-  double nb_[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) nb_[e] = fma(coef, an[e] - ah[e], an[e]);
-  edge_lo[t] = nb_[0];
-  edge_hi[t] = nb_[E - 1];
-  __syncthreads();
-  const double left = t > 0 ? edge_hi[t - 1] : 0.0;
-  const double right = t + 1 < PB ? edge_lo[t + 1] : 0.0;
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int i = i0 + e;
-    if (i < N) {
-      const double xl = e > 0 ? nb_[e - 1] : left;
-      const double xr = e + 1 < E ? nb_[e + 1] : right;
-      double bv = Tdg[i] * nb_[e];
-      if (i > 0) bv = fma(Tog[i - 1], xl, bv);
-      if (i + 1 < N) bv = fma(Tog[i], xr, bv);
-      ahat[base + i] = an[e];
-      abar[base + i] = nb_[e];
-      bmat[base + i] = bv;
-    }
+#pragma unroll 8
+  for (int i = lane; i < N; i += 64) {
+    const double an = xs[i];
+    const double nb = fma(coef, an - ahat[base + i], an);
+    ahat[base + i] = an;
+    abar[base + i] = nb;
+    xs[i] = nb;
   }
-  if (t == 0) {
+  wave_sync();
+#pragma unroll 2
+  for (int i = lane; i < N; i += 64) bmat[base + i] = band_row(bg, xs, N, i);
+  if (lane == 0) {
     beta[gc] = bn;
     bbar[gc] = fma(coef, bn - bold, bn);
     rmom[gc] = rn;
@@ -499,7 +572,7 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   const int RT = (int)ceil_div(p.N, 64);
   const int64_t sC = (int64_t)p.N * p.C;
   const int64_t sP = (int64_t)p.G * sC;
-  // f = Q (T abar) as split-K partials, then z = psi(y, f + bbar)/n_v with
+  // f = Q (B abar) as split-K partials, then z = psi(y, f + bbar)/n_v with
   // 64-row column sums
   GemmArgs g1;
   g1.M = p.N; g1.N = p.C; g1.K = p.N; g1.batch = p.G;
@@ -528,30 +601,21 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   kc_begin(KMP_KC_GEMM_ZHAT, s);
   if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP)) != 0) return rc;
   kc_end(KMP_KC_GEMM_ZHAT, s, gbytes, gflops);
-  const unsigned cols = (unsigned)(p.G * p.C);
+  const int64_t cols = (int64_t)p.G * p.C;
+  const int cw = path_waves(p.N);
+  const size_t lds = sizeof(double) * (size_t)cw * (p.N + PEXTRA);
+  KMP_HIP_TRY(hipFuncSetAttribute((const void*)update_kernel,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   kc_begin(KMP_KC_UPDATE, s);
-#define KMP_UPD(EE)                                                                              \
-  hipLaunchKernelGGL(update_kernel<EE>, dim3(cols), dim3(PB), 0, s, p.N, p.C, RT, p.nv, p.Tdiag, \
-                     p.Toff, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.bmat, p.ldl_l, p.ldl_d,   \
-                     p.vhat,                                                                     \
-                     p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt, p.flag, p.iters, \
-                     p.iters_total, tol, max_iter, restart)
-  if (p.N <= PB * 1) KMP_UPD(1);
-  else if (p.N <= PB * 2) KMP_UPD(2);
-  else if (p.N <= PB * 4) KMP_UPD(4);
-  else if (p.N <= PB * 8) KMP_UPD(8);
-  else if (p.N <= PB * 16) KMP_UPD(16);
-  else if (p.N <= PB * 32) KMP_UPD(32);
-  else {
-    set_error("path: more than 8192 training points per fold is not supported yet");
-    return KMP_EINVAL;
-  }
-#undef KMP_UPD
+  hipLaunchKernelGGL(update_kernel, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, s, p.N,
+                     p.C, cols, RT, p.nv, p.band, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.bmat,
+                     p.ldl_l, p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom,
+                     p.kkt, p.flag, p.iters, p.iters_total, tol, max_iter, restart);
   KMP_LAUNCH_CHECK();
-  // per column element: read zhat, abar, ahat, l, 1/d, vhat, u; write ahat,
-  // abar, T abar (80 bytes), counted for every column of the launch
-  kc_end(KMP_KC_UPDATE, s, over_groups(p, [&](double n) { return 80.0 * n * p.C; }),
-         over_groups(p, [&](double n) { return 30.0 * n * p.C; }));
+  // per column element: read zhat, abar (twice), ahat (twice), the factor
+  // tile row (BND, twice), 1/d, vhat, u; write ahat, abar, B abar
+  kc_end(KMP_KC_UPDATE, s, over_groups(p, [&](double n) { return 8.0 * (13.0 + 2.0 * BND) * n * p.C; }),
+         over_groups(p, [&](double n) { return (12.0 + 4.0 * BND + 4.0 * BND) * n * p.C; }));
   return 0;
 }
 
@@ -571,21 +635,27 @@ int path_count_active(hipStream_t s, const PathArrays& p) {
 }
 
 // --------------------------------------------------------------- finalize
-// B = T ahat for every column (T tridiagonal per group).
-__global__ void tri_mult_kernel(int N, int C, int64_t total, const double* __restrict__ Td,
-                                const double* __restrict__ To, const double* __restrict__ x,
-                                double* __restrict__ y) {
+// Y = B X for every column (B banded per group, band[g][r*N + j] = B[j+r][j],
+// zero for j + r >= N); unconditional loads as in band_row.
+__global__ void band_mult_kernel(int N, int C, int64_t total, const double* __restrict__ band,
+                                 const double* __restrict__ x, double* __restrict__ y) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= total) return;
   const int64_t col = idx / N;
   const int i = (int)(idx % N);
   const int g = (int)(col / C);
-  const double* d = Td + (int64_t)g * N;
-  const double* o = To + (int64_t)g * N;
+  const double* bg = band + (int64_t)g * (BND + 1) * N;
   const double* xc = x + col * N;
-  double v = d[i] * xc[i];
-  if (i > 0) v = fma(o[i - 1], xc[i - 1], v);
-  if (i + 1 < N) v = fma(o[i], xc[i + 1], v);
+  double v = bg[i] * xc[i];
+#pragma unroll
+  for (int r = 1; r <= BND; ++r) {
+    const int il = (i - r >= 0) ? i - r : 0;
+    const int iu = (i + r < N) ? i + r : N - 1;
+    const double bl = bg[(int64_t)r * N + il];
+    const double bu = bg[(int64_t)r * N + i];
+    v = fma((i - r >= 0) ? bl : 0.0, xc[il], v);
+    v = fma(bu, xc[iu], v);
+  }
   y[idx] = v;
 }
 
@@ -659,10 +729,10 @@ int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
   g.B = p.ahat; g.ldb = p.N; g.sB = sNC;
   g.C = p.zmat; g.ldc = p.N; g.sC = sNC;
   if ((rc = gemm(s, g, true, true, false)) != 0) return rc;
-  // training predictions K_v alpha = Q (T ahat)
+  // training predictions K_v alpha = Q (B ahat)
   const int64_t tot = (int64_t)p.G * sNC;
-  hipLaunchKernelGGL(tri_mult_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, s, p.N, p.C,
-                     tot, p.Tdiag, p.Toff, p.ahat, p.bmat);
+  hipLaunchKernelGGL(band_mult_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, s, p.N, p.C,
+                     tot, p.band, p.ahat, p.bmat);
   KMP_LAUNCH_CHECK();
   GemmArgs gt = g;
   gt.B = p.bmat;
