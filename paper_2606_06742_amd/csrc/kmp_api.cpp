@@ -106,9 +106,9 @@ struct Carver {
 struct Layout {
   double *A, *Qm, *diag, *off, *tau, *cvec, *ylab, *panel, *dots, *tmat, *gram, *xbuf, *ybuf;
   double *spart, *pnext, *band, *bpart;
-  double *ahat, *abar, *bmat, *zmat, *zhat, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
-  double *beta, *bbar, *rmom, *gcoef, *kkt, *lam, *taucol, *fbuf, *nrm, *inv2s2;
-  int *flag, *iters, *iters_total, *active, *nvg;
+  double *ahat, *abar, *bmat, *zmat, *anew, *estep, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
+  double *beta, *bbar, *rmom, *gcoef, *kkt, *coef, *lam, *taucol, *fbuf, *nrm, *inv2s2;
+  int *flag, *moved, *iters, *iters_total, *active, *nvg;
   int32_t *tidx, *hidx, *fold;
 };
 
@@ -137,7 +137,8 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.abar = c.take<double>(cols * N);
   l.bmat = c.take<double>(cols * N);
   l.zmat = c.take<double>(cols * N);
-  l.zhat = c.take<double>(cols * N);
+  l.anew = c.take<double>(cols * N);
+  l.estep = c.take<double>(cols * N);
   l.ldl_l = c.take<double>(cols * kBand * N);
   l.ldl_d = c.take<double>(cols * N);
   l.vhat = c.take<double>(cols * N);
@@ -150,12 +151,14 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.rmom = c.take<double>(cols);
   l.gcoef = c.take<double>(cols);
   l.kkt = c.take<double>(cols);
+  l.coef = c.take<double>(cols);
   l.lam = c.take<double>(cols);
   l.taucol = c.take<double>(cols);
   l.fbuf = c.take<double>(cols * (size_t)p.Mh);
   l.nrm = c.take<double>((size_t)p.n);
   l.inv2s2 = c.take<double>((size_t)std::max(p.S, 1));
   l.flag = c.take<int>(cols);
+  l.moved = c.take<int>(cols);
   l.iters = c.take<int>(cols);
   l.iters_total = c.take<int>(cols);
   l.active = c.take<int>(1);
@@ -542,10 +545,12 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   pa.nv = lay.nvg; pa.ylab = lay.ylab; pa.Q = lay.Qm; pa.band = lay.band;
   pa.cvec = lay.cvec; pa.lam = lay.lam; pa.tau = lay.taucol;
   pa.ahat = lay.ahat; pa.abar = lay.abar; pa.bmat = lay.bmat; pa.zmat = lay.zmat;
-  pa.zhat = lay.zhat; pa.ldl_l = lay.ldl_l; pa.ldl_d = lay.ldl_d; pa.vhat = lay.vhat;
+  pa.anew = lay.anew; pa.estep = lay.estep; pa.ldl_l = lay.ldl_l; pa.ldl_d = lay.ldl_d;
+  pa.vhat = lay.vhat;
   pa.uvec = lay.uvec; pa.partial = lay.partial; pa.beta = lay.beta; pa.bbar = lay.bbar;
   pa.fpart = lay.fpart; pa.zpart = lay.zpart;
-  pa.rmom = lay.rmom; pa.gcoef = lay.gcoef; pa.kkt = lay.kkt; pa.flag = lay.flag;
+  pa.rmom = lay.rmom; pa.gcoef = lay.gcoef; pa.kkt = lay.kkt; pa.coef = lay.coef;
+  pa.moved = lay.moved; pa.flag = lay.flag;
   pa.iters = lay.iters; pa.iters_total = lay.iters_total; pa.active_count = lay.active;
 
   for (int s0 = 0; s0 < S; s0 += Sb) {

@@ -136,7 +136,8 @@ struct PathArrays {
   double* abar = nullptr;
   double* bmat = nullptr;   // T abar, operand of the first GEMM
   double* zmat = nullptr;
-  double* zhat = nullptr;
+  double* anew = nullptr;   // a+ of the current step
+  double* estep = nullptr;  // a+ - ahat
   double* ldl_l = nullptr;  // kBand x N per column: tiles of the banded LDL' factor
   double* ldl_d = nullptr;  // N per column: 1/D
   double* vhat = nullptr;
@@ -150,6 +151,8 @@ struct PathArrays {
   double* rmom = nullptr;
   double* gcoef = nullptr;
   double* kkt = nullptr;
+  double* coef = nullptr;   // momentum coefficient of the current step
+  int* moved = nullptr;     // 1 when the column stepped in the current iteration
   int* flag = nullptr;      // 0 active, 1 converged, 2 max_iter, 3 non-finite
   int* iters = nullptr;     // per stage
   int* iters_total = nullptr;

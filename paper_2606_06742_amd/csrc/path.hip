@@ -91,6 +91,7 @@ int path_init_columns(hipStream_t s, const PathArrays& p) {
   KMP_HIP_TRY(hipMemsetAsync(p.beta, 0, cols * sizeof(double), s));
   KMP_HIP_TRY(hipMemsetAsync(p.bbar, 0, cols * sizeof(double), s));
   KMP_HIP_TRY(hipMemsetAsync(p.flag, 0, cols * sizeof(int), s));
+  KMP_HIP_TRY(hipMemsetAsync(p.moved, 0, cols * sizeof(int), s));
   KMP_HIP_TRY(hipMemsetAsync(p.iters, 0, cols * sizeof(int), s));
   KMP_HIP_TRY(hipMemsetAsync(p.iters_total, 0, cols * sizeof(int), s));
   return 0;
@@ -128,151 +129,198 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// (B x)[i] with x in LDS; bg[r*N + j] = B[j+r][j], zero for j + r >= N.
-// All loads are unconditional (clamped addresses, masked products) so that
-// they are issued together.
-__device__ __forceinline__ double band_row(const double* __restrict__ bg, const double* xs, int N,
-                                           int i) {
-  double y = bg[i] * xs[i];
-#pragma unroll
-  for (int r = 1; r <= BND; ++r) {
-    const int il = (i - r >= 0) ? i - r : 0;
-    const int iu = (i + r < N) ? i + r : N - 1;
-    const double bl = bg[(int64_t)r * N + il];
-    const double bu = bg[(int64_t)r * N + i];          // zero when i + r >= N
-    y = fma((i - r >= 0) ? bl : 0.0, xs[il], y);
-    y = fma(bu, xs[iu], y);
-  }
-  return y;
+// Sum over the four 16-lane rows of the wavefront: lane (a, g) (a = lane
+// mod 16, g = lane / 16) receives sum_g' v(a, g'), added as (row 0 + row 1)
+// + (row 2 + row 3) in every lane. gfx950's permlane16 swap exchanges the
+// odd rows of its first operand with the even rows of its second, permlane32
+// the upper half of the first with the lower half of the second.
+__device__ __forceinline__ double swap_sum16(double v) {
+  const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+  const auto lo = __builtin_amdgcn_permlane16_swap((unsigned)b, (unsigned)b, false, false);
+  const auto hi = __builtin_amdgcn_permlane16_swap((unsigned)(b >> 32), (unsigned)(b >> 32), false, false);
+  return __longlong_as_double((long long)(((unsigned long long)hi[0] << 32) | lo[0])) +
+         __longlong_as_double((long long)(((unsigned long long)hi[1] << 32) | lo[1]));
 }
+__device__ __forceinline__ double swap_sum32(double v) {
+  const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+  const auto lo = __builtin_amdgcn_permlane32_swap((unsigned)b, (unsigned)b, false, false);
+  const auto hi = __builtin_amdgcn_permlane32_swap((unsigned)(b >> 32), (unsigned)(b >> 32), false, false);
+  return __longlong_as_double((long long)(((unsigned long long)hi[0] << 32) | lo[0])) +
+         __longlong_as_double((long long)(((unsigned long long)hi[1] << 32) | lo[1]));
+}
+__device__ __forceinline__ double row4_sum(double v) { return swap_sum32(swap_sum16(v)); }
 
-// xs <- M^{-1} xs from the stored factor (Vc: BND x N tiles, Dc: 1/D).
-// The tiles pass through LDS (vs, VSTAGE doubles) in chunks of SCH blocks:
-// all 64 lanes load the next chunk into registers while the current one is
-// used, so the block recurrence does not wait on device memory. Chunk
-// element (j, 16 q + a) of blocks I0 .. I0+SCH-1 sits at vs[j * VLD + 16 q + a].
-constexpr int SCH = 4;
-constexpr int VLD = BND * SCH + 1;                  // padded row: conflict-free transposed reads
-constexpr int VSTAGE = BND * VLD;
-constexpr int VPL = BND * BND * SCH / 64;           // chunk doubles per lane
-
-__device__ __forceinline__ void vchunk_load(const double* __restrict__ Vc, int N, int I0,
-                                            int lane, double (&buf)[VPL]) {
-#pragma unroll
-  for (int q = 0; q < VPL; ++q) {
-    const int e = lane + 64 * q;
-    const int j = e / (BND * SCH), rem = e % (BND * SCH);
-    // rows past the last block are never read: clamp the address, no mask
-    const int col = (BND * I0 + rem < N) ? BND * I0 + rem : N - 1;
-    buf[q] = Vc[(int64_t)j * N + col];
-  }
-}
-__device__ __forceinline__ void vchunk_store(double* vs, int lane, const double (&buf)[VPL]) {
-#pragma unroll
-  for (int q = 0; q < VPL; ++q) {
-    const int e = lane + 64 * q;
-    vs[(e / (BND * SCH)) * VLD + e % (BND * SCH)] = buf[q];
-  }
-}
+// xs <- M^{-1} xs (xs: N doubles of LDS) from the stored factor (Vc: the
+// BND x N tiles, Dc: 1/D). Each block product of 16 terms per row is split
+// over the wavefront: lane (a, g) takes row a and terms j = 4g .. 4g+3, and
+// row4_sum adds the four parts, so a block step is four FMAs, two swaps and
+// one LDS exchange per triangular factor. The lane's four tile entries of
+// the next SPF blocks are loaded ahead into registers, so the recurrence
+// does not wait on device memory. Forward tiles are read by rows
+// (V[j*N + 16 I + a], j = 4g+t), backward tiles by columns
+// (V[a*N + 16 I + j]) as the transposed factors need.
+constexpr int SPF = 4;
 
 __device__ __forceinline__ void band_solve(const double* __restrict__ Vc,
-                                           const double* __restrict__ Dc, double* xs, double* vs,
-                                           int N, int lane) {
+                                           const double* __restrict__ Dc, double* xs, int N,
+                                           int lane) {
   const int NB = N / BND;
-  const int a = lane & (BND - 1);
-  const bool wr = lane < BND;
-  double buf[VPL];
-  // forward: chunks I0 = 0, SCH, ...
-  vchunk_load(Vc, N, 0, lane, buf);
-  for (int I0 = 0; I0 < NB; I0 += SCH) {
-    wave_sync();
-    vchunk_store(vs, lane, buf);
-    wave_sync();
-    if (I0 + SCH < NB) vchunk_load(Vc, N, I0 + SCH, lane, buf);
-    const int nbk = (NB - I0 < SCH) ? NB - I0 : SCH;
-    for (int q = 0; q < nbk; ++q) {
-      const int I = I0 + q, i0 = BND * I;
-      double vr[BND];
+  const int a = lane & 15, g = lane >> 4;
+  const bool lead = g == 0;
+  double ring[SPF][4];
+  // forward: y_I = L_I^{-1} (w_I - C_I y_{I-1}), y overwrites w in xs
 #pragma unroll
-      for (int j = 0; j < BND; ++j) vr[j] = vs[j * VLD + BND * q + a];
-      double r0 = xs[i0 + a], r1 = 0.0;
-      if (I > 0) {
+  for (int p = 0; p < SPF; ++p) {
+    const int Ib = p < NB ? p : NB - 1;
 #pragma unroll
-        for (int j = 0; j < BND; j += 2) {
-          r0 = fma((j >= a) ? -vr[j] : 0.0, xs[i0 - BND + j], r0);
-          r1 = fma((j + 1 >= a) ? -vr[j + 1] : 0.0, xs[i0 - BND + j + 1], r1);
+    for (int t = 0; t < 4; ++t) ring[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * Ib + a];
+  }
+  for (int I0 = 0; I0 < NB; I0 += SPF) {
+#pragma unroll
+    for (int p = 0; p < SPF; ++p) {
+      const int I = I0 + p;
+      if (I < NB) {
+        double cn[4], lm[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const double v = ring[p][t];
+          cn[t] = (4 * g + t >= a) ? -v : 0.0;      // C_I (upper triangle, diagonal included)
+          lm[t] = (4 * g + t < a) ? v : 0.0;        // strict lower part of L_I^{-1}
         }
-      }
-      const double r = r0 + r1;
-      wave_sync();
-      if (wr) xs[i0 + a] = r;
-      wave_sync();
-      double y0 = r, y1 = 0.0;
+        const int In = (I + SPF < NB) ? I + SPF : NB - 1;
 #pragma unroll
-      for (int j = 0; j < BND; j += 2) {
-        y0 = fma((j < a) ? vr[j] : 0.0, xs[i0 + j], y0);
-        y1 = fma((j + 1 < a) ? vr[j + 1] : 0.0, xs[i0 + j + 1], y1);
+        for (int t = 0; t < 4; ++t) ring[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * In + a];
+        double p0 = lead ? xs[BND * I + a] : 0.0, p1 = 0.0;
+        if (I > 0) {
+          const double* yp = xs + BND * (I - 1) + 4 * g;
+          p0 = fma(cn[0], yp[0], p0);
+          p1 = fma(cn[1], yp[1], p1);
+          p0 = fma(cn[2], yp[2], p0);
+          p1 = fma(cn[3], yp[3], p1);
+        }
+        const double r = row4_sum(p0 + p1);
+        if (lead) xs[BND * I + a] = r;
+        const double* rp = xs + BND * I + 4 * g;
+        double q0 = lead ? r : 0.0, q1 = 0.0;
+        q0 = fma(lm[0], rp[0], q0);
+        q1 = fma(lm[1], rp[1], q1);
+        q0 = fma(lm[2], rp[2], q0);
+        q1 = fma(lm[3], rp[3], q1);
+        const double yv = row4_sum(q0 + q1);
+        if (lead) xs[BND * I + a] = yv;
       }
-      wave_sync();
-      if (wr) xs[i0 + a] = y0 + y1;
-      wave_sync();
     }
   }
-#pragma unroll 8
-  for (int i = lane; i < N; i += 64) xs[i] *= Dc[i];
-  // backward: chunks from the last one down; vp = tile of block I+1, transposed
-  double vp[BND];
+  wave_sync();
+  // backward: x_I = L_I^{-T} (D_I^{-1} y_I - C_{I+1}' x_{I+1}), x overwrites y
+  double dring[SPF];
 #pragma unroll
-  for (int j = 0; j < BND; ++j) vp[j] = 0.0;
-  const int last0 = ((NB - 1) / SCH) * SCH;
-  vchunk_load(Vc, N, last0, lane, buf);
-  for (int I0 = last0; I0 >= 0; I0 -= SCH) {
-    wave_sync();
-    vchunk_store(vs, lane, buf);
-    wave_sync();
-    if (I0 - SCH >= 0) vchunk_load(Vc, N, I0 - SCH, lane, buf);
-    const int nbk = (NB - I0 < SCH) ? NB - I0 : SCH;
-    for (int q = nbk - 1; q >= 0; --q) {
-      const int I = I0 + q, i0 = BND * I;
-      double vt[BND];                    // vt[j] = V_I[j][a]
+  for (int p = 0; p < SPF; ++p) {
+    const int Ib = (NB - 1 - p >= 0) ? NB - 1 - p : 0;
 #pragma unroll
-      for (int j = 0; j < BND; ++j) vt[j] = vs[a * VLD + BND * q + j];
-      double s0 = xs[i0 + a], s1 = 0.0;
-      if (I + 1 < NB) {
+    for (int t = 0; t < 4; ++t) ring[p][t] = Vc[(int64_t)a * N + BND * Ib + 4 * g + t];
+    dring[p] = Dc[BND * Ib + a];
+  }
+  double vprev[4] = {0.0, 0.0, 0.0, 0.0};     // entries (4g+t, a) of the tile of block I+1
+  for (int T0 = 0; T0 < NB; T0 += SPF) {
 #pragma unroll
-        for (int j = 0; j < BND; j += 2) {
-          s0 = fma((j <= a) ? -vp[j] : 0.0, xs[i0 + BND + j], s0);
-          s1 = fma((j + 1 <= a) ? -vp[j + 1] : 0.0, xs[i0 + BND + j + 1], s1);
+    for (int p = 0; p < SPF; ++p) {
+      const int tt = T0 + p;
+      if (tt < NB) {
+        const int I = NB - 1 - tt;
+        double cn[4], lm[4], vv[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          vv[t] = ring[p][t];
+          cn[t] = (a >= 4 * g + t) ? -vprev[t] : 0.0;   // C_{I+1}' row a
+          lm[t] = (4 * g + t > a) ? vv[t] : 0.0;        // strict upper part of L_I^{-T}
         }
-      }
-      const double sv = s0 + s1;
-      wave_sync();
-      if (wr) xs[i0 + a] = sv;
-      wave_sync();
-      double x0 = sv, x1 = 0.0;
+        const double dv = dring[p];
+        const int In = (I - SPF >= 0) ? I - SPF : 0;
 #pragma unroll
-      for (int j = 0; j < BND; j += 2) {
-        x0 = fma((j > a) ? vt[j] : 0.0, xs[i0 + j], x0);
-        x1 = fma((j + 1 > a) ? vt[j + 1] : 0.0, xs[i0 + j + 1], x1);
-      }
-      wave_sync();
-      if (wr) xs[i0 + a] = x0 + x1;
-      wave_sync();
+        for (int t = 0; t < 4; ++t) ring[p][t] = Vc[(int64_t)a * N + BND * In + 4 * g + t];
+        dring[p] = Dc[BND * In + a];
+        double p0 = lead ? dv * xs[BND * I + a] : 0.0, p1 = 0.0;
+        if (tt > 0) {
+          const double* xp = xs + BND * (I + 1) + 4 * g;
+          p0 = fma(cn[0], xp[0], p0);
+          p1 = fma(cn[1], xp[1], p1);
+          p0 = fma(cn[2], xp[2], p0);
+          p1 = fma(cn[3], xp[3], p1);
+        }
+        const double sv = row4_sum(p0 + p1);
+        if (lead) xs[BND * I + a] = sv;
+        const double* sp = xs + BND * I + 4 * g;
+        double q0 = lead ? sv : 0.0, q1 = 0.0;
+        q0 = fma(lm[0], sp[0], q0);
+        q1 = fma(lm[1], sp[1], q1);
+        q0 = fma(lm[2], sp[2], q0);
+        q1 = fma(lm[3], sp[3], q1);
+        const double xv = row4_sum(q0 + q1);
+        if (lead) xs[BND * I + a] = xv;
 #pragma unroll
-      for (int j = 0; j < BND; ++j) vp[j] = vt[j];
+        for (int t = 0; t < 4; ++t) vprev[t] = vv[t];
+      }
     }
   }
+  wave_sync();
 }
 
-// Columns (wavefronts) per workgroup for order N: the LDS of a workgroup
-// holds one N-vector per column plus small per-column tiles.
+// Columns (wavefronts) per workgroup: the LDS of a workgroup holds one
+// N-vector per column plus `extra` doubles of per-column tiles. Four columns
+// share a workgroup when they fit in 64 KiB, else each has its own.
 constexpr int PTILE = 3 * BND * (BND + 1) + 2 * BND;   // precompute LDS tiles per column
-constexpr int PEXTRA = (VSTAGE > PTILE) ? VSTAGE : PTILE;   // per-column LDS beyond the vector
-static int path_waves(int N) {
-  const size_t per = sizeof(double) * ((size_t)N + PEXTRA);
-  int cw = 4;
-  while (cw > 1 && cw * per > 64 * 1024) cw /= 2;
-  return cw;
+static int path_waves(int N, int extra) {
+  const size_t per = sizeof(double) * ((size_t)N + extra);
+  return 4 * per <= 64 * 1024 ? 4 : 1;
+}
+
+// ---------------------------------------------------- band products B x
+// One workgroup per (row tile of BT rows, column): the tile of x with a halo
+// of BND rows each side is staged in LDS (zero outside 0 .. N-1), and
+// thread i adds the 2 BND + 1 band terms of row i,
+//   (B x)[i] = B[i][i] x[i] + sum_r B[i][i-r] x[i-r] + B[i+r][i] x[i+r],
+// with band loads coalesced across the tile (bg[r*N + j] = B[j+r][j], zero
+// for j + r >= N, so the upper terms past the end vanish by themselves).
+constexpr int BT = 256;
+
+__device__ __forceinline__ double band_tile_row(const double* __restrict__ bg, const double* xt,
+                                                int N, int i, int li) {
+  double y0 = bg[i] * xt[li + BND], y1 = 0.0;
+#pragma unroll
+  for (int r = 1; r <= BND; ++r) {
+    const int il = (i - r >= 0) ? i - r : 0;        // xt is zero above row 0
+    y0 = fma(bg[(int64_t)r * N + il], xt[li + BND - r], y0);
+    y1 = fma(bg[(int64_t)r * N + i], xt[li + BND + r], y1);
+  }
+  return y0 + y1;
+}
+
+__global__ __launch_bounds__(BT) void band_apply_kernel(int N, int C,
+                                                        const double* __restrict__ band,
+                                                        const double* __restrict__ x,
+                                                        double* __restrict__ y) {
+  __shared__ double xt[BT + 2 * BND];
+  const int64_t col = blockIdx.y;
+  const double* bg = band + (int64_t)(col / C) * (BND + 1) * N;
+  const double* xc = x + col * N;
+  const int t0 = blockIdx.x * BT;
+  for (int j = threadIdx.x; j < BT + 2 * BND; j += BT) {
+    const int r = t0 - BND + j;
+    xt[j] = (r >= 0 && r < N) ? xc[r] : 0.0;
+  }
+  __syncthreads();
+  const int i = t0 + threadIdx.x;
+  if (i < N) y[col * N + i] = band_tile_row(bg, xt, N, i, threadIdx.x);
+}
+
+// y = B x for every column of the path arrays (x, y: column-major N-vectors).
+static int band_apply(hipStream_t s, const PathArrays& p, const double* x, double* y) {
+  const int64_t cols = (int64_t)p.G * p.C;
+  hipLaunchKernelGGL(band_apply_kernel, dim3((unsigned)ceil_div(p.N, BT), (unsigned)cols), dim3(BT),
+                     0, s, p.N, p.C, p.band, x, y);
+  KMP_LAUNCH_CHECK();
+  return 0;
 }
 
 // ------------------------------------------------------ per-stage factors
@@ -284,15 +332,15 @@ __global__ __launch_bounds__(256) void precompute_kernel(
     int N, int C, int64_t cols, const int* __restrict__ nv, const double* __restrict__ band,
     const double* __restrict__ cvec, const double* __restrict__ lamv, double kappa,
     double* __restrict__ Vfac, double* __restrict__ Dfac, double* __restrict__ vhat,
-    double* __restrict__ uvec, double* __restrict__ gcoef, const double* __restrict__ ahat,
-    double* __restrict__ abar, double* __restrict__ bmat, const double* __restrict__ beta,
+    double* __restrict__ gcoef, const double* __restrict__ ahat,
+    double* __restrict__ abar, const double* __restrict__ beta,
     double* __restrict__ bbar, double* __restrict__ rmom, int* __restrict__ flag,
     int* __restrict__ iters) {
   extern __shared__ double lds_dyn[];
   const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t gc = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
   if (gc >= cols) return;
-  double* xs = lds_dyn + (int64_t)wv * (N + PEXTRA);
+  double* xs = lds_dyn + (int64_t)wv * (N + PTILE);
   double (*T1)[BND + 1] = reinterpret_cast<double (*)[BND + 1]>(xs + N);
   double (*T2)[BND + 1] = T1 + BND;
   double (*T3)[BND + 1] = T2 + BND;
@@ -411,30 +459,22 @@ __global__ __launch_bounds__(256) void precompute_kernel(
     if (wr) dprv[a] = dcur[a];
     wave_sync();
   }
-  // vhat = M^{-1} c sc, u = B vhat, c'vhat
+  // vhat = M^{-1} c sc and c'vhat; the stage restart abar = ahat (u = B vhat
+  // and B abar follow in band_apply_kernel)
 #pragma unroll 8
   for (int i = lane; i < N; i += 64) xs[i] = cg[i] * sc;
   wave_sync();
-  band_solve(Vc, Dc, xs, xs + N, N, lane);
+  band_solve(Vc, Dc, xs, N, lane);
   double cv = 0.0;
-#pragma unroll 2
-  for (int i = lane; i < N; i += 64) {
-    vhat[base + i] = xs[i];
-    uvec[base + i] = band_row(bg, xs, N, i);
-    cv = fma(cg[i], xs[i], cv);
-  }
-  cv = wave_sum(cv);
-  // stage restart of the accelerated iteration
-  wave_sync();
 #pragma unroll 8
   for (int i = lane; i < N; i += 64) {
-    const double ah = ahat[base + i];
-    xs[i] = ah;
-    abar[base + i] = ah;
+    const double v = xs[i];
+    vhat[base + i] = v;
+    cv = fma(cg[i], v, cv);
   }
-  wave_sync();
-#pragma unroll 2
-  for (int i = lane; i < N; i += 64) bmat[base + i] = band_row(bg, xs, N, i);
+  cv = wave_sum(cv);
+#pragma unroll 8
+  for (int i = lane; i < N; i += 64) abar[base + i] = ahat[base + i];
   if (lane == 0) {
     gcoef[gc] = 1.0 / (2.0 * lam * cv);
     bbar[gc] = beta[gc];
@@ -446,47 +486,62 @@ __global__ __launch_bounds__(256) void precompute_kernel(
 
 int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa) {
   const int64_t cols = (int64_t)p.G * p.C;
-  const int cw = path_waves(p.N);
-  const size_t lds = sizeof(double) * (size_t)cw * (p.N + PEXTRA);
+  const int cw = path_waves(p.N, PTILE);
+  const size_t lds = sizeof(double) * (size_t)cw * (p.N + PTILE);
   KMP_HIP_TRY(hipFuncSetAttribute((const void*)precompute_kernel,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   kc_begin(KMP_KC_PRECOMPUTE, s);
   hipLaunchKernelGGL(precompute_kernel, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, s,
                      p.N, p.C, cols, p.nv, p.band, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
-                     p.uvec, p.gcoef, p.ahat, p.abar, p.bmat, p.beta, p.bbar, p.rmom, p.flag,
-                     p.iters);
+                     p.gcoef, p.ahat, p.abar, p.beta, p.bbar, p.rmom, p.flag, p.iters);
   KMP_LAUNCH_CHECK();
+  int rc;
+  if ((rc = band_apply(s, p, p.vhat, p.uvec)) != 0) return rc;
+  if ((rc = band_apply(s, p, p.ahat, p.bmat)) != 0) return rc;
   // reads the band and c, writes the factor tiles (BND per element), 1/d,
-  // vhat, u, abar, B abar
+  // vhat, abar; then u = B vhat and B abar (read one vector, write one)
   kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 8.0); }),
          over_groups(p, [&](double n) { return 4.0 * BND * BND * n * p.C; }));
   return 0;
 }
 
 // ------------------------------------------------------- the update (K2)
-// One wavefront per column.
-__global__ __launch_bounds__(256) void update_kernel(
+// solve_step_kernel, one wavefront per column:
+//   d0 = 1'z (from the loss epilogue's tile sums), w = zhat + 2 lambda abar
+//   (split-K parts of zhat added in order) into LDS, t = u'w, ||w||;
+//   the KKT test at the extrapolated point; x = M^{-1} w; the step
+//   Da = g (t - d0) vhat + x, a+ = abar - Da, e = a+ - ahat, and the restart
+//   test sum Da'e + Db (b+ - beta) > 0; the momentum r and its coefficient.
+// It writes a+ and e (anew, estep) and the column's scalars; momentum_kernel
+// then forms abar = a+ + coef e, ahat = a+ and B abar over all rows at once.
+// Element loops load UL rows per lane before using them, so a lane keeps UL
+// loads of each stream in flight.
+constexpr int UL = 8;
+
+__global__ __launch_bounds__(256) void solve_step_kernel(
     int N, int C, int64_t cols, int RT, const int* __restrict__ nvv,
-    const double* __restrict__ band, const double* __restrict__ lamv,
-    const double* __restrict__ zpart, int S2, int64_t sP, double* __restrict__ ahat,
-    double* __restrict__ abar, double* __restrict__ bmat, const double* __restrict__ Vfac,
+    const double* __restrict__ lamv, const double* __restrict__ zpart, int S2, int64_t sP,
+    double* __restrict__ ahat, const double* __restrict__ abar, const double* __restrict__ Vfac,
     const double* __restrict__ Dfac, const double* __restrict__ vhat,
     const double* __restrict__ uvec, const double* __restrict__ gcoef,
     const double* __restrict__ partial, double* __restrict__ beta, double* __restrict__ bbar,
     double* __restrict__ rmom, double* __restrict__ kktv, int* __restrict__ flag,
-    int* __restrict__ iters, int* __restrict__ iters_total, double tol, int max_iter,
-    int restart) {
+    int* __restrict__ iters, int* __restrict__ iters_total, double* __restrict__ anew,
+    double* __restrict__ estep, double* __restrict__ coefv, int* __restrict__ moved, double tol,
+    int max_iter, int restart) {
   extern __shared__ double lds_dyn[];
   const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t gc = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
   if (gc >= cols) return;
-  if (flag[gc] != 0) return;
-  double* xs = lds_dyn + (int64_t)wv * (N + PEXTRA);
+  if (flag[gc] != 0) {
+    if (lane == 0) moved[gc] = 0;
+    return;
+  }
+  double* xs = lds_dyn + (int64_t)wv * N;
   const int g = (int)(gc / C), c = (int)(gc % C);
   const int64_t base = gc * (int64_t)N;
   const double lam = lamv[gc];
   const double nvd = (double)nvv[g];
-  const double* bg = band + (int64_t)g * (BND + 1) * N;
   double d0 = 0.0;
   {
     const double* pg = partial + (int64_t)g * RT * C + c;
@@ -494,66 +549,87 @@ __global__ __launch_bounds__(256) void update_kernel(
     d0 = wave_sum(d0);
   }
   double tl = 0.0, n2 = 0.0;
-#pragma unroll 8
-  for (int i = lane; i < N; i += 64) {
-    // split-K parts added in order; parts beyond S2 are not used
-    double zp[kMaxSplitK];
+  for (int i0 = 0; i0 < N; i0 += 64 * UL) {
+    double zs[UL], ab[UL], uv[UL];
 #pragma unroll
-    for (int sk = 0; sk < kMaxSplitK; ++sk) zp[sk] = zpart[(int64_t)sk * sP + base + i];
-    double zh = zp[0];
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      const int64_t ic = base + ((i < N) ? i : N - 1);
+      double z = zpart[ic];
 #pragma unroll
-    for (int sk = 1; sk < kMaxSplitK; ++sk) zh += (sk < S2) ? zp[sk] : 0.0;
-    const double w = fma(2.0 * lam, abar[base + i], zh);
-    xs[i] = w;
-    tl = fma(uvec[base + i], w, tl);
-    n2 = fma(w, w, n2);
+      for (int sk = 1; sk < kMaxSplitK; ++sk) {
+        // parts beyond S2 re-read part 0 (same line) and are not added
+        const double zz = zpart[(sk < S2 ? sk : 0) * sP + ic];
+        z += (sk < S2) ? zz : 0.0;
+      }
+      zs[q] = z;
+      ab[q] = abar[ic];
+      uv[q] = uvec[ic];
+    }
+#pragma unroll
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      if (i < N) {
+        const double w = fma(2.0 * lam, ab[q], zs[q]);
+        xs[i] = w;
+        tl = fma(uv[q], w, tl);
+        n2 = fma(w, w, n2);
+      }
+    }
   }
   const double tsum = wave_sum(tl);
   const double n2sum = wave_sum(n2);
   const double kkt = nvd * fmax(sqrt(n2sum), fabs(d0));
   const double bb = bbar[gc];
   if (!(kkt == kkt) || kkt > 1e300) {          // non-finite
-    if (lane == 0) { flag[gc] = 3; kktv[gc] = kkt; }
+    if (lane == 0) { flag[gc] = 3; kktv[gc] = kkt; moved[gc] = 0; }
     return;
   }
   if (kkt <= tol) {                            // certified at the extrapolated point
 #pragma unroll 8
     for (int i = lane; i < N; i += 64) ahat[base + i] = abar[base + i];
-    if (lane == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; }
+    if (lane == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; moved[gc] = 0; }
     return;
   }
   wave_sync();
-  band_solve(Vfac + gc * (int64_t)BND * N, Dfac + base, xs, xs + N, N, lane);
-  // step, new iterate and the restart test
+  band_solve(Vfac + gc * (int64_t)BND * N, Dfac + base, xs, N, lane);
+  // step and the restart test
   const double gco = gcoef[gc];
   const double sa = gco * (tsum - d0);
   const double db = gco * (d0 - tsum);
   const double bn = bb - db;
   const double bold = beta[gc];
   double rd = 0.0;
-#pragma unroll 8
-  for (int i = lane; i < N; i += 64) {
-    const double da = fma(sa, vhat[base + i], xs[i]);
-    const double an = abar[base + i] - da;
-    rd = fma(da, an - ahat[base + i], rd);
-    xs[i] = an;
+  for (int i0 = 0; i0 < N; i0 += 64 * UL) {
+    double vh[UL], ab[UL], ah[UL];
+#pragma unroll
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      const int64_t ic = base + ((i < N) ? i : N - 1);
+      vh[q] = vhat[ic];
+      ab[q] = abar[ic];
+      ah[q] = ahat[ic];
+    }
+#pragma unroll
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      if (i < N) {
+        const double da = fma(sa, vh[q], xs[i]);
+        const double an = ab[q] - da;
+        const double e = an - ah[q];
+        rd = fma(da, e, rd);
+        anew[base + i] = an;
+        estep[base + i] = e;
+      }
+    }
   }
   rd = wave_sum(rd) + db * (bn - bold);
   const double r = rmom[gc];
   const double rn = (restart && rd > 0.0) ? 1.0 : 0.5 * (1.0 + sqrt(1.0 + 4.0 * r * r));
   const double coef = (rn - 1.0) / (0.5 * (1.0 + sqrt(1.0 + 4.0 * rn * rn)));
-#pragma unroll 8
-  for (int i = lane; i < N; i += 64) {
-    const double an = xs[i];
-    const double nb = fma(coef, an - ahat[base + i], an);
-    ahat[base + i] = an;
-    abar[base + i] = nb;
-    xs[i] = nb;
-  }
-  wave_sync();
-#pragma unroll 2
-  for (int i = lane; i < N; i += 64) bmat[base + i] = band_row(bg, xs, N, i);
   if (lane == 0) {
+    coefv[gc] = coef;
+    moved[gc] = 1;
     beta[gc] = bn;
     bbar[gc] = fma(coef, bn - bold, bn);
     rmom[gc] = rn;
@@ -562,6 +638,33 @@ __global__ __launch_bounds__(256) void update_kernel(
     iters[gc] = it;
     iters_total[gc] += 1;
     if (it >= max_iter) flag[gc] = 2;
+  }
+}
+
+// abar = a+ + coef e, ahat = a+, bmat = B abar for the columns that moved;
+// one workgroup per (row tile, column) as in band_apply_kernel.
+__global__ __launch_bounds__(BT) void momentum_kernel(
+    int N, int C, const double* __restrict__ band, const int* __restrict__ moved,
+    const double* __restrict__ coefv, const double* __restrict__ anew,
+    const double* __restrict__ estep, double* __restrict__ ahat, double* __restrict__ abar,
+    double* __restrict__ bmat) {
+  __shared__ double xt[BT + 2 * BND];
+  const int64_t col = blockIdx.y;
+  if (moved[col] == 0) return;
+  const double coef = coefv[col];
+  const double* bg = band + (int64_t)(col / C) * (BND + 1) * N;
+  const int64_t base = col * N;
+  const int t0 = blockIdx.x * BT;
+  for (int j = threadIdx.x; j < BT + 2 * BND; j += BT) {
+    const int r = t0 - BND + j;
+    xt[j] = (r >= 0 && r < N) ? fma(coef, estep[base + r], anew[base + r]) : 0.0;
+  }
+  __syncthreads();
+  const int i = t0 + threadIdx.x;
+  if (i < N) {
+    ahat[base + i] = anew[base + i];
+    abar[base + i] = xt[threadIdx.x + BND];
+    bmat[base + i] = band_tile_row(bg, xt, N, i, threadIdx.x);
   }
 }
 
@@ -602,20 +705,28 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP)) != 0) return rc;
   kc_end(KMP_KC_GEMM_ZHAT, s, gbytes, gflops);
   const int64_t cols = (int64_t)p.G * p.C;
-  const int cw = path_waves(p.N);
-  const size_t lds = sizeof(double) * (size_t)cw * (p.N + PEXTRA);
-  KMP_HIP_TRY(hipFuncSetAttribute((const void*)update_kernel,
+  const int cw = path_waves(p.N, 0);
+  const size_t lds = sizeof(double) * (size_t)cw * p.N;
+  KMP_HIP_TRY(hipFuncSetAttribute((const void*)solve_step_kernel,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   kc_begin(KMP_KC_UPDATE, s);
-  hipLaunchKernelGGL(update_kernel, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, s, p.N,
-                     p.C, cols, RT, p.nv, p.band, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.bmat,
-                     p.ldl_l, p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom,
-                     p.kkt, p.flag, p.iters, p.iters_total, tol, max_iter, restart);
+  hipLaunchKernelGGL(solve_step_kernel, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, s,
+                     p.N, p.C, cols, RT, p.nv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l,
+                     p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt,
+                     p.flag, p.iters, p.iters_total, p.anew, p.estep, p.coef, p.moved, tol,
+                     max_iter, restart);
   KMP_LAUNCH_CHECK();
-  // per column element: read zhat, abar (twice), ahat (twice), the factor
-  // tile row (BND, twice), 1/d, vhat, u; write ahat, abar, B abar
-  kc_end(KMP_KC_UPDATE, s, over_groups(p, [&](double n) { return 8.0 * (13.0 + 2.0 * BND) * n * p.C; }),
-         over_groups(p, [&](double n) { return (12.0 + 4.0 * BND + 4.0 * BND) * n * p.C; }));
+  hipLaunchKernelGGL(momentum_kernel, dim3((unsigned)ceil_div(p.N, BT), (unsigned)cols), dim3(BT), 0,
+                     s, p.N, p.C, p.band, p.moved, p.coef, p.anew, p.estep, p.ahat, p.abar, p.bmat);
+  KMP_LAUNCH_CHECK();
+  // per column element: the solve reads S2 zhat parts, abar (twice), u, the
+  // factor tiles (BND each, forward and backward), 1/d, vhat, ahat and
+  // writes a+ and e; the momentum pass reads a+ and e and writes ahat, abar
+  // and B abar. Flops: 2 BND multiply-adds per row for the two triangular
+  // sweeps, 2 BND + 1 for the band product, 14 elementwise.
+  kc_end(KMP_KC_UPDATE, s,
+         over_groups(p, [&](double n) { return 8.0 * (S2 + 2.0 * BND + 13.0) * n * p.C; }),
+         over_groups(p, [&](double n) { return (8.0 * BND + 16.0) * n * p.C; }));
   return 0;
 }
 
@@ -635,30 +746,6 @@ int path_count_active(hipStream_t s, const PathArrays& p) {
 }
 
 // --------------------------------------------------------------- finalize
-// Y = B X for every column (B banded per group, band[g][r*N + j] = B[j+r][j],
-// zero for j + r >= N); unconditional loads as in band_row.
-__global__ void band_mult_kernel(int N, int C, int64_t total, const double* __restrict__ band,
-                                 const double* __restrict__ x, double* __restrict__ y) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= total) return;
-  const int64_t col = idx / N;
-  const int i = (int)(idx % N);
-  const int g = (int)(col / C);
-  const double* bg = band + (int64_t)g * (BND + 1) * N;
-  const double* xc = x + col * N;
-  double v = bg[i] * xc[i];
-#pragma unroll
-  for (int r = 1; r <= BND; ++r) {
-    const int il = (i - r >= 0) ? i - r : 0;
-    const int iu = (i + r < N) ? i + r : N - 1;
-    const double bl = bg[(int64_t)r * N + il];
-    const double bu = bg[(int64_t)r * N + i];
-    v = fma((i - r >= 0) ? bl : 0.0, xc[il], v);
-    v = fma(bu, xc[iu], v);
-  }
-  y[idx] = v;
-}
-
 // One workgroup per column: objective on the training points, CV sums on the
 // held-out points, scatter of alpha into the output layout.
 __global__ __launch_bounds__(256) void cv_reduce_kernel(
@@ -730,10 +817,7 @@ int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
   g.C = p.zmat; g.ldc = p.N; g.sC = sNC;
   if ((rc = gemm(s, g, true, true, false)) != 0) return rc;
   // training predictions K_v alpha = Q (B ahat)
-  const int64_t tot = (int64_t)p.G * sNC;
-  hipLaunchKernelGGL(band_mult_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, s, p.N, p.C,
-                     tot, p.band, p.ahat, p.bmat);
-  KMP_LAUNCH_CHECK();
+  if ((rc = band_apply(s, p, p.ahat, p.bmat)) != 0) return rc;
   GemmArgs gt = g;
   gt.B = p.bmat;
   gt.C = fa.ftrain;
