@@ -139,111 +139,230 @@ __global__ __launch_bounds__(PQT) void panel_qr_kernel(double* __restrict__ A, i
   }
 }
 
-// Register-resident variant for panels of at most 32 * RS rows, laid out for
-// the matrix cores: lane l of wave w holds column c = l % 16 of row
-// r = 32 m + 4 w + l / 16 in slot m (m < RS). Every column step needs only
-// the Gram matrix G = sum_{r > i} P[r][:]' P[r][:] of the current panel
-// (16 x 16): with alpha = P[i][i] and sigma = G[i][i],
-//   v_i' P[:, c] = P[i][c] + G[i][c] / (alpha - beta)            (c > i)
-//   V[:, k]' v_i = P[i][k] + G[k][i] / (alpha - beta)            (k < i)
-// the second giving column i of the compact-WY factor T (dlarft):
-// T[0:i, i] = -tau_i T[0:i, 0:i] (V[:, 0:i]' v_i), T[i][i] = tau_i.
-// One v_mfma_f64_16x16x4 per slot accumulates G (A and B operands are the
-// same register: element (c, row) of the slot), then one LDS pass adds the
-// eight waves.
-template <int RS>
-__global__ __launch_bounds__(PQT) void panel_qr_reg_kernel(double* __restrict__ A, int N, int p,
-                                                            double* __restrict__ taus,
-                                                            double* __restrict__ panel,
-                                                            double* __restrict__ tmat) {
-  __shared__ double red[PQW][BB * BB];
-  __shared__ double Gs[BB * BB];
-  __shared__ double rowb[2][BB];         // row i of P before step i (double-buffered)
-  __shared__ double Ts[BB][BB + 1];
-  const int g = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int c = lane & 15, sub = lane >> 4;
-  double* Ag = A + (int64_t)g * N * N;
-  const int m0 = p + BB, mrow = N - m0;
-  double* P = Ag + (int64_t)m0 * N + p;
-  double x[RS];
+// Register-resident panel factorisation with NW wavefronts: lane l of wave
+// w holds column c = l % 16 of row r = 4 NW m + 4 w + l / 16 in slot m
+// (m < RS). Step i needs only row i of the panel's Gram matrix,
+// h_c = sum_{r > i} P[r][i] P[r][c]: every lane multiplies its entry by
+// P[r][i], taken from lane i of its 16-lane row by a DPP row broadcast
+// (row_newbcast takes an immediate lane, so the 16 steps are unrolled), the
+// four rows of the wavefront are added by permlane swaps and the NW
+// wavefronts through LDS. With alpha = P[i][i], sigma = h_i,
+//   v_i' P[:, c] = P[i][c] + h_c / (alpha - beta)            (c > i)
+//   V[:, k]' v_i = P[i][k] + h_k / (alpha - beta) =: z_i[k]   (k < i).
+// One pass over the slots makes the update of step i and the products of
+// step i+1:
+//  - below the diagonal, column k < i keeps u_k = v_k / scale_k (scale_k =
+//    1/(alpha_k - beta_k)), so the update of a slot is one multiply-add,
+//    x_c += A_c P[r][i] with A_c = -tau scale (v_i' P[:, c]) for c > i and
+//    zero otherwise; the scales are applied when the panel is written back
+//    and folded into the z_i;
+//  - P[r][i+1] after step i is P[r][i+1] + A_{i+1} P[r][i], formed from the
+//    broadcast of the old column i+1 and, with CARRY, kept for step i+1
+//    (one broadcast and three multiply-adds per slot and step).
+// The reflectors leave through an LDS tile so that their transposed rows
+// are written contiguously, and the compact-WY factor is formed at the end
+// row by row, T[t][i] = -tau_i sum_{k=t}^{i-1} T[t][k] z_i[k].
+template <int K>
+__device__ __forceinline__ double row_bcast(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_mov_dpp((int)b, 0x150 + K, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), 0x150 + K, 0xf, 0xf, false);
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+
+__device__ __forceinline__ double swap_sum16_b(double v) {
+  const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+  const auto lo = __builtin_amdgcn_permlane16_swap((unsigned)b, (unsigned)b, false, false);
+  const auto hi = __builtin_amdgcn_permlane16_swap((unsigned)(b >> 32), (unsigned)(b >> 32), false, false);
+  return __longlong_as_double((long long)(((unsigned long long)hi[0] << 32) | lo[0])) +
+         __longlong_as_double((long long)(((unsigned long long)hi[1] << 32) | lo[1]));
+}
+__device__ __forceinline__ double swap_sum32_b(double v) {
+  const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+  const auto lo = __builtin_amdgcn_permlane32_swap((unsigned)b, (unsigned)b, false, false);
+  const auto hi = __builtin_amdgcn_permlane32_swap((unsigned)(b >> 32), (unsigned)(b >> 32), false, false);
+  return __longlong_as_double((long long)(((unsigned long long)hi[0] << 32) | lo[0])) +
+         __longlong_as_double((long long)(((unsigned long long)hi[1] << 32) | lo[1]));
+}
+
+constexpr int PVT = 256;          // rows of the reflector staging tile
+
+template <int NW>
+struct PanelLds {
+  double red[NW][BB];      // per-wave partial sums
+  double hs[BB];           // h of the current step
+  double rowb[2][BB];      // row i of the panel before step i (as held: u_k for k < i)
+  double scl[BB];          // scale_k
+  double tau[BB];
+  double z[BB][BB];        // z_i[k], k < i
+  double vt[BB][PVT + 1];  // reflector staging tile
+};
+
+template <int NW>
+struct PanelCtx {
+  PanelLds<NW>* L;
+  int w, c, sub, t;
+};
+
+// h_c over the block from the per-lane partial sums (column c of the lane);
+// leaves h in L.hs.
+template <int NW>
+__device__ __forceinline__ void panel_h_sum(double acc, const PanelCtx<NW>& st) {
+  const double v = swap_sum32_b(swap_sum16_b(acc));
+  if (st.sub == 0) st.L->red[st.w][st.c] = v;
+  __syncthreads();
+  if (st.t < BB) {
+    double s = 0.0;
 #pragma unroll
-  for (int m = 0; m < RS; ++m) {
-    const int r = 32 * m + 4 * w + sub;
-    x[m] = (r < mrow) ? P[(int64_t)r * N + c] : 0.0;
+    for (int q = 0; q < NW; ++q) s += st.L->red[q][st.t];
+    st.L->hs[st.t] = s;
   }
-  for (int e = t; e < BB * (BB + 1); e += PQT) Ts[e / (BB + 1)][e % (BB + 1)] = 0.0;
-  if (w == 0 && sub == 0) rowb[0][c] = x[0];          // row 0: slot 0, wave 0, sub 0
-  typedef double dbl4 __attribute__((ext_vector_type(4)));
-  const int nstep = mrow < BB ? mrow : BB;
-  for (int i = 0; i < nstep; ++i) {
-    // Gram of the rows below i (two independent accumulation chains)
-    dbl4 acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-    for (int m = 0; m < RS; m += 2) {
-      const int r = 32 * m + 4 * w + sub;
-      const double a0 = (r > i && r < mrow) ? x[m] : 0.0;
-      const double a1 = (r + 32 > i && r + 32 < mrow) ? x[m + 1] : 0.0;
-      acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, a0, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, a1, acc1, 0, 0, 0);
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) red[w][mfma_row(lane, q) * BB + mfma_col(lane)] = acc0[q] + acc1[q];
-    __syncthreads();
-    if (t < BB * BB) {
-      double sacc = 0.0;
-#pragma unroll
-      for (int ww = 0; ww < PQW; ++ww) sacc += red[ww][t];
-      Gs[t] = sacc;
-    }
-    __syncthreads();
-    const double* ri = rowb[i & 1];
-    const double alpha = ri[i];
-    const double sigma = Gs[i * BB + i];
+  __syncthreads();
+}
+
+template <int RS, int NW, bool CARRY, int I>
+__device__ __forceinline__ void panel_steps(double (&x)[RS], double (&xi)[RS],
+                                            const PanelCtx<NW>& st) {
+  if constexpr (I < BB) {
+    PanelLds<NW>& L = *st.L;
+    const double* ri = L.rowb[I & 1];
+    const double alpha = ri[I];
+    const double sigma = L.hs[I];
     double tau = 0.0, beta = alpha, scale = 0.0;
     if (sigma > 0.0) {
       beta = -copysign(sqrt(alpha * alpha + sigma), alpha);
       tau = (beta - alpha) / beta;
       scale = 1.0 / (alpha - beta);
     }
-    // column i of T
-    if (t < i) {
-      double sacc = 0.0;
-      for (int k = t; k < i; ++k) sacc = fma(Ts[t][k], fma(scale, Gs[k * BB + i], ri[k]), sacc);
-      Ts[t][i] = -tau * sacc;
+    if (st.t < I) L.z[I][st.t] = L.scl[st.t] * fma(scale, L.hs[st.t], ri[st.t]);
+    if (st.t == 0) {
+      L.scl[I] = scale;
+      L.tau[I] = tau;
     }
-    if (t == i) Ts[i][i] = tau;
-    if (t == 0) taus[(int64_t)g * N + p + i] = tau;
-    const double wc = (c > i) ? fma(scale, Gs[i * BB + c], ri[c]) : 0.0;   // v_i' P[:, c]
+    const int c = st.c;
+    const double tw = -tau * fma(scale, L.hs[c], ri[c]);            // -tau v_I' P[:, c]
+    const double ac = (c > I) ? tw * scale : 0.0;
+    double a1 = 0.0;
+    if constexpr (I + 1 < BB) a1 = -tau * fma(scale, L.hs[I + 1], ri[I + 1]) * scale;
+    double acc = 0.0;
 #pragma unroll
     for (int m = 0; m < RS; ++m) {
-      const int r = 32 * m + 4 * w + sub;
-      const double xi = __shfl(x[m], (lane & 48) + i, 64);   // P[r][i]
-      if (r >= i && r < mrow) {
-        const double vr = (r == i) ? 1.0 : xi * scale;
-        if (c > i) x[m] = fma(-tau * vr, wc, x[m]);
-        else if (c == i) x[m] = (r == i) ? beta : vr;
+      const double xim = CARRY ? xi[m] : row_bcast<I>(x[m]);          // P[r][I]
+      if (m == 0) {
+        const int r = 4 * st.w + st.sub;
+        double xn = x[0];
+        if (r > I) xn = fma(ac, xim, xn);
+        else if (r == I) xn = (c > I) ? xn + tw : ((c == I) ? beta : xn);
+        x[0] = xn;
+        if constexpr (I + 1 < BB) {
+          const double xo = row_bcast<I + 1>(xn);                    // column I+1, updated
+          if (r == I + 1) L.rowb[(I + 1) & 1][c] = xn;
+          acc = fma((r > I + 1) ? xo : 0.0, xn, acc);
+          if constexpr (CARRY) xi[0] = xo;
+        }
+      } else {
+        if constexpr (I + 1 < BB) {
+          const double xo = row_bcast<I + 1>(x[m]);                  // column I+1, old
+          const double xj = fma(a1, xim, xo);
+          x[m] = fma(ac, xim, x[m]);
+          acc = fma(xj, x[m], acc);
+          if constexpr (CARRY) xi[m] = xj;
+        } else {
+          x[m] = fma(ac, xim, x[m]);
+        }
       }
-      if (r == i + 1) rowb[(i + 1) & 1][c] = x[m];
     }
-    // the next step's first barrier orders these LDS writes and reads
+    if constexpr (I + 1 < BB) {
+      panel_h_sum<NW>(acc, st);
+      panel_steps<RS, NW, CARRY, I + 1>(x, xi, st);
+    }
   }
-  __syncthreads();
-  // panel back to A (R on and above the diagonal, v_k below), reflectors
-  // transposed into row p+k of A and rows k, 2BB+k of the panel buffer, T
-  double* Vt = panel + (int64_t)g * 3 * BB * N;
+}
+
+template <int RS, int NW, bool CARRY>
+__global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restrict__ A, int N,
+                                                                int p, double* __restrict__ taus,
+                                                                double* __restrict__ panel,
+                                                                double* __restrict__ tmat) {
+  constexpr int RPS = 4 * NW;                      // rows per slot
+  __shared__ PanelLds<NW> L;
+  const int g = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int c = lane & 15, sub = lane >> 4;
+  double* Ag = A + (int64_t)g * N * N;
+  const int m0 = p + BB, mrow = N - m0;
+  double* P = Ag + (int64_t)m0 * N + p;
+  double x[RS], xi[RS];
 #pragma unroll
   for (int m = 0; m < RS; ++m) {
-    const int r = 32 * m + 4 * w + sub;
-    if (r < mrow) {
-      P[(int64_t)r * N + c] = x[m];
-      const double v = (r == c) ? 1.0 : ((r > c) ? x[m] : 0.0);
-      Ag[(int64_t)(p + c) * N + m0 + r] = v;
-      Vt[(int64_t)c * N + m0 + r] = v;
-      Vt[(int64_t)(2 * BB + c) * N + m0 + r] = v;
-    }
+    const int r = RPS * m + 4 * w + sub;
+    x[m] = (r < mrow) ? P[(int64_t)r * N + c] : 0.0;
   }
-  double* Tg = tmat + (int64_t)g * kWyBlock * kWyBlock;
-  for (int e = t; e < BB * BB; e += PQT) Tg[(e / BB) * kWyBlock + e % BB] = Ts[e / BB][e % BB];
+  if (w == 0 && sub == 0) L.rowb[0][c] = x[0];          // row 0: slot 0, wave 0, sub 0
+  PanelCtx<NW> st{&L, w, c, sub, t};
+  double acc = 0.0;
+#pragma unroll
+  for (int m = 0; m < RS; ++m) {
+    const int r = RPS * m + 4 * w + sub;
+    const double x0 = row_bcast<0>(x[m]);
+    if constexpr (CARRY) xi[m] = x0;
+    acc = fma((r > 0) ? x0 : 0.0, x[m], acc);
+  }
+  panel_h_sum<NW>(acc, st);
+  panel_steps<RS, NW, CARRY, 0>(x, xi, st);
+  __syncthreads();
+  // R (rows < BB, on and above the diagonal) back into the panel; the
+  // reflectors v_k = scale_k u_k (leading 1 at row k) transposed into row
+  // p+k of A and rows k, 2BB+k of the panel buffer, through the LDS tile
+  const double sc = L.scl[c];
+  int rb = 4 * w + sub;               // fresh: keeps the slots' row indices out of registers
+  asm volatile("" : "+v"(rb));
+  if (rb < BB && rb <= c) P[(int64_t)rb * N + c] = x[0];
+  double* Vt = panel + (int64_t)g * 3 * BB * N;
+  constexpr int SPT = PVT / RPS;      // slots per tile
+#pragma unroll
+  for (int m0s = 0; m0s < RS; m0s += SPT) {
+#pragma unroll
+    for (int q = 0; q < SPT && m0s + q < RS; ++q) {
+      const int rl = RPS * q + rb;                   // row within the tile
+      const int r = RPS * (m0s + q) + rb;
+      L.vt[c][rl] = (r == c) ? 1.0 : ((r > c) ? sc * x[m0s + q] : 0.0);
+    }
+    __syncthreads();
+    const int r0 = RPS * m0s;
+    const int nr = (mrow - r0 < PVT) ? mrow - r0 : PVT;
+    for (int e = t; e < BB * PVT; e += 64 * NW) {
+      const int k = e / PVT, rr = e % PVT;
+      if (rr < nr) {
+        const double v = L.vt[k][rr];
+        const int64_t col = (int64_t)m0 + r0 + rr;
+        Ag[(int64_t)(p + k) * N + col] = v;
+        Vt[(int64_t)k * N + col] = v;
+        Vt[(int64_t)(2 * BB + k) * N + col] = v;
+      }
+    }
+    __syncthreads();
+  }
+  // T, row t per thread (z and tau from LDS into registers first)
+  if (t < BB) {
+    double tr[BB];
+#pragma unroll
+    for (int i = 0; i < BB; ++i) {
+      double zi[BB];
+#pragma unroll
+      for (int k = 0; k < i; ++k) zi[k] = L.z[i][k];
+      double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+      for (int k = 0; k < i; ++k) {
+        const double term = (k >= t) ? tr[k] * zi[k] : 0.0;
+        if (k & 1) s1 += term; else s0 += term;
+      }
+      tr[i] = (i > t) ? -L.tau[i] * (s0 + s1) : ((i == t) ? L.tau[t] : 0.0);
+    }
+    double* Tg = tmat + (int64_t)g * kWyBlock * kWyBlock + (int64_t)t * kWyBlock;
+#pragma unroll
+    for (int i = 0; i < BB; ++i) Tg[i] = tr[i];
+    taus[(int64_t)g * N + p + t] = L.tau[t];
+  }
 }
 
 // C[i][j] = sum_k A[i*lda + k] B[j*ldb + k] for M, Nc <= 64 and long K (per
@@ -369,15 +488,21 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     const int m0 = p + BB, mrow = N - m0;
     kc_begin(KMP_KC_TRI_COL, s);
     const int rs = (int)ceil_div(mrow, 32);
-    const bool reg = rs <= 64;
-#define KMP_PQR(RSV)                                                                            \
-  hipLaunchKernelGGL(panel_qr_reg_kernel<RSV>, dim3(G), dim3(PQT), 0, s, wk.A, N, p, wk.tau, \
-                     wk.panel, wk.tmat)
-    if (rs <= 8) KMP_PQR(8);
-    else if (rs <= 16) KMP_PQR(16);
-    else if (rs <= 32) KMP_PQR(32);
-    else if (rs <= 48) KMP_PQR(48);
-    else if (rs <= 64) KMP_PQR(64);
+    const bool reg = rs <= 64;     // mrow <= 2048
+#define KMP_PQR(RSV, NWV, CV)                                                                   \
+  hipLaunchKernelGGL((panel_qr_vec_kernel<RSV, NWV, CV>), dim3(G), dim3(64 * NWV), 0, s, wk.A, N, \
+                     p, wk.tau, wk.panel, wk.tmat)
+    // 8 wavefronts (32 rows per slot) up to 1280 rows, then 16 (64 rows per
+    // slot): the unrolled steps stay within the instruction cache and the
+    // slots within the registers
+    const int rs16 = (int)ceil_div(mrow, 64);
+    if (rs <= 8) KMP_PQR(8, 8, true);
+    else if (rs <= 16) KMP_PQR(16, 8, true);
+    else if (rs <= 24) KMP_PQR(24, 8, true);
+    else if (rs <= 32) KMP_PQR(32, 8, true);
+    else if (rs <= 40) KMP_PQR(40, 8, true);
+    else if (rs16 <= 24) KMP_PQR(24, 16, false);
+    else if (rs16 <= 32) KMP_PQR(32, 16, false);
 #undef KMP_PQR
     else
       hipLaunchKernelGGL(panel_qr_kernel, dim3(G), dim3(PQT), 0, s, wk.A, N, p, wk.tau, wk.panel);
