@@ -365,6 +365,182 @@ __global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restric
   }
 }
 
+// X' = Y' A22 and the partial products of M2 = V'X for one panel (A22 =
+// A[m0:, m0:], Y' = T'V' stored transposed, Yt[k][i] = Yt[16 k + i], m x 16).
+// One workgroup per 16 columns j0 .. j0+15 of X' and matrix: wave w
+// accumulates the 16-row chunks q = w, w+4, ... on the matrix cores (A
+// operand Yt[k][i], one 512-byte piece per load; B operand A22[k][j],
+// 128-byte row pieces), the four partial tiles are added in LDS,
+// X' goes to rows BB .. 2BB-1 of the panel buffer, and the workgroup's part
+// of M2, sum_{j in block} V'[a][j] X'[b][j], to part[(g NJ + block)*256].
+constexpr int XUQ = 4;            // 16-row chunks per wave and iteration
+typedef double xdbl4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__ A, int N, int m0,
+                                                       const double* __restrict__ ybuf,
+                                                       double* __restrict__ panel,
+                                                       double* __restrict__ part, int NJ) {
+  __shared__ double red[4][4][64];
+  __shared__ double Xs[BB][BB + 1];
+  const int jb = blockIdx.x, g = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int m = N - m0, j0 = BB * jb, nch = m / BB;
+  const double* Ag = A + (int64_t)g * N * N + (int64_t)m0 * N + m0;
+  const double* Yg = ybuf + (int64_t)g * kWyBlock * N;
+  double* Pg = panel + (int64_t)g * 3 * BB * N + m0;
+  const int i = lane & 15, kq = lane >> 4;
+  const double* ya = Yg + (int64_t)kq * BB + i;
+  const double* bb = Ag + (int64_t)kq * N + j0 + i;
+  xdbl4 acc = {0.0, 0.0, 0.0, 0.0};
+  for (int q = w; q < nch; q += 4 * XUQ) {
+    double av[XUQ][4], bv[XUQ][4];
+#pragma unroll
+    for (int u = 0; u < XUQ; ++u) {
+      const int qq = (q + 4 * u < nch) ? q + 4 * u : q;      // clamped: not accumulated
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4) {
+        const int k = BB * qq + 4 * s4;
+        av[u][s4] = ya[(int64_t)k * BB];
+        bv[u][s4] = bb[(int64_t)k * N];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < XUQ; ++u) {
+      const bool ok = q + 4 * u < nch;
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4)
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(ok ? av[u][s4] : 0.0, bv[u][s4], acc, 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) red[w][r][lane] = acc[r];
+  __syncthreads();
+  {
+    const int r = t >> 6, l = t & 63;
+    const double v = (red[0][r][l] + red[1][r][l]) + (red[2][r][l] + red[3][r][l]);
+    const int b = 4 * r + (l >> 4), j = l & 15;
+    Xs[b][j] = v;
+    Pg[(int64_t)(BB + b) * N + j0 + j] = v;
+  }
+  __syncthreads();
+  {
+    const int a = t >> 4, b = t & 15;
+    const double* va = Pg + (int64_t)a * N + j0;
+    double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+    for (int j = 0; j < BB; j += 2) {
+      s0 = fma(va[j], Xs[b][j], s0);
+      s1 = fma(va[j + 1], Xs[b][j + 1], s1);
+    }
+    part[((int64_t)g * NJ + jb) * 256 + t] = s0 + s1;
+  }
+}
+
+// S = T'M2 with M2 = V'X summed in order from the block products in part;
+// one workgroup per matrix, S into sbuf (16 x 16, row-major, stride sS).
+__global__ __launch_bounds__(256) void panel_s_kernel(int N, int m0, const double* __restrict__ part,
+                                                       int NJ, const double* __restrict__ tmat,
+                                                       double* __restrict__ sbuf, int64_t sS) {
+  __shared__ double M2s[BB][BB + 1];
+  const int g = blockIdx.x, t = threadIdx.x;
+  const int nch = (N - m0) / BB;
+  {
+    const double* pp = part + (int64_t)g * NJ * 256 + t;
+    double s = 0.0;
+#pragma unroll 8
+    for (int q = 0; q < nch; ++q) s += pp[(int64_t)q * 256];
+    M2s[t >> 4][t & 15] = s;
+  }
+  __syncthreads();
+  const int a = t >> 4, b = t & 15;
+  const double* Tg = tmat + (int64_t)g * kWyBlock * kWyBlock;
+  double s = 0.0;
+#pragma unroll
+  for (int q = 0; q < BB; ++q) s = fma(Tg[q * kWyBlock + a], M2s[q][b], s);
+  sbuf[(int64_t)g * sS + t] = s;
+}
+
+// W' = X' - 1/2 S'V' in place of X' in rows BB .. 2BB-1 of the panel
+// buffer; one workgroup per 64 columns and matrix.
+__global__ __launch_bounds__(256) void panel_w_kernel(int N, int m0, const double* __restrict__ sbuf,
+                                                       int64_t sS, double* __restrict__ panel) {
+  __shared__ double Ss[BB][BB + 1];
+  const int jb = blockIdx.x, g = blockIdx.y, t = threadIdx.x;
+  const int m = N - m0;
+  Ss[t >> 4][t & 15] = sbuf[(int64_t)g * sS + t];
+  __syncthreads();
+  double* Pg = panel + (int64_t)g * 3 * BB * N + m0;
+  for (int e = t; e < BB * 64; e += 256) {
+    const int ii = e >> 6, j = 64 * jb + (e & 63);
+    if (j < m) {
+      double s = 0.0;
+#pragma unroll
+      for (int q = 0; q < BB; ++q) s = fma(Ss[q][ii], Pg[(int64_t)q * N + j], s);
+      double* xw = Pg + (int64_t)(BB + ii) * N + j;
+      *xw = fma(-0.5, s, *xw);
+    }
+  }
+}
+
+// Two-sided update of the trailing matrix, A22 <- A22 - V W' - W V' =
+// A22 - P1' P2 with P1 = [V; W] and P2 = [W; V] (rows 0 .. 2BB-1 and
+// BB .. 3BB-1 of the panel buffer, K = 2 BB = 32). One workgroup per 64 x 64
+// tile; wave w updates the 32 x 32 piece at (32 (w&1), 32 (w>>1)) as 2 x 2
+// MFMA blocks: the piece of A22 is loaded straight into the accumulators
+// (register r of a block holds row 4r + l/16, column l%16: 128-byte row
+// pieces), the 2 x 8 operand values of each side are loaded up front, and
+// 32 products with the A operand negated follow. m is a multiple of 16, so
+// each 16 x 16 block is wholly inside or outside A22: outside blocks load
+// from clamped addresses and are not stored.
+__global__ __launch_bounds__(256) void panel_update_kernel(double* __restrict__ A, int N, int m0,
+                                                            const double* __restrict__ panel) {
+  const int g = blockIdx.z, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int m = N - m0;
+  const int i0 = 64 * blockIdx.x + 32 * (w & 1), j0 = 64 * blockIdx.y + 32 * (w >> 1);
+  double* Cg = A + (int64_t)g * N * N + (int64_t)m0 * N + m0;
+  const double* P1 = panel + (int64_t)g * 3 * BB * N + m0;
+  const double* P2 = P1 + (int64_t)BB * N;
+  const int li = lane & 15, lk = lane >> 4;
+  bool vi[2], vj[2];
+  int ib[2], jb[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    vi[b] = i0 + 16 * b < m;
+    vj[b] = j0 + 16 * b < m;
+    ib[b] = vi[b] ? i0 + 16 * b : 0;
+    jb[b] = vj[b] ? j0 + 16 * b : 0;
+  }
+  double av[2][8], bv[2][8];
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int s8 = 0; s8 < 8; ++s8) {
+      av[b][s8] = -P1[(int64_t)(4 * s8 + lk) * N + ib[b] + li];
+      bv[b][s8] = P2[(int64_t)(4 * s8 + lk) * N + jb[b] + li];
+    }
+  xdbl4 acc[2][2];
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[bi][bj][r] = Cg[(int64_t)(ib[bi] + 4 * r + lk) * N + jb[bj] + li];
+#pragma unroll
+  for (int s8 = 0; s8 < 8; ++s8)
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj)
+        acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[bi][s8], bv[bj][s8], acc[bi][bj], 0, 0, 0);
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+      if (vi[bi] && vj[bj]) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Cg[(int64_t)(ib[bi] + 4 * r + lk) * N + jb[bj] + li] = acc[bi][bj][r];
+      }
+}
+
 // C[i][j] = sum_k A[i*lda + k] B[j*ldb + k] for M, Nc <= 64 and long K (per
 // matrix b: A + b*sA, B + b*sB, C + b*sC, ld ldc). Every block takes one
 // 16 x 16 output tile over one chunk of TSK indices (one output per thread);
@@ -525,47 +701,33 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     g1.M = BB; g1.N = mrow; g1.K = BB; g1.batch = G;
     g1.A = wk.tmat; g1.lda = kWyBlock; g1.sA = (int64_t)kWyBlock * kWyBlock;
     g1.B = wk.panel + m0; g1.ldb = N; g1.sB = sP;
-    g1.C = wk.xbuf + m0; g1.ldc = N; g1.sC = (int64_t)kWyBlock * N;
-    if ((rc = gemm(s, g1, false, false, true)) != 0) return rc;
-    // X' = Y' A22   (BB x mrow, rows BB .. 2BB-1 of the panel buffer)
-    GemmArgs g2;
-    g2.M = BB; g2.N = mrow; g2.K = mrow; g2.batch = G;
-    g2.A = wk.xbuf + m0; g2.lda = N; g2.sA = (int64_t)kWyBlock * N;
-    g2.B = wk.A + (int64_t)m0 * N + m0; g2.ldb = N; g2.sB = (int64_t)N * N;
-    g2.C = wk.panel + (int64_t)BB * N + m0; g2.ldc = N; g2.sC = sP;
-    if ((rc = gemm(s, g2, true, false, true)) != 0) return rc;
-    // M2 = V' X  (BB x BB, in gram)
-    if ((rc = ts_gram(s, BB, BB, mrow, G, wk.panel + m0, N, sP, wk.panel + (int64_t)BB * N + m0, N,
-                      sP, wk.gram, kWyBlock, (int64_t)kWyBlock * kWyBlock, wk.part)) != 0)
-      return rc;
-    // S = T' M2  (BB x BB, in ybuf)
-    GemmArgs g4;
-    g4.M = BB; g4.N = BB; g4.K = BB; g4.batch = G;
-    g4.A = wk.tmat; g4.lda = kWyBlock; g4.sA = (int64_t)kWyBlock * kWyBlock;
-    g4.B = wk.gram; g4.ldb = kWyBlock; g4.sB = (int64_t)kWyBlock * kWyBlock;
-    g4.C = wk.ybuf; g4.ldc = kWyBlock; g4.sC = (int64_t)kWyBlock * N;
-    if ((rc = gemm(s, g4, false, false, true)) != 0) return rc;
-    // W' = X' - 1/2 S' V'
-    GemmArgs g5;
-    g5.M = BB; g5.N = mrow; g5.K = BB; g5.batch = G;
-    g5.A = wk.ybuf; g5.lda = kWyBlock; g5.sA = (int64_t)kWyBlock * N;
-    g5.B = wk.panel + m0; g5.ldb = N; g5.sB = sP;
-    g5.C = wk.panel + (int64_t)BB * N + m0; g5.ldc = N; g5.sC = sP;
-    g5.alpha = -0.5; g5.beta = 1.0;
-    if ((rc = gemm(s, g5, false, false, true)) != 0) return rc;
+    g1.C = wk.xbuf; g1.ldc = BB; g1.sC = (int64_t)kWyBlock * N;     // transposed, m x 16
+    if ((rc = gemm(s, g1, false, false, false)) != 0) return rc;
+    // X' = Y' A22 and the block products of M2 = V'X, then
+    // W' = X' - 1/2 (T'M2)' V' in place of X'
+    {
+      const int NJ = (int)ceil_div(N, BB);
+      hipLaunchKernelGGL(panel_x_kernel, dim3((unsigned)(mrow / BB), (unsigned)G), dim3(256), 0, s,
+                         wk.A, N, m0, wk.xbuf, wk.panel, wk.part, NJ);
+      KMP_LAUNCH_CHECK();
+      const int64_t sS = (int64_t)kWyBlock * N;
+      hipLaunchKernelGGL(panel_s_kernel, dim3((unsigned)G), dim3(256), 0, s, N, m0, wk.part, NJ,
+                         wk.tmat, wk.ybuf, sS);
+      KMP_LAUNCH_CHECK();
+      hipLaunchKernelGGL(panel_w_kernel, dim3((unsigned)ceil_div(mrow, 64), (unsigned)G), dim3(256),
+                         0, s, N, m0, wk.ybuf, sS, wk.panel);
+      KMP_LAUNCH_CHECK();
+    }
     kc_end(KMP_KC_TRI_SYMV, s, over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 8.0 * m * m; }),
            over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 2.0 * BB * m * m; }));
-    // A22 -= V W' + W V'  as one GEMM with K = 2 BB over the [V; W; V] rows
-    GemmArgs ga;
-    ga.M = mrow; ga.N = mrow; ga.K = 2 * BB; ga.batch = G;
-    ga.A = wk.panel + m0; ga.lda = N; ga.sA = sP;
-    ga.B = wk.panel + (int64_t)BB * N + m0; ga.ldb = N; ga.sB = sP;
-    ga.C = wk.A + (int64_t)m0 * N + m0; ga.ldc = N; ga.sC = (int64_t)N * N;
-    ga.alpha = -1.0; ga.beta = 1.0;
+    // A22 -= V W' + W V' (K = 2 BB over the [V; W; V] rows)
     kc_begin(KMP_KC_TRI_SYR2K, s);
-    if ((rc = gemm(s, ga, false, false, true)) != 0) return rc;
+    hipLaunchKernelGGL(panel_update_kernel,
+                       dim3((unsigned)ceil_div(mrow, 64), (unsigned)ceil_div(mrow, 64), (unsigned)G),
+                       dim3(256), 0, s, wk.A, N, m0, wk.panel);
+    KMP_LAUNCH_CHECK();
     kc_end(KMP_KC_TRI_SYR2K, s, over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 16.0 * m * m; }),
            over_groups(wk, [&](double n) {
