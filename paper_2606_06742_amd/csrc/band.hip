@@ -481,24 +481,30 @@ __global__ __launch_bounds__(256) void panel_w_kernel(int N, int m0, const doubl
   }
 }
 
-// Two-sided update of the trailing matrix, A22 <- A22 - V W' - W V' =
-// A22 - P1' P2 with P1 = [V; W] and P2 = [W; V] (rows 0 .. 2BB-1 and
-// BB .. 3BB-1 of the panel buffer, K = 2 BB = 32). One workgroup per 64 x 64
+// Rank-K update C <- C - P1' P2 of an m x m block (C[i][j] = C[i*ldc + j],
+// P1[k][i] = P1[k*ld1 + i], P2[k][j] = P2[k*ld2 + j], K = 32 KC; matrix g at
+// C + g sC, P1 + g s1, P2 + g s2), for the two-sided update
+// of the trailing matrix (P1 = [V; W], P2 = [W; V], K = 2 BB) and the
+// accumulation of Q (P1 = V, P2 = T V Q, K = 64). One workgroup per 64 x 64
 // tile; wave w updates the 32 x 32 piece at (32 (w&1), 32 (w>>1)) as 2 x 2
-// MFMA blocks: the piece of A22 is loaded straight into the accumulators
+// MFMA blocks: the piece of C is loaded straight into the accumulators
 // (register r of a block holds row 4r + l/16, column l%16: 128-byte row
-// pieces), the 2 x 8 operand values of each side are loaded up front, and
-// 32 products with the A operand negated follow. m is a multiple of 16, so
-// each 16 x 16 block is wholly inside or outside A22: outside blocks load
-// from clamped addresses and are not stored.
-__global__ __launch_bounds__(256) void panel_update_kernel(double* __restrict__ A, int N, int m0,
-                                                            const double* __restrict__ panel) {
+// pieces), then per 32 k the 2 x 8 operand values of each side are loaded
+// together and 32 products with the A operand negated follow. m is a
+// multiple of 16, so each 16 x 16 block is wholly inside or outside C:
+// outside blocks load from clamped addresses and are not stored.
+template <int KC>
+__global__ __launch_bounds__(256) void rank_update_kernel(double* __restrict__ C, int64_t ldc,
+                                                           int64_t sC, int m,
+                                                           const double* __restrict__ P1,
+                                                           int64_t ld1, int64_t s1,
+                                                           const double* __restrict__ P2,
+                                                           int64_t ld2, int64_t s2) {
   const int g = blockIdx.z, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int m = N - m0;
   const int i0 = 64 * blockIdx.x + 32 * (w & 1), j0 = 64 * blockIdx.y + 32 * (w >> 1);
-  double* Cg = A + (int64_t)g * N * N + (int64_t)m0 * N + m0;
-  const double* P1 = panel + (int64_t)g * 3 * BB * N + m0;
-  const double* P2 = P1 + (int64_t)BB * N;
+  double* Cg = C + (int64_t)g * sC;
+  const double* A1 = P1 + (int64_t)g * s1;
+  const double* A2 = P2 + (int64_t)g * s2;
   const int li = lane & 15, lk = lane >> 4;
   bool vi[2], vj[2];
   int ib[2], jb[2];
@@ -509,35 +515,39 @@ __global__ __launch_bounds__(256) void panel_update_kernel(double* __restrict__ 
     ib[b] = vi[b] ? i0 + 16 * b : 0;
     jb[b] = vj[b] ? j0 + 16 * b : 0;
   }
-  double av[2][8], bv[2][8];
-#pragma unroll
-  for (int b = 0; b < 2; ++b)
-#pragma unroll
-    for (int s8 = 0; s8 < 8; ++s8) {
-      av[b][s8] = -P1[(int64_t)(4 * s8 + lk) * N + ib[b] + li];
-      bv[b][s8] = P2[(int64_t)(4 * s8 + lk) * N + jb[b] + li];
-    }
   xdbl4 acc[2][2];
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
     for (int bj = 0; bj < 2; ++bj)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) acc[bi][bj][r] = Cg[(int64_t)(ib[bi] + 4 * r + lk) * N + jb[bj] + li];
+      for (int r = 0; r < 4; ++r) acc[bi][bj][r] = Cg[(int64_t)(ib[bi] + 4 * r + lk) * ldc + jb[bj] + li];
 #pragma unroll
-  for (int s8 = 0; s8 < 8; ++s8)
+  for (int kc = 0; kc < KC; ++kc) {
+    double av[2][8], bv[2][8];
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
+    for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int bj = 0; bj < 2; ++bj)
-        acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[bi][s8], bv[bj][s8], acc[bi][bj], 0, 0, 0);
+      for (int s8 = 0; s8 < 8; ++s8) {
+        const int64_t k = 32 * kc + 4 * s8 + lk;
+        av[b][s8] = -A1[k * ld1 + ib[b] + li];
+        bv[b][s8] = A2[k * ld2 + jb[b] + li];
+      }
+#pragma unroll
+    for (int s8 = 0; s8 < 8; ++s8)
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+          acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[bi][s8], bv[bj][s8], acc[bi][bj], 0, 0, 0);
+  }
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
     for (int bj = 0; bj < 2; ++bj)
       if (vi[bi] && vj[bj]) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) Cg[(int64_t)(ib[bi] + 4 * r + lk) * N + jb[bj] + li] = acc[bi][bj][r];
+        for (int r = 0; r < 4; ++r) Cg[(int64_t)(ib[bi] + 4 * r + lk) * ldc + jb[bj] + li] = acc[bi][bj][r];
       }
 }
 
@@ -724,9 +734,11 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
              const double m = std::max(0.0, n - m0); return 2.0 * BB * m * m; }));
     // A22 -= V W' + W V' (K = 2 BB over the [V; W; V] rows)
     kc_begin(KMP_KC_TRI_SYR2K, s);
-    hipLaunchKernelGGL(panel_update_kernel,
+    hipLaunchKernelGGL(rank_update_kernel<1>,
                        dim3((unsigned)ceil_div(mrow, 64), (unsigned)ceil_div(mrow, 64), (unsigned)G),
-                       dim3(256), 0, s, wk.A, N, m0, wk.panel);
+                       dim3(256), 0, s, wk.A + (int64_t)m0 * N + m0, (int64_t)N, (int64_t)N * N, mrow,
+                       (const double*)(wk.panel + m0), (int64_t)N, sP,
+                       (const double*)(wk.panel + (int64_t)BB * N + m0), (int64_t)N, sP);
     KMP_LAUNCH_CHECK();
     kc_end(KMP_KC_TRI_SYR2K, s, over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 16.0 * m * m; }),
@@ -774,13 +786,25 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     h2.B = wk.xbuf; h2.ldb = N; h2.sB = (int64_t)kWyBlock * N;
     h2.C = wk.ybuf; h2.ldc = N; h2.sC = (int64_t)kWyBlock * N;
     if ((rc = gemm(s, h2, true, false, true)) != 0) return rc;
-    GemmArgs h3;   // Q[q+BB:, q+BB:] -= V' Y
-    h3.M = m; h3.N = m; h3.K = kb; h3.batch = G;
-    h3.A = wk.A + (int64_t)q * N + q + BB; h3.lda = N; h3.sA = (int64_t)N * N;
-    h3.B = wk.ybuf; h3.ldb = N; h3.sB = (int64_t)kWyBlock * N;
-    h3.C = wk.Q + (int64_t)(q + BB) * N + q + BB; h3.ldc = N; h3.sC = (int64_t)N * N;
-    h3.alpha = -1.0; h3.beta = 1.0;
-    if ((rc = gemm(s, h3, false, false, true)) != 0) return rc;
+    // Q[q+BB:, q+BB:] -= V' Y  (K = kb = 64; the last block may be shorter
+    // only when N - BB is not a multiple of 64, then the generic product)
+    if (kb == kWyBlock) {
+      hipLaunchKernelGGL(rank_update_kernel<2>,
+                         dim3((unsigned)ceil_div(m, 64), (unsigned)ceil_div(m, 64), (unsigned)G),
+                         dim3(256), 0, s, wk.Q + (int64_t)(q + BB) * N + q + BB, (int64_t)N,
+                         (int64_t)N * N, m, (const double*)(wk.A + (int64_t)q * N + q + BB),
+                         (int64_t)N, (int64_t)N * N, (const double*)wk.ybuf, (int64_t)N,
+                         (int64_t)kWyBlock * N);
+      KMP_LAUNCH_CHECK();
+    } else {
+      GemmArgs h3;
+      h3.M = m; h3.N = m; h3.K = kb; h3.batch = G;
+      h3.A = wk.A + (int64_t)q * N + q + BB; h3.lda = N; h3.sA = (int64_t)N * N;
+      h3.B = wk.ybuf; h3.ldb = N; h3.sB = (int64_t)kWyBlock * N;
+      h3.C = wk.Q + (int64_t)(q + BB) * N + q + BB; h3.ldc = N; h3.sC = (int64_t)N * N;
+      h3.alpha = -1.0; h3.beta = 1.0;
+      if ((rc = gemm(s, h3, false, false, true)) != 0) return rc;
+    }
     kc_end(KMP_KC_QFORM, s, over_groups(wk, [&](double n) {
              const double mm = std::max(0.0, n - q - BB); return 24.0 * mm * mm; }),
            over_groups(wk, [&](double n) {
