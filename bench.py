@@ -112,7 +112,7 @@ def cpu_baseline(inp, w, ncells):
 
 # Matrix-core kernels are priced against the fp64 MFMA peak, the others
 # against HBM bandwidth.
-MFMA_CLASSES = ("gemm_f", "gemm_zhat", "tri_syr2k", "q_form", "gram")
+MFMA_CLASSES = ("gemm_f", "gemm_zhat", "panel_wy", "trail_update", "q_form", "gram")
 
 
 def roofline(kt, workload):

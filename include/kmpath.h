@@ -62,14 +62,14 @@ extern "C" {
 /* Kernel classes timed with HIP events when their bit is set in
  * kmp_path_spec.timing_mask (1 << class). */
 #define KMP_KC_GRAM 0         /* a1 Gram + fold gather                         */
-#define KMP_KC_TRI_COL 1      /* a2 per-column Householder step (one block/fold) */
-#define KMP_KC_TRI_SYMV 2     /* a2 trailing-matrix product of each step       */
-#define KMP_KC_TRI_SYR2K 3    /* a2 rank-2nb trailing update per panel (MFMA)  */
+#define KMP_KC_PANEL 1        /* a2 Householder QR of a band-reduction panel    */
+#define KMP_KC_PANEL_WY 2     /* a2 panel products Y = VT, X = A22 Y, W         */
+#define KMP_KC_TRAIL 3        /* a2 trailing update A22 -= V W' + W V' (MFMA)  */
 #define KMP_KC_QFORM 4        /* a2 compact-WY accumulation of Q (MFMA)        */
 #define KMP_KC_PRECOMPUTE 5   /* a3 per-stage column factors                   */
-#define KMP_KC_GEMM_F 6       /* a4+a5 f = Q (T abar) with the loss epilogue   */
+#define KMP_KC_GEMM_F 6       /* a4+a5 f = Q (B abar) with the loss epilogue   */
 #define KMP_KC_GEMM_ZHAT 7    /* a6 zhat = Q' z                                */
-#define KMP_KC_UPDATE 8       /* a7 spectral update, KKT, restart              */
+#define KMP_KC_UPDATE 8       /* a7 banded solve, step, KKT, restart, B abar   */
 #define KMP_KC_FINALIZE 9     /* a10                                           */
 #define KMP_NKC 10
 
@@ -171,7 +171,8 @@ int kmp_rbf_gram(void* stream, const double* X, int64_t n, int64_t d, int64_t ld
                  const int32_t* rows, int64_t m, const int32_t* cols, int64_t p,
                  const double* sigmas, int32_t S, double* out, int64_t ld_out);
 
-/* a2 on its own: G symmetric N x N matrices A (DEVICE, row-major, packed,
+/* One-stage alternative to a2 (kmp_fit_path uses kmp_band_reduce): G
+ * symmetric N x N matrices A (DEVICE, row-major, packed,
  * matrix g at A + g*N*N; destroyed) are reduced to A_g = Q_g T_g Q_g' with
  * Q_g orthogonal (DEVICE out, same layout) and T_g symmetric tridiagonal
  * with diagonal diag[g*N + i] and off-diagonal off[g*N + i] = T[i+1][i]

@@ -672,7 +672,7 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
   KMP_HIP_TRY(hipMemsetAsync(wk.tau, 0, sizeof(double) * (size_t)G * N, s));
   for (int p = 0; p + BB < N; p += BB) {
     const int m0 = p + BB, mrow = N - m0;
-    kc_begin(KMP_KC_TRI_COL, s);
+    kc_begin(KMP_KC_PANEL, s);
     const int rs = (int)ceil_div(mrow, 32);
     const bool reg = rs <= 64;     // mrow <= 2048
 #define KMP_PQR(RSV, NWV, CV)                                                                   \
@@ -694,10 +694,10 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
       hipLaunchKernelGGL(panel_qr_kernel, dim3(G), dim3(PQT), 0, s, wk.A, N, p, wk.tau, wk.panel);
     KMP_LAUNCH_CHECK();
     // panel read twice per column step and written once (algorithmic: once)
-    kc_end(KMP_KC_TRI_COL, s, over_groups(wk, [&](double n) {
+    kc_end(KMP_KC_PANEL, s, over_groups(wk, [&](double n) {
              return 16.0 * std::max(0.0, n - m0) * BB; }),
            over_groups(wk, [&](double n) { return 4.0 * std::max(0.0, n - m0) * BB * BB; }));
-    kc_begin(KMP_KC_TRI_SYMV, s);
+    kc_begin(KMP_KC_PANEL_WY, s);
     // T of the panel's block reflector (formed by the register kernel):
     // otherwise the Gram of V, then dlarft
     if (!reg) {
@@ -728,19 +728,19 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
                          0, s, N, m0, wk.ybuf, sS, wk.panel);
       KMP_LAUNCH_CHECK();
     }
-    kc_end(KMP_KC_TRI_SYMV, s, over_groups(wk, [&](double n) {
+    kc_end(KMP_KC_PANEL_WY, s, over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 8.0 * m * m; }),
            over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 2.0 * BB * m * m; }));
     // A22 -= V W' + W V' (K = 2 BB over the [V; W; V] rows)
-    kc_begin(KMP_KC_TRI_SYR2K, s);
+    kc_begin(KMP_KC_TRAIL, s);
     hipLaunchKernelGGL(rank_update_kernel<1>,
                        dim3((unsigned)ceil_div(mrow, 64), (unsigned)ceil_div(mrow, 64), (unsigned)G),
                        dim3(256), 0, s, wk.A + (int64_t)m0 * N + m0, (int64_t)N, (int64_t)N * N, mrow,
                        (const double*)(wk.panel + m0), (int64_t)N, sP,
                        (const double*)(wk.panel + (int64_t)BB * N + m0), (int64_t)N, sP);
     KMP_LAUNCH_CHECK();
-    kc_end(KMP_KC_TRI_SYR2K, s, over_groups(wk, [&](double n) {
+    kc_end(KMP_KC_TRAIL, s, over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 16.0 * m * m; }),
            over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 4.0 * BB * m * m; }));

@@ -30,6 +30,42 @@ int row_norms(hipStream_t s, const double* X, int64_t n, int64_t d, int64_t ldx,
   return 0;
 }
 
+// out[0] = number of non-finite entries of X (n x d, ldx), out[1] = of y;
+// one workgroup (16 wavefronts: rows over waves, columns over lanes), fixed
+// order, no atomics.
+__global__ __launch_bounds__(1024) void count_nonfinite_kernel(const double* __restrict__ X,
+                                                                int64_t n, int64_t d, int64_t ldx,
+                                                                const double* __restrict__ y,
+                                                                int* __restrict__ out) {
+  __shared__ double red[2][16];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  double cx = 0.0, cy = 0.0;
+  for (int64_t i = w; i < n; i += 16) {
+    const double* xr = X + i * ldx;
+    for (int64_t k = lane; k < d; k += 64) cx += isfinite(xr[k]) ? 0.0 : 1.0;
+  }
+  for (int64_t i = threadIdx.x; i < n; i += 1024) cy += isfinite(y[i]) ? 0.0 : 1.0;
+  cx = wave_sum(cx);
+  cy = wave_sum(cy);
+  if (lane == 0) {
+    red[0][w] = cx;
+    red[1][w] = cy;
+  }
+  __syncthreads();
+  if (threadIdx.x < 2) {
+    double c = 0.0;
+    for (int q = 0; q < 16; ++q) c += red[threadIdx.x][q];
+    out[threadIdx.x] = (int)c;
+  }
+}
+
+int count_nonfinite(hipStream_t s, const double* X, int64_t n, int64_t d, int64_t ldx,
+                    const double* y, int* out) {
+  hipLaunchKernelGGL(count_nonfinite_kernel, dim3(1), dim3(1024), 0, s, X, n, d, ldx, y, out);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
 constexpr int GT = 64, GK = 16, GPAD = 4, MAXS = 8;
 
 __global__ __launch_bounds__(256) void rbf_blocks_kernel(

@@ -108,7 +108,7 @@ struct Layout {
   double *spart, *pnext, *band, *bpart;
   double *ahat, *abar, *bmat, *zmat, *anew, *estep, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
   double *beta, *bbar, *rmom, *gcoef, *kkt, *coef, *lam, *taucol, *fbuf, *nrm, *inv2s2;
-  int *flag, *moved, *iters, *iters_total, *active, *nvg;
+  int *flag, *moved, *iters, *iters_total, *active, *nvg, *chk;
   int32_t *tidx, *hidx, *fold;
 };
 
@@ -162,6 +162,7 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.iters = c.take<int>(cols);
   l.iters_total = c.take<int>(cols);
   l.active = c.take<int>(1);
+  l.chk = c.take<int>(2);
   l.nvg = c.take<int>(G);
   l.tidx = c.take<int32_t>((size_t)p.V * N);
   l.hidx = c.take<int32_t>((size_t)p.V * p.Mh);
@@ -258,7 +259,7 @@ void kmp_default_spec(kmp_path_spec* s) {
 }
 
 const char* kmp_kernel_class_name(int cls) {
-  static const char* names[KMP_NKC] = {"gram",        "tri_col",  "tri_symv", "tri_syr2k",
+  static const char* names[KMP_NKC] = {"gram",        "panel",  "panel_wy", "trail_update",
                                        "q_form",      "precompute", "gemm_f", "gemm_zhat",
                                        "update",      "finalize"};
   return (cls >= 0 && cls < KMP_NKC) ? names[cls] : "";
@@ -442,40 +443,6 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   Plan plan;
   int rc = make_plan(spec, n, d, L, fold_id, V, S, Qn, S, &plan);
   if (rc != 0) return rc;
-  // inputs to host for finiteness and label checks
-  std::vector<double> hy(n), hx((size_t)n * d);
-  KMP_HIP_TRY(hipMemcpyAsync(hy.data(), y, sizeof(double) * n, hipMemcpyDeviceToHost, s));
-  KMP_HIP_TRY(hipMemcpy2DAsync(hx.data(), sizeof(double) * d, X, sizeof(double) * ldx,
-                               sizeof(double) * d, n, hipMemcpyDeviceToHost, s));
-  KMP_HIP_TRY(hipStreamSynchronize(s));
-  for (int64_t i = 0; i < n; ++i) {
-    if (!std::isfinite(hy[i])) {
-      set_error("non-finite y at index " + std::to_string(i));
-      return KMP_ENONFINITE;
-    }
-    for (int64_t k = 0; k < d; ++k)
-      if (!std::isfinite(hx[(size_t)i * d + k])) {
-        set_error("non-finite X at row " + std::to_string(i));
-        return KMP_ENONFINITE;
-      }
-  }
-  if (spec->loss != KMP_CHECK) {
-    std::vector<int64_t> pos(V, 0), neg(V, 0);
-    int64_t tp = 0, tn = 0;
-    for (int64_t i = 0; i < n; ++i) {
-      if (hy[i] == 1.0) { pos[fold_id[i]]++; tp++; }
-      else if (hy[i] == -1.0) { neg[fold_id[i]]++; tn++; }
-      else {
-        set_error("labels must be +1 or -1 for hinge and logistic losses");
-        return KMP_EINVAL;
-      }
-    }
-    for (int v = 0; v < V; ++v)
-      if (tp - pos[v] == 0 || tn - neg[v] == 0) {
-        set_error("training set of fold " + std::to_string(v) + " has a single class");
-        return KMP_EFOLD;
-      }
-  }
   // largest bandwidth batch that fits the workspace
   int Sb = 0;
   for (int b = std::min(S, 8); b >= 1; --b) {   // the Gram epilogue takes <= 8 bandwidths
@@ -494,6 +461,40 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   }
   Layout lay;
   carve(plan, workspace, &lay);
+  // finiteness of X and y counted on the device (two ints in the
+  // workspace); y and the counts come to the host for the label checks
+  if ((rc = count_nonfinite(s, X, n, d, ldx, y, lay.chk)) != 0) return rc;
+  std::vector<double> hy(n);
+  int hchk[2] = {0, 0};
+  KMP_HIP_TRY(hipMemcpyAsync(hy.data(), y, sizeof(double) * n, hipMemcpyDeviceToHost, s));
+  KMP_HIP_TRY(hipMemcpyAsync(hchk, lay.chk, sizeof(hchk), hipMemcpyDeviceToHost, s));
+  KMP_HIP_TRY(hipStreamSynchronize(s));
+  if (hchk[0] != 0) {
+    set_error(std::to_string(hchk[0]) + " non-finite entries in X");
+    return KMP_ENONFINITE;
+  }
+  if (hchk[1] != 0) {
+    set_error(std::to_string(hchk[1]) + " non-finite entries in y");
+    return KMP_ENONFINITE;
+  }
+  if (spec->loss != KMP_CHECK) {
+    std::vector<int64_t> pos(V, 0), neg(V, 0);
+    int64_t tp = 0, tn = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      if (hy[i] == 1.0) { pos[fold_id[i]]++; tp++; }
+      else if (hy[i] == -1.0) { neg[fold_id[i]]++; tn++; }
+      else {
+        set_error("labels must be +1 or -1 for hinge and logistic losses");
+        return KMP_EINVAL;
+      }
+    }
+    for (int v = 0; v < V; ++v)
+      if (tp - pos[v] == 0 || tn - neg[v] == 0) {
+        set_error("training set of fold " + std::to_string(v) + " has a single class");
+        return KMP_EFOLD;
+      }
+  }
+
   const int N = plan.N, C = plan.C, G = plan.G;
   const int nst = spec->loss == KMP_LOGISTIC ? 1 : spec->n_stages;
   const double delta_final = spec->loss == KMP_LOGISTIC

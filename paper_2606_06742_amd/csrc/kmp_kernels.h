@@ -50,6 +50,9 @@ int loss_epilogue(hipStream_t s, int M, int N, int batch, int S, const double* p
                   int64_t sC, int64_t sP, double* Z, const LossEpi& e);
 
 // ---------------------------------------------------------------- Gram
+// out[0], out[1] = counts of non-finite entries of X (n x d, ldx) and y (n).
+int count_nonfinite(hipStream_t s, const double* X, int64_t n, int64_t d, int64_t ldx,
+                    const double* y, int* out);
 // Squared row norms of X (n x d, ldx): nrm[i] = sum_k X[i][k]^2.
 int row_norms(hipStream_t s, const double* X, int64_t n, int64_t d, int64_t ldx, double* nrm);
 

@@ -409,8 +409,8 @@ int tridiagonalize_multi(const hipStream_t* ss, const TridiagWork* ws, int nch) 
       const unsigned blocks = (unsigned)(ncol + nsym * a.sparts);
       if (blocks == 0) return 0;
       const int rows_col = ncol > 0 ? N - cj : 0;
-      if (ncol > 0) kc_begin(KMP_KC_TRI_COL, s);
-      else kc_begin(KMP_KC_TRI_SYMV, s);
+      if (ncol > 0) kc_begin(KMP_KC_PANEL, s);
+      else kc_begin(KMP_KC_PANEL_WY, s);
       if (rows_col <= TB * 4) hipLaunchKernelGGL(tri_step_kernel<4>, dim3(blocks), dim3(TB), 0, s, a);
       else if (rows_col <= TB * 8) hipLaunchKernelGGL(tri_step_kernel<8>, dim3(blocks), dim3(TB), 0, s, a);
       else hipLaunchKernelGGL(tri_step_kernel<16>, dim3(blocks), dim3(TB), 0, s, a);
@@ -429,8 +429,8 @@ int tridiagonalize_multi(const hipStream_t* ss, const TridiagWork* ws, int nch) 
         bytes += 8.0 * (m * m + 2.0 * a.sjj * m);
         flops += 2.0 * m * m + 8.0 * a.sjj * m;
       }
-      if (ncol > 0) kc_end(KMP_KC_TRI_COL, s, bytes, flops);
-      else kc_end(KMP_KC_TRI_SYMV, s, bytes, flops);
+      if (ncol > 0) kc_end(KMP_KC_PANEL, s, bytes, flops);
+      else kc_end(KMP_KC_PANEL_WY, s, bytes, flops);
       if (nsym > 0) {
         if (sg0 < GA) partsA = a.sparts;
         else partsB = a.sparts;
@@ -468,9 +468,9 @@ int tridiagonalize_multi(const hipStream_t* ss, const TridiagWork* ws, int nch) 
         ga.B = wk.panel + (int64_t)nb * N + pe; ga.ldb = N; ga.sB = (int64_t)3 * nb * N;
         ga.C = wk.A + (int64_t)pe * N + pe; ga.ldc = N; ga.sC = (int64_t)N * N;
         ga.alpha = -1.0; ga.beta = 1.0;
-        kc_begin(KMP_KC_TRI_SYR2K, s);
+        kc_begin(KMP_KC_TRAIL, s);
         if ((rc = gemm(s, ga, false, false, true)) != 0) return rc;
-        kc_end(KMP_KC_TRI_SYR2K, s, over_groups(wk, [&](double n) {
+        kc_end(KMP_KC_TRAIL, s, over_groups(wk, [&](double n) {
                  const double m = std::max(0.0, n - pe); return 16.0 * m * m; }),
                over_groups(wk, [&](double n) {
                  const double m = std::max(0.0, n - pe); return 4.0 * nb * m * m; }));

@@ -20,7 +20,7 @@ KMP_EINVAL, KMP_EFOLD, KMP_EWORKSPACE, KMP_EHIP, KMP_ENONFINITE = -1, -2, -3, -4
 KMP_HINGE, KMP_LOGISTIC, KMP_CHECK = 0, 1, 2
 KMP_FLAG_RESTART = 1
 KMP_NKC = 10
-KERNEL_CLASSES = ("gram", "tri_col", "tri_symv", "tri_syr2k", "q_form", "precompute", "gemm_f",
+KERNEL_CLASSES = ("gram", "panel", "panel_wy", "trail_update", "q_form", "precompute", "gemm_f",
                   "gemm_zhat", "update", "finalize")
 LOSS_CODES = {"hinge": KMP_HINGE, "logistic": KMP_LOGISTIC, "check": KMP_CHECK}
 

@@ -95,3 +95,25 @@ def test_path_c2_full_size_sampled():
         o["cv_err"][s, q, v, l] = np.count_nonzero(y[H] * fH <= 0)
     worst = compare_cells(g, o, inp, "logistic", cells=cells)
     print("C2 sampled worst", worst, g["timings"])
+
+
+def test_path_rejects_bad_inputs():
+    """Non-finite X or y and non +-1 labels are refused before any solve;
+    a valid call afterwards still succeeds."""
+    from paper_2606_06742_amd import kmpath as km
+    device()
+    inp = W.small_problem("hinge", 64, 3, seed=9, V=3, L=3)
+    announce("fit_path input checks, hinge n=64")
+    cases = []
+    X = inp["X"].copy(); X[5, 1] = np.nan
+    cases.append((X, inp["y"], km.KMP_ENONFINITE, "X"))
+    y = inp["y"].copy(); y[7] = np.inf
+    cases.append((inp["X"], y, km.KMP_ENONFINITE, "y"))
+    y = inp["y"].copy(); y[2] = 0.5
+    cases.append((inp["X"], y, km.KMP_EINVAL, "labels"))
+    for Xc, yc, code, what in cases:
+        with pytest.raises(km.KmpError) as e:
+            km.fit_path(Xc, yc, "hinge", inp["sigmas"], inp["lambdas"], inp["fold_id"], inp["V"])
+        assert e.value.code == code, (what, str(e.value))
+    r = _gpu(inp, "hinge")
+    assert np.all(np.isfinite(r["objective"]))
