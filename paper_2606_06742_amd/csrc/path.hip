@@ -341,11 +341,12 @@ __global__ __launch_bounds__(256) void precompute_kernel(
   const int64_t gc = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
   if (gc >= cols) return;
   double* xs = lds_dyn + (int64_t)wv * (N + PTILE);
-  double (*T1)[BND + 1] = reinterpret_cast<double (*)[BND + 1]>(xs + N);
-  double (*T2)[BND + 1] = T1 + BND;
-  double (*T3)[BND + 1] = T2 + BND;
-  double* dcur = xs + N + 3 * BND * (BND + 1);
-  double* dprv = dcur + BND;
+  constexpr int TL = BND + 1;            // LDS row of a 16 x 16 tile
+  double* Cs = xs + N;                   // C_I
+  double* Ls = Cs + BND * TL;            // L_I (strict lower) and D_I (diagonal)
+  double* Xs = Ls + BND * TL;            // L_I^{-1}
+  double* colb = Xs + BND * TL;          // one column of the LDL' sweep
+  double* dprv = colb + BND;             // D_{I-1}
   const int g = (int)(gc / C);
   const double lam = lamv[gc];
   const double sc = 1.0 / ((double)nv[g] * kappa);
@@ -354,110 +355,105 @@ __global__ __launch_bounds__(256) void precompute_kernel(
   double* Vc = Vfac + gc * (int64_t)BND * N;
   double* Dc = Dfac + gc * (int64_t)N;
   const int64_t base = gc * (int64_t)N;
-  const int a = lane & (BND - 1);
-  const bool wr = lane < BND;
+  // lane (a, qg): row a of each 16 x 16 tile, columns 4 qg .. 4 qg + 3
+  const int a = lane & (BND - 1), qg = lane >> 4;
   const int NB = N / BND;
-  double cp[BND];                        // row a of C_I (zero for I = 0)
-#pragma unroll
-  for (int j = 0; j < BND; ++j) cp[j] = 0.0;
-  if (wr) dprv[a] = 0.0;
+  for (int e = lane; e < BND * TL; e += 64) Cs[e] = 0.0;
+  if (lane < BND) dprv[lane] = 0.0;
   for (int I = 0; I < NB; ++I) {
     const int i0 = BND * I;
-    // S = M_II - C_I D_{I-1} C_I'  (row a)
     wave_sync();
-    if (wr) {
+    // S = M_II - C_I D_{I-1} C_I'
+    double cr[BND];
 #pragma unroll
-      for (int j = 0; j < BND; ++j) T1[a][j] = cp[j];
-    }
-    wave_sync();
-    double sr[BND];
+    for (int j = 0; j < BND; ++j) cr[j] = Cs[a * TL + j] * dprv[j];
+    double s4[4];
 #pragma unroll
-    for (int c = 0; c < BND; ++c) {
+    for (int t = 0; t < 4; ++t) {
+      const int c = 4 * qg + t;
       const int64_t off = (c <= a) ? (int64_t)(a - c) * N + i0 + c : (int64_t)(c - a) * N + i0 + a;
-      const double bv = bg[off];
-      double m = sc * bv;
-      if (c == a) m += 2.0 * lam;
-      double acc = 0.0;
+      const double m = fma(sc, bg[off], (c == a) ? 2.0 * lam : 0.0);
+      double acc0 = 0.0, acc1 = 0.0;
 #pragma unroll
-      for (int j = 0; j < BND; ++j) acc = fma(cp[j] * dprv[j], T1[c][j], acc);
-      sr[c] = m - acc;
+      for (int j = 0; j < BND; j += 2) {
+        acc0 = fma(cr[j], Cs[c * TL + j], acc0);
+        acc1 = fma(cr[j + 1], Cs[c * TL + j + 1], acc1);
+      }
+      s4[t] = m - (acc0 + acc1);
     }
-    // dense LDL' of S, row a of L in sr (columns < a), D in dcur
+    // S = L D L' (right-looking: column k through colb, trailing update by
+    // every lane on its four entries)
 #pragma unroll
     for (int k = 0; k < BND; ++k) {
-      if (a == k) {
-        double d = sr[k];
-#pragma unroll
-        for (int m = 0; m < BND; ++m)
-          if (m < k) d = fma(-sr[m] * sr[m], dcur[m], d);
-        if (wr) dcur[k] = d;
-#pragma unroll
-        for (int m = 0; m < BND; ++m)
-          if (wr && m < k) T2[k][m] = sr[m];
-      }
       wave_sync();
-      if (a > k) {
-        double v = sr[k];
-#pragma unroll
-        for (int m = 0; m < BND; ++m)
-          if (m < k) v = fma(-sr[m] * T2[k][m], dcur[m], v);
-        sr[k] = v / dcur[k];
-      }
+      if (qg == (k >> 2)) colb[a] = s4[k & 3];
       wave_sync();
-    }
-    // rows of L in T2 (strict lower part)
-    if (wr) {
+      const double rk = 1.0 / colb[k];
+      const double la = colb[a] * rk;                 // L[a][k] for a > k
 #pragma unroll
-      for (int m = 0; m < BND; ++m)
-        if (m < a) T2[a][m] = sr[m];
+      for (int t = 0; t < 4; ++t) {
+        const int j = 4 * qg + t;
+        const double upd = fma(-la, colb[j], s4[t]);
+        s4[t] = (a > k && j > k) ? upd : s4[t];
+      }
+      s4[k & 3] = (qg == (k >> 2) && a > k) ? la : s4[k & 3];
     }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) Ls[a * TL + 4 * qg + t] = s4[t];
     wave_sync();
-    // L^{-1}: lane a computes column a, stored transposed in T3[row][a]
+    // column a of L^{-1}: x_a = 1, x_i = -sum_{m=a}^{i-1} L[i][m] x_m,
+    // with running sums over the rows still to come
     {
-      double xcol[BND];
+      double acc[BND];
 #pragma unroll
-      for (int r = 0; r < BND; ++r) {
-        double v = (r == a) ? 1.0 : 0.0;
-        if (r > a) {
+      for (int i = 0; i < BND; ++i) acc[i] = 0.0;
+      double x[BND];
 #pragma unroll
-          for (int m = 0; m < BND; ++m)
-            if (m >= a && m < r) v = fma(-T2[r][m], xcol[m], v);
-        }
-        xcol[r] = v;
+      for (int m = 0; m < BND; ++m) {
+        x[m] = (m == a) ? 1.0 : ((m > a) ? -acc[m] : 0.0);
+#pragma unroll
+        for (int i = m + 1; i < BND; ++i) acc[i] = fma(Ls[i * TL + m], x[m], acc[i]);
       }
-      if (wr) {
+      if (qg == 0) {
 #pragma unroll
-        for (int r = 0; r < BND; ++r) T3[r][a] = xcol[r];
+        for (int i = 0; i < BND; ++i) Xs[i * TL + a] = x[i];
       }
     }
     wave_sync();
-    // store the tile: j < a from L^{-1}, j >= a from C_I; 1/D
-    if (wr) {
+    // the tile (L^{-1} below the diagonal, C_I on and above) and 1/D
 #pragma unroll
-      for (int j = 0; j < BND; ++j) Vc[(int64_t)j * N + i0 + a] = (j < a) ? T3[a][j] : cp[j];
-      Dc[i0 + a] = 1.0 / dcur[a];
+    for (int t = 0; t < 4; ++t) {
+      const int j = 4 * qg + t;
+      Vc[(int64_t)j * N + i0 + a] = (j < a) ? Xs[a * TL + j] : Cs[a * TL + j];
     }
-    // C_{I+1} = M_{I+1,I} L^{-T} D^{-1}: C[a][c] = sum_{j=a..c} Mn[a][j] Linv[c][j] / D[c]
+    const double da = Ls[a * TL + a];
+    if (qg == 0) Dc[i0 + a] = 1.0 / da;
+    // C_{I+1} = M_{I+1,I} L^{-T} D^{-1}: C[a][c] = sum_{j=a..c} Mn[a][j] X[c][j] / D[c]
+    double cn[4] = {0.0, 0.0, 0.0, 0.0};
     if (I + 1 < NB) {
       double mn[BND];
 #pragma unroll
       for (int j = 0; j < BND; ++j) {
-        const int r = (j >= a) ? BND + a - j : BND;
+        const int r = (j >= a) ? BND + a - j : BND;     // band row of B[i0+16+a][i0+j]
         const double bv = bg[(int64_t)r * N + i0 + j];
         mn[j] = (j >= a) ? sc * bv : 0.0;
       }
 #pragma unroll
-      for (int c = 0; c < BND; ++c) {
-        double acc = 0.0;
+      for (int t = 0; t < 4; ++t) {
+        const int c = 4 * qg + t;
+        double acc0 = 0.0, acc1 = 0.0;
 #pragma unroll
-        for (int j = 0; j < BND; ++j)
-          if (j >= a && j <= c) acc = fma(mn[j], T3[c][j], acc);
-        cp[c] = (c >= a) ? acc / dcur[c] : 0.0;
+        for (int j = 0; j < BND; j += 2) {
+          acc0 = fma(mn[j], Xs[c * TL + j], acc0);
+          acc1 = fma(mn[j + 1], Xs[c * TL + j + 1], acc1);
+        }
+        cn[t] = (c >= a) ? (acc0 + acc1) / Ls[c * TL + c] : 0.0;
       }
     }
     wave_sync();
-    if (wr) dprv[a] = dcur[a];
-    wave_sync();
+#pragma unroll
+    for (int t = 0; t < 4; ++t) Cs[a * TL + 4 * qg + t] = cn[t];
+    if (qg == 0) dprv[a] = da;
   }
   // vhat = M^{-1} c sc and c'vhat; the stage restart abar = ahat (u = B vhat
   // and B abar follow in band_apply_kernel)
