@@ -365,6 +365,13 @@ __global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restric
   }
 }
 
+// Only the lower triangle of the trailing matrix is kept up to date (the
+// two-sided update skips the 64 x 64 tiles above the diagonal): an element
+// (R, C) with R > C lies in a tile on or below the diagonal for every tile
+// origin, and every diagonal 16 x 16 block lies inside one diagonal tile,
+// since the origins of successive panels differ by multiples of 16. So
+// A22[k][j] is read as A[k][j] for k >= j and as A[j][k] above.
+//
 // X' = Y' A22 and the partial products of M2 = V'X for one panel (A22 =
 // A[m0:, m0:], Y' = T'V' stored transposed, Yt[k][i] = Yt[16 k + i], m x 16).
 // One workgroup per 16 columns j0 .. j0+15 of X' and matrix: wave w
@@ -389,18 +396,20 @@ __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__
   double* Pg = panel + (int64_t)g * 3 * BB * N + m0;
   const int i = lane & 15, kq = lane >> 4;
   const double* ya = Yg + (int64_t)kq * BB + i;
-  const double* bb = Ag + (int64_t)kq * N + j0 + i;
+  const double* bb = Ag + (int64_t)kq * N + j0 + i;           // A22[k][j0 + i], k >= j
+  const double* bt = Ag + (int64_t)(j0 + i) * N + kq;         // A22[j0 + i][k], k < j
   xdbl4 acc = {0.0, 0.0, 0.0, 0.0};
   for (int q = w; q < nch; q += 4 * XUQ) {
     double av[XUQ][4], bv[XUQ][4];
 #pragma unroll
     for (int u = 0; u < XUQ; ++u) {
       const int qq = (q + 4 * u < nch) ? q + 4 * u : q;      // clamped: not accumulated
+      const bool below = qq >= jb;                             // chunk on or below the block row
 #pragma unroll
       for (int s4 = 0; s4 < 4; ++s4) {
         const int k = BB * qq + 4 * s4;
         av[u][s4] = ya[(int64_t)k * BB];
-        bv[u][s4] = bb[(int64_t)k * N];
+        bv[u][s4] = below ? bb[(int64_t)k * N] : bt[k];
       }
     }
 #pragma unroll
@@ -492,14 +501,17 @@ __global__ __launch_bounds__(256) void panel_w_kernel(int N, int m0, const doubl
 // pieces), then per 32 k the 2 x 8 operand values of each side are loaded
 // together and 32 products with the A operand negated follow. m is a
 // multiple of 16, so each 16 x 16 block is wholly inside or outside C:
-// outside blocks load from clamped addresses and are not stored.
-template <int KC>
+// outside blocks load from clamped addresses and are not stored. With LOWER
+// only the tiles on and below the diagonal are updated (C symmetric, its
+// lower triangle kept; see the note before panel_x_kernel).
+template <int KC, bool LOWER>
 __global__ __launch_bounds__(256) void rank_update_kernel(double* __restrict__ C, int64_t ldc,
                                                            int64_t sC, int m,
                                                            const double* __restrict__ P1,
                                                            int64_t ld1, int64_t s1,
                                                            const double* __restrict__ P2,
                                                            int64_t ld2, int64_t s2) {
+  if (LOWER && blockIdx.y > blockIdx.x) return;
   const int g = blockIdx.z, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int i0 = 64 * blockIdx.x + 32 * (w & 1), j0 = 64 * blockIdx.y + 32 * (w >> 1);
   double* Cg = C + (int64_t)g * sC;
@@ -585,15 +597,21 @@ __global__ __launch_bounds__(256) void ts_gram_partial_kernel(
   if (i < M && j < Nc) part[(((int64_t)b * nch + chunk) * 64 + i) * 64 + j] = s0 + s1;
 }
 
-__global__ void ts_gram_sum_kernel(int M, int Nc, int nch, const double* __restrict__ part,
-                                   double* __restrict__ C, int64_t ldc, int64_t sC) {
-  const int b = blockIdx.x, t = threadIdx.x;
-  for (int e = t; e < M * Nc; e += blockDim.x) {
-    const int i = e / Nc, j = e % Nc;
-    double s = 0.0;
-    for (int c = 0; c < nch; ++c) s += part[(((int64_t)b * nch + c) * 64 + i) * 64 + j];
-    C[(int64_t)b * sC + (int64_t)i * ldc + j] = s;
-  }
+// One output per thread (blockIdx.y picks 256 of the M x Nc outputs), the
+// chunk partials added in order.
+__global__ __launch_bounds__(256) void ts_gram_sum_kernel(int M, int Nc, int nch,
+                                                           const double* __restrict__ part,
+                                                           double* __restrict__ C, int64_t ldc,
+                                                           int64_t sC) {
+  const int b = blockIdx.x;
+  const int e = 256 * blockIdx.y + threadIdx.x;
+  if (e >= M * Nc) return;
+  const int i = e / Nc, j = e % Nc;
+  const double* pp = part + ((int64_t)b * nch * 64 + i) * 64 + j;
+  double s = 0.0;
+#pragma unroll 4
+  for (int c = 0; c < nch; ++c) s += pp[(int64_t)c * 64 * 64];
+  C[(int64_t)b * sC + (int64_t)i * ldc + j] = s;
 }
 
 static int ts_gram(hipStream_t s, int M, int Nc, int K, int batch, const double* A, int64_t lda,
@@ -604,8 +622,8 @@ static int ts_gram(hipStream_t s, int M, int Nc, int K, int batch, const double*
   hipLaunchKernelGGL(ts_gram_partial_kernel, dim3((unsigned)nch, (unsigned)tiles, (unsigned)batch),
                      dim3(256), 0, s, M, Nc, K, A, lda, sA, B, ldb, sB, part);
   KMP_LAUNCH_CHECK();
-  hipLaunchKernelGGL(ts_gram_sum_kernel, dim3((unsigned)batch), dim3(256), 0, s, M, Nc, nch, part,
-                     C, ldc, sC);
+  hipLaunchKernelGGL(ts_gram_sum_kernel, dim3((unsigned)batch, (unsigned)ceil_div(M * Nc, 256)),
+                     dim3(256), 0, s, M, Nc, nch, part, C, ldc, sC);
   KMP_LAUNCH_CHECK();
   return 0;
 }
@@ -734,7 +752,7 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
              const double m = std::max(0.0, n - m0); return 2.0 * BB * m * m; }));
     // A22 -= V W' + W V' (K = 2 BB over the [V; W; V] rows)
     kc_begin(KMP_KC_TRAIL, s);
-    hipLaunchKernelGGL(rank_update_kernel<1>,
+    hipLaunchKernelGGL((rank_update_kernel<1, true>),
                        dim3((unsigned)ceil_div(mrow, 64), (unsigned)ceil_div(mrow, 64), (unsigned)G),
                        dim3(256), 0, s, wk.A + (int64_t)m0 * N + m0, (int64_t)N, (int64_t)N * N, mrow,
                        (const double*)(wk.panel + m0), (int64_t)N, sP,
@@ -789,7 +807,7 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     // Q[q+BB:, q+BB:] -= V' Y  (K = kb = 64; the last block may be shorter
     // only when N - BB is not a multiple of 64, then the generic product)
     if (kb == kWyBlock) {
-      hipLaunchKernelGGL(rank_update_kernel<2>,
+      hipLaunchKernelGGL((rank_update_kernel<2, false>),
                          dim3((unsigned)ceil_div(m, 64), (unsigned)ceil_div(m, 64), (unsigned)G),
                          dim3(256), 0, s, wk.Q + (int64_t)(q + BB) * N + q + BB, (int64_t)N,
                          (int64_t)N * N, m, (const double*)(wk.A + (int64_t)q * N + q + BB),
