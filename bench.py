@@ -110,9 +110,12 @@ def cpu_baseline(inp, w, ncells):
                       f"seed 7), fold Gram blocks included, {dt:.1f} s"}
 
 
-# Matrix-core kernels are priced against the fp64 MFMA peak, the others
-# against HBM bandwidth.
+# Kernel classes that run on the matrix cores. One of them is priced against
+# the fp64 MFMA peak when its algorithmic intensity (flops per HBM byte) is
+# above the ridge point of the two peaks, otherwise against HBM bandwidth;
+# every other class is priced against HBM bandwidth.
 MFMA_CLASSES = ("gemm_f", "gemm_zhat", "panel_wy", "trail_update", "q_form", "gram")
+RIDGE = FP64_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9)
 
 
 def roofline(kt, workload):
@@ -123,7 +126,7 @@ def roofline(kt, workload):
     name = max(kt, key=lambda k: kt[k][0] / kt[k][1] * kt[k][2])
     ms, launches, seen, nbytes, flops = kt[name]
     sec = 1e-3 * ms
-    if name in MFMA_CLASSES:
+    if name in MFMA_CLASSES and nbytes > 0 and flops / nbytes >= RIDGE:
         achieved = flops / sec / 1e12
         return {"kernel": name, "bound": "mfma", "achieved": achieved, "peak": FP64_PEAK_TFS,
                 "unit": "TFLOP/s", "frac": achieved / FP64_PEAK_TFS,
@@ -135,6 +138,7 @@ def roofline(kt, workload):
             "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
             "traffic": profiled_traffic(name, workload),
             "algorithmic_bytes_per_launch": nbytes / launches,
+            "algorithmic_flops_per_launch": flops / launches,
             "avg_launch_us": 1e3 * ms / launches, "timed_launches": launches}
 
 

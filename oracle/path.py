@@ -109,8 +109,10 @@ def fit_path(X, y, loss, sigmas, lambdas, fold_id, V, taus=None, delta=2.0 ** -6
     return res
 
 
-def default_workers():
+def default_workers(cap=16):
+    """Worker processes for the cell pool: the usable cores, at most ``cap``."""
     try:
-        return max(1, len(os.sched_getaffinity(0)))
+        n = len(os.sched_getaffinity(0))
     except AttributeError:
-        return max(1, os.cpu_count() or 1)
+        n = os.cpu_count() or 1
+    return max(1, min(cap, n))

@@ -34,10 +34,13 @@ struct Tile {
 // Global -> register fetch of one K slice, and register -> LDS store.
 // Splitting the two lets the next slice be in flight while the matrix
 // cores work on the current one.
+// For k-contiguous B (BKC) each thread loads from one column, whose base
+// pointer bcol the caller resolves once (null for a column past the end).
 template <int BM, int BK, bool AK, bool BKC>
 __device__ __forceinline__ void fetch_slice(int M, int N, int K, int i0, int j0, int k0,
                                             const double* __restrict__ A, int64_t lda,
                                             const double* __restrict__ B, int64_t ldb,
+                                            const double* __restrict__ bcol,
                                             double (&ra)[Tile<BM, BK>::APT],
                                             double (&rb)[Tile<BM, BK>::BPT]) {
   constexpr int APT = Tile<BM, BK>::APT, BPT = Tile<BM, BK>::BPT;
@@ -61,14 +64,13 @@ __device__ __forceinline__ void fetch_slice(int M, int N, int K, int i0, int j0,
       ra[q] = (gi < M && gk < K) ? A[(int64_t)gk * lda + gi] : 0.0;
     }
   }
-  if (BKC) {                      // B[j*ldb + k]
+  if (BKC) {                      // B[j*ldb + k], column base bcol
     constexpr int TPR = BK / BPT;
-    const int j = t / TPR, kb = (t % TPR) * BPT;
-    const int gj = j0 + j;
+    const int kb = (t % TPR) * BPT;
 #pragma unroll
     for (int q = 0; q < BPT; ++q) {
       const int gk = k0 + kb + q;
-      rb[q] = (gj < N && gk < K) ? B[(int64_t)gj * ldb + gk] : 0.0;
+      rb[q] = (bcol && gk < K) ? bcol[gk] : 0.0;
     }
   } else {                        // B[k*ldb + j]
     constexpr int TPR = TN / BPT;
@@ -116,10 +118,17 @@ __device__ __forceinline__ void store_slice(const double (&ra)[Tile<BM, BK>::APT
 // wi + 16 bi .., cols wj + 16 bj ... Two LDS stages: slice k+1 is fetched
 // into registers before the MFMAs on slice k and stored into the other
 // stage afterwards (one barrier per slice).
+//
+// cmap (k-contiguous B only, may be null) maps tile column j0 + j to the
+// column cmap[j0 + j] of B; N then counts the mapped columns. A wave skips
+// the matrix products of a 16-column block that lies wholly past N (a
+// wave-uniform test), so a tile with few columns costs little more than
+// its loads.
 template <int BM, int BK, bool AK, bool BKC>
 __device__ __forceinline__ void tile_mainloop(int M, int N, int kbeg, int K, int i0, int j0,
                                               const double* __restrict__ A, int64_t lda,
                                               const double* __restrict__ B, int64_t ldb,
+                                              const int* __restrict__ cmap,
                                               dbl4 (&acc)[Tile<BM, BK>::MB][2]) {
   constexpr int MB = Tile<BM, BK>::MB;
   __shared__ double As[2][BK][BM + LPAD];
@@ -132,8 +141,14 @@ __device__ __forceinline__ void tile_mainloop(int M, int N, int kbeg, int K, int
   for (int a = 0; a < MB; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = dbl4{0.0, 0.0, 0.0, 0.0};
+  const double* bcol = nullptr;
+  if (BKC) {
+    const int gj = j0 + (int)threadIdx.x / (BK / Tile<BM, BK>::BPT);
+    if (gj < N) bcol = B + (int64_t)(cmap ? cmap[gj] : gj) * ldb;
+  }
+  const bool use0 = j0 + wj < N, use1 = j0 + wj + 16 < N;
   double ra[Tile<BM, BK>::APT], rb[Tile<BM, BK>::BPT];
-  fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg, A, lda, B, ldb, ra, rb);
+  fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg, A, lda, B, ldb, bcol, ra, rb);
   store_slice<BM, BK, AK, BKC>(ra, rb, As[0], Bs[0]);
   __syncthreads();
   const int nk = (K - kbeg + BK - 1) / BK;
@@ -141,18 +156,21 @@ __device__ __forceinline__ void tile_mainloop(int M, int N, int kbeg, int K, int
     const int cur = kt & 1;
     const bool more = kt + 1 < nk;
     if (more)
-      fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + (kt + 1) * BK, A, lda, B, ldb, ra, rb);
+      fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + (kt + 1) * BK, A, lda, B, ldb, bcol,
+                                   ra, rb);
+    if (use0) {
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 4) {
-      double av[MB];
+      for (int kk = 0; kk < BK; kk += 4) {
+        double av[MB];
 #pragma unroll
-      for (int a = 0; a < MB; ++a) av[a] = As[cur][kk + lk][wi + 16 * a + li];
-      const double b0 = Bs[cur][kk + lk][wj + li];
-      const double b1 = Bs[cur][kk + lk][wj + 16 + li];
+        for (int a = 0; a < MB; ++a) av[a] = As[cur][kk + lk][wi + 16 * a + li];
+        const double b0 = Bs[cur][kk + lk][wj + li];
+        const double b1 = Bs[cur][kk + lk][wj + 16 + li];
 #pragma unroll
-      for (int a = 0; a < MB; ++a) {
-        acc[a][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b0, acc[a][0], 0, 0, 0);
-        acc[a][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b1, acc[a][1], 0, 0, 0);
+        for (int a = 0; a < MB; ++a) {
+          acc[a][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b0, acc[a][0], 0, 0, 0);
+          if (use1) acc[a][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b1, acc[a][1], 0, 0, 0);
+        }
       }
     }
     if (more) store_slice<BM, BK, AK, BKC>(ra, rb, As[cur ^ 1], Bs[cur ^ 1]);
@@ -173,7 +191,7 @@ __global__ __launch_bounds__(256) void dgemm_kernel(int M, int N, int K,
   C += (int64_t)b * sC;
   const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TN;
   dbl4 acc[MB][2];
-  tile_mainloop<BM, BK, AK, BKC>(M, N, 0, K, i0, j0, A, lda, B, ldb, acc);
+  tile_mainloop<BM, BK, AK, BKC>(M, N, 0, K, i0, j0, A, lda, B, ldb, nullptr, acc);
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int wi = (w & 1) * (BM / 2), wj = (w >> 1) * 32;
@@ -210,7 +228,7 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
   C += (int64_t)b * sC;
   const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TN;
   dbl4 acc[MB][2];
-  tile_mainloop<BM, BK, true, true>(M, N, 0, K, i0, j0, A, lda, B, ldb, acc);
+  tile_mainloop<BM, BK, true, true>(M, N, 0, K, i0, j0, A, lda, B, ldb, nullptr, acc);
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int wi = (w & 1) * (BM / 2), wj = (w >> 1) * 32;
@@ -266,23 +284,30 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
 // the K range [s*Kc, min(K, (s+1)*Kc)) of batch b and stores its BM x 64
 // tile of A B (column-major, ldc) into part + s*sP + b*sC. The S partials
 // are added later in a fixed order, so results do not depend on timing.
+// Only the active columns of a batch are computed: tile column k < nact[b]
+// is column cmap[b*cstride + k] of B and of the partials (the other columns
+// of the partials are left as they were); tiles past nact[b] exit at once.
 template <int BM, int BK, bool AK>
-__global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int N, int K, int S, int Kc,
+__global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S, int Kc,
                                                              const double* __restrict__ A, int64_t lda, int64_t sA,
                                                              const double* __restrict__ B, int64_t ldb, int64_t sB,
                                                              double* __restrict__ part, int64_t ldc, int64_t sC,
-                                                             int64_t sP) {
+                                                             int64_t sP, const int* __restrict__ cmap_all,
+                                                             const int* __restrict__ nact, int cstride) {
   constexpr int MB = Tile<BM, BK>::MB;
   const int b = blockIdx.z / S, sk = blockIdx.z % S;
+  const int N = nact[b];
+  const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TN;
+  if (j0 >= N) return;
+  const int* cmap = cmap_all + (int64_t)b * cstride;
   A += (int64_t)b * sA;
   B += (int64_t)b * sB;
   double* C = part + (int64_t)sk * sP + (int64_t)b * sC;
   const int kbeg = sk * Kc;
   const int kend = min(K, kbeg + Kc);
-  const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TN;
   dbl4 acc[MB][2];
   if (kbeg < kend) {
-    tile_mainloop<BM, BK, AK, true>(M, N, kbeg, kend, i0, j0, A, lda, B, ldb, acc);
+    tile_mainloop<BM, BK, AK, true>(M, N, kbeg, kend, i0, j0, A, lda, B, ldb, cmap, acc);
   } else {
 #pragma unroll
     for (int a = 0; a < MB; ++a) acc[a][0] = acc[a][1] = dbl4{0.0, 0.0, 0.0, 0.0};
@@ -298,18 +323,21 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int N, int K,
       for (int r = 0; r < 4; ++r) {
         const int gi = i0 + wi + bi * 16 + mfma_row(lane, r);
         const int gj = j0 + wj + bj * 16 + mfma_col(lane);
-        if (gi < M && gj < N) C[(int64_t)gj * ldc + gi] = acc[bi][bj][r];
+        if (gi < M && gj < N) C[(int64_t)cmap[gj] * ldc + gi] = acc[bi][bj][r];
       }
 }
 
 // Loss epilogue over split-K partials of f: for row i < M of batch b and
-// column c < N, F = sum_s part_s[c][i] + bbar[c]; Z[c][i] = psi(y_i, F)/nv
-// (0 at padding rows); partial[b][tile][c] = sum of Z over the 64 rows of
-// the tile (lanes = rows, so the column sums are wave reductions).
+// active column c = cmap[b*N + k], k < nact[b], F = sum_s part_s[c][i] +
+// bbar[c]; Z[c][i] = psi(y_i, F)/nv (0 at padding rows); partial[b][tile][c]
+// = sum of Z over the 64 rows of the tile (lanes = rows, so the column sums
+// are wave reductions).
 __global__ __launch_bounds__(256) void loss_epilogue_kernel(int M, int N, int S,
                                                              const double* __restrict__ part,
                                                              int64_t ldc, int64_t sC, int64_t sP,
-                                                             double* __restrict__ Z, LossEpi e) {
+                                                             double* __restrict__ Z, LossEpi e,
+                                                             const int* __restrict__ cmap_all,
+                                                             const int* __restrict__ nact) {
   const int b = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int i = blockIdx.x * 64 + lane;
@@ -318,7 +346,10 @@ __global__ __launch_bounds__(256) void loss_epilogue_kernel(int M, int N, int S,
   const double yi = (i < nv) ? e.y[(int64_t)b * e.sy + i] : 0.0;
   const double* bbar = e.bbar + (int64_t)b * e.sbb;
   const double* tau = e.tau + (int64_t)b * e.stau;
-  for (int c = w; c < N; c += 4) {
+  const int* cmap = cmap_all + (int64_t)b * N;
+  const int na = nact[b];
+  for (int k = w; k < na; k += 4) {
+    const int c = cmap[k];
     double z = 0.0;
     if (i < M) {
       double f = 0.0;
@@ -375,25 +406,30 @@ int splitk_parts(const GemmArgs& g) {
   return S;
 }
 
-int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP) {
+int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP,
+                 const int* cmap, const int* nact) {
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return 0;
   const int Kc = (int)round_up(ceil_div(g.K, S), 16);
   dim3 grid((unsigned)ceil_div(g.M, 64), (unsigned)ceil_div(g.N, TN), (unsigned)(g.batch * S));
   if (a_kcontig)
-    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, true>), grid, dim3(256), 0, s, g.M, g.N, g.K, S,
-                       Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP);
+    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, true>), grid, dim3(256), 0, s, g.M, g.K, S,
+                       Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap, nact,
+                       g.N);
   else
-    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, false>), grid, dim3(256), 0, s, g.M, g.N, g.K, S,
-                       Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP);
+    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, false>), grid, dim3(256), 0, s, g.M, g.K, S,
+                       Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap, nact,
+                       g.N);
   KMP_LAUNCH_CHECK();
   return 0;
 }
 
 int loss_epilogue(hipStream_t s, int M, int N, int batch, int S, const double* part, int64_t ldc,
-                  int64_t sC, int64_t sP, double* Z, const LossEpi& e) {
+                  int64_t sC, int64_t sP, double* Z, const LossEpi& e, const int* cmap,
+                  const int* nact) {
   if (M <= 0 || N <= 0 || batch <= 0) return 0;
   dim3 grid((unsigned)ceil_div(M, 64), 1, (unsigned)batch);
-  hipLaunchKernelGGL(loss_epilogue_kernel, grid, dim3(256), 0, s, M, N, S, part, ldc, sC, sP, Z, e);
+  hipLaunchKernelGGL(loss_epilogue_kernel, grid, dim3(256), 0, s, M, N, S, part, ldc, sC, sP, Z, e,
+                     cmap, nact);
   KMP_LAUNCH_CHECK();
   return 0;
 }

@@ -108,7 +108,7 @@ struct Layout {
   double *spart, *pnext, *band, *bpart;
   double *ahat, *abar, *bmat, *zmat, *anew, *estep, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
   double *beta, *bbar, *rmom, *gcoef, *kkt, *coef, *lam, *taucol, *fbuf, *nrm, *inv2s2;
-  int *flag, *moved, *iters, *iters_total, *active, *nvg, *chk;
+  int *flag, *moved, *iters, *iters_total, *active, *nvg, *chk, *cmap, *nact;
   int32_t *tidx, *hidx, *fold;
 };
 
@@ -162,6 +162,8 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.iters = c.take<int>(cols);
   l.iters_total = c.take<int>(cols);
   l.active = c.take<int>(1);
+  l.cmap = c.take<int>(cols);
+  l.nact = c.take<int>(G);
   l.chk = c.take<int>(2);
   l.nvg = c.take<int>(G);
   l.tidx = c.take<int32_t>((size_t)p.V * N);
@@ -553,6 +555,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   pa.rmom = lay.rmom; pa.gcoef = lay.gcoef; pa.kkt = lay.kkt; pa.coef = lay.coef;
   pa.moved = lay.moved; pa.flag = lay.flag;
   pa.iters = lay.iters; pa.iters_total = lay.iters_total; pa.active_count = lay.active;
+  pa.cmap = lay.cmap; pa.nact = lay.nact;
 
   for (int s0 = 0; s0 < S; s0 += Sb) {
     const int sb = std::min(Sb, S - s0);
@@ -577,6 +580,9 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
                                hipMemcpyHostToDevice, s));
     KMP_HIP_TRY(hipMemcpyAsync(lay.nvg, nvg.data(), sizeof(int) * Gb, hipMemcpyHostToDevice, s));
     pa.nv_host = nvg.data();
+    // columns in each group's active list, as last read back (work counters)
+    std::vector<int> nact_h(Gb, C);
+    pa.nact_host = nact_h.data();
 
     // a1: Gram + fold gather into A (group g = s_local*V + v)
     KMP_HIP_TRY(hipEventRecord(tm.ev[1], s));
@@ -612,7 +618,10 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
       const double kappa = spec->loss == KMP_LOGISTIC ? 4.0 : 2.0 * delta;
       KMP_HIP_TRY(hipEventRecord(tm.ev[4], s));
       if ((rc = path_stage_precompute(s, pa, kappa)) != 0) return rc;
+      if ((rc = path_compact(s, pa)) != 0) return rc;
+      KMP_HIP_TRY(hipMemcpyAsync(nact_h.data(), lay.nact, sizeof(int) * Gb, hipMemcpyDeviceToHost, s));
       KMP_HIP_TRY(hipEventRecord(tm.ev[5], s));
+      KMP_HIP_TRY(hipStreamSynchronize(s));
       int it = 0;
       while (it < spec->max_iter) {
         if ((rc = path_iteration(s, pa, delta, kappa, spec->tol, spec->max_iter,
@@ -620,9 +629,10 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
           return rc;
         ++it;
         if (it % spec->poll_every == 0 || it >= spec->max_iter) {
-          if ((rc = path_count_active(s, pa)) != 0) return rc;
+          if ((rc = path_compact(s, pa)) != 0) return rc;
           int active = 0;
           KMP_HIP_TRY(hipMemcpyAsync(&active, lay.active, sizeof(int), hipMemcpyDeviceToHost, s));
+          KMP_HIP_TRY(hipMemcpyAsync(nact_h.data(), lay.nact, sizeof(int) * Gb, hipMemcpyDeviceToHost, s));
           KMP_HIP_TRY(hipStreamSynchronize(s));
           if (active == 0) break;
         }

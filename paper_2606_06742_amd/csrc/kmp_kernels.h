@@ -44,10 +44,14 @@ constexpr int kMaxSplitK = 4;
 // Split-K: number of K parts for g (1..4), the partial products (column-
 // major C layout per part, part stride sP), and the loss epilogue that adds
 // the parts in order and writes Z plus 64-row column sums (see LossEpi).
+// Both work on the active columns only: batch b has nact[b] of them, the
+// k-th being column cmap[b*g.N + k] (B k-contiguous, C column-major).
 int splitk_parts(const GemmArgs& g);
-int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP);
+int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP,
+                 const int* cmap, const int* nact);
 int loss_epilogue(hipStream_t s, int M, int N, int batch, int S, const double* part, int64_t ldc,
-                  int64_t sC, int64_t sP, double* Z, const LossEpi& e);
+                  int64_t sC, int64_t sP, double* Z, const LossEpi& e, const int* cmap,
+                  const int* nact);
 
 // ---------------------------------------------------------------- Gram
 // out[0], out[1] = counts of non-finite entries of X (n x d, ldx) and y (n).
@@ -160,14 +164,21 @@ struct PathArrays {
   int* iters = nullptr;     // per stage
   int* iters_total = nullptr;
   int* active_count = nullptr;  // 1 int
+  int* cmap = nullptr;      // G x C: the active columns of each group, in order
+  int* nact = nullptr;      // G: number of active columns of each group
   const int* nv_host = nullptr;  // G valid rows (host), for the work counters
+  const int* nact_host = nullptr;  // G entries of nact as last read (host), same use
 };
 
 int path_init_columns(hipStream_t s, const PathArrays& p);
 int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa);
 int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kappa, double tol,
                    int max_iter, int restart);
-int path_count_active(hipStream_t s, const PathArrays& p);
+// Rebuilds cmap/nact from the column flags and writes the total number of
+// active columns to active_count. The path GEMMs compute only the columns
+// listed in cmap, so it runs after every change of the flags that should
+// shrink the GEMMs (stage start, polls).
+int path_compact(hipStream_t s, const PathArrays& p);
 int group_ones_projection(hipStream_t s, const double* Q, const int* nv, int G, int N, double* cvec);
 
 // Finalize: alpha_loc = Q ahat (zmat reused), training predictions

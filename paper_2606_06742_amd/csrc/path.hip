@@ -104,6 +104,17 @@ static double over_groups(const PathArrays& p, F f) {
   for (int g = 0; g < p.G; ++g) a += f((double)(p.nv_host ? p.nv_host[g] : p.N));
   return a;
 }
+// Sum over groups of f(valid rows, columns in the group's active list) for
+// the work counters of the iteration kernels (groups with none are skipped).
+template <typename F>
+static double over_active(const PathArrays& p, F f) {
+  double a = 0.0;
+  for (int g = 0; g < p.G; ++g) {
+    const double c = p.nact_host ? (double)p.nact_host[g] : (double)p.C;
+    if (c > 0.0) a += f((double)(p.nv_host ? p.nv_host[g] : p.N), c);
+  }
+  return a;
+}
 
 // ------------------------------------------------------------ band solver
 // One wavefront per column. The column's working vector lives in LDS (xs,
@@ -684,11 +695,13 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   e.y = p.ylab; e.sy = p.N; e.nv = p.nv;
   e.bbar = p.bbar; e.sbb = p.C; e.tau = p.tau; e.stau = p.C;
   e.partial = p.partial; e.spart = (int64_t)RT * p.C;
-  const double gflops = over_groups(p, [&](double n) { return 2.0 * n * n * p.C; });
-  const double gbytes = over_groups(p, [&](double n) { return 8.0 * (n * n + 2.0 * n * p.C); });
+  const double gflops = over_active(p, [&](double n, double c) { return 2.0 * n * n * c; });
+  const double gbytes = over_active(p, [&](double n, double c) { return 8.0 * (n * n + 2.0 * n * c); });
   kc_begin(KMP_KC_GEMM_F, s);
-  if ((rc = gemm_partial(s, g1, true, S1, p.fpart, sP)) != 0) return rc;
-  if ((rc = loss_epilogue(s, p.N, p.C, p.G, S1, p.fpart, p.N, sC, sP, p.zmat, e)) != 0) return rc;
+  if ((rc = gemm_partial(s, g1, true, S1, p.fpart, sP, p.cmap, p.nact)) != 0) return rc;
+  if ((rc = loss_epilogue(s, p.N, p.C, p.G, S1, p.fpart, p.N, sC, sP, p.zmat, e, p.cmap,
+                          p.nact)) != 0)
+    return rc;
   kc_end(KMP_KC_GEMM_F, s, gbytes, gflops);
   // zhat = Q' z as split-K partials (added by the update kernel)
   GemmArgs g2;
@@ -698,7 +711,7 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   g2.ldc = p.N; g2.sC = sC;
   const int S2 = splitk_parts(g2);
   kc_begin(KMP_KC_GEMM_ZHAT, s);
-  if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP)) != 0) return rc;
+  if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP, p.cmap, p.nact)) != 0) return rc;
   kc_end(KMP_KC_GEMM_ZHAT, s, gbytes, gflops);
   const int64_t cols = (int64_t)p.G * p.C;
   const int cw = path_waves(p.N, 0);
@@ -721,22 +734,48 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   // and B abar. Flops: 2 BND multiply-adds per row for the two triangular
   // sweeps, 2 BND + 1 for the band product, 14 elementwise.
   kc_end(KMP_KC_UPDATE, s,
-         over_groups(p, [&](double n) { return 8.0 * (S2 + 2.0 * BND + 13.0) * n * p.C; }),
-         over_groups(p, [&](double n) { return (8.0 * BND + 16.0) * n * p.C; }));
+         over_active(p, [&](double n, double c) { return 8.0 * (S2 + 2.0 * BND + 13.0) * n * c; }),
+         over_active(p, [&](double n, double c) { return (8.0 * BND + 16.0) * n * c; }));
   return 0;
 }
 
-__global__ void count_active_kernel(const int* __restrict__ flag, int64_t cols, int* __restrict__ out) {
-  __shared__ double red[PW];
-  double c = 0.0;
-  for (int64_t i = threadIdx.x; i < cols; i += blockDim.x) c += (flag[i] == 0) ? 1.0 : 0.0;
-  c = block_sum<PW>(c, red);
-  if (threadIdx.x == 0) *out = (int)c;
+// One workgroup: wave w lists the active columns of groups w, w + 4, ...
+// in increasing order (a ballot per 64 columns, the lane's rank among the
+// active lanes below it giving its slot), then the group counts are added
+// in a fixed order for the total.
+__global__ __launch_bounds__(PB) void compact_columns_kernel(int G, int C,
+                                                             const int* __restrict__ flag,
+                                                             int* __restrict__ cmap,
+                                                             int* __restrict__ nact,
+                                                             int* __restrict__ total) {
+  __shared__ int cnt[PW];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int mine = 0;
+  for (int g = wv; g < G; g += PW) {
+    int base = 0;
+    for (int c0 = 0; c0 < C; c0 += 64) {
+      const int c = c0 + lane;
+      const bool act = c < C && flag[(int64_t)g * C + c] == 0;
+      const unsigned long long m = __ballot(act);
+      const int rank = __popcll(m & ((1ull << lane) - 1ull));
+      if (act) cmap[(int64_t)g * C + base + rank] = c;
+      base += __popcll(m);
+    }
+    if (lane == 0) nact[g] = base;
+    mine += base;
+  }
+  if (lane == 0) cnt[wv] = mine;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int t = 0;
+    for (int w = 0; w < PW; ++w) t += cnt[w];
+    *total = t;
+  }
 }
 
-int path_count_active(hipStream_t s, const PathArrays& p) {
-  hipLaunchKernelGGL(count_active_kernel, dim3(1), dim3(PB), 0, s, p.flag, (int64_t)p.G * p.C,
-                     p.active_count);
+int path_compact(hipStream_t s, const PathArrays& p) {
+  hipLaunchKernelGGL(compact_columns_kernel, dim3(1), dim3(PB), 0, s, p.G, p.C, p.flag, p.cmap,
+                     p.nact, p.active_count);
   KMP_LAUNCH_CHECK();
   return 0;
 }

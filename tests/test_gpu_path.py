@@ -117,3 +117,18 @@ def test_path_rejects_bad_inputs():
         assert e.value.code == code, (what, str(e.value))
     r = _gpu(inp, "hinge")
     assert np.all(np.isfinite(r["objective"]))
+
+
+def test_path_c4_full_parity():
+    """Kernel quantile regression at full size (n = 5000, 5 folds, 3 tau
+    levels sharing each fold's factor, 40 lambdas): every one of the 600
+    cells against the oracle."""
+    w = W.get("C4")
+    inp = W.make_inputs(w)
+    announce("fit_path C4 full size (check, n=5000, 3 taus, 40 lambdas)")
+    g = _gpu(inp, "check")
+    o = _oracle(inp, "check")
+    worst = compare_cells(g, o, inp, "check")
+    assert np.array_equal(g["selected"], o["selected"].astype(np.int32))
+    print("C4 worst", worst, "iterations", g["timings"]["iterations"],
+          g["timings"]["cell_iterations"])
