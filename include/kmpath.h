@@ -58,6 +58,10 @@ extern "C" {
 #define KMP_CHECK 2        /* smoothed check loss, any real y                */
 
 #define KMP_FLAG_RESTART 1 /* adaptive (gradient) restart of the momentum    */
+#define KMP_FLAG_GLOBAL_SOLVE 2 /* keep the banded solve's working vector in
+                          device memory at every order (it is there anyway
+                          above 8192 padded rows per fold, where it does not
+                          fit in LDS); results are identical either way     */
 
 /* Kernel classes timed with HIP events when their bit is set in
  * kmp_path_spec.timing_mask (1 << class). */
@@ -83,7 +87,7 @@ typedef struct {
                           |1'z|) <= tol at the extrapolated point (1e-9)    */
   int32_t max_iter;    /* iterations per stage per cell (100000)            */
   int32_t poll_every;  /* iterations between host convergence polls (8)     */
-  int32_t flags;       /* KMP_FLAG_RESTART (default on)                     */
+  int32_t flags;       /* KMP_FLAG_RESTART (default on), KMP_FLAG_GLOBAL_SOLVE */
   int32_t timing_mask; /* kernel classes to time with HIP events (default 0) */
   int32_t timing_every;/* bracket one launch in every timing_every launches
                           of a timed class (default 1: all)                 */

@@ -681,8 +681,8 @@ size_t band_work_doubles(int G, int N) {
 int band_reduce(hipStream_t s, const BandWork& wk) {
   const int G = wk.G, N = wk.N;
   if (G <= 0) return 0;
-  if (N % 64 != 0 || N < 64 || N > 8192) {
-    set_error("band_reduce: N must be a multiple of 64 in [64, 8192]");
+  if (N % 64 != 0 || N < 64 || N > kMaxOrder) {
+    set_error("band_reduce: N must be a multiple of 64 in [64, " + std::to_string(kMaxOrder) + "]");
     return KMP_EINVAL;
   }
   int rc;

@@ -209,8 +209,8 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
   // a fold's held-out set is no larger than any other fold's training set,
   // so the padded held-out block fits in the N x N factor buffer
   p->Mh = (int)round_up(maxm, kRowAlign);
-  if (p->N > 8192) {
-    set_error("more than 8192 training points per fold is not supported yet");
+  if (p->N > kMaxOrder) {
+    set_error("more than " + std::to_string(kMaxOrder) + " training points per fold");
     return KMP_EINVAL;
   }
   p->C = Qn * L;
@@ -375,8 +375,9 @@ int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N, double* Qout, dou
 int kmp_band_reduce(void* stream, double* A, int32_t G, int32_t N, double* Qout, double* band) {
   hipStream_t s = (hipStream_t)stream;
   static_assert(KMP_BAND == kBand, "band width of the header and the kernels differ");
-  if (!A || !Qout || !band || G < 1 || N < 64 || N > 8192 || N % 64 != 0) {
-    set_error("kmp_band_reduce: invalid arguments (N must be a multiple of 64 in [64, 8192])");
+  if (!A || !Qout || !band || G < 1 || N < 64 || N > kMaxOrder || N % 64 != 0) {
+    set_error("kmp_band_reduce: invalid arguments (N must be a multiple of 64 in [64, " +
+              std::to_string(kMaxOrder) + "])");
     return KMP_EINVAL;
   }
   BandWork w;
@@ -545,6 +546,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
 
   PathArrays pa;
   pa.N = N; pa.C = C; pa.loss = spec->loss;
+  pa.global_solve = (spec->flags & KMP_FLAG_GLOBAL_SOLVE) != 0;
   pa.nv = lay.nvg; pa.ylab = lay.ylab; pa.Q = lay.Qm; pa.band = lay.band;
   pa.cvec = lay.cvec; pa.lam = lay.lam; pa.tau = lay.taucol;
   pa.ahat = lay.ahat; pa.abar = lay.abar; pa.bmat = lay.bmat; pa.zmat = lay.zmat;

@@ -71,6 +71,9 @@ int rbf_blocks(hipStream_t s, const double* X, int64_t d, int64_t ldx, const dou
 
 // ------------------------------------------------------------ band form
 constexpr int kBand = 16;      // lower bandwidth of B (= panel width of the reduction)
+// Largest padded order per fold: N*N stays below 2^31 (32-bit row offsets
+// r*N in the kernels) and the per-fold matrices of the largest workloads fit.
+constexpr int kMaxOrder = 32768;
 constexpr int kWyBlock = 64;   // reflectors per compact-WY block when forming Q
 
 // Reduction of G symmetric N x N matrices (row-major, packed, destroyed) to
@@ -131,6 +134,7 @@ struct PathArrays {
   int N = 0;            // padded rows per group
   int C = 0;            // columns per group (tau x lambda)
   int loss = 0;
+  bool global_solve = false;     // banded solve vector in device memory at every order
   const int* nv = nullptr;       // G valid rows
   const double* ylab = nullptr;  // G x N labels (0 at padding)
   const double* Q = nullptr;     // G x N x N

@@ -211,6 +211,7 @@ __device__ __forceinline__ void band_solve(const double* __restrict__ Vc,
         }
         const double r = row4_sum(p0 + p1);
         if (lead) xs[BND * I + a] = r;
+        wave_sync();
         const double* rp = xs + BND * I + 4 * g;
         double q0 = lead ? r : 0.0, q1 = 0.0;
         q0 = fma(lm[0], rp[0], q0);
@@ -219,6 +220,7 @@ __device__ __forceinline__ void band_solve(const double* __restrict__ Vc,
         q1 = fma(lm[3], rp[3], q1);
         const double yv = row4_sum(q0 + q1);
         if (lead) xs[BND * I + a] = yv;
+        wave_sync();
       }
     }
   }
@@ -261,6 +263,7 @@ __device__ __forceinline__ void band_solve(const double* __restrict__ Vc,
         }
         const double sv = row4_sum(p0 + p1);
         if (lead) xs[BND * I + a] = sv;
+        wave_sync();
         const double* sp = xs + BND * I + 4 * g;
         double q0 = lead ? sv : 0.0, q1 = 0.0;
         q0 = fma(lm[0], sp[0], q0);
@@ -269,6 +272,7 @@ __device__ __forceinline__ void band_solve(const double* __restrict__ Vc,
         q1 = fma(lm[3], sp[3], q1);
         const double xv = row4_sum(q0 + q1);
         if (lead) xs[BND * I + a] = xv;
+        wave_sync();
 #pragma unroll
         for (int t = 0; t < 4; ++t) vprev[t] = vv[t];
       }
@@ -277,12 +281,149 @@ __device__ __forceinline__ void band_solve(const double* __restrict__ Vc,
   wave_sync();
 }
 
-// Columns (wavefronts) per workgroup: the LDS of a workgroup holds one
-// N-vector per column plus `extra` doubles of per-column tiles. Four columns
-// share a workgroup when they fit in 64 KiB, else each has its own.
+// The same solve for orders whose vector does not fit in LDS. Row r =
+// BND I + a belongs to the lead lane (a, 0) of the wavefront: it alone takes
+// the input of the row (win(r), from data written before the kernel), keeps
+// the forward result y_r in device memory (ysc[r], read back by itself in the
+// backward sweep) and hands the solution to wout(r, x_r). The blocks that the
+// other lanes need are staged in an LDS ring of two BND-double slots (block
+// I in slot I & 1). No lane reads device memory written by another lane of
+// the same launch.
+template <typename WIn, typename WOut>
+__device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
+                                             const double* __restrict__ Dc, double* ysc,
+                                             double* ring, int N, int lane, WIn win, WOut wout) {
+  const int NB = N / BND;
+  const int a = lane & 15, g = lane >> 4;
+  const bool lead = g == 0;
+  double ring_t[SPF][4], wv[SPF];
+#pragma unroll
+  for (int p = 0; p < SPF; ++p) {
+    const int Ib = p < NB ? p : NB - 1;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * Ib + a];
+    wv[p] = lead ? win(BND * Ib + a) : 0.0;
+  }
+  for (int I0 = 0; I0 < NB; I0 += SPF) {
+#pragma unroll
+    for (int p = 0; p < SPF; ++p) {
+      const int I = I0 + p;
+      if (I < NB) {
+        double cn[4], lm[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const double v = ring_t[p][t];
+          cn[t] = (4 * g + t >= a) ? -v : 0.0;
+          lm[t] = (4 * g + t < a) ? v : 0.0;
+        }
+        double p0 = wv[p], p1 = 0.0;
+        const int In = (I + SPF < NB) ? I + SPF : NB - 1;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * In + a];
+        wv[p] = lead ? win(BND * In + a) : 0.0;
+        double* cur = ring + BND * (I & 1);
+        if (I > 0) {
+          const double* yp = ring + BND * ((I - 1) & 1) + 4 * g;
+          p0 = fma(cn[0], yp[0], p0);
+          p1 = fma(cn[1], yp[1], p1);
+          p0 = fma(cn[2], yp[2], p0);
+          p1 = fma(cn[3], yp[3], p1);
+        }
+        const double r = row4_sum(p0 + p1);
+        if (lead) cur[a] = r;
+        wave_sync();
+        const double* rp = cur + 4 * g;
+        double q0 = lead ? r : 0.0, q1 = 0.0;
+        q0 = fma(lm[0], rp[0], q0);
+        q1 = fma(lm[1], rp[1], q1);
+        q0 = fma(lm[2], rp[2], q0);
+        q1 = fma(lm[3], rp[3], q1);
+        const double yv = row4_sum(q0 + q1);
+        if (lead) {
+          cur[a] = yv;
+          ysc[BND * I + a] = yv;
+        }
+        wave_sync();
+      }
+    }
+  }
+  wave_sync();
+  double dring[SPF];
+#pragma unroll
+  for (int p = 0; p < SPF; ++p) {
+    const int Ib = (NB - 1 - p >= 0) ? NB - 1 - p : 0;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)a * N + BND * Ib + 4 * g + t];
+    dring[p] = Dc[BND * Ib + a];
+    wv[p] = lead ? ysc[BND * Ib + a] : 0.0;
+  }
+  double vprev[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int T0 = 0; T0 < NB; T0 += SPF) {
+#pragma unroll
+    for (int p = 0; p < SPF; ++p) {
+      const int tt = T0 + p;
+      if (tt < NB) {
+        const int I = NB - 1 - tt;
+        double cn[4], lm[4], vv[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          vv[t] = ring_t[p][t];
+          cn[t] = (a >= 4 * g + t) ? -vprev[t] : 0.0;
+          lm[t] = (4 * g + t > a) ? vv[t] : 0.0;
+        }
+        const double dv = dring[p];
+        double p0 = lead ? dv * wv[p] : 0.0, p1 = 0.0;
+        const int In = (I - SPF >= 0) ? I - SPF : 0;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)a * N + BND * In + 4 * g + t];
+        dring[p] = Dc[BND * In + a];
+        wv[p] = lead ? ysc[BND * In + a] : 0.0;
+        double* cur = ring + BND * (I & 1);
+        if (tt > 0) {
+          const double* xp = ring + BND * ((I + 1) & 1) + 4 * g;
+          p0 = fma(cn[0], xp[0], p0);
+          p1 = fma(cn[1], xp[1], p1);
+          p0 = fma(cn[2], xp[2], p0);
+          p1 = fma(cn[3], xp[3], p1);
+        }
+        const double sv = row4_sum(p0 + p1);
+        if (lead) cur[a] = sv;
+        wave_sync();
+        const double* sp = cur + 4 * g;
+        double q0 = lead ? sv : 0.0, q1 = 0.0;
+        q0 = fma(lm[0], sp[0], q0);
+        q1 = fma(lm[1], sp[1], q1);
+        q0 = fma(lm[2], sp[2], q0);
+        q1 = fma(lm[3], sp[3], q1);
+        const double xv = row4_sum(q0 + q1);
+        if (lead) {
+          cur[a] = xv;
+          wout(BND * I + a, xv);
+        }
+        wave_sync();
+#pragma unroll
+        for (int t = 0; t < 4; ++t) vprev[t] = vv[t];
+      }
+    }
+  }
+  wave_sync();
+}
+
+// Columns (wavefronts) per workgroup and where the solve keeps its vector.
+// With the vector in LDS a workgroup holds one N-vector per column plus
+// `extra` doubles of per-column tiles, and four columns share a workgroup
+// when they fit in 64 KiB, else each has its own. Orders above kLdsVecMax
+// (or every order, with KMP_FLAG_GLOBAL_SOLVE) keep the vector in device
+// memory and only a two-block ring in LDS.
 constexpr int PTILE = 3 * BND * (BND + 1) + 2 * BND;   // precompute LDS tiles per column
-static int path_waves(int N, int extra) {
-  const size_t per = sizeof(double) * ((size_t)N + extra);
+constexpr int RING = 2 * BND;                          // LDS ring of the device-memory solve
+constexpr int kLdsVecMax = 8192;
+static bool path_global_vec(const PathArrays& p) { return p.global_solve || p.N > kLdsVecMax; }
+static int path_lds_doubles(const PathArrays& p, int extra) {
+  return path_global_vec(p) ? extra + RING : p.N + extra;
+}
+static int path_waves(const PathArrays& p, int extra) {
+  const size_t per = sizeof(double) * (size_t)path_lds_doubles(p, extra);
   return 4 * per <= 64 * 1024 ? 4 : 1;
 }
 
@@ -339,6 +480,7 @@ static int band_apply(hipStream_t s, const PathArrays& p, const double* x, doubl
 // kappa) (stored as above), vhat = M^{-1} c/(n_v kappa), u = B vhat,
 // g = 1/(2 lambda c'vhat); restart the momentum (r = 1, abar = ahat,
 // B abar) and reactivate the columns that stopped in the previous stage.
+template <bool GV>
 __global__ __launch_bounds__(256) void precompute_kernel(
     int N, int C, int64_t cols, const int* __restrict__ nv, const double* __restrict__ band,
     const double* __restrict__ cvec, const double* __restrict__ lamv, double kappa,
@@ -351,9 +493,9 @@ __global__ __launch_bounds__(256) void precompute_kernel(
   const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t gc = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
   if (gc >= cols) return;
-  double* xs = lds_dyn + (int64_t)wv * (N + PTILE);
+  double* xs = lds_dyn + (int64_t)wv * ((GV ? RING : N) + PTILE);   // vector or ring
   constexpr int TL = BND + 1;            // LDS row of a 16 x 16 tile
-  double* Cs = xs + N;                   // C_I
+  double* Cs = xs + (GV ? RING : N);     // C_I
   double* Ls = Cs + BND * TL;            // L_I (strict lower) and D_I (diagonal)
   double* Xs = Ls + BND * TL;            // L_I^{-1}
   double* colb = Xs + BND * TL;          // one column of the LDL' sweep
@@ -468,16 +610,26 @@ __global__ __launch_bounds__(256) void precompute_kernel(
   }
   // vhat = M^{-1} c sc and c'vhat; the stage restart abar = ahat (u = B vhat
   // and B abar follow in band_apply_kernel)
-#pragma unroll 8
-  for (int i = lane; i < N; i += 64) xs[i] = cg[i] * sc;
-  wave_sync();
-  band_solve(Vc, Dc, xs, N, lane);
   double cv = 0.0;
+  if constexpr (GV) {
+    // lead lanes: input c sc, forward results kept in vhat, vhat = x
+    double* vg = vhat + base;
+    band_solve_g(Vc, Dc, vg, xs, N, lane, [&](int r) { return cg[r] * sc; },
+                 [&](int r, double x) {
+                   vg[r] = x;
+                   cv = fma(cg[r], x, cv);
+                 });
+  } else {
 #pragma unroll 8
-  for (int i = lane; i < N; i += 64) {
-    const double v = xs[i];
-    vhat[base + i] = v;
-    cv = fma(cg[i], v, cv);
+    for (int i = lane; i < N; i += 64) xs[i] = cg[i] * sc;
+    wave_sync();
+    band_solve(Vc, Dc, xs, N, lane);
+#pragma unroll 8
+    for (int i = lane; i < N; i += 64) {
+      const double v = xs[i];
+      vhat[base + i] = v;
+      cv = fma(cg[i], v, cv);
+    }
   }
   cv = wave_sum(cv);
 #pragma unroll 8
@@ -493,14 +645,20 @@ __global__ __launch_bounds__(256) void precompute_kernel(
 
 int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa) {
   const int64_t cols = (int64_t)p.G * p.C;
-  const int cw = path_waves(p.N, PTILE);
-  const size_t lds = sizeof(double) * (size_t)cw * (p.N + PTILE);
-  KMP_HIP_TRY(hipFuncSetAttribute((const void*)precompute_kernel,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+  const int cw = path_waves(p, PTILE);
+  const size_t lds = sizeof(double) * (size_t)cw * path_lds_doubles(p, PTILE);
+  const void* kfn = path_global_vec(p) ? (const void*)precompute_kernel<true>
+                                       : (const void*)precompute_kernel<false>;
+  KMP_HIP_TRY(hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   kc_begin(KMP_KC_PRECOMPUTE, s);
-  hipLaunchKernelGGL(precompute_kernel, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, s,
-                     p.N, p.C, cols, p.nv, p.band, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
-                     p.gcoef, p.ahat, p.abar, p.beta, p.bbar, p.rmom, p.flag, p.iters);
+  if (path_global_vec(p))
+    hipLaunchKernelGGL(precompute_kernel<true>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds,
+                       s, p.N, p.C, cols, p.nv, p.band, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
+                       p.gcoef, p.ahat, p.abar, p.beta, p.bbar, p.rmom, p.flag, p.iters);
+  else
+    hipLaunchKernelGGL(precompute_kernel<false>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds,
+                       s, p.N, p.C, cols, p.nv, p.band, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
+                       p.gcoef, p.ahat, p.abar, p.beta, p.bbar, p.rmom, p.flag, p.iters);
   KMP_LAUNCH_CHECK();
   int rc;
   if ((rc = band_apply(s, p, p.vhat, p.uvec)) != 0) return rc;
@@ -525,6 +683,7 @@ int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa) {
 // loads of each stream in flight.
 constexpr int UL = 8;
 
+template <bool GV>
 __global__ __launch_bounds__(256) void solve_step_kernel(
     int N, int C, int64_t cols, int RT, const int* __restrict__ nvv,
     const double* __restrict__ lamv, const double* __restrict__ zpart, int S2, int64_t sP,
@@ -544,7 +703,8 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
     if (lane == 0) moved[gc] = 0;
     return;
   }
-  double* xs = lds_dyn + (int64_t)wv * N;
+  // the solve's vector in LDS (GV: only the ring of the device-memory solve)
+  double* xs = lds_dyn + (int64_t)wv * (GV ? RING : N);
   const int g = (int)(gc / C), c = (int)(gc % C);
   const int64_t base = gc * (int64_t)N;
   const double lam = lamv[gc];
@@ -578,7 +738,7 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
       const int i = i0 + lane + 64 * q;
       if (i < N) {
         const double w = fma(2.0 * lam, ab[q], zs[q]);
-        xs[i] = w;
+        if constexpr (!GV) xs[i] = w;
         tl = fma(uv[q], w, tl);
         n2 = fma(w, w, n2);
       }
@@ -598,8 +758,6 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
     if (lane == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; moved[gc] = 0; }
     return;
   }
-  wave_sync();
-  band_solve(Vfac + gc * (int64_t)BND * N, Dfac + base, xs, N, lane);
   // step and the restart test
   const double gco = gcoef[gc];
   const double sa = gco * (tsum - d0);
@@ -607,26 +765,57 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
   const double bn = bb - db;
   const double bold = beta[gc];
   double rd = 0.0;
-  for (int i0 = 0; i0 < N; i0 += 64 * UL) {
-    double vh[UL], ab[UL], ah[UL];
+  if constexpr (GV) {
+    // lead lanes: w of the row from its inputs, forward results kept in
+    // a+ (anew), and the step of the row as soon as x_r is known
+    const int64_t sPk = sP;
+    band_solve_g(
+        Vfac + gc * (int64_t)BND * N, Dfac + base, anew + base, xs, N, lane,
+        [&](int r) {
+          const int64_t ic = base + r;
+          double z = zpart[ic];
 #pragma unroll
-    for (int q = 0; q < UL; ++q) {
-      const int i = i0 + lane + 64 * q;
-      const int64_t ic = base + ((i < N) ? i : N - 1);
-      vh[q] = vhat[ic];
-      ab[q] = abar[ic];
-      ah[q] = ahat[ic];
-    }
+          for (int sk = 1; sk < kMaxSplitK; ++sk) {
+            const double zz = zpart[(sk < S2 ? sk : 0) * sPk + ic];
+            z += (sk < S2) ? zz : 0.0;
+          }
+          return fma(2.0 * lam, abar[ic], z);
+        },
+        [&](int r, double x) {
+          const int64_t ic = base + r;
+          const double da = fma(sa, vhat[ic], x);
+          const double an = abar[ic] - da;
+          const double e = an - ahat[ic];
+          rd = fma(da, e, rd);
+          anew[ic] = an;
+          estep[ic] = e;
+        });
+  } else {
+    wave_sync();
+    band_solve(Vfac + gc * (int64_t)BND * N, Dfac + base, xs, N, lane);
+    for (int i0 = 0; i0 < N; i0 += 64 * UL) {
+      double vh[UL], ab[UL], ah[UL], xv[UL];
 #pragma unroll
-    for (int q = 0; q < UL; ++q) {
-      const int i = i0 + lane + 64 * q;
-      if (i < N) {
-        const double da = fma(sa, vh[q], xs[i]);
-        const double an = ab[q] - da;
-        const double e = an - ah[q];
-        rd = fma(da, e, rd);
-        anew[base + i] = an;
-        estep[base + i] = e;
+      for (int q = 0; q < UL; ++q) {
+        const int i = i0 + lane + 64 * q;
+        const int ii = (i < N) ? i : N - 1;
+        const int64_t ic = base + ii;
+        vh[q] = vhat[ic];
+        ab[q] = abar[ic];
+        ah[q] = ahat[ic];
+        xv[q] = xs[ii];
+      }
+#pragma unroll
+      for (int q = 0; q < UL; ++q) {
+        const int i = i0 + lane + 64 * q;
+        if (i < N) {
+          const double da = fma(sa, vh[q], xv[q]);
+          const double an = ab[q] - da;
+          const double e = an - ah[q];
+          rd = fma(da, e, rd);
+          anew[base + i] = an;
+          estep[base + i] = e;
+        }
       }
     }
   }
@@ -714,16 +903,21 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP, p.cmap, p.nact)) != 0) return rc;
   kc_end(KMP_KC_GEMM_ZHAT, s, gbytes, gflops);
   const int64_t cols = (int64_t)p.G * p.C;
-  const int cw = path_waves(p.N, 0);
-  const size_t lds = sizeof(double) * (size_t)cw * p.N;
-  KMP_HIP_TRY(hipFuncSetAttribute((const void*)solve_step_kernel,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+  const int cw = path_waves(p, 0);
+  const size_t lds = sizeof(double) * (size_t)cw * path_lds_doubles(p, 0);
+  const bool gv = path_global_vec(p);
+  const void* kfn = gv ? (const void*)solve_step_kernel<true> : (const void*)solve_step_kernel<false>;
+  KMP_HIP_TRY(hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   kc_begin(KMP_KC_UPDATE, s);
-  hipLaunchKernelGGL(solve_step_kernel, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, s,
-                     p.N, p.C, cols, RT, p.nv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l,
-                     p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt,
-                     p.flag, p.iters, p.iters_total, p.anew, p.estep, p.coef, p.moved, tol,
-                     max_iter, restart);
+#define KMP_SOLVE_STEP(GVV)                                                                        \
+  hipLaunchKernelGGL(solve_step_kernel<GVV>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, \
+                     s, p.N, p.C, cols, RT, p.nv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l,  \
+                     p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt,    \
+                     p.flag, p.iters, p.iters_total, p.anew, p.estep, p.coef, p.moved, tol,         \
+                     max_iter, restart)
+  if (gv) KMP_SOLVE_STEP(true);
+  else KMP_SOLVE_STEP(false);
+#undef KMP_SOLVE_STEP
   KMP_LAUNCH_CHECK();
   hipLaunchKernelGGL(momentum_kernel, dim3((unsigned)ceil_div(p.N, BT), (unsigned)cols), dim3(BT), 0,
                      s, p.N, p.C, p.band, p.moved, p.coef, p.anew, p.estep, p.ahat, p.abar, p.bmat);

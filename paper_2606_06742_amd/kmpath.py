@@ -19,6 +19,7 @@ KMP_OK, KMP_WMAXITER = 0, 1
 KMP_EINVAL, KMP_EFOLD, KMP_EWORKSPACE, KMP_EHIP, KMP_ENONFINITE = -1, -2, -3, -4, -5
 KMP_HINGE, KMP_LOGISTIC, KMP_CHECK = 0, 1, 2
 KMP_FLAG_RESTART = 1
+KMP_FLAG_GLOBAL_SOLVE = 2
 KMP_NKC = 10
 KERNEL_CLASSES = ("gram", "panel", "panel_wy", "trail_update", "q_form", "precompute", "gemm_f",
                   "gemm_zhat", "update", "finalize")

@@ -23,11 +23,14 @@ def device():
     return torch.device("cuda")
 
 
-def compare_cells(g, o, inp, loss, cells=None, delta=2.0 ** -6):
+def compare_cells(g, o, inp, loss, cells=None, delta=2.0 ** -6, cv_expected=None):
     """Element-wise parity of GPU results g against oracle results o.
 
     cells: iterable of (s, q, v, l) to check, default all. Returns the worst
-    relative errors seen, for reporting.
+    relative errors seen, for reporting. cv_expected, if given (shape of
+    o["cv_sum"]), receives the held-out loss sum each checked cell is held
+    to: the oracle's, or, where the optimal intercept is an interval, the
+    oracle's held-out loss at the GPU's intercept.
     """
     S, Q, V, L = g["objective"].shape
     X, y, fold = inp["X"], inp["y"], inp["fold_id"]
@@ -57,12 +60,23 @@ def compare_cells(g, o, inp, loss, cells=None, delta=2.0 ** -6):
         if lo == hi:
             worst["beta"] = max(worst["beta"], abs(bg - bo) / max(1.0, abs(bo)))
         co, cg = o["cv_sum"][s, q, v, l], g["cv_sum"][s, q, v, l]
+        if lo < hi:
+            # the intercept is not unique and the held-out loss depends on
+            # it: the expected sum is the oracle's held-out loss at the
+            # oracle's alpha and the GPU's (admissible) intercept
+            co = float(OL.eval_loss(loss, y[H], Kc @ ao[T] + bg, tau).sum())
+        if cv_expected is not None:
+            cv_expected[s, q, v, l] = co
         assert abs(cg - co) <= CV_RTOL * max(1.0, abs(co)), ((s, q, v, l), cg, co)
         worst["cv"] = max(worst["cv"], abs(cg - co) / max(1.0, abs(co)))
         if loss != "check":
-            fH = Kc @ ao[T] + bo
+            # misclassified held-out points at the oracle's alpha and the
+            # intercept the sum above was held to; points within 1e-6 of the
+            # boundary may go either way
+            fH = Kc @ ao[T] + (bg if lo < hi else bo)
             border = int(np.count_nonzero(np.abs(fH) < 1e-6))
-            assert abs(int(g["cv_err"][s, q, v, l]) - int(o["cv_err"][s, q, v, l])) <= border
+            eo = int(np.count_nonzero(y[H] * fH <= 0.0)) if lo < hi else int(o["cv_err"][s, q, v, l])
+            assert abs(int(g["cv_err"][s, q, v, l]) - eo) <= border, ((s, q, v, l), g["cv_err"][s, q, v, l], eo)
     return worst
 
 
@@ -71,3 +85,16 @@ def kkt_of(Kv, yT, a, b, lam, loss, delta, tau):
     f = Kv @ a + b
     z = OL.point_psi(loss, yT, f, delta, tau) / n
     return n * max(np.abs(z + 2 * lam * a).max(), abs(z.sum()))
+
+
+def expected_selection(o, cv_expected, lambdas, n):
+    """Selected lambda index per (sigma, tau) from the expected held-out sums
+    (the oracle's selection rule: argmin of the pooled mean, ties to the
+    larger lambda)."""
+    from oracle.path import select
+    S, Q = cv_expected.shape[:2]
+    out = np.zeros((S, Q), dtype=np.int32)
+    for s in range(S):
+        for q in range(Q):
+            out[s, q], _ = select(cv_expected[s, q], lambdas, n)
+    return out

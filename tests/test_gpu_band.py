@@ -91,3 +91,15 @@ def test_band_c2_sized_fold():
     announce("band reduction C2 fold 0, N=1600")
     Q, band = _reduce(Kv[None].copy())
     _check(Kv[None], Q, band)
+
+
+def test_band_long_panels():
+    """Orders above 2048 + 16 rows take the streaming panel factorisation
+    (the panel no longer fits in registers) for the first panels."""
+    N = 2176
+    rng = np.random.default_rng(11)
+    B = rng.standard_normal((N, N))
+    A = (B + B.T)[None]
+    announce(f"band reduction random symmetric N={N} (streaming panels)")
+    Q, band = _reduce(A.copy())
+    _check(A, Q, band)
