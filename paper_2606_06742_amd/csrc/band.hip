@@ -655,11 +655,15 @@ __global__ void clear_reflector_rows_kernel(double* __restrict__ A, int N, int64
   A[(int64_t)g * N * N + (int64_t)r * N + c] = 0.0;
 }
 
-__global__ void set_identity_band_kernel(double* __restrict__ Q, int N, int64_t total) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= total) return;
-  const int64_t e = idx % ((int64_t)N * N);
-  Q[idx] = (e / N == e % N) ? 1.0 : 0.0;
+// Q_g = I for every matrix: one grid row per matrix (blockIdx.y), a
+// grid-stride loop over its N*N entries, so that no launch dimension
+// exceeds the 2^32 work-items a dispatch can describe.
+__global__ void set_identity_band_kernel(double* __restrict__ Q, int N) {
+  const int64_t nn = (int64_t)N * N;
+  double* Qg = Q + (int64_t)blockIdx.y * nn;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < nn; e += stride)
+    Qg[e] = (e / N == e % N) ? 1.0 : 0.0;
 }
 
 template <typename F>
@@ -773,9 +777,9 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     hipLaunchKernelGGL(clear_reflector_rows_kernel, dim3((unsigned)ceil_div(tz, 256)), dim3(256), 0,
                        s, wk.A, N, tz);
     KMP_LAUNCH_CHECK();
-    const int64_t tq = (int64_t)G * N * N;
-    hipLaunchKernelGGL(set_identity_band_kernel, dim3((unsigned)ceil_div(tq, 256)), dim3(256), 0, s,
-                       wk.Q, N, tq);
+    const int64_t bx = std::min<int64_t>(ceil_div((int64_t)N * N, 256), 1 << 20);
+    hipLaunchKernelGGL(set_identity_band_kernel, dim3((unsigned)bx, (unsigned)G), dim3(256), 0, s,
+                       wk.Q, N);
     KMP_LAUNCH_CHECK();
   }
   // Q = H_0 H_1 ... (reflector rows 0 .. N-BB-1), accumulated backwards in

@@ -281,6 +281,14 @@ __device__ __forceinline__ void band_solve(const double* __restrict__ Vc,
   wave_sync();
 }
 
+// Fences that order device-memory stores of some lanes of a wavefront
+// before loads of the same addresses by other lanes of it.
+__device__ __forceinline__ void grid_vec_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
 // The same solve for orders whose vector does not fit in LDS. Row r =
 // BND I + a belongs to the lead lane (a, 0) of the wavefront: it alone takes
 // the input of the row (win(r), from data written before the kernel), keeps
@@ -765,10 +773,14 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
   const double bn = bb - db;
   const double bold = beta[gc];
   double rd = 0.0;
+  // x = M^{-1} w: in LDS (xs), or (GV) in this column's e vector, which the
+  // step below overwrites row by row after reading it
+  const double* xsrc = xs;
   if constexpr (GV) {
-    // lead lanes: w of the row from its inputs, forward results kept in
-    // a+ (anew), and the step of the row as soon as x_r is known
+    // lead lanes form w of their rows from the inputs (prefetched ahead in
+    // the sweep), keep forward results in a+ (anew) and store x in e
     const int64_t sPk = sP;
+    double* xg = estep + base;
     band_solve_g(
         Vfac + gc * (int64_t)BND * N, Dfac + base, anew + base, xs, N, lane,
         [&](int r) {
@@ -781,41 +793,36 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
           }
           return fma(2.0 * lam, abar[ic], z);
         },
-        [&](int r, double x) {
-          const int64_t ic = base + r;
-          const double da = fma(sa, vhat[ic], x);
-          const double an = abar[ic] - da;
-          const double e = an - ahat[ic];
-          rd = fma(da, e, rd);
-          anew[ic] = an;
-          estep[ic] = e;
-        });
+        [&](int r, double x) { xg[r] = x; });
+    // x was written by the lead lanes and is read by every lane below
+    grid_vec_sync();
+    xsrc = xg;
   } else {
     wave_sync();
     band_solve(Vfac + gc * (int64_t)BND * N, Dfac + base, xs, N, lane);
-    for (int i0 = 0; i0 < N; i0 += 64 * UL) {
-      double vh[UL], ab[UL], ah[UL], xv[UL];
+  }
+  for (int i0 = 0; i0 < N; i0 += 64 * UL) {
+    double vh[UL], ab[UL], ah[UL], xv[UL];
 #pragma unroll
-      for (int q = 0; q < UL; ++q) {
-        const int i = i0 + lane + 64 * q;
-        const int ii = (i < N) ? i : N - 1;
-        const int64_t ic = base + ii;
-        vh[q] = vhat[ic];
-        ab[q] = abar[ic];
-        ah[q] = ahat[ic];
-        xv[q] = xs[ii];
-      }
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      const int ii = (i < N) ? i : N - 1;
+      const int64_t ic = base + ii;
+      vh[q] = vhat[ic];
+      ab[q] = abar[ic];
+      ah[q] = ahat[ic];
+      xv[q] = xsrc[ii];
+    }
 #pragma unroll
-      for (int q = 0; q < UL; ++q) {
-        const int i = i0 + lane + 64 * q;
-        if (i < N) {
-          const double da = fma(sa, vh[q], xv[q]);
-          const double an = ab[q] - da;
-          const double e = an - ah[q];
-          rd = fma(da, e, rd);
-          anew[base + i] = an;
-          estep[base + i] = e;
-        }
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      if (i < N) {
+        const double da = fma(sa, vh[q], xv[q]);
+        const double an = ab[q] - da;
+        const double e = an - ah[q];
+        rd = fma(da, e, rd);
+        anew[base + i] = an;
+        estep[base + i] = e;
       }
     }
   }

@@ -293,11 +293,14 @@ __global__ __launch_bounds__(TB) void tri_finish_kernel(double* __restrict__ P,
   for (int i = jlast + 1 + t; i < N; i += TB) wr[i] = fma(c, v[i], wr[i]);
 }
 
-__global__ void set_identity_kernel(double* __restrict__ Q, int N, int64_t total) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= total) return;
-  const int64_t e = idx % ((int64_t)N * N);
-  Q[idx] = (e / N == e % N) ? 1.0 : 0.0;
+// Q_g = I, one grid row per matrix (blockIdx.y) and a grid-stride loop, so
+// that no launch dimension exceeds 2^32 work-items.
+__global__ void set_identity_kernel(double* __restrict__ Q, int N) {
+  const int64_t nn = (int64_t)N * N;
+  double* Qg = Q + (int64_t)blockIdx.y * nn;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < nn; e += stride)
+    Qg[e] = (e / N == e % N) ? 1.0 : 0.0;
 }
 
 // Compact-WY factor of kb consecutive reflectors (LAPACK dlarft, forward):
@@ -482,9 +485,9 @@ int tridiagonalize_multi(const hipStream_t* ss, const TridiagWork* ws, int nch) 
   // reflectors: Q[p+1:, p+1:] -= V' (T (V Q[p+1:, p+1:])).
   for (int k = 0; k < nch; ++k) {
     if (ws[k].G <= 0) continue;
-    const int64_t tot = (int64_t)ws[k].G * N * N;
-    hipLaunchKernelGGL(set_identity_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, ss[k],
-                       ws[k].Q, N, tot);
+    const int64_t bx = std::min<int64_t>(ceil_div((int64_t)N * N, 256), 1 << 20);
+    hipLaunchKernelGGL(set_identity_kernel, dim3((unsigned)bx, (unsigned)ws[k].G), dim3(256), 0,
+                       ss[k], ws[k].Q, N);
     KMP_LAUNCH_CHECK();
   }
   const int last = ((N - 2) / NBQ) * NBQ;

@@ -103,3 +103,41 @@ def test_band_long_panels():
     announce(f"band reduction random symmetric N={N} (streaming panels)")
     Q, band = _reduce(A.copy())
     _check(A, Q, band)
+
+
+def test_band_groups_beyond_32bit_grid():
+    """Five folds of order 29376 (more than 2^32 entries over the batch, as
+    with five folds of 32000 points): every group is reduced, identical
+    inputs give identical factors, and sampled rows of Q B Q' reproduce the
+    input."""
+    import torch
+    from paper_2606_06742_amd import kmpath as km
+    dev = device()
+    N, G = 29376, 5
+    announce(f"band reduction G={G} N={N} ({G * N * N} entries)")
+    torch.manual_seed(0)
+    X = torch.randn(N, 8, dtype=torch.float64, device=dev)
+    d2 = (X * X).sum(1)
+    A0 = torch.exp(-(d2[:, None] + d2[None, :] - 2 * X @ X.T).clamp_min(0) / 16.0)
+    A0.fill_diagonal_(1.0)
+    A = torch.empty((G, N, N), dtype=torch.float64, device=dev)
+    for g in range(G):
+        A[g] = A0
+    Q = torch.empty_like(A)
+    band = torch.empty((G, km.KMP_BAND + 1, N), dtype=torch.float64, device=dev)
+    km.kmp_band_reduce(A, Q, band)
+    torch.cuda.synchronize()
+    del A
+    for g in range(1, G):
+        assert torch.equal(Q[g], Q[0]) and torch.equal(band[g], band[0]), g
+    Q0 = Q[0]
+    assert (Q0[:, :64].T @ Q0[:, :64] - torch.eye(64, dtype=torch.float64, device=dev)).abs().max().item() <= 40 * N * EPS
+    b = band[0]
+    for i in (0, 1, N // 2, N - 1):
+        q = Q0[i]
+        r = b[0] * q                                     # r = B q (B symmetric, banded)
+        for k in range(1, km.KMP_BAND + 1):
+            r[k:] += b[k, :N - k] * q[:N - k]
+            r[:N - k] += b[k, :N - k] * q[k:]
+        row = Q0 @ r
+        assert (row - A0[i]).abs().max().item() <= 40 * N * EPS, i

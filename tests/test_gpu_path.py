@@ -153,3 +153,50 @@ def test_path_c4_full_parity():
     assert np.array_equal(g["selected"], expected_selection(o, cv, inp["lambdas"], inp["X"].shape[0]))
     print("C4 worst", worst, "iterations", g["timings"]["iterations"],
           g["timings"]["cell_iterations"])
+
+
+def test_path_c3_full_size_sampled():
+    """Smoothed-hinge SVM at full size (n = 10000, d = 100, 10 folds, 100
+    lambdas in [1e-6, 1e1]; 9000 training points per fold).
+
+    Every cell must converge. On fold 0, sampled cells are solved by the
+    oracle and compared at the usual bars, and every cell's stationarity
+    residual is measured under the oracle's kernel matrix. The GPU iterates
+    to its tolerance on its own factorisation Q B Q' of its own Gram matrix,
+    whose entries differ from the oracle's by a few N eps; through the loss
+    curvature 1/(2 delta) that moves the residual by up to
+    (1/(2 delta)) max_i sum_j |dK_ij| |alpha_j| <= (1/(2 delta)) 4 N eps
+    ||alpha||_1, which is the allowance added to the tolerance."""
+    w = W.get("C3")
+    inp = W.make_inputs(w)
+    announce("fit_path C3 full size (hinge, n=10000, d=100, 10 folds, 100 lambdas)")
+    g = _gpu(inp, "hinge")
+    print("C3 timings", {k: v for k, v in g["timings"].items() if not isinstance(v, list)}, flush=True)
+    y, fold = inp["y"], inp["fold_id"]
+    delta = 2.0 ** -6
+    Kv, Kc, T, H = OG.fold_blocks(inp["X"], fold, 0, inp["sigmas"][0])
+    n, N = T.size, int(np.ceil(T.size / 64) * 64)
+    eps = np.finfo(float).eps
+    worst = 0.0
+    for l in range(w.L):
+        a = g["alpha"][0, 0, 0, l][T]
+        k = kkt_of(Kv, y[T], a, g["beta"][0, 0, 0, l], inp["lambdas"][l], "hinge", delta, None)
+        bar = 2e-9 + (1.0 / (2.0 * delta)) * 4.0 * N * eps * np.abs(a).sum()
+        assert k <= bar, (l, k, bar)
+        worst = max(worst, k / bar)
+    cells = [(0, 0, 0, l) for l in (10, 20, 45, 70, 99)]
+    o = {k: np.zeros_like(g[k]) for k in ("alpha", "beta", "objective", "cv_sum", "cv_err")}
+    o["beta_lo"] = np.zeros_like(g["beta"])
+    o["beta_hi"] = np.zeros_like(g["beta"])
+    for (s, q, v, l) in cells:
+        lam = inp["lambdas"][l]
+        a, b, info = oracle.solve_cell(Kv, y[T], lam, "hinge", delta)
+        o["alpha"][s, q, v, l][T] = a
+        o["beta"][s, q, v, l] = b
+        o["beta_lo"][s, q, v, l], o["beta_hi"][s, q, v, l] = oracle.beta_interval(Kv, y[T], a, b, "hinge", delta, None)
+        o["objective"][s, q, v, l] = oracle.objective(Kv, y[T], a, b, lam, "hinge", delta)
+        fH = Kc @ a + b
+        o["cv_sum"][s, q, v, l] = oracle.losses.eval_loss("hinge", y[H], fH).sum()
+        o["cv_err"][s, q, v, l] = np.count_nonzero(y[H] * fH <= 0)
+    worst_cells = compare_cells(g, o, inp, "hinge", cells=cells)
+    print("C3 sampled worst", worst_cells, "stationarity / allowance", worst)
