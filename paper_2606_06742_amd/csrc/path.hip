@@ -844,6 +844,138 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
   }
 }
 
+// The update of one column per 256-thread workgroup, for orders whose
+// vector fits in LDS (N <= kLdsVecMax): the element passes are spread over
+// the four wavefronts (four times the loads in flight of one wavefront) and
+// wavefront 0 alone runs the banded solve on the LDS vector:
+//   w = zhat + 2 lambda abar (LDS), t = u'w, ||w||, d0; KKT decision;
+//   x = M^{-1} w (wavefront 0); a+ = abar - g (t - d0) vhat - x,
+//   e = a+ - ahat, restart test, momentum coefficient.
+// a+ and e go to device memory for momentum_kernel, whose row tiles form
+// abar, ahat and B abar in parallel (the band product inside this kernel,
+// 256 threads per column, measured slower). Reductions are block sums in a
+// fixed order. LDS: N doubles.
+__global__ __launch_bounds__(256) void update_column_kernel(
+    int N, int C, int RT, const int* __restrict__ nvv, const double* __restrict__ lamv,
+    const double* __restrict__ zpart, int S2, int64_t sP, double* __restrict__ ahat,
+    const double* __restrict__ abar, double* __restrict__ anew, double* __restrict__ estep,
+    double* __restrict__ coefv, const double* __restrict__ Vfac, const double* __restrict__ Dfac,
+    const double* __restrict__ vhat, const double* __restrict__ uvec,
+    const double* __restrict__ gcoef, const double* __restrict__ partial,
+    double* __restrict__ beta, double* __restrict__ bbar, double* __restrict__ rmom,
+    double* __restrict__ kktv, int* __restrict__ flag, int* __restrict__ iters,
+    int* __restrict__ iters_total, int* __restrict__ moved, double tol, int max_iter,
+    int restart) {
+  extern __shared__ double lds_dyn[];
+  __shared__ double red[PW];
+  const int t = threadIdx.x, wv = t >> 6, lane = t & 63;
+  const int64_t gc = blockIdx.x;
+  if (flag[gc] != 0) {                                  // uniform over the block
+    if (t == 0) moved[gc] = 0;
+    return;
+  }
+  double* xs = lds_dyn;                                 // w, then x
+  const int g = (int)(gc / C), c = (int)(gc % C);
+  const int64_t base = gc * (int64_t)N;
+  const double lam = lamv[gc];
+  const double nvd = (double)nvv[g];
+  double d0 = 0.0;
+  {
+    const double* pg = partial + (int64_t)g * RT * C + c;
+    for (int r = t; r < RT; r += PB) d0 += pg[(int64_t)r * C];
+  }
+  double tl = 0.0, n2 = 0.0;
+  for (int i0 = 0; i0 < N; i0 += PB * 4) {
+    double zs[4], ab[4], uv[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + t + PB * q;
+      const int64_t ic = base + ((i < N) ? i : N - 1);
+      double z = zpart[ic];
+#pragma unroll
+      for (int sk = 1; sk < kMaxSplitK; ++sk) {
+        const double zz = zpart[(sk < S2 ? sk : 0) * sP + ic];
+        z += (sk < S2) ? zz : 0.0;
+      }
+      zs[q] = z;
+      ab[q] = abar[ic];
+      uv[q] = uvec[ic];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + t + PB * q;
+      if (i < N) {
+        const double w = fma(2.0 * lam, ab[q], zs[q]);
+        xs[i] = w;
+        tl = fma(uv[q], w, tl);
+        n2 = fma(w, w, n2);
+      }
+    }
+  }
+  d0 = block_sum<PW>(d0, red);
+  const double tsum = block_sum<PW>(tl, red);
+  const double n2sum = block_sum<PW>(n2, red);
+  const double kkt = nvd * fmax(sqrt(n2sum), fabs(d0));
+  const double bb = bbar[gc];
+  if (!(kkt == kkt) || kkt > 1e300) {                   // non-finite (uniform)
+    if (t == 0) { flag[gc] = 3; kktv[gc] = kkt; moved[gc] = 0; }
+    return;
+  }
+  if (kkt <= tol) {                                     // certified at the extrapolated point
+    for (int i = t; i < N; i += PB) ahat[base + i] = abar[base + i];
+    if (t == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; moved[gc] = 0; }
+    return;
+  }
+  __syncthreads();                                      // w complete in LDS
+  if (wv == 0) band_solve(Vfac + gc * (int64_t)BND * N, Dfac + base, xs, N, lane);
+  __syncthreads();                                      // x complete in LDS
+  const double gco = gcoef[gc];
+  const double sa = gco * (tsum - d0);
+  const double db = gco * (d0 - tsum);
+  const double bn = bb - db;
+  const double bold = beta[gc];
+  double rd = 0.0;
+  for (int i0 = 0; i0 < N; i0 += PB * 4) {
+    double vh[4], ab[4], ah[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + t + PB * q;
+      const int64_t ic = base + ((i < N) ? i : N - 1);
+      vh[q] = vhat[ic];
+      ab[q] = abar[ic];
+      ah[q] = ahat[ic];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + t + PB * q;
+      if (i < N) {
+        const double da = fma(sa, vh[q], xs[i]);
+        const double an = ab[q] - da;
+        const double e = an - ah[q];
+        rd = fma(da, e, rd);
+        anew[base + i] = an;
+        estep[base + i] = e;
+      }
+    }
+  }
+  rd = block_sum<PW>(rd, red) + db * (bn - bold);
+  const double r = rmom[gc];
+  const double rn = (restart && rd > 0.0) ? 1.0 : 0.5 * (1.0 + sqrt(1.0 + 4.0 * r * r));
+  const double coef = (rn - 1.0) / (0.5 * (1.0 + sqrt(1.0 + 4.0 * rn * rn)));
+  if (t == 0) {
+    coefv[gc] = coef;
+    moved[gc] = 1;
+    beta[gc] = bn;
+    bbar[gc] = fma(coef, bn - bold, bn);
+    rmom[gc] = rn;
+    kktv[gc] = kkt;
+    const int it = iters[gc] + 1;
+    iters[gc] = it;
+    iters_total[gc] += 1;
+    if (it >= max_iter) flag[gc] = 2;
+  }
+}
+
 // abar = a+ + coef e, ahat = a+, bmat = B abar for the columns that moved;
 // one workgroup per (row tile, column) as in band_apply_kernel.
 __global__ __launch_bounds__(BT) void momentum_kernel(
@@ -910,6 +1042,28 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP, p.cmap, p.nact)) != 0) return rc;
   kc_end(KMP_KC_GEMM_ZHAT, s, gbytes, gflops);
   const int64_t cols = (int64_t)p.G * p.C;
+  if (!path_global_vec(p)) {
+    // one workgroup per column, momentum and B abar included
+    const size_t lds_u = sizeof(double) * (size_t)p.N;
+    KMP_HIP_TRY(hipFuncSetAttribute((const void*)update_column_kernel,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_u));
+    kc_begin(KMP_KC_UPDATE, s);
+    hipLaunchKernelGGL(update_column_kernel, dim3((unsigned)cols), dim3(PB), lds_u, s, p.N, p.C, RT,
+                       p.nv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.anew, p.estep, p.coef,
+                       p.ldl_l, p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom,
+                       p.kkt, p.flag, p.iters, p.iters_total, p.moved, tol, max_iter, restart);
+    KMP_LAUNCH_CHECK();
+    hipLaunchKernelGGL(momentum_kernel, dim3((unsigned)ceil_div(p.N, BT), (unsigned)cols), dim3(BT), 0,
+                       s, p.N, p.C, p.band, p.moved, p.coef, p.anew, p.estep, p.ahat, p.abar, p.bmat);
+    KMP_LAUNCH_CHECK();
+    // per column element: S2 zhat parts, abar (twice), u, the factor tiles
+    // (BND each, forward and backward), 1/d, vhat, ahat read; ahat, abar and
+    // B abar written (band read per row)
+    kc_end(KMP_KC_UPDATE, s,
+           over_active(p, [&](double n, double c) { return 8.0 * (S2 + 2.0 * BND + 9.0) * n * c; }),
+           over_active(p, [&](double n, double c) { return (8.0 * BND + 16.0) * n * c; }));
+    return 0;
+  }
   const int cw = path_waves(p, 0);
   const size_t lds = sizeof(double) * (size_t)cw * path_lds_doubles(p, 0);
   const bool gv = path_global_vec(p);
