@@ -677,9 +677,67 @@ size_t band_part_doubles(int G, int N) {
   return (size_t)G * ceil_div(N, TSK) * 64 * 64;
 }
 
+int wy_blocks(int N) { return N > BB ? (int)ceil_div(N - BB, kWyBlock) : 0; }
+
+size_t wy_all_doubles(int G, int N) {
+  return (size_t)std::max(1, wy_blocks(N)) * G * kWyBlock * kWyBlock;
+}
+
 size_t band_work_doubles(int G, int N) {
   return (size_t)G * (3 * (size_t)BB * N + 2 * (size_t)kWyBlock * kWyBlock +
-                      2 * (size_t)kWyBlock * N) + band_part_doubles(G, N);
+                      2 * (size_t)kWyBlock * N) + band_part_doubles(G, N) +
+         2 * wy_all_doubles(G, N);
+}
+
+// Gram matrices of all blocks of kWyBlock reflector rows at once, on the
+// matrix cores: workgroup (b, g) forms G[a][c] = sum_k V[a][k] V[c][k] for
+// the reflectors q = 64 b .. q + kb - 1 of matrix g (row q + a of A holds
+// v_{q+a} from column q + a + BB, zeros before it, so the sum runs over the
+// columns q + BB .. N-1). Wave w computes the 32 x 32 quadrant (32 (w&1),
+// 32 (w>>1)) as 2 x 2 MFMA blocks over 16-column slices staged in LDS.
+__global__ __launch_bounds__(256) void wy_gram_kernel(const double* __restrict__ A, int N, int nref,
+                                                       double* __restrict__ gram_all) {
+  __shared__ double Vs[kWyBlock][BB + 1];
+  const int b = blockIdx.x, g = blockIdx.y, G = gridDim.y;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int q = kWyBlock * b;
+  const int kb = min(kWyBlock, nref - q);
+  const int m = N - q - BB;
+  const double* Vq = A + (int64_t)g * N * N + (int64_t)q * N + q + BB;
+  const int wi = 32 * (w & 1), wj = 32 * (w >> 1);
+  const int li = lane & 15, lk = lane >> 4;
+  xdbl4 acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) acc[x][y] = xdbl4{0.0, 0.0, 0.0, 0.0};
+  const int lr = t >> 2, lc = (t & 3) * 4;        // loader: row lr, columns lc .. lc+3
+  for (int c0 = 0; c0 < m; c0 += BB) {
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = c0 + lc + u;
+      Vs[lr][lc + u] = (lr < kb && c < m) ? Vq[(int64_t)lr * N + c] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int s4 = 0; s4 < BB; s4 += 4) {
+      const double a0 = Vs[wi + li][s4 + lk], a1 = Vs[wi + 16 + li][s4 + lk];
+      const double b0 = Vs[wj + li][s4 + lk], b1 = Vs[wj + 16 + li][s4 + lk];
+      acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
+    }
+  }
+  double* Gg = gram_all + ((int64_t)b * G + g) * kWyBlock * kWyBlock;
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        Gg[(wi + 16 * x + mfma_row(lane, r)) * kWyBlock + wj + 16 * y + mfma_col(lane)] = acc[x][y][r];
 }
 
 int band_reduce(hipStream_t s, const BandWork& wk) {
@@ -784,18 +842,21 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
   }
   // Q = H_0 H_1 ... (reflector rows 0 .. N-BB-1), accumulated backwards in
   // blocks of kWyBlock rows: Q[q+BB:, q+BB:] -= V' (T (V Q[q+BB:, q+BB:])).
+  // The Grams and T factors of all blocks depend on the reflectors only and
+  // are formed first, two launches for all blocks.
   const int nref = N - BB;
+  const int nblk = wy_blocks(N);
+  kc_begin(KMP_KC_QFORM, s);
+  hipLaunchKernelGGL(wy_gram_kernel, dim3((unsigned)nblk, (unsigned)G), dim3(256), 0, s, wk.A, N, nref,
+                     wk.gram_all);
+  KMP_LAUNCH_CHECK();
+  if ((rc = wy_form_t_blocks(s, wk.gram_all, wk.tau, wk.tmat_all, G, N, nref, nblk)) != 0) return rc;
   const int last = ((nref - 1) / kWyBlock) * kWyBlock;
   for (int q = last; q >= 0; q -= kWyBlock) {
     const int kb = std::min(kWyBlock, nref - q);
     const int m = N - q - BB;
-    kc_begin(KMP_KC_QFORM, s);
-    // Gram of the block's reflectors
-    const double* Vq = wk.A + (int64_t)q * N + q + BB;
-    if ((rc = ts_gram(s, kb, kb, m, G, Vq, N, (int64_t)N * N, Vq, N, (int64_t)N * N, wk.gram,
-                      kWyBlock, (int64_t)kWyBlock * kWyBlock, wk.part)) != 0)
-      return rc;
-    if ((rc = wy_form_t(s, wk.gram, wk.tau, wk.tmat, G, N, kb, q)) != 0) return rc;
+    if (q != last) kc_begin(KMP_KC_QFORM, s);
+    const double* tq = wk.tmat_all + (int64_t)(q / kWyBlock) * G * kWyBlock * kWyBlock;
     GemmArgs h1;   // X = V Q[q+BB:, q+BB:]   (kb x m)
     h1.M = kb; h1.N = m; h1.K = m; h1.batch = G;
     h1.A = wk.A + (int64_t)q * N + q + BB; h1.lda = N; h1.sA = (int64_t)N * N;
@@ -804,7 +865,7 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     if ((rc = gemm(s, h1, true, false, true)) != 0) return rc;
     GemmArgs h2;   // Y = T X
     h2.M = kb; h2.N = m; h2.K = kb; h2.batch = G;
-    h2.A = wk.tmat; h2.lda = kWyBlock; h2.sA = (int64_t)kWyBlock * kWyBlock;
+    h2.A = tq; h2.lda = kWyBlock; h2.sA = (int64_t)kWyBlock * kWyBlock;
     h2.B = wk.xbuf; h2.ldb = N; h2.sB = (int64_t)kWyBlock * N;
     h2.C = wk.ybuf; h2.ldc = N; h2.sC = (int64_t)kWyBlock * N;
     if ((rc = gemm(s, h2, true, false, true)) != 0) return rc;

@@ -90,17 +90,27 @@ struct BandWork {
   double* xbuf = nullptr;   // G x 64 x N
   double* ybuf = nullptr;   // G x 64 x N
   double* part = nullptr;   // band_part_doubles(G, N): chunk partials of the Gram products
+  double* gram_all = nullptr;  // wy_blocks(N) x G x 64 x 64: Grams of the WY blocks of Q
+  double* tmat_all = nullptr;  // same shape: their T factors
   const int* nv_host = nullptr;  // G valid orders (host), for the work counters; N if null
 };
 // Doubles of scratch band_reduce needs beyond A, Q, band and tau (the chunk
 // partials included), and of the chunk partials alone.
 size_t band_work_doubles(int G, int N);
 size_t band_part_doubles(int G, int N);
+// Number of kWyBlock-reflector blocks in which Q is accumulated, and the
+// doubles of one of the gram_all / tmat_all buffers.
+int wy_blocks(int N);
+size_t wy_all_doubles(int G, int N);
 int band_reduce(hipStream_t s, const BandWork& w);
 // Compact-WY T factor (kb x kb, ld 64, per matrix) of reflectors p .. p+kb-1
 // from their Gram matrix (ld 64) and tau[g*N + p + i].
 int wy_form_t(hipStream_t s, const double* gram, const double* taus, double* tmat, int G, int N,
               int kb, int p);
+// The same for all nblk blocks of kWyBlock reflectors 0 .., nref at once:
+// block b's Gram and T at gram / tmat + b * G * 64 * 64 (+ g * 64 * 64).
+int wy_form_t_blocks(hipStream_t s, const double* gram, const double* taus, double* tmat, int G,
+                     int N, int nref, int nblk);
 
 // --------------------------------------------------------- tridiagonal
 struct TridiagWork {

@@ -311,14 +311,23 @@ __global__ void set_identity_kernel(double* __restrict__ Q, int N) {
 // Everything stays in LDS; six levels of small products for kb <= 64.
 constexpr int NBQ = 64;
 constexpr int FTT = 256;   // threads of form_t_kernel
+// With nref > 0 the launch covers many blocks at once: grid row y is block
+// y (reflectors p + NBQ y .., kb = min(NBQ, nref - p - NBQ y)), whose Gram
+// and T sit at gram / tmat + y * bstride (+ g NBQ^2 within the block).
 __global__ __launch_bounds__(FTT) void form_t_kernel(const double* __restrict__ gram,
                                                      const double* __restrict__ taus,
                                                      double* __restrict__ tmat, int N, int kb,
-                                                     int p) {
+                                                     int p, int nref, int64_t bstride) {
   __shared__ double T[NBQ][NBQ + 1];
   __shared__ double Gs[NBQ][NBQ + 1];
   __shared__ double Ws[NBQ][NBQ + 1];
   const int g = blockIdx.x, t = threadIdx.x;
+  if (nref > 0) {
+    p += NBQ * blockIdx.y;
+    kb = min(NBQ, nref - p);
+    gram += (int64_t)blockIdx.y * bstride;
+    tmat += (int64_t)blockIdx.y * bstride;
+  }
   const double* gr = gram + (int64_t)g * NBQ * NBQ;
   for (int e = t; e < NBQ * NBQ; e += FTT) {
     const int a = e / NBQ, b = e % NBQ;
@@ -352,7 +361,17 @@ __global__ __launch_bounds__(FTT) void form_t_kernel(const double* __restrict__ 
 
 int wy_form_t(hipStream_t s, const double* gram, const double* taus, double* tmat, int G, int N,
               int kb, int p) {
-  hipLaunchKernelGGL(form_t_kernel, dim3(G), dim3(FTT), 0, s, gram, taus, tmat, N, kb, p);
+  hipLaunchKernelGGL(form_t_kernel, dim3(G), dim3(FTT), 0, s, gram, taus, tmat, N, kb, p, 0,
+                     (int64_t)0);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
+int wy_form_t_blocks(hipStream_t s, const double* gram, const double* taus, double* tmat, int G,
+                     int N, int nref, int nblk) {
+  if (nblk <= 0) return 0;
+  hipLaunchKernelGGL(form_t_kernel, dim3(G, nblk), dim3(FTT), 0, s, gram, taus, tmat, N, 0, 0,
+                     nref, (int64_t)G * NBQ * NBQ);
   KMP_LAUNCH_CHECK();
   return 0;
 }
@@ -507,7 +526,8 @@ int tridiagonalize_multi(const hipStream_t* ss, const TridiagWork* ws, int nch) 
       g0.B = wk.A + (int64_t)p * N + p + 1; g0.ldb = N; g0.sB = (int64_t)N * N;
       g0.C = wk.gram; g0.ldc = NBQ; g0.sC = (int64_t)NBQ * NBQ;
       if ((rc = gemm(s, g0, true, true, true)) != 0) return rc;
-      hipLaunchKernelGGL(form_t_kernel, dim3(G), dim3(FTT), 0, s, wk.gram, wk.tau, wk.tmat, N, kb, p);
+      hipLaunchKernelGGL(form_t_kernel, dim3(G), dim3(FTT), 0, s, wk.gram, wk.tau, wk.tmat, N, kb, p,
+                         0, (int64_t)0);
       KMP_LAUNCH_CHECK();
       GemmArgs g1;   // X = V[:, p+1:] Q[p+1:, p+1:]   (kb x m)
       g1.M = kb; g1.N = m; g1.K = m; g1.batch = G;
