@@ -63,13 +63,13 @@ __device__ __forceinline__ void block_sum_vec(double (&h)[BB], int lo, double (*
 // step i+1 are made in one pass over the rows.
 // Outputs: tau[p+i], and v_i transposed into row p+i of A (columns m0 ..,
 // zeros before its leading 1) and into rows i and 2BB+i of the panel buffer.
-__global__ __launch_bounds__(PQT) void panel_qr_kernel(double* __restrict__ A, int N, int p,
-                                                        double* __restrict__ taus,
-                                                        double* __restrict__ panel) {
+__device__ __forceinline__ void panel_qr_stream_body(double* __restrict__ A, int N, int p,
+                                                     double* __restrict__ taus,
+                                                     double* __restrict__ panel, int g) {
   __shared__ double red[PQW][BB];
   __shared__ double hs[BB];
   __shared__ double ws[BB];
-  const int g = blockIdx.x, t = threadIdx.x;
+  const int t = threadIdx.x;
   double* Ag = A + (int64_t)g * N * N;
   const int m0 = p + BB, mrow = N - m0;
   double* P = Ag + (int64_t)m0 * N + p;    // P[r][c] = P[r*N + c]
@@ -137,6 +137,12 @@ __global__ __launch_bounds__(PQT) void panel_qr_kernel(double* __restrict__ A, i
     Vt[(int64_t)i * N + m0 + r] = v;
     Vt[(int64_t)(2 * BB + i) * N + m0 + r] = v;
   }
+}
+
+__global__ __launch_bounds__(PQT) void panel_qr_kernel(double* __restrict__ A, int N, int p,
+                                                        double* __restrict__ taus,
+                                                        double* __restrict__ panel) {
+  panel_qr_stream_body(A, N, p, taus, panel, blockIdx.x);
 }
 
 // Register-resident panel factorisation with NW wavefronts: lane l of wave
@@ -280,13 +286,13 @@ __device__ __forceinline__ void panel_steps(double (&x)[RS], double (&xi)[RS],
 }
 
 template <int RS, int NW, bool CARRY>
-__global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restrict__ A, int N,
-                                                                int p, double* __restrict__ taus,
-                                                                double* __restrict__ panel,
-                                                                double* __restrict__ tmat) {
+__device__ __forceinline__ void panel_qr_vec_body(double* __restrict__ A, int N, int p,
+                                                  double* __restrict__ taus,
+                                                  double* __restrict__ panel,
+                                                  double* __restrict__ tmat, int g) {
   constexpr int RPS = 4 * NW;                      // rows per slot
   __shared__ PanelLds<NW> L;
-  const int g = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int c = lane & 15, sub = lane >> 4;
   double* Ag = A + (int64_t)g * N * N;
   const int m0 = p + BB, mrow = N - m0;
@@ -363,6 +369,14 @@ __global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restric
     for (int i = 0; i < BB; ++i) Tg[i] = tr[i];
     taus[(int64_t)g * N + p + t] = L.tau[t];
   }
+}
+
+template <int RS, int NW, bool CARRY>
+__global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restrict__ A, int N,
+                                                                int p, double* __restrict__ taus,
+                                                                double* __restrict__ panel,
+                                                                double* __restrict__ tmat) {
+  panel_qr_vec_body<RS, NW, CARRY>(A, N, p, taus, panel, tmat, blockIdx.x);
 }
 
 // Only the lower triangle of the trailing matrix is kept up to date (the
@@ -504,16 +518,14 @@ __global__ __launch_bounds__(256) void panel_w_kernel(int N, int m0, const doubl
 // outside blocks load from clamped addresses and are not stored. With LOWER
 // only the tiles on and below the diagonal are updated (C symmetric, its
 // lower triangle kept; see the note before panel_x_kernel).
-template <int KC, bool LOWER>
-__global__ __launch_bounds__(256) void rank_update_kernel(double* __restrict__ C, int64_t ldc,
-                                                           int64_t sC, int m,
-                                                           const double* __restrict__ P1,
-                                                           int64_t ld1, int64_t s1,
-                                                           const double* __restrict__ P2,
-                                                           int64_t ld2, int64_t s2) {
-  if (LOWER && blockIdx.y > blockIdx.x) return;
-  const int g = blockIdx.z, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int i0 = 64 * blockIdx.x + 32 * (w & 1), j0 = 64 * blockIdx.y + 32 * (w >> 1);
+template <int KC, bool LOWER, int PART>
+__device__ __forceinline__ void rank_update_tile(double* __restrict__ C, int64_t ldc, int64_t sC,
+                                                 int m, const double* __restrict__ P1, int64_t ld1,
+                                                 int64_t s1, const double* __restrict__ P2,
+                                                 int64_t ld2, int64_t s2, int bx, int by, int g,
+                                                 int w, int lane) {
+  const int i0 = 64 * bx + 32 * (w & 1), j0 = 64 * by + 32 * (w >> 1);
+  if (PART == 1 && j0 > 0) return;                 // waves wholly right of the strip
   double* Cg = C + (int64_t)g * sC;
   const double* A1 = P1 + (int64_t)g * s1;
   const double* A2 = P2 + (int64_t)g * s2;
@@ -556,11 +568,77 @@ __global__ __launch_bounds__(256) void rank_update_kernel(double* __restrict__ C
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-      if (vi[bi] && vj[bj]) {
+    for (int bj = 0; bj < 2; ++bj) {
+      bool st = vi[bi] && vj[bj];
+      if (PART == 1) st = st && jb[bj] == 0;
+      if (PART == 2) st = st && ib[bi] != 0 && jb[bj] != 0;
+      if (st) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) Cg[(int64_t)(ib[bi] + 4 * r + lk) * ldc + jb[bj] + li] = acc[bi][bj][r];
       }
+    }
+}
+
+template <int KC, bool LOWER, int PART = 0>
+__global__ __launch_bounds__(256) void rank_update_kernel(double* __restrict__ C, int64_t ldc,
+                                                           int64_t sC, int m,
+                                                           const double* __restrict__ P1,
+                                                           int64_t ld1, int64_t s1,
+                                                           const double* __restrict__ P2,
+                                                           int64_t ld2, int64_t s2) {
+  if (LOWER && blockIdx.y > blockIdx.x) return;
+  rank_update_tile<KC, LOWER, PART>(C, ldc, sC, m, P1, ld1, s1, P2, ld2, s2, blockIdx.x, blockIdx.y,
+                                    blockIdx.z, threadIdx.x >> 6, threadIdx.x & 63);
+}
+
+// Panel QR of the next panel and the rest of the current panel's two-sided
+// update in one launch: workgroup g < G factors panel p_next of matrix g
+// (its 16 columns were brought up to date beforehand), the other workgroups
+// apply the rank-32 update of panel p (P1/P2 from its own panel buffer) to
+// every 16 x 16 block of A22 outside its first block row and column, four
+// wavefronts per 64 x 64 tile. The two roles touch disjoint parts of A
+// (the factorisation reads the first block column of A22 and writes the
+// reflector rows of the first block row), so they run side by side and the
+// latency-bound factorisation is hidden behind the update.
+template <int TPW>
+__device__ __forceinline__ void rest_update_role(double* A, int N, int m0, int mrow, int G,
+                                                 const double* P1, const double* P2, int64_t sP,
+                                                 int tiles) {
+  // tile e of the lower triangle, row by row: (bx, by) with by <= bx
+  const int64_t e = (int64_t)(blockIdx.x - G) * TPW + (threadIdx.x >> 8);
+  const int64_t tt = (int64_t)tiles * (tiles + 1) / 2;
+  const int g = (int)(e / tt), rem = (int)(e % tt);
+  if (g >= G) return;
+  int bx = (int)((sqrt(8.0 * rem + 1.0) - 1.0) * 0.5);
+  if (bx * (bx + 1) / 2 > rem) --bx;
+  if ((bx + 1) * (bx + 2) / 2 <= rem) ++bx;
+  const int by = rem - bx * (bx + 1) / 2;
+  rank_update_tile<1, true, 2>(A + (int64_t)m0 * N + m0, (int64_t)N, (int64_t)N * N, mrow, P1,
+                               (int64_t)N, sP, P2, (int64_t)N, sP, bx, by, g,
+                               (threadIdx.x >> 6) & 3, threadIdx.x & 63);
+}
+
+template <int RS, int NW, bool CARRY>
+__global__ __launch_bounds__(64 * NW) void qr_rest_vec_kernel(
+    double* __restrict__ A, int N, int p_next, double* __restrict__ taus,
+    double* __restrict__ panel_next, double* __restrict__ tmat, int G, int m0, int mrow,
+    const double* __restrict__ P1, const double* __restrict__ P2, int64_t sP, int tiles) {
+  if (blockIdx.x < G) {
+    panel_qr_vec_body<RS, NW, CARRY>(A, N, p_next, taus, panel_next, tmat, blockIdx.x);
+    return;
+  }
+  rest_update_role<NW / 4>(A, N, m0, mrow, G, P1, P2, sP, tiles);
+}
+
+__global__ __launch_bounds__(PQT) void qr_rest_stream_kernel(
+    double* __restrict__ A, int N, int p_next, double* __restrict__ taus,
+    double* __restrict__ panel_next, int G, int m0, int mrow, const double* __restrict__ P1,
+    const double* __restrict__ P2, int64_t sP, int tiles) {
+  if (blockIdx.x < G) {
+    panel_qr_stream_body(A, N, p_next, taus, panel_next, blockIdx.x);
+    return;
+  }
+  rest_update_role<PQT / 256>(A, N, m0, mrow, G, P1, P2, sP, tiles);
 }
 
 // C[i][j] = sum_k A[i*lda + k] B[j*ldb + k] for M, Nc <= 64 and long K (per
@@ -684,7 +762,7 @@ size_t wy_all_doubles(int G, int N) {
 }
 
 size_t band_work_doubles(int G, int N) {
-  return (size_t)G * (3 * (size_t)BB * N + 2 * (size_t)kWyBlock * kWyBlock +
+  return (size_t)G * (6 * (size_t)BB * N + 2 * (size_t)kWyBlock * kWyBlock +
                       2 * (size_t)kWyBlock * N) + band_part_doubles(G, N) +
          2 * wy_all_doubles(G, N);
 }
@@ -750,18 +828,36 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
   int rc;
   const int64_t sP = (int64_t)3 * BB * N;
   KMP_HIP_TRY(hipMemsetAsync(wk.tau, 0, sizeof(double) * (size_t)G * N, s));
-  for (int p = 0; p + BB < N; p += BB) {
-    const int m0 = p + BB, mrow = N - m0;
-    kc_begin(KMP_KC_PANEL, s);
-    const int rs = (int)ceil_div(mrow, 32);
-    const bool reg = rs <= 64;     // mrow <= 2048
-#define KMP_PQR(RSV, NWV, CV)                                                                   \
-  hipLaunchKernelGGL((panel_qr_vec_kernel<RSV, NWV, CV>), dim3(G), dim3(64 * NWV), 0, s, wk.A, N, \
-                     p, wk.tau, wk.panel, wk.tmat)
-    // 8 wavefronts (32 rows per slot) up to 1280 rows, then 16 (64 rows per
-    // slot): the unrolled steps stay within the instruction cache and the
-    // slots within the registers
-    const int rs16 = (int)ceil_div(mrow, 64);
+  double* const pbuf[2] = {wk.panel, wk.panel2};
+  const auto tiles_of = [](int m) { return (int)ceil_div(m, 64); };
+  const auto dual_grid = [&](int m, int tpw) {
+    const int64_t t = tiles_of(m);
+    return (unsigned)(G + ceil_div(t * (t + 1) / 2 * G, (int64_t)tpw));
+  };
+  // Panel factorisation of panel p into buffer pb: alone (dual = false) or
+  // in one launch with the rest of the previous panel's two-sided update
+  // (dual = true; that panel's first block column is up to date already).
+  // The register kernel is chosen by the number of rows: 8 wavefronts (32
+  // rows per slot) up to 1280 rows, then 16 (64 rows per slot), so the
+  // unrolled steps stay within the instruction cache and the slots within
+  // the registers; the streaming kernel beyond 2048 rows.
+  const auto factor_panel = [&](int p, double* pb, bool dual, const double* pprev) -> int {
+    const int mrow = N - p - BB;
+    const int mprev = mrow + BB, m0prev = p;
+    const double* P1 = pprev ? pprev + m0prev : nullptr;
+    const double* P2 = pprev ? pprev + (int64_t)BB * N + m0prev : nullptr;
+    const int tp = tiles_of(mprev);
+    const int rs = (int)ceil_div(mrow, 32), rs16 = (int)ceil_div(mrow, 64);
+#define KMP_PQR(RSV, NWV, CV)                                                                     \
+  do {                                                                                            \
+    if (dual)                                                                                     \
+      hipLaunchKernelGGL((qr_rest_vec_kernel<RSV, NWV, CV>), dim3(dual_grid(mprev, NWV / 4)),     \
+                         dim3(64 * NWV), 0, s, wk.A, N, p, wk.tau, pb, wk.tmat, G, m0prev, mprev, \
+                         P1, P2, sP, tp);                                                         \
+    else                                                                                          \
+      hipLaunchKernelGGL((panel_qr_vec_kernel<RSV, NWV, CV>), dim3(G), dim3(64 * NWV), 0, s,      \
+                         wk.A, N, p, wk.tau, pb, wk.tmat);                                        \
+  } while (0)
     if (rs <= 8) KMP_PQR(8, 8, true);
     else if (rs <= 16) KMP_PQR(16, 8, true);
     else if (rs <= 24) KMP_PQR(24, 8, true);
@@ -770,60 +866,96 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     else if (rs16 <= 24) KMP_PQR(24, 16, false);
     else if (rs16 <= 32) KMP_PQR(32, 16, false);
 #undef KMP_PQR
+    else if (dual)
+      hipLaunchKernelGGL(qr_rest_stream_kernel, dim3(dual_grid(mprev, PQT / 256)), dim3(PQT), 0, s,
+                         wk.A, N, p, wk.tau, pb, G, m0prev, mprev, P1, P2, sP, tp);
     else
-      hipLaunchKernelGGL(panel_qr_kernel, dim3(G), dim3(PQT), 0, s, wk.A, N, p, wk.tau, wk.panel);
+      hipLaunchKernelGGL(panel_qr_kernel, dim3(G), dim3(PQT), 0, s, wk.A, N, p, wk.tau, pb);
     KMP_LAUNCH_CHECK();
-    // panel read twice per column step and written once (algorithmic: once)
-    kc_end(KMP_KC_PANEL, s, over_groups(wk, [&](double n) {
-             return 16.0 * std::max(0.0, n - m0) * BB; }),
-           over_groups(wk, [&](double n) { return 4.0 * std::max(0.0, n - m0) * BB * BB; }));
-    kc_begin(KMP_KC_PANEL_WY, s);
-    // T of the panel's block reflector (formed by the register kernel):
-    // otherwise the Gram of V, then dlarft
-    if (!reg) {
-      if ((rc = ts_gram(s, BB, BB, mrow, G, wk.panel + m0, N, sP, wk.panel + m0, N, sP, wk.gram,
-                        kWyBlock, (int64_t)kWyBlock * kWyBlock, wk.part)) != 0)
+    return 0;
+  };
+  // T of panel p's block reflector (the register kernel forms it; after
+  // the streaming kernel: the Gram of V, then dlarft), and Y' = T'V'
+  // (BB x mrow, transposed into xbuf)
+  const auto panel_wy = [&](int p, const double* pb) -> int {
+    const int m0 = p + BB, mrow = N - m0;
+    if (mrow > 2048) {
+      if ((rc = ts_gram(s, BB, BB, mrow, G, pb + m0, N, sP, pb + m0, N, sP, wk.gram, kWyBlock,
+                        (int64_t)kWyBlock * kWyBlock, wk.part)) != 0)
         return rc;
       if ((rc = wy_form_t(s, wk.gram, wk.tau, wk.tmat, G, N, BB, p)) != 0) return rc;
     }
-    // Y' = T' V'   (BB x mrow, in xbuf)
     GemmArgs g1;
     g1.M = BB; g1.N = mrow; g1.K = BB; g1.batch = G;
     g1.A = wk.tmat; g1.lda = kWyBlock; g1.sA = (int64_t)kWyBlock * kWyBlock;
-    g1.B = wk.panel + m0; g1.ldb = N; g1.sB = sP;
+    g1.B = pb + m0; g1.ldb = N; g1.sB = sP;
     g1.C = wk.xbuf; g1.ldc = BB; g1.sC = (int64_t)kWyBlock * N;     // transposed, m x 16
-    if ((rc = gemm(s, g1, false, false, false)) != 0) return rc;
+    return gemm(s, g1, false, false, false);
+  };
+  // panel read twice per column step and written once (algorithmic: once)
+  const auto qr_bytes = [&](int m0) {
+    return over_groups(wk, [&](double n) { return 16.0 * std::max(0.0, n - m0) * BB; });
+  };
+  const auto qr_flops = [&](int m0) {
+    return over_groups(wk, [&](double n) { return 4.0 * std::max(0.0, n - m0) * BB * BB; });
+  };
+  kc_begin(KMP_KC_PANEL, s);
+  if ((rc = factor_panel(0, pbuf[0], false, nullptr)) != 0) return rc;
+  kc_end(KMP_KC_PANEL, s, qr_bytes(BB), qr_flops(BB));
+  kc_begin(KMP_KC_PANEL_WY, s);
+  if ((rc = panel_wy(0, pbuf[0])) != 0) return rc;
+  for (int p = 0; p + BB < N; p += BB) {
+    const int m0 = p + BB, mrow = N - m0;
+    double* const pb = pbuf[(p / BB) & 1];
     // X' = Y' A22 and the block products of M2 = V'X, then
     // W' = X' - 1/2 (T'M2)' V' in place of X'
     {
       const int NJ = (int)ceil_div(N, BB);
       hipLaunchKernelGGL(panel_x_kernel, dim3((unsigned)(mrow / BB), (unsigned)G), dim3(256), 0, s,
-                         wk.A, N, m0, wk.xbuf, wk.panel, wk.part, NJ);
+                         wk.A, N, m0, wk.xbuf, pb, wk.part, NJ);
       KMP_LAUNCH_CHECK();
       const int64_t sS = (int64_t)kWyBlock * N;
       hipLaunchKernelGGL(panel_s_kernel, dim3((unsigned)G), dim3(256), 0, s, N, m0, wk.part, NJ,
                          wk.tmat, wk.ybuf, sS);
       KMP_LAUNCH_CHECK();
       hipLaunchKernelGGL(panel_w_kernel, dim3((unsigned)ceil_div(mrow, 64), (unsigned)G), dim3(256),
-                         0, s, N, m0, wk.ybuf, sS, wk.panel);
+                         0, s, N, m0, wk.ybuf, sS, pb);
       KMP_LAUNCH_CHECK();
     }
     kc_end(KMP_KC_PANEL_WY, s, over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 8.0 * m * m; }),
            over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 2.0 * BB * m * m; }));
-    // A22 -= V W' + W V' (K = 2 BB over the [V; W; V] rows)
+    // A22 -= V W' + W V' (K = 2 BB over the [V; W; V] rows). With a next
+    // panel: its 16 columns first, then its factorisation beside the rest.
+    const bool next = m0 + BB < N;
     kc_begin(KMP_KC_TRAIL, s);
-    hipLaunchKernelGGL((rank_update_kernel<1, true>),
-                       dim3((unsigned)ceil_div(mrow, 64), (unsigned)ceil_div(mrow, 64), (unsigned)G),
-                       dim3(256), 0, s, wk.A + (int64_t)m0 * N + m0, (int64_t)N, (int64_t)N * N, mrow,
-                       (const double*)(wk.panel + m0), (int64_t)N, sP,
-                       (const double*)(wk.panel + (int64_t)BB * N + m0), (int64_t)N, sP);
-    KMP_LAUNCH_CHECK();
-    kc_end(KMP_KC_TRAIL, s, over_groups(wk, [&](double n) {
-             const double m = std::max(0.0, n - m0); return 16.0 * m * m; }),
+    const double* P1 = pb + m0;
+    const double* P2 = pb + (int64_t)BB * N + m0;
+    const unsigned tl = (unsigned)tiles_of(mrow);
+    if (next) {
+      hipLaunchKernelGGL((rank_update_kernel<1, true, 1>), dim3(tl, 1u, (unsigned)G), dim3(256), 0,
+                         s, wk.A + (int64_t)m0 * N + m0, (int64_t)N, (int64_t)N * N, mrow, P1,
+                         (int64_t)N, sP, P2, (int64_t)N, sP);
+      KMP_LAUNCH_CHECK();
+      if ((rc = factor_panel(m0, pbuf[((p / BB) & 1) ^ 1], true, pb)) != 0) return rc;
+    } else {
+      hipLaunchKernelGGL((rank_update_kernel<1, true>), dim3(tl, tl, (unsigned)G), dim3(256), 0, s,
+                         wk.A + (int64_t)m0 * N + m0, (int64_t)N, (int64_t)N * N, mrow, P1,
+                         (int64_t)N, sP, P2, (int64_t)N, sP);
+      KMP_LAUNCH_CHECK();
+    }
+    kc_end(KMP_KC_TRAIL, s,
            over_groups(wk, [&](double n) {
-             const double m = std::max(0.0, n - m0); return 4.0 * BB * m * m; }));
+             const double m = std::max(0.0, n - m0); return 16.0 * m * m; }) +
+               (next ? qr_bytes(m0 + BB) : 0.0),
+           over_groups(wk, [&](double n) {
+             const double m = std::max(0.0, n - m0); return 4.0 * BB * m * m; }) +
+               (next ? qr_flops(m0 + BB) : 0.0));
+    if (next) {
+      kc_begin(KMP_KC_PANEL_WY, s);
+      if ((rc = panel_wy(m0, pbuf[((p / BB) & 1) ^ 1])) != 0) return rc;
+    }
   }
   // the band, then clean reflector rows for the accumulation of Q
   {

@@ -390,6 +390,7 @@ int kmp_band_reduce(void* stream, double* A, int32_t G, int32_t N, double* Qout,
   double* q = scratch;
   w.tau = q; q += (size_t)G * N;
   w.panel = q; q += (size_t)G * 3 * kBand * N;
+  w.panel2 = q; q += (size_t)G * 3 * kBand * N;
   w.tmat = q; q += (size_t)G * kWyBlock * kWyBlock;
   w.gram = q; q += (size_t)G * kWyBlock * kWyBlock;
   w.xbuf = q; q += (size_t)G * kWyBlock * N;
@@ -607,7 +608,9 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     // a2: factorisation
     BandWork bw;
     bw.G = Gb; bw.N = N; bw.A = lay.A; bw.Q = lay.Qm; bw.band = lay.band; bw.tau = lay.tau;
-    bw.panel = lay.panel; bw.tmat = lay.tmat; bw.gram = lay.gram; bw.xbuf = lay.xbuf;
+    static_assert(kPanel >= 2 * kBand, "two band panel buffers share the panel slot");
+    bw.panel = lay.panel; bw.panel2 = lay.panel + (size_t)Gb * 3 * kBand * N;
+    bw.tmat = lay.tmat; bw.gram = lay.gram; bw.xbuf = lay.xbuf;
     bw.ybuf = lay.ybuf; bw.part = lay.bpart; bw.nv_host = nvg.data();
     bw.gram_all = lay.gram_all; bw.tmat_all = lay.tmat_all;
     if ((rc = band_reduce(s, bw)) != 0) return rc;

@@ -84,7 +84,8 @@ struct BandWork {
   double* Q = nullptr;      // G x N x N, output
   double* band = nullptr;   // G x (kBand+1) x N, output
   double* tau = nullptr;    // G x N
-  double* panel = nullptr;  // G x 3 kBand x N ([V; W; V] rows of the current panel)
+  double* panel = nullptr;  // G x 3 kBand x N ([V; W; V] rows of the even panels)
+  double* panel2 = nullptr; // G x 3 kBand x N (the same for the odd panels)
   double* tmat = nullptr;   // G x 64 x 64
   double* gram = nullptr;   // G x 64 x 64
   double* xbuf = nullptr;   // G x 64 x N
