@@ -409,21 +409,32 @@ __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__
   const double* Yg = ybuf + (int64_t)g * kWyBlock * N;
   double* Pg = panel + (int64_t)g * 3 * BB * N + m0;
   const int i = lane & 15, kq = lane >> 4;
+  // k of MFMA step s4 in lane group kq: 16 q + 4 s4 + kq below the block
+  // row (each load covers four 128-byte row pieces), 16 q + 4 kq + s4 above
+  // it (each lane reads 32 contiguous bytes of its row)
   const double* ya = Yg + (int64_t)kq * BB + i;
+  const double* yt = Yg + (int64_t)(4 * kq) * BB + i;
   const double* bb = Ag + (int64_t)kq * N + j0 + i;           // A22[k][j0 + i], k >= j
-  const double* bt = Ag + (int64_t)(j0 + i) * N + kq;         // A22[j0 + i][k], k < j
+  const double* bt = Ag + (int64_t)(j0 + i) * N + 4 * kq;     // A22[j0 + i][k], k < j
   xdbl4 acc = {0.0, 0.0, 0.0, 0.0};
   for (int q = w; q < nch; q += 4 * XUQ) {
     double av[XUQ][4], bv[XUQ][4];
 #pragma unroll
     for (int u = 0; u < XUQ; ++u) {
       const int qq = (q + 4 * u < nch) ? q + 4 * u : q;      // clamped: not accumulated
-      const bool below = qq >= jb;                             // chunk on or below the block row
+      if (qq >= jb) {                                          // chunk on or below the block row
 #pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4) {
-        const int k = BB * qq + 4 * s4;
-        av[u][s4] = ya[(int64_t)k * BB];
-        bv[u][s4] = below ? bb[(int64_t)k * N] : bt[k];
+        for (int s4 = 0; s4 < 4; ++s4) {
+          const int k = BB * qq + 4 * s4;
+          av[u][s4] = ya[(int64_t)k * BB];
+          bv[u][s4] = bb[(int64_t)k * N];
+        }
+      } else {
+        const double2 b01 = *reinterpret_cast<const double2*>(bt + BB * qq);
+        const double2 b23 = *reinterpret_cast<const double2*>(bt + BB * qq + 2);
+        bv[u][0] = b01.x; bv[u][1] = b01.y; bv[u][2] = b23.x; bv[u][3] = b23.y;
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) av[u][s4] = yt[(int64_t)(BB * qq + s4) * BB];
       }
     }
 #pragma unroll

@@ -399,11 +399,35 @@ int gemm(hipStream_t s, const GemmArgs& g, bool ak, bool bk, bool cr) {
 
 int gemm_loss_tile_rows(const GemmArgs& g) { return pick_bm(g); }
 
-int splitk_parts(const GemmArgs& g) {
-  const int64_t tiles = ceil_div(g.M, 64) * ceil_div(g.N, TN) * g.batch;
-  int S = (int)std::min<int64_t>(4, std::max<int64_t>(1, ceil_div(1024, tiles)));
-  while (S > 1 && g.K / S < 8 * 16) --S;          // keep >= 8 K slices per part
-  return S;
+// Compute units of the current device (queried once per device).
+static int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+      n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
+// Split-K parts for dgemm_partial_kernel: the S that minimises the rounds
+// of resident workgroups (four per compute unit, bound by LDS) times the K
+// range per part, over the tiles that do work (tiles <= 0: all of them);
+// ties go to the larger S. Each part keeps at least 8 slices of 16.
+int splitk_parts(const GemmArgs& g, int64_t tiles) {
+  if (tiles <= 0) tiles = ceil_div(g.M, 64) * ceil_div(g.N, TN) * g.batch;
+  const int64_t slots = 4 * (int64_t)device_cus();
+  int best = 1;
+  int64_t best_cost = -1;
+  for (int S = 1; S <= kMaxSplitK; ++S) {
+    if (S > 1 && g.K / S < 8 * 16) break;
+    const int64_t cost = ceil_div(tiles * S, slots) * ceil_div(g.K, S);
+    if (best_cost < 0 || cost <= best_cost) { best = S; best_cost = cost; }
+  }
+  return best;
 }
 
 int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP,

@@ -46,7 +46,7 @@ constexpr int kMaxSplitK = 4;
 // the parts in order and writes Z plus 64-row column sums (see LossEpi).
 // Both work on the active columns only: batch b has nact[b] of them, the
 // k-th being column cmap[b*g.N + k] (B k-contiguous, C column-major).
-int splitk_parts(const GemmArgs& g);
+int splitk_parts(const GemmArgs& g, int64_t tiles = 0);
 int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP,
                  const int* cmap, const int* nact);
 int loss_epilogue(hipStream_t s, int M, int N, int batch, int S, const double* part, int64_t ldc,

@@ -1017,7 +1017,11 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   g1.A = p.Q; g1.lda = p.N; g1.sA = (int64_t)p.N * p.N;
   g1.B = p.bmat; g1.ldb = p.N; g1.sB = sC;
   g1.ldc = p.N; g1.sC = sC;
-  const int S1 = splitk_parts(g1);
+  // output tiles that do work: 64-row tiles of the active columns
+  int64_t work_tiles = 0;
+  for (int g = 0; g < p.G; ++g)
+    work_tiles += ceil_div(p.N, 64) * ceil_div(p.nact_host ? p.nact_host[g] : p.C, 64);
+  const int S1 = splitk_parts(g1, work_tiles);
   LossEpi e;
   e.loss = p.loss; e.delta = delta;
   e.y = p.ylab; e.sy = p.N; e.nv = p.nv;
@@ -1037,7 +1041,7 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   g2.A = p.Q; g2.lda = p.N; g2.sA = (int64_t)p.N * p.N;
   g2.B = p.zmat; g2.ldb = p.N; g2.sB = sC;
   g2.ldc = p.N; g2.sC = sC;
-  const int S2 = splitk_parts(g2);
+  const int S2 = splitk_parts(g2, work_tiles);
   kc_begin(KMP_KC_GEMM_ZHAT, s);
   if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP, p.cmap, p.nact)) != 0) return rc;
   kc_end(KMP_KC_GEMM_ZHAT, s, gbytes, gflops);
