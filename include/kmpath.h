@@ -96,7 +96,7 @@ typedef struct {
 /* Phase times in milliseconds, measured with HIP events on `stream`. */
 typedef struct {
   double gram_ms;      /* a1: Gram + fold gather                            */
-  double factor_ms;    /* a2: per-fold tridiagonal factorisation and Q      */
+  double factor_ms;    /* a2: per-fold band factorisation and Q             */
   double precompute_ms;/* a3: per-stage per-column factors                  */
   double path_ms;      /* a4-a9: iterations                                 */
   double finalize_ms;  /* a10: alpha, objectives, CV sums                   */
@@ -194,7 +194,7 @@ int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N,
  * (first stage of the successive band reduction, Bischof, Lang & Sun 2000):
  * panel QR, compact-WY two-sided trailing updates on matrix cores, Q
  * accumulated in compact-WY blocks. N must be a multiple of 64 in
- * [64, 8192]; zero padding rows are allowed.                              */
+ * [64, 32768]; zero padding rows are allowed.                             */
 #define KMP_BAND 16
 int kmp_band_reduce(void* stream, double* A, int32_t G, int32_t N, double* Qout, double* band);
 
