@@ -31,6 +31,8 @@ namespace kmp {
 
 constexpr int BB = kBand;        // band width = panel width
 
+typedef double xdbl4 __attribute__((ext_vector_type(4)));
+constexpr int kFusedYtRows = 1536;   // register panels that also form Y'
 constexpr int PQT = 512;         // threads of the panel factorisation
 constexpr int PQW = PQT / 64;
 
@@ -195,12 +197,12 @@ constexpr int PVT = 256;          // rows of the reflector staging tile
 
 template <int NW>
 struct PanelLds {
-  double red[NW][BB];      // per-wave partial sums
-  double hs[BB];           // h of the current step
+  double red[2][NW][BB];   // per-wave partial sums of h, by step parity
   double rowb[2][BB];      // row i of the panel before step i (as held: u_k for k < i)
   double scl[BB];          // scale_k
   double tau[BB];
   double z[BB][BB];        // z_i[k], k < i
+  double tq[BB][BB + 1];   // T of the block reflector
   double vt[BB][PVT + 1];  // reflector staging tile
 };
 
@@ -210,20 +212,25 @@ struct PanelCtx {
   int w, c, sub, t;
 };
 
-// h_c over the block from the per-lane partial sums (column c of the lane);
-// leaves h in L.hs.
-template <int NW>
-__device__ __forceinline__ void panel_h_sum(double acc, const PanelCtx<NW>& st) {
+// The per-wave partial sums of h (column c of the lane) into red[B], then
+// one barrier; each wavefront then adds the NW partials itself
+// (panel_h_col: lane (c, sub) reads the partials of waves sub, sub+4, ...,
+// and the four rows are added by permlane swaps, so every lane ends with
+// h_c of its column). red is double-buffered by step parity: a wavefront
+// writes red[B] again two steps later, after the barrier of the step
+// between, which every wavefront reaches only after its reads.
+template <int NW, int B>
+__device__ __forceinline__ void panel_h_put(double acc, const PanelCtx<NW>& st) {
   const double v = swap_sum32_b(swap_sum16_b(acc));
-  if (st.sub == 0) st.L->red[st.w][st.c] = v;
+  if (st.sub == 0) st.L->red[B][st.w][st.c] = v;
   __syncthreads();
-  if (st.t < BB) {
-    double s = 0.0;
+}
+template <int NW, int B>
+__device__ __forceinline__ double panel_h_col(const PanelCtx<NW>& st) {
+  double s = 0.0;
 #pragma unroll
-    for (int q = 0; q < NW; ++q) s += st.L->red[q][st.t];
-    st.L->hs[st.t] = s;
-  }
-  __syncthreads();
+  for (int j = 0; j < NW / 4; ++j) s += st.L->red[B][st.sub + 4 * j][st.c];
+  return swap_sum32_b(swap_sum16_b(s));
 }
 
 template <int RS, int NW, bool CARRY, int I>
@@ -233,23 +240,24 @@ __device__ __forceinline__ void panel_steps(double (&x)[RS], double (&xi)[RS],
     PanelLds<NW>& L = *st.L;
     const double* ri = L.rowb[I & 1];
     const double alpha = ri[I];
-    const double sigma = L.hs[I];
+    const int c = st.c;
+    const double hc = panel_h_col<NW, I & 1>(st);                   // h_c, every lane
+    const double sigma = row_bcast<I>(hc);
     double tau = 0.0, beta = alpha, scale = 0.0;
     if (sigma > 0.0) {
       beta = -copysign(sqrt(alpha * alpha + sigma), alpha);
       tau = (beta - alpha) / beta;
       scale = 1.0 / (alpha - beta);
     }
-    if (st.t < I) L.z[I][st.t] = L.scl[st.t] * fma(scale, L.hs[st.t], ri[st.t]);
+    if (st.t < I) L.z[I][st.t] = L.scl[st.t] * fma(scale, hc, ri[st.t]);   // t < 16: c = t
     if (st.t == 0) {
       L.scl[I] = scale;
       L.tau[I] = tau;
     }
-    const int c = st.c;
-    const double tw = -tau * fma(scale, L.hs[c], ri[c]);            // -tau v_I' P[:, c]
+    const double tw = -tau * fma(scale, hc, ri[c]);                 // -tau v_I' P[:, c]
     const double ac = (c > I) ? tw * scale : 0.0;
     double a1 = 0.0;
-    if constexpr (I + 1 < BB) a1 = -tau * fma(scale, L.hs[I + 1], ri[I + 1]) * scale;
+    if constexpr (I + 1 < BB) a1 = -tau * fma(scale, row_bcast<I + 1>(hc), ri[I + 1]) * scale;
     double acc = 0.0;
 #pragma unroll
     for (int m = 0; m < RS; ++m) {
@@ -279,7 +287,7 @@ __device__ __forceinline__ void panel_steps(double (&x)[RS], double (&xi)[RS],
       }
     }
     if constexpr (I + 1 < BB) {
-      panel_h_sum<NW>(acc, st);
+      panel_h_put<NW, (I + 1) & 1>(acc, st);
       panel_steps<RS, NW, CARRY, I + 1>(x, xi, st);
     }
   }
@@ -289,7 +297,8 @@ template <int RS, int NW, bool CARRY>
 __device__ __forceinline__ void panel_qr_vec_body(double* __restrict__ A, int N, int p,
                                                   double* __restrict__ taus,
                                                   double* __restrict__ panel,
-                                                  double* __restrict__ tmat, int g) {
+                                                  double* __restrict__ tmat,
+                                                  double* __restrict__ yt, int g) {
   constexpr int RPS = 4 * NW;                      // rows per slot
   __shared__ PanelLds<NW> L;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
@@ -313,17 +322,44 @@ __device__ __forceinline__ void panel_qr_vec_body(double* __restrict__ A, int N,
     if constexpr (CARRY) xi[m] = x0;
     acc = fma((r > 0) ? x0 : 0.0, x[m], acc);
   }
-  panel_h_sum<NW>(acc, st);
+  panel_h_put<NW, 0>(acc, st);
   panel_steps<RS, NW, CARRY, 0>(x, xi, st);
   __syncthreads();
+  // T, row t per thread, built in LDS (rolled loops, operands read from
+  // LDS), then into tmat; before the reflector tiles when Y' is formed
+  // with them, after them otherwise (the slots are then dead)
+  constexpr bool kYt = RPS * RS <= kFusedYtRows;
+  const auto form_t = [&]() {
+    if (t < BB) {
+      double* Tg = tmat + (int64_t)g * kWyBlock * kWyBlock + (int64_t)t * kWyBlock;
+#pragma unroll 1
+      for (int i = 0; i < BB; ++i) {
+        double s0 = 0.0, s1 = 0.0;
+        for (int k = t; k + 1 < i; k += 2) {
+          s0 = fma(L.tq[t][k], L.z[i][k], s0);
+          s1 = fma(L.tq[t][k + 1], L.z[i][k + 1], s1);
+        }
+        if (((i - t) & 1) && t < i) s0 = fma(L.tq[t][i - 1], L.z[i][i - 1], s0);
+        const double v = (i > t) ? -L.tau[i] * (s0 + s1) : ((i == t) ? L.tau[t] : 0.0);
+        L.tq[t][i] = v;
+        Tg[i] = v;
+      }
+      taus[(int64_t)g * N + p + t] = L.tau[t];
+    }
+  };
+  if constexpr (kYt) form_t();
   // R (rows < BB, on and above the diagonal) back into the panel; the
   // reflectors v_k = scale_k u_k (leading 1 at row k) transposed into row
-  // p+k of A and rows k, 2BB+k of the panel buffer, through the LDS tile
+  // p+k of A and rows k, 2BB+k of the panel buffer, through the LDS tile;
+  // from the same tile Y' = T'V' on the matrix cores, stored transposed
+  // (row r: 16 doubles), one 16-row block per wavefront (for panels of at
+  // most kFusedYtRows rows: beyond, the slots leave no registers for it)
   const double sc = L.scl[c];
   int rb = 4 * w + sub;               // fresh: keeps the slots' row indices out of registers
   asm volatile("" : "+v"(rb));
   if (rb < BB && rb <= c) P[(int64_t)rb * N + c] = x[0];
   double* Vt = panel + (int64_t)g * 3 * BB * N;
+  double* Yg = yt + (int64_t)g * kWyBlock * N;
   constexpr int SPT = PVT / RPS;      // slots per tile
 #pragma unroll
   for (int m0s = 0; m0s < RS; m0s += SPT) {
@@ -346,37 +382,31 @@ __device__ __forceinline__ void panel_qr_vec_body(double* __restrict__ A, int N,
         Vt[(int64_t)(2 * BB + k) * N + col] = v;
       }
     }
+    if constexpr (kYt)
+    for (int blk = w; 16 * blk < nr; blk += NW) {
+      xdbl4 acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4)
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(L.vt[4 * s4 + sub][16 * blk + c],
+                                                   L.tq[4 * s4 + sub][c], acc, 0, 0, 0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * blk + 4 * r + sub;
+        if (row < nr) Yg[(int64_t)(r0 + row) * BB + c] = acc[r];
+      }
+    }
     __syncthreads();
   }
-  // T, row t per thread (z and tau from LDS into registers first)
-  if (t < BB) {
-    double tr[BB];
-#pragma unroll
-    for (int i = 0; i < BB; ++i) {
-      double zi[BB];
-#pragma unroll
-      for (int k = 0; k < i; ++k) zi[k] = L.z[i][k];
-      double s0 = 0.0, s1 = 0.0;
-#pragma unroll
-      for (int k = 0; k < i; ++k) {
-        const double term = (k >= t) ? tr[k] * zi[k] : 0.0;
-        if (k & 1) s1 += term; else s0 += term;
-      }
-      tr[i] = (i > t) ? -L.tau[i] * (s0 + s1) : ((i == t) ? L.tau[t] : 0.0);
-    }
-    double* Tg = tmat + (int64_t)g * kWyBlock * kWyBlock + (int64_t)t * kWyBlock;
-#pragma unroll
-    for (int i = 0; i < BB; ++i) Tg[i] = tr[i];
-    taus[(int64_t)g * N + p + t] = L.tau[t];
-  }
+  if constexpr (!kYt) form_t();
 }
 
 template <int RS, int NW, bool CARRY>
 __global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restrict__ A, int N,
                                                                 int p, double* __restrict__ taus,
                                                                 double* __restrict__ panel,
-                                                                double* __restrict__ tmat) {
-  panel_qr_vec_body<RS, NW, CARRY>(A, N, p, taus, panel, tmat, blockIdx.x);
+                                                                double* __restrict__ tmat,
+                                                                double* __restrict__ yt) {
+  panel_qr_vec_body<RS, NW, CARRY>(A, N, p, taus, panel, tmat, yt, blockIdx.x);
 }
 
 // Only the lower triangle of the trailing matrix is kept up to date (the
@@ -395,7 +425,6 @@ __global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restric
 // X' goes to rows BB .. 2BB-1 of the panel buffer, and the workgroup's part
 // of M2, sum_{j in block} V'[a][j] X'[b][j], to part[(g NJ + block)*256].
 constexpr int XUQ = 4;            // 16-row chunks per wave and iteration
-typedef double xdbl4 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__ A, int N, int m0,
                                                        const double* __restrict__ ybuf,
@@ -632,10 +661,11 @@ __device__ __forceinline__ void rest_update_role(double* A, int N, int m0, int m
 template <int RS, int NW, bool CARRY>
 __global__ __launch_bounds__(64 * NW) void qr_rest_vec_kernel(
     double* __restrict__ A, int N, int p_next, double* __restrict__ taus,
-    double* __restrict__ panel_next, double* __restrict__ tmat, int G, int m0, int mrow,
-    const double* __restrict__ P1, const double* __restrict__ P2, int64_t sP, int tiles) {
+    double* __restrict__ panel_next, double* __restrict__ tmat, double* __restrict__ yt, int G,
+    int m0, int mrow, const double* __restrict__ P1, const double* __restrict__ P2, int64_t sP,
+    int tiles) {
   if (blockIdx.x < G) {
-    panel_qr_vec_body<RS, NW, CARRY>(A, N, p_next, taus, panel_next, tmat, blockIdx.x);
+    panel_qr_vec_body<RS, NW, CARRY>(A, N, p_next, taus, panel_next, tmat, yt, blockIdx.x);
     return;
   }
   rest_update_role<NW / 4>(A, N, m0, mrow, G, P1, P2, sP, tiles);
@@ -863,11 +893,11 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
   do {                                                                                            \
     if (dual)                                                                                     \
       hipLaunchKernelGGL((qr_rest_vec_kernel<RSV, NWV, CV>), dim3(dual_grid(mprev, NWV / 4)),     \
-                         dim3(64 * NWV), 0, s, wk.A, N, p, wk.tau, pb, wk.tmat, G, m0prev, mprev, \
-                         P1, P2, sP, tp);                                                         \
+                         dim3(64 * NWV), 0, s, wk.A, N, p, wk.tau, pb, wk.tmat, wk.xbuf, G,       \
+                         m0prev, mprev, P1, P2, sP, tp);                                          \
     else                                                                                          \
       hipLaunchKernelGGL((panel_qr_vec_kernel<RSV, NWV, CV>), dim3(G), dim3(64 * NWV), 0, s,      \
-                         wk.A, N, p, wk.tau, pb, wk.tmat);                                        \
+                         wk.A, N, p, wk.tau, pb, wk.tmat, wk.xbuf);                               \
   } while (0)
     if (rs <= 8) KMP_PQR(8, 8, true);
     else if (rs <= 16) KMP_PQR(16, 8, true);
@@ -885,11 +915,13 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     KMP_LAUNCH_CHECK();
     return 0;
   };
-  // T of panel p's block reflector (the register kernel forms it; after
-  // the streaming kernel: the Gram of V, then dlarft), and Y' = T'V'
-  // (BB x mrow, transposed into xbuf)
+  // T of panel p's block reflector and Y' = T'V' (BB x mrow, transposed
+  // into xbuf): the register kernel forms T, and Y' up to kFusedYtRows
+  // rows, else the product follows; after the streaming kernel, the Gram
+  // of V, then dlarft, then the product
   const auto panel_wy = [&](int p, const double* pb) -> int {
     const int m0 = p + BB, mrow = N - m0;
+    if (mrow <= kFusedYtRows) return 0;
     if (mrow > 2048) {
       if ((rc = ts_gram(s, BB, BB, mrow, G, pb + m0, N, sP, pb + m0, N, sP, wk.gram, kWyBlock,
                         (int64_t)kWyBlock * kWyBlock, wk.part)) != 0)

@@ -331,7 +331,8 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
 // active column c = cmap[b*N + k], k < nact[b], F = sum_s part_s[c][i] +
 // bbar[c]; Z[c][i] = psi(y_i, F)/nv (0 at padding rows); partial[b][tile][c]
 // = sum of Z over the 64 rows of the tile (lanes = rows, so the column sums
-// are wave reductions).
+// are wave reductions). Wave w of workgroup (tile, j, b) takes the active
+// column k = 4 j + w.
 __global__ __launch_bounds__(256) void loss_epilogue_kernel(int M, int N, int S,
                                                              const double* __restrict__ part,
                                                              int64_t ldc, int64_t sC, int64_t sP,
@@ -347,8 +348,8 @@ __global__ __launch_bounds__(256) void loss_epilogue_kernel(int M, int N, int S,
   const double* bbar = e.bbar + (int64_t)b * e.sbb;
   const double* tau = e.tau + (int64_t)b * e.stau;
   const int* cmap = cmap_all + (int64_t)b * N;
-  const int na = nact[b];
-  for (int k = w; k < na; k += 4) {
+  const int k = 4 * (int)blockIdx.y + w;
+  if (k < nact[b]) {
     const int c = cmap[k];
     double z = 0.0;
     if (i < M) {
@@ -451,7 +452,7 @@ int loss_epilogue(hipStream_t s, int M, int N, int batch, int S, const double* p
                   int64_t sC, int64_t sP, double* Z, const LossEpi& e, const int* cmap,
                   const int* nact) {
   if (M <= 0 || N <= 0 || batch <= 0) return 0;
-  dim3 grid((unsigned)ceil_div(M, 64), 1, (unsigned)batch);
+  dim3 grid((unsigned)ceil_div(M, 64), (unsigned)ceil_div(N, 4), (unsigned)batch);
   hipLaunchKernelGGL(loss_epilogue_kernel, grid, dim3(256), 0, s, M, N, S, part, ldc, sC, sP, Z, e,
                      cmap, nact);
   KMP_LAUNCH_CHECK();
