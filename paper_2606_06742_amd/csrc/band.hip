@@ -805,7 +805,7 @@ size_t wy_all_doubles(int G, int N) {
 size_t band_work_doubles(int G, int N) {
   return (size_t)G * (6 * (size_t)BB * N + 2 * (size_t)kWyBlock * kWyBlock +
                       2 * (size_t)kWyBlock * N) + band_part_doubles(G, N) +
-         2 * wy_all_doubles(G, N);
+         2 * wy_all_doubles(G, N) + (size_t)kMaxSplitK * G * kWyBlock * N;
 }
 
 // Gram matrices of all blocks of kWyBlock reflector rows at once, on the
@@ -857,6 +857,78 @@ __global__ __launch_bounds__(256) void wy_gram_kernel(const double* __restrict__
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         Gg[(wi + 16 * x + mfma_row(lane, r)) * kWyBlock + wj + 16 * y + mfma_col(lane)] = acc[x][y][r];
+}
+
+// Y = T X for one WY block of the Q accumulation, X given as S split-K
+// parts (X_s[a][j] = xpart[s sP + g sX + a ldx + j], added in order s =
+// 0, 1, ...): workgroup (column tile, g) stages the 64 x 64 piece of X and
+// T (kb x kb, zero beyond) in LDS, and wave w forms the 32 x 32 quadrant
+// (32 (w&1), 32 (w>>1)) of Y on the matrix cores.
+__global__ __launch_bounds__(256) void wy_apply_t_kernel(const double* __restrict__ tq, int kb,
+                                                         const double* __restrict__ xpart, int S,
+                                                         int64_t sP, int64_t sX, int64_t ldx,
+                                                         int m, double* __restrict__ Y,
+                                                         int64_t ldy, int64_t sY) {
+  __shared__ double Ts[kWyBlock][kWyBlock + 1];
+  __shared__ double Xs[kWyBlock][kWyBlock + 1];
+  const int g = blockIdx.y, j0 = kWyBlock * blockIdx.x, t = threadIdx.x;
+  const double* Tg = tq + (int64_t)g * kWyBlock * kWyBlock;
+  const double* Xg = xpart + (int64_t)g * sX;
+  {
+    // thread t stages row a = t/4, columns 16 (t%4) .. +15 of both tiles;
+    // every load is issued before the first sum
+    const int a = t >> 2, jq = 16 * (t & 3);
+    const bool ra = a < kb;
+    double tv[16], xv[kMaxSplitK][16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) tv[u] = (ra && jq + u < kb) ? Tg[a * kWyBlock + jq + u] : 0.0;
+#pragma unroll
+    for (int q = 0; q < kMaxSplitK; ++q)
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int j = j0 + jq + u;
+        xv[q][u] = (ra && q < S && j < m) ? Xg[(int64_t)q * sP + (int64_t)a * ldx + j] : 0.0;
+      }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      double v = xv[0][u];
+#pragma unroll
+      for (int q = 1; q < kMaxSplitK; ++q) v += xv[q][u];   // zero past S: same sum
+      Ts[a][jq + u] = tv[u];
+      Xs[a][jq + u] = v;
+    }
+  }
+  __syncthreads();
+  const int w = t >> 6, lane = t & 63, li = lane & 15, lk = lane >> 4;
+  const int i0 = 32 * (w & 1), jw = 32 * (w >> 1);
+  xdbl4 acc[2][2];
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = xdbl4{0.0, 0.0, 0.0, 0.0};
+  for (int k = 0; k < kb; k += 4) {
+    double av[2], bv[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      av[b] = Ts[i0 + 16 * b + li][k + lk];
+      bv[b] = Xs[k + lk][jw + 16 * b + li];
+    }
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj)
+        acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[bi], bv[bj], acc[bi][bj], 0, 0, 0);
+  }
+  double* Yg = Y + (int64_t)g * sY;
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int a = i0 + 16 * bi + 4 * r + lk, j = jw + 16 * bj + li;
+        if (a < kb && j0 + j < m) Yg[(int64_t)a * ldy + j0 + j] = acc[bi][bj][r];
+      }
 }
 
 int band_reduce(hipStream_t s, const BandWork& wk) {
@@ -1032,18 +1104,22 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     const int m = N - q - BB;
     if (q != last) kc_begin(KMP_KC_QFORM, s);
     const double* tq = wk.tmat_all + (int64_t)(q / kWyBlock) * G * kWyBlock * kWyBlock;
-    GemmArgs h1;   // X = V Q[q+BB:, q+BB:]   (kb x m)
-    h1.M = kb; h1.N = m; h1.K = m; h1.batch = G;
-    h1.A = wk.A + (int64_t)q * N + q + BB; h1.lda = N; h1.sA = (int64_t)N * N;
-    h1.B = wk.Q + (int64_t)(q + BB) * N + q + BB; h1.ldb = N; h1.sB = (int64_t)N * N;
-    h1.C = wk.xbuf; h1.ldc = N; h1.sC = (int64_t)kWyBlock * N;
-    if ((rc = gemm(s, h1, true, false, true)) != 0) return rc;
-    GemmArgs h2;   // Y = T X
-    h2.M = kb; h2.N = m; h2.K = kb; h2.batch = G;
-    h2.A = tq; h2.lda = kWyBlock; h2.sA = (int64_t)kWyBlock * kWyBlock;
-    h2.B = wk.xbuf; h2.ldb = N; h2.sB = (int64_t)kWyBlock * N;
-    h2.C = wk.ybuf; h2.ldc = N; h2.sC = (int64_t)kWyBlock * N;
-    if ((rc = gemm(s, h2, true, false, true)) != 0) return rc;
+    // X = V Q[q+BB:, q+BB:] (kb x m) as split-K parts, in the transposed
+    // form X' = Q[q+BB:, q+BB:]' V' (m x kb: the A operand is Q22 read by
+    // rows, B the reflector rows), then Y = T X
+    GemmArgs h1;
+    h1.M = m; h1.N = kb; h1.K = m; h1.batch = G;
+    h1.A = wk.Q + (int64_t)(q + BB) * N + q + BB; h1.lda = N; h1.sA = (int64_t)N * N;
+    h1.B = wk.A + (int64_t)q * N + q + BB; h1.ldb = N; h1.sB = (int64_t)N * N;
+    h1.ldc = N; h1.sC = (int64_t)kWyBlock * N;
+    const int64_t sXP = (int64_t)G * kWyBlock * N;
+    const int S1 = splitk_parts(h1);
+    if ((rc = gemm_partial(s, h1, false, S1, wk.xpart, sXP, nullptr, nullptr)) != 0) return rc;
+    hipLaunchKernelGGL(wy_apply_t_kernel, dim3((unsigned)ceil_div(m, kWyBlock), (unsigned)G),
+                       dim3(256), 0, s, tq, kb, (const double*)wk.xpart, S1, sXP,
+                       (int64_t)kWyBlock * N, (int64_t)N, m, wk.ybuf, (int64_t)N,
+                       (int64_t)kWyBlock * N);
+    KMP_LAUNCH_CHECK();
     // Q[q+BB:, q+BB:] -= V' Y  (K = kb = 64; the last block may be shorter
     // only when N - BB is not a multiple of 64, then the generic product)
     if (kb == kWyBlock) {

@@ -287,6 +287,7 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
 // Only the active columns of a batch are computed: tile column k < nact[b]
 // is column cmap[b*cstride + k] of B and of the partials (the other columns
 // of the partials are left as they were); tiles past nact[b] exit at once.
+// With cmap and nact null, all cstride columns, in order.
 template <int BM, int BK, bool AK>
 __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S, int Kc,
                                                              const double* __restrict__ A, int64_t lda, int64_t sA,
@@ -296,10 +297,10 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
                                                              const int* __restrict__ nact, int cstride) {
   constexpr int MB = Tile<BM, BK>::MB;
   const int b = blockIdx.z / S, sk = blockIdx.z % S;
-  const int N = nact[b];
+  const int N = nact ? nact[b] : cstride;
   const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TN;
   if (j0 >= N) return;
-  const int* cmap = cmap_all + (int64_t)b * cstride;
+  const int* cmap = cmap_all ? cmap_all + (int64_t)b * cstride : nullptr;
   A += (int64_t)b * sA;
   B += (int64_t)b * sB;
   double* C = part + (int64_t)sk * sP + (int64_t)b * sC;
@@ -323,7 +324,7 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
       for (int r = 0; r < 4; ++r) {
         const int gi = i0 + wi + bi * 16 + mfma_row(lane, r);
         const int gj = j0 + wj + bj * 16 + mfma_col(lane);
-        if (gi < M && gj < N) C[(int64_t)cmap[gj] * ldc + gi] = acc[bi][bj][r];
+        if (gi < M && gj < N) C[(int64_t)(cmap ? cmap[gj] : gj) * ldc + gi] = acc[bi][bj][r];
       }
 }
 
