@@ -760,16 +760,18 @@ __global__ void band_extract_kernel(const double* __restrict__ A, int N, int64_t
 }
 
 // Clear row r of A (a reflector row, r < N - BB) to the left of its stored
-// vector, from column max(0, r - 64) up to column r + BB - 1, so that any
-// compact-WY block of up to 64 consecutive reflector rows reads zeros there.
+// vector, from column max(0, r - 128) up to column r + BB - 1, so that any
+// run of up to 128 consecutive reflector rows (a pair of compact-WY blocks)
+// reads zeros there.
 __global__ void clear_reflector_rows_kernel(double* __restrict__ A, int N, int64_t total) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= total) return;
   const int64_t rows = N - BB;
-  const int g = (int)(idx / (rows * (64 + BB)));
-  const int64_t e = idx % (rows * (64 + BB));
-  const int r = (int)(e / (64 + BB)), q = (int)(e % (64 + BB));
-  const int c = r - 64 + q;              // c in [r - 64, r + BB)
+  constexpr int W = 2 * kWyBlock + BB;
+  const int g = (int)(idx / (rows * W));
+  const int64_t e = idx % (rows * W);
+  const int r = (int)(e / W), q = (int)(e % W);
+  const int c = r - 2 * kWyBlock + q;    // c in [r - 128, r + BB)
   if (c < 0) return;
   A[(int64_t)g * N * N + (int64_t)r * N + c] = 0.0;
 }
@@ -804,25 +806,34 @@ size_t wy_all_doubles(int G, int N) {
 
 size_t band_work_doubles(int G, int N) {
   return (size_t)G * (6 * (size_t)BB * N + 2 * (size_t)kWyBlock * kWyBlock +
-                      2 * (size_t)kWyBlock * N) + band_part_doubles(G, N) +
-         2 * wy_all_doubles(G, N) + (size_t)kMaxSplitK * G * kWyBlock * N;
+                      3 * (size_t)kWyBlock * N) + band_part_doubles(G, N) +
+         3 * wy_all_doubles(G, N) + (size_t)kMaxSplitK * G * 2 * kWyBlock * N;
 }
 
 // Gram matrices of all blocks of kWyBlock reflector rows at once, on the
-// matrix cores: workgroup (b, g) forms G[a][c] = sum_k V[a][k] V[c][k] for
-// the reflectors q = 64 b .. q + kb - 1 of matrix g (row q + a of A holds
-// v_{q+a} from column q + a + BB, zeros before it, so the sum runs over the
-// columns q + BB .. N-1). Wave w computes the 32 x 32 quadrant (32 (w&1),
-// 32 (w>>1)) as 2 x 2 MFMA blocks over 16-column slices staged in LDS.
+// matrix cores: workgroup (b, g, 0) forms G[a][c] = sum_k V[a][k] V[c][k]
+// for the reflectors q = 64 b .. q + kb - 1 of matrix g (row q + a of A
+// holds v_{q+a} from column q + a + BB, zeros before it, so the sum runs
+// over the columns q + BB .. N-1); workgroup (b, g, 1) the cross products
+// V_b V_{b+1}' with the next block (into cross_all). Wave w computes the
+// 32 x 32 quadrant (32 (w&1), 32 (w>>1)) as 2 x 2 MFMA blocks over
+// 16-column slices staged in LDS.
 __global__ __launch_bounds__(256) void wy_gram_kernel(const double* __restrict__ A, int N, int nref,
-                                                       double* __restrict__ gram_all) {
+                                                       double* __restrict__ gram_all,
+                                                       double* __restrict__ cross_all) {
   __shared__ double Vs[kWyBlock][BB + 1];
+  __shared__ double Ws[kWyBlock][BB + 1];
   const int b = blockIdx.x, g = blockIdx.y, G = gridDim.y;
+  const bool cross = blockIdx.z == 1;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int q = kWyBlock * b;
   const int kb = min(kWyBlock, nref - q);
+  const int kc = cross ? min(kWyBlock, nref - q - kWyBlock) : kb;   // rows of the right factor
+  if (kc <= 0) return;
   const int m = N - q - BB;
   const double* Vq = A + (int64_t)g * N * N + (int64_t)q * N + q + BB;
+  const double* Wq = cross ? Vq + (int64_t)kWyBlock * N : Vq;
+  double (*Rs)[BB + 1] = cross ? Ws : Vs;
   const int wi = 32 * (w & 1), wj = 32 * (w >> 1);
   const int li = lane & 15, lk = lane >> 4;
   xdbl4 acc[2][2];
@@ -837,19 +848,20 @@ __global__ __launch_bounds__(256) void wy_gram_kernel(const double* __restrict__
     for (int u = 0; u < 4; ++u) {
       const int c = c0 + lc + u;
       Vs[lr][lc + u] = (lr < kb && c < m) ? Vq[(int64_t)lr * N + c] : 0.0;
+      if (cross) Ws[lr][lc + u] = (lr < kc && c < m) ? Wq[(int64_t)lr * N + c] : 0.0;
     }
     __syncthreads();
 #pragma unroll
     for (int s4 = 0; s4 < BB; s4 += 4) {
       const double a0 = Vs[wi + li][s4 + lk], a1 = Vs[wi + 16 + li][s4 + lk];
-      const double b0 = Vs[wj + li][s4 + lk], b1 = Vs[wj + 16 + li][s4 + lk];
+      const double b0 = Rs[wj + li][s4 + lk], b1 = Rs[wj + 16 + li][s4 + lk];
       acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
       acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
       acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
       acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
     }
   }
-  double* Gg = gram_all + ((int64_t)b * G + g) * kWyBlock * kWyBlock;
+  double* Gg = (cross ? cross_all : gram_all) + ((int64_t)b * G + g) * kWyBlock * kWyBlock;
 #pragma unroll
   for (int x = 0; x < 2; ++x)
 #pragma unroll
@@ -929,6 +941,107 @@ __global__ __launch_bounds__(256) void wy_apply_t_kernel(const double* __restric
         const int a = i0 + 16 * bi + 4 * r + lk, j = jw + 16 * bj + li;
         if (a < kb && j0 + j < m) Yg[(int64_t)a * ldy + j0 + j] = acc[bi][bj][r];
       }
+}
+
+// Y for a pair of consecutive WY blocks a, b = a+1 applied in one pass
+// (block b first): with X = [X_a; X_b] = [V_a; V_b] Q22 given as S split-K
+// parts (rows 0..63: X_a, 64..127: X_b, row r of part s at xpart + s sP +
+// g sX + r ldx), Y_b = T_b X_b and Y_a = T_a (X_a - G_ab Y_b), G_ab =
+// V_a V_b', since V_a (Q22 - V_b' Y_b) = X_a - G_ab Y_b. Then
+// Q22 - V_b' Y_b - V_a' Y_a = Q22 - [V_a; V_b]' [Y_a; Y_b]. Workgroup
+// (32-column tile, g) stages both X tiles and one 64 x 64 factor at a time
+// in LDS; wave w forms rows 16 w .. 16 w + 15 of each product on the
+// matrix cores.
+__global__ __launch_bounds__(256) void wy_apply_pair_kernel(
+    const double* __restrict__ ta, const double* __restrict__ tb, const double* __restrict__ gab,
+    const double* __restrict__ xpart, int S, int64_t sP, int64_t sX, int64_t ldx, int m,
+    double* __restrict__ Y, int64_t ldy, int64_t sY) {
+  constexpr int W = kWyBlock, CT = 32;
+  __shared__ double Fs[W][W + 1];
+  __shared__ double Xa[W][CT + 1];
+  __shared__ double Xb[W][CT + 1];
+  const int g = blockIdx.y, j0 = CT * blockIdx.x, t = threadIdx.x;
+  const int w = t >> 6, lane = t & 63, li = lane & 15, lk = lane >> 4;
+  const int64_t fo = (int64_t)g * W * W;
+  const auto load_f = [&](const double* F) {
+#pragma unroll
+    for (int u = 0; u < W * W / 256; ++u) {
+      const int e = t + 256 * u;
+      Fs[e / W][e % W] = F[fo + e];
+    }
+  };
+  load_f(tb);
+  {
+    // thread t stages row a = t/4, columns 8 (t%4) .. +7 of both tiles;
+    // every load is issued before the first sum
+    const int a = t >> 2, jq = 8 * (t & 3);
+    const double* Xg = xpart + (int64_t)g * sX;
+    double va[kMaxSplitK][8], vb[kMaxSplitK][8];
+#pragma unroll
+    for (int q = 0; q < kMaxSplitK; ++q)
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + jq + u;
+        const bool ok = q < S && j < m;
+        const double* xr = Xg + (int64_t)q * sP + (int64_t)a * ldx + j;
+        va[q][u] = ok ? xr[0] : 0.0;
+        vb[q][u] = ok ? xr[(int64_t)W * ldx] : 0.0;
+      }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      double sa = va[0][u], sb = vb[0][u];
+#pragma unroll
+      for (int q = 1; q < kMaxSplitK; ++q) {   // zero past S: the same sums
+        sa += va[q][u];
+        sb += vb[q][u];
+      }
+      Xa[a][jq + u] = sa;
+      Xb[a][jq + u] = sb;
+    }
+  }
+  __syncthreads();
+  // acc <- +/- F rows 16w.. times X (64 x 32), added to acc
+  const auto mm = [&](double sgn, double (*X)[CT + 1], xdbl4 (&acc)[2]) {
+#pragma unroll
+    for (int k = 0; k < W; k += 4) {
+      const double a = sgn * Fs[16 * w + li][k + lk];
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj)
+        acc[bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, X[k + lk][16 * bj + li], acc[bj], 0, 0, 0);
+    }
+  };
+  double* Yg = Y + (int64_t)g * sY;
+  const auto put = [&](xdbl4 (&acc)[2], double (*X)[CT + 1], int row0) {
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int a = 16 * w + 4 * r + lk, j = 16 * bj + li;
+        if (X) X[a][j] = acc[bj][r];
+        if (j0 + j < m) Yg[(int64_t)(row0 + a) * ldy + j0 + j] = acc[bj][r];
+      }
+  };
+  xdbl4 acc[2] = {xdbl4{0.0, 0.0, 0.0, 0.0}, xdbl4{0.0, 0.0, 0.0, 0.0}};
+  mm(1.0, Xb, acc);                                   // Y_b = T_b X_b
+  __syncthreads();
+  put(acc, Xb, W);                                    // Y_b over X_b
+  load_f(gab);
+  __syncthreads();
+#pragma unroll
+  for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[bj][r] = Xa[16 * w + 4 * r + lk][16 * bj + li];
+  mm(-1.0, Xb, acc);                                  // X_a - G_ab Y_b
+  __syncthreads();
+#pragma unroll
+  for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Xa[16 * w + 4 * r + lk][16 * bj + li] = acc[bj][r];
+  load_f(ta);
+  __syncthreads();
+  acc[0] = acc[1] = xdbl4{0.0, 0.0, 0.0, 0.0};
+  mm(1.0, Xa, acc);                                   // Y_a = T_a (X_a - G_ab Y_b)
+  put(acc, nullptr, 0);
 }
 
 int band_reduce(hipStream_t s, const BandWork& wk) {
@@ -1078,7 +1191,7 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     hipLaunchKernelGGL(band_extract_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, s,
                        wk.A, N, tot, wk.band);
     KMP_LAUNCH_CHECK();
-    const int64_t tz = (int64_t)G * (N - BB) * (64 + BB);
+    const int64_t tz = (int64_t)G * (N - BB) * (2 * kWyBlock + BB);
     hipLaunchKernelGGL(clear_reflector_rows_kernel, dim3((unsigned)ceil_div(tz, 256)), dim3(256), 0,
                        s, wk.A, N, tz);
     KMP_LAUNCH_CHECK();
@@ -1089,62 +1202,91 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
   }
   // Q = H_0 H_1 ... (reflector rows 0 .. N-BB-1), accumulated backwards in
   // blocks of kWyBlock rows: Q[q+BB:, q+BB:] -= V' (T (V Q[q+BB:, q+BB:])).
-  // The Grams and T factors of all blocks depend on the reflectors only and
-  // are formed first, two launches for all blocks.
+  // The Grams, cross products and T factors of all blocks depend on the
+  // reflectors only and are formed first, two launches for all blocks.
+  // The last (partial) block goes alone, then the others in pairs, one
+  // pass over Q22 per pair (see wy_apply_pair_kernel), a single block at
+  // the bottom if one is left.
   const int nref = N - BB;
   const int nblk = wy_blocks(N);
   kc_begin(KMP_KC_QFORM, s);
-  hipLaunchKernelGGL(wy_gram_kernel, dim3((unsigned)nblk, (unsigned)G), dim3(256), 0, s, wk.A, N, nref,
-                     wk.gram_all);
+  hipLaunchKernelGGL(wy_gram_kernel, dim3((unsigned)nblk, (unsigned)G, 2u), dim3(256), 0, s, wk.A, N,
+                     nref, wk.gram_all, wk.cross_all);
   KMP_LAUNCH_CHECK();
   if ((rc = wy_form_t_blocks(s, wk.gram_all, wk.tau, wk.tmat_all, G, N, nref, nblk)) != 0) return rc;
-  const int last = ((nref - 1) / kWyBlock) * kWyBlock;
-  for (int q = last; q >= 0; q -= kWyBlock) {
-    const int kb = std::min(kWyBlock, nref - q);
+  const int64_t sW = (int64_t)G * kWyBlock * kWyBlock;      // between blocks in tmat_all, cross_all
+  const int64_t sY = (int64_t)2 * kWyBlock * N;             // per matrix in ybuf and xpart
+  const int64_t sXP = (int64_t)G * sY;                      // between split-K parts of xpart
+  bool first = true;
+  const auto step = [&](int b, bool pair) -> int {
+    const int q = kWyBlock * b;
+    const int kb = pair ? 2 * kWyBlock : std::min(kWyBlock, nref - q);
     const int m = N - q - BB;
-    if (q != last) kc_begin(KMP_KC_QFORM, s);
-    const double* tq = wk.tmat_all + (int64_t)(q / kWyBlock) * G * kWyBlock * kWyBlock;
+    if (!first) kc_begin(KMP_KC_QFORM, s);
+    first = false;
     // X = V Q[q+BB:, q+BB:] (kb x m) as split-K parts, in the transposed
     // form X' = Q[q+BB:, q+BB:]' V' (m x kb: the A operand is Q22 read by
-    // rows, B the reflector rows), then Y = T X
+    // rows, B the reflector rows)
     GemmArgs h1;
     h1.M = m; h1.N = kb; h1.K = m; h1.batch = G;
     h1.A = wk.Q + (int64_t)(q + BB) * N + q + BB; h1.lda = N; h1.sA = (int64_t)N * N;
     h1.B = wk.A + (int64_t)q * N + q + BB; h1.ldb = N; h1.sB = (int64_t)N * N;
-    h1.ldc = N; h1.sC = (int64_t)kWyBlock * N;
-    const int64_t sXP = (int64_t)G * kWyBlock * N;
+    h1.ldc = N; h1.sC = sY;
     const int S1 = splitk_parts(h1);
     if ((rc = gemm_partial(s, h1, false, S1, wk.xpart, sXP, nullptr, nullptr)) != 0) return rc;
-    hipLaunchKernelGGL(wy_apply_t_kernel, dim3((unsigned)ceil_div(m, kWyBlock), (unsigned)G),
-                       dim3(256), 0, s, tq, kb, (const double*)wk.xpart, S1, sXP,
-                       (int64_t)kWyBlock * N, (int64_t)N, m, wk.ybuf, (int64_t)N,
-                       (int64_t)kWyBlock * N);
+    const double* tq = wk.tmat_all + (int64_t)b * sW;
+    if (pair) {
+      hipLaunchKernelGGL(wy_apply_pair_kernel, dim3((unsigned)ceil_div(m, 32), (unsigned)G), dim3(256),
+                         0, s, tq, tq + sW, (const double*)(wk.cross_all + (int64_t)b * sW),
+                         (const double*)wk.xpart, S1, sXP, sY, (int64_t)N, m, wk.ybuf, (int64_t)N,
+                         sY);
+    } else {
+      hipLaunchKernelGGL(wy_apply_t_kernel, dim3((unsigned)ceil_div(m, kWyBlock), (unsigned)G),
+                         dim3(256), 0, s, tq, kb, (const double*)wk.xpart, S1, sXP, sY, (int64_t)N,
+                         m, wk.ybuf, (int64_t)N, sY);
+    }
     KMP_LAUNCH_CHECK();
-    // Q[q+BB:, q+BB:] -= V' Y  (K = kb = 64; the last block may be shorter
-    // only when N - BB is not a multiple of 64, then the generic product)
-    if (kb == kWyBlock) {
-      hipLaunchKernelGGL((rank_update_kernel<2, false>),
-                         dim3((unsigned)ceil_div(m, 64), (unsigned)ceil_div(m, 64), (unsigned)G),
-                         dim3(256), 0, s, wk.Q + (int64_t)(q + BB) * N + q + BB, (int64_t)N,
-                         (int64_t)N * N, m, (const double*)(wk.A + (int64_t)q * N + q + BB),
-                         (int64_t)N, (int64_t)N * N, (const double*)wk.ybuf, (int64_t)N,
-                         (int64_t)kWyBlock * N);
+    // Q[q+BB:, q+BB:] -= V' Y  (K = kb: 128 for a pair, 64 for a full
+    // single block, else the generic product)
+    const dim3 ug((unsigned)ceil_div(m, 64), (unsigned)ceil_div(m, 64), (unsigned)G);
+    double* Q22 = wk.Q + (int64_t)(q + BB) * N + q + BB;
+    const double* P1 = wk.A + (int64_t)q * N + q + BB;
+    if (kb == 2 * kWyBlock) {
+      hipLaunchKernelGGL((rank_update_kernel<4, false>), ug, dim3(256), 0, s, Q22, (int64_t)N,
+                         (int64_t)N * N, m, P1, (int64_t)N, (int64_t)N * N,
+                         (const double*)wk.ybuf, (int64_t)N, sY);
+      KMP_LAUNCH_CHECK();
+    } else if (kb == kWyBlock) {
+      hipLaunchKernelGGL((rank_update_kernel<2, false>), ug, dim3(256), 0, s, Q22, (int64_t)N,
+                         (int64_t)N * N, m, P1, (int64_t)N, (int64_t)N * N,
+                         (const double*)wk.ybuf, (int64_t)N, sY);
       KMP_LAUNCH_CHECK();
     } else {
       GemmArgs h3;
       h3.M = m; h3.N = m; h3.K = kb; h3.batch = G;
-      h3.A = wk.A + (int64_t)q * N + q + BB; h3.lda = N; h3.sA = (int64_t)N * N;
-      h3.B = wk.ybuf; h3.ldb = N; h3.sB = (int64_t)kWyBlock * N;
-      h3.C = wk.Q + (int64_t)(q + BB) * N + q + BB; h3.ldc = N; h3.sC = (int64_t)N * N;
+      h3.A = P1; h3.lda = N; h3.sA = (int64_t)N * N;
+      h3.B = wk.ybuf; h3.ldb = N; h3.sB = sY;
+      h3.C = Q22; h3.ldc = N; h3.sC = (int64_t)N * N;
       h3.alpha = -1.0; h3.beta = 1.0;
       if ((rc = gemm(s, h3, false, false, true)) != 0) return rc;
     }
+    // Q22 read twice, written once; flops of V Q22, T X (and G Y), V' Y
     kc_end(KMP_KC_QFORM, s, over_groups(wk, [&](double n) {
              const double mm = std::max(0.0, n - q - BB); return 24.0 * mm * mm; }),
            over_groups(wk, [&](double n) {
              const double mm = std::max(0.0, n - q - BB);
-             return 4.0 * kb * mm * mm + 2.0 * kb * kb * mm; }));
+             const double tk = pair ? 3.0 * kWyBlock * kWyBlock : (double)kb * kb;
+             return 4.0 * kb * mm * mm + 2.0 * tk * mm; }));
+    return 0;
+  };
+  int b = nblk - 1;
+  if (nref % kWyBlock != 0) {
+    if ((rc = step(b, false)) != 0) return rc;
+    --b;
   }
+  for (; b >= 1; b -= 2)
+    if ((rc = step(b - 1, true)) != 0) return rc;
+  if (b == 0 && (rc = step(0, false)) != 0) return rc;
   return 0;
 }
 

@@ -105,7 +105,7 @@ struct Carver {
 // size and to carve, so the two can never disagree.
 struct Layout {
   double *A, *Qm, *diag, *off, *tau, *cvec, *ylab, *panel, *dots, *tmat, *gram, *xbuf, *ybuf;
-  double *spart, *pnext, *band, *bpart, *gram_all, *tmat_all, *xpart;
+  double *spart, *pnext, *band, *bpart, *gram_all, *tmat_all, *cross_all, *xpart;
   double *ahat, *abar, *bmat, *zmat, *anew, *estep, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
   double *beta, *bbar, *rmom, *gcoef, *kkt, *coef, *lam, *taucol, *fbuf, *nrm, *inv2s2;
   int *flag, *moved, *iters, *iters_total, *active, *nvg, *chk, *cmap, *nact;
@@ -128,14 +128,15 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.tmat = c.take<double>(G * kWyBlock * kWyBlock);
   l.gram = c.take<double>(G * kWyBlock * kWyBlock);
   l.xbuf = c.take<double>(G * kWyBlock * N);
-  l.ybuf = c.take<double>(G * kWyBlock * N);
+  l.ybuf = c.take<double>(G * 2 * kWyBlock * N);
   l.spart = c.take<double>(G * (size_t)tridiag_parts((int)N));
   l.pnext = c.take<double>(G * N);
   l.band = c.take<double>(G * (kBand + 1) * N);
   l.bpart = c.take<double>(band_part_doubles((int)G, (int)N));
   l.gram_all = c.take<double>(wy_all_doubles((int)G, (int)N));
   l.tmat_all = c.take<double>(wy_all_doubles((int)G, (int)N));
-  l.xpart = c.take<double>((size_t)kMaxSplitK * G * kWyBlock * N);
+  l.cross_all = c.take<double>(wy_all_doubles((int)G, (int)N));
+  l.xpart = c.take<double>((size_t)kMaxSplitK * G * 2 * kWyBlock * N);
   l.ahat = c.take<double>(cols * N);
   l.abar = c.take<double>(cols * N);
   l.bmat = c.take<double>(cols * N);
@@ -395,10 +396,11 @@ int kmp_band_reduce(void* stream, double* A, int32_t G, int32_t N, double* Qout,
   w.tmat = q; q += (size_t)G * kWyBlock * kWyBlock;
   w.gram = q; q += (size_t)G * kWyBlock * kWyBlock;
   w.xbuf = q; q += (size_t)G * kWyBlock * N;
-  w.ybuf = q; q += (size_t)G * kWyBlock * N;
+  w.ybuf = q; q += (size_t)G * 2 * kWyBlock * N;
   w.gram_all = q; q += wy_all_doubles(G, N);
   w.tmat_all = q; q += wy_all_doubles(G, N);
-  w.xpart = q; q += (size_t)kMaxSplitK * G * kWyBlock * N;
+  w.cross_all = q; q += wy_all_doubles(G, N);
+  w.xpart = q; q += (size_t)kMaxSplitK * G * 2 * kWyBlock * N;
   w.part = q;
   int rc = band_reduce(s, w);
   KMP_HIP_TRY(hipFreeAsync(scratch, s));
@@ -614,7 +616,8 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     bw.panel = lay.panel; bw.panel2 = lay.panel + (size_t)Gb * 3 * kBand * N;
     bw.tmat = lay.tmat; bw.gram = lay.gram; bw.xbuf = lay.xbuf;
     bw.ybuf = lay.ybuf; bw.part = lay.bpart; bw.nv_host = nvg.data();
-    bw.gram_all = lay.gram_all; bw.tmat_all = lay.tmat_all; bw.xpart = lay.xpart;
+    bw.gram_all = lay.gram_all; bw.tmat_all = lay.tmat_all; bw.cross_all = lay.cross_all;
+    bw.xpart = lay.xpart;
     if ((rc = band_reduce(s, bw)) != 0) return rc;
     if ((rc = group_ones_projection(s, lay.Qm, lay.nvg, Gb, N, lay.cvec)) != 0) return rc;
     if ((rc = gather_labels(s, y, lay.tidx, V, sb, N, lay.ylab)) != 0) return rc;

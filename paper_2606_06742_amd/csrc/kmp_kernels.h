@@ -89,11 +89,12 @@ struct BandWork {
   double* tmat = nullptr;   // G x 64 x 64
   double* gram = nullptr;   // G x 64 x 64
   double* xbuf = nullptr;   // G x 64 x N
-  double* ybuf = nullptr;   // G x 64 x N
+  double* ybuf = nullptr;   // G x 128 x N
   double* part = nullptr;   // band_part_doubles(G, N): chunk partials of the Gram products
   double* gram_all = nullptr;  // wy_blocks(N) x G x 64 x 64: Grams of the WY blocks of Q
   double* tmat_all = nullptr;  // same shape: their T factors
-  double* xpart = nullptr;     // kMaxSplitK x G x 64 x N: split-K parts of V Q in the Q accumulation
+  double* cross_all = nullptr; // same shape: V_b V_{b+1}' of consecutive blocks
+  double* xpart = nullptr;     // kMaxSplitK x G x 128 x N: split-K parts of V Q in the Q accumulation
   const int* nv_host = nullptr;  // G valid orders (host), for the work counters; N if null
 };
 // Doubles of scratch band_reduce needs beyond A, Q, band and tau (the chunk
