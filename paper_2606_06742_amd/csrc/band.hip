@@ -418,88 +418,113 @@ __global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restric
 //
 // X' = Y' A22 and the partial products of M2 = V'X for one panel (A22 =
 // A[m0:, m0:], Y' = T'V' stored transposed, Yt[k][i] = Yt[16 k + i], m x 16).
-// One workgroup per 16 columns j0 .. j0+15 of X' and matrix: wave w
-// accumulates the 16-row chunks q = w, w+4, ... on the matrix cores (A
-// operand Yt[k][i], one 512-byte piece per load; B operand A22[k][j],
-// 128-byte row pieces), the four partial tiles are added in LDS,
-// X' goes to rows BB .. 2BB-1 of the panel buffer, and the workgroup's part
-// of M2, sum_{j in block} V'[a][j] X'[b][j], to part[(g NJ + block)*256].
-constexpr int XUQ = 4;            // 16-row chunks per wave and iteration
-
+// One workgroup per 64 columns (four 16-column blocks) of X' and matrix:
+// wave w accumulates the 16-row chunks q = w, w+4, ... of all four blocks
+// on the matrix cores (A operand Yt[k][i]; B operand A22[k][j], so that
+// below the diagonal each chunk is read as 512-byte row pieces, with its Y'
+// operand loaded once for the four blocks). A chunk may lie below some
+// blocks and above others (the test is per block and uniform over the
+// wavefront); above, a block's entries A22[j][k] are read from its
+// transposed rows, 32 contiguous bytes per lane, with the k of MFMA step s4
+// in lane group kq taken as 16 q + 4 kq + s4 (16 q + 4 s4 + kq below). The
+// four partial tiles of each block are added in LDS, X' goes to rows
+// BB .. 2BB-1 of the panel buffer, and the workgroup's parts of M2,
+// sum_{j in block} V'[a][j] X'[b][j], to part[(g NJ + block)*256].
+constexpr int XU4 = 1;            // chunks per wavefront and iteration
 __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__ A, int N, int m0,
                                                        const double* __restrict__ ybuf,
                                                        double* __restrict__ panel,
                                                        double* __restrict__ part, int NJ) {
-  __shared__ double red[4][4][64];
-  __shared__ double Xs[BB][BB + 1];
-  const int jb = blockIdx.x, g = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int m = N - m0, j0 = BB * jb, nch = m / BB;
+  __shared__ double red[4][4][4][64];              // wave, block, register, lane
+  __shared__ double Xs[4][BB][BB + 1];
+  const int g = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int m = N - m0, nch = m / BB, jb0 = 4 * blockIdx.x;
+  const int nbv = min(4, nch - jb0);               // valid blocks of this workgroup
   const double* Ag = A + (int64_t)g * N * N + (int64_t)m0 * N + m0;
   const double* Yg = ybuf + (int64_t)g * kWyBlock * N;
   double* Pg = panel + (int64_t)g * 3 * BB * N + m0;
   const int i = lane & 15, kq = lane >> 4;
-  // k of MFMA step s4 in lane group kq: 16 q + 4 s4 + kq below the block
-  // row (each load covers four 128-byte row pieces), 16 q + 4 kq + s4 above
-  // it (each lane reads 32 contiguous bytes of its row)
   const double* ya = Yg + (int64_t)kq * BB + i;
   const double* yt = Yg + (int64_t)(4 * kq) * BB + i;
-  const double* bb = Ag + (int64_t)kq * N + j0 + i;           // A22[k][j0 + i], k >= j
-  const double* bt = Ag + (int64_t)(j0 + i) * N + 4 * kq;     // A22[j0 + i][k], k < j
-  xdbl4 acc = {0.0, 0.0, 0.0, 0.0};
-  for (int q = w; q < nch; q += 4 * XUQ) {
-    double av[XUQ][4], bv[XUQ][4];
+  const double* bb = Ag + (int64_t)kq * N + BB * jb0 + i;          // + 16 c: block c, below
+  const double* bt = Ag + (int64_t)(BB * jb0 + i) * N + 4 * kq;    // + 16 c N: block c, above
+  xdbl4 acc[4];
 #pragma unroll
-    for (int u = 0; u < XUQ; ++u) {
-      const int qq = (q + 4 * u < nch) ? q + 4 * u : q;      // clamped: not accumulated
-      if (qq >= jb) {                                          // chunk on or below the block row
+  for (int c = 0; c < 4; ++c) acc[c] = xdbl4{0.0, 0.0, 0.0, 0.0};
+  for (int q = w; q < nch; q += 4 * XU4) {
+#pragma unroll
+    for (int u = 0; u < XU4; ++u) {
+      const int qq = q + 4 * u;
+      if (qq < nch) {                                // uniform over the wavefront
+        double avb[4], ava[4], bv[4][4];
+        const bool anyb = qq >= jb0, anya = qq < jb0 + nbv - 1;
 #pragma unroll
         for (int s4 = 0; s4 < 4; ++s4) {
-          const int k = BB * qq + 4 * s4;
-          av[u][s4] = ya[(int64_t)k * BB];
-          bv[u][s4] = bb[(int64_t)k * N];
+          avb[s4] = anyb ? ya[(int64_t)(BB * qq + 4 * s4) * BB] : 0.0;
+          ava[s4] = anya ? yt[(int64_t)(BB * qq + s4) * BB] : 0.0;
         }
-      } else {
-        const double2 b01 = *reinterpret_cast<const double2*>(bt + BB * qq);
-        const double2 b23 = *reinterpret_cast<const double2*>(bt + BB * qq + 2);
-        bv[u][0] = b01.x; bv[u][1] = b01.y; bv[u][2] = b23.x; bv[u][3] = b23.y;
 #pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) av[u][s4] = yt[(int64_t)(BB * qq + s4) * BB];
+        for (int c = 0; c < 4; ++c) {
+          if (c < nbv) {
+            if (qq >= jb0 + c) {
+#pragma unroll
+              for (int s4 = 0; s4 < 4; ++s4) bv[c][s4] = bb[(int64_t)(BB * qq + 4 * s4) * N + BB * c];
+            } else {
+              const double* br = bt + (int64_t)(BB * c) * N + BB * qq;
+              const double2 b01 = *reinterpret_cast<const double2*>(br);
+              const double2 b23 = *reinterpret_cast<const double2*>(br + 2);
+              bv[c][0] = b01.x; bv[c][1] = b01.y; bv[c][2] = b23.x; bv[c][3] = b23.y;
+            }
+          }
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          if (c < nbv) {
+            const bool below = qq >= jb0 + c;
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4)
+              acc[c] = __builtin_amdgcn_mfma_f64_16x16x4f64(below ? avb[s4] : ava[s4], bv[c][s4],
+                                                            acc[c], 0, 0, 0);
+          }
+        }
       }
-    }
-#pragma unroll
-    for (int u = 0; u < XUQ; ++u) {
-      const bool ok = q + 4 * u < nch;
-#pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4)
-        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(ok ? av[u][s4] : 0.0, bv[u][s4], acc, 0, 0, 0);
     }
   }
 #pragma unroll
-  for (int r = 0; r < 4; ++r) red[w][r][lane] = acc[r];
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[w][c][r][lane] = acc[c][r];
   __syncthreads();
-  {
-    const int r = t >> 6, l = t & 63;
-    const double v = (red[0][r][l] + red[1][r][l]) + (red[2][r][l] + red[3][r][l]);
-    const int b = 4 * r + (l >> 4), j = l & 15;
-    Xs[b][j] = v;
-    Pg[(int64_t)(BB + b) * N + j0 + j] = v;
+  // X' of block c, register r, lane l: row 4 r + l / 16, column l % 16
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const int c = h, r = t >> 6, l = t & 63;
+    if (c < nbv) {
+      const double v = (red[0][c][r][l] + red[1][c][r][l]) + (red[2][c][r][l] + red[3][c][r][l]);
+      const int b = 4 * r + (l >> 4), j = l & 15;
+      Xs[c][b][j] = v;
+      Pg[(int64_t)(BB + b) * N + BB * (jb0 + c) + j] = v;
+    }
   }
   __syncthreads();
   {
     const int a = t >> 4, b = t & 15;
-    const double* va = Pg + (int64_t)a * N + j0;
-    double s0 = 0.0, s1 = 0.0;
 #pragma unroll
-    for (int j = 0; j < BB; j += 2) {
-      s0 = fma(va[j], Xs[b][j], s0);
-      s1 = fma(va[j + 1], Xs[b][j + 1], s1);
+    for (int c = 0; c < 4; ++c) {
+      if (c < nbv) {
+        const double* va = Pg + (int64_t)a * N + BB * (jb0 + c);
+        double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+        for (int j = 0; j < BB; j += 2) {
+          s0 = fma(va[j], Xs[c][b][j], s0);
+          s1 = fma(va[j + 1], Xs[c][b][j + 1], s1);
+        }
+        part[((int64_t)g * NJ + jb0 + c) * 256 + t] = s0 + s1;
+      }
     }
-    part[((int64_t)g * NJ + jb) * 256 + t] = s0 + s1;
   }
 }
 
-// S = T'M2 with M2 = V'X summed in order from the block products in part;
-// one workgroup per matrix, S into sbuf (16 x 16, row-major, stride sS).
 __global__ __launch_bounds__(256) void panel_s_kernel(int N, int m0, const double* __restrict__ part,
                                                        int NJ, const double* __restrict__ tmat,
                                                        double* __restrict__ sbuf, int64_t sS) {
@@ -1139,8 +1164,8 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     // W' = X' - 1/2 (T'M2)' V' in place of X'
     {
       const int NJ = (int)ceil_div(N, BB);
-      hipLaunchKernelGGL(panel_x_kernel, dim3((unsigned)(mrow / BB), (unsigned)G), dim3(256), 0, s,
-                         wk.A, N, m0, wk.xbuf, pb, wk.part, NJ);
+      hipLaunchKernelGGL(panel_x_kernel, dim3((unsigned)ceil_div(mrow / BB, 4), (unsigned)G),
+                         dim3(256), 0, s, wk.A, N, m0, wk.xbuf, pb, wk.part, NJ);
       KMP_LAUNCH_CHECK();
       const int64_t sS = (int64_t)kWyBlock * N;
       hipLaunchKernelGGL(panel_s_kernel, dim3((unsigned)G), dim3(256), 0, s, N, m0, wk.part, NJ,
@@ -1173,12 +1198,14 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
                          (int64_t)N, sP, P2, (int64_t)N, sP);
       KMP_LAUNCH_CHECK();
     }
+    // the lower triangle of A22 read and written once, rank-2 BB products
+    // on it; with a next panel, that panel's factorisation as well
     kc_end(KMP_KC_TRAIL, s,
            over_groups(wk, [&](double n) {
-             const double m = std::max(0.0, n - m0); return 16.0 * m * m; }) +
+             const double m = std::max(0.0, n - m0); return 8.0 * m * m; }) +
                (next ? qr_bytes(m0 + BB) : 0.0),
            over_groups(wk, [&](double n) {
-             const double m = std::max(0.0, n - m0); return 4.0 * BB * m * m; }) +
+             const double m = std::max(0.0, n - m0); return 2.0 * BB * m * m; }) +
                (next ? qr_flops(m0 + BB) : 0.0));
     if (next) {
       kc_begin(KMP_KC_PANEL_WY, s);
@@ -1214,16 +1241,25 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
                      nref, wk.gram_all, wk.cross_all);
   KMP_LAUNCH_CHECK();
   if ((rc = wy_form_t_blocks(s, wk.gram_all, wk.tau, wk.tmat_all, G, N, nref, nblk)) != 0) return rc;
+  // reflector rows of each block read for its Gram and, with the next
+  // block's, for the cross products; 64 x 64 products over m columns
+  kc_end(KMP_KC_QFORM, s, over_groups(wk, [&](double n) {
+           double a = 0.0;
+           for (int b = 0; b < nblk; ++b) a += 3.0 * 8.0 * kWyBlock * std::max(0.0, n - kWyBlock * b - BB);
+           return a; }),
+         over_groups(wk, [&](double n) {
+           double a = 0.0;
+           for (int b = 0; b < nblk; ++b)
+             a += 2.0 * 2.0 * kWyBlock * kWyBlock * std::max(0.0, n - kWyBlock * b - BB);
+           return a; }));
   const int64_t sW = (int64_t)G * kWyBlock * kWyBlock;      // between blocks in tmat_all, cross_all
   const int64_t sY = (int64_t)2 * kWyBlock * N;             // per matrix in ybuf and xpart
   const int64_t sXP = (int64_t)G * sY;                      // between split-K parts of xpart
-  bool first = true;
   const auto step = [&](int b, bool pair) -> int {
     const int q = kWyBlock * b;
     const int kb = pair ? 2 * kWyBlock : std::min(kWyBlock, nref - q);
     const int m = N - q - BB;
-    if (!first) kc_begin(KMP_KC_QFORM, s);
-    first = false;
+    kc_begin(KMP_KC_QFORM, s);
     // X = V Q[q+BB:, q+BB:] (kb x m) as split-K parts, in the transposed
     // form X' = Q[q+BB:, q+BB:]' V' (m x kb: the A operand is Q22 read by
     // rows, B the reflector rows)
