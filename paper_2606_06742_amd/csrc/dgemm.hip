@@ -287,8 +287,8 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
 // Only the active columns of a batch are computed: tile column k < nact[b]
 // is column cmap[b*cstride + k] of B and of the partials (the other columns
 // of the partials are left as they were); tiles past nact[b] exit at once.
-// With cmap and nact null, all cstride columns, in order.
-template <int BM, int BK, bool AK>
+// With IDENT (cmap and nact null), all cstride columns, in order.
+template <int BM, int BK, bool AK, bool IDENT>
 __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S, int Kc,
                                                              const double* __restrict__ A, int64_t lda, int64_t sA,
                                                              const double* __restrict__ B, int64_t ldb, int64_t sB,
@@ -297,10 +297,10 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
                                                              const int* __restrict__ nact, int cstride) {
   constexpr int MB = Tile<BM, BK>::MB;
   const int b = blockIdx.z / S, sk = blockIdx.z % S;
-  const int N = nact ? nact[b] : cstride;
+  const int N = IDENT ? cstride : nact[b];
   const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TN;
   if (j0 >= N) return;
-  const int* cmap = cmap_all ? cmap_all + (int64_t)b * cstride : nullptr;
+  const int* cmap = IDENT ? nullptr : cmap_all + (int64_t)b * cstride;
   A += (int64_t)b * sA;
   B += (int64_t)b * sB;
   double* C = part + (int64_t)sk * sP + (int64_t)b * sC;
@@ -324,7 +324,7 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
       for (int r = 0; r < 4; ++r) {
         const int gi = i0 + wi + bi * 16 + mfma_row(lane, r);
         const int gj = j0 + wj + bj * 16 + mfma_col(lane);
-        if (gi < M && gj < N) C[(int64_t)(cmap ? cmap[gj] : gj) * ldc + gi] = acc[bi][bj][r];
+        if (gi < M && gj < N) C[(int64_t)(IDENT ? gj : cmap[gj]) * ldc + gi] = acc[bi][bj][r];
       }
 }
 
@@ -437,14 +437,21 @@ int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return 0;
   const int Kc = (int)round_up(ceil_div(g.K, S), 16);
   dim3 grid((unsigned)ceil_div(g.M, 64), (unsigned)ceil_div(g.N, TN), (unsigned)(g.batch * S));
-  if (a_kcontig)
-    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, true>), grid, dim3(256), 0, s, g.M, g.K, S,
-                       Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap, nact,
-                       g.N);
-  else
-    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, false>), grid, dim3(256), 0, s, g.M, g.K, S,
-                       Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap, nact,
-                       g.N);
+  const bool ident = cmap == nullptr;
+  if (ident != (nact == nullptr)) {
+    set_error("gemm_partial: cmap and nact must both be given or both be null");
+    return KMP_EINVAL;
+  }
+#define KMP_PART_CASE(AKV, IDV)                                                                  \
+  if (a_kcontig == AKV && ident == IDV)                                                          \
+    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, AKV, IDV>), grid, dim3(256), 0, s, g.M, g.K, \
+                       S, Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap,    \
+                       nact, g.N);
+  KMP_PART_CASE(true, false)
+  KMP_PART_CASE(false, false)
+  KMP_PART_CASE(true, true)
+  KMP_PART_CASE(false, true)
+#undef KMP_PART_CASE
   KMP_LAUNCH_CHECK();
   return 0;
 }
