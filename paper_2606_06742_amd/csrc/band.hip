@@ -427,14 +427,15 @@ __global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restric
 // wavefront); above, a block's entries A22[j][k] are read from its
 // transposed rows, 32 contiguous bytes per lane, with the k of MFMA step s4
 // in lane group kq taken as 16 q + 4 kq + s4 (16 q + 4 s4 + kq below). The
-// four partial tiles of each block are added in LDS, X' goes to rows
-// BB .. 2BB-1 of the panel buffer, and the workgroup's parts of M2,
+// four partial tiles of each block are added in LDS, X' goes to xq (row b
+// of matrix g at xq + g sX + b N), and the workgroup's parts of M2,
 // sum_{j in block} V'[a][j] X'[b][j], to part[(g NJ + block)*256].
 constexpr int XU4 = 1;            // chunks per wavefront and iteration
 __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__ A, int N, int m0,
                                                        const double* __restrict__ ybuf,
-                                                       double* __restrict__ panel,
-                                                       double* __restrict__ part, int NJ) {
+                                                       const double* __restrict__ panel,
+                                                       double* __restrict__ part, int NJ,
+                                                       double* __restrict__ xq, int64_t sX) {
   __shared__ double red[4][4][4][64];              // wave, block, register, lane
   __shared__ double Xs[4][BB][BB + 1];
   const int g = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
@@ -442,7 +443,8 @@ __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__
   const int nbv = min(4, nch - jb0);               // valid blocks of this workgroup
   const double* Ag = A + (int64_t)g * N * N + (int64_t)m0 * N + m0;
   const double* Yg = ybuf + (int64_t)g * kWyBlock * N;
-  double* Pg = panel + (int64_t)g * 3 * BB * N + m0;
+  const double* Pg = panel + (int64_t)g * 3 * BB * N + m0;
+  double* Xg = xq + (int64_t)g * sX + m0;
   const int i = lane & 15, kq = lane >> 4;
   const double* ya = Yg + (int64_t)kq * BB + i;
   const double* yt = Yg + (int64_t)(4 * kq) * BB + i;
@@ -503,7 +505,7 @@ __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__
       const double v = (red[0][c][r][l] + red[1][c][r][l]) + (red[2][c][r][l] + red[3][c][r][l]);
       const int b = 4 * r + (l >> 4), j = l & 15;
       Xs[c][b][j] = v;
-      Pg[(int64_t)(BB + b) * N + BB * (jb0 + c) + j] = v;
+      Xg[(int64_t)b * N + BB * (jb0 + c) + j] = v;
     }
   }
   __syncthreads();
@@ -525,12 +527,27 @@ __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__
   }
 }
 
-__global__ __launch_bounds__(256) void panel_s_kernel(int N, int m0, const double* __restrict__ part,
-                                                       int NJ, const double* __restrict__ tmat,
-                                                       double* __restrict__ sbuf, int64_t sS) {
+// S = T'M2 from the per-block parts of M2 (added in block order), W' =
+// X' - 1/2 S'V' for the workgroup's 64 columns (X' read from xq, W' into
+// rows BB .. 2BB-1 of the panel buffer), then the two-sided update of the
+// first block column of A22 for the workgroup's 64 rows:
+//   A22[i][j] -= sum_k V[k][i] W[k][j] + W[k][i] V[k][j],   j < 16,
+// wave w taking rows 16 w .. 16 w + 15 of the tile on the matrix cores
+// (C loaded into the accumulators, K = 32 over [V; W] against [W; V]).
+// The W' operands come from LDS: the workgroup's own columns, and columns
+// 0 .. 15 formed again by every workgroup, so that none reads what another
+// one writes. One workgroup per 64 rows and matrix.
+__global__ __launch_bounds__(256) void panel_ws_kernel(double* __restrict__ A, int N, int m0,
+                                                       const double* __restrict__ part, int NJ,
+                                                       const double* __restrict__ tmat,
+                                                       const double* __restrict__ xq, int64_t sX,
+                                                       double* __restrict__ panel) {
   __shared__ double M2s[BB][BB + 1];
-  const int g = blockIdx.x, t = threadIdx.x;
-  const int nch = (N - m0) / BB;
+  __shared__ double Ss[BB][BB + 1];
+  __shared__ double Wl[BB][64 + 1];                // W' of the workgroup's columns
+  __shared__ double W0[BB][BB + 1];                // W' of columns 0 .. 15
+  const int bx = blockIdx.x, g = blockIdx.y, t = threadIdx.x;
+  const int m = N - m0, nch = m / BB;
   {
     const double* pp = part + (int64_t)g * NJ * 256 + t;
     double s = 0.0;
@@ -539,41 +556,57 @@ __global__ __launch_bounds__(256) void panel_s_kernel(int N, int m0, const doubl
     M2s[t >> 4][t & 15] = s;
   }
   __syncthreads();
-  const int a = t >> 4, b = t & 15;
-  const double* Tg = tmat + (int64_t)g * kWyBlock * kWyBlock;
-  double s = 0.0;
+  {
+    const int a = t >> 4, b = t & 15;
+    const double* Tg = tmat + (int64_t)g * kWyBlock * kWyBlock;
+    double s = 0.0;
 #pragma unroll
-  for (int q = 0; q < BB; ++q) s = fma(Tg[q * kWyBlock + a], M2s[q][b], s);
-  sbuf[(int64_t)g * sS + t] = s;
-}
-
-// W' = X' - 1/2 S'V' in place of X' in rows BB .. 2BB-1 of the panel
-// buffer; one workgroup per 64 columns and matrix.
-__global__ __launch_bounds__(256) void panel_w_kernel(int N, int m0, const double* __restrict__ sbuf,
-                                                       int64_t sS, double* __restrict__ panel) {
-  __shared__ double Ss[BB][BB + 1];
-  const int jb = blockIdx.x, g = blockIdx.y, t = threadIdx.x;
-  const int m = N - m0;
-  Ss[t >> 4][t & 15] = sbuf[(int64_t)g * sS + t];
+    for (int q = 0; q < BB; ++q) s = fma(Tg[q * kWyBlock + a], M2s[q][b], s);
+    Ss[a][b] = s;
+  }
   __syncthreads();
   double* Pg = panel + (int64_t)g * 3 * BB * N + m0;
-  for (int e = t; e < BB * 64; e += 256) {
-    const int ii = e >> 6, j = 64 * jb + (e & 63);
-    if (j < m) {
-      double s = 0.0;
+  const double* Xg = xq + (int64_t)g * sX + m0;
+  const auto w_of = [&](int ii, int j) {
+    double s = 0.0;
 #pragma unroll
-      for (int q = 0; q < BB; ++q) s = fma(Ss[q][ii], Pg[(int64_t)q * N + j], s);
-      double* xw = Pg + (int64_t)(BB + ii) * N + j;
-      *xw = fma(-0.5, s, *xw);
+    for (int q = 0; q < BB; ++q) s = fma(Ss[q][ii], Pg[(int64_t)q * N + j], s);
+    return fma(-0.5, s, Xg[(int64_t)ii * N + j]);
+  };
+  for (int e = t; e < BB * 64; e += 256) {
+    const int ii = e >> 6, jl = e & 63, j = 64 * bx + jl;
+    double wv = 0.0;
+    if (j < m) {
+      wv = w_of(ii, j);
+      Pg[(int64_t)(BB + ii) * N + j] = wv;
     }
+    Wl[ii][jl] = wv;
   }
+  W0[t >> 4][t & 15] = w_of(t >> 4, t & 15);
+  __syncthreads();
+  const int w = t >> 6, lane = t & 63, li = lane & 15, lk = lane >> 4;
+  const int i0 = 64 * bx + 16 * w;                 // m is a multiple of 16
+  if (i0 >= m) return;
+  double* Cg = A + (int64_t)g * N * N + (int64_t)m0 * N + m0;
+  xdbl4 acc;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) acc[r] = Cg[(int64_t)(i0 + 4 * r + lk) * N + li];
+#pragma unroll
+  for (int s8 = 0; s8 < 8; ++s8) {
+    const int k = 4 * s8 + lk;
+    const double av = (k < BB) ? -Pg[(int64_t)k * N + i0 + li] : -Wl[k - BB][16 * w + li];
+    const double bv = (k < BB) ? W0[k][li] : Pg[(int64_t)(k - BB) * N + li];
+    acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc, 0, 0, 0);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) Cg[(int64_t)(i0 + 4 * r + lk) * N + li] = acc[r];
 }
 
 // Rank-K update C <- C - P1' P2 of an m x m block (C[i][j] = C[i*ldc + j],
 // P1[k][i] = P1[k*ld1 + i], P2[k][j] = P2[k*ld2 + j], K = 32 KC; matrix g at
 // C + g sC, P1 + g s1, P2 + g s2), for the two-sided update
 // of the trailing matrix (P1 = [V; W], P2 = [W; V], K = 2 BB) and the
-// accumulation of Q (P1 = V, P2 = T V Q, K = 64). One workgroup per 64 x 64
+// accumulation of Q (P1 = V, P2 = T V Q, K = 64 or 128). One workgroup per 64 x 64
 // tile; wave w updates the 32 x 32 piece at (32 (w&1), 32 (w>>1)) as 2 x 2
 // MFMA blocks: the piece of C is loaded straight into the accumulators
 // (register r of a block holds row 4r + l/16, column l%16: 128-byte row
@@ -582,7 +615,10 @@ __global__ __launch_bounds__(256) void panel_w_kernel(int N, int m0, const doubl
 // multiple of 16, so each 16 x 16 block is wholly inside or outside C:
 // outside blocks load from clamped addresses and are not stored. With LOWER
 // only the tiles on and below the diagonal are updated (C symmetric, its
-// lower triangle kept; see the note before panel_x_kernel).
+// lower triangle kept; see the note before panel_x_kernel). With PART == 2
+// the blocks of the first block row and column are left alone (the first
+// block column is updated beforehand, the first block row lies above the
+// diagonal).
 template <int KC, bool LOWER, int PART>
 __device__ __forceinline__ void rank_update_tile(double* __restrict__ C, int64_t ldc, int64_t sC,
                                                  int m, const double* __restrict__ P1, int64_t ld1,
@@ -590,7 +626,6 @@ __device__ __forceinline__ void rank_update_tile(double* __restrict__ C, int64_t
                                                  int64_t ld2, int64_t s2, int bx, int by, int g,
                                                  int w, int lane) {
   const int i0 = 64 * bx + 32 * (w & 1), j0 = 64 * by + 32 * (w >> 1);
-  if (PART == 1 && j0 > 0) return;                 // waves wholly right of the strip
   double* Cg = C + (int64_t)g * sC;
   const double* A1 = P1 + (int64_t)g * s1;
   const double* A2 = P2 + (int64_t)g * s2;
@@ -635,7 +670,6 @@ __device__ __forceinline__ void rank_update_tile(double* __restrict__ C, int64_t
 #pragma unroll
     for (int bj = 0; bj < 2; ++bj) {
       bool st = vi[bi] && vj[bj];
-      if (PART == 1) st = st && jb[bj] == 0;
       if (PART == 2) st = st && ib[bi] != 0 && jb[bj] != 0;
       if (st) {
 #pragma unroll
@@ -1160,41 +1194,34 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
   for (int p = 0; p + BB < N; p += BB) {
     const int m0 = p + BB, mrow = N - m0;
     double* const pb = pbuf[(p / BB) & 1];
-    // X' = Y' A22 and the block products of M2 = V'X, then
-    // W' = X' - 1/2 (T'M2)' V' in place of X'
-    {
-      const int NJ = (int)ceil_div(N, BB);
-      hipLaunchKernelGGL(panel_x_kernel, dim3((unsigned)ceil_div(mrow / BB, 4), (unsigned)G),
-                         dim3(256), 0, s, wk.A, N, m0, wk.xbuf, pb, wk.part, NJ);
-      KMP_LAUNCH_CHECK();
-      const int64_t sS = (int64_t)kWyBlock * N;
-      hipLaunchKernelGGL(panel_s_kernel, dim3((unsigned)G), dim3(256), 0, s, N, m0, wk.part, NJ,
-                         wk.tmat, wk.ybuf, sS);
-      KMP_LAUNCH_CHECK();
-      hipLaunchKernelGGL(panel_w_kernel, dim3((unsigned)ceil_div(mrow, 64), (unsigned)G), dim3(256),
-                         0, s, N, m0, wk.ybuf, sS, pb);
-      KMP_LAUNCH_CHECK();
-    }
+    // X' = Y' A22 (into ybuf) and the block products of M2 = V'X
+    const int NJ = (int)ceil_div(N, BB);
+    const int64_t sXq = (int64_t)2 * kWyBlock * N;
+    hipLaunchKernelGGL(panel_x_kernel, dim3((unsigned)ceil_div(mrow / BB, 4), (unsigned)G),
+                       dim3(256), 0, s, wk.A, N, m0, wk.xbuf, (const double*)pb, wk.part, NJ,
+                       wk.ybuf, sXq);
+    KMP_LAUNCH_CHECK();
     kc_end(KMP_KC_PANEL_WY, s, over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 8.0 * m * m; }),
            over_groups(wk, [&](double n) {
              const double m = std::max(0.0, n - m0); return 2.0 * BB * m * m; }));
-    // A22 -= V W' + W V' (K = 2 BB over the [V; W; V] rows). With a next
-    // panel: its 16 columns first, then its factorisation beside the rest.
+    // A22 -= V W' + W V' (K = 2 BB over the [V; W; V] rows), W' = X' -
+    // 1/2 (T'M2)' V': W' and the first block column in one launch; then,
+    // with a next panel, its factorisation beside the rest of the update.
     const bool next = m0 + BB < N;
     kc_begin(KMP_KC_TRAIL, s);
     const double* P1 = pb + m0;
     const double* P2 = pb + (int64_t)BB * N + m0;
     const unsigned tl = (unsigned)tiles_of(mrow);
+    hipLaunchKernelGGL(panel_ws_kernel, dim3(tl, (unsigned)G), dim3(256), 0, s, wk.A, N, m0,
+                       (const double*)wk.part, NJ, (const double*)wk.tmat,
+                       (const double*)wk.ybuf, sXq, pb);
+    KMP_LAUNCH_CHECK();
     if (next) {
-      hipLaunchKernelGGL((rank_update_kernel<1, true, 1>), dim3(tl, 1u, (unsigned)G), dim3(256), 0,
-                         s, wk.A + (int64_t)m0 * N + m0, (int64_t)N, (int64_t)N * N, mrow, P1,
-                         (int64_t)N, sP, P2, (int64_t)N, sP);
-      KMP_LAUNCH_CHECK();
       if ((rc = factor_panel(m0, pbuf[((p / BB) & 1) ^ 1], true, pb)) != 0) return rc;
     } else {
-      hipLaunchKernelGGL((rank_update_kernel<1, true>), dim3(tl, tl, (unsigned)G), dim3(256), 0, s,
-                         wk.A + (int64_t)m0 * N + m0, (int64_t)N, (int64_t)N * N, mrow, P1,
+      hipLaunchKernelGGL((rank_update_kernel<1, true, 2>), dim3(tl, tl, (unsigned)G), dim3(256), 0,
+                         s, wk.A + (int64_t)m0 * N + m0, (int64_t)N, (int64_t)N * N, mrow, P1,
                          (int64_t)N, sP, P2, (int64_t)N, sP);
       KMP_LAUNCH_CHECK();
     }
