@@ -548,6 +548,34 @@ __global__ __launch_bounds__(256) void panel_ws_kernel(double* __restrict__ A, i
   __shared__ double W0[BB][BB + 1];                // W' of columns 0 .. 15
   const int bx = blockIdx.x, g = blockIdx.y, t = threadIdx.x;
   const int m = N - m0, nch = m / BB;
+  double* Pg = panel + (int64_t)g * 3 * BB * N + m0;
+  const double* Xg = xq + (int64_t)g * sX + m0;
+  const int w = t >> 6, lane = t & 63, li = lane & 15, lk = lane >> 4;
+  const int i0 = 64 * bx + 16 * w;                 // m is a multiple of 16
+  const bool strip = i0 < m;
+  double* Cg = A + (int64_t)g * N * N + (int64_t)m0 * N + m0;
+  // every load that does not depend on S first: the strip's piece of A22,
+  // the V column and X' rows of this thread's W' entries (column jl, rows
+  // r4 .. r4+3; and column c0, row r0 of W' for columns 0 .. 15), and
+  // column a of T
+  xdbl4 acc = {0.0, 0.0, 0.0, 0.0};
+  if (strip) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] = Cg[(int64_t)(i0 + 4 * r + lk) * N + li];
+  }
+  const int jl = t & 63, j = 64 * bx + jl, r4 = 4 * (t >> 6);
+  const bool okj = j < m;
+  const int c0 = t & 15, r0 = t >> 4;
+  double vj[BB], xj[4], v0[BB], tc[BB];
+#pragma unroll
+  for (int q = 0; q < BB; ++q) {
+    vj[q] = okj ? Pg[(int64_t)q * N + j] : 0.0;
+    v0[q] = Pg[(int64_t)q * N + c0];
+    tc[q] = tmat[(int64_t)g * kWyBlock * kWyBlock + q * kWyBlock + r0];
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) xj[u] = okj ? Xg[(int64_t)(r4 + u) * N + j] : 0.0;
+  const double x0 = Xg[(int64_t)r0 * N + c0];
   {
     const double* pp = part + (int64_t)g * NJ * 256 + t;
     double s = 0.0;
@@ -557,40 +585,30 @@ __global__ __launch_bounds__(256) void panel_ws_kernel(double* __restrict__ A, i
   }
   __syncthreads();
   {
-    const int a = t >> 4, b = t & 15;
-    const double* Tg = tmat + (int64_t)g * kWyBlock * kWyBlock;
-    double s = 0.0;
+    double s = 0.0;                                // S[a][b], a = t/16, b = t%16
 #pragma unroll
-    for (int q = 0; q < BB; ++q) s = fma(Tg[q * kWyBlock + a], M2s[q][b], s);
-    Ss[a][b] = s;
+    for (int q = 0; q < BB; ++q) s = fma(tc[q], M2s[q][c0], s);
+    Ss[r0][c0] = s;
   }
   __syncthreads();
-  double* Pg = panel + (int64_t)g * 3 * BB * N + m0;
-  const double* Xg = xq + (int64_t)g * sX + m0;
-  const auto w_of = [&](int ii, int j) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int ii = r4 + u;
     double s = 0.0;
 #pragma unroll
-    for (int q = 0; q < BB; ++q) s = fma(Ss[q][ii], Pg[(int64_t)q * N + j], s);
-    return fma(-0.5, s, Xg[(int64_t)ii * N + j]);
-  };
-  for (int e = t; e < BB * 64; e += 256) {
-    const int ii = e >> 6, jl = e & 63, j = 64 * bx + jl;
-    double wv = 0.0;
-    if (j < m) {
-      wv = w_of(ii, j);
-      Pg[(int64_t)(BB + ii) * N + j] = wv;
-    }
-    Wl[ii][jl] = wv;
+    for (int q = 0; q < BB; ++q) s = fma(Ss[q][ii], vj[q], s);
+    const double wv = fma(-0.5, s, xj[u]);
+    if (okj) Pg[(int64_t)(BB + ii) * N + j] = wv;
+    Wl[ii][jl] = okj ? wv : 0.0;
   }
-  W0[t >> 4][t & 15] = w_of(t >> 4, t & 15);
-  __syncthreads();
-  const int w = t >> 6, lane = t & 63, li = lane & 15, lk = lane >> 4;
-  const int i0 = 64 * bx + 16 * w;                 // m is a multiple of 16
-  if (i0 >= m) return;
-  double* Cg = A + (int64_t)g * N * N + (int64_t)m0 * N + m0;
-  xdbl4 acc;
+  {
+    double s = 0.0;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) acc[r] = Cg[(int64_t)(i0 + 4 * r + lk) * N + li];
+    for (int q = 0; q < BB; ++q) s = fma(Ss[q][r0], v0[q], s);
+    W0[r0][c0] = fma(-0.5, s, x0);
+  }
+  __syncthreads();
+  if (!strip) return;
 #pragma unroll
   for (int s8 = 0; s8 < 8; ++s8) {
     const int k = 4 * s8 + lk;
