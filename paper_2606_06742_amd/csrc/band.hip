@@ -419,7 +419,7 @@ __global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restric
 // X' = Y' A22 and the partial products of M2 = V'X for one panel (A22 =
 // A[m0:, m0:], Y' = T'V' stored transposed, Yt[k][i] = Yt[16 k + i], m x 16).
 // One workgroup per 64 columns (four 16-column blocks) of X' and matrix:
-// wave w accumulates the 16-row chunks q = w, w+4, ... of all four blocks
+// wave w accumulates the 16-row chunks q = w, w+XW, ... of all four blocks
 // on the matrix cores (A operand Yt[k][i]; B operand A22[k][j], so that
 // below the diagonal each chunk is read as 512-byte row pieces, with its Y'
 // operand loaded once for the four blocks). A chunk may lie below some
@@ -427,11 +427,12 @@ __global__ __launch_bounds__(64 * NW) void panel_qr_vec_kernel(double* __restric
 // wavefront); above, a block's entries A22[j][k] are read from its
 // transposed rows, 32 contiguous bytes per lane, with the k of MFMA step s4
 // in lane group kq taken as 16 q + 4 kq + s4 (16 q + 4 s4 + kq below). The
-// four partial tiles of each block are added in LDS, X' goes to xq (row b
+// XW partial tiles of each block are added in LDS, X' goes to xq (row b
 // of matrix g at xq + g sX + b N), and the workgroup's parts of M2,
 // sum_{j in block} V'[a][j] X'[b][j], to part[(g NJ + block)*256].
 constexpr int XU4 = 1;            // chunks per wavefront and iteration
-__global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__ A, int N, int m0,
+constexpr int XW = 8;             // wavefronts per workgroup
+__global__ __launch_bounds__(64 * XW) void panel_x_kernel(const double* __restrict__ A, int N, int m0,
                                                        const double* __restrict__ ybuf,
                                                        const double* __restrict__ panel,
                                                        double* __restrict__ part, int NJ,
@@ -453,10 +454,10 @@ __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__
   xdbl4 acc[4];
 #pragma unroll
   for (int c = 0; c < 4; ++c) acc[c] = xdbl4{0.0, 0.0, 0.0, 0.0};
-  for (int q = w; q < nch; q += 4 * XU4) {
+  for (int q = w; q < nch; q += XW * XU4) {
 #pragma unroll
     for (int u = 0; u < XU4; ++u) {
-      const int qq = q + 4 * u;
+      const int qq = q + XW * u;
       if (qq < nch) {                                // uniform over the wavefront
         double avb[4], ava[4], bv[4][4];
         const bool anyb = qq >= jb0, anya = qq < jb0 + nbv - 1;
@@ -492,16 +493,27 @@ __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__
       }
     }
   }
+  // wavefront w + 4 hands its tiles to wavefront w, which adds its own
+  static_assert(XW == 8, "two wavefronts per LDS slot");
+  if (w >= 4) {
 #pragma unroll
-  for (int c = 0; c < 4; ++c)
+    for (int c = 0; c < 4; ++c)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) red[w][c][r][lane] = acc[c][r];
+      for (int r = 0; r < 4; ++r) red[w - 4][c][r][lane] = acc[c][r];
+  }
+  __syncthreads();
+  if (w < 4) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[w][c][r][lane] = acc[c][r] + red[w][c][r][lane];
+  }
   __syncthreads();
   // X' of block c, register r, lane l: row 4 r + l / 16, column l % 16
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
     const int c = h, r = t >> 6, l = t & 63;
-    if (c < nbv) {
+    if (t < 256 && c < nbv) {
       const double v = (red[0][c][r][l] + red[1][c][r][l]) + (red[2][c][r][l] + red[3][c][r][l]);
       const int b = 4 * r + (l >> 4), j = l & 15;
       Xs[c][b][j] = v;
@@ -509,7 +521,7 @@ __global__ __launch_bounds__(256) void panel_x_kernel(const double* __restrict__
     }
   }
   __syncthreads();
-  {
+  if (t < 256) {
     const int a = t >> 4, b = t & 15;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -1216,7 +1228,7 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     const int NJ = (int)ceil_div(N, BB);
     const int64_t sXq = (int64_t)2 * kWyBlock * N;
     hipLaunchKernelGGL(panel_x_kernel, dim3((unsigned)ceil_div(mrow / BB, 4), (unsigned)G),
-                       dim3(256), 0, s, wk.A, N, m0, wk.xbuf, (const double*)pb, wk.part, NJ,
+                       dim3(64 * XW), 0, s, wk.A, N, m0, wk.xbuf, (const double*)pb, wk.part, NJ,
                        wk.ybuf, sXq);
     KMP_LAUNCH_CHECK();
     kc_end(KMP_KC_PANEL_WY, s, over_groups(wk, [&](double n) {
