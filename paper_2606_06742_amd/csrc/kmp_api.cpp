@@ -550,6 +550,17 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   } clock_guard((uint32_t)spec->timing_mask);
   g_clock_obj.every = spec->timing_every > 0 ? spec->timing_every : 1;
   int64_t total_iters = 0;
+  // pinned host buffer for the per-group and total active counts
+  struct PollBuf {
+    int* p = nullptr;
+    hipEvent_t ev = nullptr;
+    ~PollBuf() {
+      if (p) (void)hipHostFree(p);
+      if (ev) (void)hipEventDestroy(ev);
+    }
+  } poll;
+  KMP_HIP_TRY(hipHostMalloc((void**)&poll.p, sizeof(int) * ((size_t)plan.G + 1), hipHostMallocDefault));
+  KMP_HIP_TRY(hipEventCreateWithFlags(&poll.ev, hipEventDisableTiming));
   KMP_HIP_TRY(hipEventRecord(tm.ev[0], s));
   if ((rc = row_norms(s, X, n, d, ldx, lay.nrm)) != 0) return rc;
 
@@ -634,23 +645,47 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
       KMP_HIP_TRY(hipEventRecord(tm.ev[4], s));
       if ((rc = path_stage_precompute(s, pa, kappa)) != 0) return rc;
       if ((rc = path_compact(s, pa)) != 0) return rc;
-      KMP_HIP_TRY(hipMemcpyAsync(nact_h.data(), lay.nact, sizeof(int) * Gb, hipMemcpyDeviceToHost, s));
       KMP_HIP_TRY(hipEventRecord(tm.ev[5], s));
-      KMP_HIP_TRY(hipStreamSynchronize(s));
+      // The counts of active columns (per group and in total) come back to
+      // pinned memory while the iterations go on: after a poll the next
+      // iteration is queued before the host waits for the counts, so the
+      // device never idles on the round trip (once every column has
+      // converged, that iteration finds nothing to do and the stage ends).
+      const auto post_poll = [&]() -> int {
+        KMP_HIP_TRY(hipMemcpyAsync(poll.p, lay.nact, sizeof(int) * Gb, hipMemcpyDeviceToHost, s));
+        KMP_HIP_TRY(hipMemcpyAsync(poll.p + Gb, lay.active, sizeof(int), hipMemcpyDeviceToHost, s));
+        KMP_HIP_TRY(hipEventRecord(poll.ev, s));
+        return 0;
+      };
+      const auto read_poll = [&](int* active) -> int {
+        KMP_HIP_TRY(hipEventSynchronize(poll.ev));
+        std::copy(poll.p, poll.p + Gb, nact_h.begin());
+        *active = poll.p[Gb];
+        return 0;
+      };
+      if ((rc = post_poll()) != 0) return rc;
+      bool pending = true;
       int it = 0;
       while (it < spec->max_iter) {
         if ((rc = path_iteration(s, pa, delta, kappa, spec->tol, spec->max_iter,
                                  (spec->flags & KMP_FLAG_RESTART) ? 1 : 0)) != 0)
           return rc;
         ++it;
-        if (it % spec->poll_every == 0 || it >= spec->max_iter) {
-          if ((rc = path_compact(s, pa)) != 0) return rc;
+        if (pending) {
           int active = 0;
-          KMP_HIP_TRY(hipMemcpyAsync(&active, lay.active, sizeof(int), hipMemcpyDeviceToHost, s));
-          KMP_HIP_TRY(hipMemcpyAsync(nact_h.data(), lay.nact, sizeof(int) * Gb, hipMemcpyDeviceToHost, s));
-          KMP_HIP_TRY(hipStreamSynchronize(s));
+          if ((rc = read_poll(&active)) != 0) return rc;
+          pending = false;
           if (active == 0) break;
         }
+        if (it % spec->poll_every == 0 || it >= spec->max_iter) {
+          if ((rc = path_compact(s, pa)) != 0) return rc;
+          if ((rc = post_poll()) != 0) return rc;
+          pending = true;
+        }
+      }
+      if (pending) {
+        int active = 0;
+        if ((rc = read_poll(&active)) != 0) return rc;
       }
       total_iters += it;
       KMP_HIP_TRY(hipEventRecord(tm.ev[6], s));
