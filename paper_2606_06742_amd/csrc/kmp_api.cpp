@@ -225,21 +225,38 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
   return 0;
 }
 
+// Phase times from HIP events: mark() records an event on the stream (a
+// pool that grows as needed), span() notes a pair whose elapsed time is
+// added to a total when sum() runs after the final synchronisation, so the
+// host never waits on the device to read a phase time.
 struct EventTimer {
-  hipEvent_t ev[8];
-  bool ok = false;
-  EventTimer() {
-    ok = true;
-    for (auto& e : ev)
-      if (hipEventCreate(&e) != hipSuccess) ok = false;
-  }
+  std::vector<hipEvent_t> ev;
+  size_t used = 0;
+  struct Span {
+    double* acc;
+    size_t a, b;
+  };
+  std::vector<Span> spans;
   ~EventTimer() {
-    for (auto& e : ev) hipEventDestroy(e);
+    for (auto& e : ev) (void)hipEventDestroy(e);
   }
-  float ms(int a, int b) {
-    float t = 0.f;
-    if (hipEventElapsedTime(&t, ev[a], ev[b]) != hipSuccess) return 0.f;
-    return t;
+  int mark(hipStream_t s, size_t* idx) {
+    if (used == ev.size()) {
+      hipEvent_t e;
+      KMP_HIP_TRY(hipEventCreate(&e));
+      ev.push_back(e);
+    }
+    *idx = used;
+    KMP_HIP_TRY(hipEventRecord(ev[used++], s));
+    return 0;
+  }
+  void span(double* acc, size_t a, size_t b) { spans.push_back({acc, a, b}); }
+  void sum() {
+    for (const auto& sp : spans) {
+      float t = 0.f;
+      if (hipEventElapsedTime(&t, ev[sp.a], ev[sp.b]) == hipSuccess) *sp.acc += t;
+    }
+    spans.clear();
   }
 };
 
@@ -561,7 +578,8 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   } poll;
   KMP_HIP_TRY(hipHostMalloc((void**)&poll.p, sizeof(int) * ((size_t)plan.G + 1), hipHostMallocDefault));
   KMP_HIP_TRY(hipEventCreateWithFlags(&poll.ev, hipEventDisableTiming));
-  KMP_HIP_TRY(hipEventRecord(tm.ev[0], s));
+  size_t ev_start = 0, e1 = 0, e2 = 0, e3 = 0;
+  if ((rc = tm.mark(s, &ev_start)) != 0) return rc;
   if ((rc = row_norms(s, X, n, d, ldx, lay.nrm)) != 0) return rc;
 
   PathArrays pa;
@@ -607,7 +625,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     pa.nact_host = nact_h.data();
 
     // a1: Gram + fold gather into A (group g = s_local*V + v)
-    KMP_HIP_TRY(hipEventRecord(tm.ev[1], s));
+    if ((rc = tm.mark(s, &e1)) != 0) return rc;
     kc_begin(KMP_KC_GRAM, s);
     if ((rc = rbf_blocks(s, X, d, ldx, lay.nrm, lay.tidx, N, N, lay.tidx, N, N, V, lay.inv2s2, sb,
                          lay.A, (int64_t)V * N * N, (int64_t)N * N, N)) != 0)
@@ -619,7 +637,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
       for (int v = 0; v < V; ++v) e2 += (double)plan.nv[v] * plan.nv[v];
       kc_end(KMP_KC_GRAM, s, 8.0 * sb * e2, 2.0 * d * e2);
     }
-    KMP_HIP_TRY(hipEventRecord(tm.ev[2], s));
+    if ((rc = tm.mark(s, &e2)) != 0) return rc;
     // a2: factorisation
     BandWork bw;
     bw.G = Gb; bw.N = N; bw.A = lay.A; bw.Q = lay.Qm; bw.band = lay.band; bw.tau = lay.tau;
@@ -633,19 +651,19 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     if ((rc = group_ones_projection(s, lay.Qm, lay.nvg, Gb, N, lay.cvec)) != 0) return rc;
     if ((rc = gather_labels(s, y, lay.tidx, V, sb, N, lay.ylab)) != 0) return rc;
     if ((rc = path_init_columns(s, pa)) != 0) return rc;
-    KMP_HIP_TRY(hipEventRecord(tm.ev[3], s));
-    KMP_HIP_TRY(hipEventSynchronize(tm.ev[3]));
-    t_gram += tm.ms(1, 2);
-    t_factor += tm.ms(2, 3);
+    if ((rc = tm.mark(s, &e3)) != 0) return rc;
+    tm.span(&t_gram, e1, e2);
+    tm.span(&t_factor, e2, e3);
 
     // a3-a9: smoothing stages
     for (int st = 0; st < nst; ++st) {
       const double delta = spec->loss == KMP_LOGISTIC ? 1.0 : spec->delta0 * std::pow(spec->eta, (double)st);
       const double kappa = spec->loss == KMP_LOGISTIC ? 4.0 : 2.0 * delta;
-      KMP_HIP_TRY(hipEventRecord(tm.ev[4], s));
+      size_t e4 = 0, e5 = 0, e6 = 0;
+      if ((rc = tm.mark(s, &e4)) != 0) return rc;
       if ((rc = path_stage_precompute(s, pa, kappa)) != 0) return rc;
       if ((rc = path_compact(s, pa)) != 0) return rc;
-      KMP_HIP_TRY(hipEventRecord(tm.ev[5], s));
+      if ((rc = tm.mark(s, &e5)) != 0) return rc;
       // The counts of active columns (per group and in total) come back to
       // pinned memory while the iterations go on: after a poll the next
       // iteration is queued before the host waits for the counts, so the
@@ -688,10 +706,9 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
         if ((rc = read_poll(&active)) != 0) return rc;
       }
       total_iters += it;
-      KMP_HIP_TRY(hipEventRecord(tm.ev[6], s));
-      KMP_HIP_TRY(hipEventSynchronize(tm.ev[6]));
-      t_pre += tm.ms(4, 5);
-      t_path += tm.ms(5, 6);
+      if ((rc = tm.mark(s, &e6)) != 0) return rc;
+      tm.span(&t_pre, e4, e5);
+      tm.span(&t_path, e5, e6);
     }
 
     // a10: finalize
@@ -702,15 +719,18 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     fa.hidx = lay.hidx; fa.Mh = plan.Mh; fa.kh = lay.A; fa.ftrain = lay.fpart;
     fa.alpha = alpha; fa.beta_out = beta; fa.objective = objective; fa.cv_sum = cv_sum;
     fa.cv_err = cv_err; fa.iters = iters; fa.status = status;
-    KMP_HIP_TRY(hipEventRecord(tm.ev[6], s));
+    size_t f0 = 0, f1 = 0;
+    if ((rc = tm.mark(s, &f0)) != 0) return rc;
     if ((rc = path_finalize(s, pa, fa)) != 0) return rc;
-    KMP_HIP_TRY(hipEventRecord(tm.ev[7], s));
-    KMP_HIP_TRY(hipEventSynchronize(tm.ev[7]));
-    t_fin += tm.ms(6, 7);
+    if ((rc = tm.mark(s, &f1)) != 0) return rc;
+    tm.span(&t_fin, f0, f1);
   }
-  KMP_HIP_TRY(hipEventRecord(tm.ev[7], s));
+  size_t ev_end = 0;
+  if ((rc = tm.mark(s, &ev_end)) != 0) return rc;
   KMP_HIP_TRY(hipStreamSynchronize(s));
-  const double t_total = tm.ms(0, 7);
+  double t_total = 0.0;
+  tm.span(&t_total, ev_start, ev_end);
+  tm.sum();
 
   // host-side selection and status summary
   std::vector<double> hcv(ncell);
