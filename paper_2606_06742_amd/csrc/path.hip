@@ -1199,23 +1199,54 @@ __global__ __launch_bounds__(256) void cv_reduce_kernel(
   }
 }
 
+// C = sum over S split-K parts (part s at part + s sP; column-major, ld
+// ldc, matrix b at + b sC), added in part order.
+__global__ __launch_bounds__(256) void sum_parts_kernel(int M, int Nc, int S,
+                                                        const double* __restrict__ part, int64_t sP,
+                                                        int64_t ldc, int64_t sC,
+                                                        double* __restrict__ C) {
+  const int b = blockIdx.z, j = blockIdx.y;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= M || j >= Nc) return;
+  const int64_t o = (int64_t)b * sC + (int64_t)j * ldc + i;
+  double v = part[o];
+  for (int q = 1; q < S; ++q) v += part[(int64_t)q * sP + o];
+  C[o] = v;
+}
+
+// C = A B (A k-contiguous, B k-contiguous columns, C column-major with the
+// parts' layout) by split-K parts in scratch, then their ordered sum.
+static int gemm_split(hipStream_t s, const GemmArgs& g, double* scratch, int64_t sP) {
+  int rc;
+  const int S = splitk_parts(g);
+  if ((rc = gemm_partial(s, g, true, S, scratch, sP, nullptr, nullptr)) != 0) return rc;
+  hipLaunchKernelGGL(sum_parts_kernel, dim3((unsigned)ceil_div(g.M, 256), (unsigned)g.N,
+                                            (unsigned)g.batch),
+                     dim3(256), 0, s, g.M, g.N, S, (const double*)scratch, sP, g.ldc, g.sC, g.C);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
 int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
   int rc;
   kc_begin(KMP_KC_FINALIZE, s);
   const int64_t sNC = (int64_t)p.N * p.C;
+  const int64_t sP = (int64_t)p.G * sNC;    // between split-K parts in fpart / zpart
   // alpha_loc = Q ahat (into zmat)
   GemmArgs g;
   g.M = p.N; g.N = p.C; g.K = p.N; g.batch = p.G;
   g.A = p.Q; g.lda = p.N; g.sA = (int64_t)p.N * p.N;
   g.B = p.ahat; g.ldb = p.N; g.sB = sNC;
   g.C = p.zmat; g.ldc = p.N; g.sC = sNC;
-  if ((rc = gemm(s, g, true, true, false)) != 0) return rc;
+  // (the parts of this product go to fpart, those of the next to zpart:
+  // the training predictions are stored in fpart)
+  if ((rc = gemm_split(s, g, p.fpart, sP)) != 0) return rc;
   // training predictions K_v alpha = Q (B ahat)
   if ((rc = band_apply(s, p, p.ahat, p.bmat)) != 0) return rc;
   GemmArgs gt = g;
   gt.B = p.bmat;
   gt.C = fa.ftrain;
-  if ((rc = gemm(s, gt, true, true, false)) != 0) return rc;
+  if ((rc = gemm_split(s, gt, p.zpart, sP)) != 0) return rc;
   // held-out kernel blocks K[H_v, T_v] (into the factor buffer, no longer
   // needed), then held-out predictions K[H_v, T_v] alpha
   if ((rc = rbf_blocks(s, fa.X, fa.d, fa.ldx, fa.nrm, fa.hidx, fa.Mh, fa.Mh, fa.tidx, p.N, p.N,
