@@ -54,7 +54,10 @@ def _check(A, Q, band, c=40.0):
         assert np.abs(ev_b - ev_a).max() <= c * N * EPS * np.abs(ev_a).max()
 
 
-@pytest.mark.parametrize("N,G", [(64, 1), (128, 3), (256, 2)])
+# orders 64 .. 320 take every arrangement of the accumulation of Q: the
+# partial last block alone (64, 128), then pairs of 64-blocks with (256) or
+# without (192, 320) a single block left at the bottom
+@pytest.mark.parametrize("N,G", [(64, 1), (128, 3), (192, 2), (256, 2), (320, 1)])
 def test_band_random_symmetric(N, G):
     rng = np.random.default_rng(N + G)
     B = rng.standard_normal((G, N, N))
