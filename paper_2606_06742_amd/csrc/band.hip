@@ -1275,6 +1275,7 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     hipLaunchKernelGGL(band_extract_kernel, dim3((unsigned)ceil_div(tot, 256)), dim3(256), 0, s,
                        wk.A, N, tot, wk.band);
     KMP_LAUNCH_CHECK();
+    if (wk.band_ready) KMP_HIP_TRY(hipEventRecord(wk.band_ready, s));
     const int64_t tz = (int64_t)G * (N - BB) * (2 * kWyBlock + BB);
     hipLaunchKernelGGL(clear_reflector_rows_kernel, dim3((unsigned)ceil_div(tz, 256)), dim3(256), 0,
                        s, wk.A, N, tz);

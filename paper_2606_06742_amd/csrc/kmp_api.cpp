@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <map>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -74,6 +75,25 @@ void kc_end(int cls, hipStream_t s, double bytes, double flops) {
 }
 
 namespace {
+
+// A second stream per device for work that can run beside the caller's
+// stream (joined back through events); created on first use and kept for
+// the life of the process, at the default priority.
+int side_stream(hipStream_t* out) {
+  int dev = 0;
+  KMP_HIP_TRY(hipGetDevice(&dev));
+  static std::mutex mu;
+  static std::map<int, hipStream_t> streams;
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = streams.find(dev);
+  if (it == streams.end()) {
+    hipStream_t st = nullptr;
+    KMP_HIP_TRY(hipStreamCreateWithFlags(&st, hipStreamNonBlocking));
+    it = streams.emplace(dev, st).first;
+  }
+  *out = it->second;
+  return 0;
+}
 
 constexpr int kPanel = 32;       // Householder panel width
 constexpr int kRowAlign = 64;    // padding of the per-fold matrix order
@@ -526,9 +546,14 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
 
   const int N = plan.N, C = plan.C, G = plan.G;
   const int nst = spec->loss == KMP_LOGISTIC ? 1 : spec->n_stages;
-  const double delta_final = spec->loss == KMP_LOGISTIC
-                                 ? 1.0
-                                 : spec->delta0 * std::pow(spec->eta, (double)(nst - 1));
+  // smoothing parameter and curvature bound of each stage
+  const auto stage_delta = [&](int st) {
+    return spec->loss == KMP_LOGISTIC ? 1.0 : spec->delta0 * std::pow(spec->eta, (double)st);
+  };
+  const auto stage_kappa = [&](int st) {
+    return spec->loss == KMP_LOGISTIC ? 4.0 : 2.0 * stage_delta(st);
+  };
+  const double delta_final = stage_delta(nst - 1);
 
   // host-side index lists and per-column parameters
   std::vector<int32_t> tidx((size_t)V * N, -1);
@@ -578,6 +603,22 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   } poll;
   KMP_HIP_TRY(hipHostMalloc((void**)&poll.p, sizeof(int) * ((size_t)plan.G + 1), hipHostMallocDefault));
   KMP_HIP_TRY(hipEventCreateWithFlags(&poll.ev, hipEventDisableTiming));
+  // The first stage's factors need the band only: they are formed on a side
+  // stream while the caller's stream accumulates Q, and the stage waits for
+  // them. Leaving the call (also on an error) waits for the side stream.
+  struct SideWork {
+    hipStream_t st = nullptr;
+    hipEvent_t band = nullptr, done = nullptr;
+    bool queued = false;
+    ~SideWork() {
+      if (queued) (void)hipStreamSynchronize(st);
+      if (band) (void)hipEventDestroy(band);
+      if (done) (void)hipEventDestroy(done);
+    }
+  } side;
+  if ((rc = side_stream(&side.st)) != 0) return rc;
+  KMP_HIP_TRY(hipEventCreateWithFlags(&side.band, hipEventDisableTiming));
+  KMP_HIP_TRY(hipEventCreateWithFlags(&side.done, hipEventDisableTiming));
   size_t ev_start = 0, e1 = 0, e2 = 0, e3 = 0;
   if ((rc = tm.mark(s, &ev_start)) != 0) return rc;
   if ((rc = row_norms(s, X, n, d, ldx, lay.nrm)) != 0) return rc;
@@ -647,7 +688,12 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     bw.ybuf = lay.ybuf; bw.part = lay.bpart; bw.nv_host = nvg.data();
     bw.gram_all = lay.gram_all; bw.tmat_all = lay.tmat_all; bw.cross_all = lay.cross_all;
     bw.xpart = lay.xpart;
+    bw.band_ready = side.band;
     if ((rc = band_reduce(s, bw)) != 0) return rc;
+    KMP_HIP_TRY(hipStreamWaitEvent(side.st, side.band, 0));
+    side.queued = true;
+    if ((rc = path_stage_factor(side.st, pa, stage_kappa(0))) != 0) return rc;
+    KMP_HIP_TRY(hipEventRecord(side.done, side.st));
     if ((rc = group_ones_projection(s, lay.Qm, lay.nvg, Gb, N, lay.cvec)) != 0) return rc;
     if ((rc = gather_labels(s, y, lay.tidx, V, sb, N, lay.ylab)) != 0) return rc;
     if ((rc = path_init_columns(s, pa)) != 0) return rc;
@@ -657,11 +703,15 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
 
     // a3-a9: smoothing stages
     for (int st = 0; st < nst; ++st) {
-      const double delta = spec->loss == KMP_LOGISTIC ? 1.0 : spec->delta0 * std::pow(spec->eta, (double)st);
-      const double kappa = spec->loss == KMP_LOGISTIC ? 4.0 : 2.0 * delta;
+      const double delta = stage_delta(st);
+      const double kappa = stage_kappa(st);
       size_t e4 = 0, e5 = 0, e6 = 0;
       if ((rc = tm.mark(s, &e4)) != 0) return rc;
-      if ((rc = path_stage_precompute(s, pa, kappa)) != 0) return rc;
+      if (st == 0)
+        KMP_HIP_TRY(hipStreamWaitEvent(s, side.done, 0));
+      else if ((rc = path_stage_factor(s, pa, kappa)) != 0)
+        return rc;
+      if ((rc = path_stage_vectors(s, pa, kappa)) != 0) return rc;
       if ((rc = path_compact(s, pa)) != 0) return rc;
       if ((rc = tm.mark(s, &e5)) != 0) return rc;
       // The counts of active columns (per group and in total) come back to

@@ -96,6 +96,7 @@ struct BandWork {
   double* cross_all = nullptr; // same shape: V_b V_{b+1}' of consecutive blocks
   double* xpart = nullptr;     // kMaxSplitK x G x 128 x N: split-K parts of V Q in the Q accumulation
   const int* nv_host = nullptr;  // G valid orders (host), for the work counters; N if null
+  hipEvent_t band_ready = nullptr;  // if set, recorded once the band is written
 };
 // Doubles of scratch band_reduce needs beyond A, Q, band and tau (the chunk
 // partials included), and of the chunk partials alone.
@@ -132,6 +133,7 @@ struct TridiagWork {
   double* spart = nullptr;  // G x tridiag_parts(N) partial sums of w_raw'v
   double* pnext = nullptr;  // G x N next column, partially updated
   const int* nv_host = nullptr;  // G valid orders (host), for the work counters; N if null
+  hipEvent_t band_ready = nullptr;  // if set, recorded once the band is written
 };
 // Per-matrix length of the spart buffer (partial sums of the products).
 int tridiag_parts(int N);
@@ -188,7 +190,11 @@ struct PathArrays {
 };
 
 int path_init_columns(hipStream_t s, const PathArrays& p);
-int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa);
+// A stage's setup: the LDL' factors of M = 2 lambda I + B/(n_v kappa) (they
+// read the band, lambda and n_v only), then vhat, u and the momentum restart
+// (these need c and the factors).
+int path_stage_factor(hipStream_t s, const PathArrays& p, double kappa);
+int path_stage_vectors(hipStream_t s, const PathArrays& p, double kappa);
 int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kappa, double tol,
                    int max_iter, int restart);
 // Rebuilds cmap/nact from the column flags and writes the total number of

@@ -423,7 +423,7 @@ __device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
 // when they fit in 64 KiB, else each has its own. Orders above kLdsVecMax
 // (or every order, with KMP_FLAG_GLOBAL_SOLVE) keep the vector in device
 // memory and only a two-block ring in LDS.
-constexpr int PTILE = 3 * BND * (BND + 1) + 2 * BND;   // precompute LDS tiles per column
+constexpr int PTILE = 2 * BND * (BND + 1) + 5 * BND + (BND + 1) * BND;   // LDS of one column's LDL' sweep
 constexpr int RING = 2 * BND;                          // LDS ring of the device-memory solve
 constexpr int kLdsVecMax = 8192;
 static bool path_global_vec(const PathArrays& p) { return p.global_solve || p.N > kLdsVecMax; }
@@ -484,121 +484,158 @@ static int band_apply(hipStream_t s, const PathArrays& p, const double* x, doubl
 }
 
 // ------------------------------------------------------ per-stage factors
-// One wavefront per column: the blockwise LDL' of M = 2 lambda I + B/(n_v
-// kappa) (stored as above), vhat = M^{-1} c/(n_v kappa), u = B vhat,
-// g = 1/(2 lambda c'vhat); restart the momentum (r = 1, abar = ahat,
-// B abar) and reactivate the columns that stopped in the previous stage.
-template <bool GV>
-__global__ __launch_bounds__(256) void precompute_kernel(
+// 1/x from the hardware estimate and two Newton-Raphson steps
+// r <- r + r (1 - x r), which square the relative error each; for the
+// positive, normal pivots of the LDL' sweep.
+__device__ __forceinline__ double rcp_newton(double x) {
+  double r = __builtin_amdgcn_rcp(x);
+  double e = fma(-x, r, 1.0);
+  r = fma(r, e, r);
+  e = fma(-x, r, 1.0);
+  return fma(r, e, r);
+}
+
+// ldl_factor_kernel, one wavefront per column: the blockwise LDL' of
+// M = 2 lambda I + B/(n_v kappa) (stored as above). It reads the band,
+// lambda and n_v only, so a stage's factors can be formed as soon as the
+// band is known, before c = Q'1 is. Per 16-row block I:
+//   S = M_II - C_I D_{I-1} C_I';
+//   S = L D L' by a right-looking sweep whose row operations also turn an
+//   identity into L^{-1} (the product of the elimination steps);
+//   C_{I+1} = M_{I+1,I} L^{-T} D^{-1}.
+// The band tile of block I+1 (rows 0 .. 16 of its 16 columns) is loaded
+// while block I is worked on and passes through LDS.
+constexpr int FW = 4;                  // wavefronts (columns) per workgroup
+__global__ __launch_bounds__(64 * FW) void ldl_factor_kernel(
     int N, int C, int64_t cols, const int* __restrict__ nv, const double* __restrict__ band,
-    const double* __restrict__ cvec, const double* __restrict__ lamv, double kappa,
-    double* __restrict__ Vfac, double* __restrict__ Dfac, double* __restrict__ vhat,
-    double* __restrict__ gcoef, const double* __restrict__ ahat,
-    double* __restrict__ abar, const double* __restrict__ beta,
-    double* __restrict__ bbar, double* __restrict__ rmom, int* __restrict__ flag,
-    int* __restrict__ iters) {
-  extern __shared__ double lds_dyn[];
+    const double* __restrict__ lamv, double kappa, double* __restrict__ Vfac,
+    double* __restrict__ Dfac) {
+  __shared__ double tiles[FW * PTILE];
   const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t gc = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
+  const int64_t gc = (int64_t)blockIdx.x * FW + wv;
   if (gc >= cols) return;
-  double* xs = lds_dyn + (int64_t)wv * ((GV ? RING : N) + PTILE);   // vector or ring
   constexpr int TL = BND + 1;            // LDS row of a 16 x 16 tile
-  double* Cs = xs + (GV ? RING : N);     // C_I
-  double* Ls = Cs + BND * TL;            // L_I (strict lower) and D_I (diagonal)
-  double* Xs = Ls + BND * TL;            // L_I^{-1}
-  double* colb = Xs + BND * TL;          // one column of the LDL' sweep
-  double* dprv = colb + BND;             // D_{I-1}
+  double* Cs = tiles + wv * PTILE;       // C_I (upper triangular)
+  double* Xs = Cs + BND * TL;            // L_I^{-1} (unit lower triangular)
+  double* colb = Xs + BND * TL;          // column k of the sweep
+  double* wrow = colb + BND;             // row k of the inverse being formed
+  double* rdv = wrow + BND;              // 1 / D_I
+  double* dbuf = rdv + BND;              // D_I and D_{I-1}, by the parity of I
+  double* Bt = dbuf + 2 * BND;           // band tile of block I: Bt[r * BND + j] = B[i0+j+r][i0+j]
   const int g = (int)(gc / C);
   const double lam = lamv[gc];
   const double sc = 1.0 / ((double)nv[g] * kappa);
   const double* bg = band + (int64_t)g * (BND + 1) * N;
-  const double* cg = cvec + (int64_t)g * N;
   double* Vc = Vfac + gc * (int64_t)BND * N;
   double* Dc = Dfac + gc * (int64_t)N;
-  const int64_t base = gc * (int64_t)N;
   // lane (a, qg): row a of each 16 x 16 tile, columns 4 qg .. 4 qg + 3
   const int a = lane & (BND - 1), qg = lane >> 4;
   const int NB = N / BND;
+  // the (BND + 1) x BND band tile of block I, element e = lane + 64 q
+  constexpr int BTQ = ((BND + 1) * BND + 63) / 64;
+  const auto load_tile = [&](int I, double* bt) {
+    const int i0 = BND * I;
+#pragma unroll
+    for (int q = 0; q < BTQ; ++q) {
+      const int e = lane + 64 * q;
+      bt[q] = (e < (BND + 1) * BND) ? bg[(int64_t)(e / BND) * N + i0 + e % BND] : 0.0;
+    }
+  };
   for (int e = lane; e < BND * TL; e += 64) Cs[e] = 0.0;
-  if (lane < BND) dprv[lane] = 0.0;
+  if (lane < 2 * BND) dbuf[lane] = 0.0;
+  double bt[BTQ];
+  load_tile(0, bt);
   for (int I = 0; I < NB; ++I) {
     const int i0 = BND * I;
+    const double* dp = dbuf + ((I + 1) & 1) * BND;   // D_{I-1}
+    double* dc = dbuf + (I & 1) * BND;               // D_I
     wave_sync();
-    // S = M_II - C_I D_{I-1} C_I'
-    double cr[BND];
 #pragma unroll
-    for (int j = 0; j < BND; ++j) cr[j] = Cs[a * TL + j] * dprv[j];
-    double s4[4];
+    for (int q = 0; q < BTQ; ++q)
+      if (lane + 64 * q < (BND + 1) * BND) Bt[lane + 64 * q] = bt[q];
+    load_tile(I + 1 < NB ? I + 1 : I, bt);
+    wave_sync();
+    double s4[4], w4[4];
+    {
+      double cr[BND];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int c = 4 * qg + t;
-      const int64_t off = (c <= a) ? (int64_t)(a - c) * N + i0 + c : (int64_t)(c - a) * N + i0 + a;
-      const double m = fma(sc, bg[off], (c == a) ? 2.0 * lam : 0.0);
-      double acc0 = 0.0, acc1 = 0.0;
-#pragma unroll
-      for (int j = 0; j < BND; j += 2) {
-        acc0 = fma(cr[j], Cs[c * TL + j], acc0);
-        acc1 = fma(cr[j + 1], Cs[c * TL + j + 1], acc1);
-      }
-      s4[t] = m - (acc0 + acc1);
-    }
-    // S = L D L' (right-looking: column k through colb, trailing update by
-    // every lane on its four entries)
-#pragma unroll
-    for (int k = 0; k < BND; ++k) {
-      wave_sync();
-      if (qg == (k >> 2)) colb[a] = s4[k & 3];
-      wave_sync();
-      const double rk = 1.0 / colb[k];
-      const double la = colb[a] * rk;                 // L[a][k] for a > k
+      for (int j = 0; j < BND; ++j) cr[j] = Cs[a * TL + j] * dp[j];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const int j = 4 * qg + t;
-        const double upd = fma(-la, colb[j], s4[t]);
-        s4[t] = (a > k && j > k) ? upd : s4[t];
-      }
-      s4[k & 3] = (qg == (k >> 2) && a > k) ? la : s4[k & 3];
-    }
+        const int c = 4 * qg + t;
+        const double bv = (c <= a) ? Bt[(a - c) * BND + c] : Bt[(c - a) * BND + a];
+        const double m = fma(sc, bv, (c == a) ? 2.0 * lam : 0.0);
+        double acc0 = 0.0, acc1 = 0.0;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) Ls[a * TL + 4 * qg + t] = s4[t];
-    wave_sync();
-    // column a of L^{-1}: x_a = 1, x_i = -sum_{m=a}^{i-1} L[i][m] x_m,
-    // with running sums over the rows still to come
-    {
-      double acc[BND];
-#pragma unroll
-      for (int i = 0; i < BND; ++i) acc[i] = 0.0;
-      double x[BND];
-#pragma unroll
-      for (int m = 0; m < BND; ++m) {
-        x[m] = (m == a) ? 1.0 : ((m > a) ? -acc[m] : 0.0);
-#pragma unroll
-        for (int i = m + 1; i < BND; ++i) acc[i] = fma(Ls[i * TL + m], x[m], acc[i]);
-      }
-      if (qg == 0) {
-#pragma unroll
-        for (int i = 0; i < BND; ++i) Xs[i * TL + a] = x[i];
+        for (int j = 0; j < BND; j += 2) {
+          acc0 = fma(cr[j], Cs[c * TL + j], acc0);
+          acc1 = fma(cr[j + 1], Cs[c * TL + j + 1], acc1);
+        }
+        s4[t] = m - (acc0 + acc1);
+        w4[t] = (c == a) ? 1.0 : 0.0;
       }
     }
+    // the sweep: column k of S and row k of the inverse through LDS; rows
+    // below k take off l_ak times row k (S: trailing entries, W: all)
+#pragma unroll 1
+    for (int kq = 0; kq < BND / 4; ++kq) {
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+        const int k = 4 * kq + kt;
+        wave_sync();
+        if (qg == kq) colb[a] = s4[kt];
+        if (a == k) {
+#pragma unroll
+          for (int t = 0; t < 4; ++t) wrow[4 * qg + t] = w4[t];
+        }
+        wave_sync();
+        const double rk = rcp_newton(colb[k]);
+        const double ca = colb[a];
+        double cj[4], wk[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          cj[t] = colb[4 * qg + t];
+          wk[t] = wrow[4 * qg + t];
+        }
+        // entries outside the trailing block (a <= k or j <= k), and the
+        // inverse rows a <= k, take off a zero multiple: every lane runs
+        // the same straight-line code
+        const double cam = (a > k) ? ca : 0.0;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const double cjm = (4 * qg + t > k) ? cj[t] : 0.0;
+          s4[t] = fma(-(cam * cjm), rk, s4[t]);
+        }
+        const double la = ca * rk;                    // L[a][k] for a > k
+        const double lw = cam * rk;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w4[t] = fma(-lw, wk[t], w4[t]);
+        s4[kt] = ((qg == kq) & (a > k)) ? la : s4[kt];
+      }
+    }
+    // D_I, 1/D_I and L_I^{-1} to LDS
+    if (qg == (a >> 2)) {
+      const double da = s4[a & 3];
+      dc[a] = da;
+      rdv[a] = rcp_newton(da);
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) Xs[a * TL + 4 * qg + t] = w4[t];
     wave_sync();
     // the tile (L^{-1} below the diagonal, C_I on and above) and 1/D
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const int j = 4 * qg + t;
-      Vc[(int64_t)j * N + i0 + a] = (j < a) ? Xs[a * TL + j] : Cs[a * TL + j];
+      Vc[(int64_t)j * N + i0 + a] = (j < a) ? w4[t] : Cs[a * TL + j];
     }
-    const double da = Ls[a * TL + a];
-    if (qg == 0) Dc[i0 + a] = 1.0 / da;
-    // C_{I+1} = M_{I+1,I} L^{-T} D^{-1}: C[a][c] = sum_{j=a..c} Mn[a][j] X[c][j] / D[c]
+    if (qg == 0) Dc[i0 + a] = rdv[a];
+    // C_{I+1}[a][c] = sum_{j=a..c} M_{I+1,I}[a][j] X[c][j] / D[c], with
+    // B[i0+16+a][i0+j] = Bt[(16+a-j) BND + j] for j >= a
     double cn[4] = {0.0, 0.0, 0.0, 0.0};
     if (I + 1 < NB) {
       double mn[BND];
 #pragma unroll
-      for (int j = 0; j < BND; ++j) {
-        const int r = (j >= a) ? BND + a - j : BND;     // band row of B[i0+16+a][i0+j]
-        const double bv = bg[(int64_t)r * N + i0 + j];
-        mn[j] = (j >= a) ? sc * bv : 0.0;
-      }
+      for (int j = 0; j < BND; ++j) mn[j] = (j >= a) ? Bt[(BND + a - j) * BND + j] : 0.0;
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int c = 4 * qg + t;
@@ -608,16 +645,39 @@ __global__ __launch_bounds__(256) void precompute_kernel(
           acc0 = fma(mn[j], Xs[c * TL + j], acc0);
           acc1 = fma(mn[j + 1], Xs[c * TL + j + 1], acc1);
         }
-        cn[t] = (c >= a) ? (acc0 + acc1) / Ls[c * TL + c] : 0.0;
+        cn[t] = (c >= a) ? sc * (acc0 + acc1) * rdv[c] : 0.0;
       }
     }
     wave_sync();
 #pragma unroll
     for (int t = 0; t < 4; ++t) Cs[a * TL + 4 * qg + t] = cn[t];
-    if (qg == 0) dprv[a] = da;
   }
-  // vhat = M^{-1} c sc and c'vhat; the stage restart abar = ahat (u = B vhat
-  // and B abar follow in band_apply_kernel)
+}
+
+// stage_vectors_kernel, one wavefront per column, after the factors:
+// vhat = M^{-1} c/(n_v kappa), g = 1/(2 lambda c'vhat); restart the momentum
+// (r = 1, abar = ahat) and reactivate the columns that stopped in the
+// previous stage (u = B vhat and B abar follow in band_apply_kernel).
+template <bool GV>
+__global__ __launch_bounds__(256) void stage_vectors_kernel(
+    int N, int C, int64_t cols, const int* __restrict__ nv, const double* __restrict__ cvec,
+    const double* __restrict__ lamv, double kappa, const double* __restrict__ Vfac,
+    const double* __restrict__ Dfac, double* __restrict__ vhat, double* __restrict__ gcoef,
+    const double* __restrict__ ahat, double* __restrict__ abar, const double* __restrict__ beta,
+    double* __restrict__ bbar, double* __restrict__ rmom, int* __restrict__ flag,
+    int* __restrict__ iters) {
+  extern __shared__ double lds_dyn[];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t gc = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
+  if (gc >= cols) return;
+  double* xs = lds_dyn + (int64_t)wv * (GV ? RING : N);   // vector or ring
+  const int g = (int)(gc / C);
+  const double lam = lamv[gc];
+  const double sc = 1.0 / ((double)nv[g] * kappa);
+  const double* cg = cvec + (int64_t)g * N;
+  const double* Vc = Vfac + gc * (int64_t)BND * N;
+  const double* Dc = Dfac + gc * (int64_t)N;
+  const int64_t base = gc * (int64_t)N;
   double cv = 0.0;
   if constexpr (GV) {
     // lead lanes: input c sc, forward results kept in vhat, vhat = x
@@ -651,30 +711,42 @@ __global__ __launch_bounds__(256) void precompute_kernel(
   }
 }
 
-int path_stage_precompute(hipStream_t s, const PathArrays& p, double kappa) {
+int path_stage_factor(hipStream_t s, const PathArrays& p, double kappa) {
   const int64_t cols = (int64_t)p.G * p.C;
-  const int cw = path_waves(p, PTILE);
-  const size_t lds = sizeof(double) * (size_t)cw * path_lds_doubles(p, PTILE);
-  const void* kfn = path_global_vec(p) ? (const void*)precompute_kernel<true>
-                                       : (const void*)precompute_kernel<false>;
+  kc_begin(KMP_KC_PRECOMPUTE, s);
+  hipLaunchKernelGGL(ldl_factor_kernel, dim3((unsigned)ceil_div(cols, FW)), dim3(64 * FW), 0, s, p.N,
+                     p.C, cols, p.nv, p.band, p.lam, kappa, p.ldl_l, p.ldl_d);
+  KMP_LAUNCH_CHECK();
+  // reads the band, writes the factor tiles and 1/d (BND + 1 per element)
+  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 1.0); }),
+         over_groups(p, [&](double n) { return 4.0 * BND * BND * n * p.C; }));
+  return 0;
+}
+
+int path_stage_vectors(hipStream_t s, const PathArrays& p, double kappa) {
+  const int64_t cols = (int64_t)p.G * p.C;
+  const int cw = path_waves(p, 0);
+  const size_t lds = sizeof(double) * (size_t)cw * path_lds_doubles(p, 0);
+  const void* kfn = path_global_vec(p) ? (const void*)stage_vectors_kernel<true>
+                                       : (const void*)stage_vectors_kernel<false>;
   KMP_HIP_TRY(hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   kc_begin(KMP_KC_PRECOMPUTE, s);
   if (path_global_vec(p))
-    hipLaunchKernelGGL(precompute_kernel<true>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds,
-                       s, p.N, p.C, cols, p.nv, p.band, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
+    hipLaunchKernelGGL(stage_vectors_kernel<true>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw),
+                       lds, s, p.N, p.C, cols, p.nv, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
                        p.gcoef, p.ahat, p.abar, p.beta, p.bbar, p.rmom, p.flag, p.iters);
   else
-    hipLaunchKernelGGL(precompute_kernel<false>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds,
-                       s, p.N, p.C, cols, p.nv, p.band, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
+    hipLaunchKernelGGL(stage_vectors_kernel<false>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw),
+                       lds, s, p.N, p.C, cols, p.nv, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
                        p.gcoef, p.ahat, p.abar, p.beta, p.bbar, p.rmom, p.flag, p.iters);
   KMP_LAUNCH_CHECK();
   int rc;
   if ((rc = band_apply(s, p, p.vhat, p.uvec)) != 0) return rc;
   if ((rc = band_apply(s, p, p.ahat, p.bmat)) != 0) return rc;
-  // reads the band and c, writes the factor tiles (BND per element), 1/d,
-  // vhat, abar; then u = B vhat and B abar (read one vector, write one)
-  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 8.0); }),
-         over_groups(p, [&](double n) { return 4.0 * BND * BND * n * p.C; }));
+  // the solve reads the factor (BND + 1 per element) and c, writes vhat;
+  // ahat to abar; then u = B vhat and B abar (read one vector, write one)
+  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 9.0); }),
+         over_groups(p, [&](double n) { return (4.0 * BND + 4.0 * (2 * BND + 1)) * n * p.C; }));
   return 0;
 }
 
