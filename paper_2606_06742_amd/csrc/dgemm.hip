@@ -84,6 +84,19 @@ __device__ __forceinline__ void fetch_slice(int M, int N, int K, int i0, int j0,
   }
 }
 
+// LDS column of element (k, c) of a staged slice. The columns are permuted
+// within aligned groups so that the lanes of one store instruction land in
+// distinct banks: a slice fetched along k (four consecutive k per thread,
+// KC) has rows k, k+4, k+8, k+12 in one instruction, so bits 2-3 of the
+// column take those of k; one fetched along the columns (four consecutive
+// columns per thread) has columns 4 apart, so bits 0-1 take bits 4-5.
+// The matrix-core reads (16 consecutive columns of one row per lane group)
+// stay conflict free under either permutation.
+template <bool KC>
+__device__ __forceinline__ int lds_col(int k, int c) {
+  return KC ? c ^ (((k >> 2) & 3) << 2) : c ^ ((c >> 4) & 3);
+}
+
 template <int BM, int BK, bool AK, bool BKC>
 __device__ __forceinline__ void store_slice(const double (&ra)[Tile<BM, BK>::APT],
                                             const double (&rb)[Tile<BM, BK>::BPT],
@@ -94,37 +107,62 @@ __device__ __forceinline__ void store_slice(const double (&ra)[Tile<BM, BK>::APT
     constexpr int TPR = BK / APT;
     const int i = t / TPR, kb = (t % TPR) * APT;
 #pragma unroll
-    for (int q = 0; q < APT; ++q) As[kb + q][i] = ra[q];
+    for (int q = 0; q < APT; ++q) As[kb + q][lds_col<true>(kb + q, i)] = ra[q];
   } else {
     constexpr int TPR = BM / APT;
     const int k = t / TPR, ib = (t % TPR) * APT;
 #pragma unroll
-    for (int q = 0; q < APT; ++q) As[k][ib + q] = ra[q];
+    for (int q = 0; q < APT; ++q) As[k][lds_col<false>(k, ib + q)] = ra[q];
   }
   if (BKC) {
     constexpr int TPR = BK / BPT;
     const int j = t / TPR, kb = (t % TPR) * BPT;
 #pragma unroll
-    for (int q = 0; q < BPT; ++q) Bs[kb + q][j] = rb[q];
+    for (int q = 0; q < BPT; ++q) Bs[kb + q][lds_col<true>(kb + q, j)] = rb[q];
   } else {
     constexpr int TPR = TN / BPT;
     const int k = t / TPR, jb = (t % TPR) * BPT;
 #pragma unroll
-    for (int q = 0; q < BPT; ++q) Bs[k][jb + q] = rb[q];
+    for (int q = 0; q < BPT; ++q) Bs[k][lds_col<false>(k, jb + q)] = rb[q];
+  }
+}
+
+// Matrix-core products of one LDS stage into acc (see tile_mainloop).
+template <int BM, int BK, bool AK, bool BKC>
+__device__ __forceinline__ void tile_stage_mfma(const double (*As)[BM + LPAD],
+                                                const double (*Bs)[TN + LPAD], int wi, int wj,
+                                                int li, int lk, bool use1,
+                                                dbl4 (&acc)[Tile<BM, BK>::MB][2]) {
+  constexpr int MB = Tile<BM, BK>::MB;
+#pragma unroll
+  for (int kk = 0; kk < BK; kk += 4) {
+    double av[MB];
+#pragma unroll
+    for (int a = 0; a < MB; ++a) av[a] = As[kk + lk][lds_col<AK>(kk + lk, wi + 16 * a + li)];
+    const double b0 = Bs[kk + lk][lds_col<BKC>(kk + lk, wj + li)];
+    const double b1 = Bs[kk + lk][lds_col<BKC>(kk + lk, wj + 16 + li)];
+#pragma unroll
+    for (int a = 0; a < MB; ++a) {
+      acc[a][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b0, acc[a][0], 0, 0, 0);
+      if (use1) acc[a][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b1, acc[a][1], 0, 0, 0);
+    }
   }
 }
 
 // Main loop shared by all variants. acc[bi][bj] covers rows
-// wi + 16 bi .., cols wj + 16 bj ... Two LDS stages: slice k+1 is fetched
-// into registers before the MFMAs on slice k and stored into the other
-// stage afterwards (one barrier per slice).
+// wi + 16 bi .., cols wj + 16 bj ... Two LDS stages, one barrier per slice.
+// PF = 1: slice k+1 is fetched into registers before the MFMAs on slice k
+// and stored into the other stage afterwards. PF = 2: two register sets;
+// at the start of step k slice k+1 (fetched two steps earlier) goes to the
+// free stage and slice k+3 is fetched into its registers, so every load
+// has two steps of matrix work to arrive.
 //
 // cmap (k-contiguous B only, may be null) maps tile column j0 + j to the
 // column cmap[j0 + j] of B; N then counts the mapped columns. A wave skips
 // the matrix products of a 16-column block that lies wholly past N (a
 // wave-uniform test), so a tile with few columns costs little more than
 // its loads.
-template <int BM, int BK, bool AK, bool BKC>
+template <int BM, int BK, bool AK, bool BKC, int PF = 1>
 __device__ __forceinline__ void tile_mainloop(int M, int N, int kbeg, int K, int i0, int j0,
                                               const double* __restrict__ A, int64_t lda,
                                               const double* __restrict__ B, int64_t ldb,
@@ -147,34 +185,48 @@ __device__ __forceinline__ void tile_mainloop(int M, int N, int kbeg, int K, int
     if (gj < N) bcol = B + (int64_t)(cmap ? cmap[gj] : gj) * ldb;
   }
   const bool use0 = j0 + wj < N, use1 = j0 + wj + 16 < N;
-  double ra[Tile<BM, BK>::APT], rb[Tile<BM, BK>::BPT];
-  fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg, A, lda, B, ldb, bcol, ra, rb);
-  store_slice<BM, BK, AK, BKC>(ra, rb, As[0], Bs[0]);
-  __syncthreads();
   const int nk = (K - kbeg + BK - 1) / BK;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more)
-      fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + (kt + 1) * BK, A, lda, B, ldb, bcol,
-                                   ra, rb);
-    if (use0) {
-#pragma unroll
-      for (int kk = 0; kk < BK; kk += 4) {
-        double av[MB];
-#pragma unroll
-        for (int a = 0; a < MB; ++a) av[a] = As[cur][kk + lk][wi + 16 * a + li];
-        const double b0 = Bs[cur][kk + lk][wj + li];
-        const double b1 = Bs[cur][kk + lk][wj + 16 + li];
-#pragma unroll
-        for (int a = 0; a < MB; ++a) {
-          acc[a][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b0, acc[a][0], 0, 0, 0);
-          if (use1) acc[a][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b1, acc[a][1], 0, 0, 0);
-        }
-      }
-    }
-    if (more) store_slice<BM, BK, AK, BKC>(ra, rb, As[cur ^ 1], Bs[cur ^ 1]);
+  if constexpr (PF == 1) {
+    double ra[Tile<BM, BK>::APT], rb[Tile<BM, BK>::BPT];
+    fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg, A, lda, B, ldb, bcol, ra, rb);
+    store_slice<BM, BK, AK, BKC>(ra, rb, As[0], Bs[0]);
     __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int cur = kt & 1;
+      const bool more = kt + 1 < nk;
+      if (more)
+        fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + (kt + 1) * BK, A, lda, B, ldb, bcol,
+                                     ra, rb);
+      if (use0) tile_stage_mfma<BM, BK, AK, BKC>(As[cur], Bs[cur], wi, wj, li, lk, use1, acc);
+      if (more) store_slice<BM, BK, AK, BKC>(ra, rb, As[cur ^ 1], Bs[cur ^ 1]);
+      __syncthreads();
+    }
+  } else {
+    double ra0[Tile<BM, BK>::APT], rb0[Tile<BM, BK>::BPT];
+    double ra1[Tile<BM, BK>::APT], rb1[Tile<BM, BK>::BPT];
+    fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg, A, lda, B, ldb, bcol, ra0, rb0);
+    store_slice<BM, BK, AK, BKC>(ra0, rb0, As[0], Bs[0]);
+    if (nk > 1) fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + BK, A, lda, B, ldb, bcol, ra0, rb0);
+    if (nk > 2)
+      fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + 2 * BK, A, lda, B, ldb, bcol, ra1, rb1);
+    __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+      // even step: slice kt in stage 0, slice kt+1 in (ra0, rb0)
+      if (kt + 1 < nk) store_slice<BM, BK, AK, BKC>(ra0, rb0, As[1], Bs[1]);
+      if (kt + 3 < nk)
+        fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + (kt + 3) * BK, A, lda, B, ldb, bcol,
+                                     ra0, rb0);
+      if (use0) tile_stage_mfma<BM, BK, AK, BKC>(As[0], Bs[0], wi, wj, li, lk, use1, acc);
+      __syncthreads();
+      if (kt + 1 >= nk) break;
+      // odd step: slice kt+1 in stage 1, slice kt+2 in (ra1, rb1)
+      if (kt + 2 < nk) store_slice<BM, BK, AK, BKC>(ra1, rb1, As[0], Bs[0]);
+      if (kt + 4 < nk)
+        fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + (kt + 4) * BK, A, lda, B, ldb, bcol,
+                                     ra1, rb1);
+      if (use0) tile_stage_mfma<BM, BK, AK, BKC>(As[1], Bs[1], wi, wj, li, lk, use1, acc);
+      __syncthreads();
+    }
   }
 }
 
@@ -288,7 +340,7 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
 // is column cmap[b*cstride + k] of B and of the partials (the other columns
 // of the partials are left as they were); tiles past nact[b] exit at once.
 // With IDENT (cmap and nact null), all cstride columns, in order.
-template <int BM, int BK, bool AK, bool IDENT>
+template <int BM, int BK, bool AK, bool IDENT, int PF = 1>
 __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S, int Kc,
                                                              const double* __restrict__ A, int64_t lda, int64_t sA,
                                                              const double* __restrict__ B, int64_t ldb, int64_t sB,
@@ -308,7 +360,7 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
   const int kend = min(K, kbeg + Kc);
   dbl4 acc[MB][2];
   if (kbeg < kend) {
-    tile_mainloop<BM, BK, AK, true>(M, N, kbeg, kend, i0, j0, A, lda, B, ldb, cmap, acc);
+    tile_mainloop<BM, BK, AK, true, PF>(M, N, kbeg, kend, i0, j0, A, lda, B, ldb, cmap, acc);
   } else {
 #pragma unroll
     for (int a = 0; a < MB; ++a) acc[a][0] = acc[a][1] = dbl4{0.0, 0.0, 0.0, 0.0};
@@ -444,7 +496,7 @@ int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double
   }
 #define KMP_PART_CASE(AKV, IDV)                                                                  \
   if (a_kcontig == AKV && ident == IDV)                                                          \
-    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, AKV, IDV>), grid, dim3(256), 0, s, g.M, g.K, \
+    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, AKV, IDV, 2>), grid, dim3(256), 0, s, g.M, g.K, \
                        S, Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap,    \
                        nact, g.N);
   KMP_PART_CASE(true, false)
