@@ -95,6 +95,57 @@ int side_stream(hipStream_t* out) {
   return 0;
 }
 
+// Host-side resources every call on a device reuses: pinned staging memory
+// for the small transfers (grown on demand) and events. Kept per thread and
+// device for the life of the thread and never freed (the runtime may be
+// gone when a thread ends). A call that returns before its stream has
+// drained leaves the context dirty; the next call then waits for the device
+// before it reuses the staging memory.
+struct CallCtx {
+  char* pin = nullptr;
+  size_t pin_cap = 0;
+  bool dirty = false;
+  hipEvent_t ev_check = nullptr, ev_poll = nullptr, ev_band = nullptr, ev_fact = nullptr;
+  std::vector<hipEvent_t> timing;    // pool of timing events (EventTimer)
+};
+int call_ctx(size_t pin_bytes, CallCtx** out) {
+  int dev = 0;
+  KMP_HIP_TRY(hipGetDevice(&dev));
+  static thread_local std::map<int, CallCtx> ctxs;
+  CallCtx& c = ctxs[dev];
+  if (!c.ev_check) {
+    for (hipEvent_t* e : {&c.ev_check, &c.ev_poll, &c.ev_band, &c.ev_fact})
+      KMP_HIP_TRY(hipEventCreateWithFlags(e, hipEventDisableTiming));
+  }
+  if (c.dirty) {
+    KMP_HIP_TRY(hipDeviceSynchronize());
+    c.dirty = false;
+  }
+  if (pin_bytes > c.pin_cap) {
+    if (c.pin) KMP_HIP_TRY(hipHostFree(c.pin));
+    c.pin = nullptr;
+    c.pin_cap = 0;
+    const size_t cap = std::max<size_t>(pin_bytes, 1 << 20);
+    KMP_HIP_TRY(hipHostMalloc((void**)&c.pin, cap, hipHostMallocDefault));
+    c.pin_cap = cap;
+  }
+  *out = &c;
+  return 0;
+}
+
+// Consecutive 64-byte aligned pieces of a staging buffer.
+struct Bump {
+  char* base = nullptr;
+  size_t off = 0;
+  static size_t round(size_t b) { return (b + 63) & ~(size_t)63; }
+  template <typename T>
+  T* take(size_t count) {
+    T* r = reinterpret_cast<T*>(base + off);
+    off += round(count * sizeof(T));
+    return r;
+  }
+};
+
 constexpr int kPanel = 32;       // Householder panel width
 constexpr int kRowAlign = 64;    // padding of the per-fold matrix order
 constexpr size_t kAlign = 256;
@@ -250,16 +301,14 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
 // added to a total when sum() runs after the final synchronisation, so the
 // host never waits on the device to read a phase time.
 struct EventTimer {
-  std::vector<hipEvent_t> ev;
+  std::vector<hipEvent_t>& ev;    // pool, grown on demand and reused
   size_t used = 0;
   struct Span {
     double* acc;
     size_t a, b;
   };
   std::vector<Span> spans;
-  ~EventTimer() {
-    for (auto& e : ev) (void)hipEventDestroy(e);
-  }
+  explicit EventTimer(std::vector<hipEvent_t>& pool) : ev(pool) {}
   int mark(hipStream_t s, size_t* idx) {
     if (used == ev.size()) {
       hipEvent_t e;
@@ -510,41 +559,69 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   }
   Layout lay;
   carve(plan, workspace, &lay);
-  // finiteness of X and y counted on the device (two ints in the
-  // workspace); y and the counts come to the host for the label checks
-  if ((rc = count_nonfinite(s, X, n, d, ldx, y, lay.chk)) != 0) return rc;
-  std::vector<double> hy(n);
-  int hchk[2] = {0, 0};
-  KMP_HIP_TRY(hipMemcpyAsync(hy.data(), y, sizeof(double) * n, hipMemcpyDeviceToHost, s));
-  KMP_HIP_TRY(hipMemcpyAsync(hchk, lay.chk, sizeof(hchk), hipMemcpyDeviceToHost, s));
-  KMP_HIP_TRY(hipStreamSynchronize(s));
-  if (hchk[0] != 0) {
-    set_error(std::to_string(hchk[0]) + " non-finite entries in X");
-    return KMP_ENONFINITE;
-  }
-  if (hchk[1] != 0) {
-    set_error(std::to_string(hchk[1]) + " non-finite entries in y");
-    return KMP_ENONFINITE;
-  }
-  if (spec->loss != KMP_CHECK) {
-    std::vector<int64_t> pos(V, 0), neg(V, 0);
-    int64_t tp = 0, tn = 0;
-    for (int64_t i = 0; i < n; ++i) {
-      if (hy[i] == 1.0) { pos[fold_id[i]]++; tp++; }
-      else if (hy[i] == -1.0) { neg[fold_id[i]]++; tn++; }
-      else {
-        set_error("labels must be +1 or -1 for hinge and logistic losses");
-        return KMP_EINVAL;
-      }
-    }
-    for (int v = 0; v < V; ++v)
-      if (tp - pos[v] == 0 || tn - neg[v] == 0) {
-        set_error("training set of fold " + std::to_string(v) + " has a single class");
-        return KMP_EFOLD;
-      }
-  }
-
   const int N = plan.N, C = plan.C, G = plan.G;
+  const size_t ncell = (size_t)S * Qn * V * L;
+  // pinned staging for every host<->device transfer of the call
+  const int nbatch = (S + Sb - 1) / Sb;
+  const size_t pin_bytes =
+      Bump::round(sizeof(double) * n) + Bump::round(2 * sizeof(int)) +
+      Bump::round(sizeof(int32_t) * (size_t)V * N) +
+      Bump::round(sizeof(int32_t) * (size_t)V * plan.Mh) + Bump::round(sizeof(int32_t) * n) +
+      Bump::round(sizeof(int) * ((size_t)G + 1)) +
+      (size_t)nbatch * (Bump::round(sizeof(double) * Sb) +
+                        2 * Bump::round(sizeof(double) * (size_t)G * C) +
+                        Bump::round(sizeof(int) * (size_t)G)) +
+      Bump::round(sizeof(double) * ncell) + 2 * Bump::round(sizeof(int32_t) * ncell);
+  CallCtx* ctx = nullptr;
+  if ((rc = call_ctx(pin_bytes, &ctx)) != 0) return rc;
+  Bump pin{ctx->pin, 0};
+  // an early return leaves copies into the staging memory in flight
+  struct DirtyGuard {
+    CallCtx* c;
+    bool clean = false;
+    ~DirtyGuard() {
+      if (!clean) c->dirty = true;
+    }
+  } dirty_guard{ctx};
+  // Finiteness of X and y is counted on the device (two ints in the
+  // workspace); y and the counts come back while the factorisation is
+  // queued and are checked before anything is written to the outputs.
+  if ((rc = count_nonfinite(s, X, n, d, ldx, y, lay.chk)) != 0) return rc;
+  double* hy = pin.take<double>(n);
+  int* hchk = pin.take<int>(2);
+  KMP_HIP_TRY(hipMemcpyAsync(hy, y, sizeof(double) * n, hipMemcpyDeviceToHost, s));
+  KMP_HIP_TRY(hipMemcpyAsync(hchk, lay.chk, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
+  KMP_HIP_TRY(hipEventRecord(ctx->ev_check, s));
+  const auto check_inputs = [&]() -> int {
+    KMP_HIP_TRY(hipEventSynchronize(ctx->ev_check));
+    if (hchk[0] != 0) {
+      set_error(std::to_string(hchk[0]) + " non-finite entries in X");
+      return KMP_ENONFINITE;
+    }
+    if (hchk[1] != 0) {
+      set_error(std::to_string(hchk[1]) + " non-finite entries in y");
+      return KMP_ENONFINITE;
+    }
+    if (spec->loss != KMP_CHECK) {
+      std::vector<int64_t> pos(V, 0), neg(V, 0);
+      int64_t tp = 0, tn = 0;
+      for (int64_t i = 0; i < n; ++i) {
+        if (hy[i] == 1.0) { pos[fold_id[i]]++; tp++; }
+        else if (hy[i] == -1.0) { neg[fold_id[i]]++; tn++; }
+        else {
+          set_error("labels must be +1 or -1 for hinge and logistic losses");
+          return KMP_EINVAL;
+        }
+      }
+      for (int v = 0; v < V; ++v)
+        if (tp - pos[v] == 0 || tn - neg[v] == 0) {
+          set_error("training set of fold " + std::to_string(v) + " has a single class");
+          return KMP_EFOLD;
+        }
+    }
+    return 0;
+  };
+
   const int nst = spec->loss == KMP_LOGISTIC ? 1 : spec->n_stages;
   // smoothing parameter and curvature bound of each stage
   const auto stage_delta = [&](int st) {
@@ -556,27 +633,29 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   const double delta_final = stage_delta(nst - 1);
 
   // host-side index lists and per-column parameters
-  std::vector<int32_t> tidx((size_t)V * N, -1);
+  int32_t* tidx = pin.take<int32_t>((size_t)V * N);
+  std::fill(tidx, tidx + (size_t)V * N, -1);
   for (int v = 0; v < V; ++v) {
     int k = 0;
     for (int64_t i = 0; i < n; ++i)
       if (fold_id[i] != v) tidx[(size_t)v * N + k++] = (int32_t)i;
   }
-  KMP_HIP_TRY(hipMemcpyAsync(lay.tidx, tidx.data(), sizeof(int32_t) * tidx.size(),
+  KMP_HIP_TRY(hipMemcpyAsync(lay.tidx, tidx, sizeof(int32_t) * (size_t)V * N,
                              hipMemcpyHostToDevice, s));
-  std::vector<int32_t> hidx((size_t)V * plan.Mh, -1);
+  int32_t* hidx = pin.take<int32_t>((size_t)V * plan.Mh);
+  std::fill(hidx, hidx + (size_t)V * plan.Mh, -1);
   for (int v = 0; v < V; ++v) {
     int k = 0;
     for (int64_t i = 0; i < n; ++i)
       if (fold_id[i] == v) hidx[(size_t)v * plan.Mh + k++] = (int32_t)i;
   }
-  KMP_HIP_TRY(hipMemcpyAsync(lay.hidx, hidx.data(), sizeof(int32_t) * hidx.size(),
+  KMP_HIP_TRY(hipMemcpyAsync(lay.hidx, hidx, sizeof(int32_t) * (size_t)V * plan.Mh,
                              hipMemcpyHostToDevice, s));
-  KMP_HIP_TRY(hipMemcpyAsync(lay.fold, fold_id, sizeof(int32_t) * n, hipMemcpyHostToDevice, s));
-  const size_t ncell = (size_t)S * Qn * V * L;
-  KMP_HIP_TRY(hipMemsetAsync(alpha, 0, sizeof(double) * ncell * n, s));
+  int32_t* hfold = pin.take<int32_t>(n);
+  std::copy(fold_id, fold_id + n, hfold);
+  KMP_HIP_TRY(hipMemcpyAsync(lay.fold, hfold, sizeof(int32_t) * n, hipMemcpyHostToDevice, s));
 
-  EventTimer tm;
+  EventTimer tm(ctx->timing);
   double t_gram = 0, t_factor = 0, t_pre = 0, t_path = 0, t_fin = 0;
   struct ClockGuard {
     ClockGuard(uint32_t mask) {
@@ -594,15 +673,9 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   int64_t total_iters = 0;
   // pinned host buffer for the per-group and total active counts
   struct PollBuf {
-    int* p = nullptr;
-    hipEvent_t ev = nullptr;
-    ~PollBuf() {
-      if (p) (void)hipHostFree(p);
-      if (ev) (void)hipEventDestroy(ev);
-    }
-  } poll;
-  KMP_HIP_TRY(hipHostMalloc((void**)&poll.p, sizeof(int) * ((size_t)plan.G + 1), hipHostMallocDefault));
-  KMP_HIP_TRY(hipEventCreateWithFlags(&poll.ev, hipEventDisableTiming));
+    int* p;
+    hipEvent_t ev;
+  } poll{pin.take<int>((size_t)G + 1), ctx->ev_poll};
   // The first stage's factors need the band only: they are formed on a side
   // stream while the caller's stream accumulates Q, and the stage waits for
   // them. Leaving the call (also on an error) waits for the side stream.
@@ -612,13 +685,11 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     bool queued = false;
     ~SideWork() {
       if (queued) (void)hipStreamSynchronize(st);
-      if (band) (void)hipEventDestroy(band);
-      if (done) (void)hipEventDestroy(done);
     }
   } side;
   if ((rc = side_stream(&side.st)) != 0) return rc;
-  KMP_HIP_TRY(hipEventCreateWithFlags(&side.band, hipEventDisableTiming));
-  KMP_HIP_TRY(hipEventCreateWithFlags(&side.done, hipEventDisableTiming));
+  side.band = ctx->ev_band;
+  side.done = ctx->ev_fact;
   size_t ev_start = 0, e1 = 0, e2 = 0, e3 = 0;
   if ((rc = tm.mark(s, &ev_start)) != 0) return rc;
   if ((rc = row_norms(s, X, n, d, ldx, lay.nrm)) != 0) return rc;
@@ -643,8 +714,10 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     const int Gb = sb * V;
     pa.G = Gb;
     // per-batch parameters
-    std::vector<double> f2(sb), lamc((size_t)Gb * C), tauc((size_t)Gb * C);
-    std::vector<int> nvg(Gb);
+    double* f2 = pin.take<double>(Sb);
+    double* lamc = pin.take<double>((size_t)G * C);
+    double* tauc = pin.take<double>((size_t)G * C);
+    int* nvg = pin.take<int>(G);
     for (int i = 0; i < sb; ++i) f2[i] = 1.0 / (2.0 * sigmas[s0 + i] * sigmas[s0 + i]);
     for (int g = 0; g < Gb; ++g) {
       nvg[g] = plan.nv[g % V];
@@ -654,13 +727,13 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
           tauc[(size_t)g * C + q * L + l] = spec->loss == KMP_CHECK ? taus[q] : 0.0;
         }
     }
-    KMP_HIP_TRY(hipMemcpyAsync(lay.inv2s2, f2.data(), sizeof(double) * sb, hipMemcpyHostToDevice, s));
-    KMP_HIP_TRY(hipMemcpyAsync(lay.lam, lamc.data(), sizeof(double) * lamc.size(),
+    KMP_HIP_TRY(hipMemcpyAsync(lay.inv2s2, f2, sizeof(double) * sb, hipMemcpyHostToDevice, s));
+    KMP_HIP_TRY(hipMemcpyAsync(lay.lam, lamc, sizeof(double) * (size_t)Gb * C,
                                hipMemcpyHostToDevice, s));
-    KMP_HIP_TRY(hipMemcpyAsync(lay.taucol, tauc.data(), sizeof(double) * tauc.size(),
+    KMP_HIP_TRY(hipMemcpyAsync(lay.taucol, tauc, sizeof(double) * (size_t)Gb * C,
                                hipMemcpyHostToDevice, s));
-    KMP_HIP_TRY(hipMemcpyAsync(lay.nvg, nvg.data(), sizeof(int) * Gb, hipMemcpyHostToDevice, s));
-    pa.nv_host = nvg.data();
+    KMP_HIP_TRY(hipMemcpyAsync(lay.nvg, nvg, sizeof(int) * Gb, hipMemcpyHostToDevice, s));
+    pa.nv_host = nvg;
     // columns in each group's active list, as last read back (work counters)
     std::vector<int> nact_h(Gb, C);
     pa.nact_host = nact_h.data();
@@ -685,7 +758,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     static_assert(kPanel >= 2 * kBand, "two band panel buffers share the panel slot");
     bw.panel = lay.panel; bw.panel2 = lay.panel + (size_t)Gb * 3 * kBand * N;
     bw.tmat = lay.tmat; bw.gram = lay.gram; bw.xbuf = lay.xbuf;
-    bw.ybuf = lay.ybuf; bw.part = lay.bpart; bw.nv_host = nvg.data();
+    bw.ybuf = lay.ybuf; bw.part = lay.bpart; bw.nv_host = nvg;
     bw.gram_all = lay.gram_all; bw.tmat_all = lay.tmat_all; bw.cross_all = lay.cross_all;
     bw.xpart = lay.xpart;
     bw.band_ready = side.band;
@@ -701,6 +774,16 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     tm.span(&t_gram, e1, e2);
     tm.span(&t_factor, e2, e3);
 
+    if (s0 == 0) {
+      // the inputs' checks have long come back (the factorisation is
+      // queued ahead of the device); on an error the queued work drains
+      // into the workspace only
+      if ((rc = check_inputs()) != 0) {
+        (void)hipStreamSynchronize(s);
+        return rc;
+      }
+      KMP_HIP_TRY(hipMemsetAsync(alpha, 0, sizeof(double) * ncell * n, s));
+    }
     // a3-a9: smoothing stages
     for (int st = 0; st < nst; ++st) {
       const double delta = stage_delta(st);
@@ -777,20 +860,27 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   }
   size_t ev_end = 0;
   if ((rc = tm.mark(s, &ev_end)) != 0) return rc;
+  // host-side selection and status summary: the three arrays come back
+  // with one wait
+  double* hcv = pin.take<double>(ncell);
+  int32_t* hst = pin.take<int32_t>(ncell);
+  int32_t* hit = pin.take<int32_t>(ncell);
+  KMP_HIP_TRY(hipMemcpyAsync(hcv, cv_sum, sizeof(double) * ncell, hipMemcpyDeviceToHost, s));
+  if (status)
+    KMP_HIP_TRY(hipMemcpyAsync(hst, status, sizeof(int32_t) * ncell, hipMemcpyDeviceToHost, s));
+  if (iters)
+    KMP_HIP_TRY(hipMemcpyAsync(hit, iters, sizeof(int32_t) * ncell, hipMemcpyDeviceToHost, s));
   KMP_HIP_TRY(hipStreamSynchronize(s));
+  dirty_guard.clean = true;
   double t_total = 0.0;
   tm.span(&t_total, ev_start, ev_end);
   tm.sum();
 
-  // host-side selection and status summary
-  std::vector<double> hcv(ncell);
-  KMP_HIP_TRY(hipMemcpy(hcv.data(), cv_sum, sizeof(double) * ncell, hipMemcpyDeviceToHost));
   bool any_max = false;
   int64_t cell_iters = 0;
   if (status) {
-    std::vector<int32_t> hst(ncell);
-    KMP_HIP_TRY(hipMemcpy(hst.data(), status, sizeof(int32_t) * ncell, hipMemcpyDeviceToHost));
-    for (auto v : hst) {
+    for (size_t i = 0; i < ncell; ++i) {
+      const int32_t v = hst[i];
       if (v == 1) any_max = true;
       if (v == 2) {
         set_error("non-finite values in the iteration");
@@ -798,11 +888,8 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
       }
     }
   }
-  if (iters) {
-    std::vector<int32_t> hit(ncell);
-    KMP_HIP_TRY(hipMemcpy(hit.data(), iters, sizeof(int32_t) * ncell, hipMemcpyDeviceToHost));
-    for (auto v : hit) cell_iters += v;
-  }
+  if (iters)
+    for (size_t i = 0; i < ncell; ++i) cell_iters += hit[i];
   if (selected) {
     for (int si = 0; si < S; ++si)
       for (int q = 0; q < Qn; ++q) {
