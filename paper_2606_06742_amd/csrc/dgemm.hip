@@ -86,15 +86,15 @@ __device__ __forceinline__ void fetch_slice(int M, int N, int K, int i0, int j0,
 
 // LDS column of element (k, c) of a staged slice. The columns are permuted
 // within aligned groups so that the lanes of one store instruction land in
-// distinct banks: a slice fetched along k (four consecutive k per thread,
-// KC) has rows k, k+4, k+8, k+12 in one instruction, so bits 2-3 of the
-// column take those of k; one fetched along the columns (four consecutive
-// columns per thread) has columns 4 apart, so bits 0-1 take bits 4-5.
-// The matrix-core reads (16 consecutive columns of one row per lane group)
+// distinct banks: a slice fetched along k (RS consecutive k per thread, KC)
+// has rows RS apart in one instruction, so bits 2-3 of the column take
+// those of k / RS; one fetched along the columns (consecutive columns per
+// thread) has columns 4 or more apart, so bits 0-1 take bits 4-5. The
+// matrix-core reads (16 consecutive columns of one row per lane group)
 // stay conflict free under either permutation.
-template <bool KC>
+template <bool KC, int RS>
 __device__ __forceinline__ int lds_col(int k, int c) {
-  return KC ? c ^ (((k >> 2) & 3) << 2) : c ^ ((c >> 4) & 3);
+  return KC ? c ^ (((k / RS) & 3) << 2) : c ^ ((c >> 4) & 3);
 }
 
 template <int BM, int BK, bool AK, bool BKC>
@@ -107,23 +107,23 @@ __device__ __forceinline__ void store_slice(const double (&ra)[Tile<BM, BK>::APT
     constexpr int TPR = BK / APT;
     const int i = t / TPR, kb = (t % TPR) * APT;
 #pragma unroll
-    for (int q = 0; q < APT; ++q) As[kb + q][lds_col<true>(kb + q, i)] = ra[q];
+    for (int q = 0; q < APT; ++q) As[kb + q][lds_col<true, APT>(kb + q, i)] = ra[q];
   } else {
     constexpr int TPR = BM / APT;
     const int k = t / TPR, ib = (t % TPR) * APT;
 #pragma unroll
-    for (int q = 0; q < APT; ++q) As[k][lds_col<false>(k, ib + q)] = ra[q];
+    for (int q = 0; q < APT; ++q) As[k][lds_col<false, APT>(k, ib + q)] = ra[q];
   }
   if (BKC) {
     constexpr int TPR = BK / BPT;
     const int j = t / TPR, kb = (t % TPR) * BPT;
 #pragma unroll
-    for (int q = 0; q < BPT; ++q) Bs[kb + q][lds_col<true>(kb + q, j)] = rb[q];
+    for (int q = 0; q < BPT; ++q) Bs[kb + q][lds_col<true, BPT>(kb + q, j)] = rb[q];
   } else {
     constexpr int TPR = TN / BPT;
     const int k = t / TPR, jb = (t % TPR) * BPT;
 #pragma unroll
-    for (int q = 0; q < BPT; ++q) Bs[k][lds_col<false>(k, jb + q)] = rb[q];
+    for (int q = 0; q < BPT; ++q) Bs[k][lds_col<false, BPT>(k, jb + q)] = rb[q];
   }
 }
 
@@ -134,13 +134,15 @@ __device__ __forceinline__ void tile_stage_mfma(const double (*As)[BM + LPAD],
                                                 int li, int lk, bool use1,
                                                 dbl4 (&acc)[Tile<BM, BK>::MB][2]) {
   constexpr int MB = Tile<BM, BK>::MB;
+  constexpr int APT = Tile<BM, BK>::APT, BPT = Tile<BM, BK>::BPT;
 #pragma unroll
   for (int kk = 0; kk < BK; kk += 4) {
     double av[MB];
 #pragma unroll
-    for (int a = 0; a < MB; ++a) av[a] = As[kk + lk][lds_col<AK>(kk + lk, wi + 16 * a + li)];
-    const double b0 = Bs[kk + lk][lds_col<BKC>(kk + lk, wj + li)];
-    const double b1 = Bs[kk + lk][lds_col<BKC>(kk + lk, wj + 16 + li)];
+    for (int a = 0; a < MB; ++a)
+      av[a] = As[kk + lk][lds_col<AK, APT>(kk + lk, wi + 16 * a + li)];
+    const double b0 = Bs[kk + lk][lds_col<BKC, BPT>(kk + lk, wj + li)];
+    const double b1 = Bs[kk + lk][lds_col<BKC, BPT>(kk + lk, wj + 16 + li)];
 #pragma unroll
     for (int a = 0; a < MB; ++a) {
       acc[a][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], b0, acc[a][0], 0, 0, 0);
