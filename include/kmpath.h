@@ -58,6 +58,14 @@ extern "C" {
 #define KMP_CHECK 2        /* smoothed check loss, any real y                */
 
 #define KMP_FLAG_RESTART 1 /* adaptive (gradient) restart of the momentum    */
+#define KMP_FLAG_REFIT 4   /* full-data refit: every (sigma, tau, lambda) is
+                          fitted on all n points (the fold with an empty
+                          held-out set; Algorithm 1's final refit). V must
+                          be 1 and fold_id is ignored (may be NULL);
+                          outputs keep their [S][Q][V][L] layout with V = 1,
+                          cv_sum and cv_err are zero and selected is not
+                          written. For the margin losses y must hold both
+                          classes.                                         */
 #define KMP_FLAG_GLOBAL_SOLVE 2 /* keep the banded solve's working vector in
                           device memory at every order (it is there anyway
                           above 8192 padded rows per fold, where it does not

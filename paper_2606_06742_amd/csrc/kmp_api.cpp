@@ -250,8 +250,12 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
 
 int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const int32_t* fold,
               int32_t V, int32_t S, int32_t Qn, int32_t Sb, Plan* p) {
-  if (!spec || n < 2 || d < 1 || L < 1 || V < 2 || S < 1 || Qn < 1 || !fold) {
-    set_error("invalid shape arguments");
+  // a refit is one "fold" whose held-out set is empty: V = 1, no fold ids
+  const bool refit = spec && (spec->flags & KMP_FLAG_REFIT) != 0;
+  if (!spec || n < 2 || d < 1 || L < 1 || S < 1 || Qn < 1 ||
+      (refit ? V != 1 : (V < 2 || !fold))) {
+    set_error(refit ? "invalid shape arguments (a full-data refit takes V = 1)"
+                    : "invalid shape arguments");
     return KMP_EINVAL;
   }
   if (spec->loss != KMP_CHECK && Qn != 1) {
@@ -261,7 +265,7 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
   p->n = n; p->d = d; p->V = V; p->S = S; p->Qt = Qn; p->L = L;
   p->nv.assign(V, 0);
   std::vector<int64_t> m(V, 0);
-  for (int64_t i = 0; i < n; ++i) {
+  for (int64_t i = 0; i < n && !refit; ++i) {
     const int32_t f = fold[i];
     if (f < 0 || f >= V) {
       set_error("fold id out of range at index " + std::to_string(i));
@@ -272,7 +276,7 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
   int maxnv = 0;
   int64_t maxm = 0;
   for (int v = 0; v < V; ++v) {
-    if (m[v] == 0) {
+    if (m[v] == 0 && !refit) {
       set_error("fold " + std::to_string(v) + " is empty");
       return KMP_EFOLD;
     }
@@ -502,8 +506,9 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
                  int32_t* status, int32_t* selected, kmp_timings* timings) {
   hipStream_t s = (hipStream_t)stream;
   // ---------------------------------------------------------- validation
-  if (!spec || !X || !y || !sigmas || !lambdas || !fold_id || !alpha || !beta || !objective ||
-      !cv_sum) {
+  const bool refit = spec && (spec->flags & KMP_FLAG_REFIT) != 0;
+  if (!spec || !X || !y || !sigmas || !lambdas || (!fold_id && !refit) || !alpha || !beta ||
+      !objective || !cv_sum) {
     set_error("null pointer argument");
     return KMP_EINVAL;
   }
@@ -603,11 +608,11 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
       return KMP_ENONFINITE;
     }
     if (spec->loss != KMP_CHECK) {
-      std::vector<int64_t> pos(V, 0), neg(V, 0);
+      std::vector<int64_t> pos(V, 0), neg(V, 0);   // held out per fold (none in a refit)
       int64_t tp = 0, tn = 0;
       for (int64_t i = 0; i < n; ++i) {
-        if (hy[i] == 1.0) { pos[fold_id[i]]++; tp++; }
-        else if (hy[i] == -1.0) { neg[fold_id[i]]++; tn++; }
+        if (hy[i] == 1.0) { if (!refit) pos[fold_id[i]]++; tp++; }
+        else if (hy[i] == -1.0) { if (!refit) neg[fold_id[i]]++; tn++; }
         else {
           set_error("labels must be +1 or -1 for hinge and logistic losses");
           return KMP_EINVAL;
@@ -638,7 +643,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   for (int v = 0; v < V; ++v) {
     int k = 0;
     for (int64_t i = 0; i < n; ++i)
-      if (fold_id[i] != v) tidx[(size_t)v * N + k++] = (int32_t)i;
+      if (refit || fold_id[i] != v) tidx[(size_t)v * N + k++] = (int32_t)i;
   }
   KMP_HIP_TRY(hipMemcpyAsync(lay.tidx, tidx, sizeof(int32_t) * (size_t)V * N,
                              hipMemcpyHostToDevice, s));
@@ -647,12 +652,15 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   for (int v = 0; v < V; ++v) {
     int k = 0;
     for (int64_t i = 0; i < n; ++i)
-      if (fold_id[i] == v) hidx[(size_t)v * plan.Mh + k++] = (int32_t)i;
+      if (!refit && fold_id[i] == v) hidx[(size_t)v * plan.Mh + k++] = (int32_t)i;
   }
   KMP_HIP_TRY(hipMemcpyAsync(lay.hidx, hidx, sizeof(int32_t) * (size_t)V * plan.Mh,
                              hipMemcpyHostToDevice, s));
   int32_t* hfold = pin.take<int32_t>(n);
-  std::copy(fold_id, fold_id + n, hfold);
+  if (refit)
+    std::fill(hfold, hfold + n, -1);
+  else
+    std::copy(fold_id, fold_id + n, hfold);
   KMP_HIP_TRY(hipMemcpyAsync(lay.fold, hfold, sizeof(int32_t) * n, hipMemcpyHostToDevice, s));
 
   EventTimer tm(ctx->timing);
@@ -890,7 +898,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   }
   if (iters)
     for (size_t i = 0; i < ncell; ++i) cell_iters += hit[i];
-  if (selected) {
+  if (selected && !refit) {
     for (int si = 0; si < S; ++si)
       for (int q = 0; q < Qn; ++q) {
         int best = -1;

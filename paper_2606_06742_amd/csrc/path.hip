@@ -1320,8 +1320,9 @@ int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
   gt.C = fa.ftrain;
   if ((rc = gemm_split(s, gt, p.zpart, sP)) != 0) return rc;
   // held-out kernel blocks K[H_v, T_v] (into the factor buffer, no longer
-  // needed), then held-out predictions K[H_v, T_v] alpha
-  if ((rc = rbf_blocks(s, fa.X, fa.d, fa.ldx, fa.nrm, fa.hidx, fa.Mh, fa.Mh, fa.tidx, p.N, p.N,
+  // needed), then held-out predictions K[H_v, T_v] alpha (none in a refit)
+  if (fa.Mh > 0 &&
+      (rc = rbf_blocks(s, fa.X, fa.d, fa.ldx, fa.nrm, fa.hidx, fa.Mh, fa.Mh, fa.tidx, p.N, p.N,
                        fa.V, fa.inv2s2, fa.S_b, fa.kh, (int64_t)fa.V * p.N * p.N,
                        (int64_t)p.N * p.N, p.N)) != 0)
     return rc;

@@ -20,6 +20,7 @@ KMP_EINVAL, KMP_EFOLD, KMP_EWORKSPACE, KMP_EHIP, KMP_ENONFINITE = -1, -2, -3, -4
 KMP_HINGE, KMP_LOGISTIC, KMP_CHECK = 0, 1, 2
 KMP_FLAG_RESTART = 1
 KMP_FLAG_GLOBAL_SOLVE = 2
+KMP_FLAG_REFIT = 4
 KMP_NKC = 10
 KERNEL_CLASSES = ("gram", "panel", "panel_wy", "trail_update", "q_form", "precompute", "gemm_f",
                   "gemm_zhat", "update", "finalize")
@@ -208,11 +209,17 @@ class PathRunner:
     """Holds the workspace and output tensors for repeated fits of one problem shape."""
 
     def __init__(self, X, y, loss, sigmas, lambdas, fold_id, V, taus=None, device="cuda",
-                 sigma_batch: Optional[int] = None, kernel_timing=(), **spec_overrides):
+                 sigma_batch: Optional[int] = None, kernel_timing=(), refit: bool = False,
+                 **spec_overrides):
+        """refit=True: every (sigma, tau, lambda) on all n points (fold_id and V
+        are ignored; outputs have V = 1, no CV sums, no selection)."""
         import torch
         self.torch = torch
         self.loss = loss
         self.spec = kmp_default_spec(loss, **spec_overrides)
+        if refit:
+            self.spec.flags |= KMP_FLAG_REFIT
+            fold_id, V = np.zeros(np.shape(X)[0], dtype=np.int32), 1
         self.set_kernel_timing(kernel_timing)
         self.X = torch.as_tensor(np.ascontiguousarray(X), dtype=torch.float64, device=device) \
             if not isinstance(X, torch.Tensor) else X

@@ -92,6 +92,25 @@ def _call(km, loss="hinge", n=20, d=3, sigmas=(1.0,), lambdas=(0.1, 1.0), fold=N
                            fold, V, 0x2000, ws, out, out, out, out, None, None, None, None, None)
 
 
+def test_refit_flag_shapes(km):
+    """A full-data refit (KMP_FLAG_REFIT) is one fold with no held-out rows:
+    it takes V = 1, needs no fold ids, and its workspace holds one group of
+    all n rows per bandwidth; without the flag V = 1 is refused."""
+    w = W.get("C2")
+    spec = km.kmp_default_spec("logistic")
+    spec.flags |= km.KMP_FLAG_REFIT
+    zeros = np.zeros(w.n, dtype=np.int32)
+    b_refit = km.kmp_workspace_bytes(spec, w.n, w.d, w.L, zeros, 1, 3, 1, 3)
+    assert b_refit > 0
+    assert km.kmp_workspace_bytes(spec, w.n, w.d, w.L, zeros, 2, 3, 1, 3) == 0
+    plain = km.kmp_default_spec("logistic")
+    assert km.kmp_workspace_bytes(plain, w.n, w.d, w.L, zeros, 1, 3, 1, 3) == 0
+    fold = km.kmp_make_folds(w.n, w.V, 1)
+    b_cv = km.kmp_workspace_bytes(plain, w.n, w.d, w.L, fold, w.V, 3, 1, 3)
+    # V groups of n(V-1)/V rows against one group of n rows per bandwidth
+    assert b_refit < b_cv
+
+
 def test_fit_path_argument_errors(km):
     assert _call(km, sigmas=(0.0,)) == km.KMP_EINVAL
     assert _call(km, sigmas=(np.inf,)) == km.KMP_EINVAL

@@ -1,0 +1,91 @@
+"""Full-data refit (KMP_FLAG_REFIT; Algorithm 1's final fit on all n points):
+every (sigma, tau, lambda) cell against the oracle's cell solver on the full
+Gram matrix.
+
+Bars as for the CV path: objectives within 1e-8 relative, coefficients
+within 1e-6 of max |alpha|, intercepts within 1e-6 of the oracle's optimal
+interval; no held-out sums (zero) and no selection.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import gram as OG
+from oracle.cell import beta_interval, objective, solve_cell
+from tests.gpu_common import ALPHA_RTOL, OBJ_RTOL, announce, device
+
+pytestmark = pytest.mark.gpu
+
+DELTA = 2.0 ** -6      # final smoothing of the default stages
+
+
+def _refit(inp, loss):
+    import torch
+    from paper_2606_06742_amd import kmpath as km
+    device()
+    taus = inp["taus"] if loss == "check" else None
+    r = km.PathRunner(inp["X"], inp["y"], loss, inp["sigmas"], inp["lambdas"], None, 1,
+                      taus=taus, device="cuda", refit=True, max_iter=20000)
+    sel_before = r.selected.copy()
+    code = r.run()
+    torch.cuda.synchronize()
+    g = r.results()
+    assert code == 0, code
+    assert np.all(g["status"] == 0)
+    assert np.all(g["cv_sum"] == 0.0) and np.all(g["cv_err"] == 0)
+    assert np.array_equal(r.selected, sel_before)          # selection not written
+    return g
+
+
+def _check_cells(g, inp, loss, cells):
+    X, y = inp["X"], inp["y"]
+    worst = {"obj": 0.0, "alpha": 0.0}
+    grams = {}
+    for (s, q, l) in cells:
+        if s not in grams:
+            grams[s] = OG.rbf_gram(X, X, inp["sigmas"][s])
+        K = grams[s]
+        tau = inp["taus"][q] if loss == "check" else None
+        lam = inp["lambdas"][l]
+        a, b, info = solve_cell(K, y, lam, loss, DELTA, tau, tol=1e-13)
+        Fo = objective(K, y, a, b, lam, loss, DELTA, tau)
+        Fg = g["objective"][s, q, 0, l]
+        assert abs(Fg - Fo) <= OBJ_RTOL * abs(Fo), ((s, q, l), Fg, Fo)
+        ag = g["alpha"][s, q, 0, l]
+        err = np.abs(ag - a).max()
+        assert err <= ALPHA_RTOL * np.abs(a).max() + 1e-15, ((s, q, l), err)
+        lo, hi = beta_interval(K, y, a, b, loss, DELTA, tau)
+        bg = g["beta"][s, q, 0, l]
+        btol = ALPHA_RTOL * max(1.0, abs(b))
+        assert lo - btol <= bg <= hi + btol, ((s, q, l), bg, b, lo, hi)
+        worst["obj"] = max(worst["obj"], abs(Fg - Fo) / abs(Fo))
+        worst["alpha"] = max(worst["alpha"], err / np.abs(a).max())
+    return worst
+
+
+@pytest.mark.parametrize("loss", ["hinge", "logistic", "check"])
+def test_refit_small_ragged(loss):
+    """n = 203 (ragged against the 64-row tiles), two bandwidths, six
+    lambdas (two tau levels for the check loss): every cell."""
+    inp = W.small_problem(loss, 203, 5, seed=43, V=5, L=6, lam_lo=-4.0, lam_hi=0.5,
+                          sigma_mults=(0.6, 1.5), taus=(0.25, 0.75))
+    announce(f"refit ragged n=203 loss={loss}")
+    g = _refit(inp, loss)
+    S, Q, _, L = g["objective"].shape
+    worst = _check_cells(g, inp, loss, [(s, q, l) for s in range(S) for q in range(Q) for l in range(L)])
+    print(loss, "refit worst", worst)
+
+
+def test_refit_c2_sampled():
+    """The C2 problem (logistic, n = 2000, three bandwidths, 50 lambdas)
+    refitted on all 2000 points; six cells against the oracle."""
+    inp = W.make_inputs(W.get("C2"))
+    announce("refit C2 full size (logistic, n=2000, 3 sigmas, 50 lambdas)")
+    g = _refit(inp, "logistic")
+    rng = np.random.default_rng(11)
+    S, Q, _, L = g["objective"].shape
+    cells = [(int(rng.integers(S)), 0, int(l)) for l in rng.choice(L, size=6, replace=False)]
+    worst = _check_cells(g, inp, "logistic", cells)
+    t = g["timings"]
+    print("C2 refit worst", worst, "factor_ms", t["factor_ms"], "path_ms", t["path_ms"],
+          "total_ms", t["total_ms"], "iterations", t["iterations"])
