@@ -200,3 +200,33 @@ def test_path_c3_full_size_sampled():
         o["cv_err"][s, q, v, l] = np.count_nonzero(y[H] * fH <= 0)
     worst_cells = compare_cells(g, o, inp, "hinge", cells=cells)
     print("C3 sampled worst", worst_cells, "stationarity / allowance", worst)
+
+
+def test_path_h1_mixture_sampled():
+    """The appendix's mixture-of-Gaussians simulation at n = 1000 (p = 10,
+    5 folds, 50 lambdas, smoothed hinge): ten sampled cells against
+    independent oracle solves."""
+    from oracle.cell import beta_interval
+    w = W.get("H1")
+    inp = W.make_inputs(w)
+    announce("fit_path H1 mixture (hinge, n=1000, 5 folds, 50 lambdas)")
+    g = _gpu(inp, "hinge")
+    y, fold, delta = inp["y"], inp["fold_id"], 2.0 ** -6
+    rng = np.random.default_rng(5)
+    cells = sorted({(0, 0, int(rng.integers(w.V)), int(rng.integers(w.L))) for _ in range(10)})
+    o = {k: np.zeros_like(g[k]) for k in ("alpha", "beta", "objective", "cv_sum", "cv_err")}
+    o["beta_lo"] = np.zeros_like(g["beta"])
+    o["beta_hi"] = np.zeros_like(g["beta"])
+    for (s, q, v, l) in cells:
+        Kv, Kc, T, H = OG.fold_blocks(inp["X"], fold, v, inp["sigmas"][s])
+        lam = inp["lambdas"][l]
+        a, b, info = oracle.solve_cell(Kv, y[T], lam, "hinge", delta)
+        o["alpha"][s, q, v, l][T] = a
+        o["beta"][s, q, v, l] = b
+        o["beta_lo"][s, q, v, l], o["beta_hi"][s, q, v, l] = beta_interval(Kv, y[T], a, b, "hinge", delta)
+        o["objective"][s, q, v, l] = oracle.objective(Kv, y[T], a, b, lam, "hinge", delta)
+        fH = Kc @ a + b
+        o["cv_sum"][s, q, v, l] = oracle.losses.eval_loss("hinge", y[H], fH).sum()
+        o["cv_err"][s, q, v, l] = np.count_nonzero(y[H] * fH <= 0)
+    worst = compare_cells(g, o, inp, "hinge", cells=cells)
+    print("H1 sampled worst", worst, g["timings"])

@@ -59,7 +59,7 @@ def test_median_even_count_half_split():
     assert np.count_nonzero(dists < m) == dists.size // 2
 
 
-@pytest.mark.parametrize("name", ["C1", "C2", "C4"])
+@pytest.mark.parametrize("name", ["C1", "C2", "C4", "H1"])
 def test_workload_shapes(name):
     w = W.get(name)
     X, y = W.make_data(w)
@@ -83,3 +83,22 @@ def test_c1_class_means():
 
 def test_cell_counts():
     assert [W.get(k).cells for k in ["C1", "C2", "C3", "C4", "C5"]] == [50, 750, 1000, 600, 500]
+
+
+def test_mixture_workload_structure():
+    """The appendix mixture (H2, n = 10000): balanced classes; each class
+    mean sits near its centres' mean (mu = 2 on its own half of the
+    coordinates, 0 on the other, up to the spread of ten unit-variance
+    centres); the within-class variance per coordinate is the centres'
+    spread plus sigma = 3."""
+    w = W.get("H2")
+    X, y = W.make_data(w)
+    assert np.count_nonzero(y == 1.0) == w.n // 2
+    Xp, Xn = X[y == 1.0], X[y == -1.0]
+    h = w.d // 2
+    # the mean of ten N(mu, 1) centres has standard deviation 1/sqrt(10)
+    assert np.all(np.abs(Xp[:, :h].mean(0) - 2.0) < 1.3) and np.all(np.abs(Xp[:, h:].mean(0)) < 1.3)
+    assert np.all(np.abs(Xn[:, h:].mean(0) - 2.0) < 1.3) and np.all(np.abs(Xn[:, :h].mean(0)) < 1.3)
+    # variance: 3 from the noise plus about 0.9 from the centres
+    v = np.concatenate([Xp.var(0), Xn.var(0)])
+    assert np.all(v > 3.0) and np.all(v < 6.0)

@@ -151,6 +151,12 @@ WORKLOADS = {
                    "kernel quantile, U(-1,1) features, heteroscedastic t3 noise"),
     "C5": Workload("C5", "hinge", 40000, 28, 5, 20, -6.0, 0.0, (0.5, 1.0, 2.0, 4.0, 8.0), (), 5,
                    "smoothed-hinge SVM, Gaussian + log-normal features, tanh-net labels"),
+    # the mixture-of-Gaussians simulation of the paper's appendix (Fig. 1):
+    # p = 10, 5-fold CV over 50 lambdas, n = 1000 and 10000
+    "H1": Workload("H1", "hinge", 1000, 10, 5, 50, -5.0, 0.0, (1.0,), (), 6,
+                   "smoothed-hinge SVM, two 10-centre Gaussian mixtures (mu = 2, sigma = 3)"),
+    "H2": Workload("H2", "hinge", 10000, 10, 5, 50, -5.0, 0.0, (1.0,), (), 7,
+                   "smoothed-hinge SVM, two 10-centre Gaussian mixtures (mu = 2, sigma = 3)"),
 }
 
 
@@ -196,6 +202,25 @@ def make_data(w: Workload) -> Tuple[np.ndarray, np.ndarray]:
         o = np.tanh(X @ W1.T) @ w2
         e = rng.normal(0.0, 0.5, size=n)
         y = np.where(o + e >= 0.0, 1.0, -1.0)
+    elif w.name in ("H1", "H2"):
+        # class means: mu on one half of the coordinates (first half for +1,
+        # second for -1), zero elsewhere; ten centres per class drawn from
+        # N(mean, I); a point takes one of its class's centres uniformly and
+        # adds N(0, sigma I) with sigma = 3 read as the variance; half the
+        # points in each class
+        mu, var, K = 2.0, 3.0, 10
+        half = d // 2
+        mean_p = np.zeros(d)
+        mean_p[:half] = mu
+        mean_n = np.zeros(d)
+        mean_n[half:] = mu
+        cen_p = mean_p + rng.standard_normal((K, d))
+        cen_n = mean_n + rng.standard_normal((K, d))
+        h = n // 2
+        Xp = cen_p[rng.integers(0, K, size=h)] + np.sqrt(var) * rng.standard_normal((h, d))
+        Xn = cen_n[rng.integers(0, K, size=n - h)] + np.sqrt(var) * rng.standard_normal((n - h, d))
+        X = np.vstack([Xp, Xn])
+        y = np.concatenate([np.ones(h), -np.ones(n - h)])
     else:
         raise KeyError(w.name)
     return np.ascontiguousarray(X, dtype=np.float64), np.ascontiguousarray(y, dtype=np.float64)
