@@ -91,9 +91,13 @@ __device__ __forceinline__ void panel_qr_stream_body(double* __restrict__ A, int
     const double sigma = hs[i];
     double tau = 0.0, beta = alpha, scale = 0.0;
     if (sigma > 0.0) {
-      beta = -copysign(sqrt(alpha * alpha + sigma), alpha);
-      tau = (beta - alpha) / beta;
-      scale = 1.0 / (alpha - beta);
+      // the norm and the two reciprocals are on the step's dependency
+      // chain: hardware estimates refined by Newton-Raphson (IEEE sqrt for
+      // arguments near the bottom of the normal range)
+      const double s2 = fma(alpha, alpha, sigma);
+      beta = -copysign(s2 > 1e-280 ? sqrt_newton(s2) : sqrt(s2), alpha);
+      tau = (beta - alpha) * rcp_newton(beta);
+      scale = rcp_newton(alpha - beta);
     }
     if (t < BB) ws[t] = (t > i) ? fma(scale, hs[t], rowi[t]) : 0.0;   // v_i' P[:, t]
     if (t == 0) taus[(int64_t)g * N + p + i] = tau;
@@ -245,9 +249,13 @@ __device__ __forceinline__ void panel_steps(double (&x)[RS], double (&xi)[RS],
     const double sigma = row_bcast<I>(hc);
     double tau = 0.0, beta = alpha, scale = 0.0;
     if (sigma > 0.0) {
-      beta = -copysign(sqrt(alpha * alpha + sigma), alpha);
-      tau = (beta - alpha) / beta;
-      scale = 1.0 / (alpha - beta);
+      // the norm and the two reciprocals are on the step's dependency
+      // chain: hardware estimates refined by Newton-Raphson (IEEE sqrt for
+      // arguments near the bottom of the normal range)
+      const double s2 = fma(alpha, alpha, sigma);
+      beta = -copysign(s2 > 1e-280 ? sqrt_newton(s2) : sqrt(s2), alpha);
+      tau = (beta - alpha) * rcp_newton(beta);
+      scale = rcp_newton(alpha - beta);
     }
     if (st.t < I) L.z[I][st.t] = L.scl[st.t] * fma(scale, hc, ri[st.t]);   // t < 16: c = t
     if (st.t == 0) {

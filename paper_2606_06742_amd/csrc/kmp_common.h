@@ -141,4 +141,28 @@ __device__ __forceinline__ double loss_eval(int loss, double y, double f, double
   }
 }
 
+// 1/x from the hardware estimate and two Newton-Raphson steps
+// r <- r + r (1 - x r), which square the relative error each; for the
+// positive, normal pivots of the LDL' sweep.
+__device__ __forceinline__ double rcp_newton(double x) {
+  double r = __builtin_amdgcn_rcp(x);
+  double e = fma(-x, r, 1.0);
+  r = fma(r, e, r);
+  e = fma(-x, r, 1.0);
+  return fma(r, e, r);
+}
+
+// sqrt(x) for normal x > 0 by Goldschmidt's iteration (Markstein, IA-64
+// and Elementary Functions, 2000): y ~ sqrt(x) and h ~ 1/(2 sqrt(x)) from
+// the hardware reciprocal square root, one coupled Newton-Raphson step on
+// both, then y corrected by the residual x - y^2.
+__device__ __forceinline__ double sqrt_newton(double x) {
+  const double r = __builtin_amdgcn_rsq(x);
+  double y = x * r, h = 0.5 * r;
+  const double e = fma(-y, h, 0.5);
+  y = fma(y, e, y);
+  h = fma(h, e, h);
+  return fma(fma(-y, y, x), h, y);
+}
+
 }  // namespace kmp

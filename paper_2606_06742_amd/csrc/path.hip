@@ -484,17 +484,6 @@ static int band_apply(hipStream_t s, const PathArrays& p, const double* x, doubl
 }
 
 // ------------------------------------------------------ per-stage factors
-// 1/x from the hardware estimate and two Newton-Raphson steps
-// r <- r + r (1 - x r), which square the relative error each; for the
-// positive, normal pivots of the LDL' sweep.
-__device__ __forceinline__ double rcp_newton(double x) {
-  double r = __builtin_amdgcn_rcp(x);
-  double e = fma(-x, r, 1.0);
-  r = fma(r, e, r);
-  e = fma(-x, r, 1.0);
-  return fma(r, e, r);
-}
-
 // ldl_factor_kernel, one wavefront per column: the blockwise LDL' of
 // M = 2 lambda I + B/(n_v kappa) (stored as above). It reads the band,
 // lambda and n_v only, so a stage's factors can be formed as soon as the
