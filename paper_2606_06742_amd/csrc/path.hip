@@ -494,7 +494,7 @@ static int band_apply(hipStream_t s, const PathArrays& p, const double* x, doubl
 //   C_{I+1} = M_{I+1,I} L^{-T} D^{-1}.
 // The band tile of block I+1 (rows 0 .. 16 of its 16 columns) is loaded
 // while block I is worked on and passes through LDS.
-constexpr int FW = 1;                  // wavefronts (columns) per workgroup
+constexpr int FW = 4;                  // wavefronts (columns) per workgroup
 __global__ __launch_bounds__(64 * FW) void ldl_factor_kernel(
     int N, int C, int64_t cols, const int* __restrict__ nv, const double* __restrict__ band,
     const double* __restrict__ lamv, double kappa, double* __restrict__ Vfac,
