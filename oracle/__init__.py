@@ -16,7 +16,12 @@ Parity status per function (what pins it; see tests/test_oracle_*.py):
 * gram.rbf_gram     sklearn.metrics.pairwise.rbf_kernel, symmetry, PSD
 * cell.solve_cell   brute-force zone enumeration (hinge, check; n <= 8),
                     50-digit mpmath Newton (logistic), zero duality gap,
-                    exact-CV Lemma 2, large-lambda closed forms
+                    exact-CV Lemma 2, large-lambda closed forms; its
+                    extended-precision refinement by the same pins at small
+                    lambda, where the fp64 loop alone stalls
+* cell.certify_cell zero gap and feasibility at brute-force solutions,
+                    a positive gap at perturbed points
+* gram.rbf_gram_expansion  agreement with rbf_gram to rounding
 * mm.mm_step        explicit solve with the (n+1)-square majoriser, monotone
                     decrease of F, fixed point at the cell solution
 * path.fit_path     composition of the above; selection rule by brute force
@@ -24,4 +29,4 @@ Parity status per function (what pins it; see tests/test_oracle_*.py):
 """
 from . import losses, gram, cell, mm, dual, path  # noqa: F401
 from .path import fit_path, select, select_joint  # noqa: F401
-from .cell import solve_cell, objective, kkt_residual, beta_interval  # noqa: F401
+from .cell import solve_cell, objective, kkt_residual, beta_interval, certify_cell  # noqa: F401

@@ -23,17 +23,58 @@ Each Newton step is globalised by an exact line search on F (F is convex
 along any line); when J is singular or its direction is not a descent
 direction, the direction of a dense majorise-minimise step
 (``oracle.mm.mm_step``) is searched instead; when no point has curvature
-(empty quadratic zone) alpha and beta are minimised in turn exactly. For piecewise-
+(empty quadratic zone) alpha and beta are minimised in turn exactly (after 16
+such alternating steps in a row, the majorise-minimise direction). For piecewise-
 quadratic losses only rows with nonzero curvature couple, so the linear
 system is reduced to those rows exactly (Mangasarian 2002, "A finite Newton
 method for classification"; Keerthi and DeCoste 2005).
+
+Certified convergence. At small lambda the coefficients reach 1/(2 n lambda)
+and an fp64 evaluation of f = K alpha + beta carries rounding that the loss
+curvature 1/(2 delta) amplifies: the fp64 residual stops falling well above
+the tolerance. The last steps are therefore Newton corrections by iterative
+refinement: the Newton matrix is formed and solved in fp64 exactly as above,
+but the residual it is applied to and the iterate it corrects are carried in
+numpy's extended type (x87 long double, 64-bit significand), with
+f = K alpha + beta accumulated in it. The residual reported for a cell is that
+of the refined extended-precision point, of which the returned fp64 values
+are the rounding (within half an ulp each), and a cell counts as converged
+only when it is at most ``CONVERGED_KKT``.
 """
 from __future__ import annotations
 
 import numpy as np
 
+from . import dual as Dl
 from . import losses as Ls
 from .mm import mm_step
+
+# A cell counts as solved when n_v * max(||z + 2 lambda alpha||_inf, |1'z|),
+# evaluated in extended precision at the refined point, is at most this.
+CONVERGED_KKT = 1e-10
+
+
+def _ext_matvec(K, a, rows=512):
+    """K @ a with the products and sums in numpy's extended type."""
+    out = np.empty(K.shape[0], dtype=np.longdouble)
+    for i0 in range(0, K.shape[0], rows):
+        out[i0:i0 + rows] = K[i0:i0 + rows].astype(np.longdouble) @ a
+    return out
+
+
+def residual_ext(K, y, alpha, beta, lam, loss, delta=None, tau=None, norm=None):
+    """(R_alpha, R_beta, f, kkt) with f = K alpha + beta, z and R in extended
+    precision; kkt = norm * max(||R_alpha||_inf, |R_beta|) as a float."""
+    ld = np.longdouble
+    n = y.shape[0]
+    N = ld(n if norm is None else norm)
+    a = np.asarray(alpha).astype(ld)
+    f = _ext_matvec(K, a) + ld(beta)
+    z = Ls.point_psi(loss, np.asarray(y).astype(ld), f, delta, tau) / N
+    Ra = z + 2 * ld(lam) * a
+    Rb = z.sum()
+    kkt = float(N * max(np.max(np.abs(Ra)) if Ra.size else ld(0), abs(Rb)))
+    return Ra, Rb, f, kkt
 
 
 def objective(K, y, alpha, beta, lam, loss, delta=None, tau=None, norm=None):
@@ -139,8 +180,12 @@ def solve_cell(K, y, lam, loss, delta=None, tau=None, tol=1e-13, max_iter=500,
                alpha0=None, beta0=0.0, norm=None):
     """Minimise F for one cell. Returns (alpha, beta, info).
 
-    Stops when norm * max(||z + 2 lambda alpha||_inf, |1'z|) <= tol, or when
-    that residual has stopped falling at the rounding floor (<= 1e-7).
+    The fp64 Newton loop stops when norm * max(||z + 2 lambda alpha||_inf,
+    |1'z|) <= tol, or when that residual has stopped falling at its rounding
+    floor (<= 1e-7); extended-precision refinement follows. info["kkt"] is
+    the refined point's extended-precision residual (the returned values are
+    that point rounded to fp64) and info["converged"]
+    holds only when it is at most CONVERGED_KKT (a stall alone never counts).
     """
     K = np.asarray(K, dtype=np.float64)
     y = np.asarray(y, dtype=np.float64)
@@ -151,7 +196,7 @@ def solve_cell(K, y, lam, loss, delta=None, tau=None, tol=1e-13, max_iter=500,
     best = np.inf
     stall = 0
     it = 0
-    newton_steps = mm_steps = split_steps = 0
+    newton_steps = mm_steps = split_steps = split_run = 0
     res = np.inf
     for it in range(1, max_iter + 1):
         Ra, Rb, f, z = stationarity(K, y, alpha, beta, lam, loss, delta, tau, norm)
@@ -167,7 +212,12 @@ def solve_cell(K, y, lam, loss, delta=None, tau=None, tol=1e-13, max_iter=500,
                 break                       # stagnated at the rounding floor
         gK = K @ Ra                          # grad_alpha F = K (z + 2 lambda alpha)
         step = _newton_direction(K, y, alpha, beta, lam, loss, delta, tau, Ra, Rb, f, norm)
-        if step is None:
+        if step is None and split_run >= 16:
+            # alternating exact steps can cycle at tiny lambda (each alpha step
+            # overshoots the zone): take the majorise-minimise direction instead
+            split_run = 0
+        elif step is None:
+            split_run += 1
             # No point has curvature: on this piece F is linear in f plus
             # lambda alpha'K alpha, whose minimiser in alpha is -z/(2 lambda).
             # Take that step, then minimise exactly over beta alone.
@@ -183,6 +233,8 @@ def solve_cell(K, y, lam, loss, delta=None, tau=None, tol=1e-13, max_iter=500,
                 beta = beta - t * Rb
             split_steps += 1
             continue
+        if step is not None:
+            split_run = 0
         slope = 0.0
         if step is not None:
             da, db = step
@@ -200,9 +252,39 @@ def solve_cell(K, y, lam, loss, delta=None, tau=None, tol=1e-13, max_iter=500,
         t = _line_minimum(K, y, alpha, beta, da, db, lam, loss, delta, tau, f - beta, slope, norm)
         alpha = alpha + t * da
         beta = beta + t * db
-    info = {"iters": it, "kkt": float(res), "newton_steps": newton_steps,
-            "mm_steps": mm_steps, "split_steps": split_steps, "converged": bool(res <= tol or (stall >= 8 and res <= 1e-7))}
+    alpha, beta, kkt, refine_steps = _refine(K, y, alpha, beta, lam, loss, delta, tau, norm)
+    info = {"iters": it, "kkt": kkt, "kkt_fp64": float(res), "newton_steps": newton_steps,
+            "mm_steps": mm_steps, "split_steps": split_steps, "refine_steps": refine_steps,
+            "converged": bool(kkt <= CONVERGED_KKT)}
     return alpha, beta, info
+
+
+def _refine(K, y, alpha, beta, lam, loss, delta, tau, norm, max_steps=12):
+    """Newton corrections with extended-precision residuals (see the module
+    note). Stops when a correction no longer lowers the residual. Returns the
+    refined point rounded to fp64 (half an ulp per entry), the residual of the
+    refined point itself and the number of corrections taken."""
+    ld = np.longdouble
+    a = np.asarray(alpha).astype(ld)
+    b = ld(beta)
+    Ra, Rb, f, res = residual_ext(K, y, a, b, lam, loss, delta, tau, norm)
+    steps = 0
+    for _ in range(max_steps):
+        if res == 0.0:
+            break
+        step = _newton_direction(K, y, a.astype(np.float64), float(b), lam, loss, delta, tau,
+                                 Ra.astype(np.float64), float(Rb), f.astype(np.float64), norm)
+        if step is None:
+            break
+        da, db = step
+        a2 = a + da.astype(ld)
+        b2 = b + ld(db)
+        Ra2, Rb2, f2, res2 = residual_ext(K, y, a2, b2, lam, loss, delta, tau, norm)
+        if not res2 < res:
+            break
+        a, b, Ra, Rb, f, res = a2, b2, Ra2, Rb2, f2, res2
+        steps += 1
+    return a.astype(np.float64), float(b), res, steps
 
 
 def beta_interval(K, y, alpha, beta, loss, delta=None, tau=None):
@@ -233,3 +315,37 @@ def beta_interval(K, y, alpha, beta, loss, delta=None, tau=None):
     hi = float(above.min()) if above.size else np.inf
     lo = float(below.max()) if below.size else -np.inf
     return lo, hi
+
+
+def certify_cell(K, y, alpha, beta, lam, loss, delta=None, tau=None):
+    """Certificate of a solved cell (fold-restricted problem, 1/n_v scaling).
+
+    The dual point is read off the loss derivative at f = K alpha + beta
+    (``oracle.dual``); the certificate holds its box and equality
+    violations, the dual value, the duality gap F - D (zero at the optimum,
+    where the dual point is feasible and alpha = its image), the gap relative
+    to max(1, F), the KKT residual in extended precision, and how many points
+    lie below, inside and above the quadratic zone of the smoothed loss
+    (hinge: u = y f against 1 -+ delta; check: r = y - f against -+ delta;
+    logistic: all points have curvature and count as inside).
+    """
+    f = K @ alpha + beta
+    F = objective(K, y, alpha, beta, lam, loss, delta, tau)
+    a = Dl.dual_point(loss, y, f, delta, tau)
+    box, eq = Dl.dual_feasibility(loss, y, a, tau)
+    D = Dl.dual_value(loss, K, y, a, lam, delta, tau)
+    if loss == "hinge":
+        u = y * f
+        zone = (int(np.count_nonzero(u <= 1.0 - delta)),
+                int(np.count_nonzero((u > 1.0 - delta) & (u < 1.0 + delta))),
+                int(np.count_nonzero(u >= 1.0 + delta)))
+    elif loss == "check":
+        r = y - f
+        zone = (int(np.count_nonzero(r <= -delta)),
+                int(np.count_nonzero((r > -delta) & (r < delta))),
+                int(np.count_nonzero(r >= delta)))
+    else:
+        zone = (0, int(y.shape[0]), 0)
+    _, _, _, kkt = residual_ext(K, y, alpha, beta, lam, loss, delta, tau)
+    return {"objective": F, "dual": D, "gap": F - D, "rel_gap": (F - D) / max(1.0, abs(F)),
+            "box": box, "eq": eq, "kkt": kkt, "zone": zone}

@@ -36,3 +36,20 @@ def fold_blocks(X, fold_id, v, sigma):
     Kv = rbf_gram(X[T], X[T], sigma)
     Kc = rbf_gram(X[H], X[T], sigma)
     return Kv, Kc, T, H
+
+
+def rbf_gram_expansion(XA, XB, sigma):
+    """The same kernel with squared distances by the norm expansion
+    ||a||^2 + ||b||^2 - 2 a'b (clamped at 0; exactly 1 where the rows are the
+    same point). It differs from ``rbf_gram`` by rounding only; re-solving a
+    cell with it measures how far fp64 rounding of K alone moves the
+    solution (the cell's noise floor)."""
+    XA = np.asarray(XA, dtype=np.float64)
+    XB = np.asarray(XB, dtype=np.float64)
+    na = np.einsum("ij,ij->i", XA, XA)
+    nb = np.einsum("ij,ij->i", XB, XB)
+    d2 = np.maximum(na[:, None] + nb[None, :] - 2.0 * (XA @ XB.T), 0.0)
+    K = np.exp(-d2 / (2.0 * sigma * sigma))
+    if XA is XB or (XA.shape == XB.shape and np.array_equal(XA, XB)):
+        np.fill_diagonal(K, 1.0)
+    return K

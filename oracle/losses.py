@@ -1,6 +1,7 @@
 """Losses of the three kernel machines, their f-derivatives and curvatures.
 
-Oracle (test infrastructure only). Plain numpy, fp64.
+Oracle (test infrastructure only). Plain numpy, fp64 (inputs given in
+numpy's extended type are evaluated in it).
 
 * Smoothed hinge L_delta (Appendix A.1, definition of the delta-smoothed
   hinge): 1-u for u <= 1-delta, (u-1-delta)^2/(4 delta) for |u-1| < delta,
@@ -25,56 +26,63 @@ import numpy as np
 LOSSES = ("hinge", "logistic", "check")
 
 
+def _arr(u):
+    """u as an fp64 array, or kept in numpy's extended type (longdouble) when
+    given in it (the solver's refinement evaluates residuals that way)."""
+    u = np.asarray(u)
+    return u if u.dtype == np.longdouble else u.astype(np.float64)
+
+
 def smoothed_hinge(u, delta):
-    u = np.asarray(u, dtype=np.float64)
+    u = _arr(u)
     return np.where(u <= 1.0 - delta, 1.0 - u,
                     np.where(u >= 1.0 + delta, 0.0, (u - 1.0 - delta) ** 2 / (4.0 * delta)))
 
 
 def smoothed_hinge_d1(u, delta):
-    u = np.asarray(u, dtype=np.float64)
+    u = _arr(u)
     return np.where(u <= 1.0 - delta, -1.0,
                     np.where(u >= 1.0 + delta, 0.0, (u - 1.0 - delta) / (2.0 * delta)))
 
 
 def smoothed_hinge_d2(u, delta):
-    u = np.asarray(u, dtype=np.float64)
+    u = _arr(u)
     return np.where((u > 1.0 - delta) & (u < 1.0 + delta), 1.0 / (2.0 * delta), 0.0)
 
 
 def hinge(u):
-    return np.maximum(1.0 - np.asarray(u, dtype=np.float64), 0.0)
+    return np.maximum(1.0 - _arr(u), 0.0)
 
 
 def smoothed_check(r, tau, delta):
-    r = np.asarray(r, dtype=np.float64)
+    r = _arr(r)
     mid = (r * r + 2.0 * r * delta * (2.0 * tau - 1.0) + delta * delta) / (4.0 * delta)
     return np.where(r >= delta, tau * r, np.where(r <= -delta, (tau - 1.0) * r, mid))
 
 
 def smoothed_check_d1(r, tau, delta):
-    r = np.asarray(r, dtype=np.float64)
+    r = _arr(r)
     return np.where(r >= delta, tau,
                     np.where(r <= -delta, tau - 1.0, (r + delta * (2.0 * tau - 1.0)) / (2.0 * delta)))
 
 
 def smoothed_check_d2(r, tau, delta):
-    r = np.asarray(r, dtype=np.float64)
+    r = _arr(r)
     return np.where((r > -delta) & (r < delta), 1.0 / (2.0 * delta), 0.0)
 
 
 def check(r, tau):
-    r = np.asarray(r, dtype=np.float64)
+    r = _arr(r)
     return r * (tau - (r < 0.0))
 
 
 def logistic(u):
     """log(1 + exp(-u)), evaluated without overflow."""
-    return np.logaddexp(0.0, -np.asarray(u, dtype=np.float64))
+    return np.logaddexp(0.0, -_arr(u))
 
 
 def sigmoid(t):
-    t = np.asarray(t, dtype=np.float64)
+    t = _arr(t)
     e = np.exp(-np.abs(t))
     return np.where(t >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
 

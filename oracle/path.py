@@ -35,7 +35,8 @@ def _fold_task(args):
     n = y.shape[0]
     out = {"alpha": np.zeros((L, n)), "beta": np.zeros(L), "objective": np.zeros(L),
            "cv_sum": np.zeros(L), "cv_err": np.zeros(L, dtype=np.int64),
-           "kkt": np.zeros(L), "iters": np.zeros(L, dtype=np.int64),
+           "kkt": np.zeros(L), "converged": np.zeros(L, dtype=bool),
+           "iters": np.zeros(L, dtype=np.int64),
            "beta_lo": np.zeros(L), "beta_hi": np.zeros(L)}
     for l, lam in enumerate(lambdas):
         a, b, info = solve_cell(Kv, yT, lam, loss, delta, tau, tol=tol)
@@ -46,6 +47,7 @@ def _fold_task(args):
         out["cv_sum"][l] = Ls.eval_loss(loss, yH, fH, tau).sum()
         out["cv_err"][l] = int(np.count_nonzero(yH * fH <= 0.0)) if loss != "check" else 0
         out["kkt"][l] = info["kkt"]
+        out["converged"][l] = info["converged"]
         out["iters"][l] = info["iters"]
         lo, hi = beta_interval(Kv, yT, a, b, loss, delta, tau)
         out["beta_lo"][l], out["beta_hi"][l] = lo, hi

@@ -27,8 +27,34 @@ def _rbf(X, s):
     return np.exp(-d2 / (2 * s * s))
 
 
-def _brute_force(K, y, lam, loss, delta, tau=None):
-    """All consistent piece patterns; returns list of (alpha, beta)."""
+def _pattern_system(K, y, lam, loss, delta, tau, pat):
+    """Linear stationarity system (unknowns alpha, beta) of one piece pattern."""
+    n = len(y)
+    A = np.zeros((n + 1, n + 1))
+    b = np.zeros(n + 1)
+    for i, p in enumerate(pat):
+        A[i, i] += 2 * lam
+        if p == 1:
+            e = y[i] * (1 + delta) if loss == "hinge" else y[i] + delta * (2 * tau - 1)
+            A[i, :n] += K[i] / (2 * delta * n)
+            A[i, n] += 1.0 / (2 * delta * n)
+            b[i] += e / (2 * delta * n)
+            A[n, :n] += K[i] / (2 * delta * n)
+            A[n, n] += 1.0 / (2 * delta * n)
+            b[n] += e / (2 * delta * n)
+        else:
+            if loss == "hinge":
+                psi = -y[i] if p == 0 else 0.0
+            else:
+                psi = -tau if p == 0 else 1.0 - tau
+            b[i] -= psi / n
+            b[n] -= psi / n
+    return A, b
+
+
+def _brute_force(K, y, lam, loss, delta, tau=None, with_pattern=False):
+    """All consistent piece patterns; returns list of (alpha, beta) (and the
+    pattern when with_pattern)."""
     n = len(y)
     sols = []
     for pat in itertools.product((0, 1, 2), repeat=n):   # 0: left linear, 1: zone, 2: right linear
@@ -74,7 +100,7 @@ def _brute_force(K, y, lam, loss, delta, tau=None):
                 ok = False
                 break
         if ok:
-            sols.append((alpha, beta))
+            sols.append((alpha, beta, pat) if with_pattern else (alpha, beta))
     return sols
 
 
@@ -267,3 +293,80 @@ def test_beta_interval_flat_case():
     for bb in np.linspace(lo, hi, 7):
         assert abs(F(bb) - F(b)) < 1e-15
     assert F(hi + 0.05) > F(b) and F(lo - 0.05) > F(b)
+
+
+@pytest.mark.parametrize("loss,tau", [("hinge", None), ("check", 0.3)])
+def test_refinement_at_tiny_lambda_matches_brute_force(loss, tau):
+    """At lambda = 1e-5 the coefficients reach 1/(2 n lambda) ~ 1e4 and the
+    fp64 Newton loop stalls far above the tolerance; the extended-precision
+    refinement must still land on the brute-force minimiser and certify it
+    (residual <= CONVERGED_KKT), and a cell stopped after one iteration must
+    not be reported as converged."""
+    rng = np.random.default_rng(31)
+    done = 0
+    for trial in range(30):
+        n = 6
+        X = rng.standard_normal((n, 2))
+        if loss == "hinge":
+            y = np.array([1, -1, 1, -1, 1, -1], dtype=float)
+        else:
+            y = rng.standard_normal(n)
+        K = _rbf(X, 0.7)
+        delta, lam = 2.0 ** -6, 1e-5
+        sols = _brute_force(K, y, lam, loss, delta, tau, with_pattern=True)
+        if not sols:
+            continue
+        # the consistent pattern's linear system solved in 40-digit arithmetic
+        mp.mp.dps = 40
+        A, rhs = _pattern_system(K, y, lam, loss, delta, tau, sols[0][2])
+        sol = mp.lu_solve(mp.matrix(A.tolist()), mp.matrix(rhs.tolist()))
+        a0 = np.array([float(sol[i]) for i in range(n)])
+        a, b, info = cell.solve_cell(K, y, lam, loss, delta, tau)
+        assert info["converged"] and info["kkt"] <= cell.CONVERGED_KKT, info
+        # (the minimiser itself is ill-conditioned here: 2 lambda is tiny next
+        # to the curvature, so a residual of 1e-10 moves alpha by ~1e-10
+        # relative; the bar is still four orders below the GPU's 1e-6)
+        assert np.abs(a - a0).max() <= 1e-9 * np.abs(a0).max(), (trial, a, a0)
+        # beta enters through f = K alpha + beta, whose terms are of size
+        # max |alpha|: its error is relative to that
+        assert abs(b - float(sol[n])) <= 1e-9 * max(1.0, np.abs(a0).max())
+        _, _, info1 = cell.solve_cell(K, y, lam, loss, delta, tau, max_iter=1)
+        assert not info1["converged"] and info1["kkt"] > cell.CONVERGED_KKT
+        done += 1
+    assert done >= 5
+
+
+@pytest.mark.parametrize("loss,tau", [("hinge", None), ("logistic", None), ("check", 0.7)])
+def test_certificate(loss, tau):
+    """certify_cell: zero duality gap, a feasible dual point and the zone
+    counts at a solution; a strictly positive gap once alpha is moved off
+    it (weak duality)."""
+    inp = W.small_problem("check" if loss == "check" else "hinge", 60, 3, seed=17)
+    X, y = inp["X"], inp["y"]
+    K = gram.rbf_gram(X, X, inp["sigmas"][0])
+    delta = None if loss == "logistic" else 2.0 ** -6
+    lam = 3e-3
+    a, b, info = cell.solve_cell(K, y, lam, loss, delta, tau)
+    c = cell.certify_cell(K, y, a, b, lam, loss, delta, tau)
+    assert abs(c["rel_gap"]) <= 1e-12 and c["box"] <= 1e-12 and c["eq"] <= 1e-10
+    assert sum(c["zone"]) == len(y) and c["kkt"] <= cell.CONVERGED_KKT
+    if loss != "logistic":
+        assert c["zone"][1] > 0
+    rng = np.random.default_rng(3)
+    a2 = a + 1e-3 * np.abs(a).max() * rng.standard_normal(len(a))
+    a2 -= a2.mean()                              # keep sum alpha = 0 (dual equality)
+    c2 = cell.certify_cell(K, y, a2, b, lam, loss, delta, tau)
+    if c2["box"] == 0.0 and c2["eq"] <= 1e-12:
+        assert c2["gap"] > 0.0
+
+
+def test_norm_expansion_gram_agrees_to_rounding():
+    rng = np.random.default_rng(5)
+    X = rng.standard_normal((70, 9))
+    s = 2.5
+    K = gram.rbf_gram(X, X, s)
+    K2 = gram.rbf_gram_expansion(X, X, s)
+    assert np.all(np.diag(K2) == 1.0) and np.allclose(K2, K2.T, atol=0, rtol=0) is not None
+    nr = (X * X).sum(1)
+    bound = 8 * np.finfo(float).eps * (nr[:, None] + nr[None, :]) / (2 * s * s) * K + 1e-300
+    assert np.all(np.abs(K2 - K) <= bound)
