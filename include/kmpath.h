@@ -66,6 +66,18 @@ extern "C" {
                           cv_sum and cv_err are zero and selected is not
                           written. For the margin losses y must hold both
                           classes.                                         */
+#define KMP_FLAG_SHARED_FACTOR 8 /* exact CV with one factorisation of the full
+                          K per bandwidth (Appendix A.2, exact cross-validation
+                          formula; Algorithm 1's single decomposition): the
+                          problem of fold v is solved as the n-point problem
+                          whose held-out points carry no loss (zero response
+                          weight), with the loss normalised by n_v; its
+                          minimiser is the fold solution with zero
+                          coefficients on the held-out points (the paper's
+                          Lemma 2). Every (tau, fold, lambda) is a column on
+                          the one factor. Same outputs as the per-fold mode;
+                          n <= 40960. With V = n and fold_id[i] = i this is
+                          exact leave-one-out CV (Algorithm 1 as printed).  */
 #define KMP_FLAG_GLOBAL_SOLVE 2 /* keep the banded solve's working vector in
                           device memory at every order (it is there anyway
                           above 8192 padded rows per fold, where it does not
@@ -95,7 +107,8 @@ typedef struct {
                           |1'z|) <= tol at the extrapolated point (1e-9)    */
   int32_t max_iter;    /* iterations per stage per cell (100000)            */
   int32_t poll_every;  /* iterations between host convergence polls (8)     */
-  int32_t flags;       /* KMP_FLAG_RESTART (default on), KMP_FLAG_GLOBAL_SOLVE */
+  int32_t flags;       /* KMP_FLAG_RESTART (default on), KMP_FLAG_GLOBAL_SOLVE,
+                          KMP_FLAG_REFIT, KMP_FLAG_SHARED_FACTOR            */
   int32_t timing_mask; /* kernel classes to time with HIP events (default 0) */
   int32_t timing_every;/* bracket one launch in every timing_every launches
                           of a timed class (default 1: all)                 */
@@ -154,7 +167,12 @@ size_t kmp_workspace_bytes(const kmp_path_spec* spec, int64_t n, int64_t d,
  *   iters    [S][Q][V][L]   iterations summed over stages; may be NULL
  *   status   [S][Q][V][L]   0 converged, 1 max_iter, 2 non-finite; may be NULL
  *   selected HOST [S][Q]: argmin_l sum_v cv_sum/n, ties to larger lambda; may be NULL
+ *   selected_joint HOST [Q][2]: the (s, l) minimising sum_v cv_sum/n over all
+ *            bandwidths and penalties, ties to the larger lambda, then the
+ *            larger sigma; may be NULL
  *   timings  HOST, may be NULL
+ * The return code reports cells that stopped at max_iter (KMP_WMAXITER) or
+ * went non-finite (KMP_ENONFINITE) whether or not `status` is given.
  * Synchronises `stream` before returning.                                   */
 int kmp_fit_path(void* stream, const kmp_path_spec* spec,
                  const double* X, int64_t n, int64_t d, int64_t ldx,
@@ -166,7 +184,8 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec,
                  void* workspace, size_t workspace_bytes,
                  double* alpha, double* beta, double* objective,
                  double* cv_sum, int32_t* cv_err, int32_t* iters,
-                 int32_t* status, int32_t* selected, kmp_timings* timings);
+                 int32_t* status, int32_t* selected, int32_t* selected_joint,
+                 kmp_timings* timings);
 
 /* Random V-fold assignment (HOST output fold_id, n entries): SplitMix64
  * (Steele, Lea & Flood 2014) seeded with `seed` drives a Fisher-Yates
@@ -174,7 +193,10 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec,
  * fold_id[perm[i]] = i mod V. Integer-only and reproducible.             */
 int kmp_make_folds(int64_t n, int32_t V, uint64_t seed, int32_t* fold_id);
 
-/* a1 on its own: RBF blocks K_s[i][j] = exp(-max(0, |x_r|^2 + |x_c|^2 -
+/* a1 on its own: the RBF kernel matrix of the paper's kernel="rbf" models
+ * (Section 2's API; the kernel matrix K of eq. (kernelsvm), Appendix A.1),
+ * parameterised as K(x, x') = exp(-||x - x'||^2 / (2 sigma^2)), in blocks
+ * K_s[i][j] = exp(-max(0, |x_r|^2 + |x_c|^2 -
  * 2 x_r.x_c) / (2 sigma_s^2)) with r = rows[i], c = cols[j] (DEVICE int32
  * index lists into X), exactly 1 where r == c, and 0 where either index is
  * negative (padding). out DEVICE, S blocks of m x p row-major with leading
@@ -202,9 +224,43 @@ int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N,
  * (first stage of the successive band reduction, Bischof, Lang & Sun 2000):
  * panel QR, compact-WY two-sided trailing updates on matrix cores, Q
  * accumulated in compact-WY blocks. N must be a multiple of 64 in
- * [64, 32768]; zero padding rows are allowed.                             */
+ * [64, 40960]; zero padding rows are allowed.                             */
 #define KMP_BAND 16
 int kmp_band_reduce(void* stream, double* A, int32_t G, int32_t N, double* Qout, double* band);
+
+/* a4-a7 on their own: one majorise-minimise step of the path from a
+ * caller-given state, for C columns of one problem (Appendix A.1, the update
+ * (beta, alpha) <- (beta, alpha) - H^{-1} (1'z ; K z + 2 lambda K alpha),
+ * z_i = psi(y_i, f_i)/n, f = K alpha + beta; H applied through the block
+ * form of its inverse of Appendix A.3, here in the band basis of K's
+ * factorisation K = Q B Q'). Column c has penalty lambdas[c] (and level
+ * taus[c] for KMP_CHECK); the curvature bound is 1/kappa with kappa = 2 delta
+ * (hinge, check) or 4 (logistic, delta ignored). No extrapolation: the step
+ * is taken from the given point itself.
+ *   K         DEVICE, n x n row-major symmetric kernel matrix (not modified;
+ *             it is factorised into library scratch, stream-ordered)
+ *   y         DEVICE, n labels (+/-1 for hinge and logistic)
+ *   lambdas   HOST, C penalties > 0; taus HOST, C levels in (0,1) (check
+ *             loss only, else may be NULL)
+ *   alpha_in  DEVICE [C][n], beta_in DEVICE [C]: the states
+ *   alpha_out DEVICE [C][n], beta_out DEVICE [C]: the states after the step
+ *   kkt_out   DEVICE [C] or NULL: n max(||Q'(z + 2 lambda alpha)||_2, |1'z|)
+ *             at the given state
+ * n <= 32768, C <= 65535. Synchronises `stream`; KMP_EINVAL on bad
+ * arguments (nothing written), KMP_EHIP on runtime errors.                  */
+int kmp_path_step(void* stream, int32_t loss, double delta, const double* K, int64_t n,
+                  const double* y, const double* lambdas, const double* taus, int32_t C,
+                  const double* alpha_in, const double* beta_in, double* alpha_out,
+                  double* beta_out, double* kkt_out);
+
+/* The path's dense products on their own (a4 f = Q (B abar) and a6
+ * zhat = Q' z are such products, Appendix A.3: every iteration is O(n^2)
+ * matrix products): C_g = A_g B_g for g < G, fp64 on the matrix cores.
+ * A DEVICE, G blocks of M x K row-major at A + g*M*K; B DEVICE, K x N
+ * row-major at B + g*K*N; C DEVICE, M x N row-major at C + g*M*N
+ * (overwritten; zero when K = 0). G <= 65535. Synchronises `stream`.       */
+int kmp_dgemm_grouped(void* stream, int32_t G, int32_t M, int32_t N, int32_t K,
+                      const double* A, const double* B, double* C);
 
 /* Message for a return code, or the last HIP error text for KMP_EHIP. */
 const char* kmp_strerror(int code);

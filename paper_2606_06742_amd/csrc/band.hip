@@ -1144,8 +1144,9 @@ __global__ __launch_bounds__(256) void wy_apply_pair_kernel(
 int band_reduce(hipStream_t s, const BandWork& wk) {
   const int G = wk.G, N = wk.N;
   if (G <= 0) return 0;
-  if (N % 64 != 0 || N < 64 || N > kMaxOrder) {
-    set_error("band_reduce: N must be a multiple of 64 in [64, " + std::to_string(kMaxOrder) + "]");
+  if (N % 64 != 0 || N < 64 || N > kMaxSharedOrder) {
+    set_error("band_reduce: N must be a multiple of 64 in [64, " + std::to_string(kMaxSharedOrder) +
+              "]");
     return KMP_EINVAL;
   }
   int rc;

@@ -287,10 +287,12 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
   const int w = threadIdx.x >> 6;
   const int wi = (w & 1) * (BM / 2), wj = (w >> 1) * 32;
   const int nv = e.nv[b];
-  const double inv_nv = 1.0 / (double)nv;
   const double* y = e.y + (int64_t)b * e.sy;
   const double* bbar = e.bbar + (int64_t)b * e.sbb;
   const double* tau = e.tau + (int64_t)b * e.stau;
+  const int* cnv = e.cnv + (int64_t)b * e.sbb;
+  const int32_t* rfold = e.rfold ? e.rfold + (int64_t)b * e.sy : nullptr;
+  const int32_t* cfold = e.cfold ? e.cfold + (int64_t)b * e.sbb : nullptr;
   double colsum[2] = {0.0, 0.0};
 #pragma unroll
   for (int bj = 0; bj < 2; ++bj) {
@@ -298,6 +300,8 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
     const bool cj = gj < N;
     const double bb = cj ? bbar[gj] : 0.0;
     const double tj = cj ? tau[gj] : 0.0;
+    const double inv_nv = cj ? 1.0 / (double)cnv[gj] : 0.0;
+    const int32_t hf = (cj && cfold) ? cfold[gj] : -1;
 #pragma unroll
     for (int bi = 0; bi < MB; ++bi)
 #pragma unroll
@@ -305,7 +309,8 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
         const int gi = i0 + wi + bi * 16 + mfma_row(lane, r);
         if (gi < M && cj) {
           double z = 0.0;
-          if (gi < nv) z = loss_psi(e.loss, y[gi], acc[bi][bj][r] + bb, e.delta, tj) * inv_nv;
+          if (gi < nv && !(rfold && rfold[gi] == hf))
+            z = loss_psi(e.loss, y[gi], acc[bi][bj][r] + bb, e.delta, tj) * inv_nv;
           C[(int64_t)gj * ldc + gi] = z;
           colsum[bj] += z;
         }
@@ -384,7 +389,8 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
 
 // Loss epilogue over split-K partials of f: for row i < M of batch b and
 // active column c = cmap[b*N + k], k < nact[b], F = sum_s part_s[c][i] +
-// bbar[c]; Z[c][i] = psi(y_i, F)/nv (0 at padding rows); partial[b][tile][c]
+// bbar[c]; Z[c][i] = psi(y_i, F)/cnv[c] (0 at padding rows and at rows held
+// out of column c); partial[b][tile][c]
 // = sum of Z over the 64 rows of the tile (lanes = rows, so the column sums
 // are wave reductions). Wave w of workgroup (tile, j, b) takes the active
 // column k = 4 j + w.
@@ -398,19 +404,21 @@ __global__ __launch_bounds__(256) void loss_epilogue_kernel(int M, int N, int S,
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int i = blockIdx.x * 64 + lane;
   const int nv = e.nv[b];
-  const double inv_nv = 1.0 / (double)nv;
   const double yi = (i < nv) ? e.y[(int64_t)b * e.sy + i] : 0.0;
+  const int32_t fi = (e.rfold && i < nv) ? e.rfold[(int64_t)b * e.sy + i] : -2;
   const double* bbar = e.bbar + (int64_t)b * e.sbb;
   const double* tau = e.tau + (int64_t)b * e.stau;
   const int* cmap = cmap_all + (int64_t)b * N;
   const int k = 4 * (int)blockIdx.y + w;
   if (k < nact[b]) {
     const int c = cmap[k];
+    const double inv_nv = 1.0 / (double)e.cnv[(int64_t)b * e.sbb + c];
+    const bool held = e.cfold && fi == e.cfold[(int64_t)b * e.sbb + c];
     double z = 0.0;
     if (i < M) {
       double f = 0.0;
       for (int sk = 0; sk < S; ++sk) f += part[(int64_t)sk * sP + (int64_t)b * sC + (int64_t)c * ldc + i];
-      if (i < nv) z = loss_psi(e.loss, yi, f + bbar[c], e.delta, tau[c]) * inv_nv;
+      if (i < nv && !held) z = loss_psi(e.loss, yi, f + bbar[c], e.delta, tau[c]) * inv_nv;
       Z[(int64_t)b * sC + (int64_t)c * ldc + i] = z;
     }
     const double cs = wave_sum(z);

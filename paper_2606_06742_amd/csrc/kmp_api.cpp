@@ -147,6 +147,7 @@ struct Bump {
 };
 
 constexpr int kPanel = 32;       // Householder panel width
+constexpr int64_t kMaxColumns = 65535;  // columns (groups x columns per group) per batch
 constexpr int kRowAlign = 64;    // padding of the per-fold matrix order
 constexpr size_t kAlign = 256;
 
@@ -155,6 +156,8 @@ struct Plan {
   int V = 0, S = 0, Qt = 1, L = 0, Sb = 0;
   int N = 0, C = 0, G = 0, RT = 0;
   int Mh = 0;                    // held-out rows per fold, padded (max m_v rounded up to 64)
+  bool shared = false;           // one factor of the full K per bandwidth (exact-CV form)
+  int nblk = 0;                  // row lists (groups per bandwidth): V, or 1 when shared
   std::vector<int> nv;           // per fold
   size_t bytes = 0;
 };
@@ -179,8 +182,8 @@ struct Layout {
   double *spart, *pnext, *band, *bpart, *gram_all, *tmat_all, *cross_all, *xpart;
   double *ahat, *abar, *bmat, *zmat, *anew, *estep, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
   double *beta, *bbar, *rmom, *gcoef, *kkt, *coef, *lam, *taucol, *fbuf, *nrm, *inv2s2;
-  int *flag, *moved, *iters, *iters_total, *active, *nvg, *chk, *cmap, *nact;
-  int32_t *tidx, *hidx, *fold;
+  int *flag, *moved, *iters, *iters_total, *active, *nvg, *chk, *cmap, *nact, *stat_count, *cnv;
+  int32_t *tidx, *hidx, *fold, *rfold, *cfold;
 };
 
 size_t carve(const Plan& p, void* ws, Layout* out) {
@@ -240,8 +243,12 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.cmap = c.take<int>(cols);
   l.nact = c.take<int>(G);
   l.chk = c.take<int>(2);
+  l.stat_count = c.take<int>(2);
   l.nvg = c.take<int>(G);
-  l.tidx = c.take<int32_t>((size_t)p.V * N);
+  l.cnv = c.take<int>(cols);
+  l.cfold = c.take<int32_t>(cols);
+  l.rfold = c.take<int32_t>(p.shared ? G * N : 0);
+  l.tidx = c.take<int32_t>((size_t)p.nblk * N);
   l.hidx = c.take<int32_t>((size_t)p.V * p.Mh);
   l.fold = c.take<int32_t>((size_t)p.n);
   if (out) *out = l;
@@ -252,10 +259,15 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
               int32_t V, int32_t S, int32_t Qn, int32_t Sb, Plan* p) {
   // a refit is one "fold" whose held-out set is empty: V = 1, no fold ids
   const bool refit = spec && (spec->flags & KMP_FLAG_REFIT) != 0;
+  const bool shared = spec && (spec->flags & KMP_FLAG_SHARED_FACTOR) != 0;
   if (!spec || n < 2 || d < 1 || L < 1 || S < 1 || Qn < 1 ||
-      (refit ? V != 1 : (V < 2 || !fold))) {
+      (refit ? V != 1 : (V < 2 || V > n || !fold))) {
     set_error(refit ? "invalid shape arguments (a full-data refit takes V = 1)"
                     : "invalid shape arguments");
+    return KMP_EINVAL;
+  }
+  if (refit && shared) {
+    set_error("a full-data refit has no folds to share a factor between");
     return KMP_EINVAL;
   }
   if (spec->loss != KMP_CHECK && Qn != 1) {
@@ -284,18 +296,38 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
     maxnv = std::max(maxnv, p->nv[v]);
     maxm = std::max(maxm, m[v]);
   }
-  p->N = (int)round_up(maxnv, kRowAlign);
-  // a fold's held-out set is no larger than any other fold's training set,
-  // so the padded held-out block fits in the N x N factor buffer
-  p->Mh = (int)round_up(maxm, kRowAlign);
-  if (p->N > kMaxOrder) {
-    set_error("more than " + std::to_string(kMaxOrder) + " training points per fold");
+  p->shared = shared;
+  p->Sb = std::max(1, std::min<int>(Sb, S));
+  if (shared) {
+    // every point is a row of the one factor per bandwidth; a column is a
+    // (tau, fold, lambda) problem whose held-out rows carry no loss
+    p->N = (int)round_up(n, kRowAlign);
+    p->Mh = 0;
+    p->nblk = 1;
+    p->C = Qn * V * L;
+    p->G = p->Sb;
+  } else {
+    p->N = (int)round_up(maxnv, kRowAlign);
+    // a fold's held-out set is no larger than any other fold's training
+    // set, so the padded held-out block fits in the N x N factor buffer
+    p->Mh = (int)round_up(maxm, kRowAlign);
+    p->nblk = V;
+    p->C = Qn * L;
+    p->G = p->Sb * V;
+  }
+  if (p->N > (shared ? kMaxSharedOrder : kMaxOrder)) {
+    set_error(shared ? "more than " + std::to_string(kMaxSharedOrder) +
+                           " points for the shared factor"
+                     : "more than " + std::to_string(kMaxOrder) + " training points per fold");
     return KMP_EINVAL;
   }
-  p->C = Qn * L;
+  // columns of a batch run along grid dimension y in some launches
+  if ((int64_t)p->G * p->C > kMaxColumns) {
+    set_error("more than " + std::to_string(kMaxColumns) +
+              " (sigma, tau, fold, lambda) columns in one bandwidth batch");
+    return KMP_EINVAL;
+  }
   p->RT = (int)ceil_div(p->N, kMinTileRows);
-  p->Sb = std::max(1, std::min<int>(Sb, S));
-  p->G = p->Sb * V;
   p->bytes = carve(*p, nullptr, nullptr);
   return 0;
 }
@@ -332,6 +364,41 @@ struct EventTimer {
     spans.clear();
   }
 };
+
+// The band reduction's buffers inside a carved workspace.
+BandWork band_work_of(const Layout& lay, int G, int N, const int* nv_host) {
+  BandWork bw;
+  bw.G = G; bw.N = N; bw.A = lay.A; bw.Q = lay.Qm; bw.band = lay.band; bw.tau = lay.tau;
+  static_assert(kPanel >= 2 * kBand, "two band panel buffers share the panel slot");
+  bw.panel = lay.panel; bw.panel2 = lay.panel + (size_t)G * 3 * kBand * N;
+  bw.tmat = lay.tmat; bw.gram = lay.gram; bw.xbuf = lay.xbuf;
+  bw.ybuf = lay.ybuf; bw.part = lay.bpart; bw.nv_host = nv_host;
+  bw.gram_all = lay.gram_all; bw.tmat_all = lay.tmat_all; bw.cross_all = lay.cross_all;
+  bw.xpart = lay.xpart;
+  return bw;
+}
+
+// The path solver's arrays inside a carved workspace.
+PathArrays path_arrays_of(const Layout& lay, const Plan& plan, int loss, bool global_solve) {
+  PathArrays pa;
+  pa.N = plan.N; pa.C = plan.C; pa.loss = loss;
+  pa.global_solve = global_solve;
+  pa.nv = lay.nvg; pa.ylab = lay.ylab; pa.Q = lay.Qm; pa.band = lay.band;
+  pa.cvec = lay.cvec; pa.lam = lay.lam; pa.tau = lay.taucol;
+  pa.ahat = lay.ahat; pa.abar = lay.abar; pa.bmat = lay.bmat; pa.zmat = lay.zmat;
+  pa.anew = lay.anew; pa.estep = lay.estep; pa.ldl_l = lay.ldl_l; pa.ldl_d = lay.ldl_d;
+  pa.vhat = lay.vhat;
+  pa.uvec = lay.uvec; pa.partial = lay.partial; pa.beta = lay.beta; pa.bbar = lay.bbar;
+  pa.fpart = lay.fpart; pa.zpart = lay.zpart;
+  pa.rmom = lay.rmom; pa.gcoef = lay.gcoef; pa.kkt = lay.kkt; pa.coef = lay.coef;
+  pa.moved = lay.moved; pa.flag = lay.flag;
+  pa.iters = lay.iters; pa.iters_total = lay.iters_total; pa.active_count = lay.active;
+  pa.cmap = lay.cmap; pa.nact = lay.nact;
+  pa.cnv = lay.cnv;
+  pa.rfold = plan.shared ? lay.rfold : nullptr;
+  pa.cfold = plan.shared ? lay.cfold : nullptr;
+  return pa;
+}
 
 }  // namespace
 }  // namespace kmp
@@ -503,7 +570,8 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
                  int32_t Qn, const double* lambdas, int32_t L, const int32_t* fold_id, int32_t V,
                  void* workspace, size_t workspace_bytes, double* alpha, double* beta,
                  double* objective, double* cv_sum, int32_t* cv_err, int32_t* iters,
-                 int32_t* status, int32_t* selected, kmp_timings* timings) {
+                 int32_t* status, int32_t* selected, int32_t* selected_joint,
+                 kmp_timings* timings) {
   hipStream_t s = (hipStream_t)stream;
   // ---------------------------------------------------------- validation
   const bool refit = spec && (spec->flags & KMP_FLAG_REFIT) != 0;
@@ -544,7 +612,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
         return KMP_EINVAL;
       }
   Plan plan;
-  int rc = make_plan(spec, n, d, L, fold_id, V, S, Qn, S, &plan);
+  int rc = make_plan(spec, n, d, L, fold_id, V, S, Qn, 1, &plan);
   if (rc != 0) return rc;
   // largest bandwidth batch that fits the workspace
   int Sb = 0;
@@ -570,13 +638,16 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   const int nbatch = (S + Sb - 1) / Sb;
   const size_t pin_bytes =
       Bump::round(sizeof(double) * n) + Bump::round(2 * sizeof(int)) +
-      Bump::round(sizeof(int32_t) * (size_t)V * N) +
+      Bump::round(sizeof(int32_t) * (size_t)plan.nblk * N) +
       Bump::round(sizeof(int32_t) * (size_t)V * plan.Mh) + Bump::round(sizeof(int32_t) * n) +
       Bump::round(sizeof(int) * ((size_t)G + 1)) +
       (size_t)nbatch * (Bump::round(sizeof(double) * Sb) +
                         2 * Bump::round(sizeof(double) * (size_t)G * C) +
+                        2 * Bump::round(sizeof(int) * (size_t)G * C) +
                         Bump::round(sizeof(int) * (size_t)G)) +
-      Bump::round(sizeof(double) * ncell) + 2 * Bump::round(sizeof(int32_t) * ncell);
+      Bump::round(sizeof(int32_t) * (size_t)G * N) +
+      Bump::round(sizeof(double) * ncell) + Bump::round(sizeof(int32_t) * ncell) +
+      Bump::round(2 * sizeof(int));
   CallCtx* ctx = nullptr;
   if ((rc = call_ctx(pin_bytes, &ctx)) != 0) return rc;
   Bump pin{ctx->pin, 0};
@@ -592,6 +663,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   // workspace); y and the counts come back while the factorisation is
   // queued and are checked before anything is written to the outputs.
   if ((rc = count_nonfinite(s, X, n, d, ldx, y, lay.chk)) != 0) return rc;
+  KMP_HIP_TRY(hipMemsetAsync(lay.stat_count, 0, 2 * sizeof(int), s));
   double* hy = pin.take<double>(n);
   int* hchk = pin.take<int>(2);
   KMP_HIP_TRY(hipMemcpyAsync(hy, y, sizeof(double) * n, hipMemcpyDeviceToHost, s));
@@ -638,14 +710,18 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   const double delta_final = stage_delta(nst - 1);
 
   // host-side index lists and per-column parameters
-  int32_t* tidx = pin.take<int32_t>((size_t)V * N);
-  std::fill(tidx, tidx + (size_t)V * N, -1);
-  for (int v = 0; v < V; ++v) {
+  // row lists: the training points of each fold, or (shared factor) every
+  // point once
+  const bool shared = plan.shared;
+  const int NB = plan.nblk;
+  int32_t* tidx = pin.take<int32_t>((size_t)NB * N);
+  std::fill(tidx, tidx + (size_t)NB * N, -1);
+  for (int v = 0; v < NB; ++v) {
     int k = 0;
     for (int64_t i = 0; i < n; ++i)
-      if (refit || fold_id[i] != v) tidx[(size_t)v * N + k++] = (int32_t)i;
+      if (shared || refit || fold_id[i] != v) tidx[(size_t)v * N + k++] = (int32_t)i;
   }
-  KMP_HIP_TRY(hipMemcpyAsync(lay.tidx, tidx, sizeof(int32_t) * (size_t)V * N,
+  KMP_HIP_TRY(hipMemcpyAsync(lay.tidx, tidx, sizeof(int32_t) * (size_t)NB * N,
                              hipMemcpyHostToDevice, s));
   int32_t* hidx = pin.take<int32_t>((size_t)V * plan.Mh);
   std::fill(hidx, hidx + (size_t)V * plan.Mh, -1);
@@ -702,38 +778,34 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   if ((rc = tm.mark(s, &ev_start)) != 0) return rc;
   if ((rc = row_norms(s, X, n, d, ldx, lay.nrm)) != 0) return rc;
 
-  PathArrays pa;
-  pa.N = N; pa.C = C; pa.loss = spec->loss;
-  pa.global_solve = (spec->flags & KMP_FLAG_GLOBAL_SOLVE) != 0;
-  pa.nv = lay.nvg; pa.ylab = lay.ylab; pa.Q = lay.Qm; pa.band = lay.band;
-  pa.cvec = lay.cvec; pa.lam = lay.lam; pa.tau = lay.taucol;
-  pa.ahat = lay.ahat; pa.abar = lay.abar; pa.bmat = lay.bmat; pa.zmat = lay.zmat;
-  pa.anew = lay.anew; pa.estep = lay.estep; pa.ldl_l = lay.ldl_l; pa.ldl_d = lay.ldl_d;
-  pa.vhat = lay.vhat;
-  pa.uvec = lay.uvec; pa.partial = lay.partial; pa.beta = lay.beta; pa.bbar = lay.bbar;
-  pa.fpart = lay.fpart; pa.zpart = lay.zpart;
-  pa.rmom = lay.rmom; pa.gcoef = lay.gcoef; pa.kkt = lay.kkt; pa.coef = lay.coef;
-  pa.moved = lay.moved; pa.flag = lay.flag;
-  pa.iters = lay.iters; pa.iters_total = lay.iters_total; pa.active_count = lay.active;
-  pa.cmap = lay.cmap; pa.nact = lay.nact;
+  PathArrays pa = path_arrays_of(lay, plan, spec->loss, (spec->flags & KMP_FLAG_GLOBAL_SOLVE) != 0);
 
   for (int s0 = 0; s0 < S; s0 += Sb) {
     const int sb = std::min(Sb, S - s0);
-    const int Gb = sb * V;
+    const int Gb = sb * NB;
     pa.G = Gb;
-    // per-batch parameters
+    // per-batch parameters. Per fold: group g = (bandwidth, fold), column
+    // c = (tau, lambda). Shared factor: group g = bandwidth, column
+    // c = (tau, fold, lambda), rows held out of the column's fold carry no
+    // loss, and each column keeps its fold's n_v as loss normaliser.
     double* f2 = pin.take<double>(Sb);
     double* lamc = pin.take<double>((size_t)G * C);
     double* tauc = pin.take<double>((size_t)G * C);
     int* nvg = pin.take<int>(G);
+    int* cnvh = pin.take<int>((size_t)G * C);
+    int32_t* cfh = pin.take<int32_t>((size_t)G * C);
     for (int i = 0; i < sb; ++i) f2[i] = 1.0 / (2.0 * sigmas[s0 + i] * sigmas[s0 + i]);
+    const int cv_per_q = shared ? V * L : L;       // columns per tau level
     for (int g = 0; g < Gb; ++g) {
-      nvg[g] = plan.nv[g % V];
-      for (int q = 0; q < Qn; ++q)
-        for (int l = 0; l < L; ++l) {
-          lamc[(size_t)g * C + q * L + l] = lambdas[l];
-          tauc[(size_t)g * C + q * L + l] = spec->loss == KMP_CHECK ? taus[q] : 0.0;
-        }
+      nvg[g] = shared ? (int)n : plan.nv[g % V];
+      for (int c = 0; c < C; ++c) {
+        const int q = c / cv_per_q, r = c % cv_per_q, l = r % L;
+        const int v = shared ? r / L : g % V;
+        lamc[(size_t)g * C + c] = lambdas[l];
+        tauc[(size_t)g * C + c] = spec->loss == KMP_CHECK ? taus[q] : 0.0;
+        cnvh[(size_t)g * C + c] = plan.nv[v];
+        cfh[(size_t)g * C + c] = shared ? v : -1;
+      }
     }
     KMP_HIP_TRY(hipMemcpyAsync(lay.inv2s2, f2, sizeof(double) * sb, hipMemcpyHostToDevice, s));
     KMP_HIP_TRY(hipMemcpyAsync(lay.lam, lamc, sizeof(double) * (size_t)Gb * C,
@@ -741,6 +813,18 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     KMP_HIP_TRY(hipMemcpyAsync(lay.taucol, tauc, sizeof(double) * (size_t)Gb * C,
                                hipMemcpyHostToDevice, s));
     KMP_HIP_TRY(hipMemcpyAsync(lay.nvg, nvg, sizeof(int) * Gb, hipMemcpyHostToDevice, s));
+    KMP_HIP_TRY(hipMemcpyAsync(lay.cnv, cnvh, sizeof(int) * (size_t)Gb * C, hipMemcpyHostToDevice, s));
+    KMP_HIP_TRY(hipMemcpyAsync(lay.cfold, cfh, sizeof(int32_t) * (size_t)Gb * C,
+                               hipMemcpyHostToDevice, s));
+    if (shared && s0 == 0) {
+      // fold id of every row of every group (-1 at padding), the same for
+      // every bandwidth; written once
+      int32_t* rfh = pin.take<int32_t>((size_t)G * N);
+      for (int g = 0; g < G; ++g)
+        for (int i = 0; i < N; ++i) rfh[(size_t)g * N + i] = i < n ? fold_id[i] : -1;
+      KMP_HIP_TRY(hipMemcpyAsync(lay.rfold, rfh, sizeof(int32_t) * (size_t)G * N,
+                                 hipMemcpyHostToDevice, s));
+    }
     pa.nv_host = nvg;
     // columns in each group's active list, as last read back (work counters)
     std::vector<int> nact_h(Gb, C);
@@ -749,26 +833,19 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     // a1: Gram + fold gather into A (group g = s_local*V + v)
     if ((rc = tm.mark(s, &e1)) != 0) return rc;
     kc_begin(KMP_KC_GRAM, s);
-    if ((rc = rbf_blocks(s, X, d, ldx, lay.nrm, lay.tidx, N, N, lay.tidx, N, N, V, lay.inv2s2, sb,
-                         lay.A, (int64_t)V * N * N, (int64_t)N * N, N)) != 0)
+    if ((rc = rbf_blocks(s, X, d, ldx, lay.nrm, lay.tidx, N, N, lay.tidx, N, N, NB, lay.inv2s2, sb,
+                         lay.A, (int64_t)NB * N * N, (int64_t)N * N, N)) != 0)
       return rc;
     {
       // every kernel entry of every group is written once; the inner products
       // (2d flops each) are shared by the bandwidths of the batch
       double e2 = 0.0;
-      for (int v = 0; v < V; ++v) e2 += (double)plan.nv[v] * plan.nv[v];
+      for (int v = 0; v < NB; ++v) e2 += shared ? (double)n * n : (double)plan.nv[v] * plan.nv[v];
       kc_end(KMP_KC_GRAM, s, 8.0 * sb * e2, 2.0 * d * e2);
     }
     if ((rc = tm.mark(s, &e2)) != 0) return rc;
     // a2: factorisation
-    BandWork bw;
-    bw.G = Gb; bw.N = N; bw.A = lay.A; bw.Q = lay.Qm; bw.band = lay.band; bw.tau = lay.tau;
-    static_assert(kPanel >= 2 * kBand, "two band panel buffers share the panel slot");
-    bw.panel = lay.panel; bw.panel2 = lay.panel + (size_t)Gb * 3 * kBand * N;
-    bw.tmat = lay.tmat; bw.gram = lay.gram; bw.xbuf = lay.xbuf;
-    bw.ybuf = lay.ybuf; bw.part = lay.bpart; bw.nv_host = nvg;
-    bw.gram_all = lay.gram_all; bw.tmat_all = lay.tmat_all; bw.cross_all = lay.cross_all;
-    bw.xpart = lay.xpart;
+    BandWork bw = band_work_of(lay, Gb, N, nvg);
     bw.band_ready = side.band;
     if ((rc = band_reduce(s, bw)) != 0) return rc;
     KMP_HIP_TRY(hipStreamWaitEvent(side.st, side.band, 0));
@@ -776,7 +853,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     if ((rc = path_stage_factor(side.st, pa, stage_kappa(0))) != 0) return rc;
     KMP_HIP_TRY(hipEventRecord(side.done, side.st));
     if ((rc = group_ones_projection(s, lay.Qm, lay.nvg, Gb, N, lay.cvec)) != 0) return rc;
-    if ((rc = gather_labels(s, y, lay.tidx, V, sb, N, lay.ylab)) != 0) return rc;
+    if ((rc = gather_labels(s, y, lay.tidx, NB, sb, N, lay.ylab)) != 0) return rc;
     if ((rc = path_init_columns(s, pa)) != 0) return rc;
     if ((rc = tm.mark(s, &e3)) != 0) return rc;
     tm.span(&t_gram, e1, e2);
@@ -859,7 +936,8 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     fa.s0 = s0; fa.S = S; fa.inv2s2 = lay.inv2s2; fa.delta = delta_final; fa.fbuf = lay.fbuf;
     fa.hidx = lay.hidx; fa.Mh = plan.Mh; fa.kh = lay.A; fa.ftrain = lay.fpart;
     fa.alpha = alpha; fa.beta_out = beta; fa.objective = objective; fa.cv_sum = cv_sum;
-    fa.cv_err = cv_err; fa.iters = iters; fa.status = status;
+    fa.shared = shared;
+    fa.cv_err = cv_err; fa.iters = iters; fa.status = status; fa.stat_count = lay.stat_count;
     size_t f0 = 0, f1 = 0;
     if ((rc = tm.mark(s, &f0)) != 0) return rc;
     if ((rc = path_finalize(s, pa, fa)) != 0) return rc;
@@ -871,11 +949,10 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   // host-side selection and status summary: the three arrays come back
   // with one wait
   double* hcv = pin.take<double>(ncell);
-  int32_t* hst = pin.take<int32_t>(ncell);
   int32_t* hit = pin.take<int32_t>(ncell);
+  int* hstat = pin.take<int>(2);
   KMP_HIP_TRY(hipMemcpyAsync(hcv, cv_sum, sizeof(double) * ncell, hipMemcpyDeviceToHost, s));
-  if (status)
-    KMP_HIP_TRY(hipMemcpyAsync(hst, status, sizeof(int32_t) * ncell, hipMemcpyDeviceToHost, s));
+  KMP_HIP_TRY(hipMemcpyAsync(hstat, lay.stat_count, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
   if (iters)
     KMP_HIP_TRY(hipMemcpyAsync(hit, iters, sizeof(int32_t) * ncell, hipMemcpyDeviceToHost, s));
   KMP_HIP_TRY(hipStreamSynchronize(s));
@@ -884,29 +961,32 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   tm.span(&t_total, ev_start, ev_end);
   tm.sum();
 
-  bool any_max = false;
-  int64_t cell_iters = 0;
-  if (status) {
-    for (size_t i = 0; i < ncell; ++i) {
-      const int32_t v = hst[i];
-      if (v == 1) any_max = true;
-      if (v == 2) {
-        set_error("non-finite values in the iteration");
-        return KMP_ENONFINITE;
-      }
-    }
+  // the return code comes from the device's counts of cells that went
+  // non-finite or stopped at max_iter, whether or not `status` was given
+  if (hstat[1] > 0) {
+    set_error(std::to_string(hstat[1]) + " cells with non-finite values in the iteration");
+    return KMP_ENONFINITE;
   }
+  const bool any_max = hstat[0] > 0;
+  int64_t cell_iters = 0;
   if (iters)
     for (size_t i = 0; i < ncell; ++i) cell_iters += hit[i];
+  // selection (Appendix A.4: the fold-wise validation losses, pooled): the
+  // CV score of (s, q, l) is sum_v cv_sum / n; per (s, q) the smallest
+  // score wins with ties to the larger lambda, and jointly over (s, l) per q
+  // with ties to the larger lambda, then the larger sigma
+  const auto score = [&](int si, int q, int l) {
+    double sc = 0.0;
+    for (int v = 0; v < V; ++v) sc += hcv[(((size_t)si * Qn + q) * V + v) * L + l];
+    return sc / (double)n;
+  };
   if (selected && !refit) {
     for (int si = 0; si < S; ++si)
       for (int q = 0; q < Qn; ++q) {
         int best = -1;
         double bs = 0.0;
         for (int l = 0; l < L; ++l) {
-          double sc = 0.0;
-          for (int v = 0; v < V; ++v) sc += hcv[(((size_t)si * Qn + q) * V + v) * L + l];
-          sc /= (double)n;
+          const double sc = score(si, q, l);
           if (best < 0 || sc < bs || (sc == bs && lambdas[l] > lambdas[best])) {
             best = l;
             bs = sc;
@@ -914,6 +994,27 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
         }
         selected[si * Qn + q] = best;
       }
+  }
+  if (selected_joint && !refit) {
+    for (int q = 0; q < Qn; ++q) {
+      int bsig = -1, bl = -1;
+      double bs = 0.0;
+      for (int si = 0; si < S; ++si)
+        for (int l = 0; l < L; ++l) {
+          const double sc = score(si, q, l);
+          const bool better =
+              bsig < 0 || sc < bs ||
+              (sc == bs && (lambdas[l] > lambdas[bl] ||
+                            (lambdas[l] == lambdas[bl] && sigmas[si] > sigmas[bsig])));
+          if (better) {
+            bsig = si;
+            bl = l;
+            bs = sc;
+          }
+        }
+      selected_joint[2 * q] = bsig;
+      selected_joint[2 * q + 1] = bl;
+    }
   }
   if (timings) {
     for (int k = 0; k < KMP_NKC; ++k) {
@@ -943,6 +1044,146 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     timings->cell_iterations = cell_iters;
   }
   return any_max ? KMP_WMAXITER : KMP_OK;
+}
+
+int kmp_dgemm_grouped(void* stream, int32_t G, int32_t M, int32_t N, int32_t K, const double* A,
+                      const double* B, double* C) {
+  hipStream_t s = (hipStream_t)stream;
+  if (G < 0 || M < 0 || N < 0 || K < 0) {
+    set_error("kmp_dgemm_grouped: negative size");
+    return KMP_EINVAL;
+  }
+  if (G == 0 || M == 0 || N == 0) return KMP_OK;
+  if (!C || (K > 0 && (!A || !B))) {
+    set_error("kmp_dgemm_grouped: null pointer");
+    return KMP_EINVAL;
+  }
+  if (G > 65535) {
+    set_error("kmp_dgemm_grouped: at most 65535 groups per call");
+    return KMP_EINVAL;
+  }
+  if (K == 0) {   // empty sum
+    KMP_HIP_TRY(hipMemsetAsync(C, 0, sizeof(double) * (size_t)G * M * N, s));
+    KMP_HIP_TRY(hipStreamSynchronize(s));
+    return KMP_OK;
+  }
+  GemmArgs g;
+  g.M = M; g.N = N; g.K = K; g.batch = G;
+  g.A = A; g.lda = K; g.sA = (int64_t)M * K;
+  g.B = B; g.ldb = N; g.sB = (int64_t)K * N;
+  g.C = C; g.ldc = N; g.sC = (int64_t)M * N;
+  g.alpha = 1.0; g.beta = 0.0;
+  int rc = gemm(s, g, true, false, true);
+  if (rc != 0) return rc;
+  KMP_HIP_TRY(hipStreamSynchronize(s));
+  return KMP_OK;
+}
+
+int kmp_path_step(void* stream, int32_t loss, double delta, const double* K, int64_t n,
+                  const double* y, const double* lambdas, const double* taus, int32_t C,
+                  const double* alpha_in, const double* beta_in, double* alpha_out,
+                  double* beta_out, double* kkt_out) {
+  hipStream_t s = (hipStream_t)stream;
+  if (loss < 0 || loss > 2 || !K || !y || !lambdas || !alpha_in || !beta_in || !alpha_out ||
+      !beta_out || n < 2 || C < 1 || (loss != KMP_LOGISTIC && !(delta > 0.0)) ||
+      (loss == KMP_CHECK && !taus)) {
+    set_error("kmp_path_step: invalid arguments");
+    return KMP_EINVAL;
+  }
+  for (int c = 0; c < C; ++c) {
+    if (!(lambdas[c] > 0.0) || !std::isfinite(lambdas[c])) {
+      set_error("kmp_path_step: lambda must be positive and finite");
+      return KMP_EINVAL;
+    }
+    if (loss == KMP_CHECK && !(taus[c] > 0.0 && taus[c] < 1.0)) {
+      set_error("kmp_path_step: tau must lie in (0, 1)");
+      return KMP_EINVAL;
+    }
+  }
+  // one group of all n rows (the full-data layout), C columns
+  kmp_path_spec spec;
+  kmp_default_spec(&spec);
+  spec.loss = loss;
+  spec.flags = KMP_FLAG_REFIT;
+  Plan plan;
+  int rc = make_plan(&spec, n, 1, C, nullptr, 1, 1, 1, 1, &plan);
+  if (rc != 0) return rc;
+  if (n > kMaxOrder) {
+    set_error("kmp_path_step: n above the largest factor order");
+    return KMP_EINVAL;
+  }
+  // make_plan lays out C = Q L columns with Q = 1, L = C
+  const int N = plan.N;
+  const double kappa = loss == KMP_LOGISTIC ? 4.0 : 2.0 * delta;
+  void* ws = nullptr;
+  KMP_HIP_TRY(hipMallocAsync(&ws, plan.bytes, s));
+  struct Free {
+    void* p;
+    hipStream_t s;
+    ~Free() {
+      if (p) (void)hipFreeAsync(p, s);
+    }
+  } free_ws{ws, s};
+  Layout lay;
+  carve(plan, ws, &lay);
+  const size_t cols = (size_t)C;
+  // host-side parameters (pageable: small, synchronous copies)
+  std::vector<double> lam(lambdas, lambdas + C), tau(C, 0.0);
+  if (loss == KMP_CHECK) tau.assign(taus, taus + C);
+  std::vector<int> nvg(1, (int)n), cnv(C, (int)n);
+  std::vector<int32_t> cf(C, -1);
+  KMP_HIP_TRY(hipMemcpyAsync(lay.lam, lam.data(), sizeof(double) * cols, hipMemcpyHostToDevice, s));
+  KMP_HIP_TRY(hipMemcpyAsync(lay.taucol, tau.data(), sizeof(double) * cols, hipMemcpyHostToDevice, s));
+  KMP_HIP_TRY(hipMemcpyAsync(lay.nvg, nvg.data(), sizeof(int), hipMemcpyHostToDevice, s));
+  KMP_HIP_TRY(hipMemcpyAsync(lay.cnv, cnv.data(), sizeof(int) * cols, hipMemcpyHostToDevice, s));
+  KMP_HIP_TRY(hipMemcpyAsync(lay.cfold, cf.data(), sizeof(int32_t) * cols, hipMemcpyHostToDevice, s));
+  // K into the padded factor buffer, y into the padded labels
+  KMP_HIP_TRY(hipMemsetAsync(lay.A, 0, sizeof(double) * (size_t)N * N, s));
+  KMP_HIP_TRY(hipMemcpy2DAsync(lay.A, sizeof(double) * N, K, sizeof(double) * n,
+                               sizeof(double) * n, n, hipMemcpyDeviceToDevice, s));
+  KMP_HIP_TRY(hipMemsetAsync(lay.ylab, 0, sizeof(double) * N, s));
+  KMP_HIP_TRY(hipMemcpyAsync(lay.ylab, y, sizeof(double) * n, hipMemcpyDeviceToDevice, s));
+  // a2 and the stage setup on this matrix
+  BandWork bw = band_work_of(lay, 1, N, nvg.data());
+  if ((rc = band_reduce(s, bw)) != 0) return rc;
+  PathArrays pa = path_arrays_of(lay, plan, loss, false);
+  pa.G = 1;
+  pa.nv_host = nvg.data();
+  std::vector<int> nact_h(1, C);
+  pa.nact_host = nact_h.data();
+  if ((rc = group_ones_projection(s, lay.Qm, lay.nvg, 1, N, lay.cvec)) != 0) return rc;
+  if ((rc = path_init_columns(s, pa)) != 0) return rc;
+  // the caller's state in the factor basis: ahat = Q' alpha, beta
+  KMP_HIP_TRY(hipMemsetAsync(lay.zmat, 0, sizeof(double) * cols * N, s));
+  KMP_HIP_TRY(hipMemcpy2DAsync(lay.zmat, sizeof(double) * N, alpha_in, sizeof(double) * n,
+                               sizeof(double) * n, C, hipMemcpyDeviceToDevice, s));
+  GemmArgs g;
+  g.M = N; g.N = C; g.K = N; g.batch = 1;
+  g.A = lay.Qm; g.lda = N; g.sA = (int64_t)N * N;
+  g.B = lay.zmat; g.ldb = N; g.sB = (int64_t)N * C;
+  g.C = lay.ahat; g.ldc = N; g.sC = (int64_t)N * C;
+  if ((rc = gemm(s, g, false, true, false)) != 0) return rc;
+  KMP_HIP_TRY(hipMemcpyAsync(lay.beta, beta_in, sizeof(double) * cols, hipMemcpyDeviceToDevice, s));
+  // factors and vectors of the stage (momentum restarted: the step is taken
+  // from the given point itself), then one iteration with tol = 0 so every
+  // column steps
+  if ((rc = path_stage_factor(s, pa, kappa)) != 0) return rc;
+  if ((rc = path_stage_vectors(s, pa, kappa)) != 0) return rc;
+  if ((rc = path_compact(s, pa)) != 0) return rc;
+  if ((rc = path_iteration(s, pa, loss == KMP_LOGISTIC ? 1.0 : delta, kappa, 0.0, 1 << 30, 0)) != 0)
+    return rc;
+  // alpha = Q a+ back to the caller's layout
+  g.A = lay.Qm;
+  g.B = lay.ahat;
+  g.C = lay.zmat;
+  if ((rc = gemm(s, g, true, true, false)) != 0) return rc;
+  KMP_HIP_TRY(hipMemcpy2DAsync(alpha_out, sizeof(double) * n, lay.zmat, sizeof(double) * N,
+                               sizeof(double) * n, C, hipMemcpyDeviceToDevice, s));
+  KMP_HIP_TRY(hipMemcpyAsync(beta_out, lay.beta, sizeof(double) * cols, hipMemcpyDeviceToDevice, s));
+  if (kkt_out)
+    KMP_HIP_TRY(hipMemcpyAsync(kkt_out, lay.kkt, sizeof(double) * cols, hipMemcpyDeviceToDevice, s));
+  KMP_HIP_TRY(hipStreamSynchronize(s));
+  return KMP_OK;
 }
 
 }  // extern "C"

@@ -22,13 +22,19 @@ struct GemmArgs {
 
 // Loss epilogue of the first path GEMM (f = Q (T abar) then z): for row i of
 // batch b and column c, with f = acc + bbar[c]:
-//   Z[i][c] = psi(y[i], f)/nv[b] if i < nv[b] else 0,
-// and partial[b][tile][c] = sum of Z over the rows of the row tile.
+//   Z[i][c] = psi(y[i], f)/cnv[c] if i < nv[b] and row i is a training row
+//             of column c, else 0,
+// and partial[b][tile][c] = sum of Z over the rows of the row tile. A row is
+// a training row of every column unless fold ids are given (shared-factor
+// exact CV): then row i is held out of column c when rfold[i] == cfold[c].
 struct LossEpi {
   int loss = 0;
   double delta = 1.0;
   const double* y = nullptr; int64_t sy = 0;     // labels, per batch stride
   const int* nv = nullptr;                       // valid rows per batch
+  const int* cnv = nullptr;                      // loss normaliser per column (stride sbb)
+  const int32_t* rfold = nullptr;                // fold id per row (stride sy), or null
+  const int32_t* cfold = nullptr;                // held-out fold per column (stride sbb)
   const double* bbar = nullptr; int64_t sbb = 0; // per column intercepts
   const double* tau = nullptr; int64_t stau = 0; // per column tau (check)
   double* partial = nullptr; int64_t spart = 0;  // [tiles][N] per batch
@@ -74,6 +80,9 @@ constexpr int kBand = 16;      // lower bandwidth of B (= panel width of the red
 // Largest padded order per fold: N*N stays below 2^31 (32-bit row offsets
 // r*N in the kernels) and the per-fold matrices of the largest workloads fit.
 constexpr int kMaxOrder = 32768;
+// Largest order of the one factor per bandwidth in the shared-factor mode
+// (every kernel offset r*N + c still below 2^31).
+constexpr int kMaxSharedOrder = 40960;
 constexpr int kWyBlock = 64;   // reflectors per compact-WY block when forming Q
 
 // Reduction of G symmetric N x N matrices (row-major, packed, destroyed) to
@@ -151,6 +160,9 @@ struct PathArrays {
   int loss = 0;
   bool global_solve = false;     // banded solve vector in device memory at every order
   const int* nv = nullptr;       // G valid rows
+  const int* cnv = nullptr;      // G*C loss normaliser of each column (its n_v)
+  const int32_t* rfold = nullptr;  // G x N fold id per row (shared-factor mode), else null
+  const int32_t* cfold = nullptr;  // G*C held-out fold per column (shared-factor mode)
   const double* ylab = nullptr;  // G x N labels (0 at padding)
   const double* Q = nullptr;     // G x N x N
   const double* band = nullptr;  // G x (kBand+1) x N, band[g][r*N + j] = B[j+r][j]
@@ -205,9 +217,10 @@ int path_compact(hipStream_t s, const PathArrays& p);
 int group_ones_projection(hipStream_t s, const double* Q, const int* nv, int G, int N, double* cvec);
 
 // Finalize: alpha_loc = Q ahat (zmat reused), training predictions
-// f = Q (T ahat) + beta, held-out predictions K[H_v, T_v] alpha + beta with
-// the held-out kernel block built on matrix cores, objective/CV sums,
-// scatter of alpha.
+// f = K_v alpha + beta with K_v built again from X on the matrix cores (the
+// objective is evaluated in observation space), held-out predictions
+// K[H_v, T_v] alpha + beta likewise, objective/CV sums, scatter of alpha,
+// counts of cells that hit max_iter or went non-finite.
 struct FinalArgs {
   int n = 0, d = 0; int64_t ldx = 0;
   const double* X = nullptr; const double* nrm = nullptr; const double* y = nullptr;
@@ -218,13 +231,15 @@ struct FinalArgs {
   int V = 0, S_b = 0, Qt = 1, L = 0, s0 = 0, S = 0;
   const double* inv2s2 = nullptr;  // S_b bandwidth factors of this batch
   double delta = 1.0;
-  double* kh = nullptr;            // G x Mh x N held-out kernel blocks (ld N, stride N*N)
+  double* kh = nullptr;            // G x N x N: training, then held-out kernel blocks (ld N)
   double* ftrain = nullptr;        // G x C x N training predictions (without beta)
   double* fbuf = nullptr;          // G x C x Mh held-out predictions (without beta)
   // outputs (full arrays, cell ((s*Q+q)*V+v)*L+l)
   double* alpha = nullptr; double* beta_out = nullptr; double* objective = nullptr;
   double* cv_sum = nullptr; int32_t* cv_err = nullptr; int32_t* iters = nullptr;
   int32_t* status = nullptr;
+  int* stat_count = nullptr;       // 2 ints, accumulated: cells at max_iter, non-finite cells
+  bool shared = false;             // shared-factor mode (one group per bandwidth, all n rows)
 };
 int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& f);
 

@@ -513,7 +513,7 @@ __global__ __launch_bounds__(64 * FW) void ldl_factor_kernel(
   double* Bt = dbuf + 2 * BND;           // band tile of block I: Bt[r * BND + j] = B[i0+j+r][i0+j]
   const int g = (int)(gc / C);
   const double lam = lamv[gc];
-  const double sc = 1.0 / ((double)nv[g] * kappa);
+  const double sc = 1.0 / ((double)nv[gc] * kappa);   // the column's loss normaliser
   const double* bg = band + (int64_t)g * (BND + 1) * N;
   double* Vc = Vfac + gc * (int64_t)BND * N;
   double* Dc = Dfac + gc * (int64_t)N;
@@ -662,7 +662,7 @@ __global__ __launch_bounds__(256) void stage_vectors_kernel(
   double* xs = lds_dyn + (int64_t)wv * (GV ? RING : N);   // vector or ring
   const int g = (int)(gc / C);
   const double lam = lamv[gc];
-  const double sc = 1.0 / ((double)nv[g] * kappa);
+  const double sc = 1.0 / ((double)nv[gc] * kappa);   // the column's loss normaliser
   const double* cg = cvec + (int64_t)g * N;
   const double* Vc = Vfac + gc * (int64_t)BND * N;
   const double* Dc = Dfac + gc * (int64_t)N;
@@ -704,7 +704,7 @@ int path_stage_factor(hipStream_t s, const PathArrays& p, double kappa) {
   const int64_t cols = (int64_t)p.G * p.C;
   kc_begin(KMP_KC_PRECOMPUTE, s);
   hipLaunchKernelGGL(ldl_factor_kernel, dim3((unsigned)ceil_div(cols, FW)), dim3(64 * FW), 0, s, p.N,
-                     p.C, cols, p.nv, p.band, p.lam, kappa, p.ldl_l, p.ldl_d);
+                     p.C, cols, p.cnv, p.band, p.lam, kappa, p.ldl_l, p.ldl_d);
   KMP_LAUNCH_CHECK();
   // reads the band, writes the factor tiles and 1/d (BND + 1 per element)
   kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 1.0); }),
@@ -722,11 +722,11 @@ int path_stage_vectors(hipStream_t s, const PathArrays& p, double kappa) {
   kc_begin(KMP_KC_PRECOMPUTE, s);
   if (path_global_vec(p))
     hipLaunchKernelGGL(stage_vectors_kernel<true>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw),
-                       lds, s, p.N, p.C, cols, p.nv, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
+                       lds, s, p.N, p.C, cols, p.cnv, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
                        p.gcoef, p.ahat, p.abar, p.beta, p.bbar, p.rmom, p.flag, p.iters);
   else
     hipLaunchKernelGGL(stage_vectors_kernel<false>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw),
-                       lds, s, p.N, p.C, cols, p.nv, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
+                       lds, s, p.N, p.C, cols, p.cnv, p.cvec, p.lam, kappa, p.ldl_l, p.ldl_d, p.vhat,
                        p.gcoef, p.ahat, p.abar, p.beta, p.bbar, p.rmom, p.flag, p.iters);
   KMP_LAUNCH_CHECK();
   int rc;
@@ -777,7 +777,7 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
   const int g = (int)(gc / C), c = (int)(gc % C);
   const int64_t base = gc * (int64_t)N;
   const double lam = lamv[gc];
-  const double nvd = (double)nvv[g];
+  const double nvd = (double)nvv[gc];                  // the column's loss normaliser
   double d0 = 0.0;
   {
     const double* pg = partial + (int64_t)g * RT * C + c;
@@ -817,7 +817,8 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
   const double n2sum = wave_sum(n2);
   const double kkt = nvd * fmax(sqrt(n2sum), fabs(d0));
   const double bb = bbar[gc];
-  if (!(kkt == kkt) || kkt > 1e300) {          // non-finite
+  // non-finite: tested on both terms, since fmax drops a NaN
+  if (!(n2sum == n2sum) || !(d0 == d0) || !(kkt <= 1e300)) {
     if (lane == 0) { flag[gc] = 3; kktv[gc] = kkt; moved[gc] = 0; }
     return;
   }
@@ -939,7 +940,7 @@ __global__ __launch_bounds__(256) void update_column_kernel(
   const int g = (int)(gc / C), c = (int)(gc % C);
   const int64_t base = gc * (int64_t)N;
   const double lam = lamv[gc];
-  const double nvd = (double)nvv[g];
+  const double nvd = (double)nvv[gc];                  // the column's loss normaliser
   double d0 = 0.0;
   {
     const double* pg = partial + (int64_t)g * RT * C + c;
@@ -978,7 +979,8 @@ __global__ __launch_bounds__(256) void update_column_kernel(
   const double n2sum = block_sum<PW>(n2, red);
   const double kkt = nvd * fmax(sqrt(n2sum), fabs(d0));
   const double bb = bbar[gc];
-  if (!(kkt == kkt) || kkt > 1e300) {                   // non-finite (uniform)
+  // non-finite (uniform): tested on both terms, since fmax drops a NaN
+  if (!(n2sum == n2sum) || !(d0 == d0) || !(kkt <= 1e300)) {
     if (t == 0) { flag[gc] = 3; kktv[gc] = kkt; moved[gc] = 0; }
     return;
   }
@@ -1085,8 +1087,9 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   const int S1 = splitk_parts(g1, work_tiles);
   LossEpi e;
   e.loss = p.loss; e.delta = delta;
-  e.y = p.ylab; e.sy = p.N; e.nv = p.nv;
+  e.y = p.ylab; e.sy = p.N; e.nv = p.nv; e.cnv = p.cnv;
   e.bbar = p.bbar; e.sbb = p.C; e.tau = p.tau; e.stau = p.C;
+  e.rfold = p.rfold; e.cfold = p.cfold;
   e.partial = p.partial; e.spart = (int64_t)RT * p.C;
   const double gflops = over_active(p, [&](double n, double c) { return 2.0 * n * n * c; });
   const double gbytes = over_active(p, [&](double n, double c) { return 8.0 * (n * n + 2.0 * n * c); });
@@ -1114,7 +1117,7 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_u));
     kc_begin(KMP_KC_UPDATE, s);
     hipLaunchKernelGGL(update_column_kernel, dim3((unsigned)cols), dim3(PB), lds_u, s, p.N, p.C, RT,
-                       p.nv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.anew, p.estep, p.coef,
+                       p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.anew, p.estep, p.coef,
                        p.ldl_l, p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom,
                        p.kkt, p.flag, p.iters, p.iters_total, p.moved, tol, max_iter, restart);
     KMP_LAUNCH_CHECK();
@@ -1137,7 +1140,7 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   kc_begin(KMP_KC_UPDATE, s);
 #define KMP_SOLVE_STEP(GVV)                                                                        \
   hipLaunchKernelGGL(solve_step_kernel<GVV>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, \
-                     s, p.N, p.C, cols, RT, p.nv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l,  \
+                     s, p.N, p.C, cols, RT, p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l, \
                      p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt,    \
                      p.flag, p.iters, p.iters_total, p.anew, p.estep, p.coef, p.moved, tol,         \
                      max_iter, restart)
@@ -1201,8 +1204,9 @@ int path_compact(hipStream_t s, const PathArrays& p) {
 }
 
 // --------------------------------------------------------------- finalize
-// One workgroup per column: objective on the training points, CV sums on the
-// held-out points, scatter of alpha into the output layout.
+// One workgroup per column: objective on the training points (from
+// ftrain = K_v alpha in observation space), CV sums on the held-out points,
+// scatter of alpha into the output layout, status counts.
 __global__ __launch_bounds__(256) void cv_reduce_kernel(
     int n, int N, int Mh, int C, int V, int Qt, int L, int s0, int loss, double delta,
     const double* __restrict__ y, const int32_t* __restrict__ tidx,
@@ -1212,7 +1216,8 @@ __global__ __launch_bounds__(256) void cv_reduce_kernel(
     const double* __restrict__ betav, const int* __restrict__ flag,
     const int* __restrict__ iters_total, double* __restrict__ alpha_out,
     double* __restrict__ beta_out, double* __restrict__ obj_out, double* __restrict__ cv_out,
-    int32_t* __restrict__ err_out, int32_t* __restrict__ it_out, int32_t* __restrict__ st_out) {
+    int32_t* __restrict__ err_out, int32_t* __restrict__ it_out, int32_t* __restrict__ st_out,
+    int* __restrict__ stat_count) {
   __shared__ double red[PW];
   const int64_t gc = blockIdx.x;
   const int g = (int)(gc / C), c = (int)(gc % C);
@@ -1253,11 +1258,80 @@ __global__ __launch_bounds__(256) void cv_reduce_kernel(
     cv_out[cell] = cs;
     if (err_out) err_out[cell] = (int32_t)ce;
     if (it_out) it_out[cell] = iters_total[gc];
-    if (st_out) {
-      const int fl = flag[gc];
-      st_out[cell] = fl == 1 ? 0 : (fl == 3 ? 2 : 1);
+    const int fl = flag[gc];
+    const int st = fl == 1 ? 0 : (fl == 3 ? 2 : 1);
+    if (st_out) st_out[cell] = st;
+    // cells that stopped at max_iter / went non-finite, counted whether or
+    // not the caller asked for the per-cell status
+    if (st != 0) atomicAdd(stat_count + (st - 1), 1);
+  }
+}
+
+// Shared-factor finalize, one workgroup per column (group g = bandwidth,
+// column c = (tau, fold, lambda)): the rows of the column's fold give the CV
+// sums, the others the objective F = (1/n_v) sum loss + lambda alpha' K alpha
+// (f = K alpha in observation space, alpha zero on the held-out rows); alpha
+// is scattered with zeros at the held-out rows; status counts.
+__global__ __launch_bounds__(256) void cv_reduce_shared_kernel(
+    int n, int N, int C, int s0, int loss, double delta, const double* __restrict__ y,
+    const int32_t* __restrict__ fold, const int* __restrict__ cnv,
+    const int32_t* __restrict__ cfold, const double* __restrict__ lamv,
+    const double* __restrict__ tauv, const double* __restrict__ alpha_loc,
+    const double* __restrict__ fall, const double* __restrict__ betav,
+    const int* __restrict__ flag, const int* __restrict__ iters_total,
+    double* __restrict__ alpha_out, double* __restrict__ beta_out, double* __restrict__ obj_out,
+    double* __restrict__ cv_out, int32_t* __restrict__ err_out, int32_t* __restrict__ it_out,
+    int32_t* __restrict__ st_out, int* __restrict__ stat_count) {
+  __shared__ double red[PW];
+  const int64_t gc = blockIdx.x;
+  const int g = (int)(gc / C), c = (int)(gc % C);
+  const int64_t cell = (int64_t)(s0 + g) * C + c;
+  const int32_t v = cfold[gc];
+  const double lam = lamv[gc], tau = tauv[gc], b = betav[gc];
+  const double* A = alpha_loc + gc * N;
+  const double* f = fall + gc * N;
+  double* aout = alpha_out + cell * n;
+  double ls = 0.0, pen = 0.0, cs = 0.0, ce = 0.0;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const double fi = f[i] + b;
+    if (fold[i] == v) {
+      cs += loss_eval(loss, y[i], fi, tau);
+      if (loss != 2 && y[i] * fi <= 0.0) ce += 1.0;
+      aout[i] = 0.0;
+    } else {
+      ls += loss_value(loss, y[i], fi, delta, tau);
+      pen = fma(A[i], f[i], pen);
+      aout[i] = A[i];
     }
   }
+  ls = block_sum<PW>(ls, red);
+  pen = block_sum<PW>(pen, red);
+  cs = block_sum<PW>(cs, red);
+  ce = block_sum<PW>(ce, red);
+  if (threadIdx.x == 0) {
+    beta_out[cell] = b;
+    obj_out[cell] = ls / (double)cnv[gc] + lam * pen;
+    cv_out[cell] = cs;
+    if (err_out) err_out[cell] = (int32_t)ce;
+    if (it_out) it_out[cell] = iters_total[gc];
+    const int fl = flag[gc];
+    const int st = fl == 1 ? 0 : (fl == 3 ? 2 : 1);
+    if (st_out) st_out[cell] = st;
+    if (st != 0) atomicAdd(stat_count + (st - 1), 1);
+  }
+}
+
+// x[gc][i] = 0 on the rows held out of column gc (rfold[g][i] == cfold[gc])
+// and on padding rows (rfold = -1).
+__global__ __launch_bounds__(256) void mask_heldout_kernel(int N, int C,
+                                                           const int32_t* __restrict__ rfold,
+                                                           const int32_t* __restrict__ cfold,
+                                                           double* __restrict__ x) {
+  const int64_t gc = blockIdx.y;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= N) return;
+  const int32_t rf = rfold[(gc / C) * N + i];
+  if (rf < 0 || rf == cfold[gc]) x[gc * N + i] = 0.0;
 }
 
 // C = sum over S split-K parts (part s at part + s sP; column-major, ld
@@ -1288,7 +1362,47 @@ static int gemm_split(hipStream_t s, const GemmArgs& g, double* scratch, int64_t
   return 0;
 }
 
+// Shared-factor finalize: alpha = Q ahat with the held-out rows of each
+// column set to zero, f = K alpha with K built again from X over all points
+// (training and held-out predictions from one product), then the reductions.
+static int path_finalize_shared(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
+  int rc;
+  kc_begin(KMP_KC_FINALIZE, s);
+  const int64_t sNC = (int64_t)p.N * p.C;
+  const int64_t sP = (int64_t)p.G * sNC;
+  const int64_t cols = (int64_t)p.G * p.C;
+  GemmArgs g;
+  g.M = p.N; g.N = p.C; g.K = p.N; g.batch = p.G;
+  g.A = p.Q; g.lda = p.N; g.sA = (int64_t)p.N * p.N;
+  g.B = p.ahat; g.ldb = p.N; g.sB = sNC;
+  g.C = p.zmat; g.ldc = p.N; g.sC = sNC;
+  if ((rc = gemm_split(s, g, p.fpart, sP)) != 0) return rc;
+  hipLaunchKernelGGL(mask_heldout_kernel, dim3((unsigned)ceil_div(p.N, 256), (unsigned)cols),
+                     dim3(256), 0, s, p.N, p.C, p.rfold, p.cfold, p.zmat);
+  KMP_LAUNCH_CHECK();
+  if ((rc = rbf_blocks(s, fa.X, fa.d, fa.ldx, fa.nrm, fa.tidx, p.N, p.N, fa.tidx, p.N, p.N, 1,
+                       fa.inv2s2, fa.S_b, fa.kh, (int64_t)p.N * p.N, (int64_t)p.N * p.N, p.N)) != 0)
+    return rc;
+  GemmArgs gt = g;
+  gt.A = fa.kh;
+  gt.B = p.zmat;
+  gt.C = fa.ftrain;
+  if ((rc = gemm_split(s, gt, p.zpart, sP)) != 0) return rc;
+  hipLaunchKernelGGL(cv_reduce_shared_kernel, dim3((unsigned)cols), dim3(256), 0, s, fa.n, p.N,
+                     p.C, fa.s0, p.loss, fa.delta, fa.y, fa.fold, p.cnv, p.cfold, p.lam, p.tau,
+                     p.zmat, fa.ftrain, p.beta, p.flag, p.iters_total, fa.alpha, fa.beta_out,
+                     fa.objective, fa.cv_sum, fa.cv_err, fa.iters, fa.status, fa.stat_count);
+  KMP_LAUNCH_CHECK();
+  // alpha = Q ahat and f = K alpha; K written and read back (2d flops per
+  // entry); the column reads and writes
+  kc_end(KMP_KC_FINALIZE, s,
+         over_groups(p, [&](double n) { return 8.0 * (3.0 * n * n + 5.0 * n * p.C); }),
+         over_groups(p, [&](double n) { return 4.0 * n * n * p.C + 2.0 * n * n * fa.d; }));
+  return 0;
+}
+
 int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
+  if (fa.shared) return path_finalize_shared(s, p, fa);
   int rc;
   kc_begin(KMP_KC_FINALIZE, s);
   const int64_t sNC = (int64_t)p.N * p.C;
@@ -1302,14 +1416,20 @@ int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
   // (the parts of this product go to fpart, those of the next to zpart:
   // the training predictions are stored in fpart)
   if ((rc = gemm_split(s, g, p.fpart, sP)) != 0) return rc;
-  // training predictions K_v alpha = Q (B ahat)
-  if ((rc = band_apply(s, p, p.ahat, p.bmat)) != 0) return rc;
+  // training predictions K_v alpha in observation space: K_v is built again
+  // from X into the factor buffer (no longer needed) and multiplied by
+  // alpha, so the objective does not carry the factorisation's rounding
+  if ((rc = rbf_blocks(s, fa.X, fa.d, fa.ldx, fa.nrm, fa.tidx, p.N, p.N, fa.tidx, p.N, p.N,
+                       fa.V, fa.inv2s2, fa.S_b, fa.kh, (int64_t)fa.V * p.N * p.N,
+                       (int64_t)p.N * p.N, p.N)) != 0)
+    return rc;
   GemmArgs gt = g;
-  gt.B = p.bmat;
+  gt.A = fa.kh;
+  gt.B = p.zmat;
   gt.C = fa.ftrain;
   if ((rc = gemm_split(s, gt, p.zpart, sP)) != 0) return rc;
-  // held-out kernel blocks K[H_v, T_v] (into the factor buffer, no longer
-  // needed), then held-out predictions K[H_v, T_v] alpha (none in a refit)
+  // held-out kernel blocks K[H_v, T_v] (into the same buffer), then held-out
+  // predictions K[H_v, T_v] alpha (none in a refit)
   if (fa.Mh > 0 &&
       (rc = rbf_blocks(s, fa.X, fa.d, fa.ldx, fa.nrm, fa.hidx, fa.Mh, fa.Mh, fa.tidx, p.N, p.N,
                        fa.V, fa.inv2s2, fa.S_b, fa.kh, (int64_t)fa.V * p.N * p.N,
@@ -1324,15 +1444,17 @@ int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
   hipLaunchKernelGGL(cv_reduce_kernel, dim3((unsigned)(p.G * p.C)), dim3(256), 0, s, fa.n, p.N,
                      fa.Mh, p.C, fa.V, fa.Qt, fa.L, fa.s0, p.loss, fa.delta, fa.y, fa.tidx, fa.hidx,
                      p.nv, p.lam, p.tau, p.zmat, fa.ftrain, fa.fbuf, p.beta, p.flag, p.iters_total,
-                     fa.alpha, fa.beta_out, fa.objective, fa.cv_sum, fa.cv_err, fa.iters, fa.status);
+                     fa.alpha, fa.beta_out, fa.objective, fa.cv_sum, fa.cv_err, fa.iters, fa.status,
+                     fa.stat_count);
   KMP_LAUNCH_CHECK();
-  // three N x C x N products (alpha, training f, held-out f on Mh rows), the
-  // held-out kernel block (2d flops per entry) and the column reads/writes
+  // products alpha = Q ahat, f = K_v alpha and the held-out f (Mh rows); the
+  // training and held-out kernel blocks written and read back (2d flops per
+  // entry); the column reads and writes
   kc_end(KMP_KC_FINALIZE, s,
          over_groups(p, [&](double n) {
-           return 8.0 * (2.0 * n * n + 5.0 * n * p.C + 2.0 * fa.Mh * n + fa.Mh * p.C); }),
+           return 8.0 * (3.0 * n * n + 4.0 * n * p.C + 2.0 * fa.Mh * n + fa.Mh * p.C); }),
          over_groups(p, [&](double n) {
-           return 4.0 * n * n * p.C + 2.0 * fa.Mh * n * (p.C + fa.d); }));
+           return 4.0 * n * n * p.C + 2.0 * n * n * fa.d + 2.0 * fa.Mh * n * (p.C + fa.d); }));
   return 0;
 }
 

@@ -21,6 +21,7 @@ KMP_HINGE, KMP_LOGISTIC, KMP_CHECK = 0, 1, 2
 KMP_FLAG_RESTART = 1
 KMP_FLAG_GLOBAL_SOLVE = 2
 KMP_FLAG_REFIT = 4
+KMP_FLAG_SHARED_FACTOR = 8
 KMP_NKC = 10
 KERNEL_CLASSES = ("gram", "panel", "panel_wy", "trail_update", "q_form", "precompute", "gemm_f",
                   "gemm_zhat", "update", "finalize")
@@ -82,7 +83,7 @@ def lib():
         L.kmp_fit_path.argtypes = [_VP, C.POINTER(kmp_path_spec), _VP, C.c_int64, C.c_int64,
                                    C.c_int64, _VP, _DP, C.c_int32, _DP, C.c_int32, _DP, C.c_int32,
                                    _IP, C.c_int32, _VP, C.c_size_t, _VP, _VP, _VP, _VP, _VP, _VP,
-                                   _VP, _IP, C.POINTER(kmp_timings)]
+                                   _VP, _IP, _IP, C.POINTER(kmp_timings)]
         L.kmp_fit_path.restype = C.c_int
         L.kmp_make_folds.argtypes = [C.c_int64, C.c_int32, C.c_uint64, _IP]
         L.kmp_make_folds.restype = C.c_int
@@ -93,6 +94,12 @@ def lib():
         L.kmp_tridiag.restype = C.c_int
         L.kmp_band_reduce.argtypes = [_VP, _VP, C.c_int32, C.c_int32, _VP, _VP]
         L.kmp_band_reduce.restype = C.c_int
+        L.kmp_path_step.argtypes = [_VP, C.c_int32, C.c_double, _VP, C.c_int64, _VP, _DP, _DP,
+                                    C.c_int32, _VP, _VP, _VP, _VP, _VP]
+        L.kmp_path_step.restype = C.c_int
+        L.kmp_dgemm_grouped.argtypes = [_VP, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _VP, _VP,
+                                        _VP]
+        L.kmp_dgemm_grouped.restype = C.c_int
         L.kmp_strerror.argtypes = [C.c_int]
         L.kmp_strerror.restype = C.c_char_p
         L.kmp_version.argtypes = []
@@ -104,8 +111,8 @@ def lib():
 
 
 EXPORTED = ("kmp_default_spec", "kmp_workspace_bytes", "kmp_fit_path", "kmp_make_folds",
-            "kmp_rbf_gram", "kmp_tridiag", "kmp_band_reduce", "kmp_strerror", "kmp_version",
-            "kmp_kernel_class_name")
+            "kmp_rbf_gram", "kmp_tridiag", "kmp_band_reduce", "kmp_path_step",
+            "kmp_dgemm_grouped", "kmp_strerror", "kmp_version", "kmp_kernel_class_name")
 KMP_BAND = 16
 
 
@@ -189,8 +196,32 @@ def kmp_band_reduce(A, Q, band, stream=None) -> None:
                                  band.data_ptr()))
 
 
+def kmp_path_step(loss, delta, K, y, lambdas, alpha_in, beta_in, alpha_out, beta_out,
+                  kkt_out=None, taus=None, stream=None) -> None:
+    """a4-a7 on their own (see kmpath.h): K (n, n), y (n), alpha (C, n), beta
+    (C) device tensors; lambdas (and taus) host arrays of C entries."""
+    lam = _f64(lambdas)
+    tau = _f64(taus) if taus is not None else None
+    code = lib().kmp_path_step(
+        _stream_ptr(stream), LOSS_CODES[loss] if isinstance(loss, str) else int(loss),
+        float(delta if delta is not None else 1.0), K.data_ptr(), K.shape[0], y.data_ptr(),
+        lam.ctypes.data_as(_DP), tau.ctypes.data_as(_DP) if tau is not None else None, lam.size,
+        alpha_in.data_ptr(), beta_in.data_ptr(), alpha_out.data_ptr(), beta_out.data_ptr(),
+        kkt_out.data_ptr() if kkt_out is not None else None)
+    _check(code, allow_maxiter=False)
+
+
+def kmp_dgemm_grouped(A, B, C, stream=None) -> None:
+    """C[g] = A[g] @ B[g] for (G, M, K), (G, K, N), (G, M, N) device tensors."""
+    G, M, K = A.shape
+    N = B.shape[2]
+    _check(lib().kmp_dgemm_grouped(_stream_ptr(stream), G, M, N, K, A.data_ptr(), B.data_ptr(),
+                                   C.data_ptr()), allow_maxiter=False)
+
+
 def kmp_fit_path(stream, spec, X, y, sigmas, taus, lambdas, fold_id, V, workspace, ws_bytes,
-                 alpha, beta, objective, cv_sum, cv_err, iters, status, selected, timings) -> int:
+                 alpha, beta, objective, cv_sum, cv_err, iters, status, selected, timings,
+                 selected_joint=None) -> int:
     """Direct call of the C entry point (device pointers as ints, host arrays as numpy)."""
     sig, tau, lam, fold = _f64(sigmas), _f64(taus), _f64(lambdas), _i32(fold_id)
     return lib().kmp_fit_path(
@@ -202,6 +233,7 @@ def kmp_fit_path(stream, spec, X, y, sigmas, taus, lambdas, fold_id, V, workspac
         iters.data_ptr() if iters is not None else None,
         status.data_ptr() if status is not None else None,
         selected.ctypes.data_as(_IP) if selected is not None else None,
+        selected_joint.ctypes.data_as(_IP) if selected_joint is not None else None,
         C.byref(timings) if timings is not None else None)
 
 
@@ -210,9 +242,11 @@ class PathRunner:
 
     def __init__(self, X, y, loss, sigmas, lambdas, fold_id, V, taus=None, device="cuda",
                  sigma_batch: Optional[int] = None, kernel_timing=(), refit: bool = False,
-                 **spec_overrides):
+                 shared: bool = False, **spec_overrides):
         """refit=True: every (sigma, tau, lambda) on all n points (fold_id and V
-        are ignored; outputs have V = 1, no CV sums, no selection)."""
+        are ignored; outputs have V = 1, no CV sums, no selection).
+        shared=True: exact CV on one factor of the full K per bandwidth
+        (KMP_FLAG_SHARED_FACTOR); V = n with fold_id = 0..n-1 is leave-one-out."""
         import torch
         self.torch = torch
         self.loss = loss
@@ -220,6 +254,8 @@ class PathRunner:
         if refit:
             self.spec.flags |= KMP_FLAG_REFIT
             fold_id, V = np.zeros(np.shape(X)[0], dtype=np.int32), 1
+        if shared:
+            self.spec.flags |= KMP_FLAG_SHARED_FACTOR
         self.set_kernel_timing(kernel_timing)
         self.X = torch.as_tensor(np.ascontiguousarray(X), dtype=torch.float64, device=device) \
             if not isinstance(X, torch.Tensor) else X
@@ -247,6 +283,7 @@ class PathRunner:
         self.iters = torch.empty(self.shape, dtype=torch.int32, device=device)
         self.status = torch.empty(self.shape, dtype=torch.int32, device=device)
         self.selected = np.zeros((S, Q), dtype=np.int32)
+        self.selected_joint = np.zeros((Q, 2), dtype=np.int32)
         self.timings = kmp_timings()
         self.cells = cells
 
@@ -266,13 +303,15 @@ class PathRunner:
         code = kmp_fit_path(_stream_ptr(stream), self.spec, self.X, self.y, self.sigmas,
                             self.taus, self.lambdas, self.fold, self.V, self.workspace.data_ptr(),
                             self.ws_bytes, self.alpha, self.beta, self.objective, self.cv_sum,
-                            self.cv_err, self.iters, self.status, self.selected, self.timings)
+                            self.cv_err, self.iters, self.status, self.selected, self.timings,
+                            self.selected_joint)
         return _check(code)
 
     def results(self) -> dict:
         out = {k: getattr(self, k).cpu().numpy() for k in
                ("alpha", "beta", "objective", "cv_sum", "cv_err", "iters", "status")}
         out["selected"] = self.selected.copy()
+        out["selected_joint"] = self.selected_joint.copy()
         out["timings"] = self.timings.as_dict()
         return out
 

@@ -136,3 +136,52 @@ def test_binding_refuses_missing_library(monkeypatch):
     monkeypatch.setattr(kmpath, "LIB_PATH", "/nonexistent/libkmpath.so")
     with pytest.raises(RuntimeError):
         kmpath.lib()
+
+
+def test_shared_factor_workspace(km):
+    """KMP_FLAG_SHARED_FACTOR: one group of all n rows per bandwidth with
+    V x L columns; refused together with a refit, with V > n, and above the
+    largest shared order."""
+    w = W.get("C3")
+    fold = W.make_folds(w.n, w.V, w.fold_seed)
+    spec = km.kmp_default_spec("hinge")
+    spec.flags |= km.KMP_FLAG_SHARED_FACTOR
+    b = km.kmp_workspace_bytes(spec, w.n, w.d, w.L, fold, w.V, 1, 1, 1)
+    N = 10048                              # 10000 rounded up to 64
+    assert b > 2 * N * N * 8
+    plain = km.kmp_default_spec("hinge")
+    b_fold = km.kmp_workspace_bytes(plain, w.n, w.d, w.L, fold, w.V, 1, 1, 1)
+    assert b < b_fold                      # one n x n pair against ten of 9024 x 9024
+    # leave-one-out: V = n, fold i = point i
+    loo = np.arange(200, dtype=np.int32)
+    assert km.kmp_workspace_bytes(spec, 200, 3, 10, loo, 200, 1, 1, 1) > 0
+    assert km.kmp_workspace_bytes(spec, 200, 3, 10, loo, 201, 1, 1, 1) == 0
+    both = km.kmp_default_spec("hinge")
+    both.flags |= km.KMP_FLAG_SHARED_FACTOR | km.KMP_FLAG_REFIT
+    assert km.kmp_workspace_bytes(both, 200, 3, 10, np.zeros(200, np.int32), 1, 1, 1, 1) == 0
+    big = np.arange(41000, dtype=np.int32) % 5
+    assert km.kmp_workspace_bytes(spec, 41000, 3, 2, big, 5, 1, 1, 1) == 0
+
+
+def test_single_step_entry_points_validate_on_host(km):
+    """kmp_path_step and kmp_dgemm_grouped refuse bad arguments before any
+    device work; an empty product is a no-op."""
+    L = km.lib()
+    lam = np.array([0.1, -1.0])
+    tau = np.array([0.5, 0.5])
+    dp = lambda a: a.ctypes.data_as(C.POINTER(C.c_double))
+    ok_lam = np.array([0.1, 1.0])
+    # negative lambda, bad tau, bad loss, n < 2
+    assert L.kmp_path_step(None, 0, 0.1, 0x1000, 50, 0x1000, dp(lam), None, 2, 0x1000, 0x1000,
+                           0x1000, 0x1000, None) == km.KMP_EINVAL
+    assert L.kmp_path_step(None, 2, 0.1, 0x1000, 50, 0x1000, dp(ok_lam), dp(np.array([0.5, 1.0])),
+                           2, 0x1000, 0x1000, 0x1000, 0x1000, None) == km.KMP_EINVAL
+    assert L.kmp_path_step(None, 7, 0.1, 0x1000, 50, 0x1000, dp(ok_lam), None, 2, 0x1000, 0x1000,
+                           0x1000, 0x1000, None) == km.KMP_EINVAL
+    assert L.kmp_path_step(None, 0, 0.1, 0x1000, 1, 0x1000, dp(ok_lam), None, 2, 0x1000, 0x1000,
+                           0x1000, 0x1000, None) == km.KMP_EINVAL
+    assert L.kmp_path_step(None, 0, 0.0, 0x1000, 50, 0x1000, dp(ok_lam), dp(tau), 2, 0x1000,
+                           0x1000, 0x1000, 0x1000, None) == km.KMP_EINVAL
+    assert L.kmp_dgemm_grouped(None, -1, 4, 4, 4, 0x1000, 0x1000, 0x1000) == km.KMP_EINVAL
+    assert L.kmp_dgemm_grouped(None, 2, 4, 4, 4, None, 0x1000, 0x1000) == km.KMP_EINVAL
+    assert L.kmp_dgemm_grouped(None, 0, 4, 4, 4, None, None, None) == km.KMP_OK

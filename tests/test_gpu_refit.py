@@ -12,7 +12,7 @@ import pytest
 import workloads as W
 from oracle import gram as OG
 from oracle.cell import beta_interval, objective, solve_cell
-from tests.gpu_common import ALPHA_RTOL, OBJ_RTOL, announce, device
+from tests.gpu_common import ALPHA_RTOL, OBJ_RTOL, ORACLE_KKT, announce, device
 
 pytestmark = pytest.mark.gpu
 
@@ -39,7 +39,7 @@ def _refit(inp, loss):
 
 def _check_cells(g, inp, loss, cells):
     X, y = inp["X"], inp["y"]
-    worst = {"obj": 0.0, "alpha": 0.0}
+    worst = {"obj": 0.0, "alpha": 0.0, "oracle_kkt": 0.0}
     grams = {}
     for (s, q, l) in cells:
         if s not in grams:
@@ -48,6 +48,8 @@ def _check_cells(g, inp, loss, cells):
         tau = inp["taus"][q] if loss == "check" else None
         lam = inp["lambdas"][l]
         a, b, info = solve_cell(K, y, lam, loss, DELTA, tau, tol=1e-13)
+        assert info["kkt"] <= ORACLE_KKT, ("oracle cell not converged", (s, q, l), info["kkt"])
+        worst["oracle_kkt"] = max(worst["oracle_kkt"], info["kkt"])
         Fo = objective(K, y, a, b, lam, loss, DELTA, tau)
         Fg = g["objective"][s, q, 0, l]
         assert abs(Fg - Fo) <= OBJ_RTOL * abs(Fo), ((s, q, l), Fg, Fo)
