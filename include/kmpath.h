@@ -205,6 +205,19 @@ int kmp_rbf_gram(void* stream, const double* X, int64_t n, int64_t d, int64_t ld
                  const int32_t* rows, int64_t m, const int32_t* cols, int64_t p,
                  const double* sigmas, int32_t S, double* out, int64_t ld_out);
 
+/* kmp_rbf_gram for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same arguments, layout, results and errors, but every temporary (the
+ * squared row norms of X and the bandwidth factors) lives in a static device
+ * array of 65536 doubles (512 KiB) that the library holds on each device
+ * until the process ends, and the call allocates nothing. n must be at most
+ * 65528 (KMP_EINVAL otherwise, before any device work). All calls on one
+ * device share that array: calls that overlap on one device (different
+ * streams or threads) race and must be serialised by the caller.            */
+int kmp_rbf_gram_noalloc(void* stream, const double* X, int64_t n, int64_t d, int64_t ldx,
+                         const int32_t* rows, int64_t m, const int32_t* cols, int64_t p,
+                         const double* sigmas, int32_t S, double* out, int64_t ld_out);
+
 /* One-stage alternative to a2 (kmp_fit_path uses kmp_band_reduce): G
  * symmetric N x N matrices A (DEVICE, row-major, packed,
  * matrix g at A + g*N*N; destroyed) are reduced to A_g = Q_g T_g Q_g' with

@@ -149,6 +149,25 @@ __global__ __launch_bounds__(256) void rbf_blocks_kernel(
       }
 }
 
+// out[i] = a.v[i] for i < count (small parameter arrays written without a
+// host-to-device copy: the values travel as a kernel argument).
+__global__ void store_small_kernel(Small8 a, int count, double* __restrict__ out) {
+  const int i = threadIdx.x;
+  if (i < count) out[i] = a.v[i];
+}
+
+int store_small(hipStream_t s, const double* vals, int count, double* out) {
+  if (count < 0 || count > 8) {
+    set_error("store_small: at most 8 values");
+    return KMP_EINVAL;
+  }
+  Small8 a{};
+  for (int i = 0; i < count; ++i) a.v[i] = vals[i];
+  hipLaunchKernelGGL(store_small_kernel, dim3(1), dim3(64), 0, s, a, count, out);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
 int rbf_blocks(hipStream_t s, const double* X, int64_t d, int64_t ldx, const double* nrm,
                const int32_t* idx_r, int64_t sr, int64_t m, const int32_t* idx_c, int64_t sc,
                int64_t p, int nb, const double* inv2s2, int S, double* out, int64_t sout_s,

@@ -76,6 +76,34 @@ void kc_end(int cls, hipStream_t s, double bytes, double flops) {
 
 namespace {
 
+// Device scratch of the allocation-free Gram entry point: the bandwidth
+// factors (8 doubles) and the squared row norms of X (up to
+// kStaticScratchDoubles - 8 rows). Each device holds its own copy for the
+// life of the process; host code reaches it only through the address
+// hipGetSymbolAddress returns on that device (static_scratch below).
+constexpr size_t kStaticScratchDoubles = (size_t)1 << 16;   // 512 KiB
+static __device__ __align__(256) double scratch[kStaticScratchDoubles];
+
+int static_scratch(double** out) {
+  int dev = 0;
+  KMP_HIP_TRY(hipGetDevice(&dev));
+  static std::mutex mu;
+  static std::map<int, double*> ptrs;
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = ptrs.find(dev);
+  if (it == ptrs.end()) {
+    void* p = nullptr;
+    KMP_HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) {
+      set_error("static scratch has no device address");
+      return KMP_EHIP;
+    }
+    it = ptrs.emplace(dev, static_cast<double*>(p)).first;
+  }
+  *out = it->second;
+  return 0;
+}
+
 // A second stream per device for work that can run beside the caller's
 // stream (joined back through events); created on first use and kept for
 // the life of the process, at the default priority.
@@ -503,6 +531,43 @@ int kmp_rbf_gram(void* stream, const double* X, int64_t n, int64_t d, int64_t ld
   KMP_HIP_TRY(hipFreeAsync(dinv, s));
   KMP_HIP_TRY(hipStreamSynchronize(s));
   return rc;
+}
+
+int kmp_rbf_gram_noalloc(void* stream, const double* X, int64_t n, int64_t d, int64_t ldx,
+                         const int32_t* rows, int64_t m, const int32_t* cols, int64_t p,
+                         const double* sigmas, int32_t S, double* out, int64_t ld_out) {
+  hipStream_t s = (hipStream_t)stream;
+  if (!X || !rows || !cols || !sigmas || !out || n < 1 || d < 1 || ldx < d || m < 0 || p < 0 ||
+      S < 1 || S > 8 || ld_out < p) {
+    set_error("kmp_rbf_gram_noalloc: invalid arguments");
+    return KMP_EINVAL;
+  }
+  if ((size_t)n > kStaticScratchDoubles - 8) {
+    set_error("kmp_rbf_gram_noalloc: n = " + std::to_string(n) + " above the " +
+              std::to_string(kStaticScratchDoubles - 8) + " rows its static scratch holds");
+    return KMP_EINVAL;
+  }
+  double f2[8];
+  for (int i = 0; i < S; ++i) {
+    if (!(sigmas[i] > 0.0) || !std::isfinite(sigmas[i])) {
+      set_error("kmp_rbf_gram_noalloc: sigma must be positive");
+      return KMP_EINVAL;
+    }
+    f2[i] = 1.0 / (2.0 * sigmas[i] * sigmas[i]);
+  }
+  if (m == 0 || p == 0) return KMP_OK;
+  double* sc = nullptr;
+  int rc = static_scratch(&sc);
+  if (rc != 0) return rc;
+  double* dinv = sc;          // S bandwidth factors
+  double* nrm = sc + 8;       // n squared row norms
+  if ((rc = store_small(s, f2, S, dinv)) != 0) return rc;
+  if ((rc = row_norms(s, X, n, d, ldx, nrm)) != 0) return rc;
+  if ((rc = rbf_blocks(s, X, d, ldx, nrm, rows, 0, m, cols, 0, p, 1, dinv, S, out, m * ld_out, 0,
+                       ld_out)) != 0)
+    return rc;
+  KMP_HIP_TRY(hipStreamSynchronize(s));
+  return KMP_OK;
 }
 
 int kmp_tridiag(void* stream, double* A, int32_t G, int32_t N, double* Qout, double* diag,

@@ -66,6 +66,13 @@ int count_nonfinite(hipStream_t s, const double* X, int64_t n, int64_t d, int64_
 // Squared row norms of X (n x d, ldx): nrm[i] = sum_k X[i][k]^2.
 int row_norms(hipStream_t s, const double* X, int64_t n, int64_t d, int64_t ldx, double* nrm);
 
+// Up to 8 doubles passed by value to a one-wavefront kernel that stores them
+// at out (device).
+struct Small8 {
+  double v[8];
+};
+int store_small(hipStream_t s, const double* vals, int count, double* out);
+
 // For each of `nb` index blocks (blockIdx.z = block q), rows idx_r + q*sr,
 // cols idx_c + q*sc (m and p entries, negative = padding), write for each of
 // S bandwidths: out + (s*sout_s + q*sout_q) + i*ld + j.

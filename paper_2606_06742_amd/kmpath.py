@@ -90,6 +90,8 @@ def lib():
         L.kmp_rbf_gram.argtypes = [_VP, _VP, C.c_int64, C.c_int64, C.c_int64, _VP, C.c_int64, _VP,
                                    C.c_int64, _DP, C.c_int32, _VP, C.c_int64]
         L.kmp_rbf_gram.restype = C.c_int
+        L.kmp_rbf_gram_noalloc.argtypes = L.kmp_rbf_gram.argtypes
+        L.kmp_rbf_gram_noalloc.restype = C.c_int
         L.kmp_tridiag.argtypes = [_VP, _VP, C.c_int32, C.c_int32, _VP, _VP, _VP]
         L.kmp_tridiag.restype = C.c_int
         L.kmp_band_reduce.argtypes = [_VP, _VP, C.c_int32, C.c_int32, _VP, _VP]
@@ -111,7 +113,8 @@ def lib():
 
 
 EXPORTED = ("kmp_default_spec", "kmp_workspace_bytes", "kmp_fit_path", "kmp_make_folds",
-            "kmp_rbf_gram", "kmp_tridiag", "kmp_band_reduce", "kmp_path_step",
+            "kmp_rbf_gram", "kmp_rbf_gram_noalloc", "kmp_tridiag", "kmp_band_reduce",
+            "kmp_path_step",
             "kmp_dgemm_grouped", "kmp_strerror", "kmp_version", "kmp_kernel_class_name")
 KMP_BAND = 16
 
