@@ -18,6 +18,8 @@ that the C library's ``kmp_make_folds`` reproduces it bit for bit.
 """
 from __future__ import annotations
 
+import json
+import os
 from dataclasses import dataclass, field
 from typing import Tuple
 
@@ -226,15 +228,36 @@ def make_data(w: Workload) -> Tuple[np.ndarray, np.ndarray]:
     return np.ascontiguousarray(X, dtype=np.float64), np.ascontiguousarray(y, dtype=np.float64)
 
 
-def make_inputs(w: Workload, with_sigma: bool = True) -> dict:
-    """All inputs of one workload: X, y, fold ids, lambdas, sigmas, taus."""
+MEDIANS_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "medians.json")
+
+
+def stored_median(name: str):
+    """The median pairwise distance of workload `name` as stored in
+    medians.json (written by ``python -m workloads.make_medians``, which calls
+    median_pairwise_distance on make_data's output), or None."""
+    try:
+        with open(MEDIANS_PATH) as fh:
+            return float.fromhex(json.load(fh)[name])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def make_inputs(w: Workload, with_sigma: bool = True, stored: bool = True) -> dict:
+    """All inputs of one workload: X, y, fold ids, lambdas, sigmas, taus.
+
+    The bandwidths are multiples of the median pairwise distance; with
+    stored=True the value stored for the workload is used when there is one
+    (the n = 40000 workload's median takes minutes to recompute), else it is
+    computed here."""
     X, y = make_data(w)
     fold = make_folds(w.n, w.V, w.fold_seed)
     lam = lambda_grid(w.lam_lo, w.lam_hi, w.L)
     out = {"X": X, "y": y, "fold_id": fold, "V": w.V, "lambdas": lam,
            "loss": w.loss, "taus": np.array(w.taus, dtype=np.float64)}
     if with_sigma:
-        med = median_pairwise_distance(X)
+        med = stored_median(w.name) if stored else None
+        if med is None:
+            med = median_pairwise_distance(X)
         out["sigma_median"] = med
         out["sigmas"] = np.array([m * med for m in w.sigma_mults])
     return out
