@@ -80,8 +80,8 @@ extern "C" {
                           exact leave-one-out CV (Algorithm 1 as printed).  */
 #define KMP_FLAG_GLOBAL_SOLVE 2 /* keep the banded solve's working vector in
                           device memory at every order (it is there anyway
-                          above 8192 padded rows per fold, where it does not
-                          fit in LDS); results are identical either way     */
+                          above the rows one workgroup's LDS holds: 20224
+                          padded rows on gfx950); results agree to rounding */
 
 /* Kernel classes timed with HIP events when their bit is set in
  * kmp_path_spec.timing_mask (1 << class). */

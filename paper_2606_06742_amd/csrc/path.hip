@@ -420,13 +420,28 @@ __device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
 // Columns (wavefronts) per workgroup and where the solve keeps its vector.
 // With the vector in LDS a workgroup holds one N-vector per column plus
 // `extra` doubles of per-column tiles, and four columns share a workgroup
-// when they fit in 64 KiB, else each has its own. Orders above kLdsVecMax
-// (or every order, with KMP_FLAG_GLOBAL_SOLVE) keep the vector in device
+// when they fit in 64 KiB, else each has its own. Orders above what one
+// workgroup's LDS holds (lds_vec_max: the device's LDS per workgroup, 160 KiB
+// on gfx950, less a margin for the kernels' static arrays; never below 8192
+// rows), or every order with KMP_FLAG_GLOBAL_SOLVE, keep the vector in device
 // memory and only a two-block ring in LDS.
 constexpr int PTILE = 2 * BND * (BND + 1) + 5 * BND + (BND + 1) * BND;   // LDS of one column's LDL' sweep
 constexpr int RING = 2 * BND;                          // LDS ring of the device-memory solve
-constexpr int kLdsVecMax = 8192;
-static bool path_global_vec(const PathArrays& p) { return p.global_solve || p.N > kLdsVecMax; }
+constexpr int kLdsVecFloor = 8192;
+static int lds_vec_max() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return kLdsVecFloor;
+  if (cached[dev] == 0) {
+    int bytes = 0;
+    if (hipDeviceGetAttribute(&bytes, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+      bytes = 0;
+    const int rows = (bytes - 2048) / (int)sizeof(double) / 64 * 64;
+    cached[dev] = rows > kLdsVecFloor ? rows : kLdsVecFloor;
+  }
+  return cached[dev];
+}
+static bool path_global_vec(const PathArrays& p) { return p.global_solve || p.N > lds_vec_max(); }
 static int path_lds_doubles(const PathArrays& p, int extra) {
   return path_global_vec(p) ? extra + RING : p.N + extra;
 }
@@ -907,7 +922,7 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
 }
 
 // The update of one column per 256-thread workgroup, for orders whose
-// vector fits in LDS (N <= kLdsVecMax): the element passes are spread over
+// vector fits in LDS (N <= lds_vec_max()): the element passes are spread over
 // the four wavefronts (four times the loads in flight of one wavefront) and
 // wavefront 0 alone runs the banded solve on the LDS vector:
 //   w = zhat + 2 lambda abar (LDS), t = u'w, ||w||, d0; KKT decision;

@@ -13,7 +13,10 @@ from typing import Optional
 
 import numpy as np
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkmpath.so")
+# KMPATH_LIB points the binding at another build of the library (the
+# host-sanitized build of the CPU tests); default: the in-tree libkmpath.so
+LIB_PATH = os.environ.get("KMPATH_LIB") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libkmpath.so")
 
 KMP_OK, KMP_WMAXITER = 0, 1
 KMP_EINVAL, KMP_EFOLD, KMP_EWORKSPACE, KMP_EHIP, KMP_ENONFINITE = -1, -2, -3, -4, -5

@@ -46,8 +46,11 @@ def compare_cells(g, o, inp, loss, cells=None, delta=2.0 ** -6, cv_expected=None
     for (s, q, v, l) in cells:
         key = (s, v)
         if key not in blocks:
-            blocks[key] = OG.fold_blocks(X, fold, v, inp["sigmas"][s])
-        Kv, Kc, T, H = blocks[key]
+            # only the held-out block K[H_v, T_v] is needed here
+            T = np.flatnonzero(fold != v)
+            H = np.flatnonzero(fold == v)
+            blocks[key] = (OG.rbf_gram(X[H], X[T], inp["sigmas"][s]), T, H)
+        Kc, T, H = blocks[key]
         tau = inp["taus"][q] if loss == "check" else None
         # the reference itself must be solved: its own residual, not a stall
         ko = float(o["kkt"][s, q, v, l])
