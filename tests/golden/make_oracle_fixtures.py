@@ -138,9 +138,16 @@ def job_c5_cells(args):
                      probe=(0,) if args.probe_c5 else (), on_cell=save)
 
 
+CACHE = os.path.join(ROOT, "_build", "fixture_cache")
+
+
 def _sel_task(t):
-    X, y, fold, v, sigma, lambdas, ls, loss, delta, tau, s = t
+    X, y, fold, v, sigma, lambdas, ls, loss, delta, tau, s, path = t
+    if os.path.exists(path):                       # finished by an earlier run
+        return s, v, dict(np.load(path, allow_pickle=False))
     r = solve_fold_cells(X, y, fold, v, sigma, lambdas, ls, loss, delta, tau)
+    np.savez(path + ".tmp.npz", **r)
+    os.replace(path + ".tmp.npz", path)
     return s, v, r
 
 
@@ -149,12 +156,19 @@ def _selection(name, loss, delta, chunks, workers):
     inp = W.make_inputs(w)
     S, V, L = len(inp["sigmas"]), w.V, w.L
     tasks = []
+    # each task's cells are kept under _build/fixture_cache until the job
+    # ends, so an interrupted job resumes where it stopped
+    cache = os.path.join(CACHE, name)
+    os.makedirs(cache, exist_ok=True)
     for s in range(S):
         for v in range(V):
             for c in range(chunks):
                 ls = tuple(range(c, L, chunks))
                 tasks.append((inp["X"], inp["y"], inp["fold_id"], v, float(inp["sigmas"][s]),
-                              inp["lambdas"], ls, loss, delta, None, s))
+                              inp["lambdas"], ls, loss, delta, None, s,
+                              os.path.join(cache, f"s{s}_v{v}_c{c}.npz")))
+    # the longest tasks (smallest lambdas first in chunk 0) go first
+    tasks.sort(key=lambda t: t[6][0])
     cv = np.zeros((S, V, L))
     err = np.zeros((S, V, L), dtype=np.int64)
     kkt = np.zeros((S, V, L))
