@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="C3")
+    ap.add_argument("--sigma-index", type=int, default=None,
+                    help="time only this bandwidth of the workload (e.g. 1: sigma = median "
+                         "distance for the five-bandwidth n = 40000 workload, one GPU's unit)")
     ap.add_argument("--shared", action="store_true",
                     help="time the shared-factor exact-CV mode instead of the per-fold mode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -271,6 +274,8 @@ def main():
 
     w = W.get(args.workload)
     inp = W.make_inputs(w)
+    if args.sigma_index is not None:
+        inp["sigmas"] = inp["sigmas"][args.sigma_index:args.sigma_index + 1]
     dev = torch.device("cuda:0")
     log(f"inputs of {w.name} ready")
     runner = km.PathRunner(inp["X"], inp["y"], w.loss, inp["sigmas"], inp["lambdas"],
@@ -291,11 +296,13 @@ def main():
     assert np.all(res["status"] == 0), "some cells did not converge"
 
     # the counter summaries are of the per-fold CV run: none matches another mode
-    tag = w.name + ("-refit" if args.refit else "") + ("-shared" if args.shared else "")
+    tag = (w.name + ("-refit" if args.refit else "") + ("-shared" if args.shared else "") +
+           (f"-sigma{args.sigma_index}" if args.sigma_index is not None else ""))
     roof = roofline(kt, tag)
     metric = "(sigma x lambda) fits/sec for the full-data refit" if args.refit else METRIC
-    shape = (f"{len(w.sigma_mults)} sigmas x {w.L} lambdas on all {w.n} points"
-             if args.refit else f"{len(w.sigma_mults)} sigmas x {w.V} folds x {w.L} lambdas")
+    nsig = len(inp["sigmas"])
+    shape = (f"{nsig} sigmas x {w.L} lambdas on all {w.n} points"
+             if args.refit else f"{nsig} sigmas x {w.V} folds x {w.L} lambdas")
     mode = "refit" if args.refit else ("shared-factor exact CV" if args.shared else "per-fold factors")
     out = {
         "metric": metric, "value": value, "unit": "fits/s", "n_gpus": 1, "steps": args.steps,
@@ -304,7 +311,7 @@ def main():
         "config": {"workload": f"{w.name}: {w.description}; n={w.n}, d={w.d}, {shape} = "
                                f"{runner.cells} cells, loss={w.loss}, {mode}",
                    "cells": runner.cells, "n": w.n, "d": w.d, "folds": 1 if args.refit else w.V,
-                   "lambdas": w.L, "sigmas": len(w.sigma_mults), "mode": mode},
+                   "lambdas": w.L, "sigmas": nsig, "mode": mode},
         "phases_ms_per_step": {k: v / args.steps for k, v in phases.items()},
         "path_fits_per_s": runner.cells / (1e-3 * (phases["precompute_ms"] + phases["path_ms"]
                                                    + phases["finalize_ms"]) / args.steps),

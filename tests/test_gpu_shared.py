@@ -122,3 +122,24 @@ def test_leave_one_out(loss):
     worst = compare_cells(g, o, inp, loss, cv_expected=cv)
     assert np.array_equal(g["selected"], expected_selection(o, cv, inp["lambdas"], n))
     print(loss, "leave-one-out worst", worst, "selected", g["selected"].ravel())
+
+
+def test_shared_c3_full_size():
+    """The n = 10000 smoothed-hinge workload (10 folds x 100 lambdas = 1000
+    columns on one factor of order 10000): the seven stored oracle cells of
+    fold 0 (the four smallest lambdas among them), every cell's held-out sum
+    against the oracle's, and the selected lambda."""
+    from tests.gpu_common import check_selection, fixture, fixture_cells
+    w = W.get("C3")
+    inp = W.make_inputs(w)
+    fx = fixture("c3_cells.npz")
+    announce("shared factor C3 (hinge, n=10000, 1000 columns on one factor)")
+    g = _gpu(inp, "hinge", True)
+    print("C3 shared timings", {k: v for k, v in g["timings"].items() if not isinstance(v, list)},
+          flush=True)
+    T = np.flatnonzero(inp["fold_id"] != 0)
+    o, cells = fixture_cells(fx, g["alpha"].shape, T)
+    worst = compare_cells(g, o, inp, "hinge", cells=cells)
+    sel = fixture("c3_selection.npz")
+    cvw = check_selection(g, sel, w.n, "C3 shared")
+    print("C3 shared fixture cells worst", worst, "all-cell held-out sums", cvw)
