@@ -26,7 +26,9 @@ Parity status per function (what pins it; see tests/test_oracle_*.py):
                     decrease of F, fixed point at the cell solution
 * path.fit_path     composition of the above; selection rule by brute force
 * dual.*            closed-form conjugates checked pointwise by grid search
+* hinge.*           brute force over all L/E/R patterns (n <= 7), zero duality
+                    gap against the hinge dual, sklearn's SVC
 """
-from . import losses, gram, cell, mm, dual, path  # noqa: F401
+from . import losses, gram, cell, mm, dual, path, hinge  # noqa: F401
 from .path import fit_path, select, select_joint  # noqa: F401
 from .cell import solve_cell, objective, kkt_residual, beta_interval, certify_cell  # noqa: F401
