@@ -47,6 +47,8 @@ extern "C" {
 
 #define KMP_OK 0
 #define KMP_WMAXITER 1     /* finished; some cells stopped at max_iter      */
+#define KMP_WNOTEXACT 2    /* finished; with KMP_FLAG_EXACT_HINGE some cells
+                              kept their smoothed solution (status 3)       */
 #define KMP_EINVAL (-1)    /* bad shape, lambda <= 0, sigma <= 0, tau, loss  */
 #define KMP_EFOLD (-2)     /* fold id out of range, empty fold, one class    */
 #define KMP_EWORKSPACE (-3)/* workspace missing or too small                 */
@@ -78,6 +80,23 @@ extern "C" {
                           the one factor. Same outputs as the per-fold mode;
                           n <= 40960. With V = n and fold_id[i] = i this is
                           exact leave-one-out CV (Algorithm 1 as printed).  */
+#define KMP_FLAG_EXACT_HINGE 16 /* finite smoothing to the exact hinge SVM
+                          (Appendix A.1; Algorithm 1's outer loop ends when
+                          the SVM's KKT conditions hold): after the smoothing
+                          stages every cell's exact minimiser of eq.
+                          (kernelsvm) on its fold is recovered from the point
+                          sets of its smoothed solution (below / on / above
+                          the margin: a linear system on the points on the
+                          margin, solved on the GPU, sets corrected until the
+                          KKT conditions hold to 1e-9, at most 128 rounds).
+                          alpha, beta, the held-out sums are the exact
+                          solution's and objective is the hinge objective of
+                          eq. (kernelsvm). A cell with more margin points than
+                          its system holds (min(N, 384), N its padded order)
+                          or not settled keeps the smoothed solution, status
+                          3, return KMP_WNOTEXACT. Hinge loss, per-fold
+                          factors only; the workspace grows by about
+                          (min(N, 384) + 1)^2 doubles per column.           */
 #define KMP_FLAG_GLOBAL_SOLVE 2 /* keep the banded solve's working vector in
                           device memory at every order (it is there anyway
                           above the rows one workgroup's LDS holds: 20224
@@ -108,7 +127,8 @@ typedef struct {
   int32_t max_iter;    /* iterations per stage per cell (100000)            */
   int32_t poll_every;  /* iterations between host convergence polls (8)     */
   int32_t flags;       /* KMP_FLAG_RESTART (default on), KMP_FLAG_GLOBAL_SOLVE,
-                          KMP_FLAG_REFIT, KMP_FLAG_SHARED_FACTOR            */
+                          KMP_FLAG_REFIT, KMP_FLAG_SHARED_FACTOR,
+                          KMP_FLAG_EXACT_HINGE                              */
   int32_t timing_mask; /* kernel classes to time with HIP events (default 0) */
   int32_t timing_every;/* bracket one launch in every timing_every launches
                           of a timed class (default 1: all)                 */
@@ -165,7 +185,9 @@ size_t kmp_workspace_bytes(const kmp_path_spec* spec, int64_t n, int64_t d,
  *   cv_sum   [S][Q][V][L]   sum over held-out j of the unsmoothed loss
  *   cv_err   [S][Q][V][L]   held-out y f <= 0 count (0 for KMP_CHECK); may be NULL
  *   iters    [S][Q][V][L]   iterations summed over stages; may be NULL
- *   status   [S][Q][V][L]   0 converged, 1 max_iter, 2 non-finite; may be NULL
+ *   status   [S][Q][V][L]   0 converged, 1 max_iter, 2 non-finite, 3 exact
+ *                           hinge solution not reached (KMP_FLAG_EXACT_HINGE);
+ *                           may be NULL
  *   selected HOST [S][Q]: argmin_l sum_v cv_sum/n, ties to larger lambda; may be NULL
  *   selected_joint HOST [Q][2]: the (s, l) minimising sum_v cv_sum/n over all
  *            bandwidths and penalties, ties to the larger lambda, then the

@@ -140,6 +140,21 @@ def solve_exact_hinge(K, y, lam, delta0=2.0 ** -12, max_rounds=200, tol=1e-9):
         state[bad_L | bad_R] = 1
     a = np.clip(a, 0.0, 1.0) if ok else a
     alpha = y * a / (2.0 * n * lam)
+    if ok and beta_lo == beta_hi:
+        # points on the margin with a strictly inside (0, 1) pin beta; when
+        # every one sits at a bound the intercept is an interval, the points
+        # at a = 1 keeping u <= 1 and those at a = 0 keeping u >= 1
+        E = np.flatnonzero(state == 1)
+        free = (a[E] > tol) & (a[E] < 1.0 - tol)
+        if not free.any():
+            g = K @ alpha
+            t = 1.0 - y * g
+            Lb = np.flatnonzero((state == 0) | ((state == 1) & (a >= 1.0 - tol)))
+            Rb = np.flatnonzero((state == 2) | ((state == 1) & (a <= tol)))
+            up = np.concatenate([t[Lb][y[Lb] > 0], -t[Rb][y[Rb] < 0]])
+            dn = np.concatenate([-t[Lb][y[Lb] < 0], t[Rb][y[Rb] > 0]])
+            beta_hi = float(up.min()) if up.size else np.inf
+            beta_lo = float(dn.max()) if dn.size else -np.inf
     P = hinge_objective(K, y, alpha, beta, lam)
     D = hinge_dual(K, y, a, lam)
     info = {"rounds": rounds, "E": int(np.count_nonzero(state == 1)), "converged": ok,

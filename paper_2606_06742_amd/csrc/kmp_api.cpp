@@ -176,6 +176,13 @@ struct Bump {
 
 constexpr int kPanel = 32;       // Householder panel width
 constexpr int64_t kMaxColumns = 65535;  // columns (groups x columns per group) per batch
+// Exact hinge recovery: the largest margin set a column's system holds, and
+// the doubles of that system (square matrix and right-hand side).
+inline int exact_emax(int N) { return std::min(N, 384); }
+inline int64_t exact_sys_doubles(int N) {
+  const int64_t m = exact_emax(N) + 1;
+  return m * m + m;
+}
 constexpr int kRowAlign = 64;    // padding of the per-fold matrix order
 constexpr size_t kAlign = 256;
 
@@ -185,6 +192,7 @@ struct Plan {
   int N = 0, C = 0, G = 0, RT = 0;
   int Mh = 0;                    // held-out rows per fold, padded (max m_v rounded up to 64)
   bool shared = false;           // one factor of the full K per bandwidth (exact-CV form)
+  bool exact = false;            // exact hinge recovery after the stages
   int nblk = 0;                  // row lists (groups per bandwidth): V, or 1 when shared
   std::vector<int> nv;           // per fold
   size_t bytes = 0;
@@ -212,6 +220,10 @@ struct Layout {
   double *beta, *bbar, *rmom, *gcoef, *kkt, *coef, *lam, *taucol, *fbuf, *nrm, *inv2s2;
   int *flag, *moved, *iters, *iters_total, *active, *nvg, *chk, *cmap, *nact, *stat_count, *cnv;
   int32_t *tidx, *hidx, *fold, *rfold, *cfold;
+  // exact hinge recovery (only with KMP_FLAG_EXACT_HINGE)
+  int32_t *ex_state, *ex_elist;
+  int *ex_ne, *ex_flag, *ex_pending;
+  double *ex_sumyl, *ex_beta, *ex_sys;
 };
 
 size_t carve(const Plan& p, void* ws, Layout* out) {
@@ -271,11 +283,20 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.cmap = c.take<int>(cols);
   l.nact = c.take<int>(G);
   l.chk = c.take<int>(2);
-  l.stat_count = c.take<int>(2);
+  l.stat_count = c.take<int>(3);
   l.nvg = c.take<int>(G);
   l.cnv = c.take<int>(cols);
   l.cfold = c.take<int32_t>(cols);
   l.rfold = c.take<int32_t>(p.shared ? G * N : 0);
+  const size_t xc = p.exact ? cols : 0;
+  l.ex_state = c.take<int32_t>(xc * N);
+  l.ex_elist = c.take<int32_t>(xc * N);
+  l.ex_ne = c.take<int>(xc);
+  l.ex_flag = c.take<int>(xc);
+  l.ex_pending = c.take<int>(p.exact ? 1 : 0);
+  l.ex_sumyl = c.take<double>(xc);
+  l.ex_beta = c.take<double>(xc);
+  l.ex_sys = c.take<double>(xc * (size_t)exact_sys_doubles(p.N));
   l.tidx = c.take<int32_t>((size_t)p.nblk * N);
   l.hidx = c.take<int32_t>((size_t)p.V * p.Mh);
   l.fold = c.take<int32_t>((size_t)p.n);
@@ -298,6 +319,12 @@ int make_plan(const kmp_path_spec* spec, int64_t n, int64_t d, int32_t L, const 
     set_error("a full-data refit has no folds to share a factor between");
     return KMP_EINVAL;
   }
+  const bool exact = spec && (spec->flags & KMP_FLAG_EXACT_HINGE) != 0;
+  if (exact && (spec->loss != KMP_HINGE || shared)) {
+    set_error("the exact hinge recovery needs the hinge loss and per-fold factors");
+    return KMP_EINVAL;
+  }
+  p->exact = exact;
   if (spec->loss != KMP_CHECK && Qn != 1) {
     set_error("Q must be 1 for the margin losses");
     return KMP_EINVAL;
@@ -712,7 +739,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
                         Bump::round(sizeof(int) * (size_t)G)) +
       Bump::round(sizeof(int32_t) * (size_t)G * N) +
       Bump::round(sizeof(double) * ncell) + Bump::round(sizeof(int32_t) * ncell) +
-      Bump::round(2 * sizeof(int));
+      Bump::round(3 * sizeof(int)) + Bump::round(sizeof(int));
   CallCtx* ctx = nullptr;
   if ((rc = call_ctx(pin_bytes, &ctx)) != 0) return rc;
   Bump pin{ctx->pin, 0};
@@ -728,7 +755,8 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   // workspace); y and the counts come back while the factorisation is
   // queued and are checked before anything is written to the outputs.
   if ((rc = count_nonfinite(s, X, n, d, ldx, y, lay.chk)) != 0) return rc;
-  KMP_HIP_TRY(hipMemsetAsync(lay.stat_count, 0, 2 * sizeof(int), s));
+  KMP_HIP_TRY(hipMemsetAsync(lay.stat_count, 0, 3 * sizeof(int), s));
+  int* exact_pin = pin.take<int>(1);     // open columns after a recovery round
   double* hy = pin.take<double>(n);
   int* hchk = pin.take<int>(2);
   KMP_HIP_TRY(hipMemcpyAsync(hy, y, sizeof(double) * n, hipMemcpyDeviceToHost, s));
@@ -1003,6 +1031,23 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     fa.alpha = alpha; fa.beta_out = beta; fa.objective = objective; fa.cv_sum = cv_sum;
     fa.shared = shared;
     fa.cv_err = cv_err; fa.iters = iters; fa.status = status; fa.stat_count = lay.stat_count;
+    if (plan.exact) {
+      // the recovery's work vectors reuse column buffers the finalize no
+      // longer needs
+      ExactArgs& x = fa.ex;
+      x.N = N; x.C = C; x.cols = (int64_t)Gb * C;
+      x.emax = exact_emax(N);
+      x.sys_stride = exact_sys_doubles(N);
+      x.delta = delta_final; x.tol = 1e-9;
+      x.nv = lay.nvg; x.cnv = lay.cnv; x.lam = lay.lam; x.ylab = lay.ylab; x.K = lay.A;
+      x.state = lay.ex_state; x.elist = lay.ex_elist; x.ne = lay.ex_ne;
+      x.wl = lay.abar; x.fl = lay.anew; x.alpha = lay.estep; x.fx = lay.uvec;
+      x.sumyl = lay.ex_sumyl; x.sys = lay.ex_sys; x.beta_x = lay.ex_beta;
+      x.xflag = lay.ex_flag; x.pending = lay.ex_pending;
+      fa.exact = true;
+      fa.delta = 0.0;            // the objective reported is the hinge objective
+      fa.pending_host = exact_pin;
+    }
     size_t f0 = 0, f1 = 0;
     if ((rc = tm.mark(s, &f0)) != 0) return rc;
     if ((rc = path_finalize(s, pa, fa)) != 0) return rc;
@@ -1015,9 +1060,9 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   // with one wait
   double* hcv = pin.take<double>(ncell);
   int32_t* hit = pin.take<int32_t>(ncell);
-  int* hstat = pin.take<int>(2);
+  int* hstat = pin.take<int>(3);
   KMP_HIP_TRY(hipMemcpyAsync(hcv, cv_sum, sizeof(double) * ncell, hipMemcpyDeviceToHost, s));
-  KMP_HIP_TRY(hipMemcpyAsync(hstat, lay.stat_count, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
+  KMP_HIP_TRY(hipMemcpyAsync(hstat, lay.stat_count, 3 * sizeof(int), hipMemcpyDeviceToHost, s));
   if (iters)
     KMP_HIP_TRY(hipMemcpyAsync(hit, iters, sizeof(int32_t) * ncell, hipMemcpyDeviceToHost, s));
   KMP_HIP_TRY(hipStreamSynchronize(s));
@@ -1033,6 +1078,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     return KMP_ENONFINITE;
   }
   const bool any_max = hstat[0] > 0;
+  const bool any_inexact = hstat[2] > 0;
   int64_t cell_iters = 0;
   if (iters)
     for (size_t i = 0; i < ncell; ++i) cell_iters += hit[i];
@@ -1108,7 +1154,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     timings->iterations = total_iters;
     timings->cell_iterations = cell_iters;
   }
-  return any_max ? KMP_WMAXITER : KMP_OK;
+  return any_max ? KMP_WMAXITER : (any_inexact ? KMP_WNOTEXACT : KMP_OK);
 }
 
 int kmp_dgemm_grouped(void* stream, int32_t G, int32_t M, int32_t N, int32_t K, const double* A,

@@ -223,6 +223,41 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
 int path_compact(hipStream_t s, const PathArrays& p);
 int group_ones_projection(hipStream_t s, const double* Q, const int* nv, int G, int N, double* cvec);
 
+// Exact hinge recovery after the smoothing stages (exact.hip): the buffers
+// of one bandwidth batch (cols = G*C columns of N rows).
+struct ExactArgs {
+  int N = 0, C = 0;
+  int64_t cols = 0;
+  int emax = 0;                     // largest |E| solved (system (emax+1)^2)
+  int64_t sys_stride = 0;           // doubles per column in sys
+  double delta = 0.0, tol = 1e-9;
+  const int* nv = nullptr;          // G valid rows
+  const int* cnv = nullptr;         // per column loss normaliser
+  const double* lam = nullptr;      // per column lambda
+  const double* ylab = nullptr;     // G x N labels
+  const double* K = nullptr;        // G x N x N observation-space Gram (row-major)
+  const double* ftrain = nullptr;   // cols x N: K alpha of the smoothed solution
+  const double* beta = nullptr;     // cols: smoothed intercepts
+  int32_t* state = nullptr;         // cols x N: 0 L, 1 E, 2 R, 3 padding
+  int32_t* elist = nullptr;         // cols x N: E rows in index order
+  int* ne = nullptr;                // cols: |E|
+  double* wl = nullptr;             // cols x N: y_j [j in L]
+  double* fl = nullptr;             // cols x N: K wl
+  double* sumyl = nullptr;          // cols: sum_L y_j
+  double* sys = nullptr;            // cols x sys_stride
+  double* alpha = nullptr;          // cols x N: candidate alpha
+  double* fx = nullptr;             // cols x N: K alpha
+  double* beta_x = nullptr;         // cols: candidate beta
+  int* xflag = nullptr;             // cols: 0 open, 1 settled, -1 beyond emax, -2 singular
+  int* pending = nullptr;           // 1 int: columns still open after a check
+};
+int exact_init(hipStream_t s, const ExactArgs& x);
+int exact_sets(hipStream_t s, const ExactArgs& x);
+int exact_solve(hipStream_t s, const ExactArgs& x);
+int exact_check(hipStream_t s, const ExactArgs& x);
+int exact_commit(hipStream_t s, const ExactArgs& x, double* alpha_loc, double* ftrain,
+                 double* beta);
+
 // Finalize: alpha_loc = Q ahat (zmat reused), training predictions
 // f = K_v alpha + beta with K_v built again from X on the matrix cores (the
 // objective is evaluated in observation space), held-out predictions
@@ -245,8 +280,13 @@ struct FinalArgs {
   double* alpha = nullptr; double* beta_out = nullptr; double* objective = nullptr;
   double* cv_sum = nullptr; int32_t* cv_err = nullptr; int32_t* iters = nullptr;
   int32_t* status = nullptr;
-  int* stat_count = nullptr;       // 2 ints, accumulated: cells at max_iter, non-finite cells
+  int* stat_count = nullptr;       // 3 ints, accumulated: cells at max_iter, non-finite
+                                   // cells, cells whose exact hinge solution was not reached
   bool shared = false;             // shared-factor mode (one group per bandwidth, all n rows)
+  bool exact = false;              // recover the exact hinge SVM (objective: eq. (kernelsvm))
+  ExactArgs ex;                    // its buffers (ex.cols > 0 when exact)
+  int exact_rounds = 128;          // active-set rounds at most
+  int* pending_host = nullptr;     // pinned int for the per-round count
 };
 int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& f);
 

@@ -1232,7 +1232,7 @@ __global__ __launch_bounds__(256) void cv_reduce_kernel(
     const int* __restrict__ iters_total, double* __restrict__ alpha_out,
     double* __restrict__ beta_out, double* __restrict__ obj_out, double* __restrict__ cv_out,
     int32_t* __restrict__ err_out, int32_t* __restrict__ it_out, int32_t* __restrict__ st_out,
-    int* __restrict__ stat_count) {
+    int* __restrict__ stat_count, const int* __restrict__ xflag) {
   __shared__ double red[PW];
   const int64_t gc = blockIdx.x;
   const int g = (int)(gc / C), c = (int)(gc % C);
@@ -1274,10 +1274,11 @@ __global__ __launch_bounds__(256) void cv_reduce_kernel(
     if (err_out) err_out[cell] = (int32_t)ce;
     if (it_out) it_out[cell] = iters_total[gc];
     const int fl = flag[gc];
-    const int st = fl == 1 ? 0 : (fl == 3 ? 2 : 1);
+    int st = fl == 1 ? 0 : (fl == 3 ? 2 : 1);
+    if (st == 0 && xflag && xflag[gc] != 1) st = 3;    // exact hinge solution not reached
     if (st_out) st_out[cell] = st;
-    // cells that stopped at max_iter / went non-finite, counted whether or
-    // not the caller asked for the per-cell status
+    // cells that stopped at max_iter / went non-finite / kept the smoothed
+    // solution, counted whether or not the caller asked for the status
     if (st != 0) atomicAdd(stat_count + (st - 1), 1);
   }
 }
@@ -1377,6 +1378,38 @@ static int gemm_split(hipStream_t s, const GemmArgs& g, double* scratch, int64_t
   return 0;
 }
 
+// Finite smoothing to the exact hinge SVM (exact.hip), between the training
+// predictions and the held-out block of the finalize: the Gram K_v is in the
+// factor buffer, alpha_loc in zmat, K alpha in ftrain. Each round: the point
+// sets, the products K w_L, the per-column solves, the products K alpha and
+// the KKT check; the host reads the count of open columns after each round.
+// Settled columns then take the exact solution.
+static int exact_recover(hipStream_t s, const PathArrays& p, const FinalArgs& fa,
+                         const GemmArgs& gk, int64_t sP) {
+  int rc;
+  ExactArgs x = fa.ex;
+  x.ftrain = fa.ftrain;
+  x.beta = p.beta;
+  if ((rc = exact_init(s, x)) != 0) return rc;
+  GemmArgs gl = gk;            // K_v times a column block
+  for (int round = 0; round < fa.exact_rounds; ++round) {
+    if ((rc = exact_sets(s, x)) != 0) return rc;
+    gl.B = x.wl;
+    gl.C = x.fl;
+    if ((rc = gemm_split(s, gl, p.zpart, sP)) != 0) return rc;
+    if ((rc = exact_solve(s, x)) != 0) return rc;
+    gl.B = x.alpha;
+    gl.C = x.fx;
+    if ((rc = gemm_split(s, gl, p.zpart, sP)) != 0) return rc;
+    KMP_HIP_TRY(hipMemsetAsync(x.pending, 0, sizeof(int), s));
+    if ((rc = exact_check(s, x)) != 0) return rc;
+    KMP_HIP_TRY(hipMemcpyAsync(fa.pending_host, x.pending, sizeof(int), hipMemcpyDeviceToHost, s));
+    KMP_HIP_TRY(hipStreamSynchronize(s));
+    if (*fa.pending_host == 0) break;
+  }
+  return exact_commit(s, x, p.zmat, fa.ftrain, p.beta);
+}
+
 // Shared-factor finalize: alpha = Q ahat with the held-out rows of each
 // column set to zero, f = K alpha with K built again from X over all points
 // (training and held-out predictions from one product), then the reductions.
@@ -1443,6 +1476,7 @@ int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
   gt.B = p.zmat;
   gt.C = fa.ftrain;
   if ((rc = gemm_split(s, gt, p.zpart, sP)) != 0) return rc;
+  if (fa.exact && (rc = exact_recover(s, p, fa, gt, sP)) != 0) return rc;
   // held-out kernel blocks K[H_v, T_v] (into the same buffer), then held-out
   // predictions K[H_v, T_v] alpha (none in a refit)
   if (fa.Mh > 0 &&
@@ -1460,7 +1494,7 @@ int path_finalize(hipStream_t s, const PathArrays& p, const FinalArgs& fa) {
                      fa.Mh, p.C, fa.V, fa.Qt, fa.L, fa.s0, p.loss, fa.delta, fa.y, fa.tidx, fa.hidx,
                      p.nv, p.lam, p.tau, p.zmat, fa.ftrain, fa.fbuf, p.beta, p.flag, p.iters_total,
                      fa.alpha, fa.beta_out, fa.objective, fa.cv_sum, fa.cv_err, fa.iters, fa.status,
-                     fa.stat_count);
+                     fa.stat_count, fa.exact ? fa.ex.xflag : nullptr);
   KMP_LAUNCH_CHECK();
   // products alpha = Q ahat, f = K_v alpha and the held-out f (Mh rows); the
   // training and held-out kernel blocks written and read back (2d flops per

@@ -25,6 +25,8 @@ KMP_FLAG_RESTART = 1
 KMP_FLAG_GLOBAL_SOLVE = 2
 KMP_FLAG_REFIT = 4
 KMP_FLAG_SHARED_FACTOR = 8
+KMP_FLAG_EXACT_HINGE = 16
+KMP_WNOTEXACT = 2
 KMP_NKC = 10
 KERNEL_CLASSES = ("gram", "panel", "panel_wy", "trail_update", "q_form", "precompute", "gemm_f",
                   "gemm_zhat", "update", "finalize")
@@ -135,7 +137,7 @@ def kmp_version() -> str:
 
 
 def _check(code: int, allow_maxiter: bool = True) -> int:
-    if code == KMP_OK or (allow_maxiter and code == KMP_WMAXITER):
+    if code == KMP_OK or (allow_maxiter and code in (KMP_WMAXITER, KMP_WNOTEXACT)):
         return code
     raise KmpError(code, kmp_strerror(code))
 
@@ -248,7 +250,7 @@ class PathRunner:
 
     def __init__(self, X, y, loss, sigmas, lambdas, fold_id, V, taus=None, device="cuda",
                  sigma_batch: Optional[int] = None, kernel_timing=(), refit: bool = False,
-                 shared: bool = False, **spec_overrides):
+                 shared: bool = False, exact_hinge: bool = False, **spec_overrides):
         """refit=True: every (sigma, tau, lambda) on all n points (fold_id and V
         are ignored; outputs have V = 1, no CV sums, no selection).
         shared=True: exact CV on one factor of the full K per bandwidth
@@ -262,6 +264,8 @@ class PathRunner:
             fold_id, V = np.zeros(np.shape(X)[0], dtype=np.int32), 1
         if shared:
             self.spec.flags |= KMP_FLAG_SHARED_FACTOR
+        if exact_hinge:
+            self.spec.flags |= KMP_FLAG_EXACT_HINGE
         self.set_kernel_timing(kernel_timing)
         self.X = torch.as_tensor(np.ascontiguousarray(X), dtype=torch.float64, device=device) \
             if not isinstance(X, torch.Tensor) else X

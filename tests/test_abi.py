@@ -185,3 +185,15 @@ def test_single_step_entry_points_validate_on_host(km):
     assert L.kmp_dgemm_grouped(None, -1, 4, 4, 4, 0x1000, 0x1000, 0x1000) == km.KMP_EINVAL
     assert L.kmp_dgemm_grouped(None, 2, 4, 4, 4, None, 0x1000, 0x1000) == km.KMP_EINVAL
     assert L.kmp_dgemm_grouped(None, 0, 4, 4, 4, None, None, None) == km.KMP_OK
+
+
+def test_exact_hinge_flag_validation(km):
+    """KMP_FLAG_EXACT_HINGE needs the hinge loss and per-fold factors."""
+    fold = np.arange(20, dtype=np.int32) % 4
+    for loss, extra in (("logistic", 0), ("check", 0), ("hinge", km.KMP_FLAG_SHARED_FACTOR)):
+        spec = km.kmp_default_spec(loss)
+        spec.flags |= km.KMP_FLAG_EXACT_HINGE | extra
+        assert km.kmp_workspace_bytes(spec, 20, 3, 2, fold, 4, 1, 1, 1) == 0
+    spec = km.kmp_default_spec("hinge")
+    spec.flags |= km.KMP_FLAG_EXACT_HINGE
+    assert km.kmp_workspace_bytes(spec, 20, 3, 2, fold, 4, 1, 1, 1) > 0

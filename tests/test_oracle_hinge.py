@@ -112,3 +112,37 @@ def test_exact_hinge_matches_libsvm(lam):
     P_svc = hinge_objective(K, y, a_svc, svc.intercept_[0], lam)
     assert P <= P_svc + 1e-9
     assert abs(P - P_svc) <= 1e-6 * P
+
+
+def _intercept_interval_is_the_argmin(K, y, lam):
+    """The hinge objective is convex in beta for fixed alpha: the reported
+    interval is the set of optimal intercepts when the objective is flat on
+    it and rises just outside it."""
+    alpha, beta, info = solve_exact_hinge(K, y, lam)
+    assert info["converged"]
+    lo, hi = info["beta_lo"], info["beta_hi"]
+    P = hinge_objective(K, y, alpha, beta, lam)
+    assert lo - 1e-12 <= beta <= hi + 1e-12
+    for b in (lo, hi, 0.5 * (lo + hi)):
+        if np.isfinite(b):
+            assert abs(hinge_objective(K, y, alpha, b, lam) - P) <= 1e-13 * max(1.0, P)
+    e = 1e-6 * max(1.0, abs(beta))
+    for b in (lo - e, hi + e):
+        if np.isfinite(b):
+            assert hinge_objective(K, y, alpha, b, lam) - P >= 1e-3 * e / y.size
+    return info["E"], hi - lo
+
+
+def test_intercept_interval_when_no_margin_point_is_free():
+    # cells whose margin points all sit at a bound (a_i in {0, 1}) or whose
+    # margin set is empty: the intercept is an interval, not a point
+    seen = {"empty": 0, "bounded": 0}
+    for name, ls in (("C1", None), ("H1", range(44, 50))):
+        inp = W.make_inputs(W.get(name))
+        K, _, T, _ = gram.fold_blocks(inp["X"], inp["fold_id"], 0, inp["sigmas"][0])
+        y = inp["y"][T]
+        for l in (ls if ls is not None else range(len(inp["lambdas"]))):
+            ne, width = _intercept_interval_is_the_argmin(K, y, inp["lambdas"][l])
+            if width > 0:
+                seen["bounded" if ne else "empty"] += 1
+    assert seen["empty"] >= 3 and seen["bounded"] >= 2, seen
