@@ -14,10 +14,12 @@
 #include "kmp_kernels.h"
 
 #include <algorithm>
+#include <cstdint>
 
 namespace kmp {
 
 typedef double dbl4 __attribute__((ext_vector_type(4)));
+typedef double dbl2 __attribute__((ext_vector_type(2)));
 
 constexpr int TN = 64, LPAD = 4;
 
@@ -36,7 +38,12 @@ struct Tile {
 // cores work on the current one.
 // For k-contiguous B (BKC) each thread loads from one column, whose base
 // pointer bcol the caller resolves once (null for a column past the end).
-template <int BM, int BK, bool AK, bool BKC>
+//
+// VEC: every tile row and K slice lies inside the operands (M a multiple of
+// BM, the K range of BK, leading dimensions even and bases 16-byte aligned,
+// which the host checks), so each thread's run of consecutive elements is
+// read with unchecked 16-byte loads.
+template <int BM, int BK, bool AK, bool BKC, bool VEC = false>
 __device__ __forceinline__ void fetch_slice(int M, int N, int K, int i0, int j0, int k0,
                                             const double* __restrict__ A, int64_t lda,
                                             const double* __restrict__ B, int64_t ldb,
@@ -45,6 +52,32 @@ __device__ __forceinline__ void fetch_slice(int M, int N, int K, int i0, int j0,
                                             double (&rb)[Tile<BM, BK>::BPT]) {
   constexpr int APT = Tile<BM, BK>::APT, BPT = Tile<BM, BK>::BPT;
   const int t = threadIdx.x;
+  if constexpr (VEC) {
+    static_assert(BKC && APT % 2 == 0 && BPT % 2 == 0, "vector fetch: k-contiguous B, pairs");
+    const double* pa;
+    if (AK) {
+      constexpr int TPR = BK / APT;
+      pa = A + (int64_t)(i0 + t / TPR) * lda + k0 + (t % TPR) * APT;
+    } else {
+      constexpr int TPR = BM / APT;
+      pa = A + (int64_t)(k0 + t / TPR) * lda + i0 + (t % TPR) * APT;
+    }
+#pragma unroll
+    for (int q = 0; q < APT / 2; ++q) {
+      const dbl2 v = *reinterpret_cast<const dbl2*>(pa + 2 * q);
+      ra[2 * q] = v.x;
+      ra[2 * q + 1] = v.y;
+    }
+    constexpr int TPRB = BK / BPT;
+    const double* pb = bcol ? bcol + k0 + (t % TPRB) * BPT : nullptr;
+#pragma unroll
+    for (int q = 0; q < BPT / 2; ++q) {
+      const dbl2 v = pb ? *reinterpret_cast<const dbl2*>(pb + 2 * q) : dbl2{0.0, 0.0};
+      rb[2 * q] = v.x;
+      rb[2 * q + 1] = v.y;
+    }
+    return;
+  }
   if (AK) {                       // A[i*lda + k]: threads walk k within a row
     constexpr int TPR = BK / APT;
     const int i = t / TPR, kb = (t % TPR) * APT;
@@ -164,7 +197,7 @@ __device__ __forceinline__ void tile_stage_mfma(const double (*As)[BM + LPAD],
 // the matrix products of a 16-column block that lies wholly past N (a
 // wave-uniform test), so a tile with few columns costs little more than
 // its loads.
-template <int BM, int BK, bool AK, bool BKC, int PF = 1>
+template <int BM, int BK, bool AK, bool BKC, int PF = 1, bool VEC = false>
 __device__ __forceinline__ void tile_mainloop(int M, int N, int kbeg, int K, int i0, int j0,
                                               const double* __restrict__ A, int64_t lda,
                                               const double* __restrict__ B, int64_t ldb,
@@ -190,14 +223,14 @@ __device__ __forceinline__ void tile_mainloop(int M, int N, int kbeg, int K, int
   const int nk = (K - kbeg + BK - 1) / BK;
   if constexpr (PF == 1) {
     double ra[Tile<BM, BK>::APT], rb[Tile<BM, BK>::BPT];
-    fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg, A, lda, B, ldb, bcol, ra, rb);
+    fetch_slice<BM, BK, AK, BKC, VEC>(M, N, K, i0, j0, kbeg, A, lda, B, ldb, bcol, ra, rb);
     store_slice<BM, BK, AK, BKC>(ra, rb, As[0], Bs[0]);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
       const int cur = kt & 1;
       const bool more = kt + 1 < nk;
       if (more)
-        fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + (kt + 1) * BK, A, lda, B, ldb, bcol,
+        fetch_slice<BM, BK, AK, BKC, VEC>(M, N, K, i0, j0, kbeg + (kt + 1) * BK, A, lda, B, ldb, bcol,
                                      ra, rb);
       if (use0) tile_stage_mfma<BM, BK, AK, BKC>(As[cur], Bs[cur], wi, wj, li, lk, use1, acc);
       if (more) store_slice<BM, BK, AK, BKC>(ra, rb, As[cur ^ 1], Bs[cur ^ 1]);
@@ -206,17 +239,17 @@ __device__ __forceinline__ void tile_mainloop(int M, int N, int kbeg, int K, int
   } else {
     double ra0[Tile<BM, BK>::APT], rb0[Tile<BM, BK>::BPT];
     double ra1[Tile<BM, BK>::APT], rb1[Tile<BM, BK>::BPT];
-    fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg, A, lda, B, ldb, bcol, ra0, rb0);
+    fetch_slice<BM, BK, AK, BKC, VEC>(M, N, K, i0, j0, kbeg, A, lda, B, ldb, bcol, ra0, rb0);
     store_slice<BM, BK, AK, BKC>(ra0, rb0, As[0], Bs[0]);
-    if (nk > 1) fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + BK, A, lda, B, ldb, bcol, ra0, rb0);
+    if (nk > 1) fetch_slice<BM, BK, AK, BKC, VEC>(M, N, K, i0, j0, kbeg + BK, A, lda, B, ldb, bcol, ra0, rb0);
     if (nk > 2)
-      fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + 2 * BK, A, lda, B, ldb, bcol, ra1, rb1);
+      fetch_slice<BM, BK, AK, BKC, VEC>(M, N, K, i0, j0, kbeg + 2 * BK, A, lda, B, ldb, bcol, ra1, rb1);
     __syncthreads();
     for (int kt = 0; kt < nk; kt += 2) {
       // even step: slice kt in stage 0, slice kt+1 in (ra0, rb0)
       if (kt + 1 < nk) store_slice<BM, BK, AK, BKC>(ra0, rb0, As[1], Bs[1]);
       if (kt + 3 < nk)
-        fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + (kt + 3) * BK, A, lda, B, ldb, bcol,
+        fetch_slice<BM, BK, AK, BKC, VEC>(M, N, K, i0, j0, kbeg + (kt + 3) * BK, A, lda, B, ldb, bcol,
                                      ra0, rb0);
       if (use0) tile_stage_mfma<BM, BK, AK, BKC>(As[0], Bs[0], wi, wj, li, lk, use1, acc);
       __syncthreads();
@@ -224,11 +257,108 @@ __device__ __forceinline__ void tile_mainloop(int M, int N, int kbeg, int K, int
       // odd step: slice kt+1 in stage 1, slice kt+2 in (ra1, rb1)
       if (kt + 2 < nk) store_slice<BM, BK, AK, BKC>(ra1, rb1, As[0], Bs[0]);
       if (kt + 4 < nk)
-        fetch_slice<BM, BK, AK, BKC>(M, N, K, i0, j0, kbeg + (kt + 4) * BK, A, lda, B, ldb, bcol,
+        fetch_slice<BM, BK, AK, BKC, VEC>(M, N, K, i0, j0, kbeg + (kt + 4) * BK, A, lda, B, ldb, bcol,
                                      ra1, rb1);
       if (use0) tile_stage_mfma<BM, BK, AK, BKC>(As[1], Bs[1], wi, wj, li, lk, use1, acc);
       __syncthreads();
     }
+  }
+}
+
+// Main loop of the whole-tile case (VEC above) without a branch around a
+// memory access, so that the wait before each LDS store holds only for the
+// slice it stores while the next slice's loads stay in flight: the slice
+// index of every prefetch is clamped to the last slice (the surplus loads
+// re-read it), both LDS stages are written unconditionally (the stage
+// written is never the one being read), and a column past N reads column
+// cmap[0] (or 0) and is zeroed when stored to LDS. Two register sets, each slice
+// fetched two steps before it is stored, as tile_mainloop with PF = 2.
+template <int BM, int BK, bool AK>
+__device__ __forceinline__ void tile_mainloop_vec(int N, int kbeg, int K, int i0, int j0,
+                                                  const double* __restrict__ A, int64_t lda,
+                                                  const double* __restrict__ B, int64_t ldb,
+                                                  const int* __restrict__ cmap,
+                                                  dbl4 (&acc)[Tile<BM, BK>::MB][2]) {
+  constexpr int MB = Tile<BM, BK>::MB;
+  constexpr int APT = Tile<BM, BK>::APT, BPT = Tile<BM, BK>::BPT;
+  __shared__ double As[2][BK][BM + LPAD];
+  __shared__ double Bs[2][BK][TN + LPAD];
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  // the wave index read as a scalar: the column-block tests below are then
+  // scalar branches around the matrix products, not lane masks
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wi = (w & 1) * (BM / 2), wj = (w >> 1) * 32;
+  const int li = lane & 15, lk = lane >> 4;
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = dbl4{0.0, 0.0, 0.0, 0.0};
+  const double* pa;
+  if (AK) {
+    constexpr int TPR = BK / APT;
+    pa = A + (int64_t)(i0 + t / TPR) * lda + kbeg + (t % TPR) * APT;
+  } else {
+    constexpr int TPR = BM / APT;
+    pa = A + (int64_t)(kbeg + t / TPR) * lda + i0 + (t % TPR) * APT;
+  }
+  const int64_t astep = AK ? BK : (int64_t)BK * lda;    // one slice further along K
+  constexpr int TPRB = BK / BPT;
+  const int gj = j0 + t / TPRB;
+  const bool bact = gj < N;
+  const double* pb = B + (int64_t)(cmap ? cmap[bact ? gj : 0] : (bact ? gj : 0)) * ldb + kbeg +
+                     (t % TPRB) * BPT;
+  const bool use0 = j0 + wj < N, use1 = j0 + wj + 16 < N;
+  const int nk = (K - kbeg) / BK;
+  dbl2 ra0[APT / 2], rb0[BPT / 2], ra1[APT / 2], rb1[BPT / 2];
+  auto fetch = [&](int kt, dbl2 (&ra)[APT / 2], dbl2 (&rb)[BPT / 2]) {
+    const int k = min(kt, nk - 1);
+    const double* qa = pa + k * astep;
+    const double* qb = pb + (int64_t)k * BK;
+#pragma unroll
+    for (int q = 0; q < APT / 2; ++q) ra[q] = *reinterpret_cast<const dbl2*>(qa + 2 * q);
+#pragma unroll
+    for (int q = 0; q < BPT / 2; ++q) rb[q] = *reinterpret_cast<const dbl2*>(qb + 2 * q);
+  };
+  auto store = [&](const dbl2 (&ra)[APT / 2], const dbl2 (&rb)[BPT / 2], double (*Asl)[BM + LPAD],
+                   double (*Bsl)[TN + LPAD]) {
+    if (AK) {
+      constexpr int TPR = BK / APT;
+      const int i = t / TPR, kb = (t % TPR) * APT;
+#pragma unroll
+      for (int q = 0; q < APT; ++q) Asl[kb + q][lds_col<true, APT>(kb + q, i)] = ra[q / 2][q % 2];
+    } else {
+      constexpr int TPR = BM / APT;
+      const int k = t / TPR, ib = (t % TPR) * APT;
+#pragma unroll
+      for (int q = 0; q < APT; ++q) Asl[k][lds_col<false, APT>(k, ib + q)] = ra[q / 2][q % 2];
+    }
+    const int j = t / TPRB, kb = (t % TPRB) * BPT;
+#pragma unroll
+    for (int q = 0; q < BPT; ++q)
+      Bsl[kb + q][lds_col<true, BPT>(kb + q, j)] = bact ? rb[q / 2][q % 2] : 0.0;
+  };
+  if (nk <= 0) return;
+  fetch(0, ra0, rb0);
+  store(ra0, rb0, As[0], Bs[0]);
+  fetch(1, ra0, rb0);
+  // keep slice 1's loads older than slice 2's, as in the loop (the waits
+  // are counted in issue order)
+  __builtin_amdgcn_sched_barrier(0);
+  fetch(2, ra1, rb1);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    // even step: slice kt in stage 0, slice kt+1 in (ra0, rb0)
+    store(ra0, rb0, As[1], Bs[1]);
+    fetch(kt + 3, ra0, rb0);
+    if (use0) tile_stage_mfma<BM, BK, AK, true>(As[0], Bs[0], wi, wj, li, lk, use1, acc);
+    __syncthreads();
+    if (kt + 1 >= nk) break;
+    // odd step: slice kt+1 in stage 1, slice kt+2 in (ra1, rb1)
+    store(ra1, rb1, As[0], Bs[0]);
+    fetch(kt + 4, ra1, rb1);
+    if (use0) tile_stage_mfma<BM, BK, AK, true>(As[1], Bs[1], wi, wj, li, lk, use1, acc);
+    __syncthreads();
   }
 }
 
@@ -347,7 +477,7 @@ __global__ __launch_bounds__(256) void dgemm_loss_kernel(int M, int N, int K,
 // is column cmap[b*cstride + k] of B and of the partials (the other columns
 // of the partials are left as they were); tiles past nact[b] exit at once.
 // With IDENT (cmap and nact null), all cstride columns, in order.
-template <int BM, int BK, bool AK, bool IDENT, int PF = 1>
+template <int BM, int BK, bool AK, bool IDENT, int PF = 1, bool VEC = false>
 __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S, int Kc,
                                                              const double* __restrict__ A, int64_t lda, int64_t sA,
                                                              const double* __restrict__ B, int64_t ldb, int64_t sB,
@@ -367,7 +497,10 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
   const int kend = min(K, kbeg + Kc);
   dbl4 acc[MB][2];
   if (kbeg < kend) {
-    tile_mainloop<BM, BK, AK, true, PF>(M, N, kbeg, kend, i0, j0, A, lda, B, ldb, cmap, acc);
+    if constexpr (VEC)
+      tile_mainloop_vec<BM, BK, AK>(N, kbeg, kend, i0, j0, A, lda, B, ldb, cmap, acc);
+    else
+      tile_mainloop<BM, BK, AK, true, PF>(M, N, kbeg, kend, i0, j0, A, lda, B, ldb, cmap, acc);
   } else {
 #pragma unroll
     for (int a = 0; a < MB; ++a) acc[a][0] = acc[a][1] = dbl4{0.0, 0.0, 0.0, 0.0};
@@ -504,15 +637,23 @@ int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double
     set_error("gemm_partial: cmap and nact must both be given or both be null");
     return KMP_EINVAL;
   }
-#define KMP_PART_CASE(AKV, IDV)                                                                  \
-  if (a_kcontig == AKV && ident == IDV)                                                          \
-    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, AKV, IDV, 2>), grid, dim3(256), 0, s, g.M, g.K, \
-                       S, Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap,    \
+  // whole tiles and 16-byte aligned operands: unchecked vector loads
+  const bool vec = g.M % 64 == 0 && g.K % 16 == 0 && g.lda % 2 == 0 && g.ldb % 2 == 0 &&
+                   g.sA % 2 == 0 && g.sB % 2 == 0 && (reinterpret_cast<uintptr_t>(g.A) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(g.B) & 15) == 0;
+#define KMP_PART_CASE(AKV, IDV, VV)                                                              \
+  if (a_kcontig == AKV && ident == IDV && vec == VV)                                             \
+    hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, AKV, IDV, 2, VV>), grid, dim3(256), 0, s, g.M, \
+                       g.K, S, Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap, \
                        nact, g.N);
-  KMP_PART_CASE(true, false)
-  KMP_PART_CASE(false, false)
-  KMP_PART_CASE(true, true)
-  KMP_PART_CASE(false, true)
+  KMP_PART_CASE(true, false, true)
+  KMP_PART_CASE(false, false, true)
+  KMP_PART_CASE(true, true, true)
+  KMP_PART_CASE(false, true, true)
+  KMP_PART_CASE(true, false, false)
+  KMP_PART_CASE(false, false, false)
+  KMP_PART_CASE(true, true, false)
+  KMP_PART_CASE(false, true, false)
 #undef KMP_PART_CASE
   KMP_LAUNCH_CHECK();
   return 0;

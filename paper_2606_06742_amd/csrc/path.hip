@@ -167,117 +167,134 @@ __device__ __forceinline__ double row4_sum(double v) { return swap_sum32(swap_su
 // row4_sum adds the four parts, so a block step is four FMAs, two swaps and
 // one LDS exchange per triangular factor. The lane's four tile entries of
 // the next SPF blocks are loaded ahead into registers, so the recurrence
-// does not wait on device memory. Forward tiles are read by rows
+// does not wait on device memory: a block step takes far less than a load's
+// latency under load, so the loads of several steps must be in flight (the
+// vector-memory counter allows 63 per wave: 4 loads per forward step and 5
+// per backward step here). Forward tiles are read by rows
 // (V[j*N + 16 I + a], j = 4g+t), backward tiles by columns
 // (V[a*N + 16 I + j]) as the transposed factors need.
-constexpr int SPF = 4;
+constexpr int SPF = 12;
 
+// One forward block step of the LDS solve: rg holds the lane's four entries
+// of tile I and receives those of tile min(I + SPF, NB - 1). Branch free, so
+// that the loads of the following steps stay in flight across it.
+__device__ __forceinline__ void band_fwd_step(const double* __restrict__ Vc, double* xs, int N,
+                                              int NB, int I, int a, int g, bool lead,
+                                              double (&rg)[4]) {
+  double cn[4], lm[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const double v = rg[t];
+    cn[t] = (4 * g + t >= a && I > 0) ? -v : 0.0;   // C_I (upper triangle, diagonal included)
+    lm[t] = (4 * g + t < a) ? v : 0.0;              // strict lower part of L_I^{-1}
+  }
+  const int In = min(I + SPF, NB - 1);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) rg[t] = Vc[(int64_t)(4 * g + t) * N + BND * In + a];
+  double p0 = lead ? xs[BND * I + a] : 0.0, p1 = 0.0;
+  const double* yp = xs + BND * max(I - 1, 0) + 4 * g;
+  p0 = fma(cn[0], yp[0], p0);
+  p1 = fma(cn[1], yp[1], p1);
+  p0 = fma(cn[2], yp[2], p0);
+  p1 = fma(cn[3], yp[3], p1);
+  const double r = row4_sum(p0 + p1);
+  xs[BND * I + a] = r;                 // the four lanes of row a store the same value
+  wave_sync();
+  const double* rp = xs + BND * I + 4 * g;
+  double q0 = lead ? r : 0.0, q1 = 0.0;
+  q0 = fma(lm[0], rp[0], q0);
+  q1 = fma(lm[1], rp[1], q1);
+  q0 = fma(lm[2], rp[2], q0);
+  q1 = fma(lm[3], rp[3], q1);
+  const double yv = row4_sum(q0 + q1);
+  xs[BND * I + a] = yv;
+  wave_sync();
+}
+
+// One backward block step (block I = NB - 1 - tt); vprev holds the lane's
+// entries (4g+t, a) of tile I + 1.
+__device__ __forceinline__ void band_bwd_step(const double* __restrict__ Vc,
+                                              const double* __restrict__ Dc, double* xs, int N,
+                                              int NB, int tt, int a, int g, bool lead,
+                                              double (&rg)[4], double& dr, double (&vprev)[4]) {
+  const int I = NB - 1 - tt;
+  double cn[4], lm[4], vv[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    vv[t] = rg[t];
+    cn[t] = (a >= 4 * g + t && tt > 0) ? -vprev[t] : 0.0;   // C_{I+1}' row a
+    lm[t] = (4 * g + t > a) ? vv[t] : 0.0;                  // strict upper part of L_I^{-T}
+  }
+  const double dv = dr;
+  const int In = max(I - SPF, 0);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) rg[t] = Vc[(int64_t)a * N + BND * In + 4 * g + t];
+  dr = Dc[BND * In + a];
+  double p0 = lead ? dv * xs[BND * I + a] : 0.0, p1 = 0.0;
+  const double* xp = xs + BND * min(I + 1, NB - 1) + 4 * g;
+  p0 = fma(cn[0], xp[0], p0);
+  p1 = fma(cn[1], xp[1], p1);
+  p0 = fma(cn[2], xp[2], p0);
+  p1 = fma(cn[3], xp[3], p1);
+  const double sv = row4_sum(p0 + p1);
+  xs[BND * I + a] = sv;
+  wave_sync();
+  const double* sp = xs + BND * I + 4 * g;
+  double q0 = lead ? sv : 0.0, q1 = 0.0;
+  q0 = fma(lm[0], sp[0], q0);
+  q1 = fma(lm[1], sp[1], q1);
+  q0 = fma(lm[2], sp[2], q0);
+  q1 = fma(lm[3], sp[3], q1);
+  const double xv = row4_sum(q0 + q1);
+  xs[BND * I + a] = xv;
+  wave_sync();
+#pragma unroll
+  for (int t = 0; t < 4; ++t) vprev[t] = vv[t];
+}
+
+// The sweeps run whole groups of SPF blocks without a branch (block
+// p of a group in ring slot p), then the remaining NB mod SPF blocks.
 __device__ __forceinline__ void band_solve(const double* __restrict__ Vc,
                                            const double* __restrict__ Dc, double* xs, int N,
                                            int lane) {
   const int NB = N / BND;
+  const int NBm = NB - NB % SPF;
   const int a = lane & 15, g = lane >> 4;
   const bool lead = g == 0;
   double ring[SPF][4];
   // forward: y_I = L_I^{-1} (w_I - C_I y_{I-1}), y overwrites w in xs
 #pragma unroll
   for (int p = 0; p < SPF; ++p) {
-    const int Ib = p < NB ? p : NB - 1;
+    const int Ib = min(p, NB - 1);
 #pragma unroll
     for (int t = 0; t < 4; ++t) ring[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * Ib + a];
   }
-  for (int I0 = 0; I0 < NB; I0 += SPF) {
+  for (int I0 = 0; I0 < NBm; I0 += SPF) {
 #pragma unroll
-    for (int p = 0; p < SPF; ++p) {
-      const int I = I0 + p;
-      if (I < NB) {
-        double cn[4], lm[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const double v = ring[p][t];
-          cn[t] = (4 * g + t >= a) ? -v : 0.0;      // C_I (upper triangle, diagonal included)
-          lm[t] = (4 * g + t < a) ? v : 0.0;        // strict lower part of L_I^{-1}
-        }
-        const int In = (I + SPF < NB) ? I + SPF : NB - 1;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) ring[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * In + a];
-        double p0 = lead ? xs[BND * I + a] : 0.0, p1 = 0.0;
-        if (I > 0) {
-          const double* yp = xs + BND * (I - 1) + 4 * g;
-          p0 = fma(cn[0], yp[0], p0);
-          p1 = fma(cn[1], yp[1], p1);
-          p0 = fma(cn[2], yp[2], p0);
-          p1 = fma(cn[3], yp[3], p1);
-        }
-        const double r = row4_sum(p0 + p1);
-        if (lead) xs[BND * I + a] = r;
-        wave_sync();
-        const double* rp = xs + BND * I + 4 * g;
-        double q0 = lead ? r : 0.0, q1 = 0.0;
-        q0 = fma(lm[0], rp[0], q0);
-        q1 = fma(lm[1], rp[1], q1);
-        q0 = fma(lm[2], rp[2], q0);
-        q1 = fma(lm[3], rp[3], q1);
-        const double yv = row4_sum(q0 + q1);
-        if (lead) xs[BND * I + a] = yv;
-        wave_sync();
-      }
-    }
+    for (int p = 0; p < SPF; ++p) band_fwd_step(Vc, xs, N, NB, I0 + p, a, g, lead, ring[p]);
   }
+#pragma unroll
+  for (int p = 0; p < SPF; ++p)
+    if (NBm + p < NB) band_fwd_step(Vc, xs, N, NB, NBm + p, a, g, lead, ring[p]);
   wave_sync();
   // backward: x_I = L_I^{-T} (D_I^{-1} y_I - C_{I+1}' x_{I+1}), x overwrites y
   double dring[SPF];
 #pragma unroll
   for (int p = 0; p < SPF; ++p) {
-    const int Ib = (NB - 1 - p >= 0) ? NB - 1 - p : 0;
+    const int Ib = max(NB - 1 - p, 0);
 #pragma unroll
     for (int t = 0; t < 4; ++t) ring[p][t] = Vc[(int64_t)a * N + BND * Ib + 4 * g + t];
     dring[p] = Dc[BND * Ib + a];
   }
   double vprev[4] = {0.0, 0.0, 0.0, 0.0};     // entries (4g+t, a) of the tile of block I+1
-  for (int T0 = 0; T0 < NB; T0 += SPF) {
+  for (int T0 = 0; T0 < NBm; T0 += SPF) {
 #pragma unroll
-    for (int p = 0; p < SPF; ++p) {
-      const int tt = T0 + p;
-      if (tt < NB) {
-        const int I = NB - 1 - tt;
-        double cn[4], lm[4], vv[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          vv[t] = ring[p][t];
-          cn[t] = (a >= 4 * g + t) ? -vprev[t] : 0.0;   // C_{I+1}' row a
-          lm[t] = (4 * g + t > a) ? vv[t] : 0.0;        // strict upper part of L_I^{-T}
-        }
-        const double dv = dring[p];
-        const int In = (I - SPF >= 0) ? I - SPF : 0;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) ring[p][t] = Vc[(int64_t)a * N + BND * In + 4 * g + t];
-        dring[p] = Dc[BND * In + a];
-        double p0 = lead ? dv * xs[BND * I + a] : 0.0, p1 = 0.0;
-        if (tt > 0) {
-          const double* xp = xs + BND * (I + 1) + 4 * g;
-          p0 = fma(cn[0], xp[0], p0);
-          p1 = fma(cn[1], xp[1], p1);
-          p0 = fma(cn[2], xp[2], p0);
-          p1 = fma(cn[3], xp[3], p1);
-        }
-        const double sv = row4_sum(p0 + p1);
-        if (lead) xs[BND * I + a] = sv;
-        wave_sync();
-        const double* sp = xs + BND * I + 4 * g;
-        double q0 = lead ? sv : 0.0, q1 = 0.0;
-        q0 = fma(lm[0], sp[0], q0);
-        q1 = fma(lm[1], sp[1], q1);
-        q0 = fma(lm[2], sp[2], q0);
-        q1 = fma(lm[3], sp[3], q1);
-        const double xv = row4_sum(q0 + q1);
-        if (lead) xs[BND * I + a] = xv;
-        wave_sync();
-#pragma unroll
-        for (int t = 0; t < 4; ++t) vprev[t] = vv[t];
-      }
-    }
+    for (int p = 0; p < SPF; ++p)
+      band_bwd_step(Vc, Dc, xs, N, NB, T0 + p, a, g, lead, ring[p], dring[p], vprev);
   }
+#pragma unroll
+  for (int p = 0; p < SPF; ++p)
+    if (NBm + p < NB) band_bwd_step(Vc, Dc, xs, N, NB, NBm + p, a, g, lead, ring[p], dring[p], vprev);
   wave_sync();
 }
 
@@ -297,6 +314,10 @@ __device__ __forceinline__ void grid_vec_sync() {
 // other lanes need are staged in an LDS ring of two BND-double slots (block
 // I in slot I & 1). No lane reads device memory written by another lane of
 // the same launch.
+// Prefetch depth of the device-memory solve (5 loads per forward step, 6
+// per backward step).
+constexpr int SPFG = 10;
+
 template <typename WIn, typename WOut>
 __device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
                                              const double* __restrict__ Dc, double* ysc,
@@ -304,17 +325,17 @@ __device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
   const int NB = N / BND;
   const int a = lane & 15, g = lane >> 4;
   const bool lead = g == 0;
-  double ring_t[SPF][4], wv[SPF];
+  double ring_t[SPFG][4], wv[SPFG];
 #pragma unroll
-  for (int p = 0; p < SPF; ++p) {
+  for (int p = 0; p < SPFG; ++p) {
     const int Ib = p < NB ? p : NB - 1;
 #pragma unroll
     for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * Ib + a];
     wv[p] = lead ? win(BND * Ib + a) : 0.0;
   }
-  for (int I0 = 0; I0 < NB; I0 += SPF) {
+  for (int I0 = 0; I0 < NB; I0 += SPFG) {
 #pragma unroll
-    for (int p = 0; p < SPF; ++p) {
+    for (int p = 0; p < SPFG; ++p) {
       const int I = I0 + p;
       if (I < NB) {
         double cn[4], lm[4];
@@ -325,7 +346,7 @@ __device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
           lm[t] = (4 * g + t < a) ? v : 0.0;
         }
         double p0 = wv[p], p1 = 0.0;
-        const int In = (I + SPF < NB) ? I + SPF : NB - 1;
+        const int In = (I + SPFG < NB) ? I + SPFG : NB - 1;
 #pragma unroll
         for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * In + a];
         wv[p] = lead ? win(BND * In + a) : 0.0;
@@ -356,9 +377,9 @@ __device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
     }
   }
   wave_sync();
-  double dring[SPF];
+  double dring[SPFG];
 #pragma unroll
-  for (int p = 0; p < SPF; ++p) {
+  for (int p = 0; p < SPFG; ++p) {
     const int Ib = (NB - 1 - p >= 0) ? NB - 1 - p : 0;
 #pragma unroll
     for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)a * N + BND * Ib + 4 * g + t];
@@ -366,9 +387,9 @@ __device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
     wv[p] = lead ? ysc[BND * Ib + a] : 0.0;
   }
   double vprev[4] = {0.0, 0.0, 0.0, 0.0};
-  for (int T0 = 0; T0 < NB; T0 += SPF) {
+  for (int T0 = 0; T0 < NB; T0 += SPFG) {
 #pragma unroll
-    for (int p = 0; p < SPF; ++p) {
+    for (int p = 0; p < SPFG; ++p) {
       const int tt = T0 + p;
       if (tt < NB) {
         const int I = NB - 1 - tt;
@@ -381,7 +402,7 @@ __device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
         }
         const double dv = dring[p];
         double p0 = lead ? dv * wv[p] : 0.0, p1 = 0.0;
-        const int In = (I - SPF >= 0) ? I - SPF : 0;
+        const int In = (I - SPFG >= 0) ? I - SPFG : 0;
 #pragma unroll
         for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)a * N + BND * In + 4 * g + t];
         dring[p] = Dc[BND * In + a];
