@@ -97,6 +97,13 @@ extern "C" {
                           3, return KMP_WNOTEXACT. Hinge loss, per-fold
                           factors only; the workspace grows by about
                           (min(N, 384) + 1)^2 doubles per column.           */
+#define KMP_FLAG_EAGER 32  /* launch every iteration directly. Otherwise, for
+                          padded orders up to 2048 and poll_every <= 64, the
+                          poll_every iterations between two convergence polls
+                          are recorded once per smoothing stage as a HIP graph
+                          and replayed (those orders are launch-bound); the
+                          graph's split-K factor is the one for all columns,
+                          so results agree with eager launches to rounding  */
 #define KMP_FLAG_GLOBAL_SOLVE 2 /* keep the banded solve's working vector in
                           device memory at every order (it is there anyway
                           above the rows one workgroup's LDS holds: 20224
@@ -128,7 +135,7 @@ typedef struct {
   int32_t poll_every;  /* iterations between host convergence polls (8)     */
   int32_t flags;       /* KMP_FLAG_RESTART (default on), KMP_FLAG_GLOBAL_SOLVE,
                           KMP_FLAG_REFIT, KMP_FLAG_SHARED_FACTOR,
-                          KMP_FLAG_EXACT_HINGE                              */
+                          KMP_FLAG_EXACT_HINGE, KMP_FLAG_EAGER              */
   int32_t timing_mask; /* kernel classes to time with HIP events (default 0) */
   int32_t timing_every;/* bracket one launch in every timing_every launches
                           of a timed class (default 1: all)                 */

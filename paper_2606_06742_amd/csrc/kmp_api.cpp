@@ -74,6 +74,72 @@ void kc_end(int cls, hipStream_t s, double bytes, double flops) {
   c->open_cls = -1;
 }
 
+// Iterations between two polls captured as one HIP graph. Orders up to
+// kGraphMaxOrder are launch-bound (five launches of a few microseconds of
+// work per iteration); their poll_every iterations are recorded once per
+// smoothing stage and replayed. The recorded grids cover every column (the
+// split-K factor too), since the kernels skip converged columns on the
+// device; no timing events and no memory fills are recorded.
+constexpr int kGraphMaxOrder = 2048;
+constexpr int kGraphMaxIters = 64;
+
+struct IterGraph {
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+  IterGraph() = default;
+  IterGraph(const IterGraph&) = delete;
+  IterGraph& operator=(const IterGraph&) = delete;
+  ~IterGraph() {
+    if (exec) (void)hipGraphExecDestroy(exec);
+    if (graph) (void)hipGraphDestroy(graph);
+  }
+};
+
+// The graph is recorded on a stream of its own (the caller's stream may be
+// the null stream, which cannot record) and launched on the caller's; one
+// per thread and device, created on first use, at the default priority.
+static int capture_stream(hipStream_t* out) {
+  int dev = 0;
+  KMP_HIP_TRY(hipGetDevice(&dev));
+  static thread_local std::map<int, hipStream_t> streams;
+  auto it = streams.find(dev);
+  if (it == streams.end()) {
+    hipStream_t st = nullptr;
+    KMP_HIP_TRY(hipStreamCreateWithFlags(&st, hipStreamNonBlocking));
+    it = streams.emplace(dev, st).first;
+  }
+  *out = it->second;
+  return 0;
+}
+
+static int capture_iterations(const PathArrays& pa, double delta, double kappa, double tol,
+                              int max_iter, int restart, int count, IterGraph* out) {
+  hipStream_t cs = nullptr;
+  int rc = capture_stream(&cs);
+  if (rc != 0) return rc;
+  PathArrays pg = pa;
+  pg.nact_host = nullptr;
+  KernelClock* saved = g_clock;
+  g_clock = nullptr;
+  KMP_HIP_TRY(hipStreamBeginCapture(cs, hipStreamCaptureModeRelaxed));
+  for (int k = 0; k < count && rc == 0; ++k)
+    rc = path_iteration(cs, pg, delta, kappa, tol, max_iter, restart);
+  hipGraph_t g = nullptr;
+  const hipError_t e = hipStreamEndCapture(cs, &g);
+  g_clock = saved;
+  if (rc != 0 || e != hipSuccess) {
+    if (g) (void)hipGraphDestroy(g);
+    if (rc == 0) {
+      set_error(std::string("hipStreamEndCapture: ") + hipGetErrorString(e));
+      rc = KMP_EHIP;
+    }
+    return rc;
+  }
+  out->graph = g;
+  KMP_HIP_TRY(hipGraphInstantiate(&out->exec, g, nullptr, nullptr, 0));
+  return 0;
+}
+
 namespace {
 
 // Device scratch of the allocation-free Gram entry point: the bandwidth
@@ -872,6 +938,8 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
   if ((rc = row_norms(s, X, n, d, ldx, lay.nrm)) != 0) return rc;
 
   PathArrays pa = path_arrays_of(lay, plan, spec->loss, (spec->flags & KMP_FLAG_GLOBAL_SOLVE) != 0);
+  const bool use_graphs = (spec->flags & KMP_FLAG_EAGER) == 0 && N <= kGraphMaxOrder &&
+                          spec->poll_every <= kGraphMaxIters;
 
   for (int s0 = 0; s0 < S; s0 += Sb) {
     const int sb = std::min(Sb, S - s0);
@@ -992,14 +1060,23 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
         *active = poll.p[Gb];
         return 0;
       };
+      const int restart = (spec->flags & KMP_FLAG_RESTART) ? 1 : 0;
+      IterGraph ig;
+      if (use_graphs && (rc = capture_iterations(pa, delta, kappa, spec->tol, spec->max_iter,
+                                                 restart, spec->poll_every, &ig)) != 0)
+        return rc;
       if ((rc = post_poll()) != 0) return rc;
       bool pending = true;
       int it = 0;
       while (it < spec->max_iter) {
-        if ((rc = path_iteration(s, pa, delta, kappa, spec->tol, spec->max_iter,
-                                 (spec->flags & KMP_FLAG_RESTART) ? 1 : 0)) != 0)
-          return rc;
-        ++it;
+        if (ig.exec && it % spec->poll_every == 0 && it + spec->poll_every <= spec->max_iter) {
+          KMP_HIP_TRY(hipGraphLaunch(ig.exec, s));
+          it += spec->poll_every;
+        } else {
+          if ((rc = path_iteration(s, pa, delta, kappa, spec->tol, spec->max_iter, restart)) != 0)
+            return rc;
+          ++it;
+        }
         if (pending) {
           int active = 0;
           if ((rc = read_poll(&active)) != 0) return rc;

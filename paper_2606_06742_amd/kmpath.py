@@ -26,6 +26,7 @@ KMP_FLAG_GLOBAL_SOLVE = 2
 KMP_FLAG_REFIT = 4
 KMP_FLAG_SHARED_FACTOR = 8
 KMP_FLAG_EXACT_HINGE = 16
+KMP_FLAG_EAGER = 32
 KMP_WNOTEXACT = 2
 KMP_NKC = 10
 KERNEL_CLASSES = ("gram", "panel", "panel_wy", "trail_update", "q_form", "precompute", "gemm_f",
@@ -250,11 +251,14 @@ class PathRunner:
 
     def __init__(self, X, y, loss, sigmas, lambdas, fold_id, V, taus=None, device="cuda",
                  sigma_batch: Optional[int] = None, kernel_timing=(), refit: bool = False,
-                 shared: bool = False, exact_hinge: bool = False, **spec_overrides):
+                 shared: bool = False, exact_hinge: bool = False, eager: bool = False,
+                 **spec_overrides):
         """refit=True: every (sigma, tau, lambda) on all n points (fold_id and V
         are ignored; outputs have V = 1, no CV sums, no selection).
         shared=True: exact CV on one factor of the full K per bandwidth
-        (KMP_FLAG_SHARED_FACTOR); V = n with fold_id = 0..n-1 is leave-one-out."""
+        (KMP_FLAG_SHARED_FACTOR); V = n with fold_id = 0..n-1 is leave-one-out.
+        eager=True: every iteration launched directly, never from a recorded
+        HIP graph (KMP_FLAG_EAGER)."""
         import torch
         self.torch = torch
         self.loss = loss
@@ -266,6 +270,8 @@ class PathRunner:
             self.spec.flags |= KMP_FLAG_SHARED_FACTOR
         if exact_hinge:
             self.spec.flags |= KMP_FLAG_EXACT_HINGE
+        if eager:
+            self.spec.flags |= KMP_FLAG_EAGER
         self.set_kernel_timing(kernel_timing)
         self.X = torch.as_tensor(np.ascontiguousarray(X), dtype=torch.float64, device=device) \
             if not isinstance(X, torch.Tensor) else X

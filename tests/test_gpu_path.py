@@ -85,6 +85,33 @@ def test_path_deterministic():
         assert np.array_equal(a[k], b[k]), k
 
 
+@pytest.mark.parametrize("name", ["C1", "H1"])
+def test_path_graph_replay_matches_eager(name):
+    """Orders up to 2048 replay the iterations between polls from a recorded
+    HIP graph (replayed many times per call, with the convergence polls and
+    host waits between replays). Two graph runs must agree bit for bit, and
+    with launches issued one by one (KMP_FLAG_EAGER) to the parity bars (the
+    graph's split-K factor covers all columns, so the rounding differs)."""
+    inp = W.make_inputs(W.get(name))
+    announce(f"fit_path {name}: graph replay against eager launches")
+    _gpu(inp, "hinge")                                   # warm-up (code objects, allocations)
+    e = _gpu(inp, "hinge", eager=True)
+    a = _gpu(inp, "hinge")
+    b = _gpu(inp, "hinge")
+    for k in ("alpha", "beta", "objective", "cv_sum", "cv_err", "iters", "status", "selected"):
+        assert np.array_equal(a[k], b[k]), k
+    assert np.array_equal(a["selected"], e["selected"])
+    assert np.abs(a["objective"] - e["objective"]).max() <= 1e-10 * np.abs(e["objective"]).max()
+    amax = np.abs(e["alpha"]).max(axis=-1, keepdims=True)
+    assert np.all(np.abs(a["alpha"] - e["alpha"]) <= 1e-7 * amax + 1e-300)
+    assert np.abs(a["cv_sum"] - e["cv_sum"]).max() <= 1e-8 * max(1.0, np.abs(e["cv_sum"]).max())
+    te, ta = e["timings"], a["timings"]
+    print(f"{name}: path {te['path_ms']:.2f} ms eager ({te['iterations']} iterations, "
+          f"{1e3 * te['path_ms'] / max(1, te['iterations']):.1f} us each), "
+          f"{ta['path_ms']:.2f} ms graph ({ta['iterations']} iterations, "
+          f"{1e3 * ta['path_ms'] / max(1, ta['iterations']):.1f} us each)")
+
+
 def test_path_c2_full_size_sampled():
     """Kernel logistic regression at full size (n = 2000, 3 bandwidths,
     5 folds, 50 lambdas): every cell's stationarity under the oracle's K,
