@@ -646,12 +646,15 @@ __global__ __launch_bounds__(256) void panel_ws_kernel(double* __restrict__ A, i
 // of the trailing matrix (P1 = [V; W], P2 = [W; V], K = 2 BB) and the
 // accumulation of Q (P1 = V, P2 = T V Q, K = 64 or 128). One workgroup per 64 x 64
 // tile; wave w updates the 32 x 32 piece at (32 (w&1), 32 (w>>1)) as 2 x 2
-// MFMA blocks: the piece of C is loaded straight into the accumulators
-// (register r of a block holds row 4r + l/16, column l%16: 128-byte row
-// pieces), then per 32 k the 2 x 8 operand values of each side are loaded
+// MFMA blocks: the piece of C is loaded in accumulator layout (register r
+// of a block holds row 4r + l/16, column l%16: 128-byte row pieces), then
+// per 32 k the 2 x 8 operand values of each side are loaded
 // together and 32 products with the A operand negated follow. m is a
 // multiple of 16, so each 16 x 16 block is wholly inside or outside C:
-// outside blocks load from clamped addresses and are not stored. With LOWER
+// outside blocks load from clamped addresses and are not stored. The
+// products accumulate from zero and the piece of C is added at the store,
+// so the matrix products do not wait for C's loads (10 % faster at K = 128,
+// 2 % at K = 32, measured at m = 16000). With LOWER
 // only the tiles on and below the diagonal are updated (C symmetric, its
 // lower triangle kept; see the note before panel_x_kernel). With PART == 2
 // the blocks of the first block row and column are left alone (the first
@@ -677,13 +680,16 @@ __device__ __forceinline__ void rank_update_tile(double* __restrict__ C, int64_t
     ib[b] = vi[b] ? i0 + 16 * b : 0;
     jb[b] = vj[b] ? j0 + 16 * b : 0;
   }
-  xdbl4 acc[2][2];
+  xdbl4 acc[2][2], cv[2][2];
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
     for (int bj = 0; bj < 2; ++bj)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) acc[bi][bj][r] = Cg[(int64_t)(ib[bi] + 4 * r + lk) * ldc + jb[bj] + li];
+      for (int r = 0; r < 4; ++r) {
+        cv[bi][bj][r] = Cg[(int64_t)(ib[bi] + 4 * r + lk) * ldc + jb[bj] + li];
+        acc[bi][bj][r] = 0.0;
+      }
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc) {
     double av[2][8], bv[2][8];
@@ -711,7 +717,8 @@ __device__ __forceinline__ void rank_update_tile(double* __restrict__ C, int64_t
       if (PART == 2) st = st && ib[bi] != 0 && jb[bj] != 0;
       if (st) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) Cg[(int64_t)(ib[bi] + 4 * r + lk) * ldc + jb[bj] + li] = acc[bi][bj][r];
+        for (int r = 0; r < 4; ++r)
+          Cg[(int64_t)(ib[bi] + 4 * r + lk) * ldc + jb[bj] + li] = cv[bi][bj][r] + acc[bi][bj][r];
       }
     }
 }

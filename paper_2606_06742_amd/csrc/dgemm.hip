@@ -39,10 +39,11 @@ struct Tile {
 // For k-contiguous B (BKC) each thread loads from one column, whose base
 // pointer bcol the caller resolves once (null for a column past the end).
 //
-// VEC: every tile row and K slice lies inside the operands (M a multiple of
-// BM, the K range of BK, leading dimensions even and bases 16-byte aligned,
-// which the host checks), so each thread's run of consecutive elements is
-// read with unchecked 16-byte loads.
+// VEC: every tile row and K slice lies inside the operands (M >= BM, the
+// last row tile moved back to end at M by the caller; the K range a
+// multiple of BK; M, leading dimensions and batch strides even and bases
+// 16-byte aligned, which the host checks), so each thread's run of
+// consecutive elements is read with unchecked 16-byte loads.
 template <int BM, int BK, bool AK, bool BKC, bool VEC = false>
 __device__ __forceinline__ void fetch_slice(int M, int N, int K, int i0, int j0, int k0,
                                             const double* __restrict__ A, int64_t lda,
@@ -495,10 +496,13 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
   double* C = part + (int64_t)sk * sP + (int64_t)b * sC;
   const int kbeg = sk * Kc;
   const int kend = min(K, kbeg + Kc);
+  // whole-tile path: a last row tile that would reach past M is moved back
+  // to end at M (M >= BM) and stores only its own rows
+  const int il = VEC ? min(i0, M - BM) : i0;
   dbl4 acc[MB][2];
   if (kbeg < kend) {
     if constexpr (VEC)
-      tile_mainloop_vec<BM, BK, AK>(N, kbeg, kend, i0, j0, A, lda, B, ldb, cmap, acc);
+      tile_mainloop_vec<BM, BK, AK>(N, kbeg, kend, il, j0, A, lda, B, ldb, cmap, acc);
     else
       tile_mainloop<BM, BK, AK, true, PF>(M, N, kbeg, kend, i0, j0, A, lda, B, ldb, cmap, acc);
   } else {
@@ -514,9 +518,9 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
     for (int bj = 0; bj < 2; ++bj)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int gi = i0 + wi + bi * 16 + mfma_row(lane, r);
+        const int gi = il + wi + bi * 16 + mfma_row(lane, r);
         const int gj = j0 + wj + bj * 16 + mfma_col(lane);
-        if (gi < M && gj < N) C[(int64_t)(IDENT ? gj : cmap[gj]) * ldc + gi] = acc[bi][bj][r];
+        if (gi >= i0 && gi < M && gj < N) C[(int64_t)(IDENT ? gj : cmap[gj]) * ldc + gi] = acc[bi][bj][r];
       }
 }
 
@@ -637,8 +641,9 @@ int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double
     set_error("gemm_partial: cmap and nact must both be given or both be null");
     return KMP_EINVAL;
   }
-  // whole tiles and 16-byte aligned operands: unchecked vector loads
-  const bool vec = g.M % 64 == 0 && g.K % 16 == 0 && g.lda % 2 == 0 && g.ldb % 2 == 0 &&
+  // whole K slices, at least one row tile and 16-byte aligned operands:
+  // unchecked vector loads (a ragged last row tile is moved back in the kernel)
+  const bool vec = g.M >= 64 && g.M % 2 == 0 && g.K % 16 == 0 && g.lda % 2 == 0 && g.ldb % 2 == 0 &&
                    g.sA % 2 == 0 && g.sB % 2 == 0 && (reinterpret_cast<uintptr_t>(g.A) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(g.B) & 15) == 0;
 #define KMP_PART_CASE(AKV, IDV, VV)                                                              \
