@@ -36,121 +36,6 @@ constexpr int kFusedYtRows = 1536;   // register panels that also form Y'
 constexpr int PQT = 512;         // threads of the panel factorisation
 constexpr int PQW = PQT / 64;
 
-// Sum over the block of h[c] for c in [lo, BB); result in out[c] (LDS).
-__device__ __forceinline__ void block_sum_vec(double (&h)[BB], int lo, double (*red)[BB],
-                                              double* out) {
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-#pragma unroll
-  for (int c = 0; c < BB; ++c) {
-    if (c >= lo) {                       // uniform
-      const double v = wave_sum(h[c]);
-      if (lane == 0) red[w][c] = v;
-    }
-  }
-  __syncthreads();
-  if (t < BB) {
-    double s = 0.0;
-    for (int q = 0; q < PQW; ++q) s += red[q][t];
-    out[t] = s;
-  }
-  __syncthreads();
-}
-
-// Householder QR of the panel P = A[m0:N, p:p+BB] of every matrix (one
-// workgroup per matrix), in place: R on and above the diagonal of P, v_i
-// below it (dlarfg convention, v_i[i] = 1 implicit). Thread t owns rows
-// r = t + PQT q of P. Step i needs, over rows r > i, the products
-// h_c = sum_r P[r][i] P[r][c] (c >= i): sigma = h_i, and v_i'P[:, c] =
-// P[i][c] + h_c / (alpha - beta). The update of step i and the products of
-// step i+1 are made in one pass over the rows.
-// Outputs: tau[p+i], and v_i transposed into row p+i of A (columns m0 ..,
-// zeros before its leading 1) and into rows i and 2BB+i of the panel buffer.
-__device__ __forceinline__ void panel_qr_stream_body(double* __restrict__ A, int N, int p,
-                                                     double* __restrict__ taus,
-                                                     double* __restrict__ panel, int g) {
-  __shared__ double red[PQW][BB];
-  __shared__ double hs[BB];
-  __shared__ double ws[BB];
-  const int t = threadIdx.x;
-  double* Ag = A + (int64_t)g * N * N;
-  const int m0 = p + BB, mrow = N - m0;
-  double* P = Ag + (int64_t)m0 * N + p;    // P[r][c] = P[r*N + c]
-  double h[BB];
-#pragma unroll
-  for (int c = 0; c < BB; ++c) h[c] = 0.0;
-  for (int r = 1 + t; r < mrow; r += PQT) {
-    const double* row = P + (int64_t)r * N;
-    const double x0 = row[0];
-#pragma unroll
-    for (int c = 0; c < BB; ++c) h[c] = fma(x0, row[c], h[c]);
-  }
-  block_sum_vec(h, 0, red, hs);
-  for (int i = 0; i < BB && i < mrow; ++i) {
-    const double* rowi = P + (int64_t)i * N;
-    const double alpha = rowi[i];
-    const double sigma = hs[i];
-    double tau = 0.0, beta = alpha, scale = 0.0;
-    if (sigma > 0.0) {
-      // the norm and the two reciprocals are on the step's dependency
-      // chain: hardware estimates refined by Newton-Raphson (IEEE sqrt for
-      // arguments near the bottom of the normal range)
-      const double s2 = fma(alpha, alpha, sigma);
-      beta = -copysign(s2 > 1e-280 ? sqrt_newton(s2) : sqrt(s2), alpha);
-      tau = (beta - alpha) * rcp_newton(beta);
-      scale = rcp_newton(alpha - beta);
-    }
-    if (t < BB) ws[t] = (t > i) ? fma(scale, hs[t], rowi[t]) : 0.0;   // v_i' P[:, t]
-    if (t == 0) taus[(int64_t)g * N + p + i] = tau;
-    __syncthreads();
-#pragma unroll
-    for (int c = 0; c < BB; ++c) h[c] = 0.0;
-    for (int r = t; r < mrow; r += PQT) {
-      if (r < i) continue;
-      double* row = P + (int64_t)r * N;
-      double x[BB];
-#pragma unroll
-      for (int c = 0; c < BB; ++c) x[c] = row[c];
-      const double vr = (r == i) ? 1.0 : x[i] * scale;
-#pragma unroll
-      for (int c = 0; c < BB; ++c)
-        if (c > i) x[c] = fma(-tau * vr, ws[c], x[c]);
-#pragma unroll
-      for (int c = 0; c < BB; ++c)
-        if (c == i) x[c] = (r == i) ? beta : vr;
-#pragma unroll
-      for (int c = 0; c < BB; ++c)
-        if (c >= i) row[c] = x[c];
-      if (r > i + 1 && i + 1 < BB) {
-        double x1 = 0.0;
-#pragma unroll
-        for (int c = 0; c < BB; ++c)
-          if (c == i + 1) x1 = x[c];
-#pragma unroll
-        for (int c = 0; c < BB; ++c)
-          if (c > i) h[c] = fma(x1, x[c], h[c]);
-      }
-    }
-    block_sum_vec(h, i + 1 < BB ? i + 1 : BB - 1, red, hs);
-  }
-  // reflectors, transposed: row i of Vt is v_i over rows m0 .. N-1
-  double* Vt = panel + (int64_t)g * 3 * BB * N;
-  for (int e = t; e < BB * mrow; e += PQT) {
-    const int i = e / mrow, r = e % mrow;
-    double v = 0.0;
-    if (r == i) v = 1.0;
-    else if (r > i) v = P[(int64_t)r * N + i];
-    Ag[(int64_t)(p + i) * N + m0 + r] = v;
-    Vt[(int64_t)i * N + m0 + r] = v;
-    Vt[(int64_t)(2 * BB + i) * N + m0 + r] = v;
-  }
-}
-
-__global__ __launch_bounds__(PQT) void panel_qr_kernel(double* __restrict__ A, int N, int p,
-                                                        double* __restrict__ taus,
-                                                        double* __restrict__ panel) {
-  panel_qr_stream_body(A, N, p, taus, panel, blockIdx.x);
-}
-
 // Register-resident panel factorisation with NW wavefronts: lane l of wave
 // w holds column c = l % 16 of row r = 4 NW m + 4 w + l / 16 in slot m
 // (m < RS). Step i needs only row i of the panel's Gram matrix,
@@ -195,6 +80,160 @@ __device__ __forceinline__ double swap_sum32_b(double v) {
   const auto hi = __builtin_amdgcn_permlane32_swap((unsigned)(b >> 32), (unsigned)(b >> 32), false, false);
   return __longlong_as_double((long long)(((unsigned long long)hi[0] << 32) | lo[0])) +
          __longlong_as_double((long long)(((unsigned long long)hi[1] << 32) | lo[1]));
+}
+
+// Householder QR of the panel P = A[m0:N, p:p+BB] of every matrix (one
+// workgroup per matrix), streamed from memory, in place: R on and above the
+// diagonal of P, v_i below it (dlarfg convention, v_i[i] = 1 implicit).
+// Lane l of wave w takes column c = l % 16 of the rows r = 4w + l/16 + 32k,
+// so a wavefront reads and writes four whole 128-byte rows per pass. Step i
+// needs, over rows r > i, the products h_c = sum_r P[r][i] P[r][c] (c >= i):
+// sigma = h_i, and v_i'P[:, c] = P[i][c] + h_c / (alpha - beta). P[r][i] and
+// the updated P[r][i+1] come from lanes i and i+1 of the row by DPP row
+// broadcasts (immediate lanes: the 16 steps are unrolled); the update of
+// step i and the products of step i+1 are made in one pass over the rows,
+// in batches of QB rows per lane whose loads are issued together. The
+// per-lane products are added over the four rows of a wavefront by permlane
+// swaps and over the wavefronts through LDS (double-buffered by step
+// parity), in a fixed order.
+// Outputs: tau[p+i], and v_i transposed into row p+i of A (columns m0 ..,
+// zeros before its leading 1) and into rows i and 2BB+i of the panel buffer.
+constexpr int QB = 8;            // rows per lane and batch of the streamed panel QR
+constexpr int QS = PQT / 16;     // rows per pass of the workgroup
+
+struct QrStream {
+  double* P;
+  int N, mrow, kf, s, c, w, sub, t;
+  double (*red)[PQW][BB];
+};
+
+// one pass over the rows: f(r, x) returns the new P[r][c] (stored when
+// STORE) and accumulates the products; whole batches of QB rows first
+// (every row valid), then the rest with the row index clamped for the loads
+template <bool STORE, typename F>
+__device__ __forceinline__ void qr_stream_rows(const QrStream& q, F f) {
+  int k0 = 0;
+  for (; k0 + QB <= q.kf; k0 += QB) {
+    double x[QB];
+#pragma unroll
+    for (int b = 0; b < QB; ++b) x[b] = q.P[(int64_t)(q.s + QS * (k0 + b)) * q.N + q.c];
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      const int r = q.s + QS * (k0 + b);
+      const double v = f(r, x[b]);
+      if (STORE) q.P[(int64_t)r * q.N + q.c] = v;
+    }
+  }
+  double x[QB];
+#pragma unroll
+  for (int b = 0; b < QB; ++b) x[b] = q.P[(int64_t)min(q.s + QS * (k0 + b), q.mrow - 1) * q.N + q.c];
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    const int r = q.s + QS * (k0 + b);
+    if (r < q.mrow) {
+      const double v = f(r, x[b]);
+      if (STORE) q.P[(int64_t)r * q.N + q.c] = v;
+    }
+  }
+}
+
+// h of the lane's column into red[B] (per wavefront), then one barrier
+template <int B>
+__device__ __forceinline__ void qr_stream_put(const QrStream& q, double h) {
+  const double v = swap_sum32_b(swap_sum16_b(h));
+  if (q.sub == 0) q.red[B][q.w][q.c] = v;
+  __syncthreads();
+}
+
+template <int I>
+__device__ __forceinline__ void qr_stream_steps(const QrStream& q, double* __restrict__ taus) {
+  if constexpr (I < BB) {
+    double hc = 0.0;                                   // h_c of the lane's column
+#pragma unroll
+    for (int j = 0; j < PQW; ++j) hc += q.red[I & 1][j][q.c];
+    const double sigma = row_bcast<I>(hc);
+    const double alpha = q.P[(int64_t)I * q.N + I];
+    double tau = 0.0, beta = alpha, scale = 0.0;
+    if (sigma > 0.0) {
+      // the norm and the two reciprocals are on the step's dependency
+      // chain: hardware estimates refined by Newton-Raphson (IEEE sqrt for
+      // arguments near the bottom of the normal range)
+      const double s2 = fma(alpha, alpha, sigma);
+      beta = -copysign(s2 > 1e-280 ? sqrt_newton(s2) : sqrt(s2), alpha);
+      tau = (beta - alpha) * rcp_newton(beta);
+      scale = rcp_newton(alpha - beta);
+    }
+    const double wsc = (q.c > I) ? fma(scale, hc, q.P[(int64_t)I * q.N + q.c]) : 0.0;  // v_I' P[:, c]
+    if (q.t == 0) taus[I] = tau;
+    __syncthreads();                                   // row I read by all before its update
+    const double ft = -tau;
+    const int c = q.c;
+    double h = 0.0;
+    qr_stream_rows<true>(q, [&](int r, double x) {
+      const double xi = row_bcast<I>(x);                             // P[r][I]
+      const double vr = (r == I) ? 1.0 : xi * scale;
+      const double fr = (r >= I) ? ft * vr : 0.0;
+      double xn = (c > I) ? fma(fr, wsc, x) : x;
+      if (c == I) xn = (r == I) ? beta : (r > I ? vr : x);
+      if constexpr (I + 1 < BB) {
+        const double x1 = row_bcast<I + 1>(xn);                      // updated P[r][I+1]
+        h = fma((r > I + 1) ? x1 : 0.0, xn, h);
+      }
+      return xn;
+    });
+    if constexpr (I + 1 < BB) qr_stream_put<(I + 1) & 1>(q, h);
+    qr_stream_steps<I + 1>(q, taus);
+  }
+}
+
+__device__ __forceinline__ void panel_qr_stream_body(double* __restrict__ A, int N, int p,
+                                                     double* __restrict__ taus,
+                                                     double* __restrict__ panel, int g) {
+  __shared__ double red[2][PQW][BB];
+  const int t = threadIdx.x, lane = t & 63;
+  double* Ag = A + (int64_t)g * N * N;
+  const int m0 = p + BB, mrow = N - m0;
+  QrStream q;
+  q.P = Ag + (int64_t)m0 * N + p;                    // P[r][c] = P[r*N + c]
+  q.N = N;
+  q.mrow = mrow;
+  q.kf = mrow / QS;
+  q.w = t >> 6;
+  q.sub = lane >> 4;
+  q.c = lane & 15;
+  q.s = 4 * q.w + q.sub;
+  q.t = t;
+  q.red = red;
+  // products of step 0: h_c = sum_{r >= 1} P[r][0] P[r][c]
+  {
+    double h = 0.0;
+    qr_stream_rows<false>(q, [&](int r, double x) {
+      const double x0 = row_bcast<0>(x);
+      h = fma((r >= 1) ? x0 : 0.0, x, h);
+      return x;
+    });
+    qr_stream_put<0>(q, h);
+  }
+  qr_stream_steps<0>(q, taus + (int64_t)g * N + p);
+  __syncthreads();                                   // the last step's rows
+  // reflectors, transposed: row i of Vt is v_i over rows m0 .. N-1
+  double* Vt = panel + (int64_t)g * 3 * BB * N;
+  double* P = q.P;
+  for (int e = t; e < BB * mrow; e += PQT) {
+    const int i = e / mrow, r = e % mrow;
+    double v = 0.0;
+    if (r == i) v = 1.0;
+    else if (r > i) v = P[(int64_t)r * N + i];
+    Ag[(int64_t)(p + i) * N + m0 + r] = v;
+    Vt[(int64_t)i * N + m0 + r] = v;
+    Vt[(int64_t)(2 * BB + i) * N + m0 + r] = v;
+  }
+}
+
+__global__ __launch_bounds__(PQT) void panel_qr_kernel(double* __restrict__ A, int N, int p,
+                                                        double* __restrict__ taus,
+                                                        double* __restrict__ panel) {
+  panel_qr_stream_body(A, N, p, taus, panel, blockIdx.x);
 }
 
 constexpr int PVT = 256;          // rows of the reflector staging tile
