@@ -693,8 +693,10 @@ __global__ __launch_bounds__(256) void panel_ws_kernel(double* __restrict__ A, i
 // outside blocks load from clamped addresses and are not stored. The
 // products accumulate from zero and the piece of C is added at the store,
 // so the matrix products do not wait for C's loads (10 % faster at K = 128,
-// 2 % at K = 32, measured at m = 16000). With LOWER
-// only the tiles on and below the diagonal are updated (C symmetric, its
+// 2 % at K = 32, measured at m = 16000); beyond the first 32 k, the
+// operands of each 32 are loaded during the products of the previous 32
+// (10 % more at K = 128). With LOWER only the tiles on and below the
+// diagonal are updated (C symmetric, its
 // lower triangle kept; see the note before panel_x_kernel). With PART == 2
 // the blocks of the first block row and column are left alone (the first
 // block column is updated beforehand, the first block row lies above the
@@ -729,24 +731,31 @@ __device__ __forceinline__ void rank_update_tile(double* __restrict__ C, int64_t
         cv[bi][bj][r] = Cg[(int64_t)(ib[bi] + 4 * r + lk) * ldc + jb[bj] + li];
         acc[bi][bj][r] = 0.0;
       }
-#pragma unroll
-  for (int kc = 0; kc < KC; ++kc) {
-    double av[2][8], bv[2][8];
+  // the operands of the next 32 k are loaded before the products of these
+  constexpr int NBUF = KC > 1 ? 2 : 1;
+  double av[NBUF][2][8], bv[NBUF][2][8];
+  auto load = [&](int kc, double (&a)[2][8], double (&bb)[2][8]) {
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int s8 = 0; s8 < 8; ++s8) {
         const int64_t k = 32 * kc + 4 * s8 + lk;
-        av[b][s8] = -A1[k * ld1 + ib[b] + li];
-        bv[b][s8] = A2[k * ld2 + jb[b] + li];
+        a[b][s8] = -A1[k * ld1 + ib[b] + li];
+        bb[b][s8] = A2[k * ld2 + jb[b] + li];
       }
+  };
+  load(0, av[0], bv[0]);
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc) {
+    if (kc + 1 < KC) load(kc + 1, av[(kc + 1) % NBUF], bv[(kc + 1) % NBUF]);
 #pragma unroll
     for (int s8 = 0; s8 < 8; ++s8)
 #pragma unroll
       for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj)
-          acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[bi][s8], bv[bj][s8], acc[bi][bj], 0, 0, 0);
+          acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[kc % NBUF][bi][s8], bv[kc % NBUF][bj][s8],
+                                                            acc[bi][bj], 0, 0, 0);
   }
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
