@@ -170,10 +170,13 @@ __device__ __forceinline__ double row4_sum(double v) { return swap_sum32(swap_su
 // does not wait on device memory: a block step takes far less than a load's
 // latency under load, so the loads of several steps must be in flight (the
 // vector-memory counter allows 63 per wave: 4 loads per forward step and 5
-// per backward step here). Forward tiles are read by rows
+// per backward step here). The depth also sets the registers of the
+// per-column update kernel: at 10 it stays within 256, so two of its
+// workgroups share a compute unit (at 12 it took 272 and one workgroup per
+// compute unit, which doubled the update time above 256 active columns). Forward tiles are read by rows
 // (V[j*N + 16 I + a], j = 4g+t), backward tiles by columns
 // (V[a*N + 16 I + j]) as the transposed factors need.
-constexpr int SPF = 12;
+constexpr int SPF = 10;
 
 // One forward block step of the LDS solve: rg holds the lane's four entries
 // of tile I and receives those of tile min(I + SPF, NB - 1). Branch free, so
