@@ -261,7 +261,9 @@ def solve_cell(K, y, lam, loss, delta=None, tau=None, tol=1e-13, max_iter=500,
 
 def _refine(K, y, alpha, beta, lam, loss, delta, tau, norm, max_steps=12):
     """Newton corrections with extended-precision residuals (see the module
-    note). Stops when a correction no longer lowers the residual. Returns the
+    note). Above the convergence bar a step that does not lower the residual
+    is halved until it does (at most 12 times); the refinement stops when no
+    step lowers it, or at the bar after a full step that does not. Returns the
     refined point rounded to fp64 (half an ulp per entry), the residual of the
     refined point itself and the number of corrections taken."""
     ld = np.longdouble
@@ -281,7 +283,21 @@ def _refine(K, y, alpha, beta, lam, loss, delta, tau, norm, max_steps=12):
         b2 = b + ld(db)
         Ra2, Rb2, f2, res2 = residual_ext(K, y, a2, b2, lam, loss, delta, tau, norm)
         if not res2 < res:
-            break
+            if res <= CONVERGED_KKT:
+                break
+            # the stationarity conditions are only piecewise smooth (a point
+            # entering or leaving its quadratic zone), so a full step can
+            # overshoot: halve it until the residual falls, up to 12 times
+            t = 1.0
+            for _ in range(12):
+                t *= 0.5
+                a2 = a + (t * da).astype(ld)
+                b2 = b + ld(t * db)
+                Ra2, Rb2, f2, res2 = residual_ext(K, y, a2, b2, lam, loss, delta, tau, norm)
+                if res2 < res:
+                    break
+            if not res2 < res:
+                break
         a, b, Ra, Rb, f, res = a2, b2, Ra2, Rb2, f2, res2
         steps += 1
     return a.astype(np.float64), float(b), res, steps
