@@ -187,12 +187,14 @@ def roofline(kt, workload, name=None):
         return None
     if name is None:
         name = max(kt, key=lambda k: kt[k][0] / kt[k][1] * kt[k][2])
-    ms, launches, seen, nbytes, flops = kt[name]
+    ms, launches, seen, nbytes, flops = kt[name][:5]
     sec = 1e-3 * ms
     common = {"kernel": name, "algorithmic_bytes_per_launch": nbytes / launches,
               "algorithmic_flops_per_launch": flops / launches,
               "avg_launch_us": 1e3 * ms / launches, "timed_launches": launches,
               "traffic": profiled_traffic(name, workload)}
+    if name in MFMA_CLASSES:
+        common["regimes"] = regimes(kt[name])
     if name in MFMA_CLASSES and nbytes > 0 and flops / nbytes >= RIDGE:
         achieved = flops / sec / 1e12
         return {"bound": "mfma", "achieved": achieved, "peak": FP64_PEAK_TFS, "unit": "TFLOP/s",
@@ -200,6 +202,24 @@ def roofline(kt, workload, name=None):
     achieved = nbytes / sec / 1e9
     return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS, **common}
+
+
+def regimes(v):
+    """The bracketed launches of one class split at the ridge point by their
+    own algorithmic intensity, each part priced against its own roof: the
+    launches above it against the fp64 matrix peak (flops), the others
+    against HBM bandwidth (bytes)."""
+    ms, launches, _, nbytes, flops, ms_mb, n_mb, bytes_mb, flops_mb = v
+    out = {}
+    if n_mb > 0 and ms_mb > 0:
+        a = flops_mb / (1e-3 * ms_mb) / 1e12
+        out["mfma"] = {"launches": n_mb, "ms": ms_mb, "achieved": a, "peak": FP64_PEAK_TFS,
+                       "unit": "TFLOP/s", "frac": a / FP64_PEAK_TFS}
+    if launches - n_mb > 0 and ms - ms_mb > 0:
+        a = (nbytes - bytes_mb) / (1e-3 * (ms - ms_mb)) / 1e9
+        out["hbm"] = {"launches": launches - n_mb, "ms": ms - ms_mb, "achieved": a,
+                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a / HBM_PEAK_GBS}
+    return out
 
 
 def kernel_table(kt, steps):
@@ -225,13 +245,10 @@ def run_steps(runner, stream, steps, dev):
         runner.run(stream)
         for k in phases:
             phases[k] += getattr(runner.timings, k)
-        for name, (ms, cnt, seen, nbytes, flops) in runner.kernel_times().items():
-            a = kt.setdefault(name, [0.0, 0, 0, 0.0, 0.0])
-            a[0] += ms
-            a[1] += cnt
-            a[2] += seen
-            a[3] += nbytes
-            a[4] += flops
+        for name, vals in runner.kernel_times().items():
+            a = kt.setdefault(name, [0.0, 0, 0, 0.0, 0.0, 0.0, 0, 0.0, 0.0])
+            for j, v in enumerate(vals):
+                a[j] += v
         log(f"step {i + 1}/{steps} done")
     torch.cuda.synchronize(dev)
     return time.perf_counter() - t0, phases, kt

@@ -160,6 +160,14 @@ typedef struct {
   int64_t kernel_seen[KMP_NKC];      /* all launches of the class            */
   double kernel_bytes[KMP_NKC];
   double kernel_flops[KMP_NKC];
+  /* the part of the four sums above that comes from bracketed launches whose
+   * algorithmic intensity (flops per byte) is above the ridge point of the
+   * device, fp64 matrix peak over HBM peak (78.6e12 / 8e12 flop/B): those
+   * launches are bound by the matrix cores, the others by memory bandwidth  */
+  double kernel_ms_mb[KMP_NKC];
+  int64_t kernel_launches_mb[KMP_NKC];
+  double kernel_bytes_mb[KMP_NKC];
+  double kernel_flops_mb[KMP_NKC];
 } kmp_timings;
 
 void kmp_default_spec(kmp_path_spec* spec);

@@ -19,6 +19,11 @@ static thread_local std::string g_err;
 void set_error(const std::string& msg) { g_err = msg; }
 const char* last_error() { return g_err.c_str(); }
 
+// Ridge point of the device: fp64 matrix peak over HBM peak (78.6 TFLOP/s,
+// 8 TB/s). A launch whose algorithmic flops per byte exceed it is bound by
+// the matrix cores, otherwise by memory bandwidth.
+constexpr double kRidgeFlopPerByte = 78.6e12 / 8.0e12;
+
 // Event brackets around selected launches; events come from a per-thread
 // pool that lives as long as the thread and is reused by every call.
 struct KernelClock {
@@ -1211,6 +1216,10 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
       timings->kernel_seen[k] = g_clock ? g_clock->seen[k] : 0;
       timings->kernel_bytes[k] = 0.0;
       timings->kernel_flops[k] = 0.0;
+      timings->kernel_ms_mb[k] = 0.0;
+      timings->kernel_launches_mb[k] = 0;
+      timings->kernel_bytes_mb[k] = 0.0;
+      timings->kernel_flops_mb[k] = 0.0;
     }
     if (g_clock && !g_clock->failed) {
       for (const auto& r : g_clock->recs) {
@@ -1220,6 +1229,12 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
         timings->kernel_launches[r.cls] += 1;
         timings->kernel_bytes[r.cls] += r.bytes;
         timings->kernel_flops[r.cls] += r.flops;
+        if (r.flops > kRidgeFlopPerByte * r.bytes) {
+          timings->kernel_ms_mb[r.cls] += ms;
+          timings->kernel_launches_mb[r.cls] += 1;
+          timings->kernel_bytes_mb[r.cls] += r.bytes;
+          timings->kernel_flops_mb[r.cls] += r.flops;
+        }
       }
     }
     timings->gram_ms = t_gram;

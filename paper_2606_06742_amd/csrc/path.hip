@@ -310,134 +310,159 @@ __device__ __forceinline__ void grid_vec_sync() {
 }
 
 // The same solve for orders whose vector does not fit in LDS. Row r =
-// BND I + a belongs to the lead lane (a, 0) of the wavefront: it alone takes
-// the input of the row (win(r), from data written before the kernel), keeps
-// the forward result y_r in device memory (ysc[r], read back by itself in the
-// backward sweep) and hands the solution to wout(r, x_r). The blocks that the
-// other lanes need are staged in an LDS ring of two BND-double slots (block
-// I in slot I & 1). No lane reads device memory written by another lane of
-// the same launch.
+// BND I + a belongs to lane row a of the wavefront: its input is wsc * win[r]
+// (device memory written before the solve; the four lanes of the row load
+// the same address and the lead lane (a, 0) keeps the value), the forward result
+// y_r is kept in device memory (ysc[r], stored by the four lanes of the row
+// with the same value and read back by them in the backward sweep), and the
+// solution goes to wout(r, x_r, lead), called by every lane, the lead lane
+// flagged. The blocks that the other lanes need are staged in an LDS ring of
+// two BND-double slots (block I in slot I & 1). No lane reads device memory
+// written by another lane of the same launch. As in band_solve, the sweeps
+// run whole groups of SPFG blocks through branch-free steps (prefetch index
+// clamped, the first block as a select, stores unconditional) and the
+// remaining blocks after them, and every prefetched value is a plain load
+// that is first used SPFG steps later: the loads complete in issue order,
+// so a branch around them, or arithmetic on a value just loaded, makes the
+// step wait for every load in flight, and each step then took as long as a
+// device-memory load.
 // Prefetch depth of the device-memory solve (5 loads per forward step, 6
 // per backward step).
 constexpr int SPFG = 10;
 
-template <typename WIn, typename WOut>
+__device__ __forceinline__ void bandg_fwd_step(const double* __restrict__ Vc,
+                                               const double* __restrict__ win, double wsc,
+                                               double* ysc, double* ring, int N, int NB, int I,
+                                               int a, int g, bool lead, double (&rg)[4],
+                                               double& wr) {
+  double cn[4], lm[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const double v = rg[t];
+    cn[t] = (4 * g + t >= a && I > 0) ? -v : 0.0;
+    lm[t] = (4 * g + t < a) ? v : 0.0;
+  }
+  double p0 = lead ? wsc * wr : 0.0, p1 = 0.0;
+  const int In = min(I + SPFG, NB - 1);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) rg[t] = Vc[(int64_t)(4 * g + t) * N + BND * In + a];
+  wr = win[BND * In + a];
+  double* cur = ring + BND * (I & 1);
+  const double* yp = ring + BND * ((I + 1) & 1) + 4 * g;   // block I - 1 (zeros before block 0)
+  p0 = fma(cn[0], yp[0], p0);
+  p1 = fma(cn[1], yp[1], p1);
+  p0 = fma(cn[2], yp[2], p0);
+  p1 = fma(cn[3], yp[3], p1);
+  const double r = row4_sum(p0 + p1);
+  cur[a] = r;
+  wave_sync();
+  const double* rp = cur + 4 * g;
+  double q0 = lead ? r : 0.0, q1 = 0.0;
+  q0 = fma(lm[0], rp[0], q0);
+  q1 = fma(lm[1], rp[1], q1);
+  q0 = fma(lm[2], rp[2], q0);
+  q1 = fma(lm[3], rp[3], q1);
+  const double yv = row4_sum(q0 + q1);
+  cur[a] = yv;
+  ysc[BND * I + a] = yv;
+  wave_sync();
+}
+
+template <typename WOut>
+__device__ __forceinline__ void bandg_bwd_step(const double* __restrict__ Vc,
+                                               const double* __restrict__ Dc, const double* ysc,
+                                               double* ring, int N, int NB, int tt, int a, int g,
+                                               bool lead, double (&rg)[4], double& dr, double& wr,
+                                               double (&vprev)[4], WOut wout) {
+  const int I = NB - 1 - tt;
+  double cn[4], lm[4], vv[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    vv[t] = rg[t];
+    cn[t] = (a >= 4 * g + t && tt > 0) ? -vprev[t] : 0.0;
+    lm[t] = (4 * g + t > a) ? vv[t] : 0.0;
+  }
+  double p0 = lead ? dr * wr : 0.0, p1 = 0.0;
+  const int In = max(I - SPFG, 0);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) rg[t] = Vc[(int64_t)a * N + BND * In + 4 * g + t];
+  dr = Dc[BND * In + a];
+  wr = ysc[BND * In + a];
+  double* cur = ring + BND * (I & 1);
+  const double* xp = ring + BND * ((I + 1) & 1) + 4 * g;   // block I + 1
+  p0 = fma(cn[0], xp[0], p0);
+  p1 = fma(cn[1], xp[1], p1);
+  p0 = fma(cn[2], xp[2], p0);
+  p1 = fma(cn[3], xp[3], p1);
+  const double sv = row4_sum(p0 + p1);
+  cur[a] = sv;
+  wave_sync();
+  const double* sp = cur + 4 * g;
+  double q0 = lead ? sv : 0.0, q1 = 0.0;
+  q0 = fma(lm[0], sp[0], q0);
+  q1 = fma(lm[1], sp[1], q1);
+  q0 = fma(lm[2], sp[2], q0);
+  q1 = fma(lm[3], sp[3], q1);
+  const double xv = row4_sum(q0 + q1);
+  cur[a] = xv;
+  wout(BND * I + a, xv, lead);
+  wave_sync();
+#pragma unroll
+  for (int t = 0; t < 4; ++t) vprev[t] = vv[t];
+}
+
+template <typename WOut>
 __device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
-                                             const double* __restrict__ Dc, double* ysc,
-                                             double* ring, int N, int lane, WIn win, WOut wout) {
+                                             const double* __restrict__ Dc,
+                                             const double* __restrict__ win, double wsc,
+                                             double* ysc, double* ring, int N, int lane,
+                                             WOut wout) {
   const int NB = N / BND;
+  const int NBm = NB - NB % SPFG;
   const int a = lane & 15, g = lane >> 4;
   const bool lead = g == 0;
-  double ring_t[SPFG][4], wv[SPFG];
+  // the slot read as block -1 holds zeros (its products are zero multiples)
+  ring[BND + a] = 0.0;
+  wave_sync();
+  double rt[SPFG][4], wr[SPFG];
 #pragma unroll
   for (int p = 0; p < SPFG; ++p) {
-    const int Ib = p < NB ? p : NB - 1;
+    const int Ib = min(p, NB - 1);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * Ib + a];
-    wv[p] = lead ? win(BND * Ib + a) : 0.0;
+    for (int t = 0; t < 4; ++t) rt[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * Ib + a];
+    wr[p] = win[BND * Ib + a];
   }
-  for (int I0 = 0; I0 < NB; I0 += SPFG) {
+  for (int I0 = 0; I0 < NBm; I0 += SPFG) {
 #pragma unroll
-    for (int p = 0; p < SPFG; ++p) {
-      const int I = I0 + p;
-      if (I < NB) {
-        double cn[4], lm[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const double v = ring_t[p][t];
-          cn[t] = (4 * g + t >= a) ? -v : 0.0;
-          lm[t] = (4 * g + t < a) ? v : 0.0;
-        }
-        double p0 = wv[p], p1 = 0.0;
-        const int In = (I + SPFG < NB) ? I + SPFG : NB - 1;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * In + a];
-        wv[p] = lead ? win(BND * In + a) : 0.0;
-        double* cur = ring + BND * (I & 1);
-        if (I > 0) {
-          const double* yp = ring + BND * ((I - 1) & 1) + 4 * g;
-          p0 = fma(cn[0], yp[0], p0);
-          p1 = fma(cn[1], yp[1], p1);
-          p0 = fma(cn[2], yp[2], p0);
-          p1 = fma(cn[3], yp[3], p1);
-        }
-        const double r = row4_sum(p0 + p1);
-        if (lead) cur[a] = r;
-        wave_sync();
-        const double* rp = cur + 4 * g;
-        double q0 = lead ? r : 0.0, q1 = 0.0;
-        q0 = fma(lm[0], rp[0], q0);
-        q1 = fma(lm[1], rp[1], q1);
-        q0 = fma(lm[2], rp[2], q0);
-        q1 = fma(lm[3], rp[3], q1);
-        const double yv = row4_sum(q0 + q1);
-        if (lead) {
-          cur[a] = yv;
-          ysc[BND * I + a] = yv;
-        }
-        wave_sync();
-      }
-    }
+    for (int p = 0; p < SPFG; ++p)
+      bandg_fwd_step(Vc, win, wsc, ysc, ring, N, NB, I0 + p, a, g, lead, rt[p], wr[p]);
   }
+#pragma unroll
+  for (int p = 0; p < SPFG; ++p)
+    if (NBm + p < NB)
+      bandg_fwd_step(Vc, win, wsc, ysc, ring, N, NB, NBm + p, a, g, lead, rt[p], wr[p]);
   wave_sync();
   double dring[SPFG];
 #pragma unroll
   for (int p = 0; p < SPFG; ++p) {
-    const int Ib = (NB - 1 - p >= 0) ? NB - 1 - p : 0;
+    const int Ib = max(NB - 1 - p, 0);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)a * N + BND * Ib + 4 * g + t];
+    for (int t = 0; t < 4; ++t) rt[p][t] = Vc[(int64_t)a * N + BND * Ib + 4 * g + t];
     dring[p] = Dc[BND * Ib + a];
-    wv[p] = lead ? ysc[BND * Ib + a] : 0.0;
+    wr[p] = ysc[BND * Ib + a];
   }
   double vprev[4] = {0.0, 0.0, 0.0, 0.0};
-  for (int T0 = 0; T0 < NB; T0 += SPFG) {
+  for (int T0 = 0; T0 < NBm; T0 += SPFG) {
 #pragma unroll
-    for (int p = 0; p < SPFG; ++p) {
-      const int tt = T0 + p;
-      if (tt < NB) {
-        const int I = NB - 1 - tt;
-        double cn[4], lm[4], vv[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          vv[t] = ring_t[p][t];
-          cn[t] = (a >= 4 * g + t) ? -vprev[t] : 0.0;
-          lm[t] = (4 * g + t > a) ? vv[t] : 0.0;
-        }
-        const double dv = dring[p];
-        double p0 = lead ? dv * wv[p] : 0.0, p1 = 0.0;
-        const int In = (I - SPFG >= 0) ? I - SPFG : 0;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) ring_t[p][t] = Vc[(int64_t)a * N + BND * In + 4 * g + t];
-        dring[p] = Dc[BND * In + a];
-        wv[p] = lead ? ysc[BND * In + a] : 0.0;
-        double* cur = ring + BND * (I & 1);
-        if (tt > 0) {
-          const double* xp = ring + BND * ((I + 1) & 1) + 4 * g;
-          p0 = fma(cn[0], xp[0], p0);
-          p1 = fma(cn[1], xp[1], p1);
-          p0 = fma(cn[2], xp[2], p0);
-          p1 = fma(cn[3], xp[3], p1);
-        }
-        const double sv = row4_sum(p0 + p1);
-        if (lead) cur[a] = sv;
-        wave_sync();
-        const double* sp = cur + 4 * g;
-        double q0 = lead ? sv : 0.0, q1 = 0.0;
-        q0 = fma(lm[0], sp[0], q0);
-        q1 = fma(lm[1], sp[1], q1);
-        q0 = fma(lm[2], sp[2], q0);
-        q1 = fma(lm[3], sp[3], q1);
-        const double xv = row4_sum(q0 + q1);
-        if (lead) {
-          cur[a] = xv;
-          wout(BND * I + a, xv);
-        }
-        wave_sync();
-#pragma unroll
-        for (int t = 0; t < 4; ++t) vprev[t] = vv[t];
-      }
-    }
+    for (int p = 0; p < SPFG; ++p)
+      bandg_bwd_step(Vc, Dc, ysc, ring, N, NB, T0 + p, a, g, lead, rt[p], dring[p], wr[p], vprev,
+                     wout);
   }
+#pragma unroll
+  for (int p = 0; p < SPFG; ++p)
+    if (NBm + p < NB)
+      bandg_bwd_step(Vc, Dc, ysc, ring, N, NB, NBm + p, a, g, lead, rt[p], dring[p], wr[p], vprev,
+                     wout);
   wave_sync();
 }
 
@@ -466,12 +491,60 @@ static int lds_vec_max() {
   return cached[dev];
 }
 static bool path_global_vec(const PathArrays& p) { return p.global_solve || p.N > lds_vec_max(); }
-static int path_lds_doubles(const PathArrays& p, int extra) {
-  return path_global_vec(p) ? extra + RING : p.N + extra;
+static int path_lds_doubles(const PathArrays& p, int extra, bool gv) {
+  return gv ? extra + RING : p.N + extra;
 }
-static int path_waves(const PathArrays& p, int extra) {
-  const size_t per = sizeof(double) * (size_t)path_lds_doubles(p, extra);
+static int path_lds_doubles(const PathArrays& p, int extra) {
+  return path_lds_doubles(p, extra, path_global_vec(p));
+}
+static int path_waves(const PathArrays& p, int extra, bool gv) {
+  const size_t per = sizeof(double) * (size_t)path_lds_doubles(p, extra, gv);
   return 4 * per <= 64 * 1024 ? 4 : 1;
+}
+static int path_waves(const PathArrays& p, int extra) { return path_waves(p, extra, path_global_vec(p)); }
+
+// Compute units and LDS bytes per compute unit of the current device
+// (queried once per device; zero when the query fails).
+struct CuShape {
+  int cus = 0, lds = 0;
+};
+static CuShape cu_shape() {
+  static CuShape cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return CuShape{};
+  if (cached[dev].cus == 0) {
+    int cus = 0, lds = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+            hipSuccess)
+      return CuShape{};
+    cached[dev].cus = cus;
+    cached[dev].lds = lds;
+  }
+  return cached[dev];
+}
+
+// Where this iteration's update keeps the solve's vector. The LDS form
+// (update_column_kernel: one column per workgroup, its N doubles in LDS,
+// at most 256 registers per lane) keeps two columns per compute unit at
+// most, fewer when LDS allows fewer; the device-memory form
+// (solve_step_kernel: four columns per workgroup, over 256 registers, one
+// workgroup per compute unit) keeps four. When more columns are active than
+// the LDS form holds at once, the device-memory form needs fewer rounds and
+// is taken (at C3, above 512 active columns: 623 against 717 us per
+// iteration; below, the LDS form's shorter steps win: 280 against 380 us).
+// The counts are the host's copy of the last poll, which only overestimates
+// the active columns.
+static bool iteration_global_vec(const PathArrays& p) {
+  if (path_global_vec(p)) return true;
+  if (!p.nact_host) return false;
+  const CuShape d = cu_shape();
+  if (d.cus <= 0 || d.lds <= 0) return false;
+  int64_t act = 0;
+  for (int g = 0; g < p.G; ++g) act += p.nact_host[g];
+  const int64_t per_wg = (int64_t)sizeof(double) * p.N + 2048;
+  const int64_t res_lds = std::max<int64_t>(1, std::min<int64_t>(2, d.lds / per_wg));
+  return ceil_div(act, 4 * (int64_t)d.cus) < ceil_div(act, res_lds * d.cus);
 }
 
 // ---------------------------------------------------- band products B x
@@ -708,13 +781,13 @@ __global__ __launch_bounds__(256) void stage_vectors_kernel(
   const int64_t base = gc * (int64_t)N;
   double cv = 0.0;
   if constexpr (GV) {
-    // lead lanes: input c sc, forward results kept in vhat, vhat = x
+    // input c sc, forward results kept in vhat, then vhat = x
     double* vg = vhat + base;
-    band_solve_g(Vc, Dc, vg, xs, N, lane, [&](int r) { return cg[r] * sc; },
-                 [&](int r, double x) {
-                   vg[r] = x;
-                   cv = fma(cg[r], x, cv);
-                 });
+    band_solve_g(Vc, Dc, cg, sc, vg, xs, N, lane, [&](int r, double x, bool) { vg[r] = x; });
+    // x was written by the lanes of its rows and is read by every lane
+    grid_vec_sync();
+#pragma unroll 8
+    for (int i = lane; i < N; i += 64) cv = fma(cg[i], vg[i], cv);
   } else {
 #pragma unroll 8
     for (int i = lane; i < N; i += 64) xs[i] = cg[i] * sc;
@@ -846,7 +919,8 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
       const int i = i0 + lane + 64 * q;
       if (i < N) {
         const double w = fma(2.0 * lam, ab[q], zs[q]);
-        if constexpr (!GV) xs[i] = w;
+        if constexpr (GV) estep[base + i] = w;
+        else xs[i] = w;
         tl = fma(uv[q], w, tl);
         n2 = fma(w, w, n2);
       }
@@ -878,24 +952,13 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
   // step below overwrites row by row after reading it
   const double* xsrc = xs;
   if constexpr (GV) {
-    // lead lanes form w of their rows from the inputs (prefetched ahead in
-    // the sweep), keep forward results in a+ (anew) and store x in e
-    const int64_t sPk = sP;
+    // w (stored in e by the pass above) is the solve's input, forward
+    // results are kept in a+ (anew), and x overwrites w in e
     double* xg = estep + base;
-    band_solve_g(
-        Vfac + gc * (int64_t)BND * N, Dfac + base, anew + base, xs, N, lane,
-        [&](int r) {
-          const int64_t ic = base + r;
-          double z = zpart[ic];
-#pragma unroll
-          for (int sk = 1; sk < kMaxSplitK; ++sk) {
-            const double zz = zpart[(sk < S2 ? sk : 0) * sPk + ic];
-            z += (sk < S2) ? zz : 0.0;
-          }
-          return fma(2.0 * lam, abar[ic], z);
-        },
-        [&](int r, double x) { xg[r] = x; });
-    // x was written by the lead lanes and is read by every lane below
+    grid_vec_sync();
+    band_solve_g(Vfac + gc * (int64_t)BND * N, Dfac + base, xg, 1.0, anew + base, xs, N, lane,
+                 [&](int r, double x, bool) { xg[r] = x; });
+    // x was written by the lanes of its rows and is read by every lane below
     grid_vec_sync();
     xsrc = xg;
   } else {
@@ -1149,7 +1212,8 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP, p.cmap, p.nact)) != 0) return rc;
   kc_end(KMP_KC_GEMM_ZHAT, s, gbytes, gflops);
   const int64_t cols = (int64_t)p.G * p.C;
-  if (!path_global_vec(p)) {
+  const bool gv = iteration_global_vec(p);
+  if (!gv) {
     // one workgroup per column, momentum and B abar included
     const size_t lds_u = sizeof(double) * (size_t)p.N;
     KMP_HIP_TRY(hipFuncSetAttribute((const void*)update_column_kernel,
@@ -1171,9 +1235,8 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
            over_active(p, [&](double n, double c) { return (8.0 * BND + 16.0) * n * c; }));
     return 0;
   }
-  const int cw = path_waves(p, 0);
-  const size_t lds = sizeof(double) * (size_t)cw * path_lds_doubles(p, 0);
-  const bool gv = path_global_vec(p);
+  const int cw = path_waves(p, 0, gv);
+  const size_t lds = sizeof(double) * (size_t)cw * path_lds_doubles(p, 0, gv);
   const void* kfn = gv ? (const void*)solve_step_kernel<true> : (const void*)solve_step_kernel<false>;
   KMP_HIP_TRY(hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   kc_begin(KMP_KC_UPDATE, s);

@@ -48,18 +48,24 @@ class kmp_timings(C.Structure):
                 ("iterations", C.c_int64), ("cell_iterations", C.c_int64),
                 ("kernel_ms", C.c_double * KMP_NKC), ("kernel_launches", C.c_int64 * KMP_NKC),
                 ("kernel_seen", C.c_int64 * KMP_NKC),
-                ("kernel_bytes", C.c_double * KMP_NKC), ("kernel_flops", C.c_double * KMP_NKC)]
+                ("kernel_bytes", C.c_double * KMP_NKC), ("kernel_flops", C.c_double * KMP_NKC),
+                ("kernel_ms_mb", C.c_double * KMP_NKC), ("kernel_launches_mb", C.c_int64 * KMP_NKC),
+                ("kernel_bytes_mb", C.c_double * KMP_NKC), ("kernel_flops_mb", C.c_double * KMP_NKC)]
 
     def as_dict(self):
         return {k: (list(getattr(self, k)) if k.startswith("kernel_") else getattr(self, k))
                 for k, _ in self._fields_}
 
     def kernels(self):
-        """{class: (ms, bracketed launches, all launches, bytes, flops)} of the
-        timed classes; ms, bytes and flops cover the bracketed launches."""
+        """{class: (ms, bracketed launches, all launches, bytes, flops, and
+        ms, launches, bytes, flops of the bracketed launches above the ridge
+        point)} of the timed classes; ms, bytes and flops cover the bracketed
+        launches."""
         return {KERNEL_CLASSES[i]: (self.kernel_ms[i], int(self.kernel_launches[i]),
                                     int(self.kernel_seen[i]), self.kernel_bytes[i],
-                                    self.kernel_flops[i])
+                                    self.kernel_flops[i], self.kernel_ms_mb[i],
+                                    int(self.kernel_launches_mb[i]), self.kernel_bytes_mb[i],
+                                    self.kernel_flops_mb[i])
                 for i in range(KMP_NKC) if self.kernel_launches[i] > 0}
 
 
