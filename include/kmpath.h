@@ -117,9 +117,9 @@ extern "C" {
 #define KMP_KC_TRAIL 3        /* a2 trailing update A22 -= V W' + W V' (MFMA)  */
 #define KMP_KC_QFORM 4        /* a2 compact-WY accumulation of Q (MFMA)        */
 #define KMP_KC_PRECOMPUTE 5   /* a3 per-stage column factors                   */
-#define KMP_KC_GEMM_F 6       /* a4+a5 f = Q (B abar) with the loss epilogue   */
+#define KMP_KC_GEMM_F 6       /* a4+a5 f = (Q B) abar with the loss epilogue   */
 #define KMP_KC_GEMM_ZHAT 7    /* a6 zhat = Q' z                                */
-#define KMP_KC_UPDATE 8       /* a7 banded solve, step, KKT, restart, B abar   */
+#define KMP_KC_UPDATE 8       /* a7 banded solve, step, KKT, restart, momentum */
 #define KMP_KC_FINALIZE 9     /* a10                                           */
 #define KMP_NKC 10
 
@@ -303,7 +303,7 @@ int kmp_path_step(void* stream, int32_t loss, double delta, const double* K, int
                   const double* alpha_in, const double* beta_in, double* alpha_out,
                   double* beta_out, double* kkt_out);
 
-/* The path's dense products on their own (a4 f = Q (B abar) and a6
+/* The path's dense products on their own (a4 f = (Q B) abar and a6
  * zhat = Q' z are such products, Appendix A.3: every iteration is O(n^2)
  * matrix products): C_g = A_g B_g for g < G, fp64 on the matrix cores.
  * A DEVICE, G blocks of M x K row-major at A + g*M*K; B DEVICE, K x N

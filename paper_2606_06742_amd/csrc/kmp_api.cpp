@@ -287,9 +287,9 @@ struct Carver {
 struct Layout {
   double *A, *Qm, *diag, *off, *tau, *cvec, *ylab, *panel, *dots, *tmat, *gram, *xbuf, *ybuf;
   double *spart, *pnext, *band, *bpart, *gram_all, *tmat_all, *cross_all, *xpart;
-  double *ahat, *abar, *bmat, *zmat, *anew, *estep, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
-  double *beta, *bbar, *rmom, *gcoef, *kkt, *coef, *lam, *taucol, *fbuf, *nrm, *inv2s2;
-  int *flag, *moved, *iters, *iters_total, *active, *nvg, *chk, *cmap, *nact, *stat_count, *cnv;
+  double *ahat, *abar, *zmat, *anew, *estep, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
+  double *beta, *bbar, *rmom, *gcoef, *kkt, *lam, *taucol, *fbuf, *nrm, *inv2s2;
+  int *flag, *iters, *iters_total, *active, *nvg, *chk, *cmap, *nact, *stat_count, *cnv;
   int32_t *tidx, *hidx, *fold, *rfold, *cfold;
   // exact hinge recovery (only with KMP_FLAG_EXACT_HINGE)
   int32_t *ex_state, *ex_elist;
@@ -324,7 +324,6 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.xpart = c.take<double>((size_t)kMaxSplitK * G * 2 * kWyBlock * N);
   l.ahat = c.take<double>(cols * N);
   l.abar = c.take<double>(cols * N);
-  l.bmat = c.take<double>(cols * N);
   l.zmat = c.take<double>(cols * N);
   l.anew = c.take<double>(cols * N);
   l.estep = c.take<double>(cols * N);
@@ -340,14 +339,12 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.rmom = c.take<double>(cols);
   l.gcoef = c.take<double>(cols);
   l.kkt = c.take<double>(cols);
-  l.coef = c.take<double>(cols);
   l.lam = c.take<double>(cols);
   l.taucol = c.take<double>(cols);
   l.fbuf = c.take<double>(cols * (size_t)p.Mh);
   l.nrm = c.take<double>((size_t)p.n);
   l.inv2s2 = c.take<double>((size_t)std::max(p.S, 1));
   l.flag = c.take<int>(cols);
-  l.moved = c.take<int>(cols);
   l.iters = c.take<int>(cols);
   l.iters_total = c.take<int>(cols);
   l.active = c.take<int>(1);
@@ -511,13 +508,14 @@ PathArrays path_arrays_of(const Layout& lay, const Plan& plan, int loss, bool gl
   pa.global_solve = global_solve;
   pa.nv = lay.nvg; pa.ylab = lay.ylab; pa.Q = lay.Qm; pa.band = lay.band;
   pa.cvec = lay.cvec; pa.lam = lay.lam; pa.tau = lay.taucol;
-  pa.ahat = lay.ahat; pa.abar = lay.abar; pa.bmat = lay.bmat; pa.zmat = lay.zmat;
+  pa.ahat = lay.ahat; pa.abar = lay.abar; pa.zmat = lay.zmat;
+  pa.QB = lay.A;             // the factorisation's buffer, free once Q is formed
   pa.anew = lay.anew; pa.estep = lay.estep; pa.ldl_l = lay.ldl_l; pa.ldl_d = lay.ldl_d;
   pa.vhat = lay.vhat;
   pa.uvec = lay.uvec; pa.partial = lay.partial; pa.beta = lay.beta; pa.bbar = lay.bbar;
   pa.fpart = lay.fpart; pa.zpart = lay.zpart;
-  pa.rmom = lay.rmom; pa.gcoef = lay.gcoef; pa.kkt = lay.kkt; pa.coef = lay.coef;
-  pa.moved = lay.moved; pa.flag = lay.flag;
+  pa.rmom = lay.rmom; pa.gcoef = lay.gcoef; pa.kkt = lay.kkt;
+  pa.flag = lay.flag;
   pa.iters = lay.iters; pa.iters_total = lay.iters_total; pa.active_count = lay.active;
   pa.cmap = lay.cmap; pa.nact = lay.nact;
   pa.cnv = lay.cnv;
@@ -1014,6 +1012,7 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
     BandWork bw = band_work_of(lay, Gb, N, nvg);
     bw.band_ready = side.band;
     if ((rc = band_reduce(s, bw)) != 0) return rc;
+    if ((rc = form_qb(s, lay.Qm, lay.band, N, Gb, lay.A)) != 0) return rc;
     KMP_HIP_TRY(hipStreamWaitEvent(side.st, side.band, 0));
     side.queued = true;
     if ((rc = path_stage_factor(side.st, pa, stage_kappa(0))) != 0) return rc;
@@ -1349,6 +1348,7 @@ int kmp_path_step(void* stream, int32_t loss, double delta, const double* K, int
   // a2 and the stage setup on this matrix
   BandWork bw = band_work_of(lay, 1, N, nvg.data());
   if ((rc = band_reduce(s, bw)) != 0) return rc;
+  if ((rc = form_qb(s, lay.Qm, lay.band, N, 1, lay.A)) != 0) return rc;
   PathArrays pa = path_arrays_of(lay, plan, loss, false);
   pa.G = 1;
   pa.nv_host = nvg.data();

@@ -172,6 +172,7 @@ struct PathArrays {
   const int32_t* cfold = nullptr;  // G*C held-out fold per column (shared-factor mode)
   const double* ylab = nullptr;  // G x N labels (0 at padding)
   const double* Q = nullptr;     // G x N x N
+  const double* QB = nullptr;    // G x N x N: Q B, the A operand of the first GEMM
   const double* band = nullptr;  // G x (kBand+1) x N, band[g][r*N + j] = B[j+r][j]
   const double* cvec = nullptr;  // G x N, Q' 1 over valid rows
   const double* lam = nullptr;   // G*C
@@ -179,10 +180,9 @@ struct PathArrays {
   // column-major per column N-vectors (column index gc = g*C + c)
   double* ahat = nullptr;
   double* abar = nullptr;
-  double* bmat = nullptr;   // T abar, operand of the first GEMM
   double* zmat = nullptr;
-  double* anew = nullptr;   // a+ of the current step
-  double* estep = nullptr;  // a+ - ahat
+  double* anew = nullptr;   // device-memory solve: forward results
+  double* estep = nullptr;  // device-memory solve: w, then x, then a+
   double* ldl_l = nullptr;  // kBand x N per column: tiles of the banded LDL' factor
   double* ldl_d = nullptr;  // N per column: 1/D
   double* vhat = nullptr;
@@ -196,8 +196,6 @@ struct PathArrays {
   double* rmom = nullptr;
   double* gcoef = nullptr;
   double* kkt = nullptr;
-  double* coef = nullptr;   // momentum coefficient of the current step
-  int* moved = nullptr;     // 1 when the column stepped in the current iteration
   int* flag = nullptr;      // 0 active, 1 converged, 2 max_iter, 3 non-finite
   int* iters = nullptr;     // per stage
   int* iters_total = nullptr;
@@ -222,6 +220,8 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
 // shrink the GEMMs (stage start, polls).
 int path_compact(hipStream_t s, const PathArrays& p);
 int group_ones_projection(hipStream_t s, const double* Q, const int* nv, int G, int N, double* cvec);
+// QB = Q B for G groups (Q, QB: N x N row-major each; band as in PathArrays).
+int form_qb(hipStream_t s, const double* Q, const double* band, int N, int G, double* QB);
 
 // Exact hinge recovery after the smoothing stages (exact.hip): the buffers
 // of one bandwidth batch (cols = G*C columns of N rows).

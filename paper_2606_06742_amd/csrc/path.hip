@@ -5,7 +5,8 @@
 // accelerated majorise-minimise method (Appendix A.1 update; Algorithm 1
 // inner loop; Appendix A.3 block inverse of H) is
 //
-//   f      = Q (B abar) + bbar                      (first path GEMM)
+//   f      = (Q B) abar + bbar                      (first path GEMM; Q B
+//                                                     formed once per factor)
 //   z      = psi(y, f) / n_v,  d0 = 1'z             (its epilogue)
 //   zhat   = Q' z                                   (second path GEMM)
 //   w      = zhat + 2 lambda abar                   (= Q'(z + 2 lambda alpha))
@@ -87,11 +88,9 @@ int path_init_columns(hipStream_t s, const PathArrays& p) {
   const size_t vec = cols * p.N * sizeof(double);
   KMP_HIP_TRY(hipMemsetAsync(p.ahat, 0, vec, s));
   KMP_HIP_TRY(hipMemsetAsync(p.abar, 0, vec, s));
-  KMP_HIP_TRY(hipMemsetAsync(p.bmat, 0, vec, s));
   KMP_HIP_TRY(hipMemsetAsync(p.beta, 0, cols * sizeof(double), s));
   KMP_HIP_TRY(hipMemsetAsync(p.bbar, 0, cols * sizeof(double), s));
   KMP_HIP_TRY(hipMemsetAsync(p.flag, 0, cols * sizeof(int), s));
-  KMP_HIP_TRY(hipMemsetAsync(p.moved, 0, cols * sizeof(int), s));
   KMP_HIP_TRY(hipMemsetAsync(p.iters, 0, cols * sizeof(int), s));
   KMP_HIP_TRY(hipMemsetAsync(p.iters_total, 0, cols * sizeof(int), s));
   return 0;
@@ -595,6 +594,62 @@ static int band_apply(hipStream_t s, const PathArrays& p, const double* x, doubl
   return 0;
 }
 
+// Q B, the A operand of the first path GEMM (f = (Q B) abar then needs no
+// band product per iteration): row i of Q B is B applied to row i of Q (B
+// symmetric, band[r][j] = B[j+r][j]). One workgroup per BT columns and QBR
+// rows of a group; each thread keeps the 2 BND + 1 band entries of its
+// column in registers and each row's piece of Q, with BND columns on either
+// side, passes through LDS.
+constexpr int QBR = 32;
+__global__ __launch_bounds__(BT) void form_qb_kernel(int N, const double* __restrict__ Q,
+                                                     const double* __restrict__ band,
+                                                     double* __restrict__ QB) {
+  __shared__ double qt[BT + 2 * BND];
+  const int g = blockIdx.z;
+  const int j0 = blockIdx.x * BT, j = j0 + threadIdx.x;
+  const int i0 = blockIdx.y * QBR, i1 = min(i0 + QBR, N);
+  const double* bg = band + (int64_t)g * (BND + 1) * N;
+  const double* Qg = Q + (int64_t)g * N * N;
+  double* Og = QB + (int64_t)g * N * N;
+  const bool cj = j < N;
+  // column j of B: B[j][j], B[j+r][j] = band[r][j], B[j-r][j] = band[r][j-r]
+  const double b0 = cj ? bg[j] : 0.0;
+  double bu[BND], bl[BND];
+#pragma unroll
+  for (int r = 1; r <= BND; ++r) {
+    bu[r - 1] = (cj && j + r < N) ? bg[(int64_t)r * N + j] : 0.0;
+    bl[r - 1] = (cj && j - r >= 0) ? bg[(int64_t)r * N + j - r] : 0.0;
+  }
+  for (int i = i0; i < i1; ++i) {
+    const double* qr = Qg + (int64_t)i * N;
+    for (int t = threadIdx.x; t < BT + 2 * BND; t += BT) {
+      const int c = j0 - BND + t;
+      qt[t] = (c >= 0 && c < N) ? qr[c] : 0.0;
+    }
+    __syncthreads();
+    if (cj) {
+      const int l = threadIdx.x + BND;
+      double y0 = b0 * qt[l], y1 = 0.0;
+#pragma unroll
+      for (int r = 1; r <= BND; ++r) {
+        y0 = fma(bu[r - 1], qt[l + r], y0);
+        y1 = fma(bl[r - 1], qt[l - r], y1);
+      }
+      Og[(int64_t)i * N + j] = y0 + y1;
+    }
+    __syncthreads();
+  }
+}
+
+int form_qb(hipStream_t s, const double* Q, const double* band, int N, int G, double* QB) {
+  if (N <= 0 || G <= 0) return 0;
+  hipLaunchKernelGGL(form_qb_kernel, dim3((unsigned)ceil_div(N, BT), (unsigned)ceil_div(N, QBR),
+                                          (unsigned)G),
+                     dim3(BT), 0, s, N, Q, band, QB);
+  KMP_LAUNCH_CHECK();
+  return 0;
+}
+
 // ------------------------------------------------------ per-stage factors
 // ldl_factor_kernel, one wavefront per column: the blockwise LDL' of
 // M = 2 lambda I + B/(n_v kappa) (stored as above). It reads the band,
@@ -758,7 +813,7 @@ __global__ __launch_bounds__(64 * FW) void ldl_factor_kernel(
 // stage_vectors_kernel, one wavefront per column, after the factors:
 // vhat = M^{-1} c/(n_v kappa), g = 1/(2 lambda c'vhat); restart the momentum
 // (r = 1, abar = ahat) and reactivate the columns that stopped in the
-// previous stage (u = B vhat and B abar follow in band_apply_kernel).
+// previous stage (u = B vhat follows in band_apply_kernel).
 template <bool GV>
 __global__ __launch_bounds__(256) void stage_vectors_kernel(
     int N, int C, int64_t cols, const int* __restrict__ nv, const double* __restrict__ cvec,
@@ -843,11 +898,10 @@ int path_stage_vectors(hipStream_t s, const PathArrays& p, double kappa) {
   KMP_LAUNCH_CHECK();
   int rc;
   if ((rc = band_apply(s, p, p.vhat, p.uvec)) != 0) return rc;
-  if ((rc = band_apply(s, p, p.ahat, p.bmat)) != 0) return rc;
   // the solve reads the factor (BND + 1 per element) and c, writes vhat;
-  // ahat to abar; then u = B vhat and B abar (read one vector, write one)
-  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 9.0); }),
-         over_groups(p, [&](double n) { return (4.0 * BND + 4.0 * (2 * BND + 1)) * n * p.C; }));
+  // ahat to abar; then u = B vhat (read one vector, write one)
+  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 7.0); }),
+         over_groups(p, [&](double n) { return (4.0 * BND + 2.0 * (2 * BND + 1)) * n * p.C; }));
   return 0;
 }
 
@@ -858,8 +912,9 @@ int path_stage_vectors(hipStream_t s, const PathArrays& p, double kappa) {
 //   the KKT test at the extrapolated point; x = M^{-1} w; the step
 //   Da = g (t - d0) vhat + x, a+ = abar - Da, e = a+ - ahat, and the restart
 //   test sum Da'e + Db (b+ - beta) > 0; the momentum r and its coefficient.
-// It writes a+ and e (anew, estep) and the column's scalars; momentum_kernel
-// then forms abar = a+ + coef e, ahat = a+ and B abar over all rows at once.
+// Then, with the momentum coefficient known, ahat = a+ and abar = a+ +
+// coef (a+ - ahat) (the first path GEMM multiplies Q B by abar, so no band
+// product follows), and the column's scalars.
 // Element loops load UL rows per lane before using them, so a lane keeps UL
 // loads of each stream in flight.
 constexpr int UL = 8;
@@ -868,22 +923,18 @@ template <bool GV>
 __global__ __launch_bounds__(256) void solve_step_kernel(
     int N, int C, int64_t cols, int RT, const int* __restrict__ nvv,
     const double* __restrict__ lamv, const double* __restrict__ zpart, int S2, int64_t sP,
-    double* __restrict__ ahat, const double* __restrict__ abar, const double* __restrict__ Vfac,
+    double* __restrict__ ahat, double* __restrict__ abar, const double* __restrict__ Vfac,
     const double* __restrict__ Dfac, const double* __restrict__ vhat,
     const double* __restrict__ uvec, const double* __restrict__ gcoef,
     const double* __restrict__ partial, double* __restrict__ beta, double* __restrict__ bbar,
     double* __restrict__ rmom, double* __restrict__ kktv, int* __restrict__ flag,
     int* __restrict__ iters, int* __restrict__ iters_total, double* __restrict__ anew,
-    double* __restrict__ estep, double* __restrict__ coefv, int* __restrict__ moved, double tol,
-    int max_iter, int restart) {
+    double* __restrict__ estep, double tol, int max_iter, int restart) {
   extern __shared__ double lds_dyn[];
   const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t gc = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
   if (gc >= cols) return;
-  if (flag[gc] != 0) {
-    if (lane == 0) moved[gc] = 0;
-    return;
-  }
+  if (flag[gc] != 0) return;
   // the solve's vector in LDS (GV: only the ring of the device-memory solve)
   double* xs = lds_dyn + (int64_t)wv * (GV ? RING : N);
   const int g = (int)(gc / C), c = (int)(gc % C);
@@ -932,13 +983,13 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
   const double bb = bbar[gc];
   // non-finite: tested on both terms, since fmax drops a NaN
   if (!(n2sum == n2sum) || !(d0 == d0) || !(kkt <= 1e300)) {
-    if (lane == 0) { flag[gc] = 3; kktv[gc] = kkt; moved[gc] = 0; }
+    if (lane == 0) { flag[gc] = 3; kktv[gc] = kkt; }
     return;
   }
   if (kkt <= tol) {                            // certified at the extrapolated point
 #pragma unroll 8
     for (int i = lane; i < N; i += 64) ahat[base + i] = abar[base + i];
-    if (lane == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; moved[gc] = 0; }
+    if (lane == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; }
     return;
   }
   // step and the restart test
@@ -948,9 +999,9 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
   const double bn = bb - db;
   const double bold = beta[gc];
   double rd = 0.0;
-  // x = M^{-1} w: in LDS (xs), or (GV) in this column's e vector, which the
-  // step below overwrites row by row after reading it
-  const double* xsrc = xs;
+  // x = M^{-1} w: in LDS (xs), or (GV) in this column's e vector; the step
+  // below overwrites it with a+ row by row after reading it
+  double* xsrc = xs;
   if constexpr (GV) {
     // w (stored in e by the pass above) is the solve's input, forward
     // results are kept in a+ (anew), and x overwrites w in e
@@ -983,10 +1034,8 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
       if (i < N) {
         const double da = fma(sa, vh[q], xv[q]);
         const double an = ab[q] - da;
-        const double e = an - ah[q];
-        rd = fma(da, e, rd);
-        anew[base + i] = an;
-        estep[base + i] = e;
+        rd = fma(da, an - ah[q], rd);
+        xsrc[i] = an;
       }
     }
   }
@@ -994,9 +1043,27 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
   const double r = rmom[gc];
   const double rn = (restart && rd > 0.0) ? 1.0 : 0.5 * (1.0 + sqrt(1.0 + 4.0 * r * r));
   const double coef = (rn - 1.0) / (0.5 * (1.0 + sqrt(1.0 + 4.0 * rn * rn)));
+  // momentum: ahat = a+, abar = a+ + coef (a+ - ahat), each lane on the rows
+  // whose a+ it wrote
+  for (int i0 = 0; i0 < N; i0 += 64 * UL) {
+    double ah[UL], an[UL];
+#pragma unroll
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      const int ii = (i < N) ? i : N - 1;
+      ah[q] = ahat[base + ii];
+      an[q] = xsrc[ii];
+    }
+#pragma unroll
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      if (i < N) {
+        ahat[base + i] = an[q];
+        abar[base + i] = fma(coef, an[q] - ah[q], an[q]);
+      }
+    }
+  }
   if (lane == 0) {
-    coefv[gc] = coef;
-    moved[gc] = 1;
     beta[gc] = bn;
     bbar[gc] = fma(coef, bn - bold, bn);
     rmom[gc] = rn;
@@ -1014,30 +1081,24 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
 // wavefront 0 alone runs the banded solve on the LDS vector:
 //   w = zhat + 2 lambda abar (LDS), t = u'w, ||w||, d0; KKT decision;
 //   x = M^{-1} w (wavefront 0); a+ = abar - g (t - d0) vhat - x,
-//   e = a+ - ahat, restart test, momentum coefficient.
-// a+ and e go to device memory for momentum_kernel, whose row tiles form
-// abar, ahat and B abar in parallel (the band product inside this kernel,
-// 256 threads per column, measured slower). Reductions are block sums in a
-// fixed order. LDS: N doubles.
+//   e = a+ - ahat, restart test, momentum coefficient; a+ is kept in LDS
+//   over x, then ahat = a+ and abar = a+ + coef e (no band product: the
+//   first path GEMM multiplies Q B by abar).
+// Reductions are block sums in a fixed order. LDS: N doubles.
 __global__ __launch_bounds__(256) void update_column_kernel(
     int N, int C, int RT, const int* __restrict__ nvv, const double* __restrict__ lamv,
     const double* __restrict__ zpart, int S2, int64_t sP, double* __restrict__ ahat,
-    const double* __restrict__ abar, double* __restrict__ anew, double* __restrict__ estep,
-    double* __restrict__ coefv, const double* __restrict__ Vfac, const double* __restrict__ Dfac,
+    double* __restrict__ abar, const double* __restrict__ Vfac, const double* __restrict__ Dfac,
     const double* __restrict__ vhat, const double* __restrict__ uvec,
     const double* __restrict__ gcoef, const double* __restrict__ partial,
     double* __restrict__ beta, double* __restrict__ bbar, double* __restrict__ rmom,
     double* __restrict__ kktv, int* __restrict__ flag, int* __restrict__ iters,
-    int* __restrict__ iters_total, int* __restrict__ moved, double tol, int max_iter,
-    int restart) {
+    int* __restrict__ iters_total, double tol, int max_iter, int restart) {
   extern __shared__ double lds_dyn[];
   __shared__ double red[PW];
   const int t = threadIdx.x, wv = t >> 6, lane = t & 63;
   const int64_t gc = blockIdx.x;
-  if (flag[gc] != 0) {                                  // uniform over the block
-    if (t == 0) moved[gc] = 0;
-    return;
-  }
+  if (flag[gc] != 0) return;                            // uniform over the block
   double* xs = lds_dyn;                                 // w, then x
   const int g = (int)(gc / C), c = (int)(gc % C);
   const int64_t base = gc * (int64_t)N;
@@ -1083,12 +1144,12 @@ __global__ __launch_bounds__(256) void update_column_kernel(
   const double bb = bbar[gc];
   // non-finite (uniform): tested on both terms, since fmax drops a NaN
   if (!(n2sum == n2sum) || !(d0 == d0) || !(kkt <= 1e300)) {
-    if (t == 0) { flag[gc] = 3; kktv[gc] = kkt; moved[gc] = 0; }
+    if (t == 0) { flag[gc] = 3; kktv[gc] = kkt; }
     return;
   }
   if (kkt <= tol) {                                     // certified at the extrapolated point
     for (int i = t; i < N; i += PB) ahat[base + i] = abar[base + i];
-    if (t == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; moved[gc] = 0; }
+    if (t == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; }
     return;
   }
   __syncthreads();                                      // w complete in LDS
@@ -1116,10 +1177,8 @@ __global__ __launch_bounds__(256) void update_column_kernel(
       if (i < N) {
         const double da = fma(sa, vh[q], xs[i]);
         const double an = ab[q] - da;
-        const double e = an - ah[q];
-        rd = fma(da, e, rd);
-        anew[base + i] = an;
-        estep[base + i] = e;
+        rd = fma(da, an - ah[q], rd);
+        xs[i] = an;                                     // a+ over x, row by row
       }
     }
   }
@@ -1127,9 +1186,26 @@ __global__ __launch_bounds__(256) void update_column_kernel(
   const double r = rmom[gc];
   const double rn = (restart && rd > 0.0) ? 1.0 : 0.5 * (1.0 + sqrt(1.0 + 4.0 * r * r));
   const double coef = (rn - 1.0) / (0.5 * (1.0 + sqrt(1.0 + 4.0 * rn * rn)));
+  // momentum: ahat = a+, abar = a+ + coef (a+ - ahat), each thread on the
+  // rows whose a+ it kept
+  for (int i0 = 0; i0 < N; i0 += PB * 4) {
+    double ah[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + t + PB * q;
+      ah[q] = ahat[base + ((i < N) ? i : N - 1)];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + t + PB * q;
+      if (i < N) {
+        const double an = xs[i];
+        ahat[base + i] = an;
+        abar[base + i] = fma(coef, an - ah[q], an);
+      }
+    }
+  }
   if (t == 0) {
-    coefv[gc] = coef;
-    moved[gc] = 1;
     beta[gc] = bn;
     bbar[gc] = fma(coef, bn - bold, bn);
     rmom[gc] = rn;
@@ -1141,33 +1217,6 @@ __global__ __launch_bounds__(256) void update_column_kernel(
   }
 }
 
-// abar = a+ + coef e, ahat = a+, bmat = B abar for the columns that moved;
-// one workgroup per (row tile, column) as in band_apply_kernel.
-__global__ __launch_bounds__(BT) void momentum_kernel(
-    int N, int C, const double* __restrict__ band, const int* __restrict__ moved,
-    const double* __restrict__ coefv, const double* __restrict__ anew,
-    const double* __restrict__ estep, double* __restrict__ ahat, double* __restrict__ abar,
-    double* __restrict__ bmat) {
-  __shared__ double xt[BT + 2 * BND];
-  const int64_t col = blockIdx.y;
-  if (moved[col] == 0) return;
-  const double coef = coefv[col];
-  const double* bg = band + (int64_t)(col / C) * (BND + 1) * N;
-  const int64_t base = col * N;
-  const int t0 = blockIdx.x * BT;
-  for (int j = threadIdx.x; j < BT + 2 * BND; j += BT) {
-    const int r = t0 - BND + j;
-    xt[j] = (r >= 0 && r < N) ? fma(coef, estep[base + r], anew[base + r]) : 0.0;
-  }
-  __syncthreads();
-  const int i = t0 + threadIdx.x;
-  if (i < N) {
-    ahat[base + i] = anew[base + i];
-    abar[base + i] = xt[threadIdx.x + BND];
-    bmat[base + i] = band_tile_row(bg, xt, N, i, threadIdx.x);
-  }
-}
-
 int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kappa, double tol,
                    int max_iter, int restart) {
   (void)kappa;
@@ -1175,12 +1224,12 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   const int RT = (int)ceil_div(p.N, 64);
   const int64_t sC = (int64_t)p.N * p.C;
   const int64_t sP = (int64_t)p.G * sC;
-  // f = Q (B abar) as split-K partials, then z = psi(y, f + bbar)/n_v with
+  // f = (Q B) abar as split-K partials, then z = psi(y, f + bbar)/n_v with
   // 64-row column sums
   GemmArgs g1;
   g1.M = p.N; g1.N = p.C; g1.K = p.N; g1.batch = p.G;
-  g1.A = p.Q; g1.lda = p.N; g1.sA = (int64_t)p.N * p.N;
-  g1.B = p.bmat; g1.ldb = p.N; g1.sB = sC;
+  g1.A = p.QB; g1.lda = p.N; g1.sA = (int64_t)p.N * p.N;
+  g1.B = p.abar; g1.ldb = p.N; g1.sB = sC;
   g1.ldc = p.N; g1.sC = sC;
   // output tiles that do work: 64-row tiles of the active columns
   int64_t work_tiles = 0;
@@ -1213,26 +1262,24 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   kc_end(KMP_KC_GEMM_ZHAT, s, gbytes, gflops);
   const int64_t cols = (int64_t)p.G * p.C;
   const bool gv = iteration_global_vec(p);
+  // per column element: S2 zhat parts, abar (twice), u, the factor tiles
+  // (BND each, forward and backward), 1/d, vhat and ahat (twice) read, ahat
+  // and abar written. Flops: BND multiply-adds per row in each triangular
+  // sweep, 16 elementwise.
+  const auto upd_bytes = over_active(p, [&](double n, double c) { return 8.0 * (S2 + 2.0 * BND + 9.0) * n * c; });
+  const auto upd_flops = over_active(p, [&](double n, double c) { return (4.0 * BND + 16.0) * n * c; });
   if (!gv) {
-    // one workgroup per column, momentum and B abar included
+    // one workgroup per column, the momentum step included
     const size_t lds_u = sizeof(double) * (size_t)p.N;
     KMP_HIP_TRY(hipFuncSetAttribute((const void*)update_column_kernel,
                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_u));
     kc_begin(KMP_KC_UPDATE, s);
     hipLaunchKernelGGL(update_column_kernel, dim3((unsigned)cols), dim3(PB), lds_u, s, p.N, p.C, RT,
-                       p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.anew, p.estep, p.coef,
-                       p.ldl_l, p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom,
-                       p.kkt, p.flag, p.iters, p.iters_total, p.moved, tol, max_iter, restart);
+                       p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l, p.ldl_d, p.vhat,
+                       p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt, p.flag, p.iters,
+                       p.iters_total, tol, max_iter, restart);
     KMP_LAUNCH_CHECK();
-    hipLaunchKernelGGL(momentum_kernel, dim3((unsigned)ceil_div(p.N, BT), (unsigned)cols), dim3(BT), 0,
-                       s, p.N, p.C, p.band, p.moved, p.coef, p.anew, p.estep, p.ahat, p.abar, p.bmat);
-    KMP_LAUNCH_CHECK();
-    // per column element: S2 zhat parts, abar (twice), u, the factor tiles
-    // (BND each, forward and backward), 1/d, vhat, ahat read; ahat, abar and
-    // B abar written (band read per row)
-    kc_end(KMP_KC_UPDATE, s,
-           over_active(p, [&](double n, double c) { return 8.0 * (S2 + 2.0 * BND + 9.0) * n * c; }),
-           over_active(p, [&](double n, double c) { return (8.0 * BND + 16.0) * n * c; }));
+    kc_end(KMP_KC_UPDATE, s, upd_bytes, upd_flops);
     return 0;
   }
   const int cw = path_waves(p, 0, gv);
@@ -1244,23 +1291,12 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   hipLaunchKernelGGL(solve_step_kernel<GVV>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, \
                      s, p.N, p.C, cols, RT, p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l, \
                      p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt,    \
-                     p.flag, p.iters, p.iters_total, p.anew, p.estep, p.coef, p.moved, tol,         \
-                     max_iter, restart)
+                     p.flag, p.iters, p.iters_total, p.anew, p.estep, tol, max_iter, restart)
   if (gv) KMP_SOLVE_STEP(true);
   else KMP_SOLVE_STEP(false);
 #undef KMP_SOLVE_STEP
   KMP_LAUNCH_CHECK();
-  hipLaunchKernelGGL(momentum_kernel, dim3((unsigned)ceil_div(p.N, BT), (unsigned)cols), dim3(BT), 0,
-                     s, p.N, p.C, p.band, p.moved, p.coef, p.anew, p.estep, p.ahat, p.abar, p.bmat);
-  KMP_LAUNCH_CHECK();
-  // per column element: the solve reads S2 zhat parts, abar (twice), u, the
-  // factor tiles (BND each, forward and backward), 1/d, vhat, ahat and
-  // writes a+ and e; the momentum pass reads a+ and e and writes ahat, abar
-  // and B abar. Flops: 2 BND multiply-adds per row for the two triangular
-  // sweeps, 2 BND + 1 for the band product, 14 elementwise.
-  kc_end(KMP_KC_UPDATE, s,
-         over_active(p, [&](double n, double c) { return 8.0 * (S2 + 2.0 * BND + 13.0) * n * c; }),
-         over_active(p, [&](double n, double c) { return (8.0 * BND + 16.0) * n * c; }));
+  kc_end(KMP_KC_UPDATE, s, upd_bytes, upd_flops);
   return 0;
 }
 
