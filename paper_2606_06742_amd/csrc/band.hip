@@ -586,7 +586,32 @@ __global__ __launch_bounds__(64 * XW) void panel_x_kernel(const double* __restri
   }
 }
 
-// S = T'M2 from the per-block parts of M2 (added in block order), W' =
+// M2 = V'X summed from panel_x's per-block parts in M2S fixed slices
+// (slice s: blocks floor(s nch / M2S) .. floor((s+1) nch / M2S) - 1, added
+// in order), so that each panel_ws workgroup adds M2S values per entry
+// instead of every block's part (at 32000 rows each of its 2500 workgroups
+// read all 2000 parts, 4 MB). Workgroup (s, g); m2s[(g M2S + s) 256 + t].
+constexpr int M2S = 64;
+__global__ __launch_bounds__(256) void m2_slices_kernel(const double* __restrict__ part, int NJ,
+                                                        int nch, double* __restrict__ m2s) {
+  const int sl = blockIdx.x, g = blockIdx.y, t = threadIdx.x;
+  const int q0 = (int)((int64_t)nch * sl / M2S), q1 = (int)((int64_t)nch * (sl + 1) / M2S);
+  const double* pp = part + (int64_t)g * NJ * 256 + t;
+  double s0 = 0.0, s1 = 0.0;
+  for (int q = q0; q < q1; q += 8) {
+    double v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = (q + u < q1) ? pp[(int64_t)(q + u) * 256] : 0.0;
+#pragma unroll
+    for (int u = 0; u < 8; u += 2) {
+      s0 += v[u];
+      s1 += v[u + 1];
+    }
+  }
+  m2s[((int64_t)g * M2S + sl) * 256 + t] = s0 + s1;
+}
+
+// S = T'M2 from the slices of M2 (added in slice order), W' =
 // X' - 1/2 S'V' for the workgroup's 64 columns (X' read from xq, W' into
 // rows BB .. 2BB-1 of the panel buffer), then the two-sided update of the
 // first block column of A22 for the workgroup's 64 rows:
@@ -597,7 +622,7 @@ __global__ __launch_bounds__(64 * XW) void panel_x_kernel(const double* __restri
 // 0 .. 15 formed again by every workgroup, so that none reads what another
 // one writes. One workgroup per 64 rows and matrix.
 __global__ __launch_bounds__(256) void panel_ws_kernel(double* __restrict__ A, int N, int m0,
-                                                       const double* __restrict__ part, int NJ,
+                                                       const double* __restrict__ m2s,
                                                        const double* __restrict__ tmat,
                                                        const double* __restrict__ xq, int64_t sX,
                                                        double* __restrict__ panel) {
@@ -636,10 +661,10 @@ __global__ __launch_bounds__(256) void panel_ws_kernel(double* __restrict__ A, i
   for (int u = 0; u < 4; ++u) xj[u] = okj ? Xg[(int64_t)(r4 + u) * N + j] : 0.0;
   const double x0 = Xg[(int64_t)r0 * N + c0];
   {
-    const double* pp = part + (int64_t)g * NJ * 256 + t;
+    const double* pp = m2s + (int64_t)g * M2S * 256 + t;
     double s = 0.0;
 #pragma unroll 8
-    for (int q = 0; q < nch; ++q) s += pp[(int64_t)q * 256];
+    for (int q = 0; q < M2S; ++q) s += pp[q * 256];
     M2s[t >> 4][t & 15] = s;
   }
   __syncthreads();
@@ -946,8 +971,10 @@ static double over_groups(const BandWork& wk, F f) {
   return a;
 }
 
+// chunk partials of the Gram products, then the slices of M2
+static size_t band_chunk_doubles(int G, int N) { return (size_t)G * ceil_div(N, TSK) * 64 * 64; }
 size_t band_part_doubles(int G, int N) {
-  return (size_t)G * ceil_div(N, TSK) * 64 * 64;
+  return band_chunk_doubles(G, N) + (size_t)G * M2S * 256;
 }
 
 int wy_blocks(int N) { return N > BB ? (int)ceil_div(N - BB, kWyBlock) : 0; }
@@ -1208,6 +1235,7 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
   const int64_t sP = (int64_t)3 * BB * N;
   KMP_HIP_TRY(hipMemsetAsync(wk.tau, 0, sizeof(double) * (size_t)G * N, s));
   double* const pbuf[2] = {wk.panel, wk.panel2};
+  double* const m2s = wk.part + band_chunk_doubles(G, N);   // the slices of M2
   const auto tiles_of = [](int m) { return (int)ceil_div(m, 64); };
   const auto dual_grid = [&](int m, int tpw) {
     const int64_t t = tiles_of(m);
@@ -1307,9 +1335,12 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     const double* P1 = pb + m0;
     const double* P2 = pb + (int64_t)BB * N + m0;
     const unsigned tl = (unsigned)tiles_of(mrow);
+    hipLaunchKernelGGL(m2_slices_kernel, dim3((unsigned)M2S, (unsigned)G), dim3(256), 0, s,
+                       (const double*)wk.part, NJ, mrow / BB, m2s);
+    KMP_LAUNCH_CHECK();
     hipLaunchKernelGGL(panel_ws_kernel, dim3(tl, (unsigned)G), dim3(256), 0, s, wk.A, N, m0,
-                       (const double*)wk.part, NJ, (const double*)wk.tmat,
-                       (const double*)wk.ybuf, sXq, pb);
+                       (const double*)m2s, (const double*)wk.tmat, (const double*)wk.ybuf, sXq,
+                       pb);
     KMP_LAUNCH_CHECK();
     if (next) {
       if ((rc = factor_panel(m0, pbuf[((p / BB) & 1) ^ 1], true, pb)) != 0) return rc;
