@@ -944,11 +944,11 @@ __global__ void clear_reflector_rows_kernel(double* __restrict__ A, int N, int64
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= total) return;
   const int64_t rows = N - BB;
-  constexpr int W = 2 * kWyBlock + BB;
+  constexpr int W = kWyQuad * kWyBlock + BB;
   const int g = (int)(idx / (rows * W));
   const int64_t e = idx % (rows * W);
   const int r = (int)(e / W), q = (int)(e % W);
-  const int c = r - 2 * kWyBlock + q;    // c in [r - 128, r + BB)
+  const int c = r - kWyQuad * kWyBlock + q;    // c in [r - 256, r + BB)
   if (c < 0) return;
   A[(int64_t)g * N * N + (int64_t)r * N + c] = 0.0;
 }
@@ -985,33 +985,36 @@ size_t wy_all_doubles(int G, int N) {
 
 size_t band_work_doubles(int G, int N) {
   return (size_t)G * (6 * (size_t)BB * N + 2 * (size_t)kWyBlock * kWyBlock +
-                      3 * (size_t)kWyBlock * N) + band_part_doubles(G, N) +
-         3 * wy_all_doubles(G, N) + (size_t)kMaxSplitK * G * 2 * kWyBlock * N;
+                      (1 + kWyQuad) * (size_t)kWyBlock * N) + band_part_doubles(G, N) +
+         (2 + (kWyQuad - 1)) * wy_all_doubles(G, N) +
+         (size_t)kMaxSplitK * G * kWyQuad * kWyBlock * N;
 }
 
 // Gram matrices of all blocks of kWyBlock reflector rows at once, on the
 // matrix cores: workgroup (b, g, 0) forms G[a][c] = sum_k V[a][k] V[c][k]
 // for the reflectors q = 64 b .. q + kb - 1 of matrix g (row q + a of A
 // holds v_{q+a} from column q + a + BB, zeros before it, so the sum runs
-// over the columns q + BB .. N-1); workgroup (b, g, 1) the cross products
-// V_b V_{b+1}' with the next block (into cross_all). Wave w computes the
+// over the columns q + BB .. N-1); workgroup (b, g, d), d = 1 .. 3, the
+// cross products V_b V_{b+d}' with the block d further on (into cross_all +
+// (d-1) sD). Wave w computes the
 // 32 x 32 quadrant (32 (w&1), 32 (w>>1)) as 2 x 2 MFMA blocks over
 // 16-column slices staged in LDS.
 __global__ __launch_bounds__(256) void wy_gram_kernel(const double* __restrict__ A, int N, int nref,
                                                        double* __restrict__ gram_all,
-                                                       double* __restrict__ cross_all) {
+                                                       double* __restrict__ cross_all, int64_t sD) {
   __shared__ double Vs[kWyBlock][BB + 1];
   __shared__ double Ws[kWyBlock][BB + 1];
   const int b = blockIdx.x, g = blockIdx.y, G = gridDim.y;
-  const bool cross = blockIdx.z == 1;
+  const int dz = blockIdx.z;
+  const bool cross = dz > 0;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int q = kWyBlock * b;
   const int kb = min(kWyBlock, nref - q);
-  const int kc = cross ? min(kWyBlock, nref - q - kWyBlock) : kb;   // rows of the right factor
+  const int kc = cross ? min(kWyBlock, nref - q - dz * kWyBlock) : kb;   // rows of the right factor
   if (kc <= 0) return;
   const int m = N - q - BB;
   const double* Vq = A + (int64_t)g * N * N + (int64_t)q * N + q + BB;
-  const double* Wq = cross ? Vq + (int64_t)kWyBlock * N : Vq;
+  const double* Wq = Vq + (int64_t)dz * kWyBlock * N;
   double (*Rs)[BB + 1] = cross ? Ws : Vs;
   const int wi = 32 * (w & 1), wj = 32 * (w >> 1);
   const int li = lane & 15, lk = lane >> 4;
@@ -1040,7 +1043,7 @@ __global__ __launch_bounds__(256) void wy_gram_kernel(const double* __restrict__
       acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
     }
   }
-  double* Gg = (cross ? cross_all : gram_all) + ((int64_t)b * G + g) * kWyBlock * kWyBlock;
+  double* Gg = (cross ? cross_all + (dz - 1) * sD : gram_all) + ((int64_t)b * G + g) * kWyBlock * kWyBlock;
 #pragma unroll
   for (int x = 0; x < 2; ++x)
 #pragma unroll
@@ -1223,6 +1226,113 @@ __global__ __launch_bounds__(256) void wy_apply_pair_kernel(
   put(acc, nullptr, 0);
 }
 
+// Y for four consecutive WY blocks a, b, c, d applied in one pass (d
+// first), the same recurrence one block further: with X = [X_a; X_b; X_c;
+// X_d] = [V_a; ..; V_d] Q22 as S split-K parts (rows 0..63: X_a, .., 192..255:
+// X_d) and G_xy = V_x V_y',
+//   Y_d = T_d X_d,  Y_c = T_c (X_c - G_cd Y_d),
+//   Y_b = T_b (X_b - G_bc Y_c - G_bd Y_d),
+//   Y_a = T_a (X_a - G_ab Y_b - G_ac Y_c - G_ad Y_d),
+// since V_x applied to Q22 after the later blocks' reflectors is X_x minus
+// the G_xy Y_y of those blocks. Then Q22 -= [V_a; ..; V_d]' [Y_a; ..; Y_d],
+// one rank-256 update. tq: T of block a (those of b, c, d at + sW, 2 sW,
+// 3 sW); c1, c2, c3: the cross products at distance 1, 2, 3 of block a
+// (of the following blocks at + sW, ..). Workgroup (32-column tile, g)
+// keeps the four X tiles and one 64 x 64 factor at a time in LDS; wave w
+// forms rows 16 w .. 16 w + 15 of each product on the matrix cores.
+__global__ __launch_bounds__(256) void wy_apply_quad_kernel(
+    const double* __restrict__ tq, const double* __restrict__ c1, const double* __restrict__ c2,
+    const double* __restrict__ c3, int64_t sW, const double* __restrict__ xpart, int S, int64_t sP,
+    int64_t sX, int64_t ldx, int m, double* __restrict__ Y, int64_t ldy, int64_t sY) {
+  constexpr int W = kWyBlock, CT = 32;
+  __shared__ double Fs[W][W + 1];
+  __shared__ double Xs[kWyQuad][W][CT + 1];
+  const int g = blockIdx.y, j0 = CT * blockIdx.x, t = threadIdx.x;
+  const int w = t >> 6, lane = t & 63, li = lane & 15, lk = lane >> 4;
+  const int64_t fo = (int64_t)g * W * W;
+  const auto load_f = [&](const double* F) {
+#pragma unroll
+    for (int u = 0; u < W * W / 256; ++u) {
+      const int e = t + 256 * u;
+      Fs[e / W][e % W] = F[fo + e];
+    }
+  };
+  {
+    // thread t stages row a = t/4, columns 8 (t%4) .. +7 of each tile; the
+    // parts of one tile are loaded before they are added
+    const int a = t >> 2, jq = 8 * (t & 3);
+    const double* Xg = xpart + (int64_t)g * sX;
+#pragma unroll 1
+    for (int k = 0; k < kWyQuad; ++k) {
+      double v[kMaxSplitK][8];
+#pragma unroll
+      for (int q = 0; q < kMaxSplitK; ++q)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int j = j0 + jq + u;
+          const bool ok = q < S && j < m;
+          v[q][u] = ok ? Xg[(int64_t)q * sP + (int64_t)(k * W + a) * ldx + j] : 0.0;
+        }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        double sum = v[0][u];
+#pragma unroll
+        for (int q = 1; q < kMaxSplitK; ++q) sum += v[q][u];   // zero past S: the same sum
+        Xs[k][a][jq + u] = sum;
+      }
+    }
+  }
+  __syncthreads();                                    // the four tiles staged
+  // acc <- acc +/- F rows 16w.. times X (64 x 32)
+  const auto mm = [&](double sgn, double (*X)[CT + 1], xdbl4 (&acc)[2]) {
+#pragma unroll
+    for (int k = 0; k < W; k += 4) {
+      const double f = sgn * Fs[16 * w + li][k + lk];
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj)
+        acc[bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(f, X[k + lk][16 * bj + li], acc[bj], 0, 0, 0);
+    }
+  };
+  double* Yg = Y + (int64_t)g * sY;
+  // the wave's rows of acc into X (LDS, when given) and into rows row0 + .. of Y
+  const auto put = [&](const xdbl4 (&acc)[2], double (*X)[CT + 1], int row0) {
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int a = 16 * w + 4 * r + lk, j = 16 * bj + li;
+        if (X) X[a][j] = acc[bj][r];
+        if (row0 >= 0 && j0 + j < m) Yg[(int64_t)(row0 + a) * ldy + j0 + j] = acc[bj][r];
+      }
+  };
+  const auto own = [&](double (*X)[CT + 1], xdbl4 (&acc)[2]) {
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[bj][r] = X[16 * w + 4 * r + lk][16 * bj + li];
+  };
+  xdbl4 acc[2];
+  // block k: X_k -= sum over the later blocks l of G_kl Y_l, then Y_k = T_k X_k
+  for (int k = kWyQuad - 1; k >= 0; --k) {
+    own(Xs[k], acc);
+    for (int l = k + 1; l < kWyQuad; ++l) {
+      const double* cd = (l - k == 1) ? c1 : (l - k == 2) ? c2 : c3;
+      __syncthreads();                                // the previous factor read by all
+      load_f(cd + (int64_t)k * sW);
+      __syncthreads();
+      mm(-1.0, Xs[l], acc);
+    }
+    __syncthreads();                                  // every read of Fs and of X_k done
+    put(acc, Xs[k], -1);
+    load_f(tq + (int64_t)k * sW);
+    __syncthreads();
+    acc[0] = acc[1] = xdbl4{0.0, 0.0, 0.0, 0.0};
+    mm(1.0, Xs[k], acc);
+    __syncthreads();                                  // X_k read by all before Y_k replaces it
+    put(acc, Xs[k], k * W);
+  }
+}
+
 int band_reduce(hipStream_t s, const BandWork& wk) {
   const int G = wk.G, N = wk.N;
   if (G <= 0) return 0;
@@ -1371,7 +1481,7 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
                        wk.A, N, tot, wk.band);
     KMP_LAUNCH_CHECK();
     if (wk.band_ready) KMP_HIP_TRY(hipEventRecord(wk.band_ready, s));
-    const int64_t tz = (int64_t)G * (N - BB) * (2 * kWyBlock + BB);
+    const int64_t tz = (int64_t)G * (N - BB) * (kWyQuad * kWyBlock + BB);
     hipLaunchKernelGGL(clear_reflector_rows_kernel, dim3((unsigned)ceil_div(tz, 256)), dim3(256), 0,
                        s, wk.A, N, tz);
     KMP_LAUNCH_CHECK();
@@ -1384,33 +1494,40 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
   // blocks of kWyBlock rows: Q[q+BB:, q+BB:] -= V' (T (V Q[q+BB:, q+BB:])).
   // The Grams, cross products and T factors of all blocks depend on the
   // reflectors only and are formed first, two launches for all blocks.
-  // The last (partial) block goes alone, then the others in pairs, one
-  // pass over Q22 per pair (see wy_apply_pair_kernel), a single block at
-  // the bottom if one is left.
+  // The last (partial) block goes alone, then the others in fours, one
+  // pass over Q22 and one rank-256 update per four blocks (see
+  // wy_apply_quad_kernel), then a pair and a single block at the bottom if
+  // they are left.
   const int nref = N - BB;
   const int nblk = wy_blocks(N);
   kc_begin(KMP_KC_QFORM, s);
-  hipLaunchKernelGGL(wy_gram_kernel, dim3((unsigned)nblk, (unsigned)G, 2u), dim3(256), 0, s, wk.A, N,
-                     nref, wk.gram_all, wk.cross_all);
+  const int64_t sD = (int64_t)wy_all_doubles(G, N);        // between the cross-product distances
+  hipLaunchKernelGGL(wy_gram_kernel, dim3((unsigned)nblk, (unsigned)G, (unsigned)kWyQuad), dim3(256), 0,
+                     s, wk.A, N, nref, wk.gram_all, wk.cross_all, sD);
   KMP_LAUNCH_CHECK();
   if ((rc = wy_form_t_blocks(s, wk.gram_all, wk.tau, wk.tmat_all, G, N, nref, nblk)) != 0) return rc;
-  // reflector rows of each block read for its Gram and, with the next
-  // block's, for the cross products; 64 x 64 products over m columns
+  // reflector rows of each block read for its Gram and, with those of the
+  // three next blocks, for the cross products; 64 x 64 products over m
+  // columns
   kc_end(KMP_KC_QFORM, s, over_groups(wk, [&](double n) {
            double a = 0.0;
-           for (int b = 0; b < nblk; ++b) a += 3.0 * 8.0 * kWyBlock * std::max(0.0, n - kWyBlock * b - BB);
+           for (int b = 0; b < nblk; ++b)
+             a += (2.0 * kWyQuad - 1.0) * 8.0 * kWyBlock * std::max(0.0, n - kWyBlock * b - BB);
            return a; }),
          over_groups(wk, [&](double n) {
            double a = 0.0;
            for (int b = 0; b < nblk; ++b)
-             a += 2.0 * 2.0 * kWyBlock * kWyBlock * std::max(0.0, n - kWyBlock * b - BB);
+             a += kWyQuad * 2.0 * kWyBlock * kWyBlock * std::max(0.0, n - kWyBlock * b - BB);
            return a; }));
   const int64_t sW = (int64_t)G * kWyBlock * kWyBlock;      // between blocks in tmat_all, cross_all
-  const int64_t sY = (int64_t)2 * kWyBlock * N;             // per matrix in ybuf and xpart
+  const int64_t sY = (int64_t)kWyQuad * kWyBlock * N;       // per matrix in ybuf and xpart
   const int64_t sXP = (int64_t)G * sY;                      // between split-K parts of xpart
-  const auto step = [&](int b, bool pair) -> int {
+  // nb consecutive blocks from block b in one pass: 4 (full blocks), 2, or
+  // 1 (the partial last block, or a single full one)
+  const auto step = [&](int b, int nb) -> int {
+    const bool pair = nb == 2, quad = nb == kWyQuad;
     const int q = kWyBlock * b;
-    const int kb = pair ? 2 * kWyBlock : std::min(kWyBlock, nref - q);
+    const int kb = nb > 1 ? nb * kWyBlock : std::min(kWyBlock, nref - q);
     const int m = N - q - BB;
     kc_begin(KMP_KC_QFORM, s);
     // X = V Q[q+BB:, q+BB:] (kb x m) as split-K parts, in the transposed
@@ -1424,7 +1541,13 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
     const int S1 = splitk_parts(h1);
     if ((rc = gemm_partial(s, h1, false, S1, wk.xpart, sXP, nullptr, nullptr)) != 0) return rc;
     const double* tq = wk.tmat_all + (int64_t)b * sW;
-    if (pair) {
+    if (quad) {
+      const double* c1 = wk.cross_all + (int64_t)b * sW;
+      hipLaunchKernelGGL(wy_apply_quad_kernel, dim3((unsigned)ceil_div(m, 32), (unsigned)G),
+                         dim3(256), 0, s, tq, c1, c1 + sD, c1 + 2 * sD, sW,
+                         (const double*)wk.xpart, S1, sXP, sY, (int64_t)N, m, wk.ybuf, (int64_t)N,
+                         sY);
+    } else if (pair) {
       hipLaunchKernelGGL(wy_apply_pair_kernel, dim3((unsigned)ceil_div(m, 32), (unsigned)G), dim3(256),
                          0, s, tq, tq + sW, (const double*)(wk.cross_all + (int64_t)b * sW),
                          (const double*)wk.xpart, S1, sXP, sY, (int64_t)N, m, wk.ybuf, (int64_t)N,
@@ -1435,12 +1558,17 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
                          m, wk.ybuf, (int64_t)N, sY);
     }
     KMP_LAUNCH_CHECK();
-    // Q[q+BB:, q+BB:] -= V' Y  (K = kb: 128 for a pair, 64 for a full
-    // single block, else the generic product)
+    // Q[q+BB:, q+BB:] -= V' Y  (K = kb: 256 for four blocks, 128 for a
+    // pair, 64 for a full single block, else the generic product)
     const dim3 ug((unsigned)ceil_div(m, 64), (unsigned)ceil_div(m, 64), (unsigned)G);
     double* Q22 = wk.Q + (int64_t)(q + BB) * N + q + BB;
     const double* P1 = wk.A + (int64_t)q * N + q + BB;
-    if (kb == 2 * kWyBlock) {
+    if (kb == kWyQuad * kWyBlock) {
+      hipLaunchKernelGGL((rank_update_kernel<8, false>), ug, dim3(256), 0, s, Q22, (int64_t)N,
+                         (int64_t)N * N, m, P1, (int64_t)N, (int64_t)N * N,
+                         (const double*)wk.ybuf, (int64_t)N, sY);
+      KMP_LAUNCH_CHECK();
+    } else if (kb == 2 * kWyBlock) {
       hipLaunchKernelGGL((rank_update_kernel<4, false>), ug, dim3(256), 0, s, Q22, (int64_t)N,
                          (int64_t)N * N, m, P1, (int64_t)N, (int64_t)N * N,
                          (const double*)wk.ybuf, (int64_t)N, sY);
@@ -1464,18 +1592,23 @@ int band_reduce(hipStream_t s, const BandWork& wk) {
              const double mm = std::max(0.0, n - q - BB); return 24.0 * mm * mm; }),
            over_groups(wk, [&](double n) {
              const double mm = std::max(0.0, n - q - BB);
-             const double tk = pair ? 3.0 * kWyBlock * kWyBlock : (double)kb * kb;
+             const double tk = quad ? 10.0 * kWyBlock * kWyBlock
+                                    : pair ? 3.0 * kWyBlock * kWyBlock : (double)kb * kb;
              return 4.0 * kb * mm * mm + 2.0 * tk * mm; }));
     return 0;
   };
   int b = nblk - 1;
   if (nref % kWyBlock != 0) {
-    if ((rc = step(b, false)) != 0) return rc;
+    if ((rc = step(b, 1)) != 0) return rc;
     --b;
   }
-  for (; b >= 1; b -= 2)
-    if ((rc = step(b - 1, true)) != 0) return rc;
-  if (b == 0 && (rc = step(0, false)) != 0) return rc;
+  for (; b >= kWyQuad - 1; b -= kWyQuad)
+    if ((rc = step(b - kWyQuad + 1, kWyQuad)) != 0) return rc;
+  if (b >= 1) {
+    if ((rc = step(b - 1, 2)) != 0) return rc;
+    b -= 2;
+  }
+  if (b == 0 && (rc = step(0, 1)) != 0) return rc;
   return 0;
 }
 

@@ -313,15 +313,15 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.tmat = c.take<double>(G * kWyBlock * kWyBlock);
   l.gram = c.take<double>(G * kWyBlock * kWyBlock);
   l.xbuf = c.take<double>(G * kWyBlock * N);
-  l.ybuf = c.take<double>(G * 2 * kWyBlock * N);
+  l.ybuf = c.take<double>(G * kWyQuad * kWyBlock * N);
   l.spart = c.take<double>(G * (size_t)tridiag_parts((int)N));
   l.pnext = c.take<double>(G * N);
   l.band = c.take<double>(G * (kBand + 1) * N);
   l.bpart = c.take<double>(band_part_doubles((int)G, (int)N));
   l.gram_all = c.take<double>(wy_all_doubles((int)G, (int)N));
   l.tmat_all = c.take<double>(wy_all_doubles((int)G, (int)N));
-  l.cross_all = c.take<double>(wy_all_doubles((int)G, (int)N));
-  l.xpart = c.take<double>((size_t)kMaxSplitK * G * 2 * kWyBlock * N);
+  l.cross_all = c.take<double>((kWyQuad - 1) * wy_all_doubles((int)G, (int)N));
+  l.xpart = c.take<double>((size_t)kMaxSplitK * G * kWyQuad * kWyBlock * N);
   l.ahat = c.take<double>(cols * N);
   l.abar = c.take<double>(cols * N);
   l.zmat = c.take<double>(cols * N);
@@ -714,11 +714,11 @@ int kmp_band_reduce(void* stream, double* A, int32_t G, int32_t N, double* Qout,
   w.tmat = q; q += (size_t)G * kWyBlock * kWyBlock;
   w.gram = q; q += (size_t)G * kWyBlock * kWyBlock;
   w.xbuf = q; q += (size_t)G * kWyBlock * N;
-  w.ybuf = q; q += (size_t)G * 2 * kWyBlock * N;
+  w.ybuf = q; q += (size_t)G * kWyQuad * kWyBlock * N;
   w.gram_all = q; q += wy_all_doubles(G, N);
   w.tmat_all = q; q += wy_all_doubles(G, N);
-  w.cross_all = q; q += wy_all_doubles(G, N);
-  w.xpart = q; q += (size_t)kMaxSplitK * G * 2 * kWyBlock * N;
+  w.cross_all = q; q += (kWyQuad - 1) * wy_all_doubles(G, N);
+  w.xpart = q; q += (size_t)kMaxSplitK * G * kWyQuad * kWyBlock * N;
   w.part = q;
   int rc = band_reduce(s, w);
   KMP_HIP_TRY(hipFreeAsync(scratch, s));

@@ -91,6 +91,7 @@ constexpr int kMaxOrder = 32768;
 // (every kernel offset r*N + c still below 2^31).
 constexpr int kMaxSharedOrder = 40960;
 constexpr int kWyBlock = 64;   // reflectors per compact-WY block when forming Q
+constexpr int kWyQuad = 4;     // compact-WY blocks applied to Q in one pass
 
 // Reduction of G symmetric N x N matrices (row-major, packed, destroyed) to
 // A_g = Q_g B_g Q_g' with B_g banded; band[g][r*N + j] = B_g[j+r][j], r <= kBand.
@@ -105,12 +106,12 @@ struct BandWork {
   double* tmat = nullptr;   // G x 64 x 64
   double* gram = nullptr;   // G x 64 x 64
   double* xbuf = nullptr;   // G x 64 x N
-  double* ybuf = nullptr;   // G x 128 x N
+  double* ybuf = nullptr;   // G x 256 x N
   double* part = nullptr;   // band_part_doubles(G, N): chunk partials of the Gram products
   double* gram_all = nullptr;  // wy_blocks(N) x G x 64 x 64: Grams of the WY blocks of Q
   double* tmat_all = nullptr;  // same shape: their T factors
-  double* cross_all = nullptr; // same shape: V_b V_{b+1}' of consecutive blocks
-  double* xpart = nullptr;     // kMaxSplitK x G x 128 x N: split-K parts of V Q in the Q accumulation
+  double* cross_all = nullptr; // 3 x that shape: V_b V_{b+d}' at distance d = 1, 2, 3
+  double* xpart = nullptr;     // kMaxSplitK x G x 256 x N: split-K parts of V Q in the Q accumulation
   const int* nv_host = nullptr;  // G valid orders (host), for the work counters; N if null
   hipEvent_t band_ready = nullptr;  // if set, recorded once the band is written
 };
