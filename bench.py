@@ -222,6 +222,26 @@ def regimes(v):
     return out
 
 
+def sigma_batch_that_fits(km, w, inp, args, dev):
+    """The largest number of bandwidths per batch whose workspace fits in
+    90 % of the device memory free now (all of them when that fits)."""
+    import torch
+    free = torch.cuda.mem_get_info(dev)[0]
+    S = len(inp["sigmas"])
+    spec = km.kmp_default_spec(w.loss)
+    if args.refit:
+        spec.flags |= km.KMP_FLAG_REFIT
+    if args.shared:
+        spec.flags |= km.KMP_FLAG_SHARED_FACTOR
+    n, d = inp["X"].shape
+    Q = len(inp["taus"]) if w.loss == "check" else 1
+    for sb in range(S, 0, -1):
+        b = km.kmp_workspace_bytes(spec, n, d, len(inp["lambdas"]), inp["fold_id"], w.V, S, Q, sb)
+        if 0 < b <= 0.9 * free:
+            return sb
+    return 1
+
+
 def kernel_table(kt, steps):
     return {k: {"est_ms_per_step": v[0] / v[1] * v[2] / steps,
                 "launches_per_step": v[2] / steps,
@@ -295,9 +315,10 @@ def main():
         inp["sigmas"] = inp["sigmas"][args.sigma_index:args.sigma_index + 1]
     dev = torch.device("cuda:0")
     log(f"inputs of {w.name} ready")
+    sb = sigma_batch_that_fits(km, w, inp, args, dev)
     runner = km.PathRunner(inp["X"], inp["y"], w.loss, inp["sigmas"], inp["lambdas"],
                            inp["fold_id"], w.V, taus=inp["taus"] if w.loss == "check" else None,
-                           device=dev, refit=args.refit, shared=args.shared)
+                           device=dev, refit=args.refit, shared=args.shared, sigma_batch=sb)
     # every kernel class is timed live in the timed region, one launch in
     # TIMING_EVERY bracketed by HIP events on the library's stream
     runner.set_kernel_timing(km.KERNEL_CLASSES, every=args.timing_every)
@@ -328,7 +349,7 @@ def main():
         "config": {"workload": f"{w.name}: {w.description}; n={w.n}, d={w.d}, {shape} = "
                                f"{runner.cells} cells, loss={w.loss}, {mode}",
                    "cells": runner.cells, "n": w.n, "d": w.d, "folds": 1 if args.refit else w.V,
-                   "lambdas": w.L, "sigmas": nsig, "mode": mode},
+                   "lambdas": w.L, "sigmas": nsig, "sigma_batch": sb, "mode": mode},
         "phases_ms_per_step": {k: v / args.steps for k, v in phases.items()},
         "path_fits_per_s": runner.cells / (1e-3 * (phases["precompute_ms"] + phases["path_ms"]
                                                    + phases["finalize_ms"]) / args.steps),
