@@ -316,8 +316,10 @@ __device__ __forceinline__ void grid_vec_sync() {
 // with the same value and read back by them in the backward sweep), and the
 // solution goes to wout(r, x_r, lead), called by every lane, the lead lane
 // flagged. The blocks that the other lanes need are staged in an LDS ring of
-// two BND-double slots (block I in slot I & 1). No lane reads device memory
-// written by another lane of the same launch. As in band_solve, the sweeps
+// two BND-double slots (block I in slot I & 1). Within the solve a lane
+// reads back from device memory only what it wrote itself (the input is
+// written before the solve, with a fence when by the same launch). As in
+// band_solve, the sweeps
 // run whole groups of SPFG blocks through branch-free steps (prefetch index
 // clamped, the first block as a select, stores unconditional) and the
 // remaining blocks after them, and every prefetched value is a plain load
@@ -530,8 +532,9 @@ static CuShape cu_shape() {
 // (solve_step_kernel: four columns per workgroup, over 256 registers, one
 // workgroup per compute unit) keeps four. When more columns are active than
 // the LDS form holds at once, the device-memory form needs fewer rounds and
-// is taken (at C3, above 512 active columns: 623 against 717 us per
-// iteration; below, the LDS form's shorter steps win: 280 against 380 us).
+// is taken (10 groups of order 9024: above 512 active columns 623 against
+// 717 us per iteration; below, the LDS form's shorter steps win: 280
+// against 380 us).
 // The counts are the host's copy of the last poll, which only overestimates
 // the active columns.
 static bool iteration_global_vec(const PathArrays& p) {
