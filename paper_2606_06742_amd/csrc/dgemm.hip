@@ -524,6 +524,134 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
       }
 }
 
+// The same split-K partial products with a 64 x 128 tile per workgroup,
+// for launches in which every batch has between 65 and 128 active columns:
+// wave w owns rows 16 w .. 16 w + 15 of the tile and all eight 16-column
+// blocks, so one A operand read from LDS serves eight products (two in the
+// 64 x 64 tile) and a batch's columns take one tile instead of two, each
+// A row tile being streamed once. Whole-tile path only (the conditions of
+// VEC above); the main loop has no branch around a memory access, as in
+// tile_mainloop_vec. Measured at 10 groups of order 9024 with 100 active
+// columns each: 3.2 ms per product against 3.4-3.8 ms for the 64 x 64 tile
+// in the same runs (the narrow tile stays faster below about 64 columns
+// per group). Each output element takes the same products in the same
+// order as in dgemm_partial_kernel.
+constexpr int TNW = 128;
+template <bool AK>
+__global__ __launch_bounds__(256) void dgemm_partial_wide_kernel(int M, int K, int S, int Kc,
+                                                                  const double* __restrict__ A, int64_t lda, int64_t sA,
+                                                                  const double* __restrict__ B, int64_t ldb, int64_t sB,
+                                                                  double* __restrict__ part, int64_t ldc, int64_t sC,
+                                                                  int64_t sP, const int* __restrict__ cmap_all,
+                                                                  const int* __restrict__ nact, int cstride) {
+  constexpr int BM = 64, BK = 16, NB = TNW / 16;
+  constexpr int APT = BM * BK / 256, BPT = BK * TNW / 256;   // 4 and 8 per thread
+  __shared__ double As[2][BK][BM + LPAD];
+  __shared__ double Bs[2][BK][TNW + LPAD];
+  const int b = blockIdx.z / S, sk = blockIdx.z % S;
+  const int N = nact[b];
+  const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TNW;
+  if (j0 >= N) return;
+  const int* cmap = cmap_all + (int64_t)b * cstride;
+  A += (int64_t)b * sA;
+  B += (int64_t)b * sB;
+  double* C = part + (int64_t)sk * sP + (int64_t)b * sC;
+  const int kbeg = sk * Kc;
+  const int kend = min(K, kbeg + Kc);
+  // a last row tile that would reach past M is moved back to end at M
+  const int il = min(i0, M - BM);
+  const int t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wi = 16 * w;
+  const int li = lane & 15, lk = lane >> 4;
+  const int nblk = max(0, min(NB, (N - j0 + 15) / 16));   // blocks holding active columns
+  dbl4 acc[NB];
+#pragma unroll
+  for (int y = 0; y < NB; ++y) acc[y] = dbl4{0.0, 0.0, 0.0, 0.0};
+  const double* pa;
+  if (AK) {
+    constexpr int TPR = BK / APT;
+    pa = A + (int64_t)(il + t / TPR) * lda + kbeg + (t % TPR) * APT;
+  } else {
+    constexpr int TPR = BM / APT;
+    pa = A + (int64_t)(kbeg + t / TPR) * lda + il + (t % TPR) * APT;
+  }
+  const int64_t astep = AK ? BK : (int64_t)BK * lda;
+  constexpr int TPRB = BK / BPT;
+  const int gj = j0 + t / TPRB;
+  const bool bact = gj < N;
+  const double* pb = B + (int64_t)cmap[bact ? gj : 0] * ldb + kbeg + (t % TPRB) * BPT;
+  const int nk = (kend - kbeg) / BK;
+  dbl2 ra0[APT / 2], rb0[BPT / 2], ra1[APT / 2], rb1[BPT / 2];
+  auto fetch = [&](int kt, dbl2 (&ra)[APT / 2], dbl2 (&rb)[BPT / 2]) {
+    const int k = min(kt, nk - 1);
+    const double* qa = pa + k * astep;
+    const double* qb = pb + (int64_t)k * BK;
+#pragma unroll
+    for (int q = 0; q < APT / 2; ++q) ra[q] = *reinterpret_cast<const dbl2*>(qa + 2 * q);
+#pragma unroll
+    for (int q = 0; q < BPT / 2; ++q) rb[q] = *reinterpret_cast<const dbl2*>(qb + 2 * q);
+  };
+  auto store = [&](const dbl2 (&ra)[APT / 2], const dbl2 (&rb)[BPT / 2], double (*Asl)[BM + LPAD],
+                   double (*Bsl)[TNW + LPAD]) {
+    if (AK) {
+      constexpr int TPR = BK / APT;
+      const int i = t / TPR, kb = (t % TPR) * APT;
+#pragma unroll
+      for (int q = 0; q < APT; ++q) Asl[kb + q][lds_col<true, APT>(kb + q, i)] = ra[q / 2][q % 2];
+    } else {
+      constexpr int TPR = BM / APT;
+      const int k = t / TPR, ib = (t % TPR) * APT;
+#pragma unroll
+      for (int q = 0; q < APT; ++q) Asl[k][lds_col<false, APT>(k, ib + q)] = ra[q / 2][q % 2];
+    }
+    const int j = t / TPRB, kb = (t % TPRB) * BPT;
+#pragma unroll
+    for (int q = 0; q < BPT; ++q)
+      Bsl[kb + q][lds_col<true, BPT>(kb + q, j)] = bact ? rb[q / 2][q % 2] : 0.0;
+  };
+  auto products = [&](const double (*Asl)[BM + LPAD], const double (*Bsl)[TNW + LPAD]) {
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 4) {
+      const double av = Asl[kk + lk][lds_col<AK, APT>(kk + lk, wi + li)];
+      double bv[NB];
+#pragma unroll
+      for (int y = 0; y < NB; ++y) bv[y] = Bsl[kk + lk][lds_col<true, BPT>(kk + lk, 16 * y + li)];
+#pragma unroll
+      for (int y = 0; y < NB; ++y)
+        if (y < nblk) acc[y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv[y], acc[y], 0, 0, 0);
+    }
+  };
+  if (nk > 0) {
+    fetch(0, ra0, rb0);
+    store(ra0, rb0, As[0], Bs[0]);
+    fetch(1, ra0, rb0);
+    // keep slice 1's loads older than slice 2's (the waits count in issue order)
+    __builtin_amdgcn_sched_barrier(0);
+    fetch(2, ra1, rb1);
+    __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+      store(ra0, rb0, As[1], Bs[1]);
+      fetch(kt + 3, ra0, rb0);
+      products(As[0], Bs[0]);
+      __syncthreads();
+      if (kt + 1 >= nk) break;
+      store(ra1, rb1, As[0], Bs[0]);
+      fetch(kt + 4, ra1, rb1);
+      products(As[1], Bs[1]);
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int y = 0; y < NB; ++y)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int gi = il + wi + mfma_row(lane, r);
+      const int gc = j0 + 16 * y + mfma_col(lane);
+      if (gi >= i0 && gi < M && gc < N) C[(int64_t)cmap[gc] * ldc + gi] = acc[y][r];
+    }
+}
+
 // Loss epilogue over split-K partials of f: for row i < M of batch b and
 // active column c = cmap[b*N + k], k < nact[b], F = sum_s part_s[c][i] +
 // bbar[c]; Z[c][i] = psi(y_i, F)/cnv[c] (0 at padding rows and at rows held
@@ -615,7 +743,8 @@ static int device_cus() {
 }
 
 // Split-K parts for dgemm_partial_kernel: the S that minimises the rounds
-// of resident workgroups (four per compute unit, bound by LDS) times the K
+// of resident workgroups (per_cu per compute unit: four for the 64 x 64
+// tile, bound by LDS; three for the 64 x 128 one) times the K
 // range per part, over the tiles that do work (tiles <= 0: all of them);
 // ties go to the larger S (the finer workgroups balance better: with 10
 // groups of order 9024 and 100 columns each, the smallest S among ties ran
@@ -623,9 +752,9 @@ static int device_cus() {
 // of 16: at small orders the K loop is a short dependent chain, and at
 // order 192 four parts instead of one took the iteration from 35.5 to
 // 28.1 us.
-int splitk_parts(const GemmArgs& g, int64_t tiles) {
+int splitk_parts(const GemmArgs& g, int64_t tiles, int per_cu) {
   if (tiles <= 0) tiles = ceil_div(g.M, 64) * ceil_div(g.N, TN) * g.batch;
-  const int64_t slots = 4 * (int64_t)device_cus();
+  const int64_t slots = (int64_t)per_cu * device_cus();
   int best = 1;
   int64_t best_cost = -1;
   for (int S = 1; S <= kMaxSplitK; ++S) {
@@ -637,7 +766,7 @@ int splitk_parts(const GemmArgs& g, int64_t tiles) {
 }
 
 int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP,
-                 const int* cmap, const int* nact) {
+                 const int* cmap, const int* nact, bool wide) {
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return 0;
   const int Kc = (int)round_up(ceil_div(g.K, S), 16);
   dim3 grid((unsigned)ceil_div(g.M, 64), (unsigned)ceil_div(g.N, TN), (unsigned)(g.batch * S));
@@ -651,6 +780,17 @@ int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double
   const bool vec = g.M >= 64 && g.M % 2 == 0 && g.K % 16 == 0 && g.lda % 2 == 0 && g.ldb % 2 == 0 &&
                    g.sA % 2 == 0 && g.sB % 2 == 0 && (reinterpret_cast<uintptr_t>(g.A) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(g.B) & 15) == 0;
+  if (wide && vec && !ident) {
+    grid.y = (unsigned)ceil_div(g.N, TNW);
+    if (a_kcontig)
+      hipLaunchKernelGGL(dgemm_partial_wide_kernel<true>, grid, dim3(256), 0, s, g.M, g.K, S, Kc, g.A,
+                         g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap, nact, g.N);
+    else
+      hipLaunchKernelGGL(dgemm_partial_wide_kernel<false>, grid, dim3(256), 0, s, g.M, g.K, S, Kc, g.A,
+                         g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap, nact, g.N);
+    KMP_LAUNCH_CHECK();
+    return 0;
+  }
 #define KMP_PART_CASE(AKV, IDV, VV)                                                              \
   if (a_kcontig == AKV && ident == IDV && vec == VV)                                             \
     hipLaunchKernelGGL((dgemm_partial_kernel<64, 16, AKV, IDV, 2, VV>), grid, dim3(256), 0, s, g.M, \

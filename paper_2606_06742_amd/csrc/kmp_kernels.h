@@ -52,9 +52,12 @@ constexpr int kMaxSplitK = 4;
 // the parts in order and writes Z plus 64-row column sums (see LossEpi).
 // Both work on the active columns only: batch b has nact[b] of them, the
 // k-th being column cmap[b*g.N + k] (B k-contiguous, C column-major).
-int splitk_parts(const GemmArgs& g, int64_t tiles = 0);
+// With wide (active-column lists and whole-tile operands only), 64 x 128
+// tiles, for launches whose batches all have 65 to 128 active columns; its
+// split takes per_cu = 3.
+int splitk_parts(const GemmArgs& g, int64_t tiles = 0, int per_cu = 4);
 int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP,
-                 const int* cmap, const int* nact);
+                 const int* cmap, const int* nact, bool wide = false);
 int loss_epilogue(hipStream_t s, int M, int N, int batch, int S, const double* part, int64_t ldc,
                   int64_t sC, int64_t sP, double* Z, const LossEpi& e, const int* cmap,
                   const int* nact);
