@@ -524,33 +524,38 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
       }
 }
 
-// The same split-K partial products with a 64 x 128 tile per workgroup,
-// for launches in which every batch has between 65 and 128 active columns:
-// wave w owns rows 16 w .. 16 w + 15 of the tile and all eight 16-column
-// blocks, so one A operand read from LDS serves eight products (two in the
-// 64 x 64 tile) and a batch's columns take one tile instead of two, each
-// A row tile being streamed once. Whole-tile path only (the conditions of
-// VEC above); the main loop has no branch around a memory access, as in
-// tile_mainloop_vec. Measured at 10 groups of order 9024 with 100 active
-// columns each: 3.2 ms per product against 3.4-3.8 ms for the 64 x 64 tile
-// in the same runs (the narrow tile stays faster below about 64 columns
-// per group). Each output element takes the same products in the same
-// order as in dgemm_partial_kernel.
-constexpr int TNW = 128;
-template <bool AK>
-__global__ __launch_bounds__(256) void dgemm_partial_wide_kernel(int M, int K, int S, int Kc,
+// The same split-K partial products with the four waves of a workgroup
+// stacked by rows: wave w owns rows (BM/4) w .. of a BM x TW tile and all
+// TW/16 of its column blocks, so that an A operand read from LDS serves
+// TW/16 products (two in the 2 x 2 arrangement above) and, with 64 or fewer
+// active columns, every wave has the same share of the products (in the
+// 2 x 2 arrangement the waves of the second 32 columns idle while a batch
+// has 32 or fewer, and do half the products at 33 to 48). Two shapes:
+//  - 64 x 128, for launches in which every batch has 65 to 128 active
+//    columns: a batch's columns take one tile instead of two, each A row
+//    tile being streamed once;
+//  - 128 x 64 otherwise (M >= 128).
+// Whole-tile path only (the conditions of VEC above); the main loop has no
+// branch around a memory access, as in tile_mainloop_vec. Measured at 10
+// groups of order 9024 (split-K 4, both operand orders): 100 active
+// columns each, 64 x 128 3.2 ms against 3.5-3.8 ms for the 2 x 2 64 x 64
+// tile in the same runs; 30 columns each, 128 x 64 1.6 ms against 1.8 ms;
+// 12 each 1.2 against 1.26; 60 each equal. Each output element takes the
+// same products in the same order as in dgemm_partial_kernel.
+template <int BM, int TW, bool AK>
+__global__ __launch_bounds__(256) void dgemm_partial_rows_kernel(int M, int K, int S, int Kc,
                                                                   const double* __restrict__ A, int64_t lda, int64_t sA,
                                                                   const double* __restrict__ B, int64_t ldb, int64_t sB,
                                                                   double* __restrict__ part, int64_t ldc, int64_t sC,
                                                                   int64_t sP, const int* __restrict__ cmap_all,
                                                                   const int* __restrict__ nact, int cstride) {
-  constexpr int BM = 64, BK = 16, NB = TNW / 16;
-  constexpr int APT = BM * BK / 256, BPT = BK * TNW / 256;   // 4 and 8 per thread
+  constexpr int BK = 16, MB = BM / 64, NB = TW / 16;
+  constexpr int APT = BM * BK / 256, BPT = BK * TW / 256;   // per thread and slice
   __shared__ double As[2][BK][BM + LPAD];
-  __shared__ double Bs[2][BK][TNW + LPAD];
+  __shared__ double Bs[2][BK][TW + LPAD];
   const int b = blockIdx.z / S, sk = blockIdx.z % S;
   const int N = nact[b];
-  const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TNW;
+  const int i0 = blockIdx.x * BM, j0 = blockIdx.y * TW;
   if (j0 >= N) return;
   const int* cmap = cmap_all + (int64_t)b * cstride;
   A += (int64_t)b * sA;
@@ -562,12 +567,14 @@ __global__ __launch_bounds__(256) void dgemm_partial_wide_kernel(int M, int K, i
   const int il = min(i0, M - BM);
   const int t = threadIdx.x, lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int wi = 16 * w;
+  const int wi = (BM / 4) * w;
   const int li = lane & 15, lk = lane >> 4;
   const int nblk = max(0, min(NB, (N - j0 + 15) / 16));   // blocks holding active columns
-  dbl4 acc[NB];
+  dbl4 acc[MB][NB];
 #pragma unroll
-  for (int y = 0; y < NB; ++y) acc[y] = dbl4{0.0, 0.0, 0.0, 0.0};
+  for (int x = 0; x < MB; ++x)
+#pragma unroll
+    for (int y = 0; y < NB; ++y) acc[x][y] = dbl4{0.0, 0.0, 0.0, 0.0};
   const double* pa;
   if (AK) {
     constexpr int TPR = BK / APT;
@@ -593,7 +600,7 @@ __global__ __launch_bounds__(256) void dgemm_partial_wide_kernel(int M, int K, i
     for (int q = 0; q < BPT / 2; ++q) rb[q] = *reinterpret_cast<const dbl2*>(qb + 2 * q);
   };
   auto store = [&](const dbl2 (&ra)[APT / 2], const dbl2 (&rb)[BPT / 2], double (*Asl)[BM + LPAD],
-                   double (*Bsl)[TNW + LPAD]) {
+                   double (*Bsl)[TW + LPAD]) {
     if (AK) {
       constexpr int TPR = BK / APT;
       const int i = t / TPR, kb = (t % TPR) * APT;
@@ -610,16 +617,20 @@ __global__ __launch_bounds__(256) void dgemm_partial_wide_kernel(int M, int K, i
     for (int q = 0; q < BPT; ++q)
       Bsl[kb + q][lds_col<true, BPT>(kb + q, j)] = bact ? rb[q / 2][q % 2] : 0.0;
   };
-  auto products = [&](const double (*Asl)[BM + LPAD], const double (*Bsl)[TNW + LPAD]) {
+  auto products = [&](const double (*Asl)[BM + LPAD], const double (*Bsl)[TW + LPAD]) {
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 4) {
-      const double av = Asl[kk + lk][lds_col<AK, APT>(kk + lk, wi + li)];
-      double bv[NB];
+      double av[MB], bv[NB];
+#pragma unroll
+      for (int x = 0; x < MB; ++x) av[x] = Asl[kk + lk][lds_col<AK, APT>(kk + lk, wi + 16 * x + li)];
 #pragma unroll
       for (int y = 0; y < NB; ++y) bv[y] = Bsl[kk + lk][lds_col<true, BPT>(kk + lk, 16 * y + li)];
 #pragma unroll
       for (int y = 0; y < NB; ++y)
-        if (y < nblk) acc[y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv[y], acc[y], 0, 0, 0);
+        if (y < nblk)
+#pragma unroll
+          for (int x = 0; x < MB; ++x)
+            acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[x], bv[y], acc[x][y], 0, 0, 0);
     }
   };
   if (nk > 0) {
@@ -643,13 +654,15 @@ __global__ __launch_bounds__(256) void dgemm_partial_wide_kernel(int M, int K, i
     }
   }
 #pragma unroll
-  for (int y = 0; y < NB; ++y)
+  for (int x = 0; x < MB; ++x)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int gi = il + wi + mfma_row(lane, r);
-      const int gc = j0 + 16 * y + mfma_col(lane);
-      if (gi >= i0 && gi < M && gc < N) C[(int64_t)cmap[gc] * ldc + gi] = acc[y][r];
-    }
+    for (int y = 0; y < NB; ++y)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int gi = il + wi + 16 * x + mfma_row(lane, r);
+        const int gc = j0 + 16 * y + mfma_col(lane);
+        if (gi >= i0 && gi < M && gc < N) C[(int64_t)cmap[gc] * ldc + gi] = acc[x][y][r];
+      }
 }
 
 // Loss epilogue over split-K partials of f: for row i < M of batch b and
@@ -765,8 +778,30 @@ int splitk_parts(const GemmArgs& g, int64_t tiles, int per_cu) {
   return best;
 }
 
+// The stacked-row tiles were measured at order 9024 only, so smaller
+// orders keep the 2 x 2 tile.
+PartTile pick_part_tile(int M, int G, int C, const int* na, int64_t* tiles, int* per_cu) {
+  int64_t t64 = 0, tw = 0, tt = 0;
+  bool wide = C > 64;
+  for (int g = 0; g < G; ++g) {
+    const int n = na ? na[g] : C;
+    t64 += ceil_div(M, 64) * ceil_div(n, 64);
+    tw += ceil_div(M, 64) * ceil_div(n, 128);
+    tt += ceil_div(M, 128) * ceil_div(n, 64);
+    if (n > 0 && (n <= 64 || n > 128)) wide = false;
+  }
+  if (M < 4096 || t64 == 0) {
+    *tiles = t64;
+    *per_cu = 4;
+    return PartTile::k64x64;
+  }
+  *per_cu = 3;
+  *tiles = wide ? tw : tt;
+  return wide ? PartTile::k64x128 : PartTile::k128x64;
+}
+
 int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP,
-                 const int* cmap, const int* nact, bool wide) {
+                 const int* cmap, const int* nact, PartTile tile) {
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return 0;
   const int Kc = (int)round_up(ceil_div(g.K, S), 16);
   dim3 grid((unsigned)ceil_div(g.M, 64), (unsigned)ceil_div(g.N, TN), (unsigned)(g.batch * S));
@@ -780,14 +815,18 @@ int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double
   const bool vec = g.M >= 64 && g.M % 2 == 0 && g.K % 16 == 0 && g.lda % 2 == 0 && g.ldb % 2 == 0 &&
                    g.sA % 2 == 0 && g.sB % 2 == 0 && (reinterpret_cast<uintptr_t>(g.A) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(g.B) & 15) == 0;
-  if (wide && vec && !ident) {
-    grid.y = (unsigned)ceil_div(g.N, TNW);
-    if (a_kcontig)
-      hipLaunchKernelGGL(dgemm_partial_wide_kernel<true>, grid, dim3(256), 0, s, g.M, g.K, S, Kc, g.A,
-                         g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap, nact, g.N);
-    else
-      hipLaunchKernelGGL(dgemm_partial_wide_kernel<false>, grid, dim3(256), 0, s, g.M, g.K, S, Kc, g.A,
-                         g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap, nact, g.N);
+  if (tile != PartTile::k64x64 && vec && !ident && g.M >= 128) {
+    const bool w = tile == PartTile::k64x128;
+    grid.x = (unsigned)ceil_div(g.M, w ? 64 : 128);
+    grid.y = (unsigned)ceil_div(g.N, w ? 128 : 64);
+#define KMP_ROWS_CASE(BMV, TWV, AKV)                                                              \
+  hipLaunchKernelGGL((dgemm_partial_rows_kernel<BMV, TWV, AKV>), grid, dim3(256), 0, s, g.M, g.K, S, \
+                     Kc, g.A, g.lda, g.sA, g.B, g.ldb, g.sB, part, g.ldc, g.sC, sP, cmap, nact, g.N)
+    if (w && a_kcontig) KMP_ROWS_CASE(64, 128, true);
+    else if (w) KMP_ROWS_CASE(64, 128, false);
+    else if (a_kcontig) KMP_ROWS_CASE(128, 64, true);
+    else KMP_ROWS_CASE(128, 64, false);
+#undef KMP_ROWS_CASE
     KMP_LAUNCH_CHECK();
     return 0;
   }

@@ -52,12 +52,19 @@ constexpr int kMaxSplitK = 4;
 // the parts in order and writes Z plus 64-row column sums (see LossEpi).
 // Both work on the active columns only: batch b has nact[b] of them, the
 // k-th being column cmap[b*g.N + k] (B k-contiguous, C column-major).
-// With wide (active-column lists and whole-tile operands only), 64 x 128
-// tiles, for launches whose batches all have 65 to 128 active columns; its
-// split takes per_cu = 3.
+// Tile of the partial products: 64 x 64 with the waves in a 2 x 2
+// arrangement (every case), or, with active-column lists, whole-tile
+// operands and M >= 128, the waves stacked by rows over 64 x 128 or
+// 128 x 64 (three workgroups per compute unit instead of four: the split
+// takes per_cu = 3 and the tile counts of the shape).
+enum class PartTile { k64x64, k64x128, k128x64 };
+// The tile for a launch over G batches of order M with na[g] active columns
+// (host counts, C columns each if na is null) and its work tiles and
+// resident workgroups per compute unit, for splitk_parts.
+PartTile pick_part_tile(int M, int G, int C, const int* na, int64_t* tiles, int* per_cu);
 int splitk_parts(const GemmArgs& g, int64_t tiles = 0, int per_cu = 4);
 int gemm_partial(hipStream_t s, const GemmArgs& g, bool a_kcontig, int S, double* part, int64_t sP,
-                 const int* cmap, const int* nact, bool wide = false);
+                 const int* cmap, const int* nact, PartTile tile = PartTile::k64x64);
 int loss_epilogue(hipStream_t s, int M, int N, int batch, int S, const double* part, int64_t ldc,
                   int64_t sC, int64_t sP, double* Z, const LossEpi& e, const int* cmap,
                   const int* nact);

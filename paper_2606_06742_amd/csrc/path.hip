@@ -1234,19 +1234,12 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   g1.A = p.QB; g1.lda = p.N; g1.sA = (int64_t)p.N * p.N;
   g1.B = p.abar; g1.ldb = p.N; g1.sB = sC;
   g1.ldc = p.N; g1.sC = sC;
-  // output tiles that do work: 64-row tiles of the active columns; the
-  // 64 x 128 tiles when every group that has active columns has 65 to 128
-  // of them (the counts are one poll behind: either choice is exact)
-  int64_t work_tiles = 0, wide_tiles = 0;
-  bool wide = p.C > 64;
-  for (int g = 0; g < p.G; ++g) {
-    const int na = p.nact_host ? p.nact_host[g] : p.C;
-    work_tiles += ceil_div(p.N, 64) * ceil_div(na, 64);
-    wide_tiles += ceil_div(p.N, 64) * ceil_div(na, 128);
-    if (na > 0 && (na <= 64 || na > 128)) wide = false;
-  }
-  if (wide_tiles == 0) wide = false;
-  const int S1 = wide ? splitk_parts(g1, wide_tiles, 3) : splitk_parts(g1, work_tiles);
+  // the tile shape and its work tiles (the counts are one poll behind:
+  // any choice is exact)
+  int64_t work_tiles = 0;
+  int per_cu = 4;
+  const PartTile tile = pick_part_tile(p.N, p.G, p.C, p.nact_host, &work_tiles, &per_cu);
+  const int S1 = splitk_parts(g1, work_tiles, per_cu);
   LossEpi e;
   e.loss = p.loss; e.delta = delta;
   e.y = p.ylab; e.sy = p.N; e.nv = p.nv; e.cnv = p.cnv;
@@ -1256,7 +1249,7 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   const double gflops = over_active(p, [&](double n, double c) { return 2.0 * n * n * c; });
   const double gbytes = over_active(p, [&](double n, double c) { return 8.0 * (n * n + 2.0 * n * c); });
   kc_begin(KMP_KC_GEMM_F, s);
-  if ((rc = gemm_partial(s, g1, true, S1, p.fpart, sP, p.cmap, p.nact, wide)) != 0) return rc;
+  if ((rc = gemm_partial(s, g1, true, S1, p.fpart, sP, p.cmap, p.nact, tile)) != 0) return rc;
   if ((rc = loss_epilogue(s, p.N, p.C, p.G, S1, p.fpart, p.N, sC, sP, p.zmat, e, p.cmap,
                           p.nact)) != 0)
     return rc;
@@ -1267,9 +1260,9 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
   g2.A = p.Q; g2.lda = p.N; g2.sA = (int64_t)p.N * p.N;
   g2.B = p.zmat; g2.ldb = p.N; g2.sB = sC;
   g2.ldc = p.N; g2.sC = sC;
-  const int S2 = wide ? splitk_parts(g2, wide_tiles, 3) : splitk_parts(g2, work_tiles);
+  const int S2 = splitk_parts(g2, work_tiles, per_cu);
   kc_begin(KMP_KC_GEMM_ZHAT, s);
-  if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP, p.cmap, p.nact, wide)) != 0) return rc;
+  if ((rc = gemm_partial(s, g2, false, S2, p.zpart, sP, p.cmap, p.nact, tile)) != 0) return rc;
   kc_end(KMP_KC_GEMM_ZHAT, s, gbytes, gflops);
   const int64_t cols = (int64_t)p.G * p.C;
   const bool gv = iteration_global_vec(p);
