@@ -288,6 +288,7 @@ struct Layout {
   double *A, *Qm, *diag, *off, *tau, *cvec, *ylab, *panel, *dots, *tmat, *gram, *xbuf, *ybuf;
   double *spart, *pnext, *band, *bpart, *gram_all, *tmat_all, *cross_all, *xpart;
   double *ahat, *abar, *zmat, *anew, *estep, *ldl_l, *ldl_d, *vhat, *uvec, *partial, *fpart, *zpart;
+  double *ldl_lr, *ldl_dr, *twist, *band_rev;
   double *beta, *bbar, *rmom, *gcoef, *kkt, *lam, *taucol, *fbuf, *nrm, *inv2s2;
   int *flag, *iters, *iters_total, *active, *nvg, *chk, *cmap, *nact, *stat_count, *cnv;
   int32_t *tidx, *hidx, *fold, *rfold, *cfold;
@@ -329,6 +330,10 @@ size_t carve(const Plan& p, void* ws, Layout* out) {
   l.estep = c.take<double>(cols * N);
   l.ldl_l = c.take<double>(cols * kBand * N);
   l.ldl_d = c.take<double>(cols * N);
+  l.ldl_lr = c.take<double>(cols * kBand * N);
+  l.ldl_dr = c.take<double>(cols * N);
+  l.twist = c.take<double>(cols * (kBand * kBand + kBand));
+  l.band_rev = c.take<double>(G * (kBand + 1) * N);
   l.vhat = c.take<double>(cols * N);
   l.uvec = c.take<double>(cols * N);
   l.partial = c.take<double>(G * (size_t)p.RT * C);
@@ -511,6 +516,7 @@ PathArrays path_arrays_of(const Layout& lay, const Plan& plan, int loss, bool gl
   pa.ahat = lay.ahat; pa.abar = lay.abar; pa.zmat = lay.zmat;
   pa.QB = lay.A;             // the factorisation's buffer, free once Q is formed
   pa.anew = lay.anew; pa.estep = lay.estep; pa.ldl_l = lay.ldl_l; pa.ldl_d = lay.ldl_d;
+  pa.ldl_lr = lay.ldl_lr; pa.ldl_dr = lay.ldl_dr; pa.twist = lay.twist; pa.band_rev = lay.band_rev;
   pa.vhat = lay.vhat;
   pa.uvec = lay.uvec; pa.partial = lay.partial; pa.beta = lay.beta; pa.bbar = lay.bbar;
   pa.fpart = lay.fpart; pa.zpart = lay.zpart;

@@ -196,6 +196,13 @@ struct PathArrays {
   double* estep = nullptr;  // device-memory solve: w, then x, then a+
   double* ldl_l = nullptr;  // kBand x N per column: tiles of the banded LDL' factor
   double* ldl_d = nullptr;  // N per column: 1/D
+  // the same factors of the matrix with rows and columns in reverse order,
+  // and the twist block where the two meet (kBand^2 + kBand per column);
+  // band_rev: the band of that reversed matrix (G x (kBand+1) x N)
+  double* ldl_lr = nullptr;
+  double* ldl_dr = nullptr;
+  double* twist = nullptr;
+  double* band_rev = nullptr;
   double* vhat = nullptr;
   double* uvec = nullptr;   // T vhat
   double* partial = nullptr;// G x tiles x C

@@ -177,12 +177,21 @@ __device__ __forceinline__ double row4_sum(double v) { return swap_sum32(swap_su
 // (V[a*N + 16 I + j]) as the transposed factors need.
 constexpr int SPF = 10;
 
+// Element i of the solve's vector: xs[i], or xs[N - 1 - i] for the sweeps
+// of the twisted solve that run from the last row (REV).
+template <bool REV>
+__device__ __forceinline__ double& xel(double* xs, int N, int i) {
+  return REV ? xs[N - 1 - i] : xs[i];
+}
+
 // One forward block step of the LDS solve: rg holds the lane's four entries
 // of tile I and receives those of tile min(I + SPF, NB - 1). Branch free, so
-// that the loads of the following steps stay in flight across it.
+// that the loads of the following steps stay in flight across it. With
+// LAST only r = w_I - C_I y_{I-1} is formed, into slot (lead lanes).
+template <bool REV = false, bool LAST = false>
 __device__ __forceinline__ void band_fwd_step(const double* __restrict__ Vc, double* xs, int N,
                                               int NB, int I, int a, int g, bool lead,
-                                              double (&rg)[4]) {
+                                              double (&rg)[4], double* slot = nullptr) {
   double cn[4], lm[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
@@ -193,28 +202,33 @@ __device__ __forceinline__ void band_fwd_step(const double* __restrict__ Vc, dou
   const int In = min(I + SPF, NB - 1);
 #pragma unroll
   for (int t = 0; t < 4; ++t) rg[t] = Vc[(int64_t)(4 * g + t) * N + BND * In + a];
-  double p0 = lead ? xs[BND * I + a] : 0.0, p1 = 0.0;
-  const double* yp = xs + BND * max(I - 1, 0) + 4 * g;
-  p0 = fma(cn[0], yp[0], p0);
-  p1 = fma(cn[1], yp[1], p1);
-  p0 = fma(cn[2], yp[2], p0);
-  p1 = fma(cn[3], yp[3], p1);
+  double p0 = lead ? xel<REV>(xs, N, BND * I + a) : 0.0, p1 = 0.0;
+  const int yb = BND * max(I - 1, 0) + 4 * g;
+  p0 = fma(cn[0], xel<REV>(xs, N, yb), p0);
+  p1 = fma(cn[1], xel<REV>(xs, N, yb + 1), p1);
+  p0 = fma(cn[2], xel<REV>(xs, N, yb + 2), p0);
+  p1 = fma(cn[3], xel<REV>(xs, N, yb + 3), p1);
   const double r = row4_sum(p0 + p1);
-  xs[BND * I + a] = r;                 // the four lanes of row a store the same value
+  if constexpr (LAST) {
+    if (lead) slot[a] = r;
+    return;
+  }
+  xel<REV>(xs, N, BND * I + a) = r;    // the four lanes of row a store the same value
   wave_sync();
-  const double* rp = xs + BND * I + 4 * g;
+  const int rb = BND * I + 4 * g;
   double q0 = lead ? r : 0.0, q1 = 0.0;
-  q0 = fma(lm[0], rp[0], q0);
-  q1 = fma(lm[1], rp[1], q1);
-  q0 = fma(lm[2], rp[2], q0);
-  q1 = fma(lm[3], rp[3], q1);
+  q0 = fma(lm[0], xel<REV>(xs, N, rb), q0);
+  q1 = fma(lm[1], xel<REV>(xs, N, rb + 1), q1);
+  q0 = fma(lm[2], xel<REV>(xs, N, rb + 2), q0);
+  q1 = fma(lm[3], xel<REV>(xs, N, rb + 3), q1);
   const double yv = row4_sum(q0 + q1);
-  xs[BND * I + a] = yv;
+  xel<REV>(xs, N, BND * I + a) = yv;
   wave_sync();
 }
 
 // One backward block step (block I = NB - 1 - tt); vprev holds the lane's
 // entries (4g+t, a) of tile I + 1.
+template <bool REV = false>
 __device__ __forceinline__ void band_bwd_step(const double* __restrict__ Vc,
                                               const double* __restrict__ Dc, double* xs, int N,
                                               int NB, int tt, int a, int g, bool lead,
@@ -232,23 +246,23 @@ __device__ __forceinline__ void band_bwd_step(const double* __restrict__ Vc,
 #pragma unroll
   for (int t = 0; t < 4; ++t) rg[t] = Vc[(int64_t)a * N + BND * In + 4 * g + t];
   dr = Dc[BND * In + a];
-  double p0 = lead ? dv * xs[BND * I + a] : 0.0, p1 = 0.0;
-  const double* xp = xs + BND * min(I + 1, NB - 1) + 4 * g;
-  p0 = fma(cn[0], xp[0], p0);
-  p1 = fma(cn[1], xp[1], p1);
-  p0 = fma(cn[2], xp[2], p0);
-  p1 = fma(cn[3], xp[3], p1);
+  double p0 = lead ? dv * xel<REV>(xs, N, BND * I + a) : 0.0, p1 = 0.0;
+  const int xb = BND * min(I + 1, NB - 1) + 4 * g;
+  p0 = fma(cn[0], xel<REV>(xs, N, xb), p0);
+  p1 = fma(cn[1], xel<REV>(xs, N, xb + 1), p1);
+  p0 = fma(cn[2], xel<REV>(xs, N, xb + 2), p0);
+  p1 = fma(cn[3], xel<REV>(xs, N, xb + 3), p1);
   const double sv = row4_sum(p0 + p1);
-  xs[BND * I + a] = sv;
+  xel<REV>(xs, N, BND * I + a) = sv;
   wave_sync();
-  const double* sp = xs + BND * I + 4 * g;
+  const int sb = BND * I + 4 * g;
   double q0 = lead ? sv : 0.0, q1 = 0.0;
-  q0 = fma(lm[0], sp[0], q0);
-  q1 = fma(lm[1], sp[1], q1);
-  q0 = fma(lm[2], sp[2], q0);
-  q1 = fma(lm[3], sp[3], q1);
+  q0 = fma(lm[0], xel<REV>(xs, N, sb), q0);
+  q1 = fma(lm[1], xel<REV>(xs, N, sb + 1), q1);
+  q0 = fma(lm[2], xel<REV>(xs, N, sb + 2), q0);
+  q1 = fma(lm[3], xel<REV>(xs, N, sb + 3), q1);
   const double xv = row4_sum(q0 + q1);
-  xs[BND * I + a] = xv;
+  xel<REV>(xs, N, BND * I + a) = xv;
   wave_sync();
 #pragma unroll
   for (int t = 0; t < 4; ++t) vprev[t] = vv[t];
@@ -298,6 +312,125 @@ __device__ __forceinline__ void band_solve(const double* __restrict__ Vc,
   for (int p = 0; p < SPF; ++p)
     if (NBm + p < NB) band_bwd_step(Vc, Dc, xs, N, NB, NBm + p, a, g, lead, ring[p], dring[p], vprev);
   wave_sync();
+}
+
+// Twisted form of the same solve, for a workgroup of two or more
+// wavefronts: the top-down factors of blocks 0 .. k (k = NB/2) and those of
+// the reversed matrix (rows and columns in reverse order: the bottom-up
+// factors of blocks NB-1 .. k) meet at block k, where
+//   Z = M_kk - C_k D_{k-1} C_k' - (the same term from below)
+// (the two Schur complements of block k, less M_kk once). With
+// r = w_k - C_k y_{k-1} from the top sweep and r~ from the bottom one,
+// x_k = Z^{-1} (r + r~ - w_k); from x_k the backward sweeps run outwards.
+// Wavefront 0 takes the top half, wavefront 1 the bottom half, so the
+// dependent chain is about half as long as in band_solve, for the same
+// tiles read. Vr, Dr: the reversed matrix's factors (block J of it at
+// 16 J, in its own row order); tw: L_Z^{-1} (16 x 16, row-major, strict
+// lower part) and 1/D_Z; tslot: 48 doubles of LDS. Every wavefront of the
+// workgroup calls it (it holds two barriers); the caller synchronises
+// after it before reading xs.
+
+// forward sweep over blocks 0 .. n-1, then r of block n into slot
+template <bool REV>
+__device__ __forceinline__ void band_sweep_fwd(const double* __restrict__ Vc, double* xs, int N,
+                                               int n, int a, int g, bool lead, double* slot) {
+  const int NBe = n + 1;
+  const int nm = n - n % SPF;
+  double ring[SPF][4];
+#pragma unroll
+  for (int p = 0; p < SPF; ++p) {
+    const int Ib = min(p, n);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) ring[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * Ib + a];
+  }
+  for (int I0 = 0; I0 < nm; I0 += SPF) {
+#pragma unroll
+    for (int p = 0; p < SPF; ++p) band_fwd_step<REV>(Vc, xs, N, NBe, I0 + p, a, g, lead, ring[p]);
+  }
+#pragma unroll
+  for (int p = 0; p < SPF; ++p) {
+    if (nm + p < n) band_fwd_step<REV>(Vc, xs, N, NBe, nm + p, a, g, lead, ring[p]);
+    else if (nm + p == n) band_fwd_step<REV, true>(Vc, xs, N, NBe, n, a, g, lead, ring[p], slot);
+  }
+}
+
+// backward sweep over blocks n-1 .. 0, block n's solution already in xs
+template <bool REV>
+__device__ __forceinline__ void band_sweep_bwd(const double* __restrict__ Vc,
+                                               const double* __restrict__ Dc, double* xs, int N,
+                                               int n, int a, int g, bool lead) {
+  const int NBe = n + 1;
+  // slot p serves the steps tt = p (mod SPF), tt = 1 .. n (block n - tt)
+  double ring[SPF][4], dring[SPF];
+#pragma unroll
+  for (int p = 0; p < SPF; ++p) {
+    const int Ib = max(n - (p > 0 ? p : SPF), 0);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) ring[p][t] = Vc[(int64_t)a * N + BND * Ib + 4 * g + t];
+    dring[p] = Dc[BND * Ib + a];
+  }
+  double vprev[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) vprev[t] = Vc[(int64_t)a * N + BND * n + 4 * g + t];
+#pragma unroll
+  for (int p = 1; p < SPF; ++p)
+    if (p <= n) band_bwd_step<REV>(Vc, Dc, xs, N, NBe, p, a, g, lead, ring[p], dring[p], vprev);
+  int T0 = SPF;
+  for (; T0 + SPF - 1 <= n; T0 += SPF) {
+#pragma unroll
+    for (int p = 0; p < SPF; ++p)
+      band_bwd_step<REV>(Vc, Dc, xs, N, NBe, T0 + p, a, g, lead, ring[p], dring[p], vprev);
+  }
+#pragma unroll
+  for (int p = 0; p < SPF; ++p)
+    if (T0 + p <= n) band_bwd_step<REV>(Vc, Dc, xs, N, NBe, T0 + p, a, g, lead, ring[p], dring[p], vprev);
+}
+
+// x_k = Z^{-1} (r + r~ - w_k) = L_Z^{-T} D_Z^{-1} L_Z^{-1} (.), one wavefront
+__device__ __forceinline__ void band_twist_block(const double* __restrict__ tw, double* xs,
+                                                 double* tslot, int k, int a, int g, bool lead) {
+  double* rhs = tslot + 2 * BND;
+  // r~ is in the bottom sweep's row order
+  if (lead) rhs[a] = tslot[a] + tslot[BND + (BND - 1 - a)] - xs[BND * k + a];
+  wave_sync();
+  double q0 = lead ? rhs[a] : 0.0, q1 = 0.0;
+#pragma unroll
+  for (int t = 0; t < 4; t += 2) {
+    const int j0 = 4 * g + t, j1 = j0 + 1;
+    q0 = fma((j0 < a) ? tw[a * BND + j0] : 0.0, rhs[j0], q0);
+    q1 = fma((j1 < a) ? tw[a * BND + j1] : 0.0, rhs[j1], q1);
+  }
+  const double u = row4_sum(q0 + q1) * tw[BND * BND + a];     // D_Z^{-1} L_Z^{-1} rhs
+  wave_sync();
+  if (lead) rhs[a] = u;
+  wave_sync();
+  double s0 = lead ? u : 0.0, s1 = 0.0;
+#pragma unroll
+  for (int t = 0; t < 4; t += 2) {
+    const int j0 = 4 * g + t, j1 = j0 + 1;
+    s0 = fma((j0 > a) ? tw[j0 * BND + a] : 0.0, rhs[j0], s0);
+    s1 = fma((j1 > a) ? tw[j1 * BND + a] : 0.0, rhs[j1], s1);
+  }
+  const double x = row4_sum(s0 + s1);
+  if (lead) xs[BND * k + a] = x;
+}
+
+__device__ __forceinline__ void band_solve_twist(const double* __restrict__ Vt,
+                                                 const double* __restrict__ Dt,
+                                                 const double* __restrict__ Vr,
+                                                 const double* __restrict__ Dr,
+                                                 const double* __restrict__ tw, double* xs,
+                                                 double* tslot, int N, int wv, int lane) {
+  const int NB = N / BND, k = NB / 2, J = NB - 1 - k;
+  const int a = lane & 15, g = lane >> 4;
+  const bool lead = g == 0;
+  if (wv == 0) band_sweep_fwd<false>(Vt, xs, N, k, a, g, lead, tslot);
+  else if (wv == 1) band_sweep_fwd<true>(Vr, xs, N, J, a, g, lead, tslot + BND);
+  __syncthreads();
+  if (wv == 0) band_twist_block(tw, xs, tslot, k, a, g, lead);
+  __syncthreads();
+  if (wv == 0) band_sweep_bwd<false>(Vt, Dt, xs, N, k, a, g, lead);
+  else if (wv == 1) band_sweep_bwd<true>(Vr, Dr, xs, N, J, a, g, lead);
 }
 
 // Fences that order device-memory stores of some lanes of a wavefront
@@ -870,15 +1003,128 @@ __global__ __launch_bounds__(256) void stage_vectors_kernel(
   }
 }
 
+// The band of the matrix with rows and columns in reverse order:
+// Brev[c+d][c] = B[N-1-c-d][N-1-c] = band[d][N-1-c-d] (symmetric B), zero
+// past the last row.
+__global__ void reverse_band_kernel(const double* __restrict__ band, int N, int64_t total,
+                                    double* __restrict__ brev) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = e / N;                 // g * (BND + 1) + d
+    const int c = (int)(e % N), d = (int)(row % (BND + 1));
+    const int src = N - 1 - c - d;
+    brev[e] = (src >= 0) ? band[row * N + src] : 0.0;
+  }
+}
+
+// The twist block of band_solve_twist for every column: k = NB/2,
+// J = NB-1-k,
+//   Z = M_kk - C_k D_{k-1} C_k' - P (C~_J D~_{J-1} C~_J') P
+// (C, D: the top-down factors; C~, D~: those of the reversed matrix, whose
+// block J is block k with its rows in reverse order, P that reversal;
+// both factor arrays hold 1/D), then Z = L D L' by unpivoted row
+// elimination (Z is symmetric positive definite), the same operations
+// turning an identity into L^{-1}. Stored at tw + gc * (BND*BND + BND):
+// L^{-1} row-major, then 1/D. One wavefront per column; lane a < 16 holds
+// row a.
+constexpr int TWS = BND * BND + BND;
+__global__ __launch_bounds__(64 * FW) void twist_factor_kernel(
+    int N, int C, int64_t cols, const int* __restrict__ nv, const double* __restrict__ band,
+    const double* __restrict__ lamv, double kappa, const double* __restrict__ Vt,
+    const double* __restrict__ Dt, const double* __restrict__ Vr, const double* __restrict__ Dr,
+    double* __restrict__ tw) {
+  __shared__ double zr[FW][BND][BND + 1];
+  __shared__ double wr[FW][BND][BND + 1];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t gc = (int64_t)blockIdx.x * FW + wv;
+  if (gc >= cols) return;                       // per wavefront: no barrier below
+  const int g = (int)(gc / C);
+  const double lam = lamv[gc];
+  const double sc = 1.0 / ((double)nv[gc] * kappa);
+  const double* bg = band + (int64_t)g * (BND + 1) * N;
+  const int NB = N / BND, k = NB / 2, J = NB - 1 - k;
+  const double* Vc = Vt + gc * (int64_t)BND * N;
+  const double* Dc = Dt + gc * (int64_t)N;
+  const double* Vq = Vr + gc * (int64_t)BND * N;
+  const double* Dq = Dr + gc * (int64_t)N;
+  const int a = lane;
+  double z[BND], w[BND];
+  if (a < BND) {
+    const int ar = BND - 1 - a;                 // row a of block k in the reversed order
+#pragma unroll
+    for (int c = 0; c < BND; ++c) {
+      const double bv = (c <= a) ? bg[(int64_t)(a - c) * N + BND * k + c]
+                                 : bg[(int64_t)(c - a) * N + BND * k + a];
+      double v = fma(sc, bv, (c == a) ? 2.0 * lam : 0.0);
+      const int cr = BND - 1 - c;
+      double st = 0.0, sb = 0.0;
+      if (k > 0)
+        for (int j = max(a, c); j < BND; ++j)   // C_k upper triangular
+          st = fma(Vc[(int64_t)j * N + BND * k + a] * Vc[(int64_t)j * N + BND * k + c],
+                   1.0 / Dc[BND * (k - 1) + j], st);
+      if (J > 0)
+        for (int j = max(ar, cr); j < BND; ++j)
+          sb = fma(Vq[(int64_t)j * N + BND * J + ar] * Vq[(int64_t)j * N + BND * J + cr],
+                   1.0 / Dq[BND * (J - 1) + j], sb);
+      z[c] = v - st - sb;
+      w[c] = (c == a) ? 1.0 : 0.0;
+    }
+  }
+  for (int p = 0; p < BND; ++p) {
+    wave_sync();
+    if (a == p) {
+#pragma unroll
+      for (int c = 0; c < BND; ++c) {
+        zr[wv][p][c] = z[c];
+        wr[wv][p][c] = w[c];
+      }
+    }
+    wave_sync();
+    if (a < BND && a > p) {
+      const double l = z[p] / zr[wv][p][p];
+#pragma unroll
+      for (int c = 0; c < BND; ++c) {
+        z[c] = fma(-l, zr[wv][p][c], z[c]);
+        w[c] = fma(-l, wr[wv][p][c], w[c]);
+      }
+    }
+  }
+  if (a < BND) {
+    double* out = tw + gc * (int64_t)TWS;
+#pragma unroll
+    for (int c = 0; c < BND; ++c) out[a * BND + c] = w[c];
+    out[BND * BND + a] = 1.0 / z[a];
+  }
+}
+
 int path_stage_factor(hipStream_t s, const PathArrays& p, double kappa) {
   const int64_t cols = (int64_t)p.G * p.C;
   kc_begin(KMP_KC_PRECOMPUTE, s);
   hipLaunchKernelGGL(ldl_factor_kernel, dim3((unsigned)ceil_div(cols, FW)), dim3(64 * FW), 0, s, p.N,
                      p.C, cols, p.cnv, p.band, p.lam, kappa, p.ldl_l, p.ldl_d);
   KMP_LAUNCH_CHECK();
-  // reads the band, writes the factor tiles and 1/d (BND + 1 per element)
-  kc_end(KMP_KC_PRECOMPUTE, s, over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 1.0); }),
-         over_groups(p, [&](double n) { return 4.0 * BND * BND * n * p.C; }));
+  // the twisted form for the per-column update in LDS: the factors of the
+  // reversed matrix and the twist block
+  const bool twist = !path_global_vec(p);
+  if (twist) {
+    const int64_t tb = (int64_t)p.G * (BND + 1) * p.N;
+    hipLaunchKernelGGL(reverse_band_kernel, dim3((unsigned)std::min<int64_t>(ceil_div(tb, 256), 4096)),
+                       dim3(256), 0, s, p.band, p.N, tb, p.band_rev);
+    KMP_LAUNCH_CHECK();
+    hipLaunchKernelGGL(ldl_factor_kernel, dim3((unsigned)ceil_div(cols, FW)), dim3(64 * FW), 0, s,
+                       p.N, p.C, cols, p.cnv, p.band_rev, p.lam, kappa, p.ldl_lr, p.ldl_dr);
+    KMP_LAUNCH_CHECK();
+    hipLaunchKernelGGL(twist_factor_kernel, dim3((unsigned)ceil_div(cols, FW)), dim3(64 * FW), 0, s,
+                       p.N, p.C, cols, p.cnv, p.band, p.lam, kappa, p.ldl_l, p.ldl_d, p.ldl_lr,
+                       p.ldl_dr, p.twist);
+    KMP_LAUNCH_CHECK();
+  }
+  // reads the band, writes the factor tiles and 1/d (BND + 1 per element),
+  // twice with the twisted form
+  const double fac = twist ? 2.0 : 1.0;
+  kc_end(KMP_KC_PRECOMPUTE, s,
+         fac * over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 1.0); }),
+         fac * over_groups(p, [&](double n) { return 4.0 * BND * BND * n * p.C; }));
   return 0;
 }
 
@@ -1092,13 +1338,16 @@ __global__ __launch_bounds__(256) void update_column_kernel(
     int N, int C, int RT, const int* __restrict__ nvv, const double* __restrict__ lamv,
     const double* __restrict__ zpart, int S2, int64_t sP, double* __restrict__ ahat,
     double* __restrict__ abar, const double* __restrict__ Vfac, const double* __restrict__ Dfac,
-    const double* __restrict__ vhat, const double* __restrict__ uvec,
+    const double* __restrict__ Vrev, const double* __restrict__ Drev,
+    const double* __restrict__ twist, const double* __restrict__ vhat,
+    const double* __restrict__ uvec,
     const double* __restrict__ gcoef, const double* __restrict__ partial,
     double* __restrict__ beta, double* __restrict__ bbar, double* __restrict__ rmom,
     double* __restrict__ kktv, int* __restrict__ flag, int* __restrict__ iters,
     int* __restrict__ iters_total, double tol, int max_iter, int restart) {
   extern __shared__ double lds_dyn[];
   __shared__ double red[PW];
+  __shared__ double tslot[3 * BND];
   const int t = threadIdx.x, wv = t >> 6, lane = t & 63;
   const int64_t gc = blockIdx.x;
   if (flag[gc] != 0) return;                            // uniform over the block
@@ -1156,7 +1405,8 @@ __global__ __launch_bounds__(256) void update_column_kernel(
     return;
   }
   __syncthreads();                                      // w complete in LDS
-  if (wv == 0) band_solve(Vfac + gc * (int64_t)BND * N, Dfac + base, xs, N, lane);
+  band_solve_twist(Vfac + gc * (int64_t)BND * N, Dfac + base, Vrev + gc * (int64_t)BND * N,
+                   Drev + base, twist + gc * (int64_t)TWS, xs, tslot, N, wv, lane);
   __syncthreads();                                      // x complete in LDS
   const double gco = gcoef[gc];
   const double sa = gco * (tsum - d0);
@@ -1279,7 +1529,8 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_u));
     kc_begin(KMP_KC_UPDATE, s);
     hipLaunchKernelGGL(update_column_kernel, dim3((unsigned)cols), dim3(PB), lds_u, s, p.N, p.C, RT,
-                       p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l, p.ldl_d, p.vhat,
+                       p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l, p.ldl_d, p.ldl_lr,
+                       p.ldl_dr, p.twist, p.vhat,
                        p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt, p.flag, p.iters,
                        p.iters_total, tol, max_iter, restart);
     KMP_LAUNCH_CHECK();
