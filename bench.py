@@ -235,8 +235,10 @@ def sigma_batch_that_fits(km, w, inp, args, dev):
         spec.flags |= km.KMP_FLAG_SHARED_FACTOR
     n, d = inp["X"].shape
     Q = len(inp["taus"]) if w.loss == "check" else 1
+    # the refit runs every cell on all n points: one fold (as PathRunner does)
+    fold_id, V = (np.zeros(n, dtype=np.int32), 1) if args.refit else (inp["fold_id"], w.V)
     for sb in range(S, 0, -1):
-        b = km.kmp_workspace_bytes(spec, n, d, len(inp["lambdas"]), inp["fold_id"], w.V, S, Q, sb)
+        b = km.kmp_workspace_bytes(spec, n, d, len(inp["lambdas"]), fold_id, V, S, Q, sb)
         if 0 < b <= 0.9 * free:
             return sb
     return 1
