@@ -464,11 +464,12 @@ __device__ __forceinline__ void grid_vec_sync() {
 // per backward step).
 constexpr int SPFG = 10;
 
+template <bool REV = false, bool LAST = false>
 __device__ __forceinline__ void bandg_fwd_step(const double* __restrict__ Vc,
                                                const double* __restrict__ win, double wsc,
                                                double* ysc, double* ring, int N, int NB, int I,
                                                int a, int g, bool lead, double (&rg)[4],
-                                               double& wr) {
+                                               double& wr, double* slot = nullptr) {
   double cn[4], lm[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
@@ -480,7 +481,7 @@ __device__ __forceinline__ void bandg_fwd_step(const double* __restrict__ Vc,
   const int In = min(I + SPFG, NB - 1);
 #pragma unroll
   for (int t = 0; t < 4; ++t) rg[t] = Vc[(int64_t)(4 * g + t) * N + BND * In + a];
-  wr = win[BND * In + a];
+  wr = xel<REV>(const_cast<double*>(win), N, BND * In + a);
   double* cur = ring + BND * (I & 1);
   const double* yp = ring + BND * ((I + 1) & 1) + 4 * g;   // block I - 1 (zeros before block 0)
   p0 = fma(cn[0], yp[0], p0);
@@ -488,6 +489,10 @@ __device__ __forceinline__ void bandg_fwd_step(const double* __restrict__ Vc,
   p0 = fma(cn[2], yp[2], p0);
   p1 = fma(cn[3], yp[3], p1);
   const double r = row4_sum(p0 + p1);
+  if constexpr (LAST) {
+    if (lead) slot[a] = r;
+    return;
+  }
   cur[a] = r;
   wave_sync();
   const double* rp = cur + 4 * g;
@@ -498,11 +503,11 @@ __device__ __forceinline__ void bandg_fwd_step(const double* __restrict__ Vc,
   q1 = fma(lm[3], rp[3], q1);
   const double yv = row4_sum(q0 + q1);
   cur[a] = yv;
-  ysc[BND * I + a] = yv;
+  xel<REV>(ysc, N, BND * I + a) = yv;
   wave_sync();
 }
 
-template <typename WOut>
+template <typename WOut, bool REV = false>
 __device__ __forceinline__ void bandg_bwd_step(const double* __restrict__ Vc,
                                                const double* __restrict__ Dc, const double* ysc,
                                                double* ring, int N, int NB, int tt, int a, int g,
@@ -521,7 +526,7 @@ __device__ __forceinline__ void bandg_bwd_step(const double* __restrict__ Vc,
 #pragma unroll
   for (int t = 0; t < 4; ++t) rg[t] = Vc[(int64_t)a * N + BND * In + 4 * g + t];
   dr = Dc[BND * In + a];
-  wr = ysc[BND * In + a];
+  wr = xel<REV>(const_cast<double*>(ysc), N, BND * In + a);
   double* cur = ring + BND * (I & 1);
   const double* xp = ring + BND * ((I + 1) & 1) + 4 * g;   // block I + 1
   p0 = fma(cn[0], xp[0], p0);
@@ -539,7 +544,7 @@ __device__ __forceinline__ void bandg_bwd_step(const double* __restrict__ Vc,
   q1 = fma(lm[3], sp[3], q1);
   const double xv = row4_sum(q0 + q1);
   cur[a] = xv;
-  wout(BND * I + a, xv, lead);
+  wout(REV ? N - 1 - (BND * I + a) : BND * I + a, xv, lead);
   wave_sync();
 #pragma unroll
   for (int t = 0; t < 4; ++t) vprev[t] = vv[t];
@@ -598,6 +603,132 @@ __device__ __forceinline__ void band_solve_g(const double* __restrict__ Vc,
       bandg_bwd_step(Vc, Dc, ysc, ring, N, NB, NBm + p, a, g, lead, rt[p], dring[p], wr[p], vprev,
                      wout);
   wave_sync();
+}
+
+// Twisted form of the device-memory solve (see band_solve_twist): the two
+// wavefronts of a column run the sweeps over blocks 0 .. k (role 0) and,
+// on the reversed factors and with reversed indices, NB-1 .. k (role 1),
+// each with its own ring; role 0 solves the twist block, writes x_k to
+// device memory and into both rings, and the backward sweeps run outwards.
+// Every wavefront of the workgroup calls it (two barriers); live is false
+// for a column that skips the solve (its wavefronts only take the
+// barriers). tslot: 48 doubles of LDS per column.
+template <bool REV>
+__device__ __forceinline__ void bandg_sweep_fwd(const double* __restrict__ Vc,
+                                                const double* __restrict__ win, double* ysc,
+                                                double* ring, int N, int n, int a, int g,
+                                                bool lead, double* slot) {
+  const int NBe = n + 1;
+  const int nm = n - n % SPFG;
+  ring[BND + a] = 0.0;                            // the slot read as block -1
+  wave_sync();
+  double rt[SPFG][4], wr[SPFG];
+#pragma unroll
+  for (int p = 0; p < SPFG; ++p) {
+    const int Ib = min(p, n);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) rt[p][t] = Vc[(int64_t)(4 * g + t) * N + BND * Ib + a];
+    wr[p] = xel<REV>(const_cast<double*>(win), N, BND * Ib + a);
+  }
+  for (int I0 = 0; I0 < nm; I0 += SPFG) {
+#pragma unroll
+    for (int p = 0; p < SPFG; ++p)
+      bandg_fwd_step<REV>(Vc, win, 1.0, ysc, ring, N, NBe, I0 + p, a, g, lead, rt[p], wr[p]);
+  }
+#pragma unroll
+  for (int p = 0; p < SPFG; ++p) {
+    if (nm + p < n)
+      bandg_fwd_step<REV>(Vc, win, 1.0, ysc, ring, N, NBe, nm + p, a, g, lead, rt[p], wr[p]);
+    else if (nm + p == n)
+      bandg_fwd_step<REV, true>(Vc, win, 1.0, ysc, ring, N, NBe, n, a, g, lead, rt[p], wr[p], slot);
+  }
+}
+
+template <bool REV, typename WOut>
+__device__ __forceinline__ void bandg_sweep_bwd(const double* __restrict__ Vc,
+                                                const double* __restrict__ Dc, const double* ysc,
+                                                double* ring, int N, int n, int a, int g,
+                                                bool lead, WOut wout) {
+  const int NBe = n + 1;
+  double rt[SPFG][4], dring[SPFG], wr[SPFG];
+#pragma unroll
+  for (int p = 0; p < SPFG; ++p) {
+    const int Ib = max(n - (p > 0 ? p : SPFG), 0);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) rt[p][t] = Vc[(int64_t)a * N + BND * Ib + 4 * g + t];
+    dring[p] = Dc[BND * Ib + a];
+    wr[p] = xel<REV>(const_cast<double*>(ysc), N, BND * Ib + a);
+  }
+  double vprev[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) vprev[t] = Vc[(int64_t)a * N + BND * n + 4 * g + t];
+#pragma unroll
+  for (int p = 1; p < SPFG; ++p)
+    if (p <= n)
+      bandg_bwd_step<WOut, REV>(Vc, Dc, ysc, ring, N, NBe, p, a, g, lead, rt[p], dring[p], wr[p],
+                                vprev, wout);
+  int T0 = SPFG;
+  for (; T0 + SPFG - 1 <= n; T0 += SPFG) {
+#pragma unroll
+    for (int p = 0; p < SPFG; ++p)
+      bandg_bwd_step<WOut, REV>(Vc, Dc, ysc, ring, N, NBe, T0 + p, a, g, lead, rt[p], dring[p],
+                                wr[p], vprev, wout);
+  }
+#pragma unroll
+  for (int p = 0; p < SPFG; ++p)
+    if (T0 + p <= n)
+      bandg_bwd_step<WOut, REV>(Vc, Dc, ysc, ring, N, NBe, T0 + p, a, g, lead, rt[p], dring[p],
+                                wr[p], vprev, wout);
+}
+
+template <typename WOut>
+__device__ __forceinline__ void band_solve_g_twist(
+    const double* __restrict__ Vt, const double* __restrict__ Dt, const double* __restrict__ Vr,
+    const double* __restrict__ Dr, const double* __restrict__ tw, const double* __restrict__ win,
+    double* ysc, double* ring0, double* ring1, double* tslot, int N, int role, bool live,
+    int lane, WOut wout) {
+  const int NB = N / BND, k = NB / 2, J = NB - 1 - k;
+  const int a = lane & 15, g = lane >> 4;
+  const bool lead = g == 0;
+  if (live) {
+    if (role == 0) bandg_sweep_fwd<false>(Vt, win, ysc, ring0, N, k, a, g, lead, tslot);
+    else bandg_sweep_fwd<true>(Vr, win, ysc, ring1, N, J, a, g, lead, tslot + BND);
+  }
+  __syncthreads();
+  if (live && role == 0) {
+    double* rhs = tslot + 2 * BND;
+    if (lead) rhs[a] = tslot[a] + tslot[BND + (BND - 1 - a)] - win[BND * k + a];
+    wave_sync();
+    double q0 = lead ? rhs[a] : 0.0, q1 = 0.0;
+#pragma unroll
+    for (int t = 0; t < 4; t += 2) {
+      const int j0 = 4 * g + t, j1 = j0 + 1;
+      q0 = fma((j0 < a) ? tw[a * BND + j0] : 0.0, rhs[j0], q0);
+      q1 = fma((j1 < a) ? tw[a * BND + j1] : 0.0, rhs[j1], q1);
+    }
+    const double u = row4_sum(q0 + q1) * tw[BND * BND + a];
+    wave_sync();
+    if (lead) rhs[a] = u;
+    wave_sync();
+    double s0 = lead ? u : 0.0, s1 = 0.0;
+#pragma unroll
+    for (int t = 0; t < 4; t += 2) {
+      const int j0 = 4 * g + t, j1 = j0 + 1;
+      s0 = fma((j0 > a) ? tw[j0 * BND + a] : 0.0, rhs[j0], s0);
+      s1 = fma((j1 > a) ? tw[j1 * BND + a] : 0.0, rhs[j1], s1);
+    }
+    const double x = row4_sum(s0 + s1);
+    if (lead) {
+      ring0[BND * (k & 1) + a] = x;
+      ring1[BND * (J & 1) + (BND - 1 - a)] = x;
+    }
+    wout(BND * k + a, x, lead);
+  }
+  __syncthreads();
+  if (live) {
+    if (role == 0) bandg_sweep_bwd<false>(Vt, Dt, ysc, ring0, N, k, a, g, lead, wout);
+    else bandg_sweep_bwd<true>(Vr, Dr, ysc, ring1, N, J, a, g, lead, wout);
+  }
 }
 
 // Columns (wavefronts) per workgroup and where the solve keeps its vector.
@@ -1103,10 +1234,9 @@ int path_stage_factor(hipStream_t s, const PathArrays& p, double kappa) {
   hipLaunchKernelGGL(ldl_factor_kernel, dim3((unsigned)ceil_div(cols, FW)), dim3(64 * FW), 0, s, p.N,
                      p.C, cols, p.cnv, p.band, p.lam, kappa, p.ldl_l, p.ldl_d);
   KMP_LAUNCH_CHECK();
-  // the twisted form for the per-column update in LDS: the factors of the
-  // reversed matrix and the twist block
-  const bool twist = !path_global_vec(p);
-  if (twist) {
+  // the twisted solves' data: the factors of the reversed matrix and the
+  // twist block
+  {
     const int64_t tb = (int64_t)p.G * (BND + 1) * p.N;
     hipLaunchKernelGGL(reverse_band_kernel, dim3((unsigned)std::min<int64_t>(ceil_div(tb, 256), 4096)),
                        dim3(256), 0, s, p.band, p.N, tb, p.band_rev);
@@ -1120,11 +1250,10 @@ int path_stage_factor(hipStream_t s, const PathArrays& p, double kappa) {
     KMP_LAUNCH_CHECK();
   }
   // reads the band, writes the factor tiles and 1/d (BND + 1 per element),
-  // twice with the twisted form
-  const double fac = twist ? 2.0 : 1.0;
+  // in both directions
   kc_end(KMP_KC_PRECOMPUTE, s,
-         fac * over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 1.0); }),
-         fac * over_groups(p, [&](double n) { return 4.0 * BND * BND * n * p.C; }));
+         2.0 * over_groups(p, [&](double n) { return 8.0 * n * p.C * (BND + 1.0); }),
+         2.0 * over_groups(p, [&](double n) { return 4.0 * BND * BND * n * p.C; }));
   return 0;
 }
 
@@ -1302,6 +1431,159 @@ __global__ __launch_bounds__(256) void solve_step_kernel(
       const int ii = (i < N) ? i : N - 1;
       ah[q] = ahat[base + ii];
       an[q] = xsrc[ii];
+    }
+#pragma unroll
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      if (i < N) {
+        ahat[base + i] = an[q];
+        abar[base + i] = fma(coef, an[q] - ah[q], an[q]);
+      }
+    }
+  }
+  if (lane == 0) {
+    beta[gc] = bn;
+    bbar[gc] = fma(coef, bn - bold, bn);
+    rmom[gc] = rn;
+    kktv[gc] = kkt;
+    const int it = iters[gc] + 1;
+    iters[gc] = it;
+    iters_total[gc] += 1;
+    if (it >= max_iter) flag[gc] = 2;
+  }
+}
+
+// The same update with the twisted device-memory solve: two columns per
+// 256-thread workgroup, wavefronts 2c and 2c+1 for column c. Wavefront 2c
+// makes the element passes and the decisions exactly as solve_step_kernel
+// does; both run the solve (band_solve_g_twist). A column that stops
+// before the solve (inactive, converged at the extrapolated point, non-
+// finite) still takes the workgroup's barriers, so nothing returns early.
+__global__ __launch_bounds__(256) void solve_step_twist_kernel(
+    int N, int C, int64_t cols, int RT, const int* __restrict__ nvv,
+    const double* __restrict__ lamv, const double* __restrict__ zpart, int S2, int64_t sP,
+    double* __restrict__ ahat, double* __restrict__ abar, const double* __restrict__ Vfac,
+    const double* __restrict__ Dfac, const double* __restrict__ Vrev,
+    const double* __restrict__ Drev, const double* __restrict__ twist,
+    const double* __restrict__ vhat, const double* __restrict__ uvec,
+    const double* __restrict__ gcoef, const double* __restrict__ partial,
+    double* __restrict__ beta, double* __restrict__ bbar, double* __restrict__ rmom,
+    double* __restrict__ kktv, int* __restrict__ flag, int* __restrict__ iters,
+    int* __restrict__ iters_total, double* __restrict__ anew, double* __restrict__ estep,
+    double tol, int max_iter, int restart) {
+  __shared__ double rings[4][RING];
+  __shared__ double tslot[2][3 * BND];
+  __shared__ int go[2];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int pr = wv >> 1, role = wv & 1;
+  const int64_t gc = (int64_t)blockIdx.x * 2 + pr;
+  const bool exists = gc < cols;
+  bool live = exists && flag[gc] == 0;
+  const int64_t gcs = exists ? gc : 0;                 // a valid column for the pointers
+  const int g = (int)(gcs / C), c = (int)(gcs % C);
+  const int64_t base = gcs * (int64_t)N;
+  double d0 = 0.0, tsum = 0.0, kkt = 0.0;
+  if (role == 0 && live) {
+    const double lam = lamv[gc];
+    const double nvd = (double)nvv[gc];
+    {
+      const double* pg = partial + (int64_t)g * RT * C + c;
+      for (int r = lane; r < RT; r += 64) d0 += pg[(int64_t)r * C];
+      d0 = wave_sum(d0);
+    }
+    double tl = 0.0, n2 = 0.0;
+    for (int i0 = 0; i0 < N; i0 += 64 * UL) {
+      double zs[UL], ab[UL], uv[UL];
+#pragma unroll
+      for (int q = 0; q < UL; ++q) {
+        const int i = i0 + lane + 64 * q;
+        const int64_t ic = base + ((i < N) ? i : N - 1);
+        double z = zpart[ic];
+#pragma unroll
+        for (int sk = 1; sk < kMaxSplitK; ++sk) {
+          const double zz = zpart[(sk < S2 ? sk : 0) * sP + ic];
+          z += (sk < S2) ? zz : 0.0;
+        }
+        zs[q] = z;
+        ab[q] = abar[ic];
+        uv[q] = uvec[ic];
+      }
+#pragma unroll
+      for (int q = 0; q < UL; ++q) {
+        const int i = i0 + lane + 64 * q;
+        if (i < N) {
+          const double w = fma(2.0 * lam, ab[q], zs[q]);
+          estep[base + i] = w;
+          tl = fma(uv[q], w, tl);
+          n2 = fma(w, w, n2);
+        }
+      }
+    }
+    tsum = wave_sum(tl);
+    const double n2sum = wave_sum(n2);
+    kkt = nvd * fmax(sqrt(n2sum), fabs(d0));
+    if (!(n2sum == n2sum) || !(d0 == d0) || !(kkt <= 1e300)) {
+      if (lane == 0) { flag[gc] = 3; kktv[gc] = kkt; }
+      live = false;
+    } else if (kkt <= tol) {                            // certified at the extrapolated point
+#pragma unroll 8
+      for (int i = lane; i < N; i += 64) ahat[base + i] = abar[base + i];
+      if (lane == 0) { beta[gc] = bbar[gc]; flag[gc] = 1; kktv[gc] = kkt; }
+      live = false;
+    }
+  }
+  if (role == 0 && lane == 0) go[pr] = live ? 1 : 0;
+  __syncthreads();                                      // w in e and the decision
+  live = go[pr] != 0;
+  double* xg = estep + base;
+  band_solve_g_twist(Vfac + gcs * (int64_t)BND * N, Dfac + base, Vrev + gcs * (int64_t)BND * N,
+                     Drev + base, twist + gcs * (int64_t)TWS, xg, anew + base, rings[2 * pr],
+                     rings[2 * pr + 1], tslot[pr], N, role, live, lane,
+                     [&](int r, double x, bool) { xg[r] = x; });
+  __syncthreads();                                      // x in e
+  if (role != 0 || !live) return;
+  const double gco = gcoef[gc];
+  const double sa = gco * (tsum - d0);
+  const double db = gco * (d0 - tsum);
+  const double bb = bbar[gc];
+  const double bn = bb - db;
+  const double bold = beta[gc];
+  double rd = 0.0;
+  for (int i0 = 0; i0 < N; i0 += 64 * UL) {
+    double vh[UL], ab[UL], ah[UL], xv[UL];
+#pragma unroll
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      const int ii = (i < N) ? i : N - 1;
+      const int64_t ic = base + ii;
+      vh[q] = vhat[ic];
+      ab[q] = abar[ic];
+      ah[q] = ahat[ic];
+      xv[q] = xg[ii];
+    }
+#pragma unroll
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      if (i < N) {
+        const double da = fma(sa, vh[q], xv[q]);
+        const double an = ab[q] - da;
+        rd = fma(da, an - ah[q], rd);
+        xg[i] = an;
+      }
+    }
+  }
+  rd = wave_sum(rd) + db * (bn - bold);
+  const double r = rmom[gc];
+  const double rn = (restart && rd > 0.0) ? 1.0 : 0.5 * (1.0 + sqrt(1.0 + 4.0 * r * r));
+  const double coef = (rn - 1.0) / (0.5 * (1.0 + sqrt(1.0 + 4.0 * rn * rn)));
+  for (int i0 = 0; i0 < N; i0 += 64 * UL) {
+    double ah[UL], an[UL];
+#pragma unroll
+    for (int q = 0; q < UL; ++q) {
+      const int i = i0 + lane + 64 * q;
+      const int ii = (i < N) ? i : N - 1;
+      ah[q] = ahat[base + ii];
+      an[q] = xg[ii];
     }
 #pragma unroll
     for (int q = 0; q < UL; ++q) {
@@ -1533,6 +1815,19 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
                        p.ldl_dr, p.twist, p.vhat,
                        p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt, p.flag, p.iters,
                        p.iters_total, tol, max_iter, restart);
+    KMP_LAUNCH_CHECK();
+    kc_end(KMP_KC_UPDATE, s, upd_bytes, upd_flops);
+    return 0;
+  }
+  if (path_global_vec(p)) {
+    // every iteration in device memory (orders above the LDS capacity, or
+    // forced): the twisted solve, two columns per workgroup
+    kc_begin(KMP_KC_UPDATE, s);
+    hipLaunchKernelGGL(solve_step_twist_kernel, dim3((unsigned)ceil_div(cols, 2)), dim3(256), 0, s,
+                       p.N, p.C, cols, RT, p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar,
+                       p.ldl_l, p.ldl_d, p.ldl_lr, p.ldl_dr, p.twist, p.vhat, p.uvec, p.gcoef,
+                       p.partial, p.beta, p.bbar, p.rmom, p.kkt, p.flag, p.iters,
+                       p.iters_total, p.anew, p.estep, tol, max_iter, restart);
     KMP_LAUNCH_CHECK();
     kc_end(KMP_KC_UPDATE, s, upd_bytes, upd_flops);
     return 0;
