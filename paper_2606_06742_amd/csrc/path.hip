@@ -793,8 +793,8 @@ static CuShape cu_shape() {
 // (update_column_kernel: one column per workgroup, its N doubles in LDS,
 // at most 256 registers per lane) keeps two columns per compute unit at
 // most, fewer when LDS allows fewer; the device-memory form
-// (solve_step_kernel: four columns per workgroup, over 256 registers, one
-// workgroup per compute unit) keeps four. When more columns are active than
+// (solve_step_twist_kernel: two columns per workgroup, two workgroups per
+// compute unit by its registers) keeps four. When more columns are active than
 // the LDS form holds at once, the device-memory form needs fewer rounds and
 // is taken (10 groups of order 9024: above 512 active columns 623 against
 // 717 us per iteration; below, the LDS form's shorter steps win: 280
@@ -1284,181 +1284,25 @@ int path_stage_vectors(hipStream_t s, const PathArrays& p, double kappa) {
 }
 
 // ------------------------------------------------------- the update (K2)
-// solve_step_kernel, one wavefront per column:
-//   d0 = 1'z (from the loss epilogue's tile sums), w = zhat + 2 lambda abar
-//   (split-K parts of zhat added in order) into LDS, t = u'w, ||w||;
-//   the KKT test at the extrapolated point; x = M^{-1} w; the step
-//   Da = g (t - d0) vhat + x, a+ = abar - Da, e = a+ - ahat, and the restart
-//   test sum Da'e + Db (b+ - beta) > 0; the momentum r and its coefficient.
-// Then, with the momentum coefficient known, ahat = a+ and abar = a+ +
-// coef (a+ - ahat) (the first path GEMM multiplies Q B by abar, so no band
-// product follows), and the column's scalars.
 // Element loops load UL rows per lane before using them, so a lane keeps UL
 // loads of each stream in flight.
 constexpr int UL = 8;
 
-template <bool GV>
-__global__ __launch_bounds__(256) void solve_step_kernel(
-    int N, int C, int64_t cols, int RT, const int* __restrict__ nvv,
-    const double* __restrict__ lamv, const double* __restrict__ zpart, int S2, int64_t sP,
-    double* __restrict__ ahat, double* __restrict__ abar, const double* __restrict__ Vfac,
-    const double* __restrict__ Dfac, const double* __restrict__ vhat,
-    const double* __restrict__ uvec, const double* __restrict__ gcoef,
-    const double* __restrict__ partial, double* __restrict__ beta, double* __restrict__ bbar,
-    double* __restrict__ rmom, double* __restrict__ kktv, int* __restrict__ flag,
-    int* __restrict__ iters, int* __restrict__ iters_total, double* __restrict__ anew,
-    double* __restrict__ estep, double tol, int max_iter, int restart) {
-  extern __shared__ double lds_dyn[];
-  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t gc = (int64_t)blockIdx.x * (blockDim.x >> 6) + wv;
-  if (gc >= cols) return;
-  if (flag[gc] != 0) return;
-  // the solve's vector in LDS (GV: only the ring of the device-memory solve)
-  double* xs = lds_dyn + (int64_t)wv * (GV ? RING : N);
-  const int g = (int)(gc / C), c = (int)(gc % C);
-  const int64_t base = gc * (int64_t)N;
-  const double lam = lamv[gc];
-  const double nvd = (double)nvv[gc];                  // the column's loss normaliser
-  double d0 = 0.0;
-  {
-    const double* pg = partial + (int64_t)g * RT * C + c;
-    for (int r = lane; r < RT; r += 64) d0 += pg[(int64_t)r * C];
-    d0 = wave_sum(d0);
-  }
-  double tl = 0.0, n2 = 0.0;
-  for (int i0 = 0; i0 < N; i0 += 64 * UL) {
-    double zs[UL], ab[UL], uv[UL];
-#pragma unroll
-    for (int q = 0; q < UL; ++q) {
-      const int i = i0 + lane + 64 * q;
-      const int64_t ic = base + ((i < N) ? i : N - 1);
-      double z = zpart[ic];
-#pragma unroll
-      for (int sk = 1; sk < kMaxSplitK; ++sk) {
-        // parts beyond S2 re-read part 0 (same line) and are not added
-        const double zz = zpart[(sk < S2 ? sk : 0) * sP + ic];
-        z += (sk < S2) ? zz : 0.0;
-      }
-      zs[q] = z;
-      ab[q] = abar[ic];
-      uv[q] = uvec[ic];
-    }
-#pragma unroll
-    for (int q = 0; q < UL; ++q) {
-      const int i = i0 + lane + 64 * q;
-      if (i < N) {
-        const double w = fma(2.0 * lam, ab[q], zs[q]);
-        if constexpr (GV) estep[base + i] = w;
-        else xs[i] = w;
-        tl = fma(uv[q], w, tl);
-        n2 = fma(w, w, n2);
-      }
-    }
-  }
-  const double tsum = wave_sum(tl);
-  const double n2sum = wave_sum(n2);
-  const double kkt = nvd * fmax(sqrt(n2sum), fabs(d0));
-  const double bb = bbar[gc];
-  // non-finite: tested on both terms, since fmax drops a NaN
-  if (!(n2sum == n2sum) || !(d0 == d0) || !(kkt <= 1e300)) {
-    if (lane == 0) { flag[gc] = 3; kktv[gc] = kkt; }
-    return;
-  }
-  if (kkt <= tol) {                            // certified at the extrapolated point
-#pragma unroll 8
-    for (int i = lane; i < N; i += 64) ahat[base + i] = abar[base + i];
-    if (lane == 0) { beta[gc] = bb; flag[gc] = 1; kktv[gc] = kkt; }
-    return;
-  }
-  // step and the restart test
-  const double gco = gcoef[gc];
-  const double sa = gco * (tsum - d0);
-  const double db = gco * (d0 - tsum);
-  const double bn = bb - db;
-  const double bold = beta[gc];
-  double rd = 0.0;
-  // x = M^{-1} w: in LDS (xs), or (GV) in this column's e vector; the step
-  // below overwrites it with a+ row by row after reading it
-  double* xsrc = xs;
-  if constexpr (GV) {
-    // w (stored in e by the pass above) is the solve's input, forward
-    // results are kept in a+ (anew), and x overwrites w in e
-    double* xg = estep + base;
-    grid_vec_sync();
-    band_solve_g(Vfac + gc * (int64_t)BND * N, Dfac + base, xg, 1.0, anew + base, xs, N, lane,
-                 [&](int r, double x, bool) { xg[r] = x; });
-    // x was written by the lanes of its rows and is read by every lane below
-    grid_vec_sync();
-    xsrc = xg;
-  } else {
-    wave_sync();
-    band_solve(Vfac + gc * (int64_t)BND * N, Dfac + base, xs, N, lane);
-  }
-  for (int i0 = 0; i0 < N; i0 += 64 * UL) {
-    double vh[UL], ab[UL], ah[UL], xv[UL];
-#pragma unroll
-    for (int q = 0; q < UL; ++q) {
-      const int i = i0 + lane + 64 * q;
-      const int ii = (i < N) ? i : N - 1;
-      const int64_t ic = base + ii;
-      vh[q] = vhat[ic];
-      ab[q] = abar[ic];
-      ah[q] = ahat[ic];
-      xv[q] = xsrc[ii];
-    }
-#pragma unroll
-    for (int q = 0; q < UL; ++q) {
-      const int i = i0 + lane + 64 * q;
-      if (i < N) {
-        const double da = fma(sa, vh[q], xv[q]);
-        const double an = ab[q] - da;
-        rd = fma(da, an - ah[q], rd);
-        xsrc[i] = an;
-      }
-    }
-  }
-  rd = wave_sum(rd) + db * (bn - bold);
-  const double r = rmom[gc];
-  const double rn = (restart && rd > 0.0) ? 1.0 : 0.5 * (1.0 + sqrt(1.0 + 4.0 * r * r));
-  const double coef = (rn - 1.0) / (0.5 * (1.0 + sqrt(1.0 + 4.0 * rn * rn)));
-  // momentum: ahat = a+, abar = a+ + coef (a+ - ahat), each lane on the rows
-  // whose a+ it wrote
-  for (int i0 = 0; i0 < N; i0 += 64 * UL) {
-    double ah[UL], an[UL];
-#pragma unroll
-    for (int q = 0; q < UL; ++q) {
-      const int i = i0 + lane + 64 * q;
-      const int ii = (i < N) ? i : N - 1;
-      ah[q] = ahat[base + ii];
-      an[q] = xsrc[ii];
-    }
-#pragma unroll
-    for (int q = 0; q < UL; ++q) {
-      const int i = i0 + lane + 64 * q;
-      if (i < N) {
-        ahat[base + i] = an[q];
-        abar[base + i] = fma(coef, an[q] - ah[q], an[q]);
-      }
-    }
-  }
-  if (lane == 0) {
-    beta[gc] = bn;
-    bbar[gc] = fma(coef, bn - bold, bn);
-    rmom[gc] = rn;
-    kktv[gc] = kkt;
-    const int it = iters[gc] + 1;
-    iters[gc] = it;
-    iters_total[gc] += 1;
-    if (it >= max_iter) flag[gc] = 2;
-  }
-}
-
-// The same update with the twisted device-memory solve: two columns per
-// 256-thread workgroup, wavefronts 2c and 2c+1 for column c. Wavefront 2c
-// makes the element passes and the decisions exactly as solve_step_kernel
-// does; both run the solve (band_solve_g_twist). A column that stops
-// before the solve (inactive, converged at the extrapolated point, non-
-// finite) still takes the workgroup's barriers, so nothing returns early.
+// The update with the solve's vector in device memory (orders above the
+// LDS capacity, or when it keeps more columns resident): two columns per
+// 256-thread workgroup, wavefronts 2c and 2c+1 for column c. Wavefront 2c:
+//   d0 = 1'z (from the loss epilogue's tile sums), w = zhat + 2 lambda abar
+//   (split-K parts of zhat added in order) into the column's e vector,
+//   t = u'w, ||w||; the KKT test at the extrapolated point;
+// both: x = M^{-1} w by the twisted device-memory solve (x over w in e);
+// wavefront 2c: the step Da = g (t - d0) vhat + x, a+ = abar - Da,
+//   e = a+ - ahat, the restart test sum Da'e + Db (b+ - beta) > 0, the
+//   momentum r and its coefficient; then ahat = a+ and abar = a+ +
+//   coef (a+ - ahat) (the first path GEMM multiplies Q B by abar, so no
+//   band product follows), and the column's scalars.
+// A column that stops before the solve (inactive, converged at the
+// extrapolated point, non-finite) still takes the workgroup's barriers, so
+// nothing returns early.
 __global__ __launch_bounds__(256) void solve_step_twist_kernel(
     int N, int C, int64_t cols, int RT, const int* __restrict__ nvv,
     const double* __restrict__ lamv, const double* __restrict__ zpart, int S2, int64_t sP,
@@ -1819,32 +1663,14 @@ int path_iteration(hipStream_t s, const PathArrays& p, double delta, double kapp
     kc_end(KMP_KC_UPDATE, s, upd_bytes, upd_flops);
     return 0;
   }
-  if (path_global_vec(p)) {
-    // every iteration in device memory (orders above the LDS capacity, or
-    // forced): the twisted solve, two columns per workgroup
-    kc_begin(KMP_KC_UPDATE, s);
-    hipLaunchKernelGGL(solve_step_twist_kernel, dim3((unsigned)ceil_div(cols, 2)), dim3(256), 0, s,
-                       p.N, p.C, cols, RT, p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar,
-                       p.ldl_l, p.ldl_d, p.ldl_lr, p.ldl_dr, p.twist, p.vhat, p.uvec, p.gcoef,
-                       p.partial, p.beta, p.bbar, p.rmom, p.kkt, p.flag, p.iters,
-                       p.iters_total, p.anew, p.estep, tol, max_iter, restart);
-    KMP_LAUNCH_CHECK();
-    kc_end(KMP_KC_UPDATE, s, upd_bytes, upd_flops);
-    return 0;
-  }
-  const int cw = path_waves(p, 0, gv);
-  const size_t lds = sizeof(double) * (size_t)cw * path_lds_doubles(p, 0, gv);
-  const void* kfn = gv ? (const void*)solve_step_kernel<true> : (const void*)solve_step_kernel<false>;
-  KMP_HIP_TRY(hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+  // the vector in device memory: the twisted solve, two columns per
+  // workgroup
   kc_begin(KMP_KC_UPDATE, s);
-#define KMP_SOLVE_STEP(GVV)                                                                        \
-  hipLaunchKernelGGL(solve_step_kernel<GVV>, dim3((unsigned)ceil_div(cols, cw)), dim3(64 * cw), lds, \
-                     s, p.N, p.C, cols, RT, p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l, \
-                     p.ldl_d, p.vhat, p.uvec, p.gcoef, p.partial, p.beta, p.bbar, p.rmom, p.kkt,    \
-                     p.flag, p.iters, p.iters_total, p.anew, p.estep, tol, max_iter, restart)
-  if (gv) KMP_SOLVE_STEP(true);
-  else KMP_SOLVE_STEP(false);
-#undef KMP_SOLVE_STEP
+  hipLaunchKernelGGL(solve_step_twist_kernel, dim3((unsigned)ceil_div(cols, 2)), dim3(256), 0, s,
+                     p.N, p.C, cols, RT, p.cnv, p.lam, p.zpart, S2, sP, p.ahat, p.abar, p.ldl_l,
+                     p.ldl_d, p.ldl_lr, p.ldl_dr, p.twist, p.vhat, p.uvec, p.gcoef, p.partial,
+                     p.beta, p.bbar, p.rmom, p.kkt, p.flag, p.iters, p.iters_total, p.anew,
+                     p.estep, tol, max_iter, restart);
   KMP_LAUNCH_CHECK();
   kc_end(KMP_KC_UPDATE, s, upd_bytes, upd_flops);
   return 0;
