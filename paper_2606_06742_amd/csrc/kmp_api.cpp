@@ -1086,6 +1086,10 @@ int kmp_fit_path(void* stream, const kmp_path_spec* spec, const double* X, int64
           if ((rc = path_iteration(s, pa, delta, kappa, spec->tol, spec->max_iter, restart)) != 0)
             return rc;
           ++it;
+          // the active lists follow every iteration (one small launch), so
+          // the GEMMs drop a converged column at once; the counts still
+          // come back at the polls only
+          if (it % spec->poll_every != 0 && (rc = path_compact(s, pa)) != 0) return rc;
         }
         if (pending) {
           int active = 0;
