@@ -531,9 +531,9 @@ __global__ __launch_bounds__(256) void dgemm_partial_kernel(int M, int K, int S,
 // active columns, every wave has the same share of the products (in the
 // 2 x 2 arrangement the waves of the second 32 columns idle while a batch
 // has 32 or fewer, and do half the products at 33 to 48). Two shapes:
-//  - 64 x 128, for launches in which every batch has 65 to 128 active
-//    columns: a batch's columns take one tile instead of two, each A row
-//    tile being streamed once;
+//  - 64 x 128 while most active columns are in batches with 65 to 128
+//    of them (and none has more): such a batch's columns take one tile
+//    instead of two, each A row tile being streamed once;
 //  - 128 x 64 otherwise (M >= 128).
 // Whole-tile path only (the conditions of VEC above); the main loop has no
 // branch around a memory access, as in tile_mainloop_vec. Measured at 10
@@ -781,15 +781,18 @@ int splitk_parts(const GemmArgs& g, int64_t tiles, int per_cu) {
 // The stacked-row tiles were measured at order 9024 only, so smaller
 // orders keep the 2 x 2 tile.
 PartTile pick_part_tile(int M, int G, int C, const int* na, int64_t* tiles, int* per_cu) {
-  int64_t t64 = 0, tw = 0, tt = 0;
+  int64_t t64 = 0, tw = 0, tt = 0, cwide = 0, cnarrow = 0;
   bool wide = C > 64;
   for (int g = 0; g < G; ++g) {
     const int n = na ? na[g] : C;
     t64 += ceil_div(M, 64) * ceil_div(n, 64);
     tw += ceil_div(M, 64) * ceil_div(n, 128);
     tt += ceil_div(M, 128) * ceil_div(n, 64);
-    if (n > 0 && (n <= 64 || n > 128)) wide = false;
+    if (n > 128) wide = false;
+    (n > 64 ? cwide : cnarrow) += n;
   }
+  // the 64 x 128 tile while most active columns are in groups of 65 to 128
+  if (cwide <= cnarrow) wide = false;
   if (M < 4096 || t64 == 0) {
     *tiles = t64;
     *per_cu = 4;
